@@ -1,0 +1,276 @@
+"""CPU oracle for sparse (SC) and submanifold sparse (SSC) convolutions.
+
+TEST INFRASTRUCTURE ONLY.  Nothing on the product path imports this module:
+only the test-suite, the smoke check and the CPU-baseline leg of the
+benchmark may call it.  It shares no code with the GPU library.
+
+It is a plain, slow, fp64 transcription of the paper's definitions
+(Graham, Engelcke & van der Maaten, "3D Semantic Segmentation with
+Submanifold Sparse Convolutional Networks", arXiv:1711.10275):
+
+* feature matrix + (location -> row) dictionary                 Sec. 4.2
+* filter offsets F = {0..f-1}^d and a rule book R = (R_i)       Sec. 4.2
+* SC(m, n, f, s): output active iff the f^d field holds an active
+  input; output size (l - f + s) / s; inactive inputs read as 0  Sec. 4.1
+* SSC(m, n, f): f odd, pad (f-1)/2, output active iff the centre
+  input is active, i.e. the output set is the input set         Sec. 4.1
+* DC: the SC connections inverted; output set = SC input set    Sec. 4.1
+* output = 0, then out[k] += in[j] W^i for every (j, k) in R_i   Sec. 4.2
+* backward: the adjoint of that linear map (the paper trains the
+  networks, Sec. 6.2, but does not spell the gradients out)
+
+Readings where the paper leaves a choice open (each is listed in the design
+notes of the repository):
+
+* offsets are enumerated o = i0*f^2 + i1*f + i2 (first coordinate most
+  significant); the SSC centre is o = (f^3 - 1) / 2;
+* the operation is a cross-correlation: an SSC output at y reads the input
+  at y + i - (f-1)/2, an SC output at y reads the input at s*y + i;
+* SC outputs are numbered in the order of their first visit when the input
+  rows are iterated in row order and, for each input, the filter offsets in
+  the order above (Sec. 4.2 step 1 with the iteration order fixed);
+* (L - f) must be divisible by s and L >= f (else a shape error);
+* the batch index is part of the location, so samples never interact;
+* two rows at one location is an error (one row per active site);
+* ground state 0, no bias.
+
+Only numpy is used; the dictionary is a sorted key array searched with
+numpy.searchsorted, and each per-offset product is one numpy matmul.
+"""
+from __future__ import annotations
+
+import dataclasses
+import numpy as np
+
+D = 3  # spatial dimensions of every layer here
+
+
+class OracleError(Exception):
+    code = "invalid_arg"
+
+
+class InvalidArg(OracleError):
+    code = "invalid_arg"
+
+
+class ShapeError(OracleError):
+    code = "shape"
+
+
+class OutOfRange(OracleError):
+    code = "out_of_range"
+
+
+class Duplicate(OracleError):
+    code = "duplicate"
+
+
+MAX_BATCH = 1 << 15
+MAX_EXTENT = 1 << 16
+
+
+def filter_offsets(f):
+    """F = {0..f-1}^3 as an (f^3, 3) array, row o = (o // f^2, (o // f) % f, o % f)."""
+    return np.array([(i0, i1, i2) for i0 in range(f) for i1 in range(f) for i2 in range(f)],
+                    dtype=np.int64).reshape(-1, 3)
+
+
+def location_key(coords, size):
+    """One integer per location (b, x0, x1, x2) inside a grid of extent `size`."""
+    c = np.asarray(coords, np.int64)
+    L0, L1, L2 = (int(v) for v in size)
+    return ((c[:, 0] * L0 + c[:, 1]) * L1 + c[:, 2]) * L2 + c[:, 3]
+
+
+class CoordTable:
+    """The (location -> row) dictionary of Sec. 4.2 for one layer's active sites."""
+
+    def __init__(self, coords, size):
+        coords = np.asarray(coords)
+        if coords.ndim != 2 or coords.shape[1] != 4:
+            raise InvalidArg("coords must be n x 4")
+        c = coords.astype(np.int64)
+        size = tuple(int(v) for v in size)
+        if any(v < 1 or v > MAX_EXTENT for v in size):
+            raise InvalidArg("spatial size out of range")
+        if c.shape[0]:
+            if (c[:, 0].min() < 0 or c[:, 0].max() >= MAX_BATCH
+                    or np.any(c[:, 1:] < 0) or np.any(c[:, 1:] >= np.array(size))):
+                raise OutOfRange("coordinate outside the grid")
+        self.size = size
+        self.coords = c
+        keys = location_key(c, size)
+        order = np.argsort(keys, kind="stable")
+        self.sorted_keys = keys[order]
+        self.sorted_rows = order
+        if np.any(self.sorted_keys[1:] == self.sorted_keys[:-1]):
+            raise Duplicate("two rows share one location")
+
+    def lookup(self, query):
+        """Row of each queried location, -1 where the location is not active."""
+        q = np.asarray(query, np.int64)
+        out = np.full(q.shape[0], -1, np.int64)
+        inside = np.all((q[:, 1:] >= 0) & (q[:, 1:] < np.array(self.size)), axis=1)
+        if not np.any(inside) or self.sorted_keys.size == 0:
+            return out
+        k = location_key(q[inside], self.size)
+        pos = np.searchsorted(self.sorted_keys, k)
+        pos_c = np.minimum(pos, self.sorted_keys.size - 1)
+        hit = self.sorted_keys[pos_c] == k
+        rows = np.where(hit, self.sorted_rows[pos_c], -1)
+        out[inside] = rows
+        return out
+
+
+@dataclasses.dataclass
+class Rulebook:
+    """R = (R_o : o in F), each R_o a pair of equal-length row arrays (in, out)."""
+    f: int
+    stride: int
+    submanifold: bool
+    n_in: int
+    n_out: int
+    in_size: tuple
+    out_size: tuple
+    ins: list            # K arrays of input rows
+    outs: list           # K arrays of output rows
+    out_coords: np.ndarray  # n_out x 4 int64
+
+    @property
+    def K(self):
+        return self.f ** D
+
+    def pairs_per_offset(self):
+        return np.array([a.size for a in self.ins], np.int64)
+
+    def n_pairs(self):
+        return int(sum(a.size for a in self.ins))
+
+
+def ssc_rulebook(coords, size, f):
+    """SSC(., ., f) rule book (Sec. 4.1 definition, Sec. 4.2 construction).
+
+    The input dictionary serves as the output dictionary; for every active
+    site k and offset i in F the neighbour at x_k + i - (f-1)/2 is looked up,
+    and a hit j adds the row (j, k) to R_i.
+    """
+    if f < 1 or f % 2 == 0:
+        raise InvalidArg("SSC needs an odd filter size")
+    table = CoordTable(coords, size)
+    c = table.coords
+    centre = (f - 1) // 2
+    ins, outs = [], []
+    for i in filter_offsets(f):
+        q = c.copy()
+        q[:, 1:] += i - centre
+        j = table.lookup(q)
+        k = np.nonzero(j >= 0)[0]
+        ins.append(j[k])
+        outs.append(k)
+    n = c.shape[0]
+    return Rulebook(f, 1, True, n, n, table.size, table.size, ins, outs, c.copy())
+
+
+def sc_output_size(size, f, s):
+    """Output extent (l - f + s) / s per dimension (Sec. 4.1)."""
+    if f < 1 or s < 1:
+        raise InvalidArg("filter size and stride must be positive")
+    out = []
+    for L in size:
+        if L < f or (L - f) % s != 0:
+            raise ShapeError("(L - f) must be a non-negative multiple of s")
+        out.append((L - f + s) // s)
+    return tuple(out)
+
+
+def sc_rulebook(coords, size, f, s):
+    """SC(., ., f, s) rule book built in one pass over the inputs (Sec. 4.2).
+
+    Input rows are visited in row order, and for each input x the outputs y
+    that see it are visited in offset order: x = s*y + i for i in F.  An
+    output site gets the next free row at its first visit, and the pair
+    (row(x), row(y)) is appended to R_i.
+    """
+    size = tuple(int(v) for v in size)
+    out_size = sc_output_size(size, f, s)
+    table = CoordTable(coords, size)
+    c = table.coords
+    n, F = c.shape[0], filter_offsets(f)
+    K = F.shape[0]
+    # visit (j, o): y = (x_j - i_o) / s when that is integral and inside the output grid
+    t = c[:, None, 1:] - F[None, :, :]                        # n x K x 3
+    valid = np.all((t % s == 0) & (t >= 0) & (t // s < np.array(out_size)), axis=2)
+    y = t // s
+    b = np.broadcast_to(c[:, None, 0:1], (n, K, 1))
+    ycoords = np.concatenate([b, y], axis=2).reshape(n * K, 4)
+    vflat = valid.reshape(n * K)
+    visit = np.nonzero(vflat)[0]                              # visit order = (j, o) lexicographic
+    keys = location_key(ycoords[visit], out_size)
+    # first visit of each output location -> output row in order of first visit
+    uniq, first = np.unique(keys, return_index=True)
+    order = np.argsort(first, kind="stable")
+    row_of_uniq = np.empty(uniq.size, np.int64)
+    row_of_uniq[order] = np.arange(uniq.size)
+    out_rows = row_of_uniq[np.searchsorted(uniq, keys)]
+    out_coords = ycoords[visit[first[order]]]
+    j_of_visit, o_of_visit = visit // K, visit % K
+    ins, outs = [], []
+    for o in range(K):
+        m = o_of_visit == o
+        ins.append(j_of_visit[m])
+        outs.append(out_rows[m])
+    return Rulebook(f, s, False, n, int(uniq.size), size, out_size, ins, outs, out_coords)
+
+
+def transpose(rb):
+    """DC connectivity (Sec. 4.1): the same pairs with input and output swapped."""
+    return Rulebook(rb.f, rb.stride, rb.submanifold, rb.n_out, rb.n_in, rb.out_size, rb.in_size,
+                    [a.copy() for a in rb.outs], [a.copy() for a in rb.ins], None)
+
+
+def forward(X, W, rb):
+    """out = 0; out[k] += X[j] @ W[o] for every (j, k) in R_o (Sec. 4.2 step 2), fp64."""
+    X = np.asarray(X, np.float64)
+    W = np.asarray(W, np.float64)
+    if W.shape[0] != rb.K or X.shape[0] != rb.n_in or W.shape[1] != X.shape[1]:
+        raise ShapeError("shape mismatch")
+    Y = np.zeros((rb.n_out, W.shape[2]), np.float64)
+    for o in range(rb.K):
+        if rb.ins[o].size:
+            np.add.at(Y, rb.outs[o], X[rb.ins[o]] @ W[o])
+    return Y
+
+
+def backward(X, W, dY, rb):
+    """Adjoint of `forward`: dX[j] += dY[k] @ W[o]^T, dW[o] += X[j]^T dY[k], fp64."""
+    X = np.asarray(X, np.float64)
+    W = np.asarray(W, np.float64)
+    dY = np.asarray(dY, np.float64)
+    dX = np.zeros_like(X)
+    dW = np.zeros_like(W)
+    for o in range(rb.K):
+        j, k = rb.ins[o], rb.outs[o]
+        if j.size:
+            np.add.at(dX, j, dY[k] @ W[o].T)
+            dW[o] = X[j].T @ dY[k]
+    return dX, dW
+
+
+def canonical_triples(rb):
+    """All pairs as (in, out, o) rows sorted by (o, out, in)."""
+    if rb.n_pairs() == 0:
+        return np.zeros((0, 3), np.int64)
+    t = np.concatenate([np.stack([rb.ins[o], rb.outs[o], np.full(rb.ins[o].size, o)], axis=1)
+                        for o in range(rb.K)])
+    order = np.lexsort((t[:, 0], t[:, 1], t[:, 2]))
+    return t[order].astype(np.int64)
+
+
+def macs(rb, cin, cout):
+    """Multiply-adds of one layer: sum over output sites of a*m*n (Table 2)."""
+    return rb.n_pairs() * cin * cout
+
+
+def conditioning_bound(X, W, rb):
+    """B[k][co] = sum |X[j][ci]| |W[o][ci][co]|: a scale for rounding errors."""
+    return forward(np.abs(np.asarray(X, np.float64)), np.abs(np.asarray(W, np.float64)), rb)

@@ -1,0 +1,108 @@
+"""Dense brute-force references used to pin the CPU oracle on tiny grids.
+
+The sparse layers are dense convolutions restricted to active sites
+(Sec. 4.1: inactive inputs read as zero; SSC outputs only at active input
+sites; SC outputs where the receptive field holds an active input).  These
+helpers scatter the sparse inputs into a dense zero grid, call torch's CPU
+conv3d / conv_transpose3d in float64 (a library routine, cross-correlation),
+and read the result back at the active output sites.  A second, pure numpy
+loop implementation covers the SSC case without torch.
+"""
+import numpy as np
+import torch
+import torch.nn.functional as F
+
+
+def to_dense(coords, X, size, batch=None):
+    coords = np.asarray(coords, np.int64)
+    X = np.asarray(X, np.float64)
+    B = int(coords[:, 0].max()) + 1 if batch is None else batch
+    C = X.shape[1]
+    d = np.zeros((B, C) + tuple(size), np.float64)
+    if coords.shape[0]:
+        d[coords[:, 0], :, coords[:, 1], coords[:, 2], coords[:, 3]] = X
+    return torch.from_numpy(d)
+
+
+def torch_weight(W, f):
+    """W[o][ci][co] (o = i0 f^2 + i1 f + i2) -> conv3d weight [co][ci][i0][i1][i2]."""
+    W = np.asarray(W, np.float64)
+    K, cin, cout = W.shape
+    w = W.reshape(f, f, f, cin, cout).transpose(4, 3, 0, 1, 2)
+    return torch.from_numpy(np.ascontiguousarray(w))
+
+
+def dense_ssc(coords, X, W, size, f):
+    """SSC via dense conv3d with padding (f-1)/2, read at the input sites."""
+    coords = np.asarray(coords, np.int64)
+    B = int(coords[:, 0].max()) + 1
+    y = F.conv3d(to_dense(coords, X, size, B), torch_weight(W, f), padding=(f - 1) // 2)
+    y = y.numpy()
+    return y[coords[:, 0], :, coords[:, 1], coords[:, 2], coords[:, 3]]
+
+
+def dense_sc(coords, X, W, size, f, s):
+    """SC via dense conv3d with stride s.
+
+    Returns (active output coords sorted by (b, y), features at them).  The
+    active set is where conv3d of the occupancy with an all-ones filter is
+    positive, i.e. the field holds at least one active input.
+    """
+    coords = np.asarray(coords, np.int64)
+    B = int(coords[:, 0].max()) + 1
+    occ = to_dense(coords, np.ones((coords.shape[0], 1)), size, B)
+    cnt = F.conv3d(occ, torch.ones(1, 1, f, f, f, dtype=torch.float64), stride=s).numpy()[:, 0]
+    act = np.argwhere(cnt > 0)
+    y = F.conv3d(to_dense(coords, X, size, B), torch_weight(W, f), stride=s).numpy()
+    vals = y[act[:, 0], :, act[:, 1], act[:, 2], act[:, 3]]
+    return act.astype(np.int64), vals, cnt
+
+
+def dense_dc(out_coords, Xdc, Wdc, in_coords, size, f, s):
+    """DC (inverse of SC(f, s)) via conv_transpose3d, read at the SC input sites.
+
+    Wdc[o][ci][co] maps the SC output features (ci) back to the SC input
+    sites (co).  conv_transpose3d weight layout is [in][out][i0][i1][i2].
+    """
+    out_coords = np.asarray(out_coords, np.int64)
+    in_coords = np.asarray(in_coords, np.int64)
+    B = int(in_coords[:, 0].max()) + 1
+    osize = tuple((L - f + s) // s for L in size)
+    Wdc = np.asarray(Wdc, np.float64)
+    K, cin, cout = Wdc.shape
+    w = torch.from_numpy(np.ascontiguousarray(Wdc.reshape(f, f, f, cin, cout).transpose(3, 4, 0, 1, 2)))
+    y = F.conv_transpose3d(to_dense(out_coords, Xdc, osize, B), w, stride=s).numpy()
+    return y[in_coords[:, 0], :, in_coords[:, 1], in_coords[:, 2], in_coords[:, 3]]
+
+
+def loop_ssc(coords, X, W, size, f):
+    """SSC by seven nested loops over (site, offset, ci, co) -- tiny inputs only."""
+    coords = [tuple(int(v) for v in r) for r in np.asarray(coords)]
+    row = {c: i for i, c in enumerate(coords)}
+    X = np.asarray(X, np.float64)
+    W = np.asarray(W, np.float64)
+    cin, cout = W.shape[1], W.shape[2]
+    c = (f - 1) // 2
+    Y = np.zeros((len(coords), cout))
+    for k, (b, y0, y1, y2) in enumerate(coords):
+        for i0 in range(f):
+            for i1 in range(f):
+                for i2 in range(f):
+                    j = row.get((b, y0 + i0 - c, y1 + i1 - c, y2 + i2 - c))
+                    if j is None:
+                        continue
+                    o = (i0 * f + i1) * f + i2
+                    for ci in range(cin):
+                        for co in range(cout):
+                            Y[k, co] += X[j, ci] * W[o, ci, co]
+    return Y
+
+
+def active_in_field(coords, size, f, centred=True):
+    """a = number of active inputs in each active site's f^3 field (Table 2)."""
+    coords = np.asarray(coords, np.int64)
+    B = int(coords[:, 0].max()) + 1
+    occ = to_dense(coords, np.ones((coords.shape[0], 1)), size, B)
+    cnt = F.conv3d(occ, torch.ones(1, 1, f, f, f, dtype=torch.float64),
+                   padding=(f - 1) // 2 if centred else 0).numpy()[:, 0]
+    return cnt[coords[:, 0], coords[:, 1], coords[:, 2], coords[:, 3]].astype(np.int64)

@@ -1,0 +1,111 @@
+"""Plant plausible mistakes in the CPU oracle and check that a pin catches each.
+
+Mutations are applied with monkeypatch to the oracle module only (CPU), so
+the oracle's pins are shown to be sensitive to: a sign error in the offset,
+a dropped offset (term), a transposed weight operand, a wrong SSC centre, an
+SC stride/offset mix-up and a backward that forgets an offset.
+"""
+import numpy as np
+import pytest
+
+from oracle import sscn_oracle as O
+from tests import dense_ref as R
+
+
+def _set(seed=1, size=(8, 8, 8)):
+    rng = np.random.default_rng(seed)
+    occ = rng.random((2,) + size) < 0.2
+    b, x0, x1, x2 = np.nonzero(occ)
+    return np.stack([b, x0, x1, x2], axis=1).astype(np.int32)
+
+
+def _ssc_pin_error():
+    size = (8, 8, 8)
+    rng = np.random.default_rng(5)
+    c = _set()
+    X, W = rng.standard_normal((c.shape[0], 4)), rng.standard_normal((27, 4, 4))
+    Y = O.forward(X, W, O.ssc_rulebook(c, size, 3))
+    return np.abs(Y - R.dense_ssc(c, X, W, size, 3)).max()
+
+
+def _sc_pin_error():
+    size = (9, 9, 9)
+    rng = np.random.default_rng(6)
+    c = _set(size=size)
+    X, W = rng.standard_normal((c.shape[0], 3)), rng.standard_normal((27, 3, 2))
+    rb = O.sc_rulebook(c, size, 3, 2)
+    act, vals, _ = R.dense_sc(c, X, W, size, 3, 2)
+    if rb.n_out != act.shape[0]:
+        return np.inf
+    key = {tuple(r): i for i, r in enumerate(act.tolist())}
+    try:
+        idx = [key[tuple(r)] for r in rb.out_coords.tolist()]
+    except KeyError:
+        return np.inf
+    return np.abs(O.forward(X, W, rb) - vals[idx]).max()
+
+
+def _bwd_pin_error():
+    size = (8, 8, 8)
+    rng = np.random.default_rng(7)
+    c = _set()
+    X, W = rng.standard_normal((c.shape[0], 3)), rng.standard_normal((27, 3, 3))
+    rb = O.ssc_rulebook(c, size, 3)
+    G = rng.standard_normal((c.shape[0], 3))
+    dX, dW = O.backward(X, W, G, rb)
+    lhs = np.sum(O.forward(X, W, rb) * G)
+    return max(abs(lhs - np.sum(X * dX)), abs(lhs - np.sum(W * dW)))
+
+
+def test_unmutated_pins_hold():
+    assert _ssc_pin_error() < 1e-10
+    assert _sc_pin_error() < 1e-10
+    assert _bwd_pin_error() < 1e-10
+
+
+def test_offset_sign_error_caught(monkeypatch):
+    orig = O.filter_offsets
+    monkeypatch.setattr(O, "filter_offsets", lambda f: (f - 1) - orig(f))
+    assert _ssc_pin_error() > 1e-3
+
+
+def test_dropped_offset_caught(monkeypatch):
+    orig = O.ssc_rulebook
+
+    def drop_last(*a):
+        rb = orig(*a)
+        rb.ins[-1] = rb.ins[-1][:0]
+        rb.outs[-1] = rb.outs[-1][:0]
+        return rb
+    monkeypatch.setattr(O, "ssc_rulebook", drop_last)
+    assert _ssc_pin_error() > 1e-3
+
+
+def test_transposed_weight_caught(monkeypatch):
+    orig = O.forward
+    monkeypatch.setattr(O, "forward", lambda X, W, rb: orig(X, np.asarray(W).transpose(0, 2, 1), rb))
+    assert _ssc_pin_error() > 1e-3
+
+
+def test_wrong_ssc_centre_caught(monkeypatch):
+    orig = O.filter_offsets
+    # shifting the offsets by one voxel along x2 moves the SSC field off-centre
+    monkeypatch.setattr(O, "filter_offsets", lambda f: orig(f) + np.array([0, 0, 1]))
+    assert _ssc_pin_error() > 1e-3
+
+
+def test_sc_stride_mixup_caught(monkeypatch):
+    orig = O.sc_output_size
+    monkeypatch.setattr(O, "sc_output_size", lambda size, f, s: orig(size, f, 1) if s == 2 else orig(size, f, s))
+    assert _sc_pin_error() > 1e-3
+
+
+def test_backward_dropped_offset_caught(monkeypatch):
+    orig = O.backward
+
+    def bad(X, W, dY, rb):
+        dX, dW = orig(X, W, dY, rb)
+        dW[0] = 0.0
+        return dX, dW
+    monkeypatch.setattr(O, "backward", bad)
+    assert _bwd_pin_error() > 1e-6
