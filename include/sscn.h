@@ -1,0 +1,194 @@
+/*
+ * sscn.h -- C ABI of the MI355X (gfx950) sparse / submanifold sparse
+ * convolution library (libsscn.so).
+ *
+ * Method: Graham, Engelcke & van der Maaten, "3D Semantic Segmentation with
+ * Submanifold Sparse Convolutional Networks" (arXiv:1711.10275).
+ *   - layer state = feature matrix (one row per active site) + a dictionary
+ *     (location -> row), Sec. 4.2;
+ *   - rule book R = (R_o : o in F), F = {0..f-1}^3, each R_o a list of
+ *     (input row, output row) pairs, Sec. 4.2;
+ *   - SC(m, n, f, s) and SSC(m, n, f) active sets, Sec. 4.1;
+ *   - output = 0, then out[k] += in[j] * W^o for every (j, k) in R_o,
+ *     Sec. 4.2.
+ *
+ * Conventions shared by every call
+ *   - d = 3.  Filter offsets are numbered o = i0*f*f + i1*f + i2.
+ *   - The operation is a cross-correlation: an SSC output at y reads the
+ *     input at y + i - (f-1)/2, an SC output at y reads the input at s*y + i.
+ *   - coords: int32, n x 4 rows (b, x0, x1, x2), row-major, 16-byte aligned,
+ *     row j <-> feature row j.  0 <= b < 32768, 0 <= x_d < spatial_size[d]
+ *     <= 65536.  The batch index is part of the location, so samples never
+ *     interact.
+ *   - features: row-major n x C.  weights: [K][c_in][c_out] (K = f^3).
+ *   - dtype SSCN_F32: everything fp32.  SSCN_BF16: features, weights, out
+ *     and dgrad are bfloat16; products are accumulated in fp32 and rounded
+ *     once (nearest-even) when written; wgrad is always fp32.
+ *   - Pointers are DEVICE pointers unless marked (host).  The caller owns
+ *     every feature / weight / coordinate / output buffer.  Outputs are fully
+ *     overwritten and must not alias inputs.
+ *   - Work is enqueued on `stream` (may be NULL = the default stream).  A
+ *     rule book may be used on its build stream at once; on another stream
+ *     only after the caller has ordered that stream after the build stream.
+ *   - Errors are returned as codes, never thrown across the ABI; on failure
+ *     *out is left untouched and sscn_last_error() (thread-local) describes
+ *     the failure.  A device fault surfaces at the next synchronising call as
+ *     SSCN_ERR_DEVICE.
+ *   - Sizes: n * f^3 must stay below 2^31 (positions are 32-bit).
+ */
+#ifndef SSCN_H
+#define SSCN_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SSCN_OK = 0,
+  SSCN_ERR_INVALID_ARG = 1,  /* null pointer with n > 0, n < 0, bad f / s / C / dtype, misaligned coords */
+  SSCN_ERR_SHAPE = 2,        /* SC: L < f or (L - f) % s != 0; channel count or dtype inconsistent with the rule book */
+  SSCN_ERR_OUT_OF_RANGE = 3, /* a coordinate outside [0, L) or a batch index outside [0, 32768) */
+  SSCN_ERR_DUPLICATE = 4,    /* two rows at one location (one row per active site, Sec. 4.2) */
+  SSCN_ERR_OOM = 5,          /* device allocation failed */
+  SSCN_ERR_DEVICE = 6        /* a HIP runtime error */
+} sscn_status;
+
+typedef enum { SSCN_F32 = 0, SSCN_BF16 = 1 } sscn_dtype;
+
+/* Opaque rule book; library-owned and immutable after its build. */
+typedef struct sscn_rulebook_s* sscn_rulebook;
+
+/*
+ * ssc_rulebook_build -- rule book of SSC(., ., f) (Sec. 4.1 "Submanifold
+ * sparse convolution"; Sec. 4.2, last paragraph: the input dictionary is
+ * re-used as the output dictionary).
+ *   coords        device, n x 4 int32 (see conventions)
+ *   n             number of active sites (n = 0 gives an empty rule book)
+ *   spatial_size  host, 3 extents L_d
+ *   filter_size   f, odd (else SSCN_ERR_INVALID_ARG)
+ *   out           receives the handle; free with sscn_rulebook_free
+ * The output set equals the input set and output row k is input row k.
+ * Builds a GPU open-addressing dictionary, probes the f^3 neighbours of
+ * every site and compacts the hits into R.  Blocks the host once to read
+ * back sizes and error flags.
+ */
+sscn_status ssc_rulebook_build(const int32_t* coords, int64_t n, const int32_t* spatial_size,
+                               int32_t filter_size, hipStream_t stream, sscn_rulebook* out);
+
+/*
+ * sc_rulebook_build -- rule book of SC(., ., f, s) (Sec. 4.1 "Sparse
+ * convolutional operations"; Sec. 4.2 step 1).
+ *   spatial_size  host, 3 extents L_d with L_d >= f and (L_d - f) % s == 0
+ *                 (else SSCN_ERR_SHAPE); output extent (L_d - f + s) / s
+ *   filter_size, stride  f >= 1, s >= 1
+ * An output site is active iff its f^3 field holds an active input.  Output
+ * rows are numbered in the order of first visit when input rows are taken
+ * in row order and, per input, offsets in increasing o (the single pass of
+ * Sec. 4.2 step 1 with that iteration order); read them back with
+ * sscn_rulebook_out_coords.  Blocks the host once.
+ */
+sscn_status sc_rulebook_build(const int32_t* coords, int64_t n, const int32_t* spatial_size,
+                              int32_t filter_size, int32_t stride, hipStream_t stream,
+                              sscn_rulebook* out);
+
+/*
+ * sscn_rulebook_transpose -- the inverted connections R^T_o = {(k, j) :
+ * (j, k) in R_o}: the rule book of the deconvolution DC that inverts an SC
+ * (Sec. 4.1 "Other operators"); its output set is the SC's input set, in
+ * the SC's input row order.  For an SSC rule book R^T_o = R_{K-1-o}.  The
+ * view shares storage with (and keeps alive) its parent; free it with
+ * sscn_rulebook_free.  Transposing a transposed view gives a view of the
+ * parent.  No device work, no synchronisation.
+ */
+sscn_status sscn_rulebook_transpose(sscn_rulebook rb, sscn_rulebook* out);
+
+typedef struct {
+  int64_t n_in, n_out, n_pairs;
+  int32_t filter_size, stride, submanifold, transposed, n_offsets;
+  int32_t in_size[3], out_size[3];
+} sscn_rulebook_info;
+
+/*
+ * sscn_rulebook_query -- sizes of a rule book (host only, no device work).
+ *   info              host, filled in
+ *   pairs_per_offset  host, n_offsets entries |R_o| (nullable)
+ * sum_o |R_o| * c_in * c_out is the layer's multiply-add count (Table 2:
+ * a*m*n summed over active output sites).
+ */
+sscn_status sscn_rulebook_query(sscn_rulebook rb, sscn_rulebook_info* info,
+                                int64_t* pairs_per_offset);
+
+/*
+ * sscn_rulebook_out_coords -- device n_out x 4 int32 coordinates of the
+ * output sites, in output row order, grid of extent info.out_size.
+ */
+sscn_status sscn_rulebook_out_coords(sscn_rulebook rb, int32_t* out_coords, hipStream_t stream);
+
+/*
+ * sscn_rulebook_export -- every pair as (in_rows[p], out_rows[p],
+ * offsets[p]), p < n_pairs, sorted by (offset, out row, in row).  Device
+ * int32 arrays of n_pairs entries each.
+ */
+sscn_status sscn_rulebook_export(sscn_rulebook rb, int32_t* in_rows, int32_t* out_rows,
+                                 int32_t* offsets, hipStream_t stream);
+
+/* Release a rule book or view (storage goes when its last view goes). NULL is a no-op. */
+void sscn_rulebook_free(sscn_rulebook rb);
+
+/*
+ * sparse_conv_forward -- out = 0; out[k] += features[j] * W^o for every
+ * (j, k) in R_o (Sec. 4.2 step 2).  With a transposed rule book this is
+ * the deconvolution DC with its own weights [K][c_in][c_out].
+ *   features  device n_in x c_in     weights  device K x c_in x c_out
+ *   out       device n_out x c_out, overwritten
+ * Asynchronous on `stream`.
+ */
+sscn_status sparse_conv_forward(const void* features, const void* weights, sscn_rulebook rb,
+                                int32_t c_in, int32_t c_out, sscn_dtype dtype, void* out,
+                                hipStream_t stream);
+
+/*
+ * sparse_conv_backward -- gradients of sparse_conv_forward (its adjoint):
+ *   dgrad[j] = sum_o sum_{(j,k) in R_o} dout[k] * (W^o)^T   (n_in x c_in)
+ *   wgrad[o] = sum_{(j,k) in R_o} features[j]^T dout[k]    (K x c_in x c_out, fp32)
+ * dgrad runs the forward machinery over the transposed rule book; wgrad is
+ * a per-offset gathered (c_in x pairs) x (pairs x c_out) contraction.
+ *   features  device n_in x c_in (needed only for wgrad; nullable if wgrad is NULL)
+ *   dout      device n_out x c_out
+ *   dgrad     device n_in x c_in, overwritten (nullable: skipped)
+ *   wgrad     device fp32 K x c_in x c_out, overwritten (nullable: skipped)
+ * Asynchronous on `stream`.
+ */
+sscn_status sparse_conv_backward(const void* features, const void* weights, const void* dout,
+                                 sscn_rulebook rb, int32_t c_in, int32_t c_out, sscn_dtype dtype,
+                                 void* dgrad, float* wgrad, hipStream_t stream);
+
+/*
+ * sscn_affine_relu -- y[r][c] = max(0, x[r][c] * scale[c] + shift[c]) over the
+ * n active rows: batch normalisation in inference form followed by ReLU,
+ * both restricted to active sites (Sec. 4.1 "Other operators"; the
+ * pre-activated blocks of Sec. 5).  x, y: n x c in `dtype` (may alias);
+ * scale, shift: device fp32, c entries each.
+ */
+sscn_status sscn_affine_relu(const void* x, const float* scale, const float* shift, int64_t n,
+                             int32_t c, sscn_dtype dtype, void* y, hipStream_t stream);
+
+/*
+ * sscn_concat_cols -- y = [a | b] row by row: a is n x ca, b is n x cb, y is
+ * n x (ca + cb), all in `dtype` (the skip-connection merge of the U-Net of
+ * Sec. 5).  y must not alias a or b.
+ */
+sscn_status sscn_concat_cols(const void* a, int32_t ca, const void* b, int32_t cb, int64_t n,
+                             sscn_dtype dtype, void* y, hipStream_t stream);
+
+/* Thread-local message describing the last failure on this thread ("" if none). */
+const char* sscn_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SSCN_H */

@@ -1,0 +1,116 @@
+// Internal declarations shared by the translation units of libsscn.so.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <memory>
+#include <new>
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "sscn.h"
+
+namespace sscn {
+
+// Output rows are grouped in tiles of kTile rows; the rule book stores, for
+// every (offset o, tile t), one contiguous segment of pairs whose output row
+// lies in tile t.  Segments are laid out offset-major: seg[o * n_tiles + t].
+constexpr int kTile = 64;
+constexpr int kWave = 64;
+
+constexpr uint64_t kEmptyKey = ~0ull;
+constexpr int kMaxBatch = 1 << 15;
+constexpr int kMaxExtent = 1 << 16;
+
+// error flags raised by device code
+constexpr int kFlagOutOfRange = 1;
+constexpr int kFlagDuplicate = 2;
+
+// ---------------------------------------------------------------- errors
+void set_error(const std::string& msg);
+sscn_status fail(sscn_status st, const std::string& msg);
+sscn_status hip_fail(hipError_t e, const char* what);
+
+#define SSCN_HIP(call)                                   \
+  do {                                                   \
+    hipError_t e_ = (call);                              \
+    if (e_ != hipSuccess) return ::sscn::hip_fail(e_, #call); \
+  } while (0)
+
+// ---------------------------------------------------------------- memory
+// Stream-ordered device allocation from the device's default pool (kept
+// cached by the library so repeated builds do not return memory to the OS).
+sscn_status dev_alloc(void** p, size_t bytes, hipStream_t s);
+void dev_free(void* p, hipStream_t s);
+
+// One direction of a rule book: tiles over the output rows of that
+// direction, offset-major segments, and the pair arrays.
+struct Storage {
+  int64_t n_tiles = 0;
+  int64_t* seg = nullptr;        // K * n_tiles + 1 entries
+  int32_t* in_rows = nullptr;    // n_pairs
+  int32_t* out_rows = nullptr;   // n_pairs
+};
+
+struct RulebookData {
+  std::atomic<int> refs{1};
+  int device = 0;
+  hipStream_t stream = nullptr;  // build stream (used to release storage)
+  int f = 0, stride = 1, K = 0;
+  bool submanifold = false;
+  int64_t n_in = 0, n_out = 0, n_pairs = 0;
+  int32_t in_size[3] = {0, 0, 0}, out_size[3] = {0, 0, 0};
+  std::vector<int64_t> pairs_per_offset;  // host copy, K entries
+  Storage fwd;                   // tiles over output rows
+  Storage bwd;                   // tiles over input rows (SC only; SSC mirrors fwd)
+  int32_t* out_coords = nullptr; // n_out x 4
+  int32_t* in_coords = nullptr;  // n_in x 4 (SC only; an SSC's input sites are its output sites)
+  ~RulebookData();
+};
+
+}  // namespace sscn
+
+struct sscn_rulebook_s {
+  sscn::RulebookData* d;
+  bool transposed;
+};
+
+namespace sscn {
+
+// What a kernel needs to run one direction of a rule book.
+struct View {
+  const Storage* st;
+  int K;
+  bool mirror;        // segment for offset o is stored under K-1-o
+  int64_t n_in, n_out;
+};
+
+inline View view_of(const sscn_rulebook_s* rb) {
+  const RulebookData* d = rb->d;
+  View v;
+  v.K = d->K;
+  if (!rb->transposed) {
+    v.st = &d->fwd; v.mirror = false; v.n_in = d->n_in; v.n_out = d->n_out;
+  } else if (d->submanifold) {
+    v.st = &d->fwd; v.mirror = true; v.n_in = d->n_out; v.n_out = d->n_in;
+  } else {
+    v.st = &d->bwd; v.mirror = false; v.n_in = d->n_out; v.n_out = d->n_in;
+  }
+  return v;
+}
+
+// Device-wide exclusive scan: out[i] = sum_{q<i} in[q], out[count] = total.
+// `in` and `out` may alias.  Temporary storage is allocated on `s`.
+sscn_status exclusive_scan_i64(const int64_t* in, int64_t* out, int64_t count, hipStream_t s);
+sscn_status exclusive_scan_i32(const int32_t* in, int32_t* out, int64_t count, hipStream_t s);
+
+// Fill helpers (graph-capture safe: kernels, not memset nodes).
+sscn_status fill_i32(int32_t* p, int32_t v, int64_t count, hipStream_t s);
+sscn_status fill_u64(uint64_t* p, uint64_t v, int64_t count, hipStream_t s);
+sscn_status fill_f32(float* p, float v, int64_t count, hipStream_t s);
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+}  // namespace sscn

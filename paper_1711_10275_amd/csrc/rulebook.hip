@@ -1,0 +1,612 @@
+// Rule-book construction on the GPU (Sec. 4.2 of the paper).
+//
+// Dictionary: open addressing with linear probing in HBM.  Keys are the
+// location (b, x0, x1, x2) packed into 64 bits (16 bits per field, b < 2^15
+// so no key equals the empty marker); values are feature rows.  Capacity is
+// a power of two >= 2n (load <= 1/2).
+//
+// Rule book layout: output rows are cut into tiles of kTile = 64 rows (one
+// wavefront); for every offset o and tile t the pairs whose output row lies
+// in t form one contiguous segment, segments ordered offset-major, and
+// within a segment pairs are in increasing output row.  A kernel that owns
+// a range of output tiles therefore finds all of its pairs for offset o in
+// one contiguous range, and the whole array is already sorted by
+// (offset, out row, in row) for export.
+//
+// SSC (Sec. 4.1, Sec. 4.2 last paragraph): the input dictionary is the
+// output dictionary; one wavefront per tile probes the f^3 neighbours of
+// its 64 sites, a ballot per offset counts the hits, a device-wide scan of
+// the (offset, tile) counts gives segment starts, and a second pass writes
+// each hit at its segment start + its rank among the wave's hits.
+//
+// SC (Sec. 4.1, Sec. 4.2 step 1): every input x visits the outputs y with
+// x = s*y + i; an output dictionary records, per output location, the
+// smallest visit index v = j*K + o (atomicMin).  The output rows are the
+// ranks of those first visits (a scan over visit flags), which numbers the
+// outputs in first-visit order with the inputs taken in row order.  From
+// the per-visit output rows an output-major neighbour map is written and
+// compacted exactly like the SSC one; the input-major map gives the
+// transposed (DC / dgrad) direction.
+#include <algorithm>
+#include <cstring>
+
+#include "internal.h"
+
+namespace sscn {
+
+// ------------------------------------------------------------- dictionary
+__device__ __forceinline__ uint64_t pack_key(int b, int x0, int x1, int x2) {
+  return ((uint64_t)(uint32_t)b << 48) | ((uint64_t)(uint32_t)x0 << 32) |
+         ((uint64_t)(uint32_t)x1 << 16) | (uint64_t)(uint32_t)x2;
+}
+
+// 64-bit finaliser of MurmurHash3 (public domain): spreads nearby locations
+// over the table.
+__device__ __forceinline__ uint64_t mix64(uint64_t k) {
+  k ^= k >> 33;
+  k *= 0xff51afd7ed558ccdull;
+  k ^= k >> 33;
+  k *= 0xc4ceb9fe1a85ec53ull;
+  k ^= k >> 33;
+  return k;
+}
+
+__device__ __forceinline__ int32_t table_lookup(const uint64_t* __restrict__ keys,
+                                                const int32_t* __restrict__ vals, uint64_t mask,
+                                                uint64_t key) {
+  uint64_t slot = mix64(key) & mask;
+  while (true) {
+    uint64_t k = keys[slot];
+    if (k == key) return vals[slot];
+    if (k == kEmptyKey) return -1;
+    slot = (slot + 1) & mask;
+  }
+}
+
+__device__ __forceinline__ bool in_grid(int x0, int x1, int x2, int L0, int L1, int L2) {
+  return (unsigned)x0 < (unsigned)L0 && (unsigned)x1 < (unsigned)L1 && (unsigned)x2 < (unsigned)L2;
+}
+
+// Insert every site; flag coordinates outside the grid and repeated locations.
+__global__ __launch_bounds__(256) void k_insert(const int4* __restrict__ coords, int64_t n, int L0,
+                                                int L1, int L2, uint64_t* __restrict__ keys,
+                                                int32_t* __restrict__ vals, uint64_t mask,
+                                                unsigned long long* __restrict__ flags) {
+  int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= n) return;
+  int4 c = coords[j];
+  if ((unsigned)c.x >= (unsigned)kMaxBatch || !in_grid(c.y, c.z, c.w, L0, L1, L2)) {
+    atomicOr(flags, (unsigned long long)kFlagOutOfRange);
+    return;
+  }
+  uint64_t key = pack_key(c.x, c.y, c.z, c.w);
+  uint64_t slot = mix64(key) & mask;
+  while (true) {
+    unsigned long long prev =
+        atomicCAS((unsigned long long*)&keys[slot], (unsigned long long)kEmptyKey,
+                  (unsigned long long)key);
+    if (prev == kEmptyKey) {
+      vals[slot] = (int32_t)j;
+      return;
+    }
+    if (prev == key) {
+      atomicOr(flags, (unsigned long long)kFlagDuplicate);
+      return;
+    }
+    slot = (slot + 1) & mask;
+  }
+}
+
+// ---------------------------------------------------------------- SSC probe
+// One wavefront per tile of 64 output sites.  nbr is offset-major [K][n]:
+// nbr[o*n + k] = row of the input at x_k + i_o - (f-1)/2, or -1.
+__global__ __launch_bounds__(256) void k_ssc_probe(
+    const int4* __restrict__ coords, int64_t n, int L0, int L1, int L2, int f,
+    const uint64_t* __restrict__ keys, const int32_t* __restrict__ vals, uint64_t mask,
+    int32_t* __restrict__ nbr, int64_t* __restrict__ counts, int64_t n_tiles,
+    unsigned long long* __restrict__ per_offset) {
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6);
+  if (t >= n_tiles) return;  // uniform per wavefront
+  const int64_t k = t * kTile + lane;
+  const bool valid = k < n;
+  int4 c = valid ? coords[k] : make_int4(0, 0, 0, 0);
+  const bool site_ok = valid && (unsigned)c.x < (unsigned)kMaxBatch && in_grid(c.y, c.z, c.w, L0, L1, L2);
+  const int K = f * f * f, h = (f - 1) / 2;
+  for (int o = 0; o < K; ++o) {
+    const int i0 = o / (f * f), i1 = (o / f) % f, i2 = o % f;
+    const int y0 = c.y + i0 - h, y1 = c.z + i1 - h, y2 = c.w + i2 - h;
+    int32_t row = -1;
+    if (site_ok && in_grid(y0, y1, y2, L0, L1, L2))
+      row = table_lookup(keys, vals, mask, pack_key(c.x, y0, y1, y2));
+    if (valid) nbr[(int64_t)o * n + k] = row;
+    const unsigned long long m = __ballot(row >= 0);
+    if (lane == 0) {
+      const int cnt = __popcll(m);
+      counts[(int64_t)o * n_tiles + t] = cnt;
+      if (cnt) atomicAdd(&per_offset[o], (unsigned long long)cnt);
+    }
+  }
+}
+
+// Count, per (offset, tile), the present entries of an offset-major
+// neighbour map (used for the SC directions).
+__global__ __launch_bounds__(256) void k_count_nbr(const int32_t* __restrict__ nbr, int64_t n_rows,
+                                                   int K, int64_t* __restrict__ counts,
+                                                   int64_t n_tiles) {
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6);
+  if (t >= n_tiles) return;
+  const int64_t k = t * kTile + lane;
+  const bool valid = k < n_rows;
+  for (int o = 0; o < K; ++o) {
+    const int32_t row = valid ? nbr[(int64_t)o * n_rows + k] : -1;
+    const unsigned long long m = __ballot(row >= 0);
+    if (lane == 0) counts[(int64_t)o * n_tiles + t] = __popcll(m);
+  }
+}
+
+// Write every present entry at its segment start + its rank among the
+// wavefront's present entries (so segments are sorted by output row).
+__global__ __launch_bounds__(256) void k_compact(const int32_t* __restrict__ nbr, int64_t n_rows, int K,
+                                                 const int64_t* __restrict__ seg, int64_t n_tiles,
+                                                 int32_t* __restrict__ in_rows,
+                                                 int32_t* __restrict__ out_rows) {
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6);
+  if (t >= n_tiles) return;
+  const int64_t k = t * kTile + lane;
+  const bool valid = k < n_rows;
+  const unsigned long long below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int o = 0; o < K; ++o) {
+    const int32_t row = valid ? nbr[(int64_t)o * n_rows + k] : -1;
+    const unsigned long long m = __ballot(row >= 0);
+    if (row >= 0) {
+      const int64_t pos = seg[(int64_t)o * n_tiles + t] + __popcll(m & below);
+      in_rows[pos] = row;
+      out_rows[pos] = (int32_t)k;
+    }
+  }
+}
+
+// ----------------------------------------------------------------- SC build
+struct ScGeom {
+  int f, s, K;
+  int L0, L1, L2;     // input extents
+  int M0, M1, M2;     // output extents
+};
+
+// Output location seen by input c at offset o, if any.
+__device__ __forceinline__ bool sc_target(const ScGeom& g, int4 c, int o, int& y0, int& y1, int& y2) {
+  const int i0 = o / (g.f * g.f), i1 = (o / g.f) % g.f, i2 = o % g.f;
+  const int t0 = c.y - i0, t1 = c.z - i1, t2 = c.w - i2;
+  if (t0 < 0 || t1 < 0 || t2 < 0) return false;
+  if (t0 % g.s || t1 % g.s || t2 % g.s) return false;
+  y0 = t0 / g.s; y1 = t1 / g.s; y2 = t2 / g.s;
+  return y0 < g.M0 && y1 < g.M1 && y2 < g.M2;
+}
+
+__device__ __forceinline__ bool site_in_range(int4 c, const ScGeom& g) {
+  return (unsigned)c.x < (unsigned)kMaxBatch && in_grid(c.y, c.z, c.w, g.L0, g.L1, g.L2);
+}
+
+// Record the first visit (smallest j*K + o) of every output location.
+__global__ __launch_bounds__(256) void k_sc_visit(const int4* __restrict__ coords, int64_t n, ScGeom g,
+                                                  uint64_t* __restrict__ okeys,
+                                                  int32_t* __restrict__ ovals, uint64_t omask) {
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= n) return;
+  const int4 c = coords[j];
+  if (!site_in_range(c, g)) return;
+  for (int o = 0; o < g.K; ++o) {
+    int y0, y1, y2;
+    if (!sc_target(g, c, o, y0, y1, y2)) continue;
+    const uint64_t key = pack_key(c.x, y0, y1, y2);
+    uint64_t slot = mix64(key) & omask;
+    while (true) {
+      unsigned long long prev =
+          atomicCAS((unsigned long long*)&okeys[slot], (unsigned long long)kEmptyKey,
+                    (unsigned long long)key);
+      if (prev == kEmptyKey || prev == key) break;
+      slot = (slot + 1) & omask;
+    }
+    atomicMin(&ovals[slot], (int32_t)(j * g.K + o));
+  }
+}
+
+// first[v] = 1 iff visit v is the first visit of its output; count pairs per offset.
+__global__ __launch_bounds__(256) void k_sc_mark(const int4* __restrict__ coords, int64_t n, ScGeom g,
+                                                 const uint64_t* __restrict__ okeys,
+                                                 const int32_t* __restrict__ ovals, uint64_t omask,
+                                                 int32_t* __restrict__ first,
+                                                 unsigned long long* __restrict__ per_offset) {
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const bool valid = j < n;
+  const int4 c = valid ? coords[j] : make_int4(0, 0, 0, 0);
+  const bool ok = valid && site_in_range(c, g);
+  const int lane = threadIdx.x & 63;
+  for (int o = 0; o < g.K; ++o) {
+    int y0, y1, y2;
+    int32_t is_first = 0;
+    const bool hit = ok && sc_target(g, c, o, y0, y1, y2);
+    if (hit) {
+      const int32_t v = (int32_t)(j * g.K + o);
+      is_first = table_lookup(okeys, ovals, omask, pack_key(c.x, y0, y1, y2)) == v;
+    }
+    if (valid) first[j * g.K + o] = is_first;
+    const unsigned long long m = __ballot(hit);
+    if (lane == 0 && m) atomicAdd(&per_offset[o], (unsigned long long)__popcll(m));
+  }
+}
+
+// Per visit: output row = rank of its output's first visit.  Writes the
+// output-major map nbr_out[o][k] = j, the input-major map nbr_in[o][j] = k,
+// and the output coordinates (by the first visitor).
+__global__ __launch_bounds__(256) void k_sc_assign(const int4* __restrict__ coords, int64_t n, ScGeom g,
+                                                   const uint64_t* __restrict__ okeys,
+                                                   const int32_t* __restrict__ ovals, uint64_t omask,
+                                                   const int32_t* __restrict__ rank, int64_t n_out,
+                                                   int32_t* __restrict__ nbr_out,
+                                                   int32_t* __restrict__ nbr_in,
+                                                   int4* __restrict__ out_coords) {
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= n) return;
+  const int4 c = coords[j];
+  if (!site_in_range(c, g)) return;
+  for (int o = 0; o < g.K; ++o) {
+    int y0, y1, y2;
+    if (!sc_target(g, c, o, y0, y1, y2)) continue;
+    const int32_t vmin = table_lookup(okeys, ovals, omask, pack_key(c.x, y0, y1, y2));
+    const int32_t k = rank[vmin];
+    nbr_out[(int64_t)o * n_out + k] = (int32_t)j;
+    nbr_in[(int64_t)o * n + j] = k;
+    if (vmin == (int32_t)(j * g.K + o)) out_coords[k] = make_int4(c.x, y0, y1, y2);
+  }
+}
+
+// ------------------------------------------------------------- host helpers
+static uint64_t table_capacity(int64_t n) {
+  uint64_t cap = 64;
+  while (cap < (uint64_t)(2 * n)) cap <<= 1;
+  return cap;
+}
+
+static inline unsigned grid_for(int64_t threads, int block) {
+  return (unsigned)std::max<int64_t>(1, ceil_div(threads, block));
+}
+
+// Scoped set of stream-ordered temporaries released on every exit path.
+struct Temps {
+  hipStream_t s;
+  std::vector<void*> ptrs;
+  explicit Temps(hipStream_t st) : s(st) {}
+  template <typename T>
+  sscn_status get(T** p, size_t count) {
+    sscn_status st = dev_alloc((void**)p, sizeof(T) * std::max<size_t>(count, 1), s);
+    if (st == SSCN_OK) ptrs.push_back(*p);
+    return st;
+  }
+  ~Temps() {
+    for (void* p : ptrs) dev_free(p, s);
+  }
+};
+
+#define SSCN_TRY(expr)                     \
+  do {                                     \
+    sscn_status st_ = (expr);              \
+    if (st_ != SSCN_OK) return st_;        \
+  } while (0)
+
+// Pinned host staging for the single readback of a build.
+static sscn_status readback(void* host, const void* dev, size_t bytes, hipStream_t s) {
+  static thread_local void* pinned = nullptr;
+  static thread_local size_t pinned_bytes = 0;
+  if (pinned_bytes < bytes) {
+    if (pinned) (void)hipHostFree(pinned);
+    pinned = nullptr;
+    pinned_bytes = 0;
+    SSCN_HIP(hipHostMalloc(&pinned, std::max<size_t>(bytes, 4096), hipHostMallocDefault));
+    pinned_bytes = std::max<size_t>(bytes, 4096);
+  }
+  SSCN_HIP(hipMemcpyAsync(pinned, dev, bytes, hipMemcpyDeviceToHost, s));
+  SSCN_HIP(hipStreamSynchronize(s));
+  std::memcpy(host, pinned, bytes);
+  return SSCN_OK;
+}
+
+// Build one direction's storage from an offset-major neighbour map.
+static sscn_status build_storage(const int32_t* nbr, int64_t n_rows, int K, int64_t n_pairs,
+                                 Storage& st, hipStream_t s, Temps& tmp, bool have_counts,
+                                 int64_t* counts) {
+  st.n_tiles = ceil_div(n_rows, kTile);
+  SSCN_TRY(dev_alloc((void**)&st.seg, sizeof(int64_t) * (K * st.n_tiles + 1), s));
+  if (!have_counts) {
+    if (st.n_tiles > 0) {
+      k_count_nbr<<<grid_for(st.n_tiles * 64, 256), 256, 0, s>>>(nbr, n_rows, K, st.seg, st.n_tiles);
+      SSCN_HIP(hipGetLastError());
+    }
+    SSCN_TRY(exclusive_scan_i64(st.seg, st.seg, K * st.n_tiles, s));
+  } else {
+    SSCN_TRY(exclusive_scan_i64(counts, st.seg, K * st.n_tiles, s));
+  }
+  SSCN_TRY(dev_alloc((void**)&st.in_rows, sizeof(int32_t) * std::max<int64_t>(n_pairs, 1), s));
+  SSCN_TRY(dev_alloc((void**)&st.out_rows, sizeof(int32_t) * std::max<int64_t>(n_pairs, 1), s));
+  if (st.n_tiles > 0 && n_pairs > 0) {
+    k_compact<<<grid_for(st.n_tiles * 64, 256), 256, 0, s>>>(nbr, n_rows, K, st.seg, st.n_tiles,
+                                                             st.in_rows, st.out_rows);
+    SSCN_HIP(hipGetLastError());
+  }
+  (void)tmp;
+  return SSCN_OK;
+}
+
+static sscn_status check_common(const int32_t* coords, int64_t n, const int32_t* spatial_size,
+                                int32_t f, sscn_rulebook* out) {
+  if (!out) return fail(SSCN_ERR_INVALID_ARG, "out handle pointer is NULL");
+  if (!spatial_size) return fail(SSCN_ERR_INVALID_ARG, "spatial_size is NULL");
+  if (n < 0) return fail(SSCN_ERR_INVALID_ARG, "n < 0");
+  if (n > 0 && !coords) return fail(SSCN_ERR_INVALID_ARG, "coords is NULL with n > 0");
+  if (n > 0 && ((uintptr_t)coords & 15)) return fail(SSCN_ERR_INVALID_ARG, "coords must be 16-byte aligned");
+  if (f < 1 || f > 8) return fail(SSCN_ERR_INVALID_ARG, "filter_size must be in [1, 8]");
+  for (int d = 0; d < 3; ++d)
+    if (spatial_size[d] < 1 || spatial_size[d] > kMaxExtent)
+      return fail(SSCN_ERR_INVALID_ARG, "spatial_size entries must be in [1, 65536]");
+  const int64_t K = (int64_t)f * f * f;
+  if (n * K >= (int64_t)INT32_MAX) return fail(SSCN_ERR_INVALID_ARG, "n * f^3 must be below 2^31");
+  return SSCN_OK;
+}
+
+static sscn_status flags_error(unsigned long long flags) {
+  if (flags & kFlagOutOfRange)
+    return fail(SSCN_ERR_OUT_OF_RANGE, "a coordinate lies outside the grid or the batch index outside [0, 32768)");
+  if (flags & kFlagDuplicate) return fail(SSCN_ERR_DUPLICATE, "two rows share one location");
+  return SSCN_OK;
+}
+
+static sscn_status new_handle(RulebookData* d, sscn_rulebook* out) {
+  sscn_rulebook_s* h = new (std::nothrow) sscn_rulebook_s;
+  if (!h) {
+    delete d;
+    return fail(SSCN_ERR_OOM, "host allocation failed");
+  }
+  h->d = d;
+  h->transposed = false;
+  *out = h;
+  return SSCN_OK;
+}
+
+}  // namespace sscn
+
+using namespace sscn;
+
+extern "C" sscn_status ssc_rulebook_build(const int32_t* coords, int64_t n, const int32_t* spatial_size,
+                                          int32_t filter_size, hipStream_t stream, sscn_rulebook* out) {
+  SSCN_TRY(check_common(coords, n, spatial_size, filter_size, out));
+  if (filter_size % 2 == 0) return fail(SSCN_ERR_INVALID_ARG, "SSC needs an odd filter_size");
+  const int f = filter_size, K = f * f * f;
+  const int L0 = spatial_size[0], L1 = spatial_size[1], L2 = spatial_size[2];
+  hipStream_t s = stream;
+
+  RulebookData* d = new (std::nothrow) RulebookData;
+  if (!d) return fail(SSCN_ERR_OOM, "host allocation failed");
+  std::unique_ptr<RulebookData> guard(d);
+  (void)hipGetDevice(&d->device);
+  d->stream = s;
+  d->f = f; d->stride = 1; d->K = K; d->submanifold = true;
+  d->n_in = d->n_out = n;
+  for (int i = 0; i < 3; ++i) d->in_size[i] = d->out_size[i] = spatial_size[i];
+  d->pairs_per_offset.assign(K, 0);
+
+  {
+    Temps tmp(s);
+    uint64_t cap = table_capacity(n);
+    uint64_t* keys; int32_t* vals; unsigned long long* stats;
+    SSCN_TRY(tmp.get(&keys, cap));
+    SSCN_TRY(tmp.get(&vals, cap));
+    SSCN_TRY(tmp.get(&stats, 1 + K));
+    SSCN_TRY(fill_u64((uint64_t*)stats, 0, 1 + K, s));
+    int32_t* nbr = nullptr;
+    int64_t* counts = nullptr;
+    const int64_t n_tiles = ceil_div(n, kTile);
+    if (n > 0) {
+      SSCN_TRY(fill_u64(keys, kEmptyKey, cap, s));
+      k_insert<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, L0, L1, L2, keys, vals, cap - 1,
+                                                stats);
+      SSCN_HIP(hipGetLastError());
+      SSCN_TRY(tmp.get(&nbr, (size_t)K * n));
+      SSCN_TRY(tmp.get(&counts, (size_t)K * n_tiles + 1));
+      k_ssc_probe<<<grid_for(n_tiles * 64, 256), 256, 0, s>>>((const int4*)coords, n, L0, L1, L2, f, keys,
+                                                             vals, cap - 1, nbr, counts, n_tiles, stats + 1);
+      SSCN_HIP(hipGetLastError());
+    }
+    std::vector<unsigned long long> host(1 + K);
+    SSCN_TRY(readback(host.data(), stats, sizeof(unsigned long long) * (1 + K), s));
+    SSCN_TRY(flags_error(host[0]));
+    int64_t total = 0;
+    for (int o = 0; o < K; ++o) total += (d->pairs_per_offset[o] = (int64_t)host[1 + o]);
+    d->n_pairs = total;
+    SSCN_TRY(build_storage(nbr, n, K, total, d->fwd, s, tmp, true, counts));
+    SSCN_TRY(dev_alloc((void**)&d->out_coords, sizeof(int32_t) * 4 * std::max<int64_t>(n, 1), s));
+    if (n > 0) SSCN_HIP(hipMemcpyAsync(d->out_coords, coords, sizeof(int32_t) * 4 * n, hipMemcpyDeviceToDevice, s));
+  }
+  guard.release();
+  return new_handle(d, out);
+}
+
+extern "C" sscn_status sc_rulebook_build(const int32_t* coords, int64_t n, const int32_t* spatial_size,
+                                         int32_t filter_size, int32_t stride, hipStream_t stream,
+                                         sscn_rulebook* out) {
+  SSCN_TRY(check_common(coords, n, spatial_size, filter_size, out));
+  if (stride < 1 || stride > 8) return fail(SSCN_ERR_INVALID_ARG, "stride must be in [1, 8]");
+  const int f = filter_size, s_ = stride, K = f * f * f;
+  ScGeom g;
+  g.f = f; g.s = s_; g.K = K;
+  g.L0 = spatial_size[0]; g.L1 = spatial_size[1]; g.L2 = spatial_size[2];
+  int M[3];
+  for (int dd = 0; dd < 3; ++dd) {
+    const int L = spatial_size[dd];
+    if (L < f || (L - f) % s_ != 0)
+      return fail(SSCN_ERR_SHAPE, "SC needs L >= f and (L - f) divisible by the stride in every dimension");
+    M[dd] = (L - f + s_) / s_;
+  }
+  g.M0 = M[0]; g.M1 = M[1]; g.M2 = M[2];
+  hipStream_t s = stream;
+
+  RulebookData* d = new (std::nothrow) RulebookData;
+  if (!d) return fail(SSCN_ERR_OOM, "host allocation failed");
+  std::unique_ptr<RulebookData> guard(d);
+  (void)hipGetDevice(&d->device);
+  d->stream = s;
+  d->f = f; d->stride = s_; d->K = K; d->submanifold = false;
+  d->n_in = n;
+  for (int i = 0; i < 3; ++i) { d->in_size[i] = spatial_size[i]; d->out_size[i] = M[i]; }
+  d->pairs_per_offset.assign(K, 0);
+
+  {
+    Temps tmp(s);
+    // outputs seen per input: prod over d of ceil(f / s) (at most K)
+    const int per_dim = (f + s_ - 1) / s_;
+    const int64_t max_out = n * (int64_t)per_dim * per_dim * per_dim;
+    uint64_t cap = table_capacity(n), ocap = table_capacity(max_out);
+    uint64_t* keys; int32_t* vals; uint64_t* okeys; int32_t* ovals; unsigned long long* stats;
+    int32_t* first; int32_t* rank;
+    SSCN_TRY(tmp.get(&stats, 1 + K));
+    SSCN_TRY(fill_u64((uint64_t*)stats, 0, 1 + K, s));
+    SSCN_TRY(tmp.get(&rank, (size_t)n * K + 1));
+    if (n > 0) {
+      SSCN_TRY(tmp.get(&keys, cap));
+      SSCN_TRY(tmp.get(&vals, cap));
+      SSCN_TRY(tmp.get(&okeys, ocap));
+      SSCN_TRY(tmp.get(&ovals, ocap));
+      SSCN_TRY(tmp.get(&first, (size_t)n * K));
+      SSCN_TRY(fill_u64(keys, kEmptyKey, cap, s));
+      SSCN_TRY(fill_u64(okeys, kEmptyKey, ocap, s));
+      SSCN_TRY(fill_i32(ovals, INT32_MAX, ocap, s));
+      // the input dictionary detects repeated locations and range errors
+      k_insert<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g.L0, g.L1, g.L2, keys, vals,
+                                                cap - 1, stats);
+      SSCN_HIP(hipGetLastError());
+      k_sc_visit<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, okeys, ovals, ocap - 1);
+      SSCN_HIP(hipGetLastError());
+      k_sc_mark<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, okeys, ovals, ocap - 1, first,
+                                                 stats + 1);
+      SSCN_HIP(hipGetLastError());
+      SSCN_TRY(exclusive_scan_i32(first, rank, n * K, s));
+    } else {
+      SSCN_TRY(fill_i32(rank, 0, 1, s));
+    }
+    std::vector<unsigned long long> host(1 + K);
+    SSCN_TRY(readback(host.data(), stats, sizeof(unsigned long long) * (1 + K), s));
+    int32_t n_out32 = 0;
+    SSCN_TRY(readback(&n_out32, rank + (size_t)n * K, sizeof(int32_t), s));
+    SSCN_TRY(flags_error(host[0]));
+    int64_t total = 0;
+    for (int o = 0; o < K; ++o) total += (d->pairs_per_offset[o] = (int64_t)host[1 + o]);
+    d->n_pairs = total;
+    const int64_t n_out = n_out32;
+    d->n_out = n_out;
+
+    SSCN_TRY(dev_alloc((void**)&d->out_coords, sizeof(int32_t) * 4 * std::max<int64_t>(n_out, 1), s));
+    SSCN_TRY(dev_alloc((void**)&d->in_coords, sizeof(int32_t) * 4 * std::max<int64_t>(n, 1), s));
+    if (n > 0) SSCN_HIP(hipMemcpyAsync(d->in_coords, coords, sizeof(int32_t) * 4 * n, hipMemcpyDeviceToDevice, s));
+    if (n > 0) {
+      int32_t* nbr_out; int32_t* nbr_in;
+      SSCN_TRY(tmp.get(&nbr_out, (size_t)K * n_out));
+      SSCN_TRY(tmp.get(&nbr_in, (size_t)K * n));
+      SSCN_TRY(fill_i32(nbr_out, -1, (int64_t)K * n_out, s));
+      SSCN_TRY(fill_i32(nbr_in, -1, (int64_t)K * n, s));
+      k_sc_assign<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, okeys, ovals, ocap - 1, rank,
+                                                   n_out, nbr_out, nbr_in, (int4*)d->out_coords);
+      SSCN_HIP(hipGetLastError());
+      SSCN_TRY(build_storage(nbr_out, n_out, K, total, d->fwd, s, tmp, false, nullptr));
+      SSCN_TRY(build_storage(nbr_in, n, K, total, d->bwd, s, tmp, false, nullptr));
+    } else {
+      SSCN_TRY(build_storage(nullptr, 0, K, 0, d->fwd, s, tmp, false, nullptr));
+      SSCN_TRY(build_storage(nullptr, 0, K, 0, d->bwd, s, tmp, false, nullptr));
+    }
+  }
+  guard.release();
+  return new_handle(d, out);
+}
+
+extern "C" sscn_status sscn_rulebook_transpose(sscn_rulebook rb, sscn_rulebook* out) {
+  if (!rb || !out) return fail(SSCN_ERR_INVALID_ARG, "NULL rule book or out pointer");
+  sscn_rulebook_s* h = new (std::nothrow) sscn_rulebook_s;
+  if (!h) return fail(SSCN_ERR_OOM, "host allocation failed");
+  rb->d->refs.fetch_add(1);
+  h->d = rb->d;
+  h->transposed = !rb->transposed;
+  *out = h;
+  return SSCN_OK;
+}
+
+extern "C" sscn_status sscn_rulebook_query(sscn_rulebook rb, sscn_rulebook_info* info, int64_t* ppo) {
+  if (!rb || !info) return fail(SSCN_ERR_INVALID_ARG, "NULL rule book or info pointer");
+  const RulebookData* d = rb->d;
+  const bool t = rb->transposed;
+  info->n_in = t ? d->n_out : d->n_in;
+  info->n_out = t ? d->n_in : d->n_out;
+  info->n_pairs = d->n_pairs;
+  info->filter_size = d->f;
+  info->stride = d->stride;
+  info->submanifold = d->submanifold ? 1 : 0;
+  info->transposed = t ? 1 : 0;
+  info->n_offsets = d->K;
+  for (int i = 0; i < 3; ++i) {
+    info->in_size[i] = t ? d->out_size[i] : d->in_size[i];
+    info->out_size[i] = t ? d->in_size[i] : d->out_size[i];
+  }
+  if (ppo) {
+    for (int o = 0; o < d->K; ++o) {
+      // a transposed SSC view holds R_{K-1-o} under offset o (same sizes by symmetry)
+      const int so = (t && d->submanifold) ? d->K - 1 - o : o;
+      ppo[o] = d->pairs_per_offset[so];
+    }
+  }
+  return SSCN_OK;
+}
+
+extern "C" sscn_status sscn_rulebook_out_coords(sscn_rulebook rb, int32_t* out_coords, hipStream_t s) {
+  if (!rb) return fail(SSCN_ERR_INVALID_ARG, "NULL rule book");
+  const RulebookData* d = rb->d;
+  const int64_t n_out = rb->transposed ? d->n_in : d->n_out;
+  if (n_out == 0) return SSCN_OK;
+  if (!out_coords) return fail(SSCN_ERR_INVALID_ARG, "out_coords is NULL");
+  // a transposed SC view outputs at the SC's input sites
+  const int32_t* src = (rb->transposed && !d->submanifold) ? d->in_coords : d->out_coords;
+  SSCN_HIP(hipMemcpyAsync(out_coords, src, sizeof(int32_t) * 4 * n_out, hipMemcpyDeviceToDevice, s));
+  return SSCN_OK;
+}
+
+extern "C" sscn_status sscn_rulebook_export(sscn_rulebook rb, int32_t* in_rows, int32_t* out_rows,
+                                            int32_t* offsets, hipStream_t s) {
+  if (!rb) return fail(SSCN_ERR_INVALID_ARG, "NULL rule book");
+  const RulebookData* d = rb->d;
+  if (d->n_pairs == 0) return SSCN_OK;
+  if (!in_rows || !out_rows || !offsets) return fail(SSCN_ERR_INVALID_ARG, "NULL export array");
+  const View v = view_of(rb);
+  // stored segment boundaries per offset: seg[o * n_tiles], read on the host
+  std::vector<int64_t> start(d->K + 1);
+  int64_t acc = 0;
+  for (int o = 0; o < d->K; ++o) { start[o] = acc; acc += d->pairs_per_offset[o]; }
+  start[d->K] = acc;
+  int64_t pos = 0;
+  for (int o = 0; o < d->K; ++o) {
+    const int so = v.mirror ? d->K - 1 - o : o;
+    const int64_t cnt = d->pairs_per_offset[so];
+    if (!cnt) continue;
+    SSCN_HIP(hipMemcpyAsync(in_rows + pos, v.st->in_rows + start[so], sizeof(int32_t) * cnt,
+                            hipMemcpyDeviceToDevice, s));
+    SSCN_HIP(hipMemcpyAsync(out_rows + pos, v.st->out_rows + start[so], sizeof(int32_t) * cnt,
+                            hipMemcpyDeviceToDevice, s));
+    SSCN_TRY(fill_i32(offsets + pos, o, cnt, s));
+    pos += cnt;
+  }
+  return SSCN_OK;
+}
+
+extern "C" void sscn_rulebook_free(sscn_rulebook rb) {
+  if (!rb) return;
+  if (rb->d->refs.fetch_sub(1) == 1) delete rb->d;
+  delete rb;
+}

@@ -1,0 +1,226 @@
+// Error reporting, stream-ordered device memory, fills and a device-wide
+// exclusive scan used by the rule-book builders.
+#include <cstdio>
+#include <mutex>
+
+#include "internal.h"
+
+namespace sscn {
+
+static thread_local std::string g_last_error;
+
+void set_error(const std::string& msg) { g_last_error = msg; }
+
+sscn_status fail(sscn_status st, const std::string& msg) {
+  set_error(msg);
+  return st;
+}
+
+sscn_status hip_fail(hipError_t e, const char* what) {
+  set_error(std::string(what) + ": " + hipGetErrorString(e));
+  return e == hipErrorOutOfMemory ? SSCN_ERR_OOM : SSCN_ERR_DEVICE;
+}
+
+// ------------------------------------------------------------------ memory
+static std::once_flag g_pool_once[64];
+
+static void keep_pool_cached(int dev) {
+  if (dev < 0 || dev >= 64) return;
+  std::call_once(g_pool_once[dev], [dev] {
+    hipMemPool_t pool;
+    if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
+      uint64_t threshold = ~0ull;
+      (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &threshold);
+    }
+  });
+}
+
+sscn_status dev_alloc(void** p, size_t bytes, hipStream_t s) {
+  *p = nullptr;
+  if (bytes == 0) return SSCN_OK;
+  int dev = 0;
+  SSCN_HIP(hipGetDevice(&dev));
+  keep_pool_cached(dev);
+  hipError_t e = hipMallocAsync(p, bytes, s);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    *p = nullptr;
+    return fail(e == hipErrorOutOfMemory ? SSCN_ERR_OOM : SSCN_ERR_DEVICE,
+                std::string("device allocation of ") + std::to_string(bytes) + " bytes failed: " +
+                    hipGetErrorString(e));
+  }
+  return SSCN_OK;
+}
+
+void dev_free(void* p, hipStream_t s) {
+  if (p) (void)hipFreeAsync(p, s);
+}
+
+RulebookData::~RulebookData() {
+  int cur = 0;
+  (void)hipGetDevice(&cur);
+  if (cur != device) (void)hipSetDevice(device);
+  for (Storage* st : {&fwd, &bwd}) {
+    dev_free(st->seg, stream);
+    dev_free(st->in_rows, stream);
+    dev_free(st->out_rows, stream);
+  }
+  dev_free(out_coords, stream);
+  dev_free(in_coords, stream);
+  if (cur != device) (void)hipSetDevice(cur);
+}
+
+// ------------------------------------------------------------------- fills
+template <typename T>
+__global__ void k_fill(T* __restrict__ p, T v, int64_t count) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  int64_t step = (int64_t)gridDim.x * blockDim.x;
+  for (; i < count; i += step) p[i] = v;
+}
+
+template <typename T>
+static sscn_status fill(T* p, T v, int64_t count, hipStream_t s) {
+  if (count <= 0) return SSCN_OK;
+  int64_t blocks = ceil_div(count, 256);
+  if (blocks > 65536) blocks = 65536;
+  k_fill<T><<<dim3((unsigned)blocks), dim3(256), 0, s>>>(p, v, count);
+  SSCN_HIP(hipGetLastError());
+  return SSCN_OK;
+}
+
+sscn_status fill_i32(int32_t* p, int32_t v, int64_t count, hipStream_t s) { return fill(p, v, count, s); }
+sscn_status fill_u64(uint64_t* p, uint64_t v, int64_t count, hipStream_t s) { return fill(p, v, count, s); }
+sscn_status fill_f32(float* p, float v, int64_t count, hipStream_t s) { return fill(p, v, count, s); }
+
+// -------------------------------------------------------------------- scan
+// Two-level reduce-then-scan.  A block covers kScanItems * kScanThreads
+// consecutive elements; block totals are scanned recursively.
+constexpr int kScanThreads = 256;
+constexpr int kScanItems = 16;
+constexpr int64_t kScanChunk = (int64_t)kScanThreads * kScanItems;
+
+template <typename T>
+__device__ T block_exclusive_sum(T v, T* lds_wave, T& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  T x = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    T y = __shfl_up(x, d, 64);
+    if (lane >= d) x += y;
+  }
+  if (lane == 63) lds_wave[wave] = x;
+  __syncthreads();
+  T wave_off = 0, tot = 0;
+  for (int w = 0; w < kScanThreads / 64; ++w) {
+    T t = lds_wave[w];
+    if (w < wave) wave_off += t;
+    tot += t;
+  }
+  total = tot;
+  __syncthreads();
+  return wave_off + x - v;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kScanThreads) void k_scan_reduce(const T* __restrict__ in, int64_t count,
+                                                             T* __restrict__ partial) {
+  __shared__ T lds_wave[kScanThreads / 64];
+  const int64_t base = (int64_t)blockIdx.x * kScanChunk;
+  T s = 0;
+#pragma unroll
+  for (int i = 0; i < kScanItems; ++i) {
+    int64_t idx = base + (int64_t)i * kScanThreads + threadIdx.x;
+    if (idx < count) s += in[idx];
+  }
+  T total;
+  (void)block_exclusive_sum<T>(s, lds_wave, total);
+  if (threadIdx.x == 0) partial[blockIdx.x] = total;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kScanThreads) void k_scan_apply(const T* in, int64_t count,
+                                                            const T* __restrict__ partial, T* out) {
+  __shared__ T tile[kScanChunk];
+  __shared__ T lds_wave[kScanThreads / 64];
+  const int64_t base = (int64_t)blockIdx.x * kScanChunk;
+  // coalesced load into LDS
+#pragma unroll
+  for (int i = 0; i < kScanItems; ++i) {
+    int e = i * kScanThreads + threadIdx.x;
+    int64_t idx = base + e;
+    tile[e] = idx < count ? in[idx] : T(0);
+  }
+  __syncthreads();
+  // each thread owns kScanItems consecutive elements
+  T local[kScanItems];
+  T s = 0;
+#pragma unroll
+  for (int i = 0; i < kScanItems; ++i) {
+    local[i] = tile[threadIdx.x * kScanItems + i];
+    s += local[i];
+  }
+  T total;
+  const T carry = partial ? partial[blockIdx.x] : T(0);
+  T run = block_exclusive_sum<T>(s, lds_wave, total) + carry;
+#pragma unroll
+  for (int i = 0; i < kScanItems; ++i) {
+    tile[threadIdx.x * kScanItems + i] = run;
+    run += local[i];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < kScanItems; ++i) {
+    int e = i * kScanThreads + threadIdx.x;
+    int64_t idx = base + e;
+    if (idx < count) out[idx] = tile[e];
+  }
+  // the block holding the last element also writes the grand total
+  if (count - 1 < base + kScanChunk && threadIdx.x == 0) out[count] = carry + total;
+}
+
+template <typename T>
+__global__ void k_scan_store_zero(T* out) { out[0] = 0; }
+
+template <typename T>
+static sscn_status exclusive_scan(const T* in, T* out, int64_t count, hipStream_t s) {
+  if (count <= 0) {
+    k_scan_store_zero<T><<<1, 1, 0, s>>>(out);
+    SSCN_HIP(hipGetLastError());
+    return SSCN_OK;
+  }
+  const int64_t blocks = ceil_div(count, kScanChunk);
+  if (blocks == 1) {
+    k_scan_apply<T><<<1, kScanThreads, 0, s>>>(in, count, nullptr, out);
+    SSCN_HIP(hipGetLastError());
+    return SSCN_OK;
+  }
+  T* partial = nullptr;
+  sscn_status st = dev_alloc((void**)&partial, sizeof(T) * (blocks + 1), s);
+  if (st != SSCN_OK) return st;
+  k_scan_reduce<T><<<dim3((unsigned)blocks), kScanThreads, 0, s>>>(in, count, partial);
+  hipError_t e = hipGetLastError();
+  if (e == hipSuccess) {
+    st = exclusive_scan<T>(partial, partial, blocks, s);
+    if (st == SSCN_OK) {
+      k_scan_apply<T><<<dim3((unsigned)blocks), kScanThreads, 0, s>>>(in, count, partial, out);
+      e = hipGetLastError();
+    }
+  }
+  dev_free(partial, s);
+  if (e != hipSuccess) return hip_fail(e, "scan launch");
+  return st;
+}
+
+// The recursive call above scans `partial` in place; in-place use is safe
+// because every block reads all of its chunk into LDS before writing it and
+// the grand total goes to index `count`, past the input.
+sscn_status exclusive_scan_i64(const int64_t* in, int64_t* out, int64_t count, hipStream_t s) {
+  return exclusive_scan<int64_t>(in, out, count, s);
+}
+sscn_status exclusive_scan_i32(const int32_t* in, int32_t* out, int64_t count, hipStream_t s) {
+  return exclusive_scan<int32_t>(in, out, count, s);
+}
+
+}  // namespace sscn
+
+extern "C" const char* sscn_last_error(void) { return sscn::g_last_error.c_str(); }

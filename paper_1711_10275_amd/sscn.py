@@ -1,0 +1,259 @@
+"""Python binding of libsscn.so (ctypes; argument marshalling only).
+
+Every step of the layers runs in the library's HIP kernels.  torch supplies
+device memory (outputs are allocated with torch.empty on the input's device)
+and the stream (the current torch stream of that device).  There is no CPU
+fallback: if the library is missing or a tensor is not on a GPU, the call
+raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libsscn.so")
+HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "sscn.h")
+
+F32, BF16 = 0, 1
+STATUS = {0: "ok", 1: "invalid_arg", 2: "shape", 3: "out_of_range", 4: "duplicate", 5: "oom", 6: "device"}
+
+
+class SSCNError(RuntimeError):
+    def __init__(self, code, msg):
+        self.code = STATUS.get(code, str(code))
+        super().__init__(f"sscn error {self.code}: {msg}")
+
+
+class RulebookInfo(ctypes.Structure):
+    _fields_ = [("n_in", ctypes.c_int64), ("n_out", ctypes.c_int64), ("n_pairs", ctypes.c_int64),
+                ("filter_size", ctypes.c_int32), ("stride", ctypes.c_int32),
+                ("submanifold", ctypes.c_int32), ("transposed", ctypes.c_int32),
+                ("n_offsets", ctypes.c_int32), ("in_size", ctypes.c_int32 * 3),
+                ("out_size", ctypes.c_int32 * 3)]
+
+
+_lib = None
+_vp, _i32, _i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+_SIGS = {
+    "ssc_rulebook_build": [_vp, _i64, _vp, _i32, _vp, _vp],
+    "sc_rulebook_build": [_vp, _i64, _vp, _i32, _i32, _vp, _vp],
+    "sscn_rulebook_transpose": [_vp, _vp],
+    "sscn_rulebook_query": [_vp, _vp, _vp],
+    "sscn_rulebook_out_coords": [_vp, _vp, _vp],
+    "sscn_rulebook_export": [_vp, _vp, _vp, _vp, _vp],
+    "sscn_rulebook_free": [_vp],
+    "sparse_conv_forward": [_vp, _vp, _vp, _i32, _i32, ctypes.c_int, _vp, _vp],
+    "sparse_conv_backward": [_vp, _vp, _vp, _vp, _i32, _i32, ctypes.c_int, _vp, _vp, _vp],
+    "sscn_affine_relu": [_vp, _vp, _vp, _i64, _i32, ctypes.c_int, _vp, _vp],
+    "sscn_concat_cols": [_vp, _i32, _vp, _i32, _i64, ctypes.c_int, _vp, _vp],
+    "sscn_last_error": [],
+}
+
+
+def lib():
+    """Load libsscn.so (built in-tree by the package's _build module)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it first (__graft_entry__.build())")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, args in _SIGS.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = ctypes.c_char_p if name == "sscn_last_error" else (
+                None if name == "sscn_rulebook_free" else ctypes.c_int)
+        _lib = L
+    return _lib
+
+
+def header_functions():
+    """Names of the functions declared in include/sscn.h."""
+    text = open(HEADER_PATH).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(\w+)\s*\([^;{]*\)\s*;", text)) - {"if", "while"})
+
+
+def _check(code):
+    if code != 0:
+        raise SSCNError(code, lib().sscn_last_error().decode())
+
+
+def _stream(t):
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _dev_tensor(t, name, dtype=None):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _dtype_code(t):
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise ValueError(f"unsupported dtype {t.dtype} (float32 or bfloat16)")
+
+
+class Rulebook:
+    """Owning wrapper of an sscn_rulebook handle."""
+
+    def __init__(self, handle, device):
+        self._h = handle
+        self.device = device
+        info = RulebookInfo()
+        _check(lib().sscn_rulebook_query(self._h, ctypes.byref(info), None))
+        K = info.n_offsets
+        ppo = (ctypes.c_int64 * K)()
+        _check(lib().sscn_rulebook_query(self._h, ctypes.byref(info), ppo))
+        self.n_in, self.n_out, self.n_pairs = info.n_in, info.n_out, info.n_pairs
+        self.filter_size, self.stride = info.filter_size, info.stride
+        self.submanifold, self.transposed = bool(info.submanifold), bool(info.transposed)
+        self.n_offsets = K
+        self.in_size, self.out_size = tuple(info.in_size), tuple(info.out_size)
+        self.pairs_per_offset = list(ppo)
+
+    @property
+    def handle(self):
+        return self._h
+
+    def transpose(self):
+        h = ctypes.c_void_p()
+        _check(lib().sscn_rulebook_transpose(self._h, ctypes.byref(h)))
+        return Rulebook(h, self.device)
+
+    def out_coords(self):
+        out = torch.empty((self.n_out, 4), dtype=torch.int32, device=self.device)
+        with torch.cuda.device(self.device):
+            _check(lib().sscn_rulebook_out_coords(self._h, ctypes.c_void_p(out.data_ptr()), _stream(out)))
+        return out
+
+    def export(self):
+        """(in_rows, out_rows, offsets) int32 tensors sorted by (offset, out, in)."""
+        a = [torch.empty(self.n_pairs, dtype=torch.int32, device=self.device) for _ in range(3)]
+        with torch.cuda.device(self.device):
+            _check(lib().sscn_rulebook_export(self._h, *[ctypes.c_void_p(x.data_ptr()) for x in a],
+                                              _stream(a[0])))
+        return tuple(a)
+
+    def macs(self, cin, cout):
+        return self.n_pairs * cin * cout
+
+    def free(self):
+        if self._h is not None and self._h.value:
+            lib().sscn_rulebook_free(self._h)
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
+def _sizes(spatial_size):
+    s = tuple(int(v) for v in spatial_size)
+    if len(s) != 3:
+        raise ValueError("spatial_size must have 3 entries")
+    return (ctypes.c_int32 * 3)(*s)
+
+
+def ssc_rulebook_build(coords, spatial_size, filter_size=3):
+    coords = _dev_tensor(coords, "coords", torch.int32)
+    h = ctypes.c_void_p()
+    with torch.cuda.device(coords.device):
+        _check(lib().ssc_rulebook_build(ctypes.c_void_p(coords.data_ptr()), coords.shape[0],
+                                        _sizes(spatial_size), int(filter_size), _stream(coords),
+                                        ctypes.byref(h)))
+    return Rulebook(h, coords.device)
+
+
+def sc_rulebook_build(coords, spatial_size, filter_size=2, stride=2):
+    coords = _dev_tensor(coords, "coords", torch.int32)
+    h = ctypes.c_void_p()
+    with torch.cuda.device(coords.device):
+        _check(lib().sc_rulebook_build(ctypes.c_void_p(coords.data_ptr()), coords.shape[0],
+                                       _sizes(spatial_size), int(filter_size), int(stride),
+                                       _stream(coords), ctypes.byref(h)))
+    return Rulebook(h, coords.device)
+
+
+def sparse_conv_forward(features, weights, rulebook):
+    """out[k] = sum over (j, k) in R_o of features[j] @ weights[o]."""
+    features = _dev_tensor(features, "features")
+    weights = _dev_tensor(weights, "weights", features.dtype)
+    K, cin, cout = weights.shape
+    if K != rulebook.n_offsets or features.shape != (rulebook.n_in, cin):
+        raise ValueError("features / weights do not match the rule book")
+    out = torch.empty((rulebook.n_out, cout), dtype=features.dtype, device=features.device)
+    with torch.cuda.device(features.device):
+        _check(lib().sparse_conv_forward(ctypes.c_void_p(features.data_ptr()),
+                                         ctypes.c_void_p(weights.data_ptr()), rulebook.handle, cin, cout,
+                                         _dtype_code(features), ctypes.c_void_p(out.data_ptr()),
+                                         _stream(features)))
+    return out
+
+
+def sparse_conv_backward(features, weights, dout, rulebook, dgrad=True, wgrad=True):
+    """(dgrad, wgrad) of sparse_conv_forward; wgrad is float32."""
+    weights = _dev_tensor(weights, "weights")
+    dout = _dev_tensor(dout, "dout", weights.dtype)
+    K, cin, cout = weights.shape
+    if K != rulebook.n_offsets or dout.shape != (rulebook.n_out, cout):
+        raise ValueError("dout / weights do not match the rule book")
+    dev = weights.device
+    fptr = None
+    if wgrad:
+        features = _dev_tensor(features, "features", weights.dtype)
+        if features.shape != (rulebook.n_in, cin):
+            raise ValueError("features do not match the rule book")
+        fptr = ctypes.c_void_p(features.data_ptr())
+    dx = torch.empty((rulebook.n_in, cin), dtype=weights.dtype, device=dev) if dgrad else None
+    dw = torch.empty((K, cin, cout), dtype=torch.float32, device=dev) if wgrad else None
+    with torch.cuda.device(dev):
+        _check(lib().sparse_conv_backward(fptr, ctypes.c_void_p(weights.data_ptr()),
+                                          ctypes.c_void_p(dout.data_ptr()), rulebook.handle, cin, cout,
+                                          _dtype_code(weights),
+                                          ctypes.c_void_p(dx.data_ptr()) if dx is not None else None,
+                                          ctypes.c_void_p(dw.data_ptr()) if dw is not None else None,
+                                          _stream(dout)))
+    return dx, dw
+
+
+def affine_relu(x, scale, shift, out=None):
+    """max(0, x * scale + shift) per channel over the active rows."""
+    x = _dev_tensor(x, "x")
+    n, c = x.shape
+    scale = _dev_tensor(scale, "scale", torch.float32)
+    shift = _dev_tensor(shift, "shift", torch.float32)
+    if scale.numel() != c or shift.numel() != c:
+        raise ValueError("scale / shift must have one entry per channel")
+    y = torch.empty_like(x) if out is None else _dev_tensor(out, "out", x.dtype)
+    with torch.cuda.device(x.device):
+        _check(lib().sscn_affine_relu(ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(scale.data_ptr()),
+                                      ctypes.c_void_p(shift.data_ptr()), n, c, _dtype_code(x),
+                                      ctypes.c_void_p(y.data_ptr()), _stream(x)))
+    return y
+
+
+def concat_cols(a, b):
+    """[a | b] row by row."""
+    a = _dev_tensor(a, "a")
+    b = _dev_tensor(b, "b", a.dtype)
+    if a.shape[0] != b.shape[0]:
+        raise ValueError("row counts differ")
+    y = torch.empty((a.shape[0], a.shape[1] + b.shape[1]), dtype=a.dtype, device=a.device)
+    with torch.cuda.device(a.device):
+        _check(lib().sscn_concat_cols(ctypes.c_void_p(a.data_ptr()), a.shape[1], ctypes.c_void_p(b.data_ptr()),
+                                      b.shape[1], a.shape[0], _dtype_code(a), ctypes.c_void_p(y.data_ptr()),
+                                      _stream(a)))
+    return y

@@ -1,0 +1,185 @@
+"""GPU forward / backward of SSC, SC and DC layers against the fp64 CPU oracle."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import sscn_oracle as O
+from paper_1711_10275_amd import sscn
+from paper_1711_10275_amd import synthetic as S
+from tests.gpu_common import coords_for, dev, host, small_set
+from tests.parity import assert_close
+
+pytestmark = pytest.mark.gpu
+
+TD = {"f32": torch.float32, "bf16": torch.bfloat16}
+
+
+def _draw(n, cin, cout, K, seed, dtype):
+    bf = dtype == "bf16"
+    X = S.features(n, cin, S.SEED_FEAT + seed, bf16=bf)
+    W = S.weights(K, cin, cout, S.SEED_WEIGHT + seed, bf16=bf)
+    return X, W
+
+
+def _fwd(rb, X, W, dtype):
+    return host(sscn.sparse_conv_forward(dev(X, TD[dtype]), dev(W, TD[dtype]), rb))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("config,c", [("shell32", 16), ("shapes128", 64)])
+def test_ssc_forward_workloads(config, c, dtype):
+    coords, size = coords_for(config)
+    rb = sscn.ssc_rulebook_build(dev(coords), size, 3)
+    orb = O.ssc_rulebook(coords, size, 3)
+    X, W = _draw(coords.shape[0], c, c, 27, 1, dtype)
+    assert_close(_fwd(rb, X, W, dtype), O.forward(X, W, orb), dtype, f"{config} {dtype}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_sc_then_ssc_forward(dtype):
+    """SC(2,2) 64 -> 96 channels at 128^3 -> 64^3, then SSC 3^3 with 96 channels."""
+    coords, size = coords_for("shapes128")
+    sc = sscn.sc_rulebook_build(dev(coords), size, 2, 2)
+    osc = O.sc_rulebook(coords, size, 2, 2)
+    X, W = _draw(coords.shape[0], 64, 96, 8, 2, dtype)
+    Y = _fwd(sc, X, W, dtype)
+    assert_close(Y, O.forward(X, W, osc), dtype, "sc22")
+    oc = host(sc.out_coords())
+    ssc = sscn.ssc_rulebook_build(dev(oc), sc.out_size, 3)
+    W2 = S.weights(27, 96, 96, S.SEED_WEIGHT + 22, bf16=dtype == "bf16")
+    Yr = Y.astype(np.float32)  # the GPU's own SC output feeds both sides
+    assert_close(_fwd(ssc, Yr, W2, dtype), O.forward(Yr, W2, O.ssc_rulebook(oc, sc.out_size, 3)), dtype, "ssc64")
+
+
+CH = [(1, 1), (3, 5), (16, 16), (32, 48), (70, 33), (130, 20), (64, 136), (8, 300)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("cin,cout", CH)
+def test_ssc_forward_channel_shapes(cin, cout, dtype):
+    size = (9, 10, 11)
+    c = small_set(cin * 7 + cout, size, batch=2, density=0.2)
+    rb = sscn.ssc_rulebook_build(dev(c), size, 3)
+    X, W = _draw(c.shape[0], cin, cout, 27, cin + cout, dtype)
+    assert_close(_fwd(rb, X, W, dtype), O.forward(X, W, O.ssc_rulebook(c, size, 3)), dtype, f"{cin}x{cout}")
+
+
+@pytest.mark.parametrize("f,s", [(2, 2), (3, 2), (3, 1), (1, 1)])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_sc_and_dc_forward_small(f, s, dtype):
+    size = (9, 9, 9) if f == 3 and s == 2 else (8, 8, 8)
+    if (f, s) == (1, 1):
+        size = (7, 7, 7)
+    c = small_set(f * 10 + s, size, batch=2, density=0.25)
+    rb = sscn.sc_rulebook_build(dev(c), size, f, s)
+    orb = O.sc_rulebook(c, size, f, s)
+    X, W = _draw(c.shape[0], 12, 20, f ** 3, 5, dtype)
+    assert_close(_fwd(rb, X, W, dtype), O.forward(X, W, orb), dtype, "sc")
+    # DC: transposed rule book with its own weights, outputs at the SC input sites
+    Xd, Wd = _draw(rb.n_out, 20, 7, f ** 3, 6, dtype)
+    assert_close(_fwd(rb.transpose(), Xd, Wd, dtype), O.forward(Xd, Wd, O.transpose(orb)), dtype, "dc")
+
+
+def test_shapecontext_identity_is_exact():
+    """SSC(1,27,3) with identity weights and X[j] = j + 1 decodes the rule book exactly."""
+    coords, size = coords_for("shell32")
+    n = coords.shape[0]
+    rb = sscn.ssc_rulebook_build(dev(coords), size, 3)
+    X = (np.arange(n, dtype=np.float32) + 1)[:, None]
+    W = np.eye(27, dtype=np.float32).reshape(27, 1, 27)
+    Y = _fwd(rb, X, W, "f32")
+    orb = O.ssc_rulebook(coords, size, 3)
+    np.testing.assert_array_equal(Y, O.forward(X, W, orb))
+    for o in range(27):
+        k = np.nonzero(Y[:, o])[0]
+        np.testing.assert_array_equal(k, orb.outs[o])
+        np.testing.assert_array_equal(Y[k, o].astype(np.int64) - 1, orb.ins[o])
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_integer_inputs_are_exact(dtype):
+    coords, size = coords_for("shell32")
+    rng = np.random.default_rng(0)
+    X = rng.integers(-1, 2, (coords.shape[0], 4)).astype(np.float32)
+    W = rng.integers(-1, 2, (27, 4, 6)).astype(np.float32)
+    rb = sscn.ssc_rulebook_build(dev(coords), size, 3)
+    Y = _fwd(rb, X, W, dtype)
+    np.testing.assert_array_equal(Y, O.forward(X, W, O.ssc_rulebook(coords, size, 3)))
+    G = rng.integers(-1, 2, (coords.shape[0], 6)).astype(np.float32)
+    dx, dw = sscn.sparse_conv_backward(dev(X, TD[dtype]), dev(W, TD[dtype]), dev(G, TD[dtype]), rb)
+    rdx, rdw = O.backward(X, W, G, O.ssc_rulebook(coords, size, 3))
+    np.testing.assert_array_equal(host(dx), rdx)
+    np.testing.assert_array_equal(host(dw), rdw)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_ssc_backward_shapes128(dtype):
+    """The 128^3 layer (C = 64): dgrad via the transposed rule book and per-offset wgrad."""
+    coords, size = coords_for("shapes128")
+    rb = sscn.ssc_rulebook_build(dev(coords), size, 3)
+    orb = O.ssc_rulebook(coords, size, 3)
+    X, W = _draw(coords.shape[0], 64, 64, 27, 4, dtype)
+    G = S.features(coords.shape[0], 64, S.SEED_GRAD + 4, bf16=dtype == "bf16")
+    dx, dw = sscn.sparse_conv_backward(dev(X, TD[dtype]), dev(W, TD[dtype]), dev(G, TD[dtype]), rb)
+    rdx, rdw = O.backward(X, W, G, orb)
+    assert_close(host(dx), rdx, dtype, "dgrad")
+    assert_close(host(dw), rdw, "f32" if dtype == "f32" else "bf16", "wgrad")
+    # dgrad only / wgrad only
+    dx2, none = sscn.sparse_conv_backward(None, dev(W, TD[dtype]), dev(G, TD[dtype]), rb, wgrad=False)
+    assert none is None
+    np.testing.assert_array_equal(host(dx2), host(dx))
+
+
+@pytest.mark.parametrize("f,s", [(2, 2), (3, 2)])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_sc_and_dc_backward_small(f, s, dtype):
+    size = (8, 8, 8) if s == 2 and f == 2 else (9, 9, 9)
+    c = small_set(40 + f, size, batch=2, density=0.25)
+    rb = sscn.sc_rulebook_build(dev(c), size, f, s)
+    orb = O.sc_rulebook(c, size, f, s)
+    for view, oview, (cin, cout) in ((rb, orb, (10, 18)), (rb.transpose(), O.transpose(orb), (18, 10))):
+        X, W = _draw(view.n_in, cin, cout, f ** 3, 8, dtype)
+        G = S.features(view.n_out, cout, S.SEED_GRAD + 8, bf16=dtype == "bf16")
+        dx, dw = sscn.sparse_conv_backward(dev(X, TD[dtype]), dev(W, TD[dtype]), dev(G, TD[dtype]), view)
+        rdx, rdw = O.backward(X, W, G, oview)
+        assert_close(host(dx), rdx, dtype, "dgrad")
+        assert_close(host(dw), rdw, dtype, "wgrad")
+
+
+def test_sc22_backward_shapes128():
+    coords, size = coords_for("shapes128")
+    rb = sscn.sc_rulebook_build(dev(coords), size, 2, 2)
+    orb = O.sc_rulebook(coords, size, 2, 2)
+    X, W = _draw(coords.shape[0], 64, 96, 8, 9, "f32")
+    G = S.features(rb.n_out, 96, S.SEED_GRAD + 9)
+    dx, dw = sscn.sparse_conv_backward(dev(X), dev(W), dev(G), rb)
+    rdx, rdw = O.backward(X, W, G, orb)
+    assert_close(host(dx), rdx, "f32", "dgrad")
+    assert_close(host(dw), rdw, "f32", "wgrad")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_affine_relu_and_concat(dtype):
+    rng = np.random.default_rng(3)
+    n, c = 1000, 24
+    x = S.bf16_round(rng.standard_normal((n, c)).astype(np.float32)) if dtype == "bf16" else \
+        rng.standard_normal((n, c)).astype(np.float32)
+    scale = rng.uniform(0.5, 1.5, c).astype(np.float32)
+    shift = rng.normal(0, 0.1, c).astype(np.float32)
+    y = host(sscn.affine_relu(dev(x, TD[dtype]), dev(scale), dev(shift)))
+    ref = np.maximum(0.0, x.astype(np.float64) * scale + shift)
+    assert_close(y, ref, dtype, "affine_relu")
+    b = rng.standard_normal((n, 7)).astype(np.float32)
+    b = S.bf16_round(b) if dtype == "bf16" else b
+    cat = host(sscn.concat_cols(dev(x, TD[dtype]), dev(b, TD[dtype])))
+    np.testing.assert_array_equal(cat, np.concatenate([x, b], axis=1))
+
+
+def test_empty_layer():
+    empty = torch.zeros((0, 4), dtype=torch.int32, device="cuda:0")
+    rb = sscn.ssc_rulebook_build(empty, (8, 8, 8), 3)
+    y = sscn.sparse_conv_forward(torch.zeros((0, 4), device="cuda:0"), torch.zeros((27, 4, 5), device="cuda:0"), rb)
+    assert y.shape == (0, 5)
+    dx, dw = sscn.sparse_conv_backward(torch.zeros((0, 4), device="cuda:0"), torch.zeros((27, 4, 5), device="cuda:0"),
+                                       torch.zeros((0, 5), device="cuda:0"), rb)
+    assert dx.shape == (0, 4) and float(dw.abs().sum()) == 0.0

@@ -1,0 +1,132 @@
+"""GPU rule books are bit-exact against the CPU oracle (sorted (in, out, offset) pairs)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import sscn_oracle as O
+from paper_1711_10275_amd import sscn
+from tests.gpu_common import assert_same_rulebook, coords_for, dev, host, small_set
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("config", ["shell32", "shapes128"])
+def test_ssc_rulebook_workloads(config):
+    c, size = coords_for(config)
+    rb = sscn.ssc_rulebook_build(dev(c), size, 3)
+    orb = O.ssc_rulebook(c, size, 3)
+    assert_same_rulebook(rb, orb, config)
+    np.testing.assert_array_equal(host(rb.out_coords()), c)
+    # transposed view = mirrored offsets
+    assert_same_rulebook(rb.transpose(), O.transpose(orb), config + " transposed")
+
+
+def test_sc_then_ssc_on_shapes128():
+    """SC(2,2) 128^3 -> 64^3, then SSC 3^3 at 64^3 on the SC's output set."""
+    c, size = coords_for("shapes128")
+    rb = sscn.sc_rulebook_build(dev(c), size, 2, 2)
+    orb = O.sc_rulebook(c, size, 2, 2)
+    assert rb.out_size == (64, 64, 64)
+    assert_same_rulebook(rb, orb, "sc22")
+    oc = host(rb.out_coords())
+    np.testing.assert_array_equal(oc, orb.out_coords)
+    assert_same_rulebook(rb.transpose(), O.transpose(orb), "sc22 transposed")
+    rb2 = sscn.ssc_rulebook_build(dev(oc), rb.out_size, 3)
+    assert_same_rulebook(rb2, O.ssc_rulebook(oc, rb.out_size, 3), "ssc64")
+
+
+def test_scenes256_level0_rulebooks():
+    """Full-size 256^3 x 8 scenes (about 2M sites): SSC and SC(2,2) rule books."""
+    c, size = coords_for("scenes256")
+    rb = sscn.ssc_rulebook_build(dev(c), size, 3)
+    assert_same_rulebook(rb, O.ssc_rulebook(c, size, 3), "scenes ssc")
+    del rb
+    sc = sscn.sc_rulebook_build(dev(c), size, 2, 2)
+    osc = O.sc_rulebook(c, size, 2, 2)
+    assert_same_rulebook(sc, osc, "scenes sc22")
+    np.testing.assert_array_equal(host(sc.out_coords()), osc.out_coords)
+
+
+CASES = [((8, 8, 8), 3), ((7, 9, 6), 3), ((6, 6, 6), 1), ((9, 9, 9), 5), ((5, 11, 4), 3)]
+
+
+@pytest.mark.parametrize("size,f", CASES)
+@pytest.mark.parametrize("seed", range(4))
+def test_ssc_rulebook_small(size, f, seed):
+    c = small_set(seed, size, batch=1 + seed % 3, density=0.1 + 0.1 * (seed % 3))
+    rb = sscn.ssc_rulebook_build(dev(c), size, f)
+    orb = O.ssc_rulebook(c, size, f)
+    assert_same_rulebook(rb, orb, f"ssc {size} f={f}")
+    assert_same_rulebook(rb.transpose(), O.transpose(orb), "transposed")
+
+
+SC_CASES = [((8, 8, 8), 2, 2), ((9, 7, 11), 3, 2), ((8, 8, 8), 3, 1), ((6, 6, 6), 1, 1),
+            ((9, 9, 9), 3, 3), ((10, 6, 8), 2, 1), ((7, 7, 7), 1, 2)]
+
+
+@pytest.mark.parametrize("size,f,s", SC_CASES)
+@pytest.mark.parametrize("seed", range(3))
+def test_sc_rulebook_small(size, f, s, seed):
+    c = small_set(10 + seed, size, batch=1 + seed, density=0.12 + 0.1 * seed)
+    rb = sscn.sc_rulebook_build(dev(c), size, f, s)
+    orb = O.sc_rulebook(c, size, f, s)
+    assert rb.out_size == orb.out_size
+    assert_same_rulebook(rb, orb, f"sc {size} f={f} s={s}")
+    np.testing.assert_array_equal(host(rb.out_coords()), orb.out_coords)
+    rbt = rb.transpose()
+    assert_same_rulebook(rbt, O.transpose(orb), "transposed")
+    np.testing.assert_array_equal(host(rbt.out_coords()), c)
+
+
+def test_worked_example_on_gpu():
+    """One interior site: SSC keeps it; SC(3,1) twice gives 27 then 125 sites (Sec. 3)."""
+    site = np.array([[0, 5, 5, 5]], np.int32)
+    assert sscn.ssc_rulebook_build(dev(site), (11, 11, 11), 3).n_out == 1
+    rb = sscn.sc_rulebook_build(dev(site), (11, 11, 11), 3, 1)
+    assert rb.n_out == 27
+    rb2 = sscn.sc_rulebook_build(rb.out_coords(), rb.out_size, 3, 1)
+    assert rb2.n_out == 125
+
+
+def test_empty_and_errors():
+    empty = torch.zeros((0, 4), dtype=torch.int32, device="cuda:0")
+    rb = sscn.ssc_rulebook_build(empty, (8, 8, 8), 3)
+    assert rb.n_out == 0 and rb.n_pairs == 0
+    sc = sscn.sc_rulebook_build(empty, (8, 8, 8), 2, 2)
+    assert sc.n_out == 0 and sc.n_pairs == 0
+    c = np.array([[0, 1, 1, 1], [1, 2, 2, 2], [0, 1, 1, 1]], np.int32)
+    for build in (lambda t: sscn.ssc_rulebook_build(t, (8, 8, 8), 3),
+                  lambda t: sscn.sc_rulebook_build(t, (8, 8, 8), 2, 2)):
+        with pytest.raises(sscn.SSCNError) as e:
+            build(dev(c))
+        assert e.value.code == "duplicate"
+        for bad in ([[0, 8, 0, 0]], [[0, 0, -1, 0]], [[-1, 0, 0, 0]], [[32768, 0, 0, 0]]):
+            with pytest.raises(sscn.SSCNError) as e:
+                build(dev(np.array(bad, np.int32)))
+            assert e.value.code == "out_of_range"
+    with pytest.raises(sscn.SSCNError) as e:
+        sscn.ssc_rulebook_build(dev(c[:2]), (8, 8, 8), 4)
+    assert e.value.code == "invalid_arg"
+    with pytest.raises(sscn.SSCNError) as e:
+        sscn.sc_rulebook_build(dev(c[:2]), (9, 8, 8), 2, 2)
+    assert e.value.code == "shape"
+
+
+def test_rulebook_build_is_deterministic():
+    c, size = coords_for("shapes128")
+    a = [host(x) for x in sscn.ssc_rulebook_build(dev(c), size, 3).export()]
+    b = [host(x) for x in sscn.ssc_rulebook_build(dev(c), size, 3).export()]
+    for x, y in zip(a, b):
+        np.testing.assert_array_equal(x, y)
+
+
+def test_shuffled_rows():
+    """Row order is arbitrary: a permuted input gives the permuted rule book."""
+    c, size = coords_for("shell32")
+    perm = np.random.default_rng(0).permutation(c.shape[0])
+    cp = np.ascontiguousarray(c[perm])
+    assert_same_rulebook(sscn.ssc_rulebook_build(dev(cp), size, 3), O.ssc_rulebook(cp, size, 3), "shuffled")
+    sc = sscn.sc_rulebook_build(dev(cp), size, 2, 2)
+    osc = O.sc_rulebook(cp, size, 2, 2)
+    assert_same_rulebook(sc, osc, "shuffled sc")
+    np.testing.assert_array_equal(host(sc.out_coords()), osc.out_coords)
