@@ -46,7 +46,8 @@ sscn_status dev_alloc(void** p, size_t bytes, hipStream_t s);
 void dev_free(void* p, hipStream_t s);
 
 // One direction of a rule book: tiles over the output rows of that
-// direction, offset-major segments, and the pair arrays.
+// direction, offset-major segments, and the pair arrays (pointers into the
+// rule book's device blocks).
 struct Storage {
   int64_t n_tiles = 0;
   int64_t* seg = nullptr;        // K * n_tiles + 1 entries
@@ -67,6 +68,7 @@ struct RulebookData {
   Storage bwd;                   // tiles over input rows (SC only; SSC mirrors fwd)
   int32_t* out_coords = nullptr; // n_out x 4
   int32_t* in_coords = nullptr;  // n_in x 4 (SC only; an SSC's input sites are its output sites)
+  std::vector<void*> blocks;     // device allocations owning all of the above
   ~RulebookData();
 };
 

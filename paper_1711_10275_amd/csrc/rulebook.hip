@@ -1,9 +1,10 @@
 // Rule-book construction on the GPU (Sec. 4.2 of the paper).
 //
-// Dictionary: open addressing with linear probing in HBM.  Keys are the
-// location (b, x0, x1, x2) packed into 64 bits (16 bits per field, b < 2^15
-// so no key equals the empty marker); values are feature rows.  Capacity is
-// a power of two >= 2n (load <= 1/2).
+// Dictionary: open addressing with linear probing in HBM.  A slot is 16
+// bytes {key, row}: the location (b, x0, x1, x2) packed into 64 bits (16
+// bits per field, b < 2^15 so no key equals the empty marker) and the
+// feature row, so one 16-byte load answers a probe.  Capacity is a power of
+// two >= 2n (load <= 1/2).
 //
 // Rule book layout: output rows are cut into tiles of kTile = 64 rows (one
 // wavefront); for every offset o and tile t the pairs whose output row lies
@@ -51,15 +52,32 @@ __device__ __forceinline__ uint64_t mix64(uint64_t k) {
   return k;
 }
 
-__device__ __forceinline__ int32_t table_lookup(const uint64_t* __restrict__ keys,
-                                                const int32_t* __restrict__ vals, uint64_t mask,
-                                                uint64_t key) {
+struct __align__(16) Slot {
+  uint64_t key;
+  int32_t row;
+  int32_t pad;
+};
+
+__device__ __forceinline__ int32_t table_lookup(const Slot* __restrict__ table, uint64_t mask, uint64_t key) {
   uint64_t slot = mix64(key) & mask;
   while (true) {
-    uint64_t k = keys[slot];
-    if (k == key) return vals[slot];
-    if (k == kEmptyKey) return -1;
+    const Slot v = table[slot];
+    if (v.key == key) return v.row;
+    if (v.key == kEmptyKey) return -1;
     slot = (slot + 1) & mask;
+  }
+}
+
+// Every slot empty; the row field starts at row_init (INT32_MAX for the
+// first-visit minimum of the SC output dictionary).
+__global__ void k_fill_slots(Slot* __restrict__ table, uint64_t cap, int32_t row_init) {
+  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < cap;
+       i += (uint64_t)gridDim.x * blockDim.x) {
+    Slot v;
+    v.key = kEmptyKey;
+    v.row = row_init;
+    v.pad = 0;
+    table[i] = v;
   }
 }
 
@@ -69,8 +87,7 @@ __device__ __forceinline__ bool in_grid(int x0, int x1, int x2, int L0, int L1, 
 
 // Insert every site; flag coordinates outside the grid and repeated locations.
 __global__ __launch_bounds__(256) void k_insert(const int4* __restrict__ coords, int64_t n, int L0,
-                                                int L1, int L2, uint64_t* __restrict__ keys,
-                                                int32_t* __restrict__ vals, uint64_t mask,
+                                                int L1, int L2, Slot* __restrict__ table, uint64_t mask,
                                                 unsigned long long* __restrict__ flags) {
   int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (j >= n) return;
@@ -83,10 +100,10 @@ __global__ __launch_bounds__(256) void k_insert(const int4* __restrict__ coords,
   uint64_t slot = mix64(key) & mask;
   while (true) {
     unsigned long long prev =
-        atomicCAS((unsigned long long*)&keys[slot], (unsigned long long)kEmptyKey,
+        atomicCAS((unsigned long long*)&table[slot].key, (unsigned long long)kEmptyKey,
                   (unsigned long long)key);
     if (prev == kEmptyKey) {
-      vals[slot] = (int32_t)j;
+      table[slot].row = (int32_t)j;
       return;
     }
     if (prev == key) {
@@ -100,33 +117,63 @@ __global__ __launch_bounds__(256) void k_insert(const int4* __restrict__ coords,
 // ---------------------------------------------------------------- SSC probe
 // One wavefront per tile of 64 output sites.  nbr is offset-major [K][n]:
 // nbr[o*n + k] = row of the input at x_k + i_o - (f-1)/2, or -1.
+// counts[o*n_tiles + t] = number of hits of tile t at offset o (ballot).
+// F > 0: compile-time filter size; the probes of one i0-plane (F*F offsets)
+// are issued together so their loads overlap.  F == 0: runtime f.
+template <int F>
 __global__ __launch_bounds__(256) void k_ssc_probe(
-    const int4* __restrict__ coords, int64_t n, int L0, int L1, int L2, int f,
-    const uint64_t* __restrict__ keys, const int32_t* __restrict__ vals, uint64_t mask,
-    int32_t* __restrict__ nbr, int64_t* __restrict__ counts, int64_t n_tiles,
-    unsigned long long* __restrict__ per_offset) {
+    const int4* __restrict__ coords, int64_t n, int L0, int L1, int L2, int f_rt,
+    const Slot* __restrict__ table, uint64_t mask, int32_t* __restrict__ nbr, int64_t* __restrict__ counts,
+    int64_t n_tiles) {
+  const int f = F > 0 ? F : f_rt;
   const int lane = threadIdx.x & 63;
   const int64_t t = (int64_t)blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6);
   if (t >= n_tiles) return;  // uniform per wavefront
   const int64_t k = t * kTile + lane;
   const bool valid = k < n;
-  int4 c = valid ? coords[k] : make_int4(0, 0, 0, 0);
+  const int4 c = valid ? coords[k] : make_int4(0, 0, 0, 0);
   const bool site_ok = valid && (unsigned)c.x < (unsigned)kMaxBatch && in_grid(c.y, c.z, c.w, L0, L1, L2);
-  const int K = f * f * f, h = (f - 1) / 2;
-  for (int o = 0; o < K; ++o) {
-    const int i0 = o / (f * f), i1 = (o / f) % f, i2 = o % f;
-    const int y0 = c.y + i0 - h, y1 = c.z + i1 - h, y2 = c.w + i2 - h;
-    int32_t row = -1;
-    if (site_ok && in_grid(y0, y1, y2, L0, L1, L2))
-      row = table_lookup(keys, vals, mask, pack_key(c.x, y0, y1, y2));
-    if (valid) nbr[(int64_t)o * n + k] = row;
-    const unsigned long long m = __ballot(row >= 0);
-    if (lane == 0) {
-      const int cnt = __popcll(m);
-      counts[(int64_t)o * n_tiles + t] = cnt;
-      if (cnt) atomicAdd(&per_offset[o], (unsigned long long)cnt);
+  const int h = (f - 1) / 2;
+  constexpr int P = F > 0 ? F * F : 1;  // probes in flight per lane
+  const int plane = f * f;
+  for (int o0 = 0; o0 < f * f * f; o0 += (F > 0 ? P : 1)) {
+    uint64_t key[P];
+    uint64_t slot[P];
+    bool live[P];
+    Slot v[P];
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+      const int o = o0 + q;
+      const int i0 = o / plane, i1 = (o / f) % f, i2 = o % f;
+      const int y0 = c.y + i0 - h, y1 = c.z + i1 - h, y2 = c.w + i2 - h;
+      live[q] = site_ok && in_grid(y0, y1, y2, L0, L1, L2);
+      key[q] = pack_key(c.x, y0, y1, y2);
+      slot[q] = mix64(key[q]) & mask;
+      if (live[q]) v[q] = table[slot[q]];
+    }
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+      const int o = o0 + q;
+      int32_t row = -1;
+      if (live[q]) {
+        while (v[q].key != key[q] && v[q].key != kEmptyKey) {
+          slot[q] = (slot[q] + 1) & mask;
+          v[q] = table[slot[q]];
+        }
+        if (v[q].key == key[q]) row = v[q].row;
+      }
+      if (valid) nbr[(int64_t)o * n + k] = row;
+      const unsigned long long bal = __ballot(row >= 0);
+      if (lane == 0) counts[(int64_t)o * n_tiles + t] = __popcll(bal);
     }
   }
+}
+
+// stats[1 + o] = |R_o| = seg[(o+1) T] - seg[o T] after the scan.
+__global__ void k_offset_totals(const int64_t* __restrict__ seg, int64_t n_tiles, int K,
+                                unsigned long long* __restrict__ stats) {
+  const int o = blockIdx.x * blockDim.x + threadIdx.x;
+  if (o < K) stats[1 + o] = (unsigned long long)(seg[(int64_t)(o + 1) * n_tiles] - seg[(int64_t)o * n_tiles]);
 }
 
 // Count, per (offset, tile), the present entries of an offset-major
@@ -192,8 +239,7 @@ __device__ __forceinline__ bool site_in_range(int4 c, const ScGeom& g) {
 
 // Record the first visit (smallest j*K + o) of every output location.
 __global__ __launch_bounds__(256) void k_sc_visit(const int4* __restrict__ coords, int64_t n, ScGeom g,
-                                                  uint64_t* __restrict__ okeys,
-                                                  int32_t* __restrict__ ovals, uint64_t omask) {
+                                                  Slot* __restrict__ otable, uint64_t omask) {
   const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (j >= n) return;
   const int4 c = coords[j];
@@ -205,21 +251,25 @@ __global__ __launch_bounds__(256) void k_sc_visit(const int4* __restrict__ coord
     uint64_t slot = mix64(key) & omask;
     while (true) {
       unsigned long long prev =
-          atomicCAS((unsigned long long*)&okeys[slot], (unsigned long long)kEmptyKey,
+          atomicCAS((unsigned long long*)&otable[slot].key, (unsigned long long)kEmptyKey,
                     (unsigned long long)key);
       if (prev == kEmptyKey || prev == key) break;
       slot = (slot + 1) & omask;
     }
-    atomicMin(&ovals[slot], (int32_t)(j * g.K + o));
+    atomicMin(&otable[slot].row, (int32_t)(j * g.K + o));
   }
 }
 
-// first[v] = 1 iff visit v is the first visit of its output; count pairs per offset.
+// first[v] = 1 iff visit v is the first visit of its output; count pairs
+// per offset (wave ballots summed in LDS, one global atomic per block and
+// offset).
 __global__ __launch_bounds__(256) void k_sc_mark(const int4* __restrict__ coords, int64_t n, ScGeom g,
-                                                 const uint64_t* __restrict__ okeys,
-                                                 const int32_t* __restrict__ ovals, uint64_t omask,
+                                                 const Slot* __restrict__ otable, uint64_t omask,
                                                  int32_t* __restrict__ first,
                                                  unsigned long long* __restrict__ per_offset) {
+  __shared__ unsigned int cnt[512];
+  for (int o = threadIdx.x; o < g.K; o += blockDim.x) cnt[o] = 0;
+  __syncthreads();
   const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const bool valid = j < n;
   const int4 c = valid ? coords[j] : make_int4(0, 0, 0, 0);
@@ -231,20 +281,22 @@ __global__ __launch_bounds__(256) void k_sc_mark(const int4* __restrict__ coords
     const bool hit = ok && sc_target(g, c, o, y0, y1, y2);
     if (hit) {
       const int32_t v = (int32_t)(j * g.K + o);
-      is_first = table_lookup(okeys, ovals, omask, pack_key(c.x, y0, y1, y2)) == v;
+      is_first = table_lookup(otable, omask, pack_key(c.x, y0, y1, y2)) == v;
     }
     if (valid) first[j * g.K + o] = is_first;
     const unsigned long long m = __ballot(hit);
-    if (lane == 0 && m) atomicAdd(&per_offset[o], (unsigned long long)__popcll(m));
+    if (lane == 0 && m) atomicAdd(&cnt[o], (unsigned int)__popcll(m));
   }
+  __syncthreads();
+  for (int o = threadIdx.x; o < g.K; o += blockDim.x)
+    if (cnt[o]) atomicAdd(&per_offset[o], (unsigned long long)cnt[o]);
 }
 
 // Per visit: output row = rank of its output's first visit.  Writes the
 // output-major map nbr_out[o][k] = j, the input-major map nbr_in[o][j] = k,
 // and the output coordinates (by the first visitor).
 __global__ __launch_bounds__(256) void k_sc_assign(const int4* __restrict__ coords, int64_t n, ScGeom g,
-                                                   const uint64_t* __restrict__ okeys,
-                                                   const int32_t* __restrict__ ovals, uint64_t omask,
+                                                   const Slot* __restrict__ otable, uint64_t omask,
                                                    const int32_t* __restrict__ rank, int64_t n_out,
                                                    int32_t* __restrict__ nbr_out,
                                                    int32_t* __restrict__ nbr_in,
@@ -256,7 +308,7 @@ __global__ __launch_bounds__(256) void k_sc_assign(const int4* __restrict__ coor
   for (int o = 0; o < g.K; ++o) {
     int y0, y1, y2;
     if (!sc_target(g, c, o, y0, y1, y2)) continue;
-    const int32_t vmin = table_lookup(okeys, ovals, omask, pack_key(c.x, y0, y1, y2));
+    const int32_t vmin = table_lookup(otable, omask, pack_key(c.x, y0, y1, y2));
     const int32_t k = rank[vmin];
     nbr_out[(int64_t)o * n_out + k] = (int32_t)j;
     nbr_in[(int64_t)o * n + j] = k;
@@ -275,27 +327,50 @@ static inline unsigned grid_for(int64_t threads, int block) {
   return (unsigned)std::max<int64_t>(1, ceil_div(threads, block));
 }
 
-// Scoped set of stream-ordered temporaries released on every exit path.
+#define SSCN_TRY(expr)                     \
+  do {                                     \
+    sscn_status st_ = (expr);              \
+    if (st_ != SSCN_OK) return st_;        \
+  } while (0)
+
+// One device allocation carved into 256-byte aligned parts.
+struct Arena {
+  size_t total = 0;
+  std::vector<std::pair<void**, size_t>> parts;
+  template <typename T>
+  void add(T** p, size_t count) {
+    parts.push_back({(void**)p, total});
+    total += (std::max<size_t>(count, 1) * sizeof(T) + 255) & ~(size_t)255;
+  }
+  sscn_status alloc(void** base, hipStream_t s) {
+    SSCN_TRY(dev_alloc(base, total, s));
+    for (auto& pr : parts) *pr.first = (char*)*base + pr.second;
+    return SSCN_OK;
+  }
+};
+
+// Stream-ordered temporaries released (after the queued work) on every exit path.
 struct Temps {
   hipStream_t s;
   std::vector<void*> ptrs;
   explicit Temps(hipStream_t st) : s(st) {}
-  template <typename T>
-  sscn_status get(T** p, size_t count) {
-    sscn_status st = dev_alloc((void**)p, sizeof(T) * std::max<size_t>(count, 1), s);
-    if (st == SSCN_OK) ptrs.push_back(*p);
-    return st;
+  sscn_status alloc(Arena& a) {
+    void* base = nullptr;
+    SSCN_TRY(a.alloc(&base, s));
+    ptrs.push_back(base);
+    return SSCN_OK;
   }
   ~Temps() {
     for (void* p : ptrs) dev_free(p, s);
   }
 };
 
-#define SSCN_TRY(expr)                     \
-  do {                                     \
-    sscn_status st_ = (expr);              \
-    if (st_ != SSCN_OK) return st_;        \
-  } while (0)
+static sscn_status owned_alloc(RulebookData* d, Arena& a, hipStream_t s) {
+  void* base = nullptr;
+  SSCN_TRY(a.alloc(&base, s));
+  d->blocks.push_back(base);
+  return SSCN_OK;
+}
 
 // Pinned host staging for the single readback of a build.
 static sscn_status readback(void* host, const void* dev, size_t bytes, hipStream_t s) {
@@ -314,29 +389,26 @@ static sscn_status readback(void* host, const void* dev, size_t bytes, hipStream
   return SSCN_OK;
 }
 
-// Build one direction's storage from an offset-major neighbour map.
-static sscn_status build_storage(const int32_t* nbr, int64_t n_rows, int K, int64_t n_pairs,
-                                 Storage& st, hipStream_t s, Temps& tmp, bool have_counts,
-                                 int64_t* counts) {
-  st.n_tiles = ceil_div(n_rows, kTile);
-  SSCN_TRY(dev_alloc((void**)&st.seg, sizeof(int64_t) * (K * st.n_tiles + 1), s));
-  if (!have_counts) {
-    if (st.n_tiles > 0) {
-      k_count_nbr<<<grid_for(st.n_tiles * 64, 256), 256, 0, s>>>(nbr, n_rows, K, st.seg, st.n_tiles);
-      SSCN_HIP(hipGetLastError());
-    }
-    SSCN_TRY(exclusive_scan_i64(st.seg, st.seg, K * st.n_tiles, s));
-  } else {
-    SSCN_TRY(exclusive_scan_i64(counts, st.seg, K * st.n_tiles, s));
-  }
-  SSCN_TRY(dev_alloc((void**)&st.in_rows, sizeof(int32_t) * std::max<int64_t>(n_pairs, 1), s));
-  SSCN_TRY(dev_alloc((void**)&st.out_rows, sizeof(int32_t) * std::max<int64_t>(n_pairs, 1), s));
-  if (st.n_tiles > 0 && n_pairs > 0) {
-    k_compact<<<grid_for(st.n_tiles * 64, 256), 256, 0, s>>>(nbr, n_rows, K, st.seg, st.n_tiles,
-                                                             st.in_rows, st.out_rows);
+static sscn_status launch_fill_slots(Slot* t, uint64_t cap, int32_t row_init, hipStream_t s) {
+  k_fill_slots<<<(unsigned)std::min<uint64_t>((cap + 255) / 256, 16384), 256, 0, s>>>(t, cap, row_init);
+  SSCN_HIP(hipGetLastError());
+  return SSCN_OK;
+}
+
+// Segment table and pair arrays of one direction from an offset-major
+// neighbour map (st.seg, st.in_rows and st.out_rows already allocated).
+static sscn_status compact_storage(const int32_t* nbr, int64_t n_rows, int K, Storage& st, hipStream_t s,
+                                   bool counted) {
+  if (!counted && st.n_tiles > 0) {
+    k_count_nbr<<<grid_for(st.n_tiles * 64, 256), 256, 0, s>>>(nbr, n_rows, K, st.seg, st.n_tiles);
     SSCN_HIP(hipGetLastError());
   }
-  (void)tmp;
+  if (!counted) SSCN_TRY(exclusive_scan_i64(st.seg, st.seg, K * st.n_tiles, s));
+  if (st.n_tiles > 0) {
+    k_compact<<<grid_for(st.n_tiles * 64, 256), 256, 0, s>>>(nbr, n_rows, K, st.seg, st.n_tiles, st.in_rows,
+                                                             st.out_rows);
+    SSCN_HIP(hipGetLastError());
+  }
   return SSCN_OK;
 }
 
@@ -396,28 +468,42 @@ extern "C" sscn_status ssc_rulebook_build(const int32_t* coords, int64_t n, cons
   d->n_in = d->n_out = n;
   for (int i = 0; i < 3; ++i) d->in_size[i] = d->out_size[i] = spatial_size[i];
   d->pairs_per_offset.assign(K, 0);
+  const int64_t n_tiles = ceil_div(n, kTile);
+  d->fwd.n_tiles = n_tiles;
 
   {
     Temps tmp(s);
-    uint64_t cap = table_capacity(n);
-    uint64_t* keys; int32_t* vals; unsigned long long* stats;
-    SSCN_TRY(tmp.get(&keys, cap));
-    SSCN_TRY(tmp.get(&vals, cap));
-    SSCN_TRY(tmp.get(&stats, 1 + K));
+    const uint64_t cap = table_capacity(n);
+    Slot* table; int32_t* nbr; int64_t* counts; unsigned long long* stats;
+    Arena ta;
+    ta.add(&table, cap);
+    ta.add(&nbr, (size_t)K * n);
+    ta.add(&counts, (size_t)K * n_tiles + 1);
+    ta.add(&stats, 1 + K);
+    SSCN_TRY(tmp.alloc(ta));
+    Arena oa;  // owned by the rule book, needed before the readback
+    oa.add(&d->fwd.seg, (size_t)K * n_tiles + 1);
+    oa.add(&d->out_coords, (size_t)4 * n);
+    SSCN_TRY(owned_alloc(d, oa, s));
+
     SSCN_TRY(fill_u64((uint64_t*)stats, 0, 1 + K, s));
-    int32_t* nbr = nullptr;
-    int64_t* counts = nullptr;
-    const int64_t n_tiles = ceil_div(n, kTile);
     if (n > 0) {
-      SSCN_TRY(fill_u64(keys, kEmptyKey, cap, s));
-      k_insert<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, L0, L1, L2, keys, vals, cap - 1,
-                                                stats);
+      SSCN_TRY(launch_fill_slots(table, cap, -1, s));
+      k_insert<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, L0, L1, L2, table, cap - 1, stats);
       SSCN_HIP(hipGetLastError());
-      SSCN_TRY(tmp.get(&nbr, (size_t)K * n));
-      SSCN_TRY(tmp.get(&counts, (size_t)K * n_tiles + 1));
-      k_ssc_probe<<<grid_for(n_tiles * 64, 256), 256, 0, s>>>((const int4*)coords, n, L0, L1, L2, f, keys,
-                                                             vals, cap - 1, nbr, counts, n_tiles, stats + 1);
+      if (f == 3)
+        k_ssc_probe<3><<<grid_for(n_tiles * 64, 256), 256, 0, s>>>((const int4*)coords, n, L0, L1, L2, f, table,
+                                                                  cap - 1, nbr, counts, n_tiles);
+      else
+        k_ssc_probe<0><<<grid_for(n_tiles * 64, 256), 256, 0, s>>>((const int4*)coords, n, L0, L1, L2, f, table,
+                                                                  cap - 1, nbr, counts, n_tiles);
       SSCN_HIP(hipGetLastError());
+    }
+    SSCN_TRY(exclusive_scan_i64(counts, d->fwd.seg, K * n_tiles, s));
+    if (n > 0) {
+      k_offset_totals<<<grid_for(K, 256), 256, 0, s>>>(d->fwd.seg, n_tiles, K, stats);
+      SSCN_HIP(hipGetLastError());
+      SSCN_HIP(hipMemcpyAsync(d->out_coords, coords, sizeof(int32_t) * 4 * n, hipMemcpyDeviceToDevice, s));
     }
     std::vector<unsigned long long> host(1 + K);
     SSCN_TRY(readback(host.data(), stats, sizeof(unsigned long long) * (1 + K), s));
@@ -425,9 +511,11 @@ extern "C" sscn_status ssc_rulebook_build(const int32_t* coords, int64_t n, cons
     int64_t total = 0;
     for (int o = 0; o < K; ++o) total += (d->pairs_per_offset[o] = (int64_t)host[1 + o]);
     d->n_pairs = total;
-    SSCN_TRY(build_storage(nbr, n, K, total, d->fwd, s, tmp, true, counts));
-    SSCN_TRY(dev_alloc((void**)&d->out_coords, sizeof(int32_t) * 4 * std::max<int64_t>(n, 1), s));
-    if (n > 0) SSCN_HIP(hipMemcpyAsync(d->out_coords, coords, sizeof(int32_t) * 4 * n, hipMemcpyDeviceToDevice, s));
+    Arena pa;
+    pa.add(&d->fwd.in_rows, total);
+    pa.add(&d->fwd.out_rows, total);
+    SSCN_TRY(owned_alloc(d, pa, s));
+    if (total > 0) SSCN_TRY(compact_storage(nbr, n, K, d->fwd, s, /*counted=*/true));
   }
   guard.release();
   return new_handle(d, out);
@@ -467,62 +555,71 @@ extern "C" sscn_status sc_rulebook_build(const int32_t* coords, int64_t n, const
     // outputs seen per input: prod over d of ceil(f / s) (at most K)
     const int per_dim = (f + s_ - 1) / s_;
     const int64_t max_out = n * (int64_t)per_dim * per_dim * per_dim;
-    uint64_t cap = table_capacity(n), ocap = table_capacity(max_out);
-    uint64_t* keys; int32_t* vals; uint64_t* okeys; int32_t* ovals; unsigned long long* stats;
-    int32_t* first; int32_t* rank;
-    SSCN_TRY(tmp.get(&stats, 1 + K));
-    SSCN_TRY(fill_u64((uint64_t*)stats, 0, 1 + K, s));
-    SSCN_TRY(tmp.get(&rank, (size_t)n * K + 1));
+    const uint64_t cap = table_capacity(n), ocap = table_capacity(max_out);
+    Slot* table; Slot* otable; unsigned long long* stats; int32_t* first; int32_t* rank;
+    Arena ta;
+    ta.add(&table, cap);
+    ta.add(&otable, ocap);
+    ta.add(&stats, 2 + K);
+    ta.add(&first, (size_t)n * K);
+    ta.add(&rank, (size_t)n * K + 1);
+    SSCN_TRY(tmp.alloc(ta));
+    Arena ia;
+    ia.add(&d->in_coords, (size_t)4 * n);
+    SSCN_TRY(owned_alloc(d, ia, s));
+
+    SSCN_TRY(fill_u64((uint64_t*)stats, 0, 2 + K, s));
     if (n > 0) {
-      SSCN_TRY(tmp.get(&keys, cap));
-      SSCN_TRY(tmp.get(&vals, cap));
-      SSCN_TRY(tmp.get(&okeys, ocap));
-      SSCN_TRY(tmp.get(&ovals, ocap));
-      SSCN_TRY(tmp.get(&first, (size_t)n * K));
-      SSCN_TRY(fill_u64(keys, kEmptyKey, cap, s));
-      SSCN_TRY(fill_u64(okeys, kEmptyKey, ocap, s));
-      SSCN_TRY(fill_i32(ovals, INT32_MAX, ocap, s));
+      SSCN_TRY(launch_fill_slots(table, cap, -1, s));
+      SSCN_TRY(launch_fill_slots(otable, ocap, INT32_MAX, s));
       // the input dictionary detects repeated locations and range errors
-      k_insert<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g.L0, g.L1, g.L2, keys, vals,
-                                                cap - 1, stats);
+      k_insert<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g.L0, g.L1, g.L2, table, cap - 1, stats);
       SSCN_HIP(hipGetLastError());
-      k_sc_visit<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, okeys, ovals, ocap - 1);
+      k_sc_visit<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1);
       SSCN_HIP(hipGetLastError());
-      k_sc_mark<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, okeys, ovals, ocap - 1, first,
-                                                 stats + 1);
+      k_sc_mark<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, first, stats + 1);
       SSCN_HIP(hipGetLastError());
       SSCN_TRY(exclusive_scan_i32(first, rank, n * K, s));
-    } else {
-      SSCN_TRY(fill_i32(rank, 0, 1, s));
+      // n_out = rank[n K] joins the readback
+      SSCN_HIP(hipMemcpyAsync(stats + 1 + K, rank + (size_t)n * K, sizeof(int32_t), hipMemcpyDeviceToDevice, s));
+      SSCN_HIP(hipMemcpyAsync(d->in_coords, coords, sizeof(int32_t) * 4 * n, hipMemcpyDeviceToDevice, s));
     }
-    std::vector<unsigned long long> host(1 + K);
-    SSCN_TRY(readback(host.data(), stats, sizeof(unsigned long long) * (1 + K), s));
-    int32_t n_out32 = 0;
-    SSCN_TRY(readback(&n_out32, rank + (size_t)n * K, sizeof(int32_t), s));
+    std::vector<unsigned long long> host(2 + K);
+    SSCN_TRY(readback(host.data(), stats, sizeof(unsigned long long) * (2 + K), s));
     SSCN_TRY(flags_error(host[0]));
     int64_t total = 0;
     for (int o = 0; o < K; ++o) total += (d->pairs_per_offset[o] = (int64_t)host[1 + o]);
     d->n_pairs = total;
-    const int64_t n_out = n_out32;
+    const int64_t n_out = (int64_t)(uint32_t)(host[1 + K] & 0xffffffffull);
     d->n_out = n_out;
+    d->fwd.n_tiles = ceil_div(n_out, kTile);
+    d->bwd.n_tiles = ceil_div(n, kTile);
 
-    SSCN_TRY(dev_alloc((void**)&d->out_coords, sizeof(int32_t) * 4 * std::max<int64_t>(n_out, 1), s));
-    SSCN_TRY(dev_alloc((void**)&d->in_coords, sizeof(int32_t) * 4 * std::max<int64_t>(n, 1), s));
-    if (n > 0) SSCN_HIP(hipMemcpyAsync(d->in_coords, coords, sizeof(int32_t) * 4 * n, hipMemcpyDeviceToDevice, s));
+    Arena oa;
+    oa.add(&d->out_coords, (size_t)4 * n_out);
+    oa.add(&d->fwd.seg, (size_t)K * d->fwd.n_tiles + 1);
+    oa.add(&d->bwd.seg, (size_t)K * d->bwd.n_tiles + 1);
+    oa.add(&d->fwd.in_rows, total);
+    oa.add(&d->fwd.out_rows, total);
+    oa.add(&d->bwd.in_rows, total);
+    oa.add(&d->bwd.out_rows, total);
+    SSCN_TRY(owned_alloc(d, oa, s));
     if (n > 0) {
       int32_t* nbr_out; int32_t* nbr_in;
-      SSCN_TRY(tmp.get(&nbr_out, (size_t)K * n_out));
-      SSCN_TRY(tmp.get(&nbr_in, (size_t)K * n));
+      Arena na;
+      na.add(&nbr_out, (size_t)K * n_out);
+      na.add(&nbr_in, (size_t)K * n);
+      SSCN_TRY(tmp.alloc(na));
       SSCN_TRY(fill_i32(nbr_out, -1, (int64_t)K * n_out, s));
       SSCN_TRY(fill_i32(nbr_in, -1, (int64_t)K * n, s));
-      k_sc_assign<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, okeys, ovals, ocap - 1, rank,
-                                                   n_out, nbr_out, nbr_in, (int4*)d->out_coords);
+      k_sc_assign<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, rank, n_out,
+                                                   nbr_out, nbr_in, (int4*)d->out_coords);
       SSCN_HIP(hipGetLastError());
-      SSCN_TRY(build_storage(nbr_out, n_out, K, total, d->fwd, s, tmp, false, nullptr));
-      SSCN_TRY(build_storage(nbr_in, n, K, total, d->bwd, s, tmp, false, nullptr));
+      SSCN_TRY(compact_storage(nbr_out, n_out, K, d->fwd, s, false));
+      SSCN_TRY(compact_storage(nbr_in, n, K, d->bwd, s, false));
     } else {
-      SSCN_TRY(build_storage(nullptr, 0, K, 0, d->fwd, s, tmp, false, nullptr));
-      SSCN_TRY(build_storage(nullptr, 0, K, 0, d->bwd, s, tmp, false, nullptr));
+      SSCN_TRY(exclusive_scan_i64(d->fwd.seg, d->fwd.seg, 0, s));
+      SSCN_TRY(exclusive_scan_i64(d->bwd.seg, d->bwd.seg, 0, s));
     }
   }
   guard.release();

@@ -60,13 +60,7 @@ RulebookData::~RulebookData() {
   int cur = 0;
   (void)hipGetDevice(&cur);
   if (cur != device) (void)hipSetDevice(device);
-  for (Storage* st : {&fwd, &bwd}) {
-    dev_free(st->seg, stream);
-    dev_free(st->in_rows, stream);
-    dev_free(st->out_rows, stream);
-  }
-  dev_free(out_coords, stream);
-  dev_free(in_coords, stream);
+  for (void* p : blocks) dev_free(p, stream);
   if (cur != device) (void)hipSetDevice(cur);
 }
 
