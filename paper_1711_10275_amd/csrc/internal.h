@@ -33,6 +33,12 @@ void set_error(const std::string& msg);
 sscn_status fail(sscn_status st, const std::string& msg);
 sscn_status hip_fail(hipError_t e, const char* what);
 
+#define SSCN_TRY(expr)              \
+  do {                              \
+    sscn_status st_ = (expr);       \
+    if (st_ != SSCN_OK) return st_; \
+  } while (0)
+
 #define SSCN_HIP(call)                                   \
   do {                                                   \
     hipError_t e_ = (call);                              \
@@ -53,6 +59,7 @@ struct Storage {
   int64_t* seg = nullptr;        // K * n_tiles + 1 entries
   int32_t* in_rows = nullptr;    // n_pairs
   int32_t* out_rows = nullptr;   // n_pairs
+  int32_t* order = nullptr;      // n_tiles: tiles by decreasing work (chunks of 16 pairs)
 };
 
 struct RulebookData {

@@ -216,6 +216,31 @@ __global__ __launch_bounds__(256) void k_compact(const int32_t* __restrict__ nbr
   }
 }
 
+// ------------------------------------------------------------- tile order
+// Work of a tile = number of 16-pair chunks over all offsets.  Tiles are
+// listed by decreasing work (a counting sort on the chunk count) so that a
+// kernel handing tiles out from a queue finishes on its smallest tiles.
+__global__ void k_tile_work(const int64_t* __restrict__ seg, int64_t n_tiles, int K, int max_key,
+                            int32_t* __restrict__ key, int32_t* __restrict__ hist) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= n_tiles) return;
+  int chunks = 0;
+  for (int o = 0; o < K; ++o) {
+    const int64_t n = seg[(int64_t)o * n_tiles + t + 1] - seg[(int64_t)o * n_tiles + t];
+    chunks += (int)((n + 15) >> 4);
+  }
+  const int k = max_key - min(chunks, max_key);  // larger work -> smaller key
+  key[t] = k;
+  atomicAdd(&hist[k], 1);
+}
+
+__global__ void k_tile_scatter(const int32_t* __restrict__ key, int64_t n_tiles, int32_t* __restrict__ cursor,
+                               int32_t* __restrict__ order) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= n_tiles) return;
+  order[atomicAdd(&cursor[key[t]], 1)] = (int32_t)t;
+}
+
 // ----------------------------------------------------------------- SC build
 struct ScGeom {
   int f, s, K;
@@ -327,11 +352,6 @@ static inline unsigned grid_for(int64_t threads, int block) {
   return (unsigned)std::max<int64_t>(1, ceil_div(threads, block));
 }
 
-#define SSCN_TRY(expr)                     \
-  do {                                     \
-    sscn_status st_ = (expr);              \
-    if (st_ != SSCN_OK) return st_;        \
-  } while (0)
 
 // One device allocation carved into 256-byte aligned parts.
 struct Arena {
@@ -409,6 +429,25 @@ static sscn_status compact_storage(const int32_t* nbr, int64_t n_rows, int K, St
                                                              st.out_rows);
     SSCN_HIP(hipGetLastError());
   }
+  return SSCN_OK;
+}
+
+// st.order from st.seg (st.order already allocated, n_tiles entries).
+static sscn_status build_tile_order(Storage& st, int K, hipStream_t s) {
+  if (st.n_tiles == 0) return SSCN_OK;
+  const int max_key = K * (kTile / 16 + 1);
+  Temps tmp(s);
+  int32_t* key; int32_t* hist;
+  Arena a;
+  a.add(&key, st.n_tiles);
+  a.add(&hist, max_key + 2);
+  SSCN_TRY(tmp.alloc(a));
+  SSCN_TRY(fill_i32(hist, 0, max_key + 2, s));
+  k_tile_work<<<grid_for(st.n_tiles, 256), 256, 0, s>>>(st.seg, st.n_tiles, K, max_key, key, hist);
+  SSCN_HIP(hipGetLastError());
+  SSCN_TRY(exclusive_scan_i32(hist, hist, max_key + 1, s));
+  k_tile_scatter<<<grid_for(st.n_tiles, 256), 256, 0, s>>>(key, st.n_tiles, hist, st.order);
+  SSCN_HIP(hipGetLastError());
   return SSCN_OK;
 }
 
@@ -514,8 +553,10 @@ extern "C" sscn_status ssc_rulebook_build(const int32_t* coords, int64_t n, cons
     Arena pa;
     pa.add(&d->fwd.in_rows, total);
     pa.add(&d->fwd.out_rows, total);
+    pa.add(&d->fwd.order, n_tiles);
     SSCN_TRY(owned_alloc(d, pa, s));
     if (total > 0) SSCN_TRY(compact_storage(nbr, n, K, d->fwd, s, /*counted=*/true));
+    SSCN_TRY(build_tile_order(d->fwd, K, s));
   }
   guard.release();
   return new_handle(d, out);
@@ -603,6 +644,8 @@ extern "C" sscn_status sc_rulebook_build(const int32_t* coords, int64_t n, const
     oa.add(&d->fwd.out_rows, total);
     oa.add(&d->bwd.in_rows, total);
     oa.add(&d->bwd.out_rows, total);
+    oa.add(&d->fwd.order, d->fwd.n_tiles);
+    oa.add(&d->bwd.order, d->bwd.n_tiles);
     SSCN_TRY(owned_alloc(d, oa, s));
     if (n > 0) {
       int32_t* nbr_out; int32_t* nbr_in;
@@ -617,6 +660,8 @@ extern "C" sscn_status sc_rulebook_build(const int32_t* coords, int64_t n, const
       SSCN_HIP(hipGetLastError());
       SSCN_TRY(compact_storage(nbr_out, n_out, K, d->fwd, s, false));
       SSCN_TRY(compact_storage(nbr_in, n, K, d->bwd, s, false));
+      SSCN_TRY(build_tile_order(d->fwd, K, s));
+      SSCN_TRY(build_tile_order(d->bwd, K, s));
     } else {
       SSCN_TRY(exclusive_scan_i64(d->fwd.seg, d->fwd.seg, 0, s));
       SSCN_TRY(exclusive_scan_i64(d->bwd.seg, d->bwd.seg, 0, s));
