@@ -175,6 +175,22 @@ template <> struct Oct<bf16_t> {
     v = __builtin_bit_cast(bf16x8, u);
   }
 };
+// The same operand gathered with a stride of `step` bytes between the 8
+// channels (weights stored [offset][c_in][c_out], read along c_in).
+__device__ __forceinline__ void load_strided(Oct<float>& o, rsrc_t r, uint32_t voff, uint32_t step, uint32_t soff) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+    o.v[i] = __uint_as_float((uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)(voff + i * step), (int)soff, 0));
+}
+__device__ __forceinline__ void load_strided(Oct<bf16_t>& o, rsrc_t r, uint32_t voff, uint32_t step, uint32_t soff) {
+  uint32_t t[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) t[i] = (uint16_t)__builtin_amdgcn_raw_buffer_load_b16(r, (int)(voff + i * step), (int)soff, 0);
+  uint4 u;
+  u.x = t[0] | (t[1] << 16); u.y = t[2] | (t[3] << 16); u.z = t[4] | (t[5] << 16); u.w = t[6] | (t[7] << 16);
+  o.v = __builtin_bit_cast(bf16x8, u);
+}
+
 __device__ __forceinline__ f32x4 mma_oct(const Oct<float>& a, const Oct<float>& b, f32x4 d) {
 #pragma unroll
   for (int i = 0; i < 8; ++i) d = __builtin_amdgcn_mfma_f32_16x16x4f32(a.v[i], b.v[i], d, 0, 0, 0);
@@ -213,20 +229,26 @@ struct QuadLds {
 // no address arithmetic.  Loads are raw buffer loads: a lane's offset
 // within the row and its weight column are constants, the filter offset is
 // a scalar offset, and masked lanes use an out-of-range offset that reads as
-// zero.  The loop runs a RING-slot register ring with straight-line code:
+// zero.  Weights are read either from the stored layout W[o][c_in][c_out]
+// (WT = false: a lane's 8 channels are c_out apart) or from a layout with
+// c_in contiguous (WT = true, dgrad: W[o] read transposed).  The loop runs
+// a RING-slot register ring with straight-line code:
 // the gathered fragment of chunk c + RING - 1 is requested while chunk c is
 // multiplied, and weights are requested only for the first chunk of each
 // offset and kept in registers for the rest.  Partial sums of the two
 // channel halves go to two LDS accumulators (each element has one writing
 // wavefront, updated in chunk order) that are added at the end: the result
-// is deterministic.  The workgroups are persistent and take tiles from a
-// queue ordered by decreasing work (one queue per column group).
-template <typename T, int RING, int KB>
+// is deterministic.  The workgroups are persistent.  The grid is a multiple
+// of kTileGroups; workgroup b serves tile group b % kTileGroups (one group
+// of contiguous tiles per XCD, as workgroups are dispatched round-robin over
+// the XCDs), and the group's tiles, listed by decreasing work, are dealt to
+// its workgroups in boustrophedon order (0..G-1, G-1..0, ...).
+template <typename T, int RING, int KB, bool WT>
 __global__ __launch_bounds__(256) void k_conv_quad(
-    const T* __restrict__ X, uint32_t x_bytes, const T* __restrict__ Bt, uint32_t bt_bytes,
+    const T* __restrict__ X, uint32_t x_bytes, const T* __restrict__ W, uint32_t w_bytes,
     const int64_t* __restrict__ seg, const int32_t* __restrict__ in_rows, const int32_t* __restrict__ out_rows,
-    const int32_t* __restrict__ order, int* __restrict__ queue, int64_t n_tiles, int K, int mirror, int cin,
-    int cout, int64_t n_out, int max_chunks, T* __restrict__ Y) {
+    const int32_t* __restrict__ order, int64_t n_tiles, int K, int mirror, int cin, int cout, int64_t n_out,
+    int max_chunks, T* __restrict__ Y) {
   constexpr int LDW = 64 + 1;
   constexpr int ACC = (kTile + 1) * LDW;  // 64 rows + one dummy row for masked lanes
   extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -238,7 +260,7 @@ __global__ __launch_bounds__(256) void k_conv_quad(
   int64_t* seg_s = reinterpret_cast<int64_t*>(smem + L.seg_s);  // [K]
   int32_t* seg_n = reinterpret_cast<int32_t*>(smem + L.seg_n);  // [K]
   int32_t* seg_c0 = reinterpret_cast<int32_t*>(smem + L.seg_c0);  // [K]
-  __shared__ int n_chunks_sh, tile_sh;
+  __shared__ int n_chunks_sh;
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int m = lane & 15, g = lane >> 4;
@@ -255,21 +277,22 @@ __global__ __launch_bounds__(256) void k_conv_quad(
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
       const int col = col_base + chf * 32 + nb * 16 + m;
-      b_lane[kb][nb] = (col < cout && k_in) ? ((uint32_t)col * cin + k0) * (uint32_t)sizeof(T) : kOobOffset;
+      const uint32_t e = WT ? (uint32_t)col * cin + k0 : (uint32_t)k0 * cout + col;  // element of W[o]
+      b_lane[kb][nb] = (col < cout && k_in) ? e * (uint32_t)sizeof(T) : kOobOffset;
     }
   }
   const uint32_t w_stride = (uint32_t)cout * cin * sizeof(T);  // bytes per filter offset
-  const rsrc_t rx = make_rsrc(X, x_bytes), rb = make_rsrc(Bt, bt_bytes);
+  const uint32_t k_step = (uint32_t)cout * sizeof(T);           // bytes between channels (WT = false)
+  const rsrc_t rx = make_rsrc(X, x_bytes), rb = make_rsrc(W, w_bytes);
   char* acc_lane = reinterpret_cast<char*>(acc_all + kh * ACC + chf * 32 + m);
 
-  // Persistent workgroup: take tiles from the queue (largest first) until it
-  // runs dry; every workgroup reaches the exit.
-  for (;;) {
-    __syncthreads();
-    if (threadIdx.x == 0) tile_sh = atomicAdd(queue + blockIdx.y, 1);
-    __syncthreads();
-    if (tile_sh >= n_tiles) break;
-    const int64_t t0 = order[tile_sh];
+  const int64_t grp = blockIdx.x % kTileGroups;
+  const int64_t G = gridDim.x / kTileGroups, b = blockIdx.x / kTileGroups;
+  const int64_t first = (grp * n_tiles + kTileGroups - 1) / kTileGroups;
+  const int64_t count = ((grp + 1) * n_tiles + kTileGroups - 1) / kTileGroups - first;
+  for (int64_t idx = b, round = 0; idx < count; ++round, idx = round * G + ((round & 1) ? G - 1 - b : b)) {
+    __syncthreads();  // the previous tile's LDS is free
+    const int64_t t0 = order[first + idx];
     const int64_t row0 = t0 * kTile;
 
     // segment starts, pair counts and first chunk per offset; chunk -> offset
@@ -355,7 +378,12 @@ __global__ __launch_bounds__(256) void k_conv_quad(
 #pragma unroll
           for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-            for (int nb = 0; nb < 2; ++nb) b_ring[slot][kb][nb].load(rb, b_lane[kb][nb], soff);
+            for (int nb = 0; nb < 2; ++nb) {
+              if constexpr (WT)
+                b_ring[slot][kb][nb].load(rb, b_lane[kb][nb], soff);
+              else
+                load_strided(b_ring[slot][kb][nb], rb, b_lane[kb][nb], k_step, soff);
+            }
         }
       };
 #pragma unroll
@@ -430,7 +458,10 @@ __global__ void k_transpose_w(const T* __restrict__ W, int K, int cin, int cout,
 // wavefront accumulates the whole CA*16 x CB*16 block over a quarter of
 // the workgroup's pairs, with pair indices and rows fetched one iteration
 // (16 pairs) ahead; the four partial blocks are summed through LDS and
-// added to dW with fp32 atomics.
+// added to dW with fp32 atomics.  A workgroup's pairs are those of one
+// offset whose output rows lie in a range of `tr` consecutive tiles, so the
+// rows it gathers are spatially close; workgroups are numbered so that each
+// XCD takes contiguous tile ranges (L2 locality).
 template <int N>
 __device__ __forceinline__ void load_n(const float* __restrict__ p, bool ok, float (&v)[N]) {
   if (!ok) {
@@ -460,15 +491,17 @@ __global__ __launch_bounds__(256) void k_wgrad_reg(const T* __restrict__ X, cons
                                                    const int64_t* __restrict__ seg, int64_t n_tiles,
                                                    const int32_t* __restrict__ in_rows,
                                                    const int32_t* __restrict__ out_rows, int K, int mirror,
-                                                   int cin, int cout, int pch, int nzc, float* __restrict__ dW) {
+                                                   int cin, int cout, int tr, int nzc, float* __restrict__ dW) {
   constexpr int STEPS = 4;  // MFMA steps (4 pairs each) per iteration
-  const int o = blockIdx.y;
+  const int64_t item = xcd_remap(blockIdx.x, gridDim.x);
+  const int o = (int)(item % K);
+  const int64_t r = item / K;
   const int so = mirror ? K - 1 - o : o;
-  const int64_t start = seg[(int64_t)so * n_tiles], end = seg[(int64_t)(so + 1) * n_tiles];
-  const int64_t pb = start + (int64_t)blockIdx.x * pch;
-  if (pb >= end) return;
-  const int64_t pe = min<int64_t>(pb + pch, end);
-  const int ci0 = (blockIdx.z % nzc) * 16 * CA, co0 = (blockIdx.z / nzc) * 16 * CB;
+  const int64_t t_lo = r * tr, t_hi = min<int64_t>(t_lo + tr, n_tiles);
+  const int64_t pb = seg[(int64_t)so * n_tiles + t_lo];
+  const int64_t pe = seg[(int64_t)so * n_tiles + t_hi];
+  if (pb >= pe) return;
+  const int ci0 = (blockIdx.y % nzc) * 16 * CA, co0 = (blockIdx.y / nzc) * 16 * CB;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int m = lane & 15, g = lane >> 4;
   // a lane's channels are fully inside or fully outside [0, cin) / [0, cout)
@@ -560,29 +593,28 @@ __global__ __launch_bounds__(256) void k_wgrad_reg(const T* __restrict__ X, cons
 }
 
 // ---------------------------------------------------------------- launchers
-// Workgroups that fit on the device at once (capped by the work).
+// Workgroups that fit on the device at once, capped by the work and rounded
+// up to a multiple of kTileGroups (every tile group gets workgroups).
 static unsigned persistent_grid(const void* kern, size_t lds, int64_t n_items) {
   int dev = 0, cus = 256, per_cu = 1;
   (void)hipGetDevice(&dev);
   (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 256, lds) != hipSuccess || per_cu < 1) per_cu = 1;
-  const int64_t g = std::min<int64_t>((int64_t)cus * per_cu, std::max<int64_t>(n_items, 1));
+  int64_t g = std::min<int64_t>((int64_t)cus * per_cu, std::max<int64_t>(n_items, 1));
+  g = ceil_div(g, kTileGroups) * kTileGroups;
   return (unsigned)g;
 }
 
-constexpr int kMaxColGroups = 64;  // queue counters available per call
-
-template <typename T, int RING, int KB>
-static sscn_status launch_quad(const T* X, uint32_t x_bytes, const T* Bt, uint32_t bt_bytes, const View& v, int cin,
-                               int cout, T* Y, hipStream_t s, int* queue) {
+template <typename T, int RING, int KB, bool WT>
+static sscn_status launch_quad(const T* X, uint32_t x_bytes, const T* W, uint32_t w_bytes, const View& v, int cin,
+                               int cout, T* Y, hipStream_t s) {
   const int max_chunks = v.K * (kTile / 16 + 1);
   const QuadLds L(max_chunks, v.K);
   const int groups = (cout + 63) / 64;
-  SSCN_TRY(fill_i32(queue, 0, groups, s));
-  auto kern = k_conv_quad<T, RING, KB>;
+  auto kern = k_conv_quad<T, RING, KB, WT>;
   const unsigned g = persistent_grid((const void*)kern, L.total, v.st->n_tiles);
-  kern<<<dim3(g, (unsigned)groups), 256, L.total, s>>>(X, x_bytes, Bt, bt_bytes, v.st->seg, v.st->in_rows,
-                                                       v.st->out_rows, v.st->order, queue, v.st->n_tiles, v.K,
+  kern<<<dim3(g, (unsigned)groups), 256, L.total, s>>>(X, x_bytes, W, w_bytes, v.st->seg, v.st->in_rows,
+                                                       v.st->out_rows, v.st->order, v.st->n_tiles, v.K,
                                                        v.mirror ? 1 : 0, cin, cout, v.n_out, max_chunks, Y);
   SSCN_HIP(hipGetLastError());
   return SSCN_OK;
@@ -602,29 +634,8 @@ static sscn_status launch_generic_nw(const T* X, const T* Bt, const View& v, int
   return SSCN_OK;
 }
 
-// Y (n_out x cout) = forward of X (n_in x cin) over view v with weights Bt
-// (K x cout x cin).  queue: >= kMaxColGroups device ints of scratch.
 template <typename T>
-static sscn_status launch_conv(const T* X, const T* Bt, const View& v, int cin, int cout, T* Y, hipStream_t s,
-                               int* queue) {
-  if (v.st->n_tiles == 0) return SSCN_OK;
-  const uint64_t x_bytes = (uint64_t)std::max<int64_t>(v.n_in, 1) * cin * sizeof(T);
-  const uint64_t bt_bytes = (uint64_t)v.K * cout * cin * sizeof(T);
-  const int kb = (cin + 63) / 64;
-  const int max_kb = sizeof(T) == 4 ? 2 : 4;  // register budget of the main kernel
-  if (v.K <= 32767 && cin % 8 == 0 && kb <= max_kb && (cout + 63) / 64 <= kMaxColGroups &&
-      x_bytes < kOobOffset && bt_bytes < kOobOffset) {
-    switch (kb) {
-      case 1: return launch_quad<T, 4, 1>(X, (uint32_t)x_bytes, Bt, (uint32_t)bt_bytes, v, cin, cout, Y, s, queue);
-      case 2: return launch_quad<T, 3, 2>(X, (uint32_t)x_bytes, Bt, (uint32_t)bt_bytes, v, cin, cout, Y, s, queue);
-      default:
-        if constexpr (sizeof(T) == 2) {
-          if (kb == 3) return launch_quad<T, 3, 3>(X, (uint32_t)x_bytes, Bt, (uint32_t)bt_bytes, v, cin, cout, Y, s, queue);
-          return launch_quad<T, 3, 4>(X, (uint32_t)x_bytes, Bt, (uint32_t)bt_bytes, v, cin, cout, Y, s, queue);
-        }
-        break;
-    }
-  }
+static sscn_status launch_generic(const T* X, const T* Bt, const View& v, int cin, int cout, T* Y, hipStream_t s) {
   const int ncb = (cout + 15) / 16;
   const int grid_y = (ncb + 7) / 8;
   const int nw = (ncb + grid_y - 1) / grid_y;
@@ -640,17 +651,63 @@ static sscn_status launch_conv(const T* X, const T* Bt, const View& v, int cin, 
   }
 }
 
+// Y (n_out x cout) = forward of X (n_in x cin) over view v.  W holds the
+// K (cin x cout) weight matrices, stored [o][cin][cout] (WT = false,
+// forward) or [o][cout][cin] (WT = true, dgrad reads W^o transposed).  The
+// generic fallback needs the [o][cout][cin] layout and receives it in Bt
+// (a transposed copy made by the caller when WT = false).
+template <typename T, bool WT>
+static sscn_status launch_conv(const T* X, const T* W, const View& v, int cin, int cout, T* Y, hipStream_t s) {
+  if (v.st->n_tiles == 0) return SSCN_OK;
+  const uint64_t x_bytes = (uint64_t)std::max<int64_t>(v.n_in, 1) * cin * sizeof(T);
+  const uint64_t w_bytes = (uint64_t)v.K * cout * cin * sizeof(T);
+  const int kb = (cin + 63) / 64;
+  const int max_kb = sizeof(T) == 4 ? 2 : 4;  // register budget of the main kernel
+  if (v.K <= 32767 && cin % 8 == 0 && kb <= max_kb && x_bytes < kOobOffset && w_bytes < kOobOffset) {
+    const uint32_t xb = (uint32_t)x_bytes, wb = (uint32_t)w_bytes;
+    switch (kb) {
+      case 1: return launch_quad<T, 4, 1, WT>(X, xb, W, wb, v, cin, cout, Y, s);
+      case 2: return launch_quad<T, 3, 2, WT>(X, xb, W, wb, v, cin, cout, Y, s);
+      default:
+        if constexpr (sizeof(T) == 2) {
+          if (kb == 3) return launch_quad<T, 3, 3, WT>(X, xb, W, wb, v, cin, cout, Y, s);
+          return launch_quad<T, 3, 4, WT>(X, xb, W, wb, v, cin, cout, Y, s);
+        }
+        break;
+    }
+  }
+  const T* Bt = W;
+  T* tmp = nullptr;
+  if constexpr (!WT) {
+    const int64_t total = (int64_t)v.K * cin * cout;
+    SSCN_TRY(dev_alloc((void**)&tmp, sizeof(T) * total, s));
+    k_transpose_w<T><<<(unsigned)std::min<int64_t>(ceil_div(total, 256), 4096), 256, 0, s>>>(W, v.K, cin, cout, tmp);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) {
+      dev_free(tmp, s);
+      return hip_fail(e, "transpose launch");
+    }
+    Bt = tmp;
+  }
+  sscn_status st = launch_generic(X, Bt, v, cin, cout, Y, s);
+  dev_free(tmp, s);
+  return st;
+}
+
+
 template <typename T, int CA, int CB>
 static sscn_status launch_wgrad_reg(const T* X, const T* dY, const View& v, int cin, int cout, float* dW,
                                     hipStream_t s, int64_t max_ppo, int64_t n_pairs) {
-  // about 1024 workgroups over all offsets, each a multiple of 64 pairs
-  int64_t pch = ceil_div(n_pairs, 1024);
-  pch = std::min<int64_t>(std::max<int64_t>(ceil_div(pch, 64) * 64, 256), 1 << 20);
+  (void)max_ppo;
+  (void)n_pairs;
+  if (v.st->n_tiles == 0) return SSCN_OK;
+  // about 1024 (tile range, offset) items
+  const int64_t tr = std::max<int64_t>(1, ceil_div(v.st->n_tiles * v.K, 1024));
+  const int64_t n_items = ceil_div(v.st->n_tiles, tr) * v.K;
   const int nzc = (cin + 16 * CA - 1) / (16 * CA);
   const int nzo = (cout + 16 * CB - 1) / (16 * CB);
-  const int64_t gx = std::max<int64_t>(1, ceil_div(max_ppo, pch));
-  k_wgrad_reg<T, CA, CB><<<dim3((unsigned)gx, (unsigned)v.K, (unsigned)(nzc * nzo)), 256, 0, s>>>(
-      X, dY, v.st->seg, v.st->n_tiles, v.st->in_rows, v.st->out_rows, v.K, v.mirror ? 1 : 0, cin, cout, (int)pch,
+  k_wgrad_reg<T, CA, CB><<<dim3((unsigned)n_items, (unsigned)(nzc * nzo)), 256, 0, s>>>(
+      X, dY, v.st->seg, v.st->n_tiles, v.st->in_rows, v.st->out_rows, v.K, v.mirror ? 1 : 0, cin, cout, (int)tr,
       nzc, dW);
   SSCN_HIP(hipGetLastError());
   return SSCN_OK;
@@ -690,23 +747,24 @@ static sscn_status check_conv_args(sscn_rulebook rb, int32_t c_in, int32_t c_out
   return SSCN_OK;
 }
 
+// fp32: a transposed copy of W (one small kernel) gives the main kernel
+// contiguous weight loads, which is faster than gathering the stored layout;
+// bf16 reads the stored layout directly.
 template <typename T>
 static sscn_status forward_t(const T* X, const T* W, const View& v, int cin, int cout, T* Y, hipStream_t s) {
-  const int64_t K = v.K;
-  // transposed weights, then the work-queue counters (256-byte aligned)
-  const size_t bt_bytes = (sizeof(T) * K * cin * cout + 255) & ~(size_t)255;
-  T* Bt = nullptr;
-  sscn_status st = dev_alloc((void**)&Bt, bt_bytes + sizeof(int) * kMaxColGroups, s);
-  if (st != SSCN_OK) return st;
-  int* queue = reinterpret_cast<int*>(reinterpret_cast<char*>(Bt) + bt_bytes);
-  const int64_t total = K * cin * cout;
-  k_transpose_w<T><<<(unsigned)std::min<int64_t>(ceil_div(total, 256), 4096), 256, 0, s>>>(W, (int)K, cin,
-                                                                                            cout, Bt);
-  hipError_t e = hipGetLastError();
-  if (e == hipSuccess) st = launch_conv<T>(X, Bt, v, cin, cout, Y, s, queue);
-  dev_free(Bt, s);
-  if (e != hipSuccess) return hip_fail(e, "transpose launch");
-  return st;
+  if constexpr (sizeof(T) == 2) {
+    return launch_conv<T, false>(X, W, v, cin, cout, Y, s);
+  } else {
+    if (v.st->n_tiles == 0) return SSCN_OK;
+    const int64_t total = (int64_t)v.K * cin * cout;
+    T* Bt = nullptr;
+    SSCN_TRY(dev_alloc((void**)&Bt, sizeof(T) * total, s));
+    k_transpose_w<T><<<(unsigned)std::min<int64_t>(ceil_div(total, 256), 4096), 256, 0, s>>>(W, v.K, cin, cout, Bt);
+    hipError_t e = hipGetLastError();
+    sscn_status st = e == hipSuccess ? launch_conv<T, true>(X, Bt, v, cin, cout, Y, s) : hip_fail(e, "transpose");
+    dev_free(Bt, s);
+    return st;
+  }
 }
 
 }  // namespace sscn
@@ -739,16 +797,12 @@ extern "C" sscn_status sparse_conv_backward(const void* features, const void* we
     // dgrad = forward over the transposed rule book with B = W^o (as stored:
     // row ci of W[o] holds the c_out weights feeding input channel ci)
     const View vt = transposed_view(rb);
-    int* queue = nullptr;
-    st = dev_alloc((void**)&queue, sizeof(int) * kMaxColGroups, stream);
-    if (st != SSCN_OK) return st;
     if (dtype == SSCN_F32)
-      st = launch_conv<float>((const float*)dout, (const float*)weights, vt, c_out, c_in, (float*)dgrad,
-                                    stream, queue);
+      st = launch_conv<float, true>((const float*)dout, (const float*)weights, vt, c_out, c_in, (float*)dgrad,
+                                    stream);
     else
-      st = launch_conv<bf16_t>((const bf16_t*)dout, (const bf16_t*)weights, vt, c_out, c_in,
-                                     (bf16_t*)dgrad, stream, queue);
-    dev_free(queue, stream);
+      st = launch_conv<bf16_t, true>((const bf16_t*)dout, (const bf16_t*)weights, vt, c_out, c_in,
+                                     (bf16_t*)dgrad, stream);
     if (st != SSCN_OK) return st;
   }
   if (wgrad) {

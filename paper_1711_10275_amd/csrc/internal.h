@@ -19,6 +19,9 @@ namespace sscn {
 // lies in tile t.  Segments are laid out offset-major: seg[o * n_tiles + t].
 constexpr int kTile = 64;
 constexpr int kWave = 64;
+// Tiles are grouped into this many contiguous ranges, one per XCD of the
+// chip (each XCD has its own L2); see the tile order of a rule book.
+constexpr int kTileGroups = 8;
 
 constexpr uint64_t kEmptyKey = ~0ull;
 constexpr int kMaxBatch = 1 << 15;
@@ -59,7 +62,7 @@ struct Storage {
   int64_t* seg = nullptr;        // K * n_tiles + 1 entries
   int32_t* in_rows = nullptr;    // n_pairs
   int32_t* out_rows = nullptr;   // n_pairs
-  int32_t* order = nullptr;      // n_tiles: tiles by decreasing work (chunks of 16 pairs)
+  int32_t* order = nullptr;      // n_tiles: per tile group (contiguous range), tiles by decreasing work
 };
 
 struct RulebookData {
@@ -121,5 +124,14 @@ sscn_status fill_u64(uint64_t* p, uint64_t v, int64_t count, hipStream_t s);
 sscn_status fill_f32(float* p, float v, int64_t count, hipStream_t s);
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Workgroup i of a launch is dispatched to XCD i % kTileGroups.  Renumber a
+// grid of n workgroups so that each XCD takes one contiguous range of logical
+// items (bijective on [0, n)).
+__device__ inline int64_t xcd_remap(int64_t bid, int64_t n) {
+  const int64_t per = n / kTileGroups, rem = n % kTileGroups;
+  const int64_t x = bid % kTileGroups, k = bid / kTileGroups;
+  return x * per + (x < rem ? x : rem) + k;
+}
 
 }  // namespace sscn

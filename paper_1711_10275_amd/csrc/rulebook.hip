@@ -217,9 +217,11 @@ __global__ __launch_bounds__(256) void k_compact(const int32_t* __restrict__ nbr
 }
 
 // ------------------------------------------------------------- tile order
-// Work of a tile = number of 16-pair chunks over all offsets.  Tiles are
-// listed by decreasing work (a counting sort on the chunk count) so that a
-// kernel handing tiles out from a queue finishes on its smallest tiles.
+// Work of a tile = number of 16-pair chunks over all offsets.  The tiles are
+// cut into kTileGroups contiguous index ranges (group g = t * groups / T,
+// one per XCD, so that neighbouring tiles share an L2) and listed group by
+// group, each group by decreasing work (a counting sort), so that the
+// workgroups dealing out a group's tiles finish on its smallest ones.
 __global__ void k_tile_work(const int64_t* __restrict__ seg, int64_t n_tiles, int K, int max_key,
                             int32_t* __restrict__ key, int32_t* __restrict__ hist) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -229,7 +231,8 @@ __global__ void k_tile_work(const int64_t* __restrict__ seg, int64_t n_tiles, in
     const int64_t n = seg[(int64_t)o * n_tiles + t + 1] - seg[(int64_t)o * n_tiles + t];
     chunks += (int)((n + 15) >> 4);
   }
-  const int k = max_key - min(chunks, max_key);  // larger work -> smaller key
+  const int grp = (int)(t * kTileGroups / n_tiles);
+  const int k = grp * (max_key + 1) + max_key - min(chunks, max_key);  // larger work -> smaller key
   key[t] = k;
   atomicAdd(&hist[k], 1);
 }
@@ -436,16 +439,17 @@ static sscn_status compact_storage(const int32_t* nbr, int64_t n_rows, int K, St
 static sscn_status build_tile_order(Storage& st, int K, hipStream_t s) {
   if (st.n_tiles == 0) return SSCN_OK;
   const int max_key = K * (kTile / 16 + 1);
+  const int bins = kTileGroups * (max_key + 1);
   Temps tmp(s);
   int32_t* key; int32_t* hist;
   Arena a;
   a.add(&key, st.n_tiles);
-  a.add(&hist, max_key + 2);
+  a.add(&hist, bins + 1);
   SSCN_TRY(tmp.alloc(a));
-  SSCN_TRY(fill_i32(hist, 0, max_key + 2, s));
+  SSCN_TRY(fill_i32(hist, 0, bins + 1, s));
   k_tile_work<<<grid_for(st.n_tiles, 256), 256, 0, s>>>(st.seg, st.n_tiles, K, max_key, key, hist);
   SSCN_HIP(hipGetLastError());
-  SSCN_TRY(exclusive_scan_i32(hist, hist, max_key + 1, s));
+  SSCN_TRY(exclusive_scan_i32(hist, hist, bins, s));
   k_tile_scatter<<<grid_for(st.n_tiles, 256), 256, 0, s>>>(key, st.n_tiles, hist, st.order);
   SSCN_HIP(hipGetLastError());
   return SSCN_OK;
