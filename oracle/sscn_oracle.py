@@ -274,3 +274,87 @@ def macs(rb, cin, cout):
 def conditioning_bound(X, W, rb):
     """B[k][co] = sum |X[j][ci]| |W[o][ci][co]|: a scale for rounding errors."""
     return forward(np.abs(np.asarray(X, np.float64)), np.abs(np.asarray(W, np.float64)), rb)
+
+
+# --------------------------------------------------------------------------
+# network pieces (Sec. 5): pre-activation, row-sampled layers, the U-Net
+# --------------------------------------------------------------------------
+def affine_relu(X, scale, shift):
+    """max(0, x * scale + shift) per channel on the active rows (inference-form
+    batch normalisation followed by ReLU; inactive sites are not stored, so
+    they keep the ground state 0, Sec. 4.1), fp64."""
+    X = np.asarray(X, np.float64)
+    return np.maximum(0.0, X * np.asarray(scale, np.float64) + np.asarray(shift, np.float64))
+
+
+def forward_rows(X, W, rb, rows):
+    """Rows `rows` of forward(X, W, rb): for each requested output site, the
+    sum over the pairs (j, k) of every R_o that reach it (Sec. 4.2 step 2)."""
+    X = np.asarray(X, np.float64)
+    W = np.asarray(W, np.float64)
+    rows = np.asarray(rows, np.int64)
+    pos = np.full(rb.n_out, -1, np.int64)
+    pos[rows] = np.arange(rows.size)
+    Y = np.zeros((rows.size, W.shape[2]), np.float64)
+    for o in range(rb.K):
+        p = pos[rb.outs[o]]
+        m = p >= 0
+        if m.any():
+            np.add.at(Y, p[m], X[rb.ins[o][m]] @ W[o])
+    return Y
+
+
+def round_bf16(a):
+    """Nearest bfloat16 value (8 significant bits, ties to even) of each
+    finite element, returned as float64."""
+    a = np.asarray(a, np.float64)
+    m, e = np.frexp(a)                      # a = m 2^e, 0.5 <= |m| < 1
+    return np.ldexp(np.round(m * 256.0) / 256.0, e)
+
+
+def unet_forward(coords, size, X, params, channels, round_to_bf16=True):
+    """Submanifold U-Net of Sec. 5 on level-0 sites `coords`.
+
+    Levels l = 0 .. len(channels) - 1 with C_l = channels[l].  Encoder: two
+    pre-activated SSC(3) units C_l -> C_l per level (the result is the skip
+    of level l), then a pre-activated SC(2, 2) unit C_l -> C_{l+1} to the
+    next level.  Decoder, from the second-lowest level up: a pre-activated
+    DC unit C_{l+1} -> C_l over the inverted SC connections, the skip and
+    the upsampled features side by side (skip first), and two
+    pre-activated SSC(3) units 2 C_l -> C_l and C_l -> C_l.
+
+    params(name, k, cin, cout) -> (scale, shift, W) for the units named
+    enc{l}a, enc{l}b, down{l}, up{l}, dec{l}a, dec{l}b.  With
+    round_to_bf16 every stored activation (pre-activated input and
+    convolution output) is rounded to bfloat16, as a bf16 network stores
+    them; the arithmetic itself is fp64.
+    """
+    rnd = round_bf16 if round_to_bf16 else (lambda a: a)
+    depth = len(channels)
+
+    def unit(name, x, rb, cin, cout):
+        scale, shift, W = params(name, rb.K, cin, cout)
+        return rnd(forward(rnd(affine_relu(x, scale, shift)), W, rb))
+
+    ssc_rb, sc_rb = [], []
+    c, sz = np.asarray(coords), tuple(size)
+    for l in range(depth):
+        ssc_rb.append(ssc_rulebook(c, sz, 3))
+        if l + 1 < depth:
+            sc_rb.append(sc_rulebook(c, sz, 2, 2))
+            c, sz = sc_rb[-1].out_coords, sc_rb[-1].out_size
+
+    x = rnd(np.asarray(X, np.float64))
+    skip = []
+    for l in range(depth):
+        x = unit(f"enc{l}a", x, ssc_rb[l], channels[l], channels[l])
+        x = unit(f"enc{l}b", x, ssc_rb[l], channels[l], channels[l])
+        skip.append(x)
+        if l + 1 < depth:
+            x = unit(f"down{l}", x, sc_rb[l], channels[l], channels[l + 1])
+    for l in range(depth - 2, -1, -1):
+        up = unit(f"up{l}", x, transpose(sc_rb[l]), channels[l + 1], channels[l])
+        x = np.concatenate([skip[l], up], axis=1)
+        x = unit(f"dec{l}a", x, ssc_rb[l], 2 * channels[l], channels[l])
+        x = unit(f"dec{l}b", x, ssc_rb[l], channels[l], channels[l])
+    return x

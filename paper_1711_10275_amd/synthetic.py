@@ -16,6 +16,8 @@ representable in bf16.
 from __future__ import annotations
 
 import dataclasses
+import zlib
+
 import numpy as np
 
 # Seed bases: geometry, features, weights, upstream gradient (+ config index).
@@ -167,8 +169,10 @@ def scenes_256(seed=SEED_GEOM + 3, batch=8, L=256, target_per_sample=250_000):
     Floor and walls are large axis-aligned planar patches; objects are random
     sphere shells, cylinder shells and tilted patches.  Objects are added
     until the sample holds `target_per_sample` sites (within 10%); an object
-    that would overshoot by more than 8% is redrawn.
+    that would overshoot by more than 8% is redrawn.  Object sizes scale
+    with L / 256.
     """
+    g = L / 256.0
     per = []
     for b in range(batch):
         rng = np.random.default_rng(seed * 1000 + b)
@@ -184,16 +188,17 @@ def scenes_256(seed=SEED_GEOM + 3, batch=8, L=256, target_per_sample=250_000):
         for _ in range(2000):
             if count >= 0.97 * target_per_sample and n_obj >= 20:
                 break
-            q = np.array([rng.uniform(16, L - 16), rng.uniform(16, L - 16), rng.uniform(12, L / 2)])
+            q = np.array([rng.uniform(16 * g, L - 16 * g), rng.uniform(16 * g, L - 16 * g),
+                          rng.uniform(12 * g, L / 2)])
             kind = rng.integers(0, 3)
             s = rng.uniform(1.0, 1.8)
             if kind == 0:
-                obj = sphere_shell(q, rng.uniform(8, 22) * s, L)
+                obj = sphere_shell(q, rng.uniform(8, 22) * s * g, L)
             elif kind == 1:
-                obj = plane_patch(q, _unit(rng), rng.uniform(10, 24) * s, rng.uniform(10, 24) * s, L,
+                obj = plane_patch(q, _unit(rng), rng.uniform(10, 24) * s * g, rng.uniform(10, 24) * s * g, L,
                                   rot=rng.uniform(0, np.pi))
             else:
-                obj = cylinder_shell(q, _unit(rng), rng.uniform(5, 14) * s, rng.uniform(10, 24) * s, L)
+                obj = cylinder_shell(q, _unit(rng), rng.uniform(5, 14) * s * g, rng.uniform(10, 24) * s * g, L)
             new = int(np.count_nonzero(~occ[obj[:, 0], obj[:, 1], obj[:, 2]]))
             if count + new > 1.08 * target_per_sample:
                 continue
@@ -229,6 +234,26 @@ def weights(k, cin, cout, seed, bf16=False):
     w = np.random.default_rng(seed).standard_normal((k, cin, cout), dtype=np.float32)
     w *= np.float32(1.0 / np.sqrt(k * cin))
     return bf16_round(w) if bf16 else w
+
+
+def layer_params(name, k, cin, cout, seed=SEED_WEIGHT + 3, bf16=True):
+    """Parameters of one named network layer: a per-input-channel affine map
+    (inference-form batch normalisation: scale ~ U(0.5, 1.5), shift ~
+    N(0, 0.1)) and weights W[o][ci][co] ~ N(0, 1/(k cin)).
+
+    The draw depends only on (seed, name, k, cin, cout), so any code that
+    names its layers the same way gets the same parameters.
+    """
+    s = seed * 1_000_003 + zlib.crc32(name.encode()) + 7919 * (k * 1_000_000 + cin * 1000 + cout)
+    rng = np.random.default_rng(s)
+    scale = rng.uniform(0.5, 1.5, cin).astype(np.float32)
+    shift = rng.normal(0.0, 0.1, cin).astype(np.float32)
+    return scale, shift, weights(k, cin, cout, s + 1, bf16=bf16)
+
+
+def scenes_small(seed=SEED_GEOM + 13, batch=2, L=64, target_per_sample=15_000):
+    """The indoor-scene recipe on a small grid (end-to-end network checks)."""
+    return scenes_256(seed=seed, batch=batch, L=L, target_per_sample=target_per_sample)
 
 
 @dataclasses.dataclass

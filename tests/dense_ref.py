@@ -106,3 +106,53 @@ def active_in_field(coords, size, f, centred=True):
     cnt = F.conv3d(occ, torch.ones(1, 1, f, f, f, dtype=torch.float64),
                    padding=(f - 1) // 2 if centred else 0).numpy()[:, 0]
     return cnt[coords[:, 0], coords[:, 1], coords[:, 2], coords[:, 3]].astype(np.int64)
+
+
+def dense_unet(coords, size, X, params, channels):
+    """The U-Net of Sec. 5 on dense grids: every layer is a dense conv3d /
+    conv_transpose3d in float64 followed by a mask that zeroes the inactive
+    sites of the layer's output level (level l + 1 is active where a 2^3
+    block of level l holds an active site); pre-activations are masked too,
+    since an inactive site stays at the ground state 0.  Returns the features
+    at the level-0 input sites, in input row order."""
+    coords = np.asarray(coords, np.int64)
+    B = int(coords[:, 0].max()) + 1
+    depth = len(channels)
+    masks = [to_dense(coords, np.ones((coords.shape[0], 1)), size, B)]
+    for _ in range(depth - 1):
+        masks.append((F.conv3d(masks[-1], torch.ones(1, 1, 2, 2, 2, dtype=torch.float64), stride=2) > 0).double())
+
+    def pre(name, x, mask, k, cin, cout):
+        scale, shift, W = params(name, k, cin, cout)
+        sc = torch.from_numpy(np.asarray(scale, np.float64)).view(1, -1, 1, 1, 1)
+        sh = torch.from_numpy(np.asarray(shift, np.float64)).view(1, -1, 1, 1, 1)
+        return torch.relu(x * sc + sh) * mask, np.asarray(W, np.float64)
+
+    def ssc(name, x, l, cin, cout):
+        a, W = pre(name, x, masks[l], 27, cin, cout)
+        return F.conv3d(a, torch_weight(W, 3), padding=1) * masks[l]
+
+    def down(name, x, l):
+        a, W = pre(name, x, masks[l], 8, channels[l], channels[l + 1])
+        return F.conv3d(a, torch_weight(W, 2), stride=2) * masks[l + 1]
+
+    def up(name, x, l):
+        a, W = pre(name, x, masks[l + 1], 8, channels[l + 1], channels[l])
+        w = torch.from_numpy(np.ascontiguousarray(W.reshape(2, 2, 2, channels[l + 1], channels[l]).transpose(3, 4, 0, 1, 2)))
+        return F.conv_transpose3d(a, w, stride=2) * masks[l]
+
+    x = to_dense(coords, X, size, B)
+    skip = []
+    for l in range(depth):
+        x = ssc(f"enc{l}a", x, l, channels[l], channels[l])
+        x = ssc(f"enc{l}b", x, l, channels[l], channels[l])
+        skip.append(x)
+        if l + 1 < depth:
+            x = down(f"down{l}", x, l)
+    for l in range(depth - 2, -1, -1):
+        u = up(f"up{l}", x, l)
+        x = torch.cat([skip[l], u], dim=1)
+        x = ssc(f"dec{l}a", x, l, 2 * channels[l], channels[l])
+        x = ssc(f"dec{l}b", x, l, channels[l], channels[l])
+    y = x.numpy()
+    return y[coords[:, 0], :, coords[:, 1], coords[:, 2], coords[:, 3]]

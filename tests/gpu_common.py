@@ -76,3 +76,19 @@ def assert_same_rulebook(rb, orb, what=""):
     for q in range(orb.K):
         np.testing.assert_array_equal(g[q][0], o[q][0], err_msg=f"{what} in rows, offset {q}")
         np.testing.assert_array_equal(g[q][1], o[q][1], err_msg=f"{what} out rows, offset {q}")
+
+
+@functools.lru_cache(maxsize=None)
+def oracle_levels(config, depth):
+    """Oracle geometry of a U-Net: per level (coords, size, SSC(3) rule book,
+    SC(2, 2) rule book or None), built from the level-0 sites of `config`."""
+    from oracle import sscn_oracle as O
+    coords, size = coords_for(config) if config != "scenes_small" else (S.scenes_small(), (64, 64, 64))
+    out = []
+    for l in range(depth):
+        ssc = O.ssc_rulebook(coords, size, 3)
+        sc = O.sc_rulebook(coords, size, 2, 2) if l + 1 < depth else None
+        out.append((coords, size, ssc, sc))
+        if sc is not None:
+            coords, size = sc.out_coords, sc.out_size
+    return tuple(out)

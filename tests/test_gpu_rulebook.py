@@ -5,7 +5,7 @@ import torch
 
 from oracle import sscn_oracle as O
 from paper_1711_10275_amd import sscn
-from tests.gpu_common import assert_same_rulebook, coords_for, dev, host, small_set
+from tests.gpu_common import assert_same_rulebook, coords_for, dev, host, oracle_levels, small_set
 
 pytestmark = pytest.mark.gpu
 
@@ -38,11 +38,11 @@ def test_sc_then_ssc_on_shapes128():
 def test_scenes256_level0_rulebooks():
     """Full-size 256^3 x 8 scenes (about 2M sites): SSC and SC(2,2) rule books."""
     c, size = coords_for("scenes256")
+    _, _, ossc, osc = oracle_levels("scenes256", 5)[0]
     rb = sscn.ssc_rulebook_build(dev(c), size, 3)
-    assert_same_rulebook(rb, O.ssc_rulebook(c, size, 3), "scenes ssc")
+    assert_same_rulebook(rb, ossc, "scenes ssc")
     del rb
     sc = sscn.sc_rulebook_build(dev(c), size, 2, 2)
-    osc = O.sc_rulebook(c, size, 2, 2)
     assert_same_rulebook(sc, osc, "scenes sc22")
     np.testing.assert_array_equal(host(sc.out_coords()), osc.out_coords)
 
