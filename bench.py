@@ -72,6 +72,8 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="bound on the CPU oracle sample")
     p.add_argument("--copy-calibration", action="store_true",
                    help="also run a 256 MiB device copy (counter calibration)")
+    p.add_argument("--no-extra", action="store_true",
+                   help="skip the SC -> SSC and U-Net figures reported beside the headline layer")
     return p.parse_args()
 
 
@@ -95,6 +97,81 @@ def cpu_baseline(coords, size, X, W, G, budget_s):
     return {"value": n * steps / t_total, "unit": "active-sites/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{steps} whole steps (rule book + forward + backward, numpy fp64) of the same "
                       f"{n}-site workload, {t_total:.1f} s"}
+
+
+def _event_ms(fn, reps, stream):
+    import torch
+    fn()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        fn()
+    e1.record(stream)
+    e1.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def _wall_ms(fn, reps):
+    import torch
+    fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        fn()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / reps
+
+
+def sc_then_ssc(tc, size, stream, reps):
+    """SC(2, 2) 64 -> 96 channels (128^3 -> 64^3), then SSC 3^3 at 64^3 with 96 channels."""
+    import torch
+    from paper_1711_10275_amd import sscn
+    from paper_1711_10275_amd import synthetic as S
+    dev = tc.device
+    sc_build = _wall_ms(lambda: sscn.sc_rulebook_build(tc, size, 2, 2), reps)
+    sc = sscn.sc_rulebook_build(tc, size, 2, 2)
+    oc = sc.out_coords()
+    ssc_build = _wall_ms(lambda: sscn.ssc_rulebook_build(oc, sc.out_size, 3), reps)
+    ssc = sscn.ssc_rulebook_build(oc, sc.out_size, 3)
+    out = {"workload": "sc2x2x2s2_grid128to64_c64to96_then_ssc3x3x3_grid64_c96", "sc_out_sites": sc.n_out,
+           "sc_pairs": sc.n_pairs, "ssc_pairs": ssc.n_pairs, "sc_rulebook_build_ms": sc_build,
+           "ssc_rulebook_build_ms": ssc_build}
+    for name, dt in (("f32", torch.float32), ("bf16", torch.bfloat16)):
+        X = torch.from_numpy(S.features(tc.shape[0], 64, S.SEED_FEAT + 2)).to(dt).to(dev)
+        W1 = torch.from_numpy(S.weights(8, 64, 96, S.SEED_WEIGHT + 2)).to(dt).to(dev)
+        W2 = torch.from_numpy(S.weights(27, 96, 96, S.SEED_WEIGHT + 22)).to(dt).to(dev)
+        Y = sscn.sparse_conv_forward(X, W1, sc)
+        t1 = _event_ms(lambda: sscn.sparse_conv_forward(X, W1, sc), reps, stream)
+        t2 = _event_ms(lambda: sscn.sparse_conv_forward(Y, W2, ssc), reps, stream)
+        out[f"sc_forward_ms_{name}"] = t1
+        out[f"ssc_forward_ms_{name}"] = t2
+        out[f"sc_tflops_{name}"] = 2.0 * 64 * 96 * sc.n_pairs / (t1 * 1e-3) / 1e12
+        out[f"ssc_tflops_{name}"] = 2.0 * 96 * 96 * ssc.n_pairs / (t2 * 1e-3) / 1e12
+    return out
+
+
+def unet_scenes(stream, reps):
+    """Five-level submanifold U-Net forward, 256^3 x 8 scenes, bf16."""
+    import torch
+    from paper_1711_10275_amd import unet
+    from paper_1711_10275_amd import synthetic as S
+    dev = torch.device("cuda:0")
+    c = S.scenes_256()
+    tc = torch.from_numpy(c).to(dev)
+    X = torch.from_numpy(S.features(c.shape[0], 32, S.SEED_FEAT + 3, bf16=True)).to(torch.bfloat16).to(dev)
+    params = unet.device_params(draw=lambda n, k, ci, co: S.layer_params(n, k, ci, co, bf16=True))
+    geom_ms = _wall_ms(lambda: unet.Geometry(tc, (256, 256, 256)), reps)
+    # a fresh input: rule books of every level, then the network (lazily built
+    # chunk tables included)
+    fresh_ms = _wall_ms(lambda: unet.forward(X, unet.Geometry(tc, (256, 256, 256)), params), reps)
+    geom = unet.Geometry(tc, (256, 256, 256))
+    fwd_ms = _event_ms(lambda: unet.forward(X, geom, params), reps, stream)
+    fl = unet.flops(geom)
+    return {"workload": "unet5_grid256_batch8_scenes_c32to160_bf16", "level_sites": [int(x.shape[0]) for x in geom.coords],
+            "geometry_build_ms": geom_ms, "forward_ms": fwd_ms, "forward_sites_per_s": c.shape[0] / (fwd_ms * 1e-3),
+            "forward_effective_tflops": fl / (fwd_ms * 1e-3) / 1e12, "flops": fl,
+            "geometry_plus_forward_ms": fresh_ms,
+            "geometry_plus_forward_sites_per_s": c.shape[0] / (fresh_ms * 1e-3)}
 
 
 def main():
@@ -201,6 +278,8 @@ def main():
                      "launch_ms": dgrad_ms, "flops_per_launch": flops_layer,
                      "traffic": recorded_traffic()},
     }
+    if not args.no_extra:
+        result["extra"] = {"sc_then_ssc": sc_then_ssc(tc, size, stream, reps), "unet": unet_scenes(stream, 5)}
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(coords, size, X, W, G, args.cpu_seconds)
     print(json.dumps(result))

@@ -592,6 +592,249 @@ __global__ __launch_bounds__(256) void k_wgrad_reg(const T* __restrict__ X, cons
   }
 }
 
+// ------------------------------------------------- column-owner kernel
+// One lane's operand for one 64-channel block: 16 channels as NJ b128
+// loads of EPB elements; load j of lane group g covers channels
+// 4 EPB j + EPB g .. + EPB - 1, so that the four lane groups of one load
+// read 64 contiguous bytes of a row (one instruction touches half as many
+// cache lines as with 16 contiguous channels per lane).
+template <typename T> struct Frag16;
+template <> struct Frag16<float> {
+  static constexpr int kLoads = 4;
+  float v[16];
+  __device__ __forceinline__ void load(rsrc_t r, uint32_t base, const uint32_t (&lo)[4], uint32_t soff) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const auto q = __builtin_amdgcn_raw_buffer_load_b128(r, (int)(base + lo[j]), (int)soff, 0);
+      v[4 * j + 0] = __uint_as_float(q[0]); v[4 * j + 1] = __uint_as_float(q[1]);
+      v[4 * j + 2] = __uint_as_float(q[2]); v[4 * j + 3] = __uint_as_float(q[3]);
+    }
+  }
+  __device__ __forceinline__ void select(bool take, const Frag16& o) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) v[i] = take ? o.v[i] : v[i];
+  }
+};
+template <> struct Frag16<bf16_t> {
+  static constexpr int kLoads = 2;
+  bf16x8 v[2];
+  __device__ __forceinline__ void load(rsrc_t r, uint32_t base, const uint32_t (&lo)[4], uint32_t soff) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const auto q = __builtin_amdgcn_raw_buffer_load_b128(r, (int)(base + lo[j]), (int)soff, 0);
+      uint4 u;
+      u.x = q[0]; u.y = q[1]; u.z = q[2]; u.w = q[3];
+      v[j] = __builtin_bit_cast(bf16x8, u);
+    }
+  }
+  __device__ __forceinline__ void select(bool take, const Frag16& o) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) v[j] = take ? o.v[j] : v[j];
+  }
+};
+__device__ __forceinline__ f32x4 mma16(const Frag16<float>& a, const Frag16<float>& b, f32x4 d) {
+#pragma unroll
+  for (int i = 0; i < 16; ++i) d = __builtin_amdgcn_mfma_f32_16x16x4f32(a.v[i], b.v[i], d, 0, 0, 0);
+  return d;
+}
+__device__ __forceinline__ f32x4 mma16(const Frag16<bf16_t>& a, const Frag16<bf16_t>& b, f32x4 d) {
+  d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v[0], b.v[0], d, 0, 0, 0);
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v[1], b.v[1], d, 0, 0, 0);
+}
+
+constexpr int kColLdw = 17;                               // LDS row stride (floats) of a wave's tile
+constexpr int kColRegion = (kChunkRows + 1) * kColLdw;    // floats per wave (one padding row)
+
+// Forward / dgrad over the padded chunk table.  Every wavefront owns 16
+// output columns and all input channels: per chunk (16 pairs of one
+// offset) it multiplies the 16 gathered rows by the offset's weight block
+// and adds the 16 x 16 result into a private fp32 tile of kChunkRows rows
+// in LDS, at the pairs' output rows (a row occurs at most once per chunk).
+// When the last chunk of a tile has been added, the wavefront writes its
+// columns of the tile to Y and clears them.  No LDS location is shared
+// between wavefronts, so there are no barriers, and the chunk stream of a
+// workgroup runs across its tiles: chunk records (input rows, output rows)
+// are loaded 2 RING chunks ahead, gathered rows RING chunks ahead and the
+// weight block (only when the offset changes) together with the rows, into
+// register rings with compile-time slots.  Record and row loads are issued
+// unconditionally (a row that is not needed reads an out-of-range offset,
+// which returns zeros without touching memory), so the compiler's wait
+// counts stay close to exact and the loads of later chunks remain in
+// flight; only the tile write-out, once per tile, waits for everything.
+//
+// Workgroups serve tile groups (one contiguous range of tiles per XCD, as
+// workgroups are dispatched round-robin over XCDs); a group's tiles are
+// dealt to its workgroups in boustrophedon order.  blockIdx.y selects a
+// range of 16 * (blockDim.x / 64) output columns.
+//
+// Wt is the weight block with the reduction index contiguous:
+// Wt[o][n][k], n < cout, k < cin.
+template <typename T, int KB, int RING>
+__global__ __launch_bounds__(256) void k_conv_col(
+    const T* __restrict__ X, uint32_t x_bytes, const T* __restrict__ Wt, uint32_t w_bytes,
+    const int32_t* __restrict__ ctile, const int32_t* __restrict__ c_in, const uint32_t* __restrict__ c_out,
+    const int32_t* __restrict__ c_off, int n_ct, int K, int mirror, int cin, int cout, int n_out,
+    T* __restrict__ Y) {
+  constexpr int IR = 2 * RING;                 // chunk-record ring
+  constexpr int TR = kChunkRows;
+  constexpr int EPB = 16 / sizeof(T);          // elements per b128 load
+  constexpr uint32_t kPadRows = (uint32_t)TR * 0x01010101u;
+  constexpr int kNoOff = 0xffff;               // meta of a chunk past the end
+  extern __shared__ float lds_col[];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int m = lane & 15, g = lane >> 4;
+  const int ncol = blockDim.x >> 6;
+  const int col0 = (blockIdx.y * ncol + wave) * 16;
+  if (col0 >= cout) return;                    // wave-uniform; nothing is shared across waves
+  float* acc = lds_col + wave * kColRegion;
+  for (int i = lane; i < kColRegion; i += 64) acc[i] = 0.f;
+
+  // lane constants
+  const uint32_t row_bytes = (uint32_t)cin * sizeof(T);
+  const int col = col0 + m;
+  uint32_t a_lo[KB][4], b_lo[KB][4];
+#pragma unroll
+  for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int k0 = kb * 64 + 4 * EPB * j + EPB * g;
+      const bool ok = k0 + EPB <= cin;
+      a_lo[kb][j] = ok ? (uint32_t)k0 * sizeof(T) : kOobOffset;
+      b_lo[kb][j] = (ok && col < cout) ? ((uint32_t)col * cin + k0) * sizeof(T) : kOobOffset;
+    }
+  const uint32_t w_stride = (uint32_t)cout * cin * sizeof(T);
+  const rsrc_t rx = make_rsrc(X, x_bytes), rw = make_rsrc(Wt, w_bytes);
+  float* acc_lane = acc + m;
+
+  // this workgroup's tiles
+  const int ngrp = min((int)gridDim.x, kTileGroups);
+  const int grp = blockIdx.x % ngrp;
+  const int G = ((int)gridDim.x - grp + ngrp - 1) / ngrp, bi = blockIdx.x / ngrp;
+  const int t_first = (int)((int64_t)grp * n_ct / ngrp);
+  const int t_count = (int)((int64_t)(grp + 1) * n_ct / ngrp) - t_first;
+  auto tile_of = [&](int r) -> int {
+    const int idx = r * G + ((r & 1) ? G - 1 - bi : bi);
+    return idx < t_count ? t_first + idx : -1;
+  };
+  int n_stream = 0;
+  for (int r = 0;; ++r) {
+    const int t = tile_of(r);
+    if (t < 0) break;
+    n_stream += ctile[(t + 1) * K] - ctile[t * K];
+  }
+
+  // record cursor over (tile, chunk); compute-side tile
+  int cur_r = 0, cur_t = tile_of(0), cur_c = 0, cur_e = 0;
+  if (cur_t >= 0) { cur_c = ctile[cur_t * K]; cur_e = ctile[(cur_t + 1) * K]; }
+  int comp_r = 0;
+
+  // Chunk records (loaded 2 RING chunks ahead) are read once, when the
+  // chunk's operands are requested (RING chunks ahead): the output rows and
+  // the offset then move into the operand ring.  A record slot is never read
+  // in the step that refills it, so every slot keeps one register across the
+  // loop and no wait lands on the loop's back edge.  The weight block of a
+  // chunk is requested together with its gathered rows (same distance: loads
+  // complete in order, so a later request would shorten the effective
+  // prefetch distance of everything before it).
+  int32_t r_in[IR];
+  uint32_t r_out[IR];
+  int r_meta[IR];         // stored offset (kNoOff past the end) | last chunk of its tile << 16
+  uint32_t o_ring[RING];  // output rows of the chunk in operand slot
+  int m_ring[RING];       // meta of the chunk in operand slot
+  bool f_ring[RING];      // its weight block differs from the previous chunk's
+  Frag16<T> a_ring[RING][KB], b_ring[RING][KB], b_cur[KB];
+  int req_off = -1;       // offset of the last real chunk whose operands were requested
+
+  auto fetch_record = [&](int slot) {
+    const bool valid = cur_t >= 0;
+    const int c = valid ? cur_c : 0;         // chunk 0 always exists: loads stay unconditional
+    r_in[slot] = c_in[(int64_t)c * 16 + m];
+    r_out[slot] = c_out[(int64_t)c * 4 + g];
+    if (valid) {
+      r_meta[slot] = c_off[c] | ((c + 1 == cur_e) ? (1 << 16) : 0);
+      if (++cur_c == cur_e) {
+        cur_t = tile_of(++cur_r);
+        if (cur_t >= 0) { cur_c = ctile[cur_t * K]; cur_e = ctile[(cur_t + 1) * K]; }
+      }
+    } else {
+      r_meta[slot] = kNoOff;
+    }
+  };
+  auto fetch_operands = [&](int rs, int as) {
+    const int meta = r_meta[rs];
+    const int off = meta & 0xffff;
+    const bool valid = off != kNoOff;
+    const int32_t irow = r_in[rs];
+    const uint32_t base = (valid && irow >= 0) ? (uint32_t)irow * row_bytes : kOobOffset;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) a_ring[as][kb].load(rx, base, a_lo[kb], 0);
+    const bool fresh = valid && off != req_off;
+    if (valid) req_off = off;
+    const int ow = mirror ? K - 1 - off : off;
+    const uint32_t soff = (uint32_t)ow * w_stride;
+    if (fresh) {
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) b_ring[as][kb].load(rw, 0u, b_lo[kb], soff);
+    }
+    f_ring[as] = fresh;
+    o_ring[as] = valid ? r_out[rs] : kPadRows;
+    asm volatile("" : "+v"(o_ring[as]));  // keep the read of the record slot here
+    m_ring[as] = meta;
+  };
+
+#pragma unroll
+  for (int sl = 0; sl < IR; ++sl) fetch_record(sl);
+#pragma unroll
+  for (int sl = 0; sl < RING; ++sl) fetch_operands(sl, sl);
+
+  f32x4 d_prev = {0.f, 0.f, 0.f, 0.f};
+  uint32_t out_prev = kPadRows;
+  bool last_prev = false;
+  for (int i0 = 0; i0 <= n_stream; i0 += IR) {
+#pragma unroll
+    for (int sl = 0; sl < IR; ++sl) {
+      const int as = sl % RING;
+      // 1. this chunk's product
+      const int meta = m_ring[as];
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) b_cur[kb].select(f_ring[as], b_ring[as][kb]);
+      f32x4 d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) d = mma16(a_ring[as][kb], b_cur[kb], d);
+      // 2. add the previous chunk into its tile
+      {
+        float* q0 = acc_lane + ((out_prev >> 0) & 0xff) * kColLdw;
+        float* q1 = acc_lane + ((out_prev >> 8) & 0xff) * kColLdw;
+        float* q2 = acc_lane + ((out_prev >> 16) & 0xff) * kColLdw;
+        float* q3 = acc_lane + ((out_prev >> 24) & 0xff) * kColLdw;
+        const float v0 = *q0, v1 = *q1, v2 = *q2, v3 = *q3;
+        *q0 = v0 + d_prev[0];
+        *q1 = v1 + d_prev[1];
+        *q2 = v2 + d_prev[2];
+        *q3 = v3 + d_prev[3];
+      }
+      // ... and write the tile out after its last chunk (once per tile)
+      if (last_prev) {
+        const int64_t row0 = (int64_t)tile_of(comp_r++) * TR;
+        for (int r = g; r < TR; r += 4) {
+          float* q = acc_lane + r * kColLdw;
+          const float v = *q;
+          *q = 0.f;
+          const int64_t row = row0 + r;
+          if (row < n_out && col < cout) Elem<T>::store(Y + row * cout + col, v);
+        }
+        __builtin_amdgcn_s_waitcnt(0);
+      }
+      d_prev = d;
+      out_prev = o_ring[as];
+      last_prev = (meta >> 16) & 1;
+      // 3. operands RING chunks ahead, record 2 RING chunks ahead
+      fetch_operands((sl + RING) % IR, as);
+      fetch_record(sl);
+    }
+  }
+}
+
 // ---------------------------------------------------------------- launchers
 // Workgroups that fit on the device at once, capped by the work and rounded
 // up to a multiple of kTileGroups (every tile group gets workgroups).
@@ -656,14 +899,94 @@ static sscn_status launch_generic(const T* X, const T* Bt, const View& v, int ci
 // forward) or [o][cout][cin] (WT = true, dgrad reads W^o transposed).  The
 // generic fallback needs the [o][cout][cin] layout and receives it in Bt
 // (a transposed copy made by the caller when WT = false).
-template <typename T, bool WT>
-static sscn_status launch_conv(const T* X, const T* W, const View& v, int cin, int cout, T* Y, hipStream_t s) {
-  if (v.st->n_tiles == 0) return SSCN_OK;
+// Column-owner kernel over the chunk table: Bt = weights with the
+// reduction index contiguous ([o][cout][cin]).  Returns SSCN_ERR_SHAPE
+// (without launching) when the shape is outside what the kernel covers.
+template <typename T, int KB, int RING>
+static sscn_status launch_col_kb(const T* X, uint32_t xb, const T* Bt, uint32_t wb, const View& v, int cin,
+                                 int cout, T* Y, hipStream_t s) {
+  const Storage& st = *v.st;
+  const int ng = (cout + 15) / 16;
+  int ncol = std::min(ng, 4);
+  for (int c : {4, 3, 2})
+    if (ng % c == 0) { ncol = c; break; }
+  const int gy = (ng + ncol - 1) / ncol;
+  const size_t lds = sizeof(float) * kColRegion * ncol;
+  auto kern = k_conv_col<T, KB, RING>;
+  int dev = 0, cus = 256, per_cu = 1;
+  (void)hipGetDevice(&dev);
+  (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 64 * ncol, lds) != hipSuccess || per_cu < 1)
+    per_cu = 1;
+  const int64_t gx = std::min<int64_t>(st.n_ctiles, std::max<int64_t>(1, (int64_t)cus * per_cu / gy));
+  kern<<<dim3((unsigned)gx, (unsigned)gy), 64 * ncol, lds, s>>>(
+      X, xb, Bt, wb, st.ctile, st.c_in, reinterpret_cast<const uint32_t*>(st.c_out), st.c_off, (int)st.n_ctiles,
+      v.K, v.mirror ? 1 : 0, cin, cout, (int)v.n_out, Y);
+  SSCN_HIP(hipGetLastError());
+  return SSCN_OK;
+}
+
+// Which forward / dgrad kernel: the column kernel where its shape rules
+// allow and either the output width is not a multiple of 64 (the quad
+// kernel computes 64 columns per workgroup row) or output rows have few
+// pairs (DC layers: one pair per output row; short chunks in 64-row tiles);
+// the quad kernel otherwise.  Measured on the U-Net's layers.
+template <typename T>
+static bool quad_eligible(const View& v, int cin, int cout);
+template <typename T>
+static bool col_eligible(const View& v, int cin, int cout);
+template <typename T>
+static bool prefer_col(const View& v, int cin, int cout) {
+  if (!col_eligible<T>(v, cin, cout)) return false;
+  if (!quad_eligible<T>(v, cin, cout)) return true;
+  return cout % 64 != 0 || v.n_pairs < 4 * v.n_out;
+}
+
+template <typename T>
+static bool col_eligible(const View& v, int cin, int cout) {
   const uint64_t x_bytes = (uint64_t)std::max<int64_t>(v.n_in, 1) * cin * sizeof(T);
   const uint64_t w_bytes = (uint64_t)v.K * cout * cin * sizeof(T);
   const int kb = (cin + 63) / 64;
-  const int max_kb = sizeof(T) == 4 ? 2 : 4;  // register budget of the main kernel
-  if (v.K <= 32767 && cin % 8 == 0 && kb <= max_kb && x_bytes < kOobOffset && w_bytes < kOobOffset) {
+  return cin % (16 / (int)sizeof(T)) == 0 && kb <= (sizeof(T) == 4 ? 2 : 4) && x_bytes < kOobOffset &&
+         w_bytes < kOobOffset && v.n_out < INT32_MAX &&
+         ceil_div(v.n_out, kChunkRows) * (v.K + 1) + ceil_div(v.n_pairs, 16) < INT32_MAX;
+}
+
+template <typename T>
+static sscn_status launch_col(const T* X, const T* Bt, const View& v, int cin, int cout, T* Y, hipStream_t s) {
+  if (v.n_out == 0) return SSCN_OK;
+  SSCN_TRY(ensure_chunks(v, s));
+  const uint32_t xb = (uint32_t)((uint64_t)std::max<int64_t>(v.n_in, 1) * cin * sizeof(T));
+  const uint32_t wb = (uint32_t)((uint64_t)v.K * cout * cin * sizeof(T));
+  switch ((cin + 63) / 64) {
+    case 1: return launch_col_kb<T, 1, 3>(X, xb, Bt, wb, v, cin, cout, Y, s);
+    case 2: return launch_col_kb<T, 2, 2>(X, xb, Bt, wb, v, cin, cout, Y, s);
+    default:
+      if constexpr (sizeof(T) == 2) {
+        if ((cin + 63) / 64 == 3) return launch_col_kb<T, 3, 2>(X, xb, Bt, wb, v, cin, cout, Y, s);
+        return launch_col_kb<T, 4, 2>(X, xb, Bt, wb, v, cin, cout, Y, s);
+      }
+      return fail(SSCN_ERR_SHAPE, "channel count outside the column kernel");
+  }
+}
+
+template <typename T>
+static bool quad_eligible(const View& v, int cin, int cout) {
+  const uint64_t x_bytes = (uint64_t)std::max<int64_t>(v.n_in, 1) * cin * sizeof(T);
+  const uint64_t w_bytes = (uint64_t)v.K * cout * cin * sizeof(T);
+  const int kb = (cin + 63) / 64;
+  const int max_kb = sizeof(T) == 4 ? 2 : 4;  // register budget of the quad kernel
+  return v.K <= 32767 && cin % 8 == 0 && kb <= max_kb && x_bytes < kOobOffset && w_bytes < kOobOffset;
+}
+
+template <typename T, bool WT>
+static sscn_status launch_conv(const T* X, const T* W, const View& v, int cin, int cout, T* Y, hipStream_t s) {
+  if (v.st->n_tiles == 0) return SSCN_OK;
+  if (WT && prefer_col<T>(v, cin, cout)) return launch_col<T>(X, W, v, cin, cout, Y, s);
+  const uint64_t x_bytes = (uint64_t)std::max<int64_t>(v.n_in, 1) * cin * sizeof(T);
+  const uint64_t w_bytes = (uint64_t)v.K * cout * cin * sizeof(T);
+  const int kb = (cin + 63) / 64;
+  if (quad_eligible<T>(v, cin, cout)) {
     const uint32_t xb = (uint32_t)x_bytes, wb = (uint32_t)w_bytes;
     switch (kb) {
       case 1: return launch_quad<T, 4, 1, WT>(X, xb, W, wb, v, cin, cout, Y, s);
@@ -752,6 +1075,17 @@ static sscn_status check_conv_args(sscn_rulebook rb, int32_t c_in, int32_t c_out
 // bf16 reads the stored layout directly.
 template <typename T>
 static sscn_status forward_t(const T* X, const T* W, const View& v, int cin, int cout, T* Y, hipStream_t s) {
+  if (prefer_col<T>(v, cin, cout)) {
+    if (v.n_out == 0) return SSCN_OK;
+    const int64_t total = (int64_t)v.K * cin * cout;
+    T* Bt = nullptr;
+    SSCN_TRY(dev_alloc((void**)&Bt, sizeof(T) * total, s));
+    k_transpose_w<T><<<(unsigned)std::min<int64_t>(ceil_div(total, 256), 4096), 256, 0, s>>>(W, v.K, cin, cout, Bt);
+    hipError_t e = hipGetLastError();
+    sscn_status st = e == hipSuccess ? launch_col<T>(X, Bt, v, cin, cout, Y, s) : hip_fail(e, "transpose");
+    dev_free(Bt, s);
+    return st;
+  }
   if constexpr (sizeof(T) == 2) {
     return launch_conv<T, false>(X, W, v, cin, cout, Y, s);
   } else {

@@ -8,6 +8,7 @@
 #include <new>
 #include <cstdint>
 #include <string>
+#include <mutex>
 #include <vector>
 
 #include "sscn.h"
@@ -18,6 +19,9 @@ namespace sscn {
 // every (offset o, tile t), one contiguous segment of pairs whose output row
 // lies in tile t.  Segments are laid out offset-major: seg[o * n_tiles + t].
 constexpr int kTile = 64;
+// Output rows per tile of the padded chunk table (a multiple of kTile, at
+// most 255 so that a row inside a tile and the padding row fit in a byte).
+constexpr int kChunkRows = 128;
 constexpr int kWave = 64;
 // Tiles are grouped into this many contiguous ranges, one per XCD of the
 // chip (each XCD has its own L2); see the tile order of a rule book.
@@ -63,6 +67,14 @@ struct Storage {
   int32_t* in_rows = nullptr;    // n_pairs
   int32_t* out_rows = nullptr;   // n_pairs
   int32_t* order = nullptr;      // n_tiles: per tile group (contiguous range), tiles by decreasing work
+  // The same pairs as a padded chunk table: output rows cut into tiles of
+  // kChunkRows rows; within a tile, per offset, the pairs in chunks of 16
+  // (the last chunk padded).  Chunks are numbered tile-major, then by offset.
+  int64_t n_ctiles = 0;
+  int32_t* ctile = nullptr;      // K * n_ctiles + 1: first chunk of (tile, offset); last entry = chunk count
+  int32_t* c_in = nullptr;       // 16 per chunk: input row, -1 for padding
+  uint8_t* c_out = nullptr;      // 16 per chunk: output row - tile start, kChunkRows for padding
+  int32_t* c_off = nullptr;      // per chunk: offset (as stored)
 };
 
 struct RulebookData {
@@ -79,6 +91,11 @@ struct RulebookData {
   int32_t* out_coords = nullptr; // n_out x 4
   int32_t* in_coords = nullptr;  // n_in x 4 (SC only; an SSC's input sites are its output sites)
   std::vector<void*> blocks;     // device allocations owning all of the above
+  // The chunk tables are built on first use (by the kernels that read
+  // them) on the build stream; `chunk_ready` is recorded after the build so
+  // that work on other streams can wait for it.
+  std::mutex chunk_mu;
+  hipEvent_t chunk_ready = nullptr;
   ~RulebookData();
 };
 
@@ -97,12 +114,20 @@ struct View {
   int K;
   bool mirror;        // segment for offset o is stored under K-1-o
   int64_t n_in, n_out;
+  int64_t n_pairs;
+  RulebookData* owner;
 };
+
+// Builds the padded chunk table of the view's storage if it is not there
+// yet and makes `s` wait for it.
+sscn_status ensure_chunks(const View& v, hipStream_t s);
 
 inline View view_of(const sscn_rulebook_s* rb) {
   const RulebookData* d = rb->d;
   View v;
   v.K = d->K;
+  v.n_pairs = d->n_pairs;
+  v.owner = rb->d;
   if (!rb->transposed) {
     v.st = &d->fwd; v.mirror = false; v.n_in = d->n_in; v.n_out = d->n_out;
   } else if (d->submanifold) {

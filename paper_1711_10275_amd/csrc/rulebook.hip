@@ -356,6 +356,72 @@ static inline unsigned grid_for(int64_t threads, int block) {
 }
 
 
+// ------------------------------------------------------- chunk table
+// Chunks per (tile, offset) of the padded chunk table.  A tile without any
+// pair gets one padding chunk, so that its output rows are still written.
+__global__ void k_chunk_count(const int64_t* __restrict__ seg, int64_t n_tiles, int K, int64_t n_ct,
+                              int32_t* __restrict__ cnt) {
+  const int64_t tt = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (tt >= n_ct) return;
+  constexpr int S = kChunkRows / kTile;
+  const int64_t t_lo = tt * S, t_hi = min<int64_t>(t_lo + S, n_tiles);
+  int total = 0;
+  for (int o = 0; o < K; ++o) {
+    const int64_t c = seg[o * n_tiles + t_hi] - seg[o * n_tiles + t_lo];
+    const int ch = (int)((c + 15) >> 4);
+    cnt[tt * K + o] = ch;
+    total += ch;
+  }
+  if (total == 0) cnt[tt * K] = 1;
+}
+
+// One thread per pair of offset blockIdx.y: its chunk and slot follow from
+// its rank inside the (tile, offset) segment; the segment's last pair pads
+// the rest of its chunk.
+__global__ void k_chunk_fill(const int64_t* __restrict__ seg, int64_t n_tiles, int K,
+                             const int32_t* __restrict__ in_rows, const int32_t* __restrict__ out_rows,
+                             const int32_t* __restrict__ ctile, int32_t* __restrict__ c_in,
+                             uint8_t* __restrict__ c_out, int32_t* __restrict__ c_off) {
+  constexpr int S = kChunkRows / kTile;
+  const int o = blockIdx.y;
+  const int64_t p = seg[(int64_t)o * n_tiles] + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= seg[(int64_t)(o + 1) * n_tiles]) return;
+  const int32_t orow = out_rows[p];
+  const int64_t tt = orow / kChunkRows;
+  const int64_t base = seg[o * n_tiles + tt * S];
+  const int64_t end = seg[o * n_tiles + min<int64_t>(tt * S + S, n_tiles)];
+  const int64_t q = p - base;
+  const int64_t ch = ctile[tt * K + o] + (q >> 4);
+  const int slot = (int)(q & 15);
+  c_in[ch * 16 + slot] = in_rows[p];
+  c_out[ch * 16 + slot] = (uint8_t)(orow - tt * kChunkRows);
+  if (slot == 0) c_off[ch] = o;
+  if (p + 1 == end)
+    for (int e = slot + 1; e < 16; ++e) {
+      c_in[ch * 16 + e] = -1;
+      c_out[ch * 16 + e] = (uint8_t)kChunkRows;
+    }
+}
+
+// The padding chunk of a tile without pairs.
+__global__ void k_chunk_pad(const int64_t* __restrict__ seg, int64_t n_tiles, int K, int64_t n_ct,
+                            const int32_t* __restrict__ ctile, int32_t* __restrict__ c_in,
+                            uint8_t* __restrict__ c_out, int32_t* __restrict__ c_off) {
+  const int64_t tt = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (tt >= n_ct) return;
+  constexpr int S = kChunkRows / kTile;
+  const int64_t t_lo = tt * S, t_hi = min<int64_t>(t_lo + S, n_tiles);
+  int64_t pairs = 0;
+  for (int o = 0; o < K; ++o) pairs += seg[o * n_tiles + t_hi] - seg[o * n_tiles + t_lo];
+  if (pairs != 0) return;
+  const int64_t ch = ctile[tt * K];
+  for (int e = 0; e < 16; ++e) {
+    c_in[ch * 16 + e] = -1;
+    c_out[ch * 16 + e] = (uint8_t)kChunkRows;
+  }
+  c_off[ch] = 0;
+}
+
 // One device allocation carved into 256-byte aligned parts.
 struct Arena {
   size_t total = 0;
@@ -452,6 +518,54 @@ static sscn_status build_tile_order(Storage& st, int K, hipStream_t s) {
   SSCN_TRY(exclusive_scan_i32(hist, hist, bins, s));
   k_tile_scatter<<<grid_for(st.n_tiles, 256), 256, 0, s>>>(key, st.n_tiles, hist, st.order);
   SSCN_HIP(hipGetLastError());
+  return SSCN_OK;
+}
+
+// Padded chunk table of one direction (seg and pair arrays complete).
+// Allocated in the rule book's own blocks.
+static sscn_status build_chunks(RulebookData* d, Storage& st, int64_t n_rows, int K, hipStream_t s) {
+  const int64_t n_ct = ceil_div(n_rows, kChunkRows);
+  st.n_ctiles = n_ct;
+  const int64_t cap = ceil_div(d->n_pairs, 16) + n_ct * (K + 1);
+  Arena a;
+  a.add(&st.ctile, (size_t)K * n_ct + 1);
+  a.add(&st.c_in, (size_t)cap * 16);
+  a.add(&st.c_out, (size_t)cap * 16);
+  a.add(&st.c_off, (size_t)cap);
+  SSCN_TRY(owned_alloc(d, a, s));
+  if (n_ct == 0) return fill_i32(st.ctile, 0, 1, s);
+  k_chunk_count<<<grid_for(n_ct, 256), 256, 0, s>>>(st.seg, st.n_tiles, K, n_ct, st.ctile);
+  SSCN_HIP(hipGetLastError());
+  SSCN_TRY(exclusive_scan_i32(st.ctile, st.ctile, (int64_t)K * n_ct, s));
+  int64_t max_ppo = 0;
+  for (int64_t c : d->pairs_per_offset) max_ppo = std::max(max_ppo, c);
+  if (max_ppo > 0) {
+    k_chunk_fill<<<dim3((unsigned)ceil_div(max_ppo, 256), (unsigned)K), 256, 0, s>>>(
+        st.seg, st.n_tiles, K, st.in_rows, st.out_rows, st.ctile, st.c_in, st.c_out, st.c_off);
+    SSCN_HIP(hipGetLastError());
+  }
+  k_chunk_pad<<<grid_for(n_ct, 256), 256, 0, s>>>(st.seg, st.n_tiles, K, n_ct, st.ctile, st.c_in, st.c_out,
+                                                   st.c_off);
+  SSCN_HIP(hipGetLastError());
+  return SSCN_OK;
+}
+
+sscn_status ensure_chunks(const View& v, hipStream_t s) {
+  RulebookData* d = v.owner;
+  Storage& st = v.st == &d->fwd ? d->fwd : d->bwd;
+  {
+    std::lock_guard<std::mutex> lock(d->chunk_mu);
+    if (st.ctile == nullptr) {
+      int cur = 0;
+      SSCN_HIP(hipGetDevice(&cur));
+      if (cur != d->device) return fail(SSCN_ERR_INVALID_ARG, "rule book used on another device");
+      const int64_t n_rows = &st == &d->fwd ? d->n_out : d->n_in;
+      SSCN_TRY(build_chunks(d, st, n_rows, d->K, d->stream));
+      if (!d->chunk_ready) SSCN_HIP(hipEventCreateWithFlags(&d->chunk_ready, hipEventDisableTiming));
+      SSCN_HIP(hipEventRecord(d->chunk_ready, d->stream));
+    }
+  }
+  if (s != d->stream) SSCN_HIP(hipStreamWaitEvent(s, d->chunk_ready, 0));
   return SSCN_OK;
 }
 

@@ -61,6 +61,7 @@ RulebookData::~RulebookData() {
   (void)hipGetDevice(&cur);
   if (cur != device) (void)hipSetDevice(device);
   for (void* p : blocks) dev_free(p, stream);
+  if (chunk_ready) (void)hipEventDestroy(chunk_ready);
   if (cur != device) (void)hipSetDevice(cur);
 }
 

@@ -51,7 +51,7 @@ def test_sc_then_ssc_forward(dtype):
     assert_close(_fwd(ssc, Yr, W2, dtype), O.forward(Yr, W2, O.ssc_rulebook(oc, sc.out_size, 3)), dtype, "ssc64")
 
 
-CH = [(1, 1), (3, 5), (16, 16), (32, 48), (70, 33), (130, 20), (64, 136), (8, 300)]
+CH = [(1, 1), (3, 5), (16, 16), (32, 48), (70, 33), (130, 20), (64, 136), (8, 300), (48, 64), (96, 128)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
