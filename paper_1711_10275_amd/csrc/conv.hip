@@ -457,7 +457,7 @@ __global__ void k_transpose_w(const T* __restrict__ W, int K, int cin, int cout,
 // each.  One MFMA step consumes 4 pairs (one per lane group).  Each
 // wavefront accumulates the whole CA*16 x CB*16 block over a quarter of
 // the workgroup's pairs, with pair indices and rows fetched one iteration
-// (16 pairs) ahead; the four partial blocks are summed through LDS and
+// (4 pairs) ahead; the four partial blocks are summed through LDS and
 // added to dW with fp32 atomics.  A workgroup's pairs are those of one
 // offset whose output rows lie in a range of `tr` consecutive tiles, so the
 // rows it gathers are spatially close; workgroups are numbered so that each
@@ -492,7 +492,7 @@ __global__ __launch_bounds__(256) void k_wgrad_reg(const T* __restrict__ X, cons
                                                    const int32_t* __restrict__ in_rows,
                                                    const int32_t* __restrict__ out_rows, int K, int mirror,
                                                    int cin, int cout, int tr, int nzc, float* __restrict__ dW) {
-  constexpr int STEPS = 4;  // MFMA steps (4 pairs each) per iteration
+  constexpr int STEPS = 1;  // MFMA steps (4 pairs each) per iteration (more costs occupancy)
   const int64_t item = xcd_remap(blockIdx.x, gridDim.x);
   const int o = (int)(item % K);
   const int64_t r = item / K;
@@ -568,23 +568,35 @@ __global__ __launch_bounds__(256) void k_wgrad_reg(const T* __restrict__ X, cons
       }
     }
   }
-  // sum the four wavefronts' partial blocks (LDS atomic adds into one
-  // block), then add the block to dW.  D[4g + r][m] of block (a, b) is
-  // dW[ci0 + CA (4g + r) + a][co0 + CB m + b].
+  // sum the four wavefronts' partial blocks, then add the block to dW.
+  // Waves 0 and 1 store theirs in two LDS copies, waves 2 and 3 add theirs
+  // (plain loads and stores: LDS float atomics are several times slower),
+  // and every thread adds the two copies of its elements to dW.
+  // D[4g + r][m] of block (a, b) is dW[ci0 + CA (4g + r) + a][co0 + CB m + b].
   constexpr int NE = CA * CB * 4;  // values per lane
-  __shared__ float part[NE][64];
-  for (int e = threadIdx.x; e < NE * 64; e += 256) (&part[0][0])[e] = 0.f;
+  __shared__ float part[2][NE][64];
+  float(*mine)[64] = part[wave & 1];
+  if (wave < 2) {
+#pragma unroll
+    for (int a = 0; a < CA; ++a)
+#pragma unroll
+      for (int b = 0; b < CB; ++b)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) mine[(a * CB + b) * 4 + r][lane] = d[a][b][r];
+  }
   __syncthreads();
+  if (wave >= 2) {
 #pragma unroll
-  for (int a = 0; a < CA; ++a)
+    for (int a = 0; a < CA; ++a)
 #pragma unroll
-    for (int b = 0; b < CB; ++b)
+      for (int b = 0; b < CB; ++b)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) atomicAdd(&part[(a * CB + b) * 4 + r][lane], d[a][b][r]);
+        for (int r = 0; r < 4; ++r) mine[(a * CB + b) * 4 + r][lane] += d[a][b][r];
+  }
   __syncthreads();
   for (int e = threadIdx.x; e < NE * 64; e += 256) {
     const int v = e / 64, l = e % 64;
-    const float sum = part[v][l];
+    const float sum = part[0][v][l] + part[1][v][l];
     const int a = v / (CB * 4), b = (v / 4) % CB, r = v % 4;
     const int mm = l & 15, gg = l >> 4;
     const int ci = ci0 + CA * (4 * gg + r) + a, co = co0 + CB * mm + b;
@@ -1018,6 +1030,177 @@ static sscn_status launch_conv(const T* X, const T* W, const View& v, int cin, i
 }
 
 
+// N contiguous channels of one row as fp32, one raw buffer load (an
+// out-of-range offset reads zeros).
+template <typename T, int N> struct RowLoad;
+template <int N> struct RowLoad<float, N> {
+  static __device__ __forceinline__ void load(rsrc_t r, uint32_t off, float (&v)[N]) {
+    if constexpr (N == 4) {
+      const auto q = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+      v[0] = __uint_as_float(q[0]); v[1] = __uint_as_float(q[1]); v[2] = __uint_as_float(q[2]); v[3] = __uint_as_float(q[3]);
+    } else if constexpr (N == 2) {
+      const auto q = __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0);
+      v[0] = __uint_as_float(q[0]); v[1] = __uint_as_float(q[1]);
+    } else {
+      v[0] = __uint_as_float((uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0));
+    }
+  }
+};
+template <int N> struct RowLoad<bf16_t, N> {
+  static __device__ __forceinline__ void load(rsrc_t r, uint32_t off, float (&v)[N]) {
+    if constexpr (N == 4) {
+      const auto q = __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0);
+      v[0] = bf16_to_f32(q[0] & 0xffff); v[1] = bf16_to_f32(q[0] >> 16);
+      v[2] = bf16_to_f32(q[1] & 0xffff); v[3] = bf16_to_f32(q[1] >> 16);
+    } else if constexpr (N == 2) {
+      const uint32_t q = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0);
+      v[0] = bf16_to_f32(q & 0xffff); v[1] = bf16_to_f32(q >> 16);
+    } else {
+      v[0] = bf16_to_f32((uint16_t)__builtin_amdgcn_raw_buffer_load_b16(r, (int)off, 0, 0));
+    }
+  }
+};
+
+// Work items of k_wgrad_ring: the output tiles are cut into ranges of `tr`
+// tiles; within a range, offset o contributes sub[o] items that split its
+// pairs in that range evenly (sub[o] ~ pairs of o / mean pairs per offset,
+// so that items have similar sizes).  first[o] = sum of sub[q], q < o.
+constexpr int kWgradMaxK = 128;
+struct WgradItems {
+  int32_t first[kWgradMaxK + 1];
+};
+
+// The same contraction as k_wgrad_reg with balanced items and a deeper
+// pipeline.  Items are numbered range-major (all items of tile range r, then
+// r + 1, ...) and renumbered so that each XCD takes a contiguous run of
+// ranges (L2 locality across the offsets of one range).  Each wavefront
+// walks its pairs 4 at a time (one MFMA step).  The pairs' row indices come
+// in batches of 64 (one coalesced load per 16 steps, two batches ahead) and
+// reach the lanes by shuffles; the rows are loaded R steps ahead into a
+// register ring with compile-time slots.  Row loads are branch-free (a pair
+// past the end reads out-of-range offsets, i.e. zeros), so the compiler's
+// wait counts stay exact; a wave's last batch is padded with such empty
+// steps.  Needs X and dY below kOobOffset bytes.
+template <typename T, int CA, int CB, int R>
+__global__ __launch_bounds__(256) void k_wgrad_ring(const T* __restrict__ X, uint32_t x_bytes,
+                                                    const T* __restrict__ dY, uint32_t y_bytes,
+                                                    const int64_t* __restrict__ seg, int64_t n_tiles,
+                                                    const int32_t* __restrict__ in_rows,
+                                                    const int32_t* __restrict__ out_rows, int K, int mirror,
+                                                    int cin, int cout, int tr, WgradItems items, int nzc,
+                                                    float* __restrict__ dW) {
+  static_assert(16 % R == 0, "ring depth must divide a batch");
+  const int S = items.first[K];
+  const int64_t item = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t r = item / S;
+  const int w = (int)(item % S);
+  int o = 0;
+  while (items.first[o + 1] <= w) ++o;
+  const int sub = w - items.first[o], n_sub = items.first[o + 1] - items.first[o];
+  const int so = mirror ? K - 1 - o : o;
+  const int64_t t_lo = r * tr, t_hi = min<int64_t>(t_lo + tr, n_tiles);
+  const int64_t rb = seg[(int64_t)so * n_tiles + t_lo];
+  const int64_t rn = seg[(int64_t)so * n_tiles + t_hi] - rb;
+  const int64_t pb = rb + rn * sub / n_sub, pe = rb + rn * (sub + 1) / n_sub;
+  if (pb >= pe) return;
+  const int ci0 = (blockIdx.y % nzc) * 16 * CA, co0 = (blockIdx.y / nzc) * 16 * CB;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int m = lane & 15, g = lane >> 4;
+  // a lane's channels are fully inside or fully outside [0, cin) / [0, cout)
+  const uint32_t a_lane = ci0 + CA * m + CA <= cin ? (uint32_t)(ci0 + CA * m) * sizeof(T) : kOobOffset;
+  const uint32_t b_lane = co0 + CB * m + CB <= cout ? (uint32_t)(co0 + CB * m) * sizeof(T) : kOobOffset;
+  const uint32_t x_row = (uint32_t)cin * sizeof(T), y_row = (uint32_t)cout * sizeof(T);
+  const rsrc_t rx = make_rsrc(X, x_bytes), ry = make_rsrc(dY, y_bytes);
+  const int64_t per = ((pe - pb + 3) / 4 + 3) / 4 * 4;
+  const int64_t wb = pb + wave * per, we = min<int64_t>(wb + per, pe);
+
+  f32x4 d[CA][CB];
+#pragma unroll
+  for (int a = 0; a < CA; ++a)
+#pragma unroll
+    for (int b = 0; b < CB; ++b) d[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  if (wb < we) {
+    // pair indices: one coalesced load per 64 pairs (16 steps), lane l
+    // holding pair base + l; a step's pair for lane group g is taken from
+    // lane 4 s + g of the batch by a shuffle
+    int32_t bi_in[3], bi_out[3];   // batches k, k + 1, k + 2 (in flight)
+    float xa[R][CA], yb[R][CB];
+    auto load_batch = [&](int64_t base, int slot) {
+      const int64_t q = min<int64_t>(base + lane, we - 1);
+      bi_in[slot] = in_rows[q];
+      bi_out[slot] = out_rows[q];
+    };
+    // rows of step t (t = 16 batch + s; `slot` holds that batch)
+    const int n_mine = (int)(we - wb);  // pairs of this wavefront
+    auto fetch_rows = [&](int t, int slot, int s16, int ds) {
+      const int src = 4 * s16 + g;
+      const int32_t irow = __shfl(bi_in[slot], src, 64);
+      const int32_t orow = __shfl(bi_out[slot], src, 64);
+      const bool ok = 4 * t + g < n_mine;
+      const uint32_t xo = ok ? (uint32_t)irow * x_row : kOobOffset;
+      const uint32_t yo = ok ? (uint32_t)orow * y_row : kOobOffset;
+      RowLoad<T, CA>::load(rx, xo + a_lane, xa[ds]);
+      RowLoad<T, CB>::load(ry, yo + b_lane, yb[ds]);
+    };
+    const int n_steps = (n_mine + 3) / 4;
+    load_batch(wb, 0);
+    load_batch(wb + 64, 1);
+#pragma unroll
+    for (int sl = 0; sl < R; ++sl) fetch_rows(sl, 0, sl, sl);
+    for (int b0 = 0; b0 < n_steps; b0 += 16) {
+      load_batch(wb + 4 * (b0 + 32), 2);
+#pragma unroll
+      for (int s16 = 0; s16 < 16; ++s16) {
+        const int ds = s16 % R;
+#pragma unroll
+        for (int a = 0; a < CA; ++a)
+#pragma unroll
+          for (int b = 0; b < CB; ++b)
+            d[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(xa[ds][a], yb[ds][b], d[a][b], 0, 0, 0);
+        const int nx = s16 + R;  // step to request, relative to this batch
+        if (nx < 16)
+          fetch_rows(b0 + nx, 0, nx, ds);
+        else
+          fetch_rows(b0 + nx, 1, nx - 16, ds);
+      }
+      bi_in[0] = bi_in[1]; bi_out[0] = bi_out[1];
+      bi_in[1] = bi_in[2]; bi_out[1] = bi_out[2];
+    }
+  }
+  // sum the four wavefronts' partial blocks, then add the block to dW
+  // (as in k_wgrad_reg)
+  constexpr int NE = CA * CB * 4;
+  __shared__ float part[2][NE][64];
+  float(*mine)[64] = part[wave & 1];
+  if (wave < 2) {
+#pragma unroll
+    for (int a = 0; a < CA; ++a)
+#pragma unroll
+      for (int b = 0; b < CB; ++b)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) mine[(a * CB + b) * 4 + q][lane] = d[a][b][q];
+  }
+  __syncthreads();
+  if (wave >= 2) {
+#pragma unroll
+    for (int a = 0; a < CA; ++a)
+#pragma unroll
+      for (int b = 0; b < CB; ++b)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) mine[(a * CB + b) * 4 + q][lane] += d[a][b][q];
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < NE * 64; e += 256) {
+    const int v = e / 64, l = e % 64;
+    const float sum = part[0][v][l] + part[1][v][l];
+    const int a = v / (CB * 4), b = (v / 4) % CB, q = v % 4;
+    const int mm = l & 15, gg = l >> 4;
+    const int ci = ci0 + CA * (4 * gg + q) + a, co = co0 + CB * mm + b;
+    if (ci < cin && co < cout && sum != 0.f) atomicAdd(dW + ((int64_t)o * cin + ci) * cout + co, sum);
+  }
+}
+
 template <typename T, int CA, int CB>
 static sscn_status launch_wgrad_reg(const T* X, const T* dY, const View& v, int cin, int cout, float* dW,
                                     hipStream_t s, int64_t max_ppo, int64_t n_pairs) {
@@ -1029,6 +1212,29 @@ static sscn_status launch_wgrad_reg(const T* X, const T* dY, const View& v, int 
   const int64_t n_items = ceil_div(v.st->n_tiles, tr) * v.K;
   const int nzc = (cin + 16 * CA - 1) / (16 * CA);
   const int nzo = (cout + 16 * CB - 1) / (16 * CB);
+  const uint64_t x_bytes = (uint64_t)std::max<int64_t>(v.n_in, 1) * cin * sizeof(T);
+  const uint64_t y_bytes = (uint64_t)std::max<int64_t>(v.n_out, 1) * cout * sizeof(T);
+  if (x_bytes < kOobOffset && y_bytes < kOobOffset && v.K <= kWgradMaxK) {
+    // sub-items per offset ~ its share of the pairs, about 1536 items in all
+    const std::vector<int64_t>& ppo = v.owner->pairs_per_offset;
+    const double mean = (double)std::max<int64_t>(v.n_pairs, 1) / v.K;
+    WgradItems items{};
+    items.first[0] = 0;
+    for (int o = 0; o < v.K; ++o) {
+      const double p = (double)ppo[v.mirror ? v.K - 1 - o : o];
+      items.first[o + 1] = items.first[o] + std::max(1, (int)(p / mean + 0.5));
+    }
+    const int S = items.first[v.K];
+    const int64_t tr2 = std::max<int64_t>(1, ceil_div(v.st->n_tiles * S, 1536));
+    const int64_t total = ceil_div(v.st->n_tiles, tr2) * S;
+    SSCN_TRY(fill_f32(dW, 0.f, (int64_t)v.K * cin * cout, s));
+    k_wgrad_ring<T, CA, CB, 4><<<dim3((unsigned)total, (unsigned)(nzc * nzo)), 256, 0, s>>>(
+        X, (uint32_t)x_bytes, dY, (uint32_t)y_bytes, v.st->seg, v.st->n_tiles, v.st->in_rows, v.st->out_rows, v.K,
+        v.mirror ? 1 : 0, cin, cout, (int)tr2, items, nzc, dW);
+    SSCN_HIP(hipGetLastError());
+    return SSCN_OK;
+  }
+  SSCN_TRY(fill_f32(dW, 0.f, (int64_t)v.K * cin * cout, s));
   k_wgrad_reg<T, CA, CB><<<dim3((unsigned)n_items, (unsigned)(nzc * nzo)), 256, 0, s>>>(
       X, dY, v.st->seg, v.st->n_tiles, v.st->in_rows, v.st->out_rows, v.K, v.mirror ? 1 : 0, cin, cout, (int)tr,
       nzc, dW);
@@ -1141,10 +1347,11 @@ extern "C" sscn_status sparse_conv_backward(const void* features, const void* we
   }
   if (wgrad) {
     const int64_t total = (int64_t)v.K * c_in * c_out;
-    st = fill_f32(wgrad, 0.f, total, stream);
-    if (st != SSCN_OK) return st;
     const RulebookData* d = rb->d;
-    if (d->n_pairs > 0) {
+    if (d->n_pairs == 0) {
+      st = fill_f32(wgrad, 0.f, total, stream);
+      if (st != SSCN_OK) return st;
+    } else {
       if (!features || !dout) return fail(SSCN_ERR_INVALID_ARG, "NULL features or dout");
       int64_t mx = 0;
       for (int64_t c : d->pairs_per_offset) mx = std::max(mx, c);
