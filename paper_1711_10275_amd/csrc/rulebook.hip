@@ -70,7 +70,11 @@ __device__ __forceinline__ int32_t table_lookup(const Slot* __restrict__ table, 
 
 // Every slot empty; the row field starts at row_init (INT32_MAX for the
 // first-visit minimum of the SC output dictionary).
-__global__ void k_fill_slots(Slot* __restrict__ table, uint64_t cap, int32_t row_init) {
+// Also zeroes the first n_zero words of `zero` (the build's counters).
+__global__ void k_fill_slots(Slot* __restrict__ table, uint64_t cap, int32_t row_init,
+                             unsigned long long* __restrict__ zero, int n_zero) {
+  if (blockIdx.x == 0)
+    for (int i = threadIdx.x; i < n_zero; i += blockDim.x) zero[i] = 0;
   for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < cap;
        i += (uint64_t)gridDim.x * blockDim.x) {
     Slot v;
@@ -85,13 +89,15 @@ __device__ __forceinline__ bool in_grid(int x0, int x1, int x2, int L0, int L1, 
   return (unsigned)x0 < (unsigned)L0 && (unsigned)x1 < (unsigned)L1 && (unsigned)x2 < (unsigned)L2;
 }
 
-// Insert every site; flag coordinates outside the grid and repeated locations.
+// Insert every site; flag coordinates outside the grid and repeated
+// locations.  copy (if not NULL) receives the coordinates.
 __global__ __launch_bounds__(256) void k_insert(const int4* __restrict__ coords, int64_t n, int L0,
                                                 int L1, int L2, Slot* __restrict__ table, uint64_t mask,
-                                                unsigned long long* __restrict__ flags) {
+                                                unsigned long long* __restrict__ flags, int4* __restrict__ copy) {
   int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (j >= n) return;
   int4 c = coords[j];
+  if (copy) copy[j] = c;
   if ((unsigned)c.x >= (unsigned)kMaxBatch || !in_grid(c.y, c.z, c.w, L0, L1, L2)) {
     atomicOr(flags, (unsigned long long)kFlagOutOfRange);
     return;
@@ -115,17 +121,17 @@ __global__ __launch_bounds__(256) void k_insert(const int4* __restrict__ coords,
 }
 
 // ---------------------------------------------------------------- SSC probe
-// One wavefront per tile of 64 output sites.  nbr is offset-major [K][n]:
-// nbr[o*n + k] = row of the input at x_k + i_o - (f-1)/2, or -1.
-// counts[o*n_tiles + t] = number of hits of tile t at offset o (ballot).
-// F > 0: compile-time filter size; the probes of one i0-plane (F*F offsets)
-// are issued together so their loads overlap.  F == 0: runtime f.
-template <int F>
+// One wavefront per (tile of 64 output sites, slice of P consecutive
+// offsets); blockIdx.y selects the slice.  Many small wavefronts keep enough
+// independent lookups in flight (the probe is bound by the latency of the
+// table reads).  nbr is offset-major [K][n]: nbr[o*n + k] = row of the input
+// at x_k + i_o - (f-1)/2, or -1.  counts[o*n_tiles + t] = number of hits of
+// tile t at offset o (ballot).
+template <int P>
 __global__ __launch_bounds__(256) void k_ssc_probe(
-    const int4* __restrict__ coords, int64_t n, int L0, int L1, int L2, int f_rt,
+    const int4* __restrict__ coords, int64_t n, int L0, int L1, int L2, int f,
     const Slot* __restrict__ table, uint64_t mask, int32_t* __restrict__ nbr, int64_t* __restrict__ counts,
     int64_t n_tiles) {
-  const int f = F > 0 ? F : f_rt;
   const int lane = threadIdx.x & 63;
   const int64_t t = (int64_t)blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6);
   if (t >= n_tiles) return;  // uniform per wavefront
@@ -134,38 +140,37 @@ __global__ __launch_bounds__(256) void k_ssc_probe(
   const int4 c = valid ? coords[k] : make_int4(0, 0, 0, 0);
   const bool site_ok = valid && (unsigned)c.x < (unsigned)kMaxBatch && in_grid(c.y, c.z, c.w, L0, L1, L2);
   const int h = (f - 1) / 2;
-  constexpr int P = F > 0 ? F * F : 1;  // probes in flight per lane
-  const int plane = f * f;
-  for (int o0 = 0; o0 < f * f * f; o0 += (F > 0 ? P : 1)) {
-    uint64_t key[P];
-    uint64_t slot[P];
-    bool live[P];
-    Slot v[P];
+  const int plane = f * f, K = f * f * f;
+  const int o0 = (int)blockIdx.y * P;
+  uint64_t key[P];
+  uint64_t slot[P];
+  bool live[P];
+  Slot v[P];
 #pragma unroll
-    for (int q = 0; q < P; ++q) {
-      const int o = o0 + q;
-      const int i0 = o / plane, i1 = (o / f) % f, i2 = o % f;
-      const int y0 = c.y + i0 - h, y1 = c.z + i1 - h, y2 = c.w + i2 - h;
-      live[q] = site_ok && in_grid(y0, y1, y2, L0, L1, L2);
-      key[q] = pack_key(c.x, y0, y1, y2);
-      slot[q] = mix64(key[q]) & mask;
-      if (live[q]) v[q] = table[slot[q]];
-    }
+  for (int q = 0; q < P; ++q) {
+    const int o = o0 + q;
+    const int i0 = o / plane, i1 = (o / f) % f, i2 = o % f;
+    const int y0 = c.y + i0 - h, y1 = c.z + i1 - h, y2 = c.w + i2 - h;
+    live[q] = o < K && site_ok && in_grid(y0, y1, y2, L0, L1, L2);
+    key[q] = pack_key(c.x, y0, y1, y2);
+    slot[q] = mix64(key[q]) & mask;
+    if (live[q]) v[q] = table[slot[q]];
+  }
 #pragma unroll
-    for (int q = 0; q < P; ++q) {
-      const int o = o0 + q;
-      int32_t row = -1;
-      if (live[q]) {
-        while (v[q].key != key[q] && v[q].key != kEmptyKey) {
-          slot[q] = (slot[q] + 1) & mask;
-          v[q] = table[slot[q]];
-        }
-        if (v[q].key == key[q]) row = v[q].row;
+  for (int q = 0; q < P; ++q) {
+    const int o = o0 + q;
+    if (o >= K) break;  // uniform
+    int32_t row = -1;
+    if (live[q]) {
+      while (v[q].key != key[q] && v[q].key != kEmptyKey) {
+        slot[q] = (slot[q] + 1) & mask;
+        v[q] = table[slot[q]];
       }
-      if (valid) nbr[(int64_t)o * n + k] = row;
-      const unsigned long long bal = __ballot(row >= 0);
-      if (lane == 0) counts[(int64_t)o * n_tiles + t] = __popcll(bal);
+      if (v[q].key == key[q]) row = v[q].row;
     }
+    if (valid) nbr[(int64_t)o * n + k] = row;
+    const unsigned long long bal = __ballot(row >= 0);
+    if (lane == 0) counts[(int64_t)o * n_tiles + t] = __popcll(bal);
   }
 }
 
@@ -478,8 +483,10 @@ static sscn_status readback(void* host, const void* dev, size_t bytes, hipStream
   return SSCN_OK;
 }
 
-static sscn_status launch_fill_slots(Slot* t, uint64_t cap, int32_t row_init, hipStream_t s) {
-  k_fill_slots<<<(unsigned)std::min<uint64_t>((cap + 255) / 256, 16384), 256, 0, s>>>(t, cap, row_init);
+static sscn_status launch_fill_slots(Slot* t, uint64_t cap, int32_t row_init, hipStream_t s,
+                                     unsigned long long* zero = nullptr, int n_zero = 0) {
+  k_fill_slots<<<(unsigned)std::min<uint64_t>((cap + 255) / 256, 16384), 256, 0, s>>>(t, cap, row_init, zero,
+                                                                                       n_zero);
   SSCN_HIP(hipGetLastError());
   return SSCN_OK;
 }
@@ -643,38 +650,43 @@ extern "C" sscn_status ssc_rulebook_build(const int32_t* coords, int64_t n, cons
     oa.add(&d->out_coords, (size_t)4 * n);
     SSCN_TRY(owned_alloc(d, oa, s));
 
-    SSCN_TRY(fill_u64((uint64_t*)stats, 0, 1 + K, s));
+    SSCN_TRY(launch_fill_slots(table, cap, -1, s, stats, 1 + K));
     if (n > 0) {
-      SSCN_TRY(launch_fill_slots(table, cap, -1, s));
-      k_insert<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, L0, L1, L2, table, cap - 1, stats);
+      k_insert<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, L0, L1, L2, table, cap - 1, stats,
+                                               (int4*)d->out_coords);
       SSCN_HIP(hipGetLastError());
-      if (f == 3)
-        k_ssc_probe<3><<<grid_for(n_tiles * 64, 256), 256, 0, s>>>((const int4*)coords, n, L0, L1, L2, f, table,
-                                                                  cap - 1, nbr, counts, n_tiles);
-      else
-        k_ssc_probe<0><<<grid_for(n_tiles * 64, 256), 256, 0, s>>>((const int4*)coords, n, L0, L1, L2, f, table,
-                                                                  cap - 1, nbr, counts, n_tiles);
+      constexpr int P = 3;  // lookups per wavefront
+      k_ssc_probe<P><<<dim3(grid_for(n_tiles * 64, 256), (unsigned)ceil_div(K, P)), 256, 0, s>>>(
+          (const int4*)coords, n, L0, L1, L2, f, table, cap - 1, nbr, counts, n_tiles);
       SSCN_HIP(hipGetLastError());
     }
     SSCN_TRY(exclusive_scan_i64(counts, d->fwd.seg, K * n_tiles, s));
     if (n > 0) {
       k_offset_totals<<<grid_for(K, 256), 256, 0, s>>>(d->fwd.seg, n_tiles, K, stats);
       SSCN_HIP(hipGetLastError());
-      SSCN_HIP(hipMemcpyAsync(d->out_coords, coords, sizeof(int32_t) * 4 * n, hipMemcpyDeviceToDevice, s));
     }
+    // Pair storage for the worst case (every offset of every site) when that
+    // is modest: then compaction and the tile order are queued before the
+    // one readback, and the host waits once.  Otherwise the exact size comes
+    // from the readback first.
+    const bool one_phase = (uint64_t)K * (uint64_t)n * 8u <= (512ull << 20);
+    auto finish = [&](int64_t cap_pairs) -> sscn_status {
+      Arena pa;
+      pa.add(&d->fwd.in_rows, cap_pairs);
+      pa.add(&d->fwd.out_rows, cap_pairs);
+      pa.add(&d->fwd.order, n_tiles);
+      SSCN_TRY(owned_alloc(d, pa, s));
+      if (n > 0) SSCN_TRY(compact_storage(nbr, n, K, d->fwd, s, /*counted=*/true));
+      return build_tile_order(d->fwd, K, s);
+    };
+    if (one_phase) SSCN_TRY(finish((int64_t)K * n));
     std::vector<unsigned long long> host(1 + K);
     SSCN_TRY(readback(host.data(), stats, sizeof(unsigned long long) * (1 + K), s));
     SSCN_TRY(flags_error(host[0]));
     int64_t total = 0;
     for (int o = 0; o < K; ++o) total += (d->pairs_per_offset[o] = (int64_t)host[1 + o]);
     d->n_pairs = total;
-    Arena pa;
-    pa.add(&d->fwd.in_rows, total);
-    pa.add(&d->fwd.out_rows, total);
-    pa.add(&d->fwd.order, n_tiles);
-    SSCN_TRY(owned_alloc(d, pa, s));
-    if (total > 0) SSCN_TRY(compact_storage(nbr, n, K, d->fwd, s, /*counted=*/true));
-    SSCN_TRY(build_tile_order(d->fwd, K, s));
+    if (!one_phase) SSCN_TRY(finish(total));
   }
   guard.release();
   return new_handle(d, out);
@@ -727,12 +739,12 @@ extern "C" sscn_status sc_rulebook_build(const int32_t* coords, int64_t n, const
     ia.add(&d->in_coords, (size_t)4 * n);
     SSCN_TRY(owned_alloc(d, ia, s));
 
-    SSCN_TRY(fill_u64((uint64_t*)stats, 0, 2 + K, s));
+    SSCN_TRY(launch_fill_slots(table, cap, -1, s, stats, 2 + K));
     if (n > 0) {
-      SSCN_TRY(launch_fill_slots(table, cap, -1, s));
       SSCN_TRY(launch_fill_slots(otable, ocap, INT32_MAX, s));
       // the input dictionary detects repeated locations and range errors
-      k_insert<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g.L0, g.L1, g.L2, table, cap - 1, stats);
+      k_insert<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g.L0, g.L1, g.L2, table, cap - 1, stats,
+                                               (int4*)d->in_coords);
       SSCN_HIP(hipGetLastError());
       k_sc_visit<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1);
       SSCN_HIP(hipGetLastError());
@@ -741,7 +753,7 @@ extern "C" sscn_status sc_rulebook_build(const int32_t* coords, int64_t n, const
       SSCN_TRY(exclusive_scan_i32(first, rank, n * K, s));
       // n_out = rank[n K] joins the readback
       SSCN_HIP(hipMemcpyAsync(stats + 1 + K, rank + (size_t)n * K, sizeof(int32_t), hipMemcpyDeviceToDevice, s));
-      SSCN_HIP(hipMemcpyAsync(d->in_coords, coords, sizeof(int32_t) * 4 * n, hipMemcpyDeviceToDevice, s));
+
     }
     std::vector<unsigned long long> host(2 + K);
     SSCN_TRY(readback(host.data(), stats, sizeof(unsigned long long) * (2 + K), s));
