@@ -851,10 +851,8 @@ __global__ __launch_bounds__(256) void k_conv_col(
 // Workgroups that fit on the device at once, capped by the work and rounded
 // up to a multiple of kTileGroups (every tile group gets workgroups).
 static unsigned persistent_grid(const void* kern, size_t lds, int64_t n_items) {
-  int dev = 0, cus = 256, per_cu = 1;
-  (void)hipGetDevice(&dev);
-  (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 256, lds) != hipSuccess || per_cu < 1) per_cu = 1;
+  int cus = 256, per_cu = 1;
+  occupancy(kern, 256, lds, &per_cu, &cus);
   int64_t g = std::min<int64_t>((int64_t)cus * per_cu, std::max<int64_t>(n_items, 1));
   g = ceil_div(g, kTileGroups) * kTileGroups;
   return (unsigned)g;
@@ -925,11 +923,8 @@ static sscn_status launch_col_kb(const T* X, uint32_t xb, const T* Bt, uint32_t 
   const int gy = (ng + ncol - 1) / ncol;
   const size_t lds = sizeof(float) * kColRegion * ncol;
   auto kern = k_conv_col<T, KB, RING>;
-  int dev = 0, cus = 256, per_cu = 1;
-  (void)hipGetDevice(&dev);
-  (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 64 * ncol, lds) != hipSuccess || per_cu < 1)
-    per_cu = 1;
+  int cus = 256, per_cu = 1;
+  occupancy((const void*)kern, 64 * ncol, lds, &per_cu, &cus);
   const int64_t gx = std::min<int64_t>(st.n_ctiles, std::max<int64_t>(1, (int64_t)cus * per_cu / gy));
   kern<<<dim3((unsigned)gx, (unsigned)gy), 64 * ncol, lds, s>>>(
       X, xb, Bt, wb, st.ctile, st.c_in, reinterpret_cast<const uint32_t*>(st.c_out), st.c_off, (int)st.n_ctiles,

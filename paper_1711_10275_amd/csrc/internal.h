@@ -143,6 +143,10 @@ inline View view_of(const sscn_rulebook_s* rb) {
 sscn_status exclusive_scan_i64(const int64_t* in, int64_t* out, int64_t count, hipStream_t s);
 sscn_status exclusive_scan_i32(const int32_t* in, int32_t* out, int64_t count, hipStream_t s);
 
+// Resident workgroups of `kern` per CU (block threads, dynamic LDS bytes) and
+// the CU count of the current device; cached per (device, kernel, shape).
+void occupancy(const void* kern, int block, size_t lds, int* per_cu, int* cus);
+
 // Fill helpers (graph-capture safe: kernels, not memset nodes).
 sscn_status fill_i32(int32_t* p, int32_t v, int64_t count, hipStream_t s);
 sscn_status fill_u64(uint64_t* p, uint64_t v, int64_t count, hipStream_t s);

@@ -249,6 +249,156 @@ __global__ void k_tile_scatter(const int32_t* __restrict__ key, int64_t n_tiles,
   order[atomicAdd(&cursor[key[t]], 1)] = (int32_t)t;
 }
 
+// --------------------------------------------------- one-workgroup passes
+// For the small arrays of a build a single workgroup of 1024 threads does a
+// whole pass in one launch (launches dominate such passes).
+constexpr int kOneBlock = 1024;
+constexpr int64_t kOneBlockScanMax = 1 << 17;     // elements
+
+// Exclusive prefix of the per-thread values `v` over the workgroup (1024
+// threads = 16 wavefronts); returns the total through `total`.
+__device__ int64_t block_exclusive_scan(int64_t v, int64_t* wave_tot, int64_t& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int64_t x = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int64_t y = __shfl_up(x, d, 64);
+    if (lane >= d) x += y;
+  }
+  if (lane == 63) wave_tot[wave] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int64_t run = 0;
+    for (int w = 0; w < kOneBlock / 64; ++w) {
+      const int64_t t = wave_tot[w];
+      wave_tot[w] = run;
+      run += t;
+    }
+    wave_tot[kOneBlock / 64] = run;
+  }
+  __syncthreads();
+  total = wave_tot[kOneBlock / 64];
+  return wave_tot[wave] + x - v;
+}
+
+// seg = exclusive scan of counts (count entries; seg[count] = total).  If
+// stats is not NULL, stats[1 + o] = seg[(o+1) T] - seg[o T] (pairs per
+// offset) for o < K.  One workgroup of kOneBlock threads: each wavefront
+// scans a contiguous range in coalesced 64-element chunks (16 chunks loaded
+// per round), twice: once for its total, once to write the prefix.
+__global__ __launch_bounds__(kOneBlock) void k_scan_one_block(const int64_t* counts,  // may alias seg
+                                                              int64_t* seg, int64_t count,
+                                                              int64_t n_tiles, int K,
+                                                              unsigned long long* __restrict__ stats) {
+  constexpr int U = 16;
+  constexpr int NW = kOneBlock / 64;
+  __shared__ int64_t wave_base[NW + 1];
+  extern __shared__ int64_t bound[];  // K + 1 entries: seg[o T]
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t per = (count + NW - 1) / NW;
+  const int64_t lo = min<int64_t>((int64_t)wave * per, count), hi = min<int64_t>(lo + per, count);
+  // pass 1: the wave's total
+  int64_t part = 0;
+  for (int64_t i0 = lo; i0 < hi; i0 += 64 * U) {
+    int64_t v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t i = i0 + 64 * u + lane;
+      v[u] = i < hi ? counts[i] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) part += v[u];
+  }
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) part += __shfl_xor(part, d, 64);
+  if (lane == 0) wave_base[wave] = part;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int64_t run = 0;
+    for (int w = 0; w < NW; ++w) {
+      const int64_t t = wave_base[w];
+      wave_base[w] = run;
+      run += t;
+    }
+    wave_base[NW] = run;
+  }
+  __syncthreads();
+  // pass 2: prefix within 64-element chunks plus a running carry
+  int64_t carry = wave_base[wave];
+  for (int64_t i0 = lo; i0 < hi; i0 += 64 * U) {
+    int64_t v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t i = i0 + 64 * u + lane;
+      v[u] = i < hi ? counts[i] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      int64_t x = v[u];
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {
+        const int64_t y = __shfl_up(x, d, 64);
+        if (lane >= d) x += y;
+      }
+      const int64_t i = i0 + 64 * u + lane;
+      const int64_t ex = carry + x - v[u];
+      if (i < hi) {
+        seg[i] = ex;
+        if (stats && i % n_tiles == 0) bound[i / n_tiles] = ex;
+      }
+      carry += __shfl(x, 63, 64);
+    }
+  }
+  if (threadIdx.x == 0) {
+    seg[count] = wave_base[NW];
+    if (stats) bound[K] = wave_base[NW];
+  }
+  __syncthreads();
+  if (stats)
+    for (int o = threadIdx.x; o < K; o += blockDim.x) stats[1 + o] = (unsigned long long)(bound[o + 1] - bound[o]);
+}
+
+// The tile order (see build_tile_order) in one workgroup: keys from the
+// chunk counts (kept in LDS), then a counting sort in LDS.
+constexpr int64_t kOneBlockOrderMax = 1 << 15;    // tiles (16-bit keys in LDS)
+__global__ __launch_bounds__(kOneBlock) void k_tile_order_one_block(const int64_t* __restrict__ seg,
+                                                                    int64_t n_tiles, int K, int max_key,
+                                                                    int32_t* __restrict__ order) {
+  extern __shared__ int32_t hist[];  // bins = kTileGroups (max_key + 1), then n_tiles 16-bit keys
+  __shared__ int64_t wave_tot[kOneBlock / 64 + 1];
+  const int bins = kTileGroups * (max_key + 1);
+  uint16_t* keys = reinterpret_cast<uint16_t*>(hist + bins);
+  for (int i = threadIdx.x; i < bins; i += blockDim.x) hist[i] = 0;
+  __syncthreads();
+  for (int64_t t = threadIdx.x; t < n_tiles; t += blockDim.x) {
+    int chunks = 0;
+#pragma unroll 9
+    for (int o = 0; o < K; ++o) {
+      const int64_t n = seg[(int64_t)o * n_tiles + t + 1] - seg[(int64_t)o * n_tiles + t];
+      chunks += (int)((n + 15) >> 4);
+    }
+    const int grp = (int)(t * kTileGroups / n_tiles);
+    const int key = grp * (max_key + 1) + max_key - min(chunks, max_key);  // larger work -> smaller key
+    keys[t] = (uint16_t)key;
+    atomicAdd(&hist[key], 1);
+  }
+  __syncthreads();
+  // exclusive scan of the bins: each thread a contiguous run
+  const int per = (bins + kOneBlock - 1) / kOneBlock;
+  const int lo = min((int)threadIdx.x * per, bins), hi = min(lo + per, bins);
+  int64_t sum = 0;
+  for (int i = lo; i < hi; ++i) sum += hist[i];
+  int64_t total;
+  int64_t run = block_exclusive_scan(sum, wave_tot, total);
+  for (int i = lo; i < hi; ++i) {
+    const int c = hist[i];
+    hist[i] = (int)run;
+    run += c;
+  }
+  __syncthreads();
+  for (int64_t t = threadIdx.x; t < n_tiles; t += blockDim.x) order[atomicAdd(&hist[keys[t]], 1)] = (int32_t)t;
+}
+
 // ----------------------------------------------------------------- SC build
 struct ScGeom {
   int f, s, K;
@@ -499,7 +649,15 @@ static sscn_status compact_storage(const int32_t* nbr, int64_t n_rows, int K, St
     k_count_nbr<<<grid_for(st.n_tiles * 64, 256), 256, 0, s>>>(nbr, n_rows, K, st.seg, st.n_tiles);
     SSCN_HIP(hipGetLastError());
   }
-  if (!counted) SSCN_TRY(exclusive_scan_i64(st.seg, st.seg, K * st.n_tiles, s));
+  if (!counted) {
+    if (K * st.n_tiles <= kOneBlockScanMax) {
+      k_scan_one_block<<<1, kOneBlock, sizeof(int64_t), s>>>(st.seg, st.seg, K * st.n_tiles, std::max<int64_t>(st.n_tiles, 1),
+                                                              K, nullptr);
+      SSCN_HIP(hipGetLastError());
+    } else {
+      SSCN_TRY(exclusive_scan_i64(st.seg, st.seg, K * st.n_tiles, s));
+    }
+  }
   if (st.n_tiles > 0) {
     k_compact<<<grid_for(st.n_tiles * 64, 256), 256, 0, s>>>(nbr, n_rows, K, st.seg, st.n_tiles, st.in_rows,
                                                              st.out_rows);
@@ -513,6 +671,12 @@ static sscn_status build_tile_order(Storage& st, int K, hipStream_t s) {
   if (st.n_tiles == 0) return SSCN_OK;
   const int max_key = K * (kTile / 16 + 1);
   const int bins = kTileGroups * (max_key + 1);
+  const size_t lds = sizeof(int32_t) * bins + sizeof(uint16_t) * st.n_tiles;
+  if (st.n_tiles <= kOneBlockOrderMax && bins <= 65536 && lds <= 128 * 1024) {
+    k_tile_order_one_block<<<1, kOneBlock, lds, s>>>(st.seg, st.n_tiles, K, max_key, st.order);
+    SSCN_HIP(hipGetLastError());
+    return SSCN_OK;
+  }
   Temps tmp(s);
   int32_t* key; int32_t* hist;
   Arena a;
@@ -660,10 +824,16 @@ extern "C" sscn_status ssc_rulebook_build(const int32_t* coords, int64_t n, cons
           (const int4*)coords, n, L0, L1, L2, f, table, cap - 1, nbr, counts, n_tiles);
       SSCN_HIP(hipGetLastError());
     }
-    SSCN_TRY(exclusive_scan_i64(counts, d->fwd.seg, K * n_tiles, s));
-    if (n > 0) {
-      k_offset_totals<<<grid_for(K, 256), 256, 0, s>>>(d->fwd.seg, n_tiles, K, stats);
+    if (K * n_tiles <= kOneBlockScanMax) {
+      k_scan_one_block<<<1, kOneBlock, sizeof(int64_t) * (K + 1), s>>>(counts, d->fwd.seg, K * n_tiles, n_tiles, K,
+                                                                      n > 0 ? stats : nullptr);
       SSCN_HIP(hipGetLastError());
+    } else {
+      SSCN_TRY(exclusive_scan_i64(counts, d->fwd.seg, K * n_tiles, s));
+      if (n > 0) {
+        k_offset_totals<<<grid_for(K, 256), 256, 0, s>>>(d->fwd.seg, n_tiles, K, stats);
+        SSCN_HIP(hipGetLastError());
+      }
     }
     // Pair storage for the worst case (every offset of every site) when that
     // is modest: then compaction and the tile order are queued before the

@@ -3,6 +3,8 @@
 #include <cstdio>
 #include <mutex>
 
+#include <map>
+#include <tuple>
 #include "internal.h"
 
 namespace sscn {
@@ -54,6 +56,41 @@ sscn_status dev_alloc(void** p, size_t bytes, hipStream_t s) {
 
 void dev_free(void* p, hipStream_t s) {
   if (p) (void)hipFreeAsync(p, s);
+}
+
+void occupancy(const void* kern, int block, size_t lds, int* per_cu, int* cus) {
+  struct Key {
+    int dev;
+    const void* kern;
+    int block;
+    size_t lds;
+    bool operator<(const Key& o) const {
+      return std::tie(dev, kern, block, lds) < std::tie(o.dev, o.kern, o.block, o.lds);
+    }
+  };
+  static std::mutex mu;
+  static std::map<Key, std::pair<int, int>> cache;
+  int dev = 0;
+  (void)hipGetDevice(&dev);
+  const Key k{dev, kern, block, lds};
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    auto it = cache.find(k);
+    if (it != cache.end()) {
+      *per_cu = it->second.first;
+      *cus = it->second.second;
+      return;
+    }
+  }
+  int n_cu = 256, n = 1;
+  (void)hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kern, block, lds) != hipSuccess || n < 1) n = 1;
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    cache[k] = {n, n_cu};
+  }
+  *per_cu = n;
+  *cus = n_cu;
 }
 
 RulebookData::~RulebookData() {
