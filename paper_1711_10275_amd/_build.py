@@ -25,10 +25,14 @@ HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
-    # no packed fp32 instructions (some of their forms are unreliable here)
+    # packed fp32 instructions are kept out of all device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     # fp32 atomic adds in wgrad map to the hardware instruction
     "-munsafe-fp-atomics",
+    # MFMA results go straight to VGPRs: no accumulator-register reads in the
+    # inner loops (VALU work beyond ~2 instructions per fp32 MFMA is not
+    # hidden behind the matrix unit)
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-Wall", "-Wno-unused-function",
     "-I", INCLUDE, "-I", CSRC,
 ]

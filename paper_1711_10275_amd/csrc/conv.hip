@@ -219,11 +219,13 @@ struct QuadLds {
 // Main forward / dgrad kernel: c_in % 8 == 0, c_in <= 64 KB, any c_out
 // (64 columns per workgroup row of the grid).
 //
-// Workgroup = 4 wavefronts over one 64-row output tile and 64 output
-// columns.  Wavefront w takes input-channel half kh = w & 1 of every
-// 64-channel block and output-column half ch = w >> 1: per chunk of 16
-// pairs it multiplies the pairs' gathered channels by a (32 KB) x 32 weight
-// block.  At the start of a tile the workgroup lists its chunks
+// Workgroup = 8 / NB wavefronts over one 64-row output tile and 64 output
+// columns (NB = column blocks of 16 per wavefront; the library uses NB = 2,
+// 4 wavefronts: with NB = 4 a workgroup has half the wavefronts for the same
+// LDS, which halves occupancy).  Wavefront w takes input-channel half
+// kh = w & 1 of every 64-channel block and, for NB = 2, output-column half
+// ch = w >> 1: per chunk of 16 pairs it multiplies the pairs' gathered
+// channels by a (32 KB) x 16 NB weight block.  At the start of a tile the workgroup lists its chunks
 // (offset-major) and stores, per pair slot, the byte offset of the gathered
 // row and the LDS offset of the output row, so the main loop does almost
 // no address arithmetic.  Loads are raw buffer loads: a lane's offset
@@ -243,7 +245,7 @@ struct QuadLds {
 // of contiguous tiles per XCD, as workgroups are dispatched round-robin over
 // the XCDs), and the group's tiles, listed by decreasing work, are dealt to
 // its workgroups in boustrophedon order (0..G-1, G-1..0, ...).
-template <typename T, int RING, int KB, bool WT>
+template <typename T, int RING, int KB, bool WT, int NB>
 __global__ __launch_bounds__(256) void k_conv_quad(
     const T* __restrict__ X, uint32_t x_bytes, const T* __restrict__ W, uint32_t w_bytes,
     const int64_t* __restrict__ seg, const int32_t* __restrict__ in_rows, const int32_t* __restrict__ out_rows,
@@ -264,19 +266,22 @@ __global__ __launch_bounds__(256) void k_conv_quad(
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int m = lane & 15, g = lane >> 4;
-  const int kh = wave & 1, chf = wave >> 1;
+  constexpr int NWB = 8 / NB;             // wavefronts per workgroup
+  constexpr int NT = 64 * NWB;             // threads per workgroup
+  static_assert(NB == 2 || NB == 4, "2 or 4 column blocks per wavefront");
+  const int kh = wave & 1, chf = NB == 2 ? wave >> 1 : 0;
   const int col_base = blockIdx.y * 64;
   const uint32_t row_bytes = (uint32_t)cin * (uint32_t)sizeof(T);
   // lane constants: channel octets of the gathered row, weight columns
-  uint32_t a_lane[KB], b_lane[KB][2];
+  uint32_t a_lane[KB], b_lane[KB][NB];
 #pragma unroll
   for (int kb = 0; kb < KB; ++kb) {
     const int k0 = kb * 64 + kh * 32 + 8 * g;
     const bool k_in = k0 + 8 <= cin;
     a_lane[kb] = k_in ? (uint32_t)k0 * sizeof(T) : kOobOffset;
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-      const int col = col_base + chf * 32 + nb * 16 + m;
+    for (int nb = 0; nb < NB; ++nb) {
+      const int col = col_base + chf * 16 * NB + nb * 16 + m;
       const uint32_t e = WT ? (uint32_t)col * cin + k0 : (uint32_t)k0 * cout + col;  // element of W[o]
       b_lane[kb][nb] = (col < cout && k_in) ? e * (uint32_t)sizeof(T) : kOobOffset;
     }
@@ -284,7 +289,7 @@ __global__ __launch_bounds__(256) void k_conv_quad(
   const uint32_t w_stride = (uint32_t)cout * cin * sizeof(T);  // bytes per filter offset
   const uint32_t k_step = (uint32_t)cout * sizeof(T);           // bytes between channels (WT = false)
   const rsrc_t rx = make_rsrc(X, x_bytes), rb = make_rsrc(W, w_bytes);
-  char* acc_lane = reinterpret_cast<char*>(acc_all + kh * ACC + chf * 32 + m);
+  char* acc_lane = reinterpret_cast<char*>(acc_all + kh * ACC + chf * 16 * NB + m);
 
   const int64_t grp = blockIdx.x % kTileGroups;
   const int64_t G = gridDim.x / kTileGroups, b = blockIdx.x / kTileGroups;
@@ -333,12 +338,12 @@ __global__ __launch_bounds__(256) void k_conv_quad(
     // empty).  Each thread issues all of its index loads before writing.
     {
       constexpr int PER = 8;
-      for (int q0 = 0; q0 < n_chunks * 16; q0 += 256 * PER) {
+      for (int q0 = 0; q0 < n_chunks * 16; q0 += NT * PER) {
         int32_t vi[PER], vo[PER];
         bool ok[PER];
 #pragma unroll
         for (int u = 0; u < PER; ++u) {
-          const int q = q0 + u * 256 + threadIdx.x;
+          const int q = q0 + u * NT + threadIdx.x;
           const bool live = q < n_chunks * 16;
           const int o = chof[live ? q >> 4 : 0];
           const int j = q - seg_c0[o] * 16;
@@ -349,7 +354,7 @@ __global__ __launch_bounds__(256) void k_conv_quad(
         }
 #pragma unroll
         for (int u = 0; u < PER; ++u) {
-          const int q = q0 + u * 256 + threadIdx.x;
+          const int q = q0 + u * NT + threadIdx.x;
           if (q < n_chunks * 16) {
             prow[q] = ok[u] ? (uint32_t)vi[u] * row_bytes : kOobOffset;
             pacc[q] = (uint16_t)(((ok[u] ? (int)(vo[u] - row0) : kTile) * LDW) * 4);
@@ -360,7 +365,7 @@ __global__ __launch_bounds__(256) void k_conv_quad(
     __syncthreads();
 
     if (n_chunks > 0) {
-      Oct<T> a_ring[RING][KB], b_ring[RING][KB][2], b_cur[KB][2];
+      Oct<T> a_ring[RING][KB], b_ring[RING][KB][NB], b_cur[KB][NB];
       // weights are requested only for the first chunk of each offset
       auto fresh_at = [&](int c) -> bool {
         const int cc = c < n_chunks ? c : n_chunks - 1;
@@ -378,7 +383,7 @@ __global__ __launch_bounds__(256) void k_conv_quad(
 #pragma unroll
           for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-            for (int nb = 0; nb < 2; ++nb) {
+            for (int nb = 0; nb < NB; ++nb) {
               if constexpr (WT)
                 b_ring[slot][kb][nb].load(rb, b_lane[kb][nb], soff);
               else
@@ -388,33 +393,50 @@ __global__ __launch_bounds__(256) void k_conv_quad(
       };
 #pragma unroll
       for (int q = 0; q < RING - 1; ++q) request(q, q);
-      auto step = [&](int c, int slot) {
-        request(c + RING - 1, (slot + RING - 1) % RING);
-        if (fresh_at(c)) {
+      // lane holds D[4g + r][m]: pair 4g + r, column chf*32 + nb*16 + m.  One
+      // writer per element: plain read-modify-write; empty slots hit the dummy
+      // row.  A chunk's sum is added one step later, after the next chunk's
+      // MFMAs are issued, so the LDS round trip overlaps matrix work.
+      constexpr uint32_t kDummy = (uint32_t)(kTile * LDW * 4);
+      f32x4 dp[NB];
 #pragma unroll
-          for (int kb = 0; kb < KB; ++kb) {
-            b_cur[kb][0] = b_ring[slot][kb][0];
-            b_cur[kb][1] = b_ring[slot][kb][1];
-          }
-        }
-        f32x4 d[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+      for (int nb = 0; nb < NB; ++nb) dp[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      uint2 rows_prev = make_uint2(kDummy | (kDummy << 16), kDummy | (kDummy << 16));
+      auto add_prev = [&]() {
+        const uint32_t ra[4] = {rows_prev.x & 0xffffu, rows_prev.x >> 16, rows_prev.y & 0xffffu,
+                                rows_prev.y >> 16};
+        float old[NB][4];
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-          for (int nb = 0; nb < 2; ++nb) d[nb] = mma_oct(a_ring[slot][kb], b_cur[kb][nb], d[nb]);
-        // lane holds D[4g + r][m]: pair 4g + r, column chf*32 + nb*16 + m.  One
-        // writer per element: plain read-modify-write; empty slots hit the dummy row.
-        const uint2 rows = *reinterpret_cast<const uint2*>(&pacc[c * 16 + 4 * g]);
-        const uint32_t ra[4] = {rows.x & 0xffffu, rows.x >> 16, rows.y & 0xffffu, rows.y >> 16};
-        float old[2][4];
-#pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
+        for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
           for (int r = 0; r < 4; ++r) old[nb][r] = *reinterpret_cast<const float*>(acc_lane + ra[r] + nb * 64);
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
+        for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) *reinterpret_cast<float*>(acc_lane + ra[r] + nb * 64) = old[nb][r] + d[nb][r];
+          for (int r = 0; r < 4; ++r) *reinterpret_cast<float*>(acc_lane + ra[r] + nb * 64) = old[nb][r] + dp[nb][r];
+      };
+      auto step = [&](int c, int slot) {
+        request(c + RING - 1, (slot + RING - 1) % RING);
+        if (fresh_at(c)) {
+          // a real (uniform) branch: the copy runs only when the offset
+          // changes, instead of a select per register on every chunk
+          asm volatile("");
+#pragma unroll
+          for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) b_cur[kb][nb] = b_ring[slot][kb][nb];
+        }
+        f32x4 d[NB];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) d[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) d[nb] = mma_oct(a_ring[slot][kb], b_cur[kb][nb], d[nb]);
+        add_prev();
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) dp[nb] = d[nb];
+        rows_prev = *reinterpret_cast<const uint2*>(&pacc[c * 16 + 4 * g]);
       };
       int c = 0;
       for (; c + RING <= n_chunks; c += RING) {
@@ -424,6 +446,7 @@ __global__ __launch_bounds__(256) void k_conv_quad(
 #pragma unroll
       for (int q = 0; q < RING - 1; ++q)
         if (c + q < n_chunks) step(c + q, q);
+      add_prev();
     }
     __syncthreads();
     for (int i = threadIdx.x; i < kTile * 64; i += blockDim.x) {
@@ -850,23 +873,24 @@ __global__ __launch_bounds__(256) void k_conv_col(
 // ---------------------------------------------------------------- launchers
 // Workgroups that fit on the device at once, capped by the work and rounded
 // up to a multiple of kTileGroups (every tile group gets workgroups).
-static unsigned persistent_grid(const void* kern, size_t lds, int64_t n_items) {
+static unsigned persistent_grid(const void* kern, size_t lds, int64_t n_items, int block = 256) {
   int cus = 256, per_cu = 1;
-  occupancy(kern, 256, lds, &per_cu, &cus);
+  occupancy(kern, block, lds, &per_cu, &cus);
   int64_t g = std::min<int64_t>((int64_t)cus * per_cu, std::max<int64_t>(n_items, 1));
   g = ceil_div(g, kTileGroups) * kTileGroups;
   return (unsigned)g;
 }
 
-template <typename T, int RING, int KB, bool WT>
+template <typename T, int RING, int KB, bool WT, int NB = 2>
 static sscn_status launch_quad(const T* X, uint32_t x_bytes, const T* W, uint32_t w_bytes, const View& v, int cin,
                                int cout, T* Y, hipStream_t s) {
   const int max_chunks = v.K * (kTile / 16 + 1);
   const QuadLds L(max_chunks, v.K);
   const int groups = (cout + 63) / 64;
-  auto kern = k_conv_quad<T, RING, KB, WT>;
-  const unsigned g = persistent_grid((const void*)kern, L.total, v.st->n_tiles);
-  kern<<<dim3(g, (unsigned)groups), 256, L.total, s>>>(X, x_bytes, W, w_bytes, v.st->seg, v.st->in_rows,
+  constexpr int NT = 64 * (8 / NB);
+  auto kern = k_conv_quad<T, RING, KB, WT, NB>;
+  const unsigned g = persistent_grid((const void*)kern, L.total, v.st->n_tiles, NT);
+  kern<<<dim3(g, (unsigned)groups), NT, L.total, s>>>(X, x_bytes, W, w_bytes, v.st->seg, v.st->in_rows,
                                                        v.st->out_rows, v.st->order, v.st->n_tiles, v.K,
                                                        v.mirror ? 1 : 0, cin, cout, v.n_out, max_chunks, Y);
   SSCN_HIP(hipGetLastError());
