@@ -166,11 +166,12 @@ def unet_scenes(stream, reps):
     fresh_ms = _wall_ms(lambda: unet.forward(X, unet.Geometry(tc, (256, 256, 256)), params), reps)
     geom = unet.Geometry(tc, (256, 256, 256))
     fwd_ms = _event_ms(lambda: unet.forward(X, geom, params), reps, stream)
+    unfused_ms = _event_ms(lambda: unet.forward(X, geom, params, fused=False), reps, stream)
     fl = unet.flops(geom)
     return {"workload": "unet5_grid256_batch8_scenes_c32to160_bf16", "level_sites": [int(x.shape[0]) for x in geom.coords],
             "geometry_build_ms": geom_ms, "forward_ms": fwd_ms, "forward_sites_per_s": c.shape[0] / (fwd_ms * 1e-3),
             "forward_effective_tflops": fl / (fwd_ms * 1e-3) / 1e12, "flops": fl,
-            "geometry_plus_forward_ms": fresh_ms,
+            "forward_unfused_ms": unfused_ms, "geometry_plus_forward_ms": fresh_ms,
             "geometry_plus_forward_sites_per_s": c.shape[0] / (fresh_ms * 1e-3)}
 
 

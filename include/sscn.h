@@ -151,6 +151,36 @@ sscn_status sparse_conv_forward(const void* features, const void* weights, sscn_
                                 hipStream_t stream);
 
 /*
+ * One destination of sparse_conv_forward_heads.  The layer output y (n_out x
+ * c_out) is written as max(0, y[k][c] * scale[c] + shift[c]) -- the
+ * inference-form batch normalisation and ReLU that pre-activate the next
+ * unit of a network (Sec. 5) -- or as y itself when scale is NULL, rounded
+ * once to the layer's dtype.
+ *   data        device, row k at data + k * row_stride (elements of dtype),
+ *               c_out consecutive elements per row
+ *   row_stride  >= c_out; a wider stride writes into the columns of a
+ *               concatenation buffer
+ *   scale/shift device fp32, c_out entries each; both NULL or both set
+ */
+typedef struct {
+  void* data;
+  int64_t row_stride;
+  const float* scale;
+  const float* shift;
+} sscn_conv_output;
+
+/*
+ * sparse_conv_forward_heads -- sparse_conv_forward writing the result to
+ * n_heads (1 or 2) destinations (host array `heads`), each with its own
+ * optional activation.  Destinations must not overlap each other or the
+ * inputs.  SSCN_ERR_INVALID_ARG for a bad head (NULL data, stride < c_out,
+ * only one of scale / shift).  Asynchronous on `stream`.
+ */
+sscn_status sparse_conv_forward_heads(const void* features, const void* weights, sscn_rulebook rb,
+                                      int32_t c_in, int32_t c_out, sscn_dtype dtype, int32_t n_heads,
+                                      const sscn_conv_output* heads, hipStream_t stream);
+
+/*
  * sparse_conv_backward -- gradients of sparse_conv_forward (its adjoint):
  *   dgrad[j] = sum_o sum_{(j,k) in R_o} dout[k] * (W^o)^T   (n_in x c_in)
  *   wgrad[o] = sum_{(j,k) in R_o} features[j]^T dout[k]    (K x c_in x c_out, fp32)

@@ -46,6 +46,35 @@ template <> struct Elem<bf16_t> {
   static __device__ __forceinline__ void store(bf16_t* p, float v) { p->bits = f32_to_bf16(v); }
 };
 
+// Destinations of a layer's output: up to two, each with its own row stride
+// and an optional per-column affine map followed by ReLU (the next unit's
+// pre-activation), rounded once to T.
+template <typename T>
+struct Heads {
+  T* out[2];
+  int64_t ld[2];
+  const float* scale[2];
+  const float* shift[2];
+  int n;
+  __device__ __forceinline__ void store(int64_t row, int col, float v) const {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      if (h < n) {
+        const float a = scale[h] ? fmaxf(0.f, v * scale[h][col] + shift[h][col]) : v;
+        Elem<T>::store(out[h] + row * ld[h] + col, a);
+      }
+    }
+  }
+};
+template <typename T>
+static Heads<T> plain_heads(T* Y, int cout) {
+  Heads<T> h{};
+  h.out[0] = Y;
+  h.ld[0] = cout;
+  h.n = 1;
+  return h;
+}
+
 // ------------------------------------------------------- generic fallback
 // 16 consecutive values of a row (zero beyond kmax) as MFMA operands.
 __device__ __forceinline__ void load16(const float* __restrict__ row, int k0, int kmax, float (&v)[16]) {
@@ -93,7 +122,7 @@ template <typename T, int NW>
 __global__ __launch_bounds__(NW * 64) void k_gather_mma(
     const T* __restrict__ X, const T* __restrict__ Bt, const int64_t* __restrict__ seg,
     const int32_t* __restrict__ in_rows, const int32_t* __restrict__ out_rows, int64_t n_tiles, int K,
-    int mirror, int cin, int cout, int64_t n_out, int tpw, T* __restrict__ Y) {
+    int mirror, int cin, int cout, int64_t n_out, int tpw, Heads<T> Y) {
   extern __shared__ float acc[];
   constexpr int WCOLS = 16 * NW;
   constexpr int LDW = WCOLS + 1;
@@ -141,7 +170,7 @@ __global__ __launch_bounds__(NW * 64) void k_gather_mma(
     const int r = i / WCOLS, c = i % WCOLS;
     const int64_t row = row0 + r;
     const int cc = col_base + c;
-    if (row < n_out && cc < cout) Elem<T>::store(Y + row * cout + cc, acc[r * LDW + c]);
+    if (row < n_out && cc < cout) Y.store(row, cc, acc[r * LDW + c]);
   }
 }
 
@@ -250,7 +279,7 @@ __global__ __launch_bounds__(256) void k_conv_quad(
     const T* __restrict__ X, uint32_t x_bytes, const T* __restrict__ W, uint32_t w_bytes,
     const int64_t* __restrict__ seg, const int32_t* __restrict__ in_rows, const int32_t* __restrict__ out_rows,
     const int32_t* __restrict__ order, int64_t n_tiles, int K, int mirror, int cin, int cout, int64_t n_out,
-    int max_chunks, T* __restrict__ Y) {
+    int max_chunks, Heads<T> Y) {
   constexpr int LDW = 64 + 1;
   constexpr int ACC = (kTile + 1) * LDW;  // 64 rows + one dummy row for masked lanes
   extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -454,7 +483,7 @@ __global__ __launch_bounds__(256) void k_conv_quad(
       const int64_t row = row0 + r;
       const int col = col_base + cc;
       if (row < n_out && col < cout)
-        Elem<T>::store(Y + row * cout + col, acc_all[r * LDW + cc] + acc_all[ACC + r * LDW + cc]);
+        Y.store(row, col, acc_all[r * LDW + cc] + acc_all[ACC + r * LDW + cc]);
     }
   }
 }
@@ -709,7 +738,7 @@ __global__ __launch_bounds__(256) void k_conv_col(
     const T* __restrict__ X, uint32_t x_bytes, const T* __restrict__ Wt, uint32_t w_bytes,
     const int32_t* __restrict__ ctile, const int32_t* __restrict__ c_in, const uint32_t* __restrict__ c_out,
     const int32_t* __restrict__ c_off, int n_ct, int K, int mirror, int cin, int cout, int n_out,
-    T* __restrict__ Y) {
+    Heads<T> Y) {
   constexpr int IR = 2 * RING;                 // chunk-record ring
   constexpr int TR = kChunkRows;
   constexpr int EPB = 16 / sizeof(T);          // elements per b128 load
@@ -856,7 +885,7 @@ __global__ __launch_bounds__(256) void k_conv_col(
           const float v = *q;
           *q = 0.f;
           const int64_t row = row0 + r;
-          if (row < n_out && col < cout) Elem<T>::store(Y + row * cout + col, v);
+          if (row < n_out && col < cout) Y.store(row, col, v);
         }
         __builtin_amdgcn_s_waitcnt(0);
       }
@@ -883,7 +912,7 @@ static unsigned persistent_grid(const void* kern, size_t lds, int64_t n_items, i
 
 template <typename T, int RING, int KB, bool WT, int NB = 2>
 static sscn_status launch_quad(const T* X, uint32_t x_bytes, const T* W, uint32_t w_bytes, const View& v, int cin,
-                               int cout, T* Y, hipStream_t s) {
+                               int cout, const Heads<T>& Y, hipStream_t s) {
   const int max_chunks = v.K * (kTile / 16 + 1);
   const QuadLds L(max_chunks, v.K);
   const int groups = (cout + 63) / 64;
@@ -898,7 +927,7 @@ static sscn_status launch_quad(const T* X, uint32_t x_bytes, const T* W, uint32_
 }
 
 template <typename T, int NW>
-static sscn_status launch_generic_nw(const T* X, const T* Bt, const View& v, int cin, int cout, int grid_y, T* Y,
+static sscn_status launch_generic_nw(const T* X, const T* Bt, const View& v, int cin, int cout, int grid_y, const Heads<T>& Y,
                                      hipStream_t s) {
   // accumulator tile (tpw * 64 rows x (16 NW + 1) fp32) within 64 KiB of LDS
   const int tpw = NW >= 8 ? 1 : 2;
@@ -912,7 +941,7 @@ static sscn_status launch_generic_nw(const T* X, const T* Bt, const View& v, int
 }
 
 template <typename T>
-static sscn_status launch_generic(const T* X, const T* Bt, const View& v, int cin, int cout, T* Y, hipStream_t s) {
+static sscn_status launch_generic(const T* X, const T* Bt, const View& v, int cin, int cout, const Heads<T>& Y, hipStream_t s) {
   const int ncb = (cout + 15) / 16;
   const int grid_y = (ncb + 7) / 8;
   const int nw = (ncb + grid_y - 1) / grid_y;
@@ -938,7 +967,7 @@ static sscn_status launch_generic(const T* X, const T* Bt, const View& v, int ci
 // (without launching) when the shape is outside what the kernel covers.
 template <typename T, int KB, int RING>
 static sscn_status launch_col_kb(const T* X, uint32_t xb, const T* Bt, uint32_t wb, const View& v, int cin,
-                                 int cout, T* Y, hipStream_t s) {
+                                 int cout, const Heads<T>& Y, hipStream_t s) {
   const Storage& st = *v.st;
   const int ng = (cout + 15) / 16;
   int ncol = std::min(ng, 4);
@@ -984,7 +1013,7 @@ static bool col_eligible(const View& v, int cin, int cout) {
 }
 
 template <typename T>
-static sscn_status launch_col(const T* X, const T* Bt, const View& v, int cin, int cout, T* Y, hipStream_t s) {
+static sscn_status launch_col(const T* X, const T* Bt, const View& v, int cin, int cout, const Heads<T>& Y, hipStream_t s) {
   if (v.n_out == 0) return SSCN_OK;
   SSCN_TRY(ensure_chunks(v, s));
   const uint32_t xb = (uint32_t)((uint64_t)std::max<int64_t>(v.n_in, 1) * cin * sizeof(T));
@@ -1011,7 +1040,7 @@ static bool quad_eligible(const View& v, int cin, int cout) {
 }
 
 template <typename T, bool WT>
-static sscn_status launch_conv(const T* X, const T* W, const View& v, int cin, int cout, T* Y, hipStream_t s) {
+static sscn_status launch_conv(const T* X, const T* W, const View& v, int cin, int cout, const Heads<T>& Y, hipStream_t s) {
   if (v.st->n_tiles == 0) return SSCN_OK;
   if (WT && prefer_col<T>(v, cin, cout)) return launch_col<T>(X, W, v, cin, cout, Y, s);
   const uint64_t x_bytes = (uint64_t)std::max<int64_t>(v.n_in, 1) * cin * sizeof(T);
@@ -1299,7 +1328,7 @@ static sscn_status check_conv_args(sscn_rulebook rb, int32_t c_in, int32_t c_out
 // contiguous weight loads, which is faster than gathering the stored layout;
 // bf16 reads the stored layout directly.
 template <typename T>
-static sscn_status forward_t(const T* X, const T* W, const View& v, int cin, int cout, T* Y, hipStream_t s) {
+static sscn_status forward_t(const T* X, const T* W, const View& v, int cin, int cout, const Heads<T>& Y, hipStream_t s) {
   if (prefer_col<T>(v, cin, cout)) {
     if (v.n_out == 0) return SSCN_OK;
     const int64_t total = (int64_t)v.K * cin * cout;
@@ -1340,9 +1369,46 @@ extern "C" sscn_status sparse_conv_forward(const void* features, const void* wei
   if (!out || !weights || (v.n_in > 0 && !features))
     return fail(SSCN_ERR_INVALID_ARG, "NULL features, weights or out");
   if (dtype == SSCN_F32)
-    return forward_t<float>((const float*)features, (const float*)weights, v, c_in, c_out, (float*)out, stream);
-  return forward_t<bf16_t>((const bf16_t*)features, (const bf16_t*)weights, v, c_in, c_out, (bf16_t*)out,
+    return forward_t<float>((const float*)features, (const float*)weights, v, c_in, c_out,
+                            plain_heads((float*)out, c_out), stream);
+  return forward_t<bf16_t>((const bf16_t*)features, (const bf16_t*)weights, v, c_in, c_out,
+                           plain_heads((bf16_t*)out, c_out),
                            stream);
+}
+
+template <typename T>
+static Heads<T> heads_of(int n, const sscn_conv_output* h) {
+  Heads<T> r{};
+  r.n = n;
+  for (int i = 0; i < n; ++i) {
+    r.out[i] = (T*)h[i].data;
+    r.ld[i] = h[i].row_stride;
+    r.scale[i] = h[i].scale;
+    r.shift[i] = h[i].shift;
+  }
+  return r;
+}
+
+extern "C" sscn_status sparse_conv_forward_heads(const void* features, const void* weights, sscn_rulebook rb,
+                                                 int32_t c_in, int32_t c_out, sscn_dtype dtype, int32_t n_heads,
+                                                 const sscn_conv_output* heads, hipStream_t stream) {
+  sscn_status st = check_conv_args(rb, c_in, c_out, dtype);
+  if (st != SSCN_OK) return st;
+  if (n_heads < 1 || n_heads > 2 || !heads) return fail(SSCN_ERR_INVALID_ARG, "1 or 2 output heads");
+  for (int i = 0; i < n_heads; ++i) {
+    if (!heads[i].data || heads[i].row_stride < c_out)
+      return fail(SSCN_ERR_INVALID_ARG, "output head: NULL data or row stride < c_out");
+    if ((heads[i].scale == nullptr) != (heads[i].shift == nullptr))
+      return fail(SSCN_ERR_INVALID_ARG, "output head: scale and shift must both be set or both NULL");
+  }
+  const View v = view_of(rb);
+  if (v.n_out == 0) return SSCN_OK;
+  if (!weights || (v.n_in > 0 && !features)) return fail(SSCN_ERR_INVALID_ARG, "NULL features or weights");
+  if (dtype == SSCN_F32)
+    return forward_t<float>((const float*)features, (const float*)weights, v, c_in, c_out,
+                            heads_of<float>(n_heads, heads), stream);
+  return forward_t<bf16_t>((const bf16_t*)features, (const bf16_t*)weights, v, c_in, c_out,
+                           heads_of<bf16_t>(n_heads, heads), stream);
 }
 
 extern "C" sscn_status sparse_conv_backward(const void* features, const void* weights, const void* dout,
@@ -1357,11 +1423,12 @@ extern "C" sscn_status sparse_conv_backward(const void* features, const void* we
     // row ci of W[o] holds the c_out weights feeding input channel ci)
     const View vt = transposed_view(rb);
     if (dtype == SSCN_F32)
-      st = launch_conv<float, true>((const float*)dout, (const float*)weights, vt, c_out, c_in, (float*)dgrad,
+      st = launch_conv<float, true>((const float*)dout, (const float*)weights, vt, c_out, c_in,
+                                    plain_heads((float*)dgrad, c_in),
                                     stream);
     else
       st = launch_conv<bf16_t, true>((const bf16_t*)dout, (const bf16_t*)weights, vt, c_out, c_in,
-                                     (bf16_t*)dgrad, stream);
+                                     plain_heads((bf16_t*)dgrad, c_in), stream);
     if (st != SSCN_OK) return st;
   }
   if (wgrad) {

@@ -36,6 +36,12 @@ class RulebookInfo(ctypes.Structure):
                 ("out_size", ctypes.c_int32 * 3)]
 
 
+class ConvOutput(ctypes.Structure):
+    """sscn_conv_output: one destination of sparse_conv_forward_heads."""
+    _fields_ = [("data", ctypes.c_void_p), ("row_stride", ctypes.c_int64), ("scale", ctypes.c_void_p),
+                ("shift", ctypes.c_void_p)]
+
+
 _lib = None
 _vp, _i32, _i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
 _SIGS = {
@@ -47,6 +53,7 @@ _SIGS = {
     "sscn_rulebook_export": [_vp, _vp, _vp, _vp, _vp],
     "sscn_rulebook_free": [_vp],
     "sparse_conv_forward": [_vp, _vp, _vp, _i32, _i32, ctypes.c_int, _vp, _vp],
+    "sparse_conv_forward_heads": [_vp, _vp, _vp, _i32, _i32, ctypes.c_int, _i32, _vp, _vp],
     "sparse_conv_backward": [_vp, _vp, _vp, _vp, _i32, _i32, ctypes.c_int, _vp, _vp, _vp],
     "sscn_affine_relu": [_vp, _vp, _vp, _i64, _i32, ctypes.c_int, _vp, _vp],
     "sscn_concat_cols": [_vp, _i32, _vp, _i32, _i64, ctypes.c_int, _vp, _vp],
@@ -201,6 +208,47 @@ def sparse_conv_forward(features, weights, rulebook):
                                          _dtype_code(features), ctypes.c_void_p(out.data_ptr()),
                                          _stream(features)))
     return out
+
+
+def sparse_conv_forward_heads(features, weights, rulebook, heads):
+    """sparse_conv_forward written to 1 or 2 destinations.
+
+    heads: list of (out, scale, shift); out is a device tensor of shape
+    (n_out, c_out) in the features' dtype whose rows may be strided (a
+    column slice of a wider tensor, unit column stride); scale and shift are
+    fp32 (c_out,) device tensors, or None for the plain output.  Each
+    destination receives max(0, y * scale + shift), or y.
+    """
+    features = _dev_tensor(features, "features")
+    weights = _dev_tensor(weights, "weights", features.dtype)
+    K, cin, cout = weights.shape
+    if K != rulebook.n_offsets or features.shape != (rulebook.n_in, cin):
+        raise ValueError("features / weights do not match the rule book")
+    if not 1 <= len(heads) <= 2:
+        raise ValueError("1 or 2 output heads")
+    arr = (ConvOutput * len(heads))()
+    for i, (out, scale, shift) in enumerate(heads):
+        if out.dtype != features.dtype or out.device != features.device or tuple(out.shape) != (rulebook.n_out, cout):
+            raise ValueError(f"head {i}: expected a ({rulebook.n_out}, {cout}) {features.dtype} tensor")
+        if out.stride(1) != 1:
+            raise ValueError(f"head {i}: columns must be contiguous")
+        if (scale is None) != (shift is None):
+            raise ValueError(f"head {i}: scale and shift go together")
+        if scale is not None:
+            scale = _dev_tensor(scale, "scale", torch.float32)
+            shift = _dev_tensor(shift, "shift", torch.float32)
+            if scale.shape != (cout,) or shift.shape != (cout,):
+                raise ValueError(f"head {i}: scale / shift must have {cout} entries")
+        arr[i].data = out.data_ptr()
+        arr[i].row_stride = out.stride(0)
+        arr[i].scale = scale.data_ptr() if scale is not None else None
+        arr[i].shift = shift.data_ptr() if shift is not None else None
+    with torch.cuda.device(features.device):
+        _check(lib().sparse_conv_forward_heads(ctypes.c_void_p(features.data_ptr()),
+                                               ctypes.c_void_p(weights.data_ptr()), rulebook.handle, cin, cout,
+                                               _dtype_code(features), len(heads), ctypes.cast(arr, ctypes.c_void_p),
+                                               _stream(features)))
+    return [h[0] for h in heads]
 
 
 def sparse_conv_backward(features, weights, dout, rulebook, dgrad=True, wgrad=True):

@@ -93,15 +93,28 @@ class Geometry:
         return self.rulebook(unit).n_pairs
 
 
-def forward(x, geom, params, channels=CHANNELS, trace=None):
+def forward(x, geom, params, channels=CHANNELS, trace=None, fused=True):
     """Run the network on level-0 features x (n_0 x channels[0]).
 
     params[name] = (scale, shift, W): device fp32 scale and shift over the
-    unit's input channels, W [k][cin][cout] in x's dtype.  If `trace` is a
-    list, (unit, unit input, unit output) is appended for every unit.
+    unit's input channels, W [k][cin][cout] in x's dtype.
+
+    fused (default): every unit writes its output already pre-activated for
+    the unit(s) that consume it (the convolution's write-out applies their
+    affine map and ReLU), and the skip and upsampled halves of each decoder
+    concatenation are written straight into one buffer; only the network
+    input is pre-activated separately.  If `trace` is a list, (unit, the
+    convolution's input, [(destination, scale, shift), ...]) is appended
+    for every unit.
+
+    fused=False: one pre-activation, convolution and concatenation call
+    after another; `trace` receives (unit, unit input before its
+    pre-activation, unit output).
     """
     if len(channels) != geom.levels:
         raise ValueError("channel list and geometry disagree on the number of levels")
+    if fused:
+        return _forward_fused(x, geom, params, channels, trace)
 
     def run(u, inp):
         scale, shift, w = params[u.name]
@@ -126,6 +139,54 @@ def forward(x, geom, params, channels=CHANNELS, trace=None):
         else:
             x = run(u, x)
     return x
+
+
+def _forward_fused(x, geom, params, channels, trace):
+    L = len(channels)
+    by_name = {u.name: u for u in units(channels)}
+
+    def new(level, c):
+        return torch.empty((geom.coords[level].shape[0], c), dtype=x.dtype, device=x.device)
+
+    def act(name, lo=None, hi=None):
+        scale, shift, _ = params[name]
+        return scale[lo:hi], shift[lo:hi]
+
+    def conv(name, inp, heads):
+        u = by_name[name]
+        w = params[name][2]
+        if tuple(w.shape) != (u.k, u.cin, u.cout):
+            raise ValueError(f"{name}: weights {tuple(w.shape)}, expected {(u.k, u.cin, u.cout)}")
+        sscn.sparse_conv_forward_heads(inp, w, geom.rulebook(u), heads)
+        if trace is not None:
+            trace.append((u, inp, heads))
+        return [h[0] for h in heads]
+
+    s0, b0 = act("enc0a")
+    cur = sscn.affine_relu(x, s0, b0)
+    cat = {}
+    for l in range(L):
+        c = channels[l]
+        (y,) = conv(f"enc{l}a", cur, [(new(l, c), *act(f"enc{l}b"))])
+        if l < L - 1:
+            cat[l] = new(l, 2 * c)
+            a_down, _ = conv(f"enc{l}b", y, [(new(l, c), *act(f"down{l}")),
+                                             (cat[l][:, :c], *act(f"dec{l}a", 0, c))])
+            (cur,) = conv(f"down{l}", a_down, [(new(l + 1, channels[l + 1]), *act(f"enc{l + 1}a"))])
+        else:
+            (cur,) = conv(f"enc{l}b", y, [(new(l, c), *act(f"up{l - 1}"))]) if L > 1 else \
+                conv(f"enc{l}b", y, [(new(l, c), None, None)])
+    if L == 1:
+        return cur
+    for l in reversed(range(L - 1)):
+        c = channels[l]
+        conv(f"up{l}", cur, [(cat[l][:, c:], *act(f"dec{l}a", c, 2 * c))])
+        (z,) = conv(f"dec{l}a", cat.pop(l), [(new(l, c), *act(f"dec{l}b"))])
+        if l > 0:
+            (cur,) = conv(f"dec{l}b", z, [(new(l, c), *act(f"up{l - 1}"))])
+        else:
+            (cur,) = conv(f"dec{l}b", z, [(new(l, c), None, None)])
+    return cur
 
 
 def flops(geom, channels=CHANNELS):

@@ -183,3 +183,61 @@ def test_empty_layer():
     dx, dw = sscn.sparse_conv_backward(torch.zeros((0, 4), device="cuda:0"), torch.zeros((27, 4, 5), device="cuda:0"),
                                        torch.zeros((0, 5), device="cuda:0"), rb)
     assert dx.shape == (0, 4) and float(dw.abs().sum()) == 0.0
+
+
+def _heads_case(rb, orb, cin, cout, dtype, seed):
+    """Two destinations: an activated one (affine + ReLU) written into the
+    right half of a wider buffer, and a plain one; both against the oracle's
+    convolution followed by the same map, and the buffer's left half must
+    stay untouched."""
+    rng = np.random.default_rng(seed)
+    X, W = _draw(orb.n_in, cin, cout, orb.K, seed, dtype)
+    scale = rng.uniform(0.5, 1.5, cout).astype(np.float32)
+    shift = rng.normal(0, 0.1, cout).astype(np.float32)
+    wide = torch.full((orb.n_out, 2 * cout + 3), 7.0, dtype=TD[dtype], device="cuda:0")
+    plain = torch.empty((orb.n_out, cout), dtype=TD[dtype], device="cuda:0")
+    sscn.sparse_conv_forward_heads(dev(X, TD[dtype]), dev(W, TD[dtype]), rb,
+                                   [(wide[:, cout:2 * cout], dev(scale), dev(shift)), (plain, None, None)])
+    ref = O.forward(X, W, orb)
+    got = host(wide)
+    assert_close(got[:, cout:2 * cout], O.affine_relu(ref, scale, shift), dtype, "activated head")
+    assert_close(host(plain), ref, dtype, "plain head")
+    assert np.all(got[:, :cout] == 7.0) and np.all(got[:, 2 * cout:] == 7.0), "writes outside the head"
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("cin,cout", [(64, 64), (32, 48), (24, 128)])
+def test_forward_heads_ssc(cin, cout, dtype):
+    """Activated + plain heads on the 128^3 shapes workload (64-multiple c_out
+    takes the quad kernel, the others the column kernel)."""
+    coords, size = coords_for("shapes128")
+    _heads_case(sscn.ssc_rulebook_build(dev(coords), size, 3), O.ssc_rulebook(coords, size, 3),
+                cin, cout, dtype, 41)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_forward_heads_sc_and_dc(dtype):
+    """Heads on an SC(2, 2) rule book and on its transpose (the DC path)."""
+    coords = small_set(29, (20, 18, 22))
+    size = (20, 18, 22)
+    sc = sscn.sc_rulebook_build(dev(coords), size, 2, 2)
+    osc = O.sc_rulebook(coords, size, 2, 2)
+    _heads_case(sc, osc, 32, 64, dtype, 43)
+    _heads_case(sc.transpose(), O.transpose(osc), 64, 32, dtype, 44)
+
+
+def test_forward_heads_rejects_bad_heads():
+    coords = small_set(30, (6, 6, 6))
+    rb = sscn.ssc_rulebook_build(dev(coords), (6, 6, 6), 3)
+    X = torch.zeros((coords.shape[0], 4), device="cuda:0")
+    W = torch.zeros((27, 4, 8), device="cuda:0")
+    out = torch.empty((coords.shape[0], 8), device="cuda:0")
+    s = torch.ones(8, device="cuda:0")
+    with pytest.raises(ValueError):
+        sscn.sparse_conv_forward_heads(X, W, rb, [])
+    with pytest.raises(ValueError):
+        sscn.sparse_conv_forward_heads(X, W, rb, [(out, s, None)])
+    with pytest.raises(ValueError):
+        sscn.sparse_conv_forward_heads(X, W, rb, [(out[:, :4], None, None)])
+    with pytest.raises(ValueError):
+        sscn.sparse_conv_forward_heads(X, W, rb, [(out, None, None)] * 3)

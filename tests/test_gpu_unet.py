@@ -1,8 +1,12 @@
 """The U-Net of Sec. 5 on the GPU against the oracle.
 
 Every unit is checked teacher-forced: the oracle runs the unit on the GPU's
-own input to that unit (pre-activation, rounding to the stored dtype,
-convolution) and the GPU's output must match it at the layer tolerance.
+own input to that unit and the GPU's output must match it at the layer
+tolerance.  In the fused network each unit's output is written already
+pre-activated for its consumers (and the skip half of a decoder input
+straight into the concatenation buffer), so every such destination is
+checked against the oracle's convolution followed by that destination's
+affine map and ReLU.
 The small network is also compared end to end with the oracle's own
 composition; at 256^3 x 8 scenes the units are checked on sampled output
 rows, and all rule books of levels 1-4 (level 0 is checked in the rule-book
@@ -46,26 +50,35 @@ def _check_geometry(geom, levels, first_level=0):
             assert_same_rulebook(geom.up[l], O.transpose(osc), f"level {l} dc")
 
 
-def _teacher_forced(trace, levels, dtype, rows=None, seed=0):
+def _teacher_forced(trace, levels, dtype, rows=None, seed=0, fused=True):
+    """fused: trace entries (unit, convolution input, [(dest, scale, shift)]);
+    each destination must hold the oracle's convolution of that input with
+    the destination's pre-activation (affine + ReLU, or none) applied.
+    Unfused: (unit, unit input, output); the oracle pre-activates the input
+    with the unit's own parameters and rounds it to the stored dtype."""
     rng = np.random.default_rng(seed)
     draw = _draw(dtype)
     rnd = O.round_bf16 if dtype == "bf16" else (lambda a: a)
-    for u, inp, y in trace:
+    for u, inp, outs in trace:
         rb = _oracle_rb(levels, u)
         scale, shift, W = draw(u.name, u.k, u.cin, u.cout)
-        a = rnd(O.affine_relu(host(inp), scale, shift))
-        got = host(y)
-        assert got.shape == (rb.n_out, u.cout), u.name
-        if rows is None:
-            ref = O.forward(a, W, rb)
+        if fused:
+            a = host(inp)
         else:
-            pick = rng.choice(rb.n_out, size=min(rows, rb.n_out), replace=False)
-            ref, got = O.forward_rows(a, W, rb, pick), got[pick]
-        assert_close(got, ref, dtype, u.name)
+            a = rnd(O.affine_relu(host(inp), scale, shift))
+            outs = [(outs, None, None)]
+        pick = None if rows is None else rng.choice(rb.n_out, size=min(rows, rb.n_out), replace=False)
+        ref = O.forward(a, W, rb) if pick is None else O.forward_rows(a, W, rb, pick)
+        for i, (dest, hs, hb) in enumerate(outs):
+            got = host(dest)
+            assert got.shape == (rb.n_out, u.cout), u.name
+            want = ref if hs is None else O.affine_relu(ref, host(hs), host(hb))
+            assert_close(got if pick is None else got[pick], want, dtype, f"{u.name} head {i}")
 
 
+@pytest.mark.parametrize("fused", [True, False], ids=["fused", "unfused"])
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
-def test_unet_small_scenes(dtype):
+def test_unet_small_scenes(dtype, fused):
     """64^3 x 2 scenes, five levels 64 -> 4, channels 32 .. 160."""
     levels = oracle_levels("scenes_small", 5)
     coords, size = levels[0][0], levels[0][1]
@@ -74,9 +87,9 @@ def test_unet_small_scenes(dtype):
     X = S.features(coords.shape[0], 32, S.SEED_FEAT + 13, bf16=dtype == "bf16")
     params = unet.device_params(dtype=TD[dtype], draw=_draw(dtype))
     trace = []
-    y = unet.forward(dev(X, TD[dtype]), geom, params, trace=trace)
+    y = unet.forward(dev(X, TD[dtype]), geom, params, trace=trace, fused=fused)
     assert len(trace) == len(unet.units())
-    _teacher_forced(trace, levels, dtype)
+    _teacher_forced(trace, levels, dtype, fused=fused)
     ref = O.unet_forward(coords, size, X, _draw(dtype), unet.CHANNELS, round_to_bf16=dtype == "bf16")
     got = host(y)
     err = np.linalg.norm(got - ref) / np.linalg.norm(ref)
