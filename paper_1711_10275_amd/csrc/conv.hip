@@ -229,6 +229,17 @@ __device__ __forceinline__ f32x4 mma_oct(const Oct<bf16_t>& a, const Oct<bf16_t>
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b.v, d, 0, 0, 0);
 }
 
+// An operand (8 channels) from LDS.
+__device__ __forceinline__ void lds_oct(Oct<float>& o, const char* p) {
+  const uint4 x = *reinterpret_cast<const uint4*>(p);
+  const uint4 y = *reinterpret_cast<const uint4*>(p + 16);
+  o.v[0] = __uint_as_float(x.x); o.v[1] = __uint_as_float(x.y); o.v[2] = __uint_as_float(x.z); o.v[3] = __uint_as_float(x.w);
+  o.v[4] = __uint_as_float(y.x); o.v[5] = __uint_as_float(y.y); o.v[6] = __uint_as_float(y.z); o.v[7] = __uint_as_float(y.w);
+}
+__device__ __forceinline__ void lds_oct(Oct<bf16_t>& o, const char* p) {
+  o.v = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(p));
+}
+
 // LDS layout of k_conv_quad (bytes, each part 16-byte aligned).
 struct QuadLds {
   size_t acc, prow, pacc, chof, seg_s, seg_n, seg_c0, total;
@@ -485,6 +496,177 @@ __global__ __launch_bounds__(256) void k_conv_quad(
       if (row < n_out && col < cout)
         Y.store(row, col, acc_all[r * LDW + cc] + acc_all[ACC + r * LDW + cc]);
     }
+  }
+}
+
+// ---------------------------------------------------- row-block kernel
+// Forward / dgrad over a row-block plan.  A workgroup owns one block of
+// kPlanRows = 64 output rows (rows whose offset sets are alike) and 16 NB
+// output columns; wavefront w owns rows 16 w .. 16 w + 15 with its
+// accumulators in registers.  The workgroup walks the block's items (one
+// offset each) in steps of WB bytes of reduction channels; per step every
+// wavefront gathers its 16 rows' input rows (a row without a pair for the
+// item reads zeros) and the workgroup stages the offset's weight tile, both
+// through LDS, then multiplies.  Each output element is written once.
+//
+// Loads: gathers whose lanes follow the MFMA layout (consecutive lanes on
+// consecutive rows) issue at about a third of the rate of loads in which
+// several consecutive lanes read one contiguous piece of a row, so rows and
+// weights are loaded WB bytes per row with WB / 16 lanes per row, written
+// to LDS, and read back in the MFMA layout: lane (m, g) takes channels
+// 32 j + 8 g + [0, 8) (j < S) of row m of the step's window (A) and of
+// weight row m of each column block (B).  The MFMAs sum over exactly these
+// channels, so a row's result does not depend on which rows share its
+// block.  B is laid out [o][ncols][kdim] (a contiguous row of reduction
+// channels per output column).  Global loads run D - 1 steps ahead in
+// registers; the weight tile is double-buffered in LDS with one barrier per
+// step; each wavefront's row tile is private to it.
+template <typename T, int WB, int NB, int D>
+__global__ __launch_bounds__(256) void k_conv_rows(
+    const T* __restrict__ X, uint32_t x_bytes, const T* __restrict__ B, uint32_t b_bytes,
+    const int32_t* __restrict__ perm, const int32_t* __restrict__ b_first, const uint32_t* __restrict__ items,
+    int K, int mirror, int kdim, int ncols, Heads<T> Y) {
+  constexpr int LPR = WB / 16;              // lanes per row window
+  constexpr int RPI = 64 / LPR;             // rows per wavefront load
+  constexpr int NA = 16 / RPI;              // row loads per wavefront and step
+  constexpr int COLS = 16 * NB;             // output columns per workgroup
+  constexpr int NBP = (COLS * LPR + 255) / 256;  // weight pieces per thread and step
+  constexpr int PITCH = WB + 16;            // LDS bytes per row (bank spread)
+  constexpr int S = WB / (32 * (int)sizeof(T));  // 32-channel MFMA groups per step
+  static_assert(S >= 1 && 16 % RPI == 0, "window");
+  __shared__ __attribute__((aligned(16))) char As[4][16 * PITCH];
+  __shared__ __attribute__((aligned(16))) char Bs[2][COLS * PITCH];
+  __shared__ uint32_t ent[32 * kPlanRows];  // K <= 32 items per block
+
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int m = lane & 15, g = lane >> 4;
+  const int64_t blk = blockIdx.x;
+  const int col0 = blockIdx.y * COLS;
+  const int first = b_first[blk];
+  const int n_items = b_first[blk + 1] - first;
+  const uint32_t row_bytes = (uint32_t)kdim * sizeof(T);
+  const int ks_n = (int)((row_bytes + WB - 1) / WB);  // steps per item
+  const int n_steps = n_items * ks_n;
+  const uint32_t w_stride = (uint32_t)ncols * row_bytes;  // bytes per offset
+  const rsrc_t rx = make_rsrc(X, x_bytes), rb = make_rsrc(B, b_bytes);
+
+  f32x4 acc[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  if (n_steps > 0) {
+    {
+      // all of the block's entries in one round trip
+      const int n_ent = n_items * kPlanRows;
+      const uint32_t* src = items + (int64_t)first * kPlanRows;
+      uint32_t t[32 * kPlanRows / 256];
+#pragma unroll
+      for (int q = 0; q < 32 * kPlanRows / 256; ++q) t[q] = src[min(tid + 256 * q, n_ent - 1)];
+#pragma unroll
+      for (int q = 0; q < 32 * kPlanRows / 256; ++q)
+        if (tid + 256 * q < n_ent) ent[tid + 256 * q] = t[q];
+    }
+    __syncthreads();
+
+    // lane constants of the coalesced loads
+    const uint32_t a_byte = (uint32_t)(lane % LPR) * 16;  // within the window
+    int a_row[NA];                                          // row within the wavefront's 16
+#pragma unroll
+    for (int i = 0; i < NA; ++i) a_row[i] = lane / LPR + RPI * i;
+    int b_col[NBP];
+    uint32_t b_byte[NBP], b_base[NBP];
+#pragma unroll
+    for (int q = 0; q < NBP; ++q) {
+      const int p = tid + 256 * q;
+      b_col[q] = p / LPR;
+      b_byte[q] = (uint32_t)(p % LPR) * 16;
+      const int col = col0 + b_col[q];
+      b_base[q] = (b_col[q] < COLS && col < ncols) ? (uint32_t)col * row_bytes : kOobOffset;
+    }
+
+    uint4 ga[D][NA], gb[D][NBP];  // global loads in flight
+    int ld_item = 0, ld_ks = 0, ld_step = 0;
+    auto issue = [&](int slot) {
+      const bool live = ld_step < n_steps;
+      const int it = min(ld_item, n_items - 1);
+      const uint32_t e0 = ent[it * kPlanRows];
+      const int o = (int)((uint32_t)__builtin_amdgcn_readfirstlane((int)e0) >> kPlanRowBits);
+      const int ow = mirror ? K - 1 - o : o;
+      const uint32_t win = (uint32_t)ld_ks * WB;
+#pragma unroll
+      for (int i = 0; i < NA; ++i) {
+        const uint32_t r = ent[it * kPlanRows + wave * 16 + a_row[i]] & kPlanNoRow;
+        const bool ok = live && r != kPlanNoRow && win + a_byte < row_bytes;
+        const auto v = __builtin_amdgcn_raw_buffer_load_b128(rx, (int)(ok ? r * row_bytes + win + a_byte : kOobOffset),
+                                                             0, 0);
+        ga[slot][i] = make_uint4(v[0], v[1], v[2], v[3]);
+      }
+#pragma unroll
+      for (int q = 0; q < NBP; ++q) {
+        const bool ok = live && win + b_byte[q] < row_bytes && b_base[q] != kOobOffset;
+        const auto v = __builtin_amdgcn_raw_buffer_load_b128(
+            rb, (int)(ok ? b_base[q] + win + b_byte[q] : kOobOffset), (int)((uint32_t)ow * w_stride), 0);
+        gb[slot][q] = make_uint4(v[0], v[1], v[2], v[3]);
+      }
+      if (++ld_ks == ks_n) { ld_ks = 0; ++ld_item; }
+      ++ld_step;
+    };
+    auto stage = [&](int slot, int buf) {
+#pragma unroll
+      for (int i = 0; i < NA; ++i)
+        *reinterpret_cast<uint4*>(&As[wave][a_row[i] * PITCH + a_byte]) = ga[slot][i];
+#pragma unroll
+      for (int q = 0; q < NBP; ++q)
+        if (b_col[q] < COLS) *reinterpret_cast<uint4*>(&Bs[buf][b_col[q] * PITCH + b_byte[q]]) = gb[slot][q];
+    };
+    auto multiply = [&](int buf) {
+      Oct<T> a[S], b[S][NB];
+#pragma unroll
+      for (int j = 0; j < S; ++j) {
+        const int byte = (32 * j + 8 * g) * (int)sizeof(T);
+        lds_oct(a[j], &As[wave][m * PITCH + byte]);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) lds_oct(b[j][nb], &Bs[buf][(nb * 16 + m) * PITCH + byte]);
+      }
+#pragma unroll
+      for (int j = 0; j < S; ++j)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) acc[nb] = mma_oct(a[j], b[j][nb], acc[nb]);
+    };
+
+    // step t: its loads are issued at step t - D (ring slot t % D), staged
+    // into LDS at step t - 1 (weight buffer t % 2) and multiplied at step t
+#pragma unroll
+    for (int q = 0; q < D; ++q) issue(q);
+    stage(0, 0);
+    __syncthreads();
+    // u = t % (2 D) keeps the ring positions compile-time constants; the row
+    // tile of step t is read before step t + 1's rows overwrite it
+    auto step = [&](int u) {
+      multiply(u % 2);
+      stage((u + 1) % D, (u + 1) % 2);
+      issue(u % D);  // loads of step t + D
+      __syncthreads();
+    };
+    int t0 = 0;
+    for (; t0 + 2 * D <= n_steps; t0 += 2 * D) {
+#pragma unroll
+      for (int u = 0; u < 2 * D; ++u) step(u);
+    }
+#pragma unroll
+    for (int u = 0; u < 2 * D - 1; ++u)
+      if (t0 + u < n_steps) step(u);
+  }
+  // lane holds rows 4 g + r of the wavefront's 16, column m of each column block
+  const int4 rows = *reinterpret_cast<const int4*>(perm + blk * kPlanRows + wave * 16 + 4 * g);
+  const int rr[4] = {rows.x, rows.y, rows.z, rows.w};
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int col = col0 + nb * 16 + m;
+    if (col < ncols)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        if (rr[r] >= 0) Y.store(rr[r], col, acc[nb][r]);
   }
 }
 
@@ -1078,6 +1260,48 @@ static sscn_status launch_conv(const T* X, const T* W, const View& v, int cin, i
 }
 
 
+// Row-block kernel: B laid out [o][ncols][kdim]; K <= 32 (offset sets as
+// 32-bit masks), whole 8-channel runs, 32-bit buffer offsets.
+template <typename T>
+static bool rows_eligible(const View& v, int kdim, int ncols) {
+  const uint64_t x_bytes = (uint64_t)std::max<int64_t>(v.n_in, 1) * kdim * sizeof(T);
+  const uint64_t b_bytes = (uint64_t)v.K * ncols * kdim * sizeof(T);
+  return v.K <= 32 && kdim % 8 == 0 && x_bytes < kOobOffset && b_bytes < kOobOffset &&
+         std::max(v.n_in, v.n_out) < (int64_t)kPlanNoRow && ceil_div(v.n_out, kPlanRows) * v.K < INT32_MAX;
+}
+
+template <typename T, int WB, int NB>
+static sscn_status launch_rows_nb(const T* X, const T* B, const View& v, int kdim, int ncols, const Heads<T>& Y,
+                                  hipStream_t s) {
+  const int64_t nb = v.st->n_blocks;
+  if (nb == 0) return SSCN_OK;
+  const int gy = (ncols + 16 * NB - 1) / (16 * NB);
+  const uint32_t xb = (uint32_t)((uint64_t)std::max<int64_t>(v.n_in, 1) * kdim * sizeof(T));
+  const uint32_t bb = (uint32_t)((uint64_t)v.K * ncols * kdim * sizeof(T));
+  k_conv_rows<T, WB, NB, 3><<<dim3((unsigned)nb, (unsigned)gy), 256, 0, s>>>(
+      X, xb, B, bb, v.st->perm, v.st->b_first, v.st->items, v.K, v.mirror ? 1 : 0, kdim, ncols, Y);
+  SSCN_HIP(hipGetLastError());
+  return SSCN_OK;
+}
+
+template <typename T>
+static sscn_status launch_rows(const T* X, const T* B, const View& v, int kdim, int ncols, const Heads<T>& Y,
+                               hipStream_t s) {
+  if (v.n_out == 0) return SSCN_OK;
+  SSCN_TRY(ensure_plan(v, s));
+  // 64 output columns per workgroup when they divide the width, else 32;
+  // 128-byte windows (32 fp32 or 64 bf16 channels) unless a bf16 row is not
+  // a multiple of 128 bytes
+  const bool wide_cols = ncols % 64 == 0;
+  if constexpr (sizeof(T) == 2) {
+    if (kdim % 64 != 0)
+      return wide_cols ? launch_rows_nb<T, 64, 4>(X, B, v, kdim, ncols, Y, s)
+                       : launch_rows_nb<T, 64, 2>(X, B, v, kdim, ncols, Y, s);
+  }
+  return wide_cols ? launch_rows_nb<T, 128, 4>(X, B, v, kdim, ncols, Y, s)
+                   : launch_rows_nb<T, 128, 2>(X, B, v, kdim, ncols, Y, s);
+}
+
 // N contiguous channels of one row as fp32, one raw buffer load (an
 // out-of-range offset reads zeros).
 template <typename T, int N> struct RowLoad;
@@ -1329,6 +1553,17 @@ static sscn_status check_conv_args(sscn_rulebook rb, int32_t c_in, int32_t c_out
 // bf16 reads the stored layout directly.
 template <typename T>
 static sscn_status forward_t(const T* X, const T* W, const View& v, int cin, int cout, const Heads<T>& Y, hipStream_t s) {
+  if (rows_eligible<T>(v, cin, cout)) {
+    if (v.n_out == 0) return SSCN_OK;
+    const int64_t total = (int64_t)v.K * cin * cout;
+    T* Bt = nullptr;
+    SSCN_TRY(dev_alloc((void**)&Bt, sizeof(T) * total, s));
+    k_transpose_w<T><<<(unsigned)std::min<int64_t>(ceil_div(total, 256), 4096), 256, 0, s>>>(W, v.K, cin, cout, Bt);
+    hipError_t e = hipGetLastError();
+    sscn_status st = e == hipSuccess ? launch_rows<T>(X, Bt, v, cin, cout, Y, s) : hip_fail(e, "transpose");
+    dev_free(Bt, s);
+    return st;
+  }
   if (prefer_col<T>(v, cin, cout)) {
     if (v.n_out == 0) return SSCN_OK;
     const int64_t total = (int64_t)v.K * cin * cout;
@@ -1423,12 +1658,17 @@ extern "C" sscn_status sparse_conv_backward(const void* features, const void* we
     // row ci of W[o] holds the c_out weights feeding input channel ci)
     const View vt = transposed_view(rb);
     if (dtype == SSCN_F32)
-      st = launch_conv<float, true>((const float*)dout, (const float*)weights, vt, c_out, c_in,
-                                    plain_heads((float*)dgrad, c_in),
-                                    stream);
+      st = rows_eligible<float>(vt, c_out, c_in)
+               ? launch_rows<float>((const float*)dout, (const float*)weights, vt, c_out, c_in,
+                                    plain_heads((float*)dgrad, c_in), stream)
+               : launch_conv<float, true>((const float*)dout, (const float*)weights, vt, c_out, c_in,
+                                          plain_heads((float*)dgrad, c_in), stream);
     else
-      st = launch_conv<bf16_t, true>((const bf16_t*)dout, (const bf16_t*)weights, vt, c_out, c_in,
-                                     plain_heads((bf16_t*)dgrad, c_in), stream);
+      st = rows_eligible<bf16_t>(vt, c_out, c_in)
+               ? launch_rows<bf16_t>((const bf16_t*)dout, (const bf16_t*)weights, vt, c_out, c_in,
+                                     plain_heads((bf16_t*)dgrad, c_in), stream)
+               : launch_conv<bf16_t, true>((const bf16_t*)dout, (const bf16_t*)weights, vt, c_out, c_in,
+                                           plain_heads((bf16_t*)dgrad, c_in), stream);
     if (st != SSCN_OK) return st;
   }
   if (wgrad) {

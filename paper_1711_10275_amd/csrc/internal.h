@@ -23,6 +23,14 @@ constexpr int kTile = 64;
 // most 255 so that a row inside a tile and the padding row fit in a byte).
 constexpr int kChunkRows = 128;
 constexpr int kWave = 64;
+// Output rows per block of the row-block plan (four MFMA row tiles, one
+// per wavefront of a workgroup).
+constexpr int kPlanRows = 64;
+// Bits of the key that orders rows by their offset set.
+constexpr int kPlanKeyBits = 17;
+// A plan entry packs an input row (kPlanNoRow: none) below the item's offset.
+constexpr int kPlanRowBits = 27;
+constexpr uint32_t kPlanNoRow = (1u << kPlanRowBits) - 1;
 // Tiles are grouped into this many contiguous ranges, one per XCD of the
 // chip (each XCD has its own L2); see the tile order of a rule book.
 constexpr int kTileGroups = 8;
@@ -75,6 +83,14 @@ struct Storage {
   int32_t* c_in = nullptr;       // 16 per chunk: input row, -1 for padding
   uint8_t* c_out = nullptr;      // 16 per chunk: output row - tile start, kChunkRows for padding
   int32_t* c_off = nullptr;      // per chunk: offset (as stored)
+  // Row-block plan (K <= 32): the output rows ordered by the set of offsets
+  // that reach them (rows with similar sets side by side) and cut into
+  // blocks of kPlanRows; per block, one item per offset that reaches any of
+  // its rows, holding each row's input row for that offset (-1 if none).
+  int64_t n_blocks = 0;
+  int32_t* perm = nullptr;       // kPlanRows * n_blocks: output row at each position, -1 past the end
+  int32_t* b_first = nullptr;    // n_blocks + 1: first item of each block
+  uint32_t* items = nullptr;     // kPlanRows per item: input row | offset (as stored) << kPlanRowBits
 };
 
 struct RulebookData {
@@ -96,6 +112,7 @@ struct RulebookData {
   // that work on other streams can wait for it.
   std::mutex chunk_mu;
   hipEvent_t chunk_ready = nullptr;
+  hipEvent_t plan_ready = nullptr;   // the same for the row-block plans
   ~RulebookData();
 };
 
@@ -121,6 +138,8 @@ struct View {
 // Builds the padded chunk table of the view's storage if it is not there
 // yet and makes `s` wait for it.
 sscn_status ensure_chunks(const View& v, hipStream_t s);
+// The same for the row-block plan (K <= 32).
+sscn_status ensure_plan(const View& v, hipStream_t s);
 
 inline View view_of(const sscn_rulebook_s* rb) {
   const RulebookData* d = rb->d;

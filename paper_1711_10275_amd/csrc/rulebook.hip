@@ -740,6 +740,198 @@ sscn_status ensure_chunks(const View& v, hipStream_t s) {
   return SSCN_OK;
 }
 
+// ------------------------------------------------------ row-block plan
+// Offset set of every output row as a bit mask.  One thread per pair of
+// offset blockIdx.y (pairs of one offset have distinct output rows).
+__global__ void k_plan_mask(const int64_t* __restrict__ seg, int64_t n_tiles,
+                            const int32_t* __restrict__ out_rows, uint32_t* __restrict__ mask) {
+  const int o = blockIdx.y;
+  const int64_t p = seg[(int64_t)o * n_tiles] + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= seg[(int64_t)(o + 1) * n_tiles]) return;
+  atomicOr(&mask[out_rows[p]], 1u << o);
+}
+
+// Sort key of an offset set: the set itself when it has at most
+// kPlanKeyBits offsets; for 3^3 filters the 12 edge neighbours and 5 of the
+// 6 face neighbours (o = 9 i0 + 3 i1 + i2; the centre is in nearly every
+// set and the corners vary least between neighbouring surface sites);
+// otherwise the highest kPlanKeyBits offsets.
+__device__ __forceinline__ uint32_t plan_key(uint32_t m, int K) {
+  if (K <= kPlanKeyBits) return m;
+  if (K == 27) {
+    constexpr int sel[kPlanKeyBits] = {1, 3, 5, 7, 9, 11, 15, 17, 19, 21, 23, 25, 10, 12, 14, 16, 22};
+    uint32_t k = 0;
+#pragma unroll
+    for (int i = 0; i < kPlanKeyBits; ++i) k = (k << 1) | ((m >> sel[i]) & 1u);
+    return k;
+  }
+  return m >> (K - kPlanKeyBits);
+}
+
+// Adds one to counter[key] for every active lane with one atomic per distinct
+// key of the wavefront (offset sets repeat a lot: a plain atomic per row
+// serialises on the common ones); returns the counter's value before this
+// lane's increment.
+__device__ __forceinline__ int wave_count(int32_t* counter, uint32_t key, bool active) {
+  const int lane = threadIdx.x & 63;
+  uint64_t todo = __ballot(active);
+  int res = 0;
+  while (todo) {
+    const int leader = __ffsll((unsigned long long)todo) - 1;
+    const uint32_t k = __shfl(key, leader, 64);
+    const bool mine = active && key == k;
+    const uint64_t peers = __ballot(mine);
+    int base = 0;
+    if (lane == leader) base = atomicAdd(&counter[k], __popcll(peers));
+    base = __shfl(base, leader, 64);
+    if (mine) res = base + __popcll(peers & ((1ull << lane) - 1ull));
+    todo &= ~peers;
+  }
+  return res;
+}
+
+__global__ void k_plan_hist(const uint32_t* __restrict__ mask, int64_t n, int K, int32_t* __restrict__ hist) {
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const bool ok = r < n;
+  (void)wave_count(hist, ok ? plan_key(mask[r], K) : 0u, ok);
+}
+
+// Counting sort by key (the order inside one key is arbitrary: it changes
+// which rows share a block, never a row's result).
+__global__ void k_plan_sort(const uint32_t* __restrict__ mask, int64_t n, int K, int32_t* __restrict__ cursor,
+                            int32_t* __restrict__ perm, int32_t* __restrict__ pos_of) {
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const bool ok = r < n;
+  const int32_t p = wave_count(cursor, ok ? plan_key(mask[r], K) : 0u, ok);
+  if (ok) {
+    perm[p] = (int32_t)r;
+    pos_of[r] = p;
+  }
+}
+
+// One wavefront per block: union of the offset sets of its rows and its item
+// count; the positions past the last row are marked empty.
+static_assert(kPlanRows == 64, "one wavefront per plan block");
+__global__ void k_plan_blocks(const uint32_t* __restrict__ mask, int32_t* __restrict__ perm, int64_t n,
+                              int64_t n_blocks, uint32_t* __restrict__ bmask, int32_t* __restrict__ cnt) {
+  const int64_t b = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int lane = threadIdx.x & 63;
+  if (b >= n_blocks) return;
+  const int64_t p = b * kPlanRows + lane;
+  uint32_t u = 0;
+  if (p < n)
+    u = mask[perm[p]];
+  else
+    perm[p] = -1;
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) u |= (uint32_t)__shfl_xor((int)u, d, 64);
+  if (lane == 0) {
+    bmask[b] = u;
+    cnt[b] = __popc(u);
+  }
+}
+
+// Thread (block, slot): marks its slot of every item of the block empty
+// (items in ascending offset order).
+__global__ void k_plan_items(const uint32_t* __restrict__ bmask, const int32_t* __restrict__ b_first,
+                             int64_t n_blocks, uint32_t* __restrict__ items) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t b = t / kPlanRows;
+  const int m = (int)(t % kPlanRows);
+  if (b >= n_blocks) return;
+  uint32_t u = bmask[b];
+  int64_t item = b_first[b];
+  while (u) {
+    const uint32_t o = (uint32_t)(__ffs(u) - 1);
+    u &= u - 1;
+    items[item * kPlanRows + m] = kPlanNoRow | (o << kPlanRowBits);
+    ++item;
+  }
+}
+
+// Every pair into its block's item for its offset, at its row's slot.
+__global__ void k_plan_pairs(const int64_t* __restrict__ seg, int64_t n_tiles, const int32_t* __restrict__ in_rows,
+                             const int32_t* __restrict__ out_rows, const int32_t* __restrict__ pos_of,
+                             const uint32_t* __restrict__ bmask, const int32_t* __restrict__ b_first,
+                             uint32_t* __restrict__ items) {
+  const int o = blockIdx.y;
+  const int64_t p = seg[(int64_t)o * n_tiles] + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= seg[(int64_t)(o + 1) * n_tiles]) return;
+  const int32_t pos = pos_of[out_rows[p]];
+  const int64_t b = pos / kPlanRows;
+  const int64_t item = b_first[b] + __popc(bmask[b] & ((1u << o) - 1u));
+  items[item * kPlanRows + pos % kPlanRows] = (uint32_t)in_rows[p] | ((uint32_t)o << kPlanRowBits);
+}
+
+// Row-block plan of one direction (seg and pair arrays complete), in the
+// rule book's own blocks.
+static sscn_status build_plan(RulebookData* d, Storage& st, int64_t n_rows, int K, hipStream_t s) {
+  const int64_t nb = ceil_div(n_rows, kPlanRows);
+  st.n_blocks = nb;
+  const int64_t cap = std::max<int64_t>(1, std::min<int64_t>(d->n_pairs, nb * K));
+  Arena a;
+  a.add(&st.perm, (size_t)nb * kPlanRows);
+  a.add(&st.b_first, (size_t)nb + 1);
+  a.add(&st.items, (size_t)cap * kPlanRows);
+  SSCN_TRY(owned_alloc(d, a, s));
+  if (nb == 0) return fill_i32(st.b_first, 0, 1, s);
+  const int bins = 1 << std::min(K, kPlanKeyBits);
+  Temps tmp(s);
+  uint32_t* mask; uint32_t* bmask; int32_t* hist; int32_t* pos_of;
+  Arena t;
+  t.add(&mask, (size_t)n_rows);
+  t.add(&bmask, (size_t)nb);
+  t.add(&hist, (size_t)bins + 1);
+  t.add(&pos_of, (size_t)n_rows);
+  SSCN_TRY(tmp.alloc(t));
+  SSCN_TRY(fill_i32((int32_t*)mask, 0, n_rows, s));
+  SSCN_TRY(fill_i32(hist, 0, bins + 1, s));
+  int64_t max_ppo = 0;
+  for (int64_t c : d->pairs_per_offset) max_ppo = std::max(max_ppo, c);
+  if (max_ppo > 0) {
+    k_plan_mask<<<dim3((unsigned)ceil_div(max_ppo, 256), (unsigned)K), 256, 0, s>>>(st.seg, st.n_tiles,
+                                                                                    st.out_rows, mask);
+    SSCN_HIP(hipGetLastError());
+  }
+  k_plan_hist<<<grid_for(n_rows, 256), 256, 0, s>>>(mask, n_rows, K, hist);
+  SSCN_HIP(hipGetLastError());
+  SSCN_TRY(exclusive_scan_i32(hist, hist, bins, s));
+  k_plan_sort<<<grid_for(n_rows, 256), 256, 0, s>>>(mask, n_rows, K, hist, st.perm, pos_of);
+  SSCN_HIP(hipGetLastError());
+  k_plan_blocks<<<grid_for(nb * 64, 256), 256, 0, s>>>(mask, st.perm, n_rows, nb, bmask, st.b_first);
+  SSCN_HIP(hipGetLastError());
+  SSCN_TRY(exclusive_scan_i32(st.b_first, st.b_first, nb, s));
+  k_plan_items<<<grid_for(nb * kPlanRows, 256), 256, 0, s>>>(bmask, st.b_first, nb, st.items);
+  SSCN_HIP(hipGetLastError());
+  if (max_ppo > 0) {
+    k_plan_pairs<<<dim3((unsigned)ceil_div(max_ppo, 256), (unsigned)K), 256, 0, s>>>(
+        st.seg, st.n_tiles, st.in_rows, st.out_rows, pos_of, bmask, st.b_first, st.items);
+    SSCN_HIP(hipGetLastError());
+  }
+  return SSCN_OK;
+}
+
+sscn_status ensure_plan(const View& v, hipStream_t s) {
+  RulebookData* d = v.owner;
+  if (d->K > 32 || std::max(d->n_in, d->n_out) >= (int64_t)kPlanNoRow)
+    return fail(SSCN_ERR_INVALID_ARG, "row-block plan needs at most 32 offsets and fewer than 2^27 rows");
+  Storage& st = v.st == &d->fwd ? d->fwd : d->bwd;
+  {
+    std::lock_guard<std::mutex> lock(d->chunk_mu);
+    if (st.b_first == nullptr) {
+      int cur = 0;
+      SSCN_HIP(hipGetDevice(&cur));
+      if (cur != d->device) return fail(SSCN_ERR_INVALID_ARG, "rule book used on another device");
+      const int64_t n_rows = &st == &d->fwd ? d->n_out : d->n_in;
+      SSCN_TRY(build_plan(d, st, n_rows, d->K, d->stream));
+      if (!d->plan_ready) SSCN_HIP(hipEventCreateWithFlags(&d->plan_ready, hipEventDisableTiming));
+      SSCN_HIP(hipEventRecord(d->plan_ready, d->stream));
+    }
+  }
+  if (s != d->stream) SSCN_HIP(hipStreamWaitEvent(s, d->plan_ready, 0));
+  return SSCN_OK;
+}
+
 static sscn_status check_common(const int32_t* coords, int64_t n, const int32_t* spatial_size,
                                 int32_t f, sscn_rulebook* out) {
   if (!out) return fail(SSCN_ERR_INVALID_ARG, "out handle pointer is NULL");

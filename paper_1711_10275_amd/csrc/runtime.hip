@@ -99,6 +99,7 @@ RulebookData::~RulebookData() {
   if (cur != device) (void)hipSetDevice(device);
   for (void* p : blocks) dev_free(p, stream);
   if (chunk_ready) (void)hipEventDestroy(chunk_ready);
+  if (plan_ready) (void)hipEventDestroy(plan_ready);
   if (cur != device) (void)hipSetDevice(cur);
 }
 
