@@ -522,10 +522,11 @@ __global__ __launch_bounds__(256) void k_conv_quad(
 // registers; the weight tile is double-buffered in LDS with one barrier per
 // step; each wavefront's row tile is private to it.
 template <typename T, int WB, int NB, int D>
-__global__ __launch_bounds__(256) void k_conv_rows(
+__device__ __forceinline__ void conv_rows_block(
     const T* __restrict__ X, uint32_t x_bytes, const T* __restrict__ B, uint32_t b_bytes,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ b_first, const uint32_t* __restrict__ items,
-    int K, int mirror, int kdim, int ncols, Heads<T> Y) {
+    int64_t blk, int K, int mirror, int kdim, int ncols, const Heads<T>& Y, char (*As)[16 * (WB + 16)],
+    char (*Bs)[16 * NB * (WB + 16)], uint32_t* ent, int tid, int wave, int lane, int m, int g, int col0) {
   constexpr int LPR = WB / 16;              // lanes per row window
   constexpr int RPI = 64 / LPR;             // rows per wavefront load
   constexpr int NA = 16 / RPI;              // row loads per wavefront and step
@@ -533,15 +534,6 @@ __global__ __launch_bounds__(256) void k_conv_rows(
   constexpr int NBP = (COLS * LPR + 255) / 256;  // weight pieces per thread and step
   constexpr int PITCH = WB + 16;            // LDS bytes per row (bank spread)
   constexpr int S = WB / (32 * (int)sizeof(T));  // 32-channel MFMA groups per step
-  static_assert(S >= 1 && 16 % RPI == 0, "window");
-  __shared__ __attribute__((aligned(16))) char As[4][16 * PITCH];
-  __shared__ __attribute__((aligned(16))) char Bs[2][COLS * PITCH];
-  __shared__ uint32_t ent[32 * kPlanRows];  // K <= 32 items per block
-
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int m = lane & 15, g = lane >> 4;
-  const int64_t blk = blockIdx.x;
-  const int col0 = blockIdx.y * COLS;
   const int first = b_first[blk];
   const int n_items = b_first[blk + 1] - first;
   const uint32_t row_bytes = (uint32_t)kdim * sizeof(T);
@@ -619,7 +611,12 @@ __global__ __launch_bounds__(256) void k_conv_rows(
       for (int q = 0; q < NBP; ++q)
         if (b_col[q] < COLS) *reinterpret_cast<uint4*>(&Bs[buf][b_col[q] * PITCH + b_byte[q]]) = gb[slot][q];
     };
+    int mul_item = 0, mul_ks = 0;  // item of the step being multiplied
     auto multiply = [&](int buf) {
+      // a wavefront whose 16 rows have no pair for the item skips the MFMAs
+      const uint32_t e = ent[mul_item * kPlanRows + wave * 16 + m];
+      if (++mul_ks == ks_n) { mul_ks = 0; ++mul_item; }
+      if (__ballot((e & kPlanNoRow) != kPlanNoRow) == 0) return;
       Oct<T> a[S], b[S][NB];
 #pragma unroll
       for (int j = 0; j < S; ++j) {
@@ -667,6 +664,32 @@ __global__ __launch_bounds__(256) void k_conv_rows(
 #pragma unroll
       for (int r = 0; r < 4; ++r)
         if (rr[r] >= 0) Y.store(rr[r], col, acc[nb][r]);
+  }
+}
+
+template <typename T, int WB, int NB, int D>
+__global__ __launch_bounds__(256) void k_conv_rows(
+    const T* __restrict__ X, uint32_t x_bytes, const T* __restrict__ B, uint32_t b_bytes,
+    const int32_t* __restrict__ perm, const int32_t* __restrict__ b_first, const int32_t* __restrict__ b_order,
+    const uint32_t* __restrict__ items, int64_t n_blocks, int K, int mirror, int kdim, int ncols, Heads<T> Y) {
+  constexpr int RPI = 64 / (WB / 16);       // rows per wavefront load
+  constexpr int COLS = 16 * NB;             // output columns per workgroup
+  constexpr int PITCH = WB + 16;            // LDS bytes per row (bank spread)
+  static_assert(WB / (32 * (int)sizeof(T)) >= 1 && 16 % RPI == 0, "window");
+  __shared__ __attribute__((aligned(16))) char As[4][16 * PITCH];
+  __shared__ __attribute__((aligned(16))) char Bs[2][COLS * PITCH];
+  __shared__ uint32_t ent[32 * kPlanRows];  // K <= 32 items per block
+
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int m = lane & 15, g = lane >> 4;
+  const int col0 = blockIdx.y * COLS;
+  const int64_t G = gridDim.x, wg = blockIdx.x;
+  // persistent: the blocks, longest first, are dealt to the workgroups in
+  // boustrophedon order (0 .. G-1, G-1 .. 0, ...)
+  for (int64_t idx = wg, round = 0; idx < n_blocks; ++round, idx = round * G + ((round & 1) ? G - 1 - wg : wg)) {
+    __syncthreads();  // the previous block's LDS is free
+    conv_rows_block<T, WB, NB, D>(X, x_bytes, B, b_bytes, perm, b_first, items, b_order[idx], K, mirror, kdim,
+                                  ncols, Y, As, Bs, ent, tid, wave, lane, m, g, col0);
   }
 }
 
@@ -1278,8 +1301,13 @@ static sscn_status launch_rows_nb(const T* X, const T* B, const View& v, int kdi
   const int gy = (ncols + 16 * NB - 1) / (16 * NB);
   const uint32_t xb = (uint32_t)((uint64_t)std::max<int64_t>(v.n_in, 1) * kdim * sizeof(T));
   const uint32_t bb = (uint32_t)((uint64_t)v.K * ncols * kdim * sizeof(T));
-  k_conv_rows<T, WB, NB, 3><<<dim3((unsigned)nb, (unsigned)gy), 256, 0, s>>>(
-      X, xb, B, bb, v.st->perm, v.st->b_first, v.st->items, v.K, v.mirror ? 1 : 0, kdim, ncols, Y);
+  auto kern = k_conv_rows<T, WB, NB, 3>;
+  int cus = 256, per_cu = 1;
+  occupancy((const void*)kern, 256, 0, &per_cu, &cus);
+  // persistent: one resident wave of workgroups per column group
+  const int64_t gx = std::min<int64_t>(nb, std::max<int64_t>(1, (int64_t)cus * per_cu / gy));
+  kern<<<dim3((unsigned)gx, (unsigned)gy), 256, 0, s>>>(X, xb, B, bb, v.st->perm, v.st->b_first, v.st->b_order,
+                                                         v.st->items, nb, v.K, v.mirror ? 1 : 0, kdim, ncols, Y);
   SSCN_HIP(hipGetLastError());
   return SSCN_OK;
 }

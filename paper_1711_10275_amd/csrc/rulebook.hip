@@ -281,6 +281,19 @@ __device__ int64_t block_exclusive_scan(int64_t v, int64_t* wave_tot, int64_t& t
   return wave_tot[wave] + x - v;
 }
 
+// Inclusive prefix sum over the 64 lanes of a wavefront with DPP moves (no
+// LDS round trips): shifts by 1, 2, 4, 8 inside each row of 16 lanes, then
+// the row totals are carried into the following rows.
+__device__ __forceinline__ int wave_inclusive_scan(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, true);  // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, true);  // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, true);  // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, true);  // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false); // row_bcast:15 into rows 1, 3
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false); // row_bcast:31 into rows 2, 3
+  return x;
+}
+
 // seg = exclusive scan of counts (count entries; seg[count] = total).  If
 // stats is not NULL, stats[1 + o] = seg[(o+1) T] - seg[o T] (pairs per
 // offset) for o < K.  One workgroup of kOneBlock threads: each wavefront
@@ -334,19 +347,16 @@ __global__ __launch_bounds__(kOneBlock) void k_scan_one_block(const int64_t* cou
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      int64_t x = v[u];
-#pragma unroll
-      for (int d = 1; d < 64; d <<= 1) {
-        const int64_t y = __shfl_up(x, d, 64);
-        if (lane >= d) x += y;
-      }
+      // an element counts the pairs of one (offset, tile): at most kTile, so
+      // a chunk of 64 fits 32-bit arithmetic
+      const int x = wave_inclusive_scan((int)v[u]);
       const int64_t i = i0 + 64 * u + lane;
       const int64_t ex = carry + x - v[u];
       if (i < hi) {
         seg[i] = ex;
         if (stats && i % n_tiles == 0) bound[i / n_tiles] = ex;
       }
-      carry += __shfl(x, 63, 64);
+      carry += __builtin_amdgcn_readlane(x, 63);
     }
   }
   if (threadIdx.x == 0) {
@@ -770,24 +780,23 @@ __device__ __forceinline__ uint32_t plan_key(uint32_t m, int K) {
 
 // Adds one to counter[key] for every active lane with one atomic per distinct
 // key of the wavefront (offset sets repeat a lot: a plain atomic per row
-// serialises on the common ones); returns the counter's value before this
-// lane's increment.
+// serialises on the common ones) and returns the counter's value before this
+// lane's increment.  Lanes find the lanes with the same key by one ballot
+// per key bit, so all of the wavefront's atomics are issued at once.
 __device__ __forceinline__ int wave_count(int32_t* counter, uint32_t key, bool active) {
   const int lane = threadIdx.x & 63;
-  uint64_t todo = __ballot(active);
-  int res = 0;
-  while (todo) {
-    const int leader = __ffsll((unsigned long long)todo) - 1;
-    const uint32_t k = __shfl(key, leader, 64);
-    const bool mine = active && key == k;
-    const uint64_t peers = __ballot(mine);
-    int base = 0;
-    if (lane == leader) base = atomicAdd(&counter[k], __popcll(peers));
-    base = __shfl(base, leader, 64);
-    if (mine) res = base + __popcll(peers & ((1ull << lane) - 1ull));
-    todo &= ~peers;
+  uint64_t peers = __ballot(active);
+#pragma unroll
+  for (int bit = 0; bit < kPlanKeyBits; ++bit) {
+    const bool set = (key >> bit) & 1u;
+    const uint64_t x = __ballot(set);
+    peers &= set ? x : ~x;
   }
-  return res;
+  const int leader = peers ? __ffsll((unsigned long long)peers) - 1 : lane;
+  int base = 0;
+  if (active && lane == leader) base = atomicAdd(&counter[key], __popcll(peers));
+  base = __shfl(base, leader, 64);
+  return base + __popcll(peers & ((1ull << lane) - 1ull));
 }
 
 __global__ void k_plan_hist(const uint32_t* __restrict__ mask, int64_t n, int K, int32_t* __restrict__ hist) {
@@ -863,6 +872,28 @@ __global__ void k_plan_pairs(const int64_t* __restrict__ seg, int64_t n_tiles, c
   items[item * kPlanRows + pos % kPlanRows] = (uint32_t)in_rows[p] | ((uint32_t)o << kPlanRowBits);
 }
 
+// Blocks by decreasing item count (a counting sort over the K + 1 possible
+// counts in one workgroup; the order inside one count is arbitrary), so
+// that workgroups take the longest blocks first.
+__global__ __launch_bounds__(kOneBlock) void k_plan_order(const int32_t* __restrict__ b_first, int64_t nb, int K,
+                                                          int32_t* __restrict__ order) {
+  __shared__ int32_t hist[33], cur[33];
+  if (threadIdx.x < 33) hist[threadIdx.x] = 0;
+  __syncthreads();
+  for (int64_t b = threadIdx.x; b < nb; b += blockDim.x) atomicAdd(&hist[K - (b_first[b + 1] - b_first[b])], 1);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int run = 0;
+    for (int c = 0; c <= K; ++c) {
+      cur[c] = run;
+      run += hist[c];
+    }
+  }
+  __syncthreads();
+  for (int64_t b = threadIdx.x; b < nb; b += blockDim.x)
+    order[atomicAdd(&cur[K - (b_first[b + 1] - b_first[b])], 1)] = (int32_t)b;
+}
+
 // Row-block plan of one direction (seg and pair arrays complete), in the
 // rule book's own blocks.
 static sscn_status build_plan(RulebookData* d, Storage& st, int64_t n_rows, int K, hipStream_t s) {
@@ -872,6 +903,7 @@ static sscn_status build_plan(RulebookData* d, Storage& st, int64_t n_rows, int 
   Arena a;
   a.add(&st.perm, (size_t)nb * kPlanRows);
   a.add(&st.b_first, (size_t)nb + 1);
+  a.add(&st.b_order, (size_t)nb);
   a.add(&st.items, (size_t)cap * kPlanRows);
   SSCN_TRY(owned_alloc(d, a, s));
   if (nb == 0) return fill_i32(st.b_first, 0, 1, s);
@@ -901,6 +933,8 @@ static sscn_status build_plan(RulebookData* d, Storage& st, int64_t n_rows, int 
   k_plan_blocks<<<grid_for(nb * 64, 256), 256, 0, s>>>(mask, st.perm, n_rows, nb, bmask, st.b_first);
   SSCN_HIP(hipGetLastError());
   SSCN_TRY(exclusive_scan_i32(st.b_first, st.b_first, nb, s));
+  k_plan_order<<<1, kOneBlock, 0, s>>>(st.b_first, nb, K, st.b_order);
+  SSCN_HIP(hipGetLastError());
   k_plan_items<<<grid_for(nb * kPlanRows, 256), 256, 0, s>>>(bmask, st.b_first, nb, st.items);
   SSCN_HIP(hipGetLastError());
   if (max_ppo > 0) {
