@@ -576,18 +576,41 @@ __device__ __forceinline__ void conv_rows_block(
       b_base[q] = (b_col[q] < COLS && col < ncols) ? (uint32_t)col * row_bytes : kOobOffset;
     }
 
+    // items for which this wavefront's 16 rows have at least one pair (bit
+    // per item, wavefront-uniform): lane l tests item l / 16 + 4 q, row l % 16
+    uint32_t have = 0;
+    {
+      uint32_t e[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) e[q] = ent[min((lane >> 4) + 4 * q, n_items - 1) * kPlanRows + wave * 16 + m];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const uint64_t bits = __ballot((e[q] & kPlanNoRow) != kPlanNoRow);
+#pragma unroll
+        for (int h = 0; h < 4; ++h)
+          if ((bits >> (16 * h)) & 0xffffull) have |= 1u << (4 * q + h);
+      }
+    }
+
     uint4 ga[D][NA], gb[D][NBP];  // global loads in flight
     int ld_item = 0, ld_ks = 0, ld_step = 0;
+    // entries of the next step to be issued, read one step ahead
+    uint32_t nx_e0, nx_r[NA];
+    auto fetch_ent = [&]() {
+      const int it = min(ld_item, n_items - 1);
+      nx_e0 = ent[it * kPlanRows];
+#pragma unroll
+      for (int i = 0; i < NA; ++i) nx_r[i] = ent[it * kPlanRows + wave * 16 + a_row[i]];
+    };
+    fetch_ent();
     auto issue = [&](int slot) {
       const bool live = ld_step < n_steps;
-      const int it = min(ld_item, n_items - 1);
-      const uint32_t e0 = ent[it * kPlanRows];
-      const int o = (int)((uint32_t)__builtin_amdgcn_readfirstlane((int)e0) >> kPlanRowBits);
+      const int o = (int)((uint32_t)__builtin_amdgcn_readfirstlane((int)nx_e0) >> kPlanRowBits);
       const int ow = mirror ? K - 1 - o : o;
       const uint32_t win = (uint32_t)ld_ks * WB;
 #pragma unroll
       for (int i = 0; i < NA; ++i) {
-        const uint32_t r = ent[it * kPlanRows + wave * 16 + a_row[i]] & kPlanNoRow;
+        const uint32_t r = nx_r[i] & kPlanNoRow;
         const bool ok = live && r != kPlanNoRow && win + a_byte < row_bytes;
         const auto v = __builtin_amdgcn_raw_buffer_load_b128(rx, (int)(ok ? r * row_bytes + win + a_byte : kOobOffset),
                                                              0, 0);
@@ -602,6 +625,7 @@ __device__ __forceinline__ void conv_rows_block(
       }
       if (++ld_ks == ks_n) { ld_ks = 0; ++ld_item; }
       ++ld_step;
+      fetch_ent();
     };
     auto stage = [&](int slot, int buf) {
 #pragma unroll
@@ -614,9 +638,9 @@ __device__ __forceinline__ void conv_rows_block(
     int mul_item = 0, mul_ks = 0;  // item of the step being multiplied
     auto multiply = [&](int buf) {
       // a wavefront whose 16 rows have no pair for the item skips the MFMAs
-      const uint32_t e = ent[mul_item * kPlanRows + wave * 16 + m];
+      const bool skip = ((have >> mul_item) & 1u) == 0;
       if (++mul_ks == ks_n) { mul_ks = 0; ++mul_item; }
-      if (__ballot((e & kPlanNoRow) != kPlanNoRow) == 0) return;
+      if (skip) return;
       Oct<T> a[S], b[S][NB];
 #pragma unroll
       for (int j = 0; j < S; ++j) {
@@ -668,7 +692,7 @@ __device__ __forceinline__ void conv_rows_block(
 }
 
 template <typename T, int WB, int NB, int D>
-__global__ __launch_bounds__(256) void k_conv_rows(
+__global__ __launch_bounds__(256, 4) void k_conv_rows(
     const T* __restrict__ X, uint32_t x_bytes, const T* __restrict__ B, uint32_t b_bytes,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ b_first, const int32_t* __restrict__ b_order,
     const uint32_t* __restrict__ items, int64_t n_blocks, int K, int mirror, int kdim, int ncols, Heads<T> Y) {

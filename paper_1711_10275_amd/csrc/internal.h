@@ -27,7 +27,7 @@ constexpr int kWave = 64;
 // per wavefront of a workgroup).
 constexpr int kPlanRows = 64;
 // Bits of the key that orders rows by their offset set.
-constexpr int kPlanKeyBits = 17;
+constexpr int kPlanKeyBits = 15;
 // A plan entry packs an input row (kPlanNoRow: none) below the item's offset.
 constexpr int kPlanRowBits = 27;
 constexpr uint32_t kPlanNoRow = (1u << kPlanRowBits) - 1;
@@ -87,6 +87,7 @@ struct Storage {
   // that reach them (rows with similar sets side by side) and cut into
   // blocks of kPlanRows; per block, one item per offset that reaches any of
   // its rows, holding each row's input row for that offset (-1 if none).
+  uint32_t* row_mask = nullptr;  // n_rows when the build provides it: offsets reaching each output row
   int64_t n_blocks = 0;
   int32_t* perm = nullptr;       // kPlanRows * n_blocks: output row at each position, -1 past the end
   int32_t* b_first = nullptr;    // n_blocks + 1: first item of each block

@@ -199,17 +199,20 @@ __global__ __launch_bounds__(256) void k_count_nbr(const int32_t* __restrict__ n
 }
 
 // Write every present entry at its segment start + its rank among the
-// wavefront's present entries (so segments are sorted by output row).
+// wavefront's present entries (so segments are sorted by output row).  With
+// row_mask (K <= 32), also the set of offsets present for each row.
 __global__ __launch_bounds__(256) void k_compact(const int32_t* __restrict__ nbr, int64_t n_rows, int K,
                                                  const int64_t* __restrict__ seg, int64_t n_tiles,
                                                  int32_t* __restrict__ in_rows,
-                                                 int32_t* __restrict__ out_rows) {
+                                                 int32_t* __restrict__ out_rows,
+                                                 uint32_t* __restrict__ row_mask) {
   const int lane = threadIdx.x & 63;
   const int64_t t = (int64_t)blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6);
   if (t >= n_tiles) return;
   const int64_t k = t * kTile + lane;
   const bool valid = k < n_rows;
   const unsigned long long below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  uint32_t present = 0;
   for (int o = 0; o < K; ++o) {
     const int32_t row = valid ? nbr[(int64_t)o * n_rows + k] : -1;
     const unsigned long long m = __ballot(row >= 0);
@@ -217,8 +220,10 @@ __global__ __launch_bounds__(256) void k_compact(const int32_t* __restrict__ nbr
       const int64_t pos = seg[(int64_t)o * n_tiles + t] + __popcll(m & below);
       in_rows[pos] = row;
       out_rows[pos] = (int32_t)k;
+      present |= 1u << (o & 31);
     }
   }
+  if (row_mask && valid) row_mask[k] = present;
 }
 
 // ------------------------------------------------------------- tile order
@@ -366,6 +371,88 @@ __global__ __launch_bounds__(kOneBlock) void k_scan_one_block(const int64_t* cou
   __syncthreads();
   if (stats)
     for (int o = threadIdx.x; o < K; o += blockDim.x) stats[1 + o] = (unsigned long long)(bound[o + 1] - bound[o]);
+}
+
+// The same scan with the whole array in registers (each element counts the
+// pairs of one (offset, tile): at most kTile, so 32-bit arithmetic inside a
+// wavefront): wavefront w holds chunks of 64 elements [64 C w, 64 C (w + 1)),
+// loaded coalesced in one round trip; one pass gives the wavefront totals,
+// a second scans the chunks with DPP.  count <= 16 * 64 * C.
+template <int C>
+__global__ __launch_bounds__(kOneBlock) void k_scan_seg_regs(const int64_t* counts,  // may alias seg
+                                                             int64_t* seg, int64_t count, int64_t n_tiles, int K,
+                                                             unsigned long long* __restrict__ stats) {
+  constexpr int NW = kOneBlock / 64;
+  __shared__ int64_t wsum[NW + 1];
+  extern __shared__ int64_t bound[];  // K + 1 entries: seg[o T]
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int64_t base = (int64_t)wave * 64 * C;
+  // low words through a buffer resource: one lane offset, the chunk in the
+  // scalar offset; elements past the end read zero
+  const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<int64_t*>(counts), (short)0, (int)(count * sizeof(int64_t)), 0x00020000);
+  const int voff = (int)((base + lane) * sizeof(int64_t));
+  int v[C], tot = 0;
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    v[c] = __builtin_amdgcn_raw_buffer_load_b32(rc, voff, c * 64 * (int)sizeof(int64_t), 0);
+    tot += v[c];
+  }
+  const int wtot = __builtin_amdgcn_readlane(wave_inclusive_scan(tot), 63);
+  if (lane == 0) wsum[wave] = wtot;
+  __syncthreads();
+  if (t == 0) {
+    int64_t run = 0;
+    for (int w = 0; w < NW; ++w) {
+      const int64_t x = wsum[w];
+      wsum[w] = run;
+      run += x;
+    }
+    wsum[NW] = run;
+  }
+  __syncthreads();
+  int64_t carry = wsum[wave];
+  // i mod T and i / T, advanced by 64 per chunk (no division in the loop);
+  // an empty rule book has no tiles
+  const int64_t T = n_tiles > 0 ? n_tiles : 1;
+  int64_t rem = (base + lane) % T, quo = (base + lane) / T;
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    const int x = wave_inclusive_scan(v[c]);
+    const int64_t i = base + 64 * c + lane;
+    const int64_t ex = carry + x - v[c];
+    if (i < count) {
+      seg[i] = ex;
+      if (stats && rem == 0) bound[quo] = ex;
+    }
+    carry += __builtin_amdgcn_readlane(x, 63);
+    rem += 64;
+    while (rem >= T) {
+      rem -= T;
+      ++quo;
+    }
+  }
+  if (t == 0) {
+    seg[count] = wsum[NW];
+    if (stats) bound[K] = wsum[NW];
+  }
+  __syncthreads();
+  if (stats)
+    for (int o = t; o < K; o += blockDim.x) stats[1 + o] = (unsigned long long)(bound[o + 1] - bound[o]);
+}
+
+// seg from counts in one launch where that fits (see k_scan_one_block).
+static void launch_seg_scan_one(const int64_t* counts, int64_t* seg, int64_t count, int64_t n_tiles, int K,
+                                unsigned long long* stats, hipStream_t s) {
+  const size_t lds = sizeof(int64_t) * (K + 1);
+  if (count <= 16 * 64 * 32)
+    k_scan_seg_regs<32><<<1, kOneBlock, lds, s>>>(counts, seg, count, n_tiles, K, stats);
+  else if (count <= 16 * 64 * 48)
+    k_scan_seg_regs<48><<<1, kOneBlock, lds, s>>>(counts, seg, count, n_tiles, K, stats);
+  else if (count <= 16 * 64 * 96)
+    k_scan_seg_regs<96><<<1, kOneBlock, lds, s>>>(counts, seg, count, n_tiles, K, stats);
+  else
+    k_scan_one_block<<<1, kOneBlock, lds, s>>>(counts, seg, count, n_tiles, K, stats);
 }
 
 // The tile order (see build_tile_order) in one workgroup: keys from the
@@ -654,15 +741,14 @@ static sscn_status launch_fill_slots(Slot* t, uint64_t cap, int32_t row_init, hi
 // Segment table and pair arrays of one direction from an offset-major
 // neighbour map (st.seg, st.in_rows and st.out_rows already allocated).
 static sscn_status compact_storage(const int32_t* nbr, int64_t n_rows, int K, Storage& st, hipStream_t s,
-                                   bool counted) {
+                                   bool counted, uint32_t* row_mask = nullptr) {
   if (!counted && st.n_tiles > 0) {
     k_count_nbr<<<grid_for(st.n_tiles * 64, 256), 256, 0, s>>>(nbr, n_rows, K, st.seg, st.n_tiles);
     SSCN_HIP(hipGetLastError());
   }
   if (!counted) {
     if (K * st.n_tiles <= kOneBlockScanMax) {
-      k_scan_one_block<<<1, kOneBlock, sizeof(int64_t), s>>>(st.seg, st.seg, K * st.n_tiles, std::max<int64_t>(st.n_tiles, 1),
-                                                              K, nullptr);
+      launch_seg_scan_one(st.seg, st.seg, K * st.n_tiles, std::max<int64_t>(st.n_tiles, 1), K, nullptr, s);
       SSCN_HIP(hipGetLastError());
     } else {
       SSCN_TRY(exclusive_scan_i64(st.seg, st.seg, K * st.n_tiles, s));
@@ -670,7 +756,7 @@ static sscn_status compact_storage(const int32_t* nbr, int64_t n_rows, int K, St
   }
   if (st.n_tiles > 0) {
     k_compact<<<grid_for(st.n_tiles * 64, 256), 256, 0, s>>>(nbr, n_rows, K, st.seg, st.n_tiles, st.in_rows,
-                                                             st.out_rows);
+                                                             st.out_rows, K <= 32 ? row_mask : nullptr);
     SSCN_HIP(hipGetLastError());
   }
   return SSCN_OK;
@@ -762,14 +848,14 @@ __global__ void k_plan_mask(const int64_t* __restrict__ seg, int64_t n_tiles,
 }
 
 // Sort key of an offset set: the set itself when it has at most
-// kPlanKeyBits offsets; for 3^3 filters the 12 edge neighbours and 5 of the
+// kPlanKeyBits offsets; for 3^3 filters the 12 edge neighbours and 3 of the
 // 6 face neighbours (o = 9 i0 + 3 i1 + i2; the centre is in nearly every
 // set and the corners vary least between neighbouring surface sites);
 // otherwise the highest kPlanKeyBits offsets.
 __device__ __forceinline__ uint32_t plan_key(uint32_t m, int K) {
   if (K <= kPlanKeyBits) return m;
   if (K == 27) {
-    constexpr int sel[kPlanKeyBits] = {1, 3, 5, 7, 9, 11, 15, 17, 19, 21, 23, 25, 10, 12, 14, 16, 22};
+    constexpr int sel[kPlanKeyBits] = {1, 3, 5, 7, 9, 11, 15, 17, 19, 21, 23, 25, 10, 12, 14};
     uint32_t k = 0;
 #pragma unroll
     for (int i = 0; i < kPlanKeyBits; ++i) k = (k << 1) | ((m >> sel[i]) & 1u);
@@ -872,6 +958,56 @@ __global__ void k_plan_pairs(const int64_t* __restrict__ seg, int64_t n_tiles, c
   items[item * kPlanRows + pos % kPlanRows] = (uint32_t)in_rows[p] | ((uint32_t)o << kPlanRowBits);
 }
 
+// Exclusive scan of at most kSmallScanMax int32 values in one launch (out
+// may alias in; out[count] = total).  Wavefront w holds elements
+// [2048 w, 2048 w + 2048) in registers, loaded in coalesced chunks of 64;
+// one pass gives the wavefront totals, a second scans the chunks with DPP.
+constexpr int kSmallScanMax = kOneBlock * 32;
+__global__ __launch_bounds__(kOneBlock) void k_scan_small(const int32_t* in, int32_t* out, int count) {
+  constexpr int NW = kOneBlock / 64;
+  __shared__ int wsum[NW + 1];
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int base = wave * 2048;
+  int v[32], tot = 0;
+#pragma unroll
+  for (int c = 0; c < 32; ++c) {
+    const int i = base + 64 * c + lane;
+    v[c] = i < count ? in[i] : 0;
+    tot += v[c];
+  }
+  const int wtot = __builtin_amdgcn_readlane(wave_inclusive_scan(tot), 63);
+  if (lane == 0) wsum[wave] = wtot;
+  __syncthreads();
+  if (t == 0) {
+    int run = 0;
+    for (int w = 0; w < NW; ++w) {
+      const int x = wsum[w];
+      wsum[w] = run;
+      run += x;
+    }
+    wsum[NW] = run;
+  }
+  __syncthreads();
+  int carry = wsum[wave];
+#pragma unroll
+  for (int c = 0; c < 32; ++c) {
+    const int x = wave_inclusive_scan(v[c]);
+    const int i = base + 64 * c + lane;
+    if (i < count) out[i] = carry + x - v[c];
+    carry += __builtin_amdgcn_readlane(x, 63);
+  }
+  if (t == 0) out[count] = wsum[NW];
+}
+
+static sscn_status scan_i32(int32_t* p, int64_t count, hipStream_t s) {
+  if (count <= kSmallScanMax) {
+    k_scan_small<<<1, kOneBlock, 0, s>>>(p, p, (int)count);
+    SSCN_HIP(hipGetLastError());
+    return SSCN_OK;
+  }
+  return exclusive_scan_i32(p, p, count, s);
+}
+
 // Blocks by decreasing item count (a counting sort over the K + 1 possible
 // counts in one workgroup; the order inside one count is arbitrary), so
 // that workgroups take the longest blocks first.
@@ -909,30 +1045,33 @@ static sscn_status build_plan(RulebookData* d, Storage& st, int64_t n_rows, int 
   if (nb == 0) return fill_i32(st.b_first, 0, 1, s);
   const int bins = 1 << std::min(K, kPlanKeyBits);
   Temps tmp(s);
-  uint32_t* mask; uint32_t* bmask; int32_t* hist; int32_t* pos_of;
+  uint32_t* mask = st.row_mask; uint32_t* bmask; int32_t* hist; int32_t* pos_of;
   Arena t;
-  t.add(&mask, (size_t)n_rows);
-  t.add(&bmask, (size_t)nb);
   t.add(&hist, (size_t)bins + 1);
+  if (!mask) t.add(&mask, (size_t)n_rows);  // right after hist: one fill clears both
+  t.add(&bmask, (size_t)nb);
   t.add(&pos_of, (size_t)n_rows);
   SSCN_TRY(tmp.alloc(t));
-  SSCN_TRY(fill_i32((int32_t*)mask, 0, n_rows, s));
-  SSCN_TRY(fill_i32(hist, 0, bins + 1, s));
   int64_t max_ppo = 0;
   for (int64_t c : d->pairs_per_offset) max_ppo = std::max(max_ppo, c);
-  if (max_ppo > 0) {
-    k_plan_mask<<<dim3((unsigned)ceil_div(max_ppo, 256), (unsigned)K), 256, 0, s>>>(st.seg, st.n_tiles,
-                                                                                    st.out_rows, mask);
-    SSCN_HIP(hipGetLastError());
+  if (st.row_mask) {
+    SSCN_TRY(fill_i32(hist, 0, bins + 1, s));
+  } else {
+    SSCN_TRY(fill_i32(hist, 0, (int32_t*)(mask + n_rows) - hist, s));
+    if (max_ppo > 0) {
+      k_plan_mask<<<dim3((unsigned)ceil_div(max_ppo, 256), (unsigned)K), 256, 0, s>>>(st.seg, st.n_tiles,
+                                                                                      st.out_rows, mask);
+      SSCN_HIP(hipGetLastError());
+    }
   }
   k_plan_hist<<<grid_for(n_rows, 256), 256, 0, s>>>(mask, n_rows, K, hist);
   SSCN_HIP(hipGetLastError());
-  SSCN_TRY(exclusive_scan_i32(hist, hist, bins, s));
+  SSCN_TRY(scan_i32(hist, bins, s));
   k_plan_sort<<<grid_for(n_rows, 256), 256, 0, s>>>(mask, n_rows, K, hist, st.perm, pos_of);
   SSCN_HIP(hipGetLastError());
   k_plan_blocks<<<grid_for(nb * 64, 256), 256, 0, s>>>(mask, st.perm, n_rows, nb, bmask, st.b_first);
   SSCN_HIP(hipGetLastError());
-  SSCN_TRY(exclusive_scan_i32(st.b_first, st.b_first, nb, s));
+  SSCN_TRY(scan_i32(st.b_first, nb, s));
   k_plan_order<<<1, kOneBlock, 0, s>>>(st.b_first, nb, K, st.b_order);
   SSCN_HIP(hipGetLastError());
   k_plan_items<<<grid_for(nb * kPlanRows, 256), 256, 0, s>>>(bmask, st.b_first, nb, st.items);
@@ -1051,8 +1190,8 @@ extern "C" sscn_status ssc_rulebook_build(const int32_t* coords, int64_t n, cons
       SSCN_HIP(hipGetLastError());
     }
     if (K * n_tiles <= kOneBlockScanMax) {
-      k_scan_one_block<<<1, kOneBlock, sizeof(int64_t) * (K + 1), s>>>(counts, d->fwd.seg, K * n_tiles, n_tiles, K,
-                                                                      n > 0 ? stats : nullptr);
+      launch_seg_scan_one(counts, d->fwd.seg, K * n_tiles, std::max<int64_t>(n_tiles, 1), K, n > 0 ? stats : nullptr,
+                          s);
       SSCN_HIP(hipGetLastError());
     } else {
       SSCN_TRY(exclusive_scan_i64(counts, d->fwd.seg, K * n_tiles, s));
@@ -1071,8 +1210,9 @@ extern "C" sscn_status ssc_rulebook_build(const int32_t* coords, int64_t n, cons
       pa.add(&d->fwd.in_rows, cap_pairs);
       pa.add(&d->fwd.out_rows, cap_pairs);
       pa.add(&d->fwd.order, n_tiles);
+      if (K <= 32) pa.add(&d->fwd.row_mask, n);
       SSCN_TRY(owned_alloc(d, pa, s));
-      if (n > 0) SSCN_TRY(compact_storage(nbr, n, K, d->fwd, s, /*counted=*/true));
+      if (n > 0) SSCN_TRY(compact_storage(nbr, n, K, d->fwd, s, /*counted=*/true, d->fwd.row_mask));
       return build_tile_order(d->fwd, K, s);
     };
     if (one_phase) SSCN_TRY(finish((int64_t)K * n));
@@ -1172,6 +1312,10 @@ extern "C" sscn_status sc_rulebook_build(const int32_t* coords, int64_t n, const
     oa.add(&d->bwd.out_rows, total);
     oa.add(&d->fwd.order, d->fwd.n_tiles);
     oa.add(&d->bwd.order, d->bwd.n_tiles);
+    if (K <= 32 && n > 0) {
+      oa.add(&d->fwd.row_mask, n_out);
+      oa.add(&d->bwd.row_mask, n);
+    }
     SSCN_TRY(owned_alloc(d, oa, s));
     if (n > 0) {
       int32_t* nbr_out; int32_t* nbr_in;
@@ -1184,8 +1328,8 @@ extern "C" sscn_status sc_rulebook_build(const int32_t* coords, int64_t n, const
       k_sc_assign<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, rank, n_out,
                                                    nbr_out, nbr_in, (int4*)d->out_coords);
       SSCN_HIP(hipGetLastError());
-      SSCN_TRY(compact_storage(nbr_out, n_out, K, d->fwd, s, false));
-      SSCN_TRY(compact_storage(nbr_in, n, K, d->bwd, s, false));
+      SSCN_TRY(compact_storage(nbr_out, n_out, K, d->fwd, s, false, d->fwd.row_mask));
+      SSCN_TRY(compact_storage(nbr_in, n, K, d->bwd, s, false, d->bwd.row_mask));
       SSCN_TRY(build_tile_order(d->fwd, K, s));
       SSCN_TRY(build_tile_order(d->bwd, K, s));
     } else {
