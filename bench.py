@@ -15,12 +15,14 @@ the multiply-adds of real pairs (2 C_in C_out per pair, Table 2), the
 roofline of the dominant kernel and the CPU oracle timed on a bounded
 sample of the same workload on the host cores.
 
-Dominant kernel: k_conv_quad, which runs the forward and the dgrad of the
-layer (same pairs, same channel counts).  Its duration is measured with HIP
-events around the dgrad call, which is exactly one launch of it on the
-current stream.  `traffic` (HBM bytes per launch) comes from the committed
-counter record in profiles/, and is null when the kernel source has changed
-since those counters were taken.
+Dominant kernel: k_conv_rows, which runs the forward and the dgrad of the
+layer (same pairs, same channel counts) over the rule book's row-block
+plan.  Its duration is measured with HIP events around the dgrad call,
+which is exactly one launch of it on the current stream (the plan is built
+once per rule book, on its first use; its cost is in every step and is
+reported as plan_build_ms).  `traffic` (HBM bytes per launch) comes from the
+committed counter record in profiles/, and is null when the kernel source
+has changed since those counters were taken.
 
 --copy-calibration runs a plain device copy of known size (256 MiB) so
 that a counter run can scale FETCH_SIZE / WRITE_SIZE by what they read for
@@ -45,7 +47,7 @@ PEAK_BF16_MFMA_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 METRIC = "SSC 3^3 layer active-sites/s + effective TFLOP/s; rulebook build ms"
 KERNEL_SRC = os.path.join(ROOT, "paper_1711_10275_amd", "csrc", "conv.hip")
-TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "k_conv_quad_ssc128_c64_traffic.json")
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "k_conv_rows_ssc128_c64_traffic.json")
 
 
 def kernel_source_hash():
@@ -236,6 +238,13 @@ def main():
         return e0.elapsed_time(e1) / reps
 
     fwd_ms = timed(lambda: sscn.sparse_conv_forward(tX, tW, rb))
+    # a fresh rule book's first forward also builds its row-block plan
+    torch.cuda.synchronize()
+    tb = time.perf_counter()
+    for _ in range(reps):
+        sscn.sparse_conv_forward(tX, tW, sscn.ssc_rulebook_build(tc, size, 3))
+    torch.cuda.synchronize()
+    build_fwd_ms = (time.perf_counter() - tb) * 1e3 / reps
     dgrad_ms = timed(lambda: sscn.sparse_conv_backward(None, tW, tG, rb, dgrad=True, wgrad=False))
     if args.copy_calibration:
         src = torch.empty(64 << 20, dtype=torch.float32, device=dev)
@@ -266,6 +275,7 @@ def main():
                    "step": "rule-book build + forward + backward (dgrad + wgrad)"},
         "effective_tflops_step": 3 * flops_layer / (ms_step * 1e-3) / 1e12,
         "rulebook_build_ms": build_ms,
+        "plan_build_ms": build_fwd_ms - build_ms - fwd_ms,
         "forward_ms": fwd_ms,
         "forward_tflops": flops_layer / (fwd_ms * 1e-3) / 1e12,
         "forward_sites_per_s": n / (fwd_ms * 1e-3),
@@ -273,7 +283,7 @@ def main():
         "wgrad_ms": wgrad_ms,
         "forward_bf16_ms": fwd_bf16_ms,
         "forward_bf16_tflops": flops_layer / (fwd_bf16_ms * 1e-3) / 1e12,
-        "roofline": {"kernel": "k_conv_quad<float> (forward/dgrad main kernel; timed on the dgrad call)",
+        "roofline": {"kernel": "k_conv_rows<float, 128, 4, 3> (forward/dgrad main kernel; timed on the dgrad call)",
                      "bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_MFMA_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_FP32_MFMA_TFLOPS,
                      "launch_ms": dgrad_ms, "flops_per_launch": flops_layer,
