@@ -241,3 +241,41 @@ def test_forward_heads_rejects_bad_heads():
         sscn.sparse_conv_forward_heads(X, W, rb, [(out[:, :4], None, None)])
     with pytest.raises(ValueError):
         sscn.sparse_conv_forward_heads(X, W, rb, [(out, None, None)] * 3)
+
+
+@pytest.mark.parametrize("f,s", [(2, 2), (3, 2), (1, 2)])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_sc_and_dc_row_blocks(f, s, dtype):
+    """SC / DC with channel counts the row-block kernel takes (multiples of
+    8): forward and backward of both directions.  With f = 1, s = 2 the SC
+    inputs at odd positions reach no output, so the DC direction has output
+    rows without any pair (they must come out zero)."""
+    size = (8, 8, 8) if (f, s) == (2, 2) else (9, 9, 9)
+    c = small_set(60 + 3 * f + s, size, batch=2, density=0.3)
+    rb = sscn.sc_rulebook_build(dev(c), size, f, s)
+    orb = O.sc_rulebook(c, size, f, s)
+    for view, oview, (cin, cout) in ((rb, orb, (16, 24)), (rb.transpose(), O.transpose(orb), (24, 40))):
+        X, W = _draw(view.n_in, cin, cout, f ** 3, 9, dtype)
+        assert_close(_fwd(view, X, W, dtype), O.forward(X, W, oview), dtype, "forward")
+        G = S.features(view.n_out, cout, S.SEED_GRAD + 9, bf16=dtype == "bf16")
+        dx, dw = sscn.sparse_conv_backward(dev(X, TD[dtype]), dev(W, TD[dtype]), dev(G, TD[dtype]), view)
+        rdx, rdw = O.backward(X, W, G, oview)
+        assert_close(host(dx), rdx, dtype, "dgrad")
+        assert_close(host(dw), rdw, dtype, "wgrad")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_ssc_filter5(dtype):
+    """SSC 5^3 (125 offsets: more than the row-block plan takes, so the
+    chunk kernels run) forward and backward."""
+    size = (9, 8, 10)
+    c = small_set(71, size, batch=2, density=0.2)
+    rb = sscn.ssc_rulebook_build(dev(c), size, 5)
+    orb = O.ssc_rulebook(c, size, 5)
+    X, W = _draw(c.shape[0], 16, 24, 125, 10, dtype)
+    assert_close(_fwd(rb, X, W, dtype), O.forward(X, W, orb), dtype, "forward")
+    G = S.features(c.shape[0], 24, S.SEED_GRAD + 10, bf16=dtype == "bf16")
+    dx, dw = sscn.sparse_conv_backward(dev(X, TD[dtype]), dev(W, TD[dtype]), dev(G, TD[dtype]), rb)
+    rdx, rdw = O.backward(X, W, G, orb)
+    assert_close(host(dx), rdx, dtype, "dgrad")
+    assert_close(host(dw), rdw, dtype, "wgrad")
