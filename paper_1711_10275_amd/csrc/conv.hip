@@ -1487,6 +1487,9 @@ __global__ __launch_bounds__(256) void k_wgrad_ring(const T* __restrict__ X, uin
           fetch_rows(b0 + nx, 0, nx, ds);
         else
           fetch_rows(b0 + nx, 1, nx - 16, ds);
+        // keep this step's row loads here: the compiler otherwise sinks them
+        // towards their use R steps later, which empties the ring
+        __builtin_amdgcn_sched_barrier(0);
       }
       bi_in[0] = bi_in[1]; bi_out[0] = bi_out[1];
       bi_in[1] = bi_in[2]; bi_out[1] = bi_out[2];

@@ -133,15 +133,21 @@ __global__ __launch_bounds__(256) void k_ssc_probe(
     const Slot* __restrict__ table, uint64_t mask, int32_t* __restrict__ nbr, int64_t* __restrict__ counts,
     int64_t n_tiles) {
   const int lane = threadIdx.x & 63;
-  const int64_t t = (int64_t)blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6);
+  const int plane = f * f, K = f * f * f;
+  // Workgroup = 4 tiles x one slice of P offsets.  Logical order: tile
+  // groups major, slices minor, and each XCD takes a contiguous run of it,
+  // so the lookups that the slices of neighbouring sites share stay in that
+  // XCD's L2.
+  const int slices = (K + P - 1) / P;
+  const int64_t lb = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t t = (lb / slices) * (blockDim.x / 64) + (threadIdx.x >> 6);
   if (t >= n_tiles) return;  // uniform per wavefront
   const int64_t k = t * kTile + lane;
   const bool valid = k < n;
   const int4 c = valid ? coords[k] : make_int4(0, 0, 0, 0);
   const bool site_ok = valid && (unsigned)c.x < (unsigned)kMaxBatch && in_grid(c.y, c.z, c.w, L0, L1, L2);
   const int h = (f - 1) / 2;
-  const int plane = f * f, K = f * f * f;
-  const int o0 = (int)blockIdx.y * P;
+  const int o0 = (int)(lb % slices) * P;
   uint64_t key[P];
   uint64_t slot[P];
   bool live[P];
@@ -213,8 +219,18 @@ __global__ __launch_bounds__(256) void k_compact(const int32_t* __restrict__ nbr
   const bool valid = k < n_rows;
   const unsigned long long below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   uint32_t present = 0;
+  // the rows of up to 8 offsets are requested together (one round trip per 8)
+  constexpr int B = 8;
+  int32_t rows[B];
   for (int o = 0; o < K; ++o) {
-    const int32_t row = valid ? nbr[(int64_t)o * n_rows + k] : -1;
+    if (o % B == 0) {
+#pragma unroll
+      for (int q = 0; q < B; ++q) rows[q] = (valid && o + q < K) ? nbr[(int64_t)(o + q) * n_rows + k] : -1;
+    }
+    int32_t row = rows[0];
+#pragma unroll
+    for (int q = 1; q < B; ++q)
+      if (o % B == q) row = rows[q];
     const unsigned long long m = __ballot(row >= 0);
     if (row >= 0) {
       const int64_t pos = seg[(int64_t)o * n_tiles + t] + __popcll(m & below);
@@ -457,7 +473,9 @@ static void launch_seg_scan_one(const int64_t* counts, int64_t* seg, int64_t cou
 
 // The tile order (see build_tile_order) in one workgroup: keys from the
 // chunk counts (kept in LDS), then a counting sort in LDS.
-constexpr int64_t kOneBlockOrderMax = 1 << 15;    // tiles (16-bit keys in LDS)
+// (one workgroup reads K seg entries per tile: beyond a few thousand tiles
+// the multi-workgroup passes are faster)
+constexpr int64_t kOneBlockOrderMax = 1 << 12;    // tiles
 __global__ __launch_bounds__(kOneBlock) void k_tile_order_one_block(const int64_t* __restrict__ seg,
                                                                     int64_t n_tiles, int K, int max_key,
                                                                     int32_t* __restrict__ order) {
@@ -1185,7 +1203,7 @@ extern "C" sscn_status ssc_rulebook_build(const int32_t* coords, int64_t n, cons
                                                (int4*)d->out_coords);
       SSCN_HIP(hipGetLastError());
       constexpr int P = 3;  // lookups per wavefront
-      k_ssc_probe<P><<<dim3(grid_for(n_tiles * 64, 256), (unsigned)ceil_div(K, P)), 256, 0, s>>>(
+      k_ssc_probe<P><<<(unsigned)(grid_for(n_tiles * 64, 256) * ceil_div(K, P)), 256, 0, s>>>(
           (const int4*)coords, n, L0, L1, L2, f, table, cap - 1, nbr, counts, n_tiles);
       SSCN_HIP(hipGetLastError());
     }
