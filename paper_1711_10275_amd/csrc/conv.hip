@@ -520,13 +520,15 @@ __global__ __launch_bounds__(256) void k_conv_quad(
 // block.  B is laid out [o][ncols][kdim] (a contiguous row of reduction
 // channels per output column).  Global loads run D - 1 steps ahead in
 // registers; the weight tile is double-buffered in LDS with one barrier per
-// step; each wavefront's row tile is private to it.
+// step; each wavefront's row tile is private to it.  The plan entries are
+// read from global memory (L2) a step ahead of their use, which keeps the
+// LDS footprint at 27 KB (five workgroups per CU).
 template <typename T, int WB, int NB, int D>
 __device__ __forceinline__ void conv_rows_block(
     const T* __restrict__ X, uint32_t x_bytes, const T* __restrict__ B, uint32_t b_bytes,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ b_first, const uint32_t* __restrict__ items,
     int64_t blk, int K, int mirror, int kdim, int ncols, const Heads<T>& Y, char (*As)[16 * (WB + 16)],
-    char (*Bs)[16 * NB * (WB + 16)], uint32_t* ent, int tid, int wave, int lane, int m, int g, int col0) {
+    char (*Bs)[16 * NB * (WB + 16)], int tid, int wave, int lane, int m, int g, int col0) {
   constexpr int LPR = WB / 16;              // lanes per row window
   constexpr int RPI = 64 / LPR;             // rows per wavefront load
   constexpr int NA = 16 / RPI;              // row loads per wavefront and step
@@ -547,18 +549,7 @@ __device__ __forceinline__ void conv_rows_block(
   for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   if (n_steps > 0) {
-    {
-      // all of the block's entries in one round trip
-      const int n_ent = n_items * kPlanRows;
-      const uint32_t* src = items + (int64_t)first * kPlanRows;
-      uint32_t t[32 * kPlanRows / 256];
-#pragma unroll
-      for (int q = 0; q < 32 * kPlanRows / 256; ++q) t[q] = src[min(tid + 256 * q, n_ent - 1)];
-#pragma unroll
-      for (int q = 0; q < 32 * kPlanRows / 256; ++q)
-        if (tid + 256 * q < n_ent) ent[tid + 256 * q] = t[q];
-    }
-    __syncthreads();
+    const uint32_t* ents = items + (int64_t)first * kPlanRows;  // the block's entries
 
     // lane constants of the coalesced loads
     const uint32_t a_byte = (uint32_t)(lane % LPR) * 16;  // within the window
@@ -582,7 +573,7 @@ __device__ __forceinline__ void conv_rows_block(
     {
       uint32_t e[8];
 #pragma unroll
-      for (int q = 0; q < 8; ++q) e[q] = ent[min((lane >> 4) + 4 * q, n_items - 1) * kPlanRows + wave * 16 + m];
+      for (int q = 0; q < 8; ++q) e[q] = ents[min((lane >> 4) + 4 * q, n_items - 1) * kPlanRows + wave * 16 + m];
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
         const uint64_t bits = __ballot((e[q] & kPlanNoRow) != kPlanNoRow);
@@ -594,18 +585,18 @@ __device__ __forceinline__ void conv_rows_block(
 
     uint4 ga[D][NA], gb[D][NBP];  // global loads in flight
     int ld_item = 0, ld_ks = 0, ld_step = 0;
-    // entries of the next step to be issued, read one step ahead
-    uint32_t nx_e0, nx_r[NA];
+    // entries of the next step to be issued, read one step ahead (every
+    // entry of an item carries the item's offset)
+    uint32_t nx_r[NA];
     auto fetch_ent = [&]() {
       const int it = min(ld_item, n_items - 1);
-      nx_e0 = ent[it * kPlanRows];
 #pragma unroll
-      for (int i = 0; i < NA; ++i) nx_r[i] = ent[it * kPlanRows + wave * 16 + a_row[i]];
+      for (int i = 0; i < NA; ++i) nx_r[i] = ents[it * kPlanRows + wave * 16 + a_row[i]];
     };
     fetch_ent();
     auto issue = [&](int slot) {
       const bool live = ld_step < n_steps;
-      const int o = (int)((uint32_t)__builtin_amdgcn_readfirstlane((int)nx_e0) >> kPlanRowBits);
+      const int o = (int)((uint32_t)__builtin_amdgcn_readfirstlane((int)nx_r[0]) >> kPlanRowBits);
       const int ow = mirror ? K - 1 - o : o;
       const uint32_t win = (uint32_t)ld_ks * WB;
 #pragma unroll
@@ -692,7 +683,7 @@ __device__ __forceinline__ void conv_rows_block(
 }
 
 template <typename T, int WB, int NB, int D>
-__global__ __launch_bounds__(256, 4) void k_conv_rows(
+__global__ __launch_bounds__(256, 5) void k_conv_rows(
     const T* __restrict__ X, uint32_t x_bytes, const T* __restrict__ B, uint32_t b_bytes,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ b_first, const int32_t* __restrict__ b_order,
     const uint32_t* __restrict__ items, int64_t n_blocks, int K, int mirror, int kdim, int ncols, Heads<T> Y) {
@@ -702,7 +693,6 @@ __global__ __launch_bounds__(256, 4) void k_conv_rows(
   static_assert(WB / (32 * (int)sizeof(T)) >= 1 && 16 % RPI == 0, "window");
   __shared__ __attribute__((aligned(16))) char As[4][16 * PITCH];
   __shared__ __attribute__((aligned(16))) char Bs[2][COLS * PITCH];
-  __shared__ uint32_t ent[32 * kPlanRows];  // K <= 32 items per block
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int m = lane & 15, g = lane >> 4;
@@ -710,10 +700,25 @@ __global__ __launch_bounds__(256, 4) void k_conv_rows(
   const int64_t G = gridDim.x, wg = blockIdx.x;
   // persistent: the blocks, longest first, are dealt to the workgroups in
   // boustrophedon order (0 .. G-1, G-1 .. 0, ...)
-  for (int64_t idx = wg, round = 0; idx < n_blocks; ++round, idx = round * G + ((round & 1) ? G - 1 - wg : wg)) {
+  auto next = [&](int64_t round) { return round * G + ((round & 1) ? G - 1 - wg : wg); };
+  {
+    // Workgroups with more than their share of the items issue first (wave
+    // priority), so that the ones that finish last are the ones that started
+    // with the most work.
+    int mine = 0;
+    for (int64_t idx = wg, round = 0; idx < n_blocks; idx = next(++round)) {
+      const int b = b_order[idx];
+      mine += b_first[b + 1] - b_first[b];
+    }
+    const float share = (float)mine * (float)G / (float)max(b_first[n_blocks], 1);
+    if (share > 1.1f) __builtin_amdgcn_s_setprio(3);
+    else if (share > 1.0f) __builtin_amdgcn_s_setprio(2);
+    else if (share > 0.9f) __builtin_amdgcn_s_setprio(1);
+  }
+  for (int64_t idx = wg, round = 0; idx < n_blocks; idx = next(++round)) {
     __syncthreads();  // the previous block's LDS is free
     conv_rows_block<T, WB, NB, D>(X, x_bytes, B, b_bytes, perm, b_first, items, b_order[idx], K, mirror, kdim,
-                                  ncols, Y, As, Bs, ent, tid, wave, lane, m, g, col0);
+                                  ncols, Y, As, Bs, tid, wave, lane, m, g, col0);
   }
 }
 
@@ -1325,7 +1330,8 @@ static sscn_status launch_rows_nb(const T* X, const T* B, const View& v, int kdi
   const int gy = (ncols + 16 * NB - 1) / (16 * NB);
   const uint32_t xb = (uint32_t)((uint64_t)std::max<int64_t>(v.n_in, 1) * kdim * sizeof(T));
   const uint32_t bb = (uint32_t)((uint64_t)v.K * ncols * kdim * sizeof(T));
-  auto kern = k_conv_rows<T, WB, NB, 3>;
+  // loads two steps ahead for 64-byte windows (short steps), one otherwise
+  auto kern = k_conv_rows<T, WB, NB, WB == 64 ? 3 : 2>;
   int cus = 256, per_cu = 1;
   occupancy((const void*)kern, 256, 0, &per_cu, &cus);
   // persistent: one resident wave of workgroups per column group
