@@ -1548,7 +1548,9 @@ static sscn_status launch_wgrad_reg(const T* X, const T* dY, const View& v, int 
   const uint64_t x_bytes = (uint64_t)std::max<int64_t>(v.n_in, 1) * cin * sizeof(T);
   const uint64_t y_bytes = (uint64_t)std::max<int64_t>(v.n_out, 1) * cout * sizeof(T);
   if (x_bytes < kOobOffset && y_bytes < kOobOffset && v.K <= kWgradMaxK) {
-    // sub-items per offset ~ its share of the pairs, about 1536 items in all
+    // sub-items per offset ~ its share of the pairs; about one resident
+    // round of workgroups in all (each item adds its block to dW with
+    // atomics, so fewer, longer items cost less)
     const std::vector<int64_t>& ppo = v.owner->pairs_per_offset;
     const double mean = (double)std::max<int64_t>(v.n_pairs, 1) / v.K;
     WgradItems items{};
@@ -1558,10 +1560,14 @@ static sscn_status launch_wgrad_reg(const T* X, const T* dY, const View& v, int 
       items.first[o + 1] = items.first[o] + std::max(1, (int)(p / mean + 0.5));
     }
     const int S = items.first[v.K];
-    const int64_t tr2 = std::max<int64_t>(1, ceil_div(v.st->n_tiles * S, 1536));
+    auto kern = k_wgrad_ring<T, CA, CB, 4>;
+    int cus = 256, per_cu = 1;
+    occupancy((const void*)kern, 256, 0, &per_cu, &cus);
+    const int64_t target = std::max<int64_t>(1, (int64_t)cus * per_cu / (nzc * nzo));
+    const int64_t tr2 = std::max<int64_t>(1, ceil_div(v.st->n_tiles * S, target));
     const int64_t total = ceil_div(v.st->n_tiles, tr2) * S;
     SSCN_TRY(fill_f32(dW, 0.f, (int64_t)v.K * cin * cout, s));
-    k_wgrad_ring<T, CA, CB, 4><<<dim3((unsigned)total, (unsigned)(nzc * nzo)), 256, 0, s>>>(
+    kern<<<dim3((unsigned)total, (unsigned)(nzc * nzo)), 256, 0, s>>>(
         X, (uint32_t)x_bytes, dY, (uint32_t)y_bytes, v.st->seg, v.st->n_tiles, v.st->in_rows, v.st->out_rows, v.K,
         v.mirror ? 1 : 0, cin, cout, (int)tr2, items, nzc, dW);
     SSCN_HIP(hipGetLastError());
