@@ -148,10 +148,19 @@ __global__ __launch_bounds__(256) void k_ssc_probe(
   const bool site_ok = valid && (unsigned)c.x < (unsigned)kMaxBatch && in_grid(c.y, c.z, c.w, L0, L1, L2);
   const int h = (f - 1) / 2;
   const int o0 = (int)(lb % slices) * P;
+  // A lookup reads the whole aligned 64-byte line (4 slots) that holds its
+  // first slot, and the following lines while the probe sequence runs on
+  // (linear probing: stop at the key or at an empty slot), so most lookups
+  // take a single round trip.
   uint64_t key[P];
   uint64_t slot[P];
   bool live[P];
-  Slot v[P];
+  Slot v[P][4];
+  auto read_line = [&](int q) {
+    const uint64_t line = slot[q] & ~3ull;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) v[q][j] = table[line + j];
+  };
 #pragma unroll
   for (int q = 0; q < P; ++q) {
     const int o = o0 + q;
@@ -160,19 +169,31 @@ __global__ __launch_bounds__(256) void k_ssc_probe(
     live[q] = o < K && site_ok && in_grid(y0, y1, y2, L0, L1, L2);
     key[q] = pack_key(c.x, y0, y1, y2);
     slot[q] = mix64(key[q]) & mask;
-    if (live[q]) v[q] = table[slot[q]];
+    if (live[q]) read_line(q);
   }
 #pragma unroll
   for (int q = 0; q < P; ++q) {
     const int o = o0 + q;
     if (o >= K) break;  // uniform
     int32_t row = -1;
-    if (live[q]) {
-      while (v[q].key != key[q] && v[q].key != kEmptyKey) {
-        slot[q] = (slot[q] + 1) & mask;
-        v[q] = table[slot[q]];
+    bool done = !live[q];
+    while (!done) {
+      const int from = (int)(slot[q] & 3);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (!done && j >= from) {
+          if (v[q][j].key == key[q]) {
+            row = v[q][j].row;
+            done = true;
+          } else if (v[q][j].key == kEmptyKey) {
+            done = true;
+          }
+        }
       }
-      if (v[q].key == key[q]) row = v[q].row;
+      if (!done) {
+        slot[q] = ((slot[q] | 3) + 1) & mask;  // first slot of the next line
+        read_line(q);
+      }
     }
     if (valid) nbr[(int64_t)o * n + k] = row;
     const unsigned long long bal = __ballot(row >= 0);
@@ -218,6 +239,14 @@ __global__ __launch_bounds__(256) void k_compact(const int32_t* __restrict__ nbr
   const int64_t k = t * kTile + lane;
   const bool valid = k < n_rows;
   const unsigned long long below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  // the tile's segment starts, offset o in lane o % 64 of word o / 64 (one
+  // round trip instead of one per offset; K <= 128, else read in the loop)
+  const bool seg_regs = K <= 128;
+  int64_t s_lo = 0, s_hi = 0;
+  if (seg_regs) {
+    if (lane < K) s_lo = seg[(int64_t)lane * n_tiles + t];
+    if (lane + 64 < K) s_hi = seg[(int64_t)(lane + 64) * n_tiles + t];
+  }
   uint32_t present = 0;
   // the rows of up to 8 offsets are requested together (one round trip per 8)
   constexpr int B = 8;
@@ -232,8 +261,17 @@ __global__ __launch_bounds__(256) void k_compact(const int32_t* __restrict__ nbr
     for (int q = 1; q < B; ++q)
       if (o % B == q) row = rows[q];
     const unsigned long long m = __ballot(row >= 0);
+    int64_t start;
+    if (seg_regs) {
+      const int64_t w = o < 64 ? s_lo : s_hi;
+      const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)w, o & 63);
+      const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(w >> 32), o & 63);
+      start = (int64_t)(((uint64_t)hi << 32) | lo);
+    } else {
+      start = m ? seg[(int64_t)o * n_tiles + t] : 0;
+    }
     if (row >= 0) {
-      const int64_t pos = seg[(int64_t)o * n_tiles + t] + __popcll(m & below);
+      const int64_t pos = start + __popcll(m & below);
       in_rows[pos] = row;
       out_rows[pos] = (int32_t)k;
       present |= 1u << (o & 31);
@@ -428,10 +466,12 @@ __global__ __launch_bounds__(kOneBlock) void k_scan_seg_regs(const int64_t* coun
   }
   __syncthreads();
   int64_t carry = wsum[wave];
-  // i mod T and i / T, advanced by 64 per chunk (no division in the loop);
-  // an empty rule book has no tiles
-  const int64_t T = n_tiles > 0 ? n_tiles : 1;
-  int64_t rem = (base + lane) % T, quo = (base + lane) / T;
+  // i mod T and i / T, advanced by 64 = q64 T + r64 per chunk with one
+  // compare (a loop here is turned into a 64-bit division per chunk by the
+  // compiler); an empty rule book has no tiles.  count < 2^17, so 32 bits.
+  const uint32_t T = (uint32_t)(n_tiles > 0 ? n_tiles : 1);
+  const uint32_t q64 = 64u / T, r64 = 64u % T;
+  uint32_t rem = (uint32_t)(base + lane) % T, quo = (uint32_t)(base + lane) / T;
 #pragma unroll
   for (int c = 0; c < C; ++c) {
     const int x = wave_inclusive_scan(v[c]);
@@ -442,8 +482,9 @@ __global__ __launch_bounds__(kOneBlock) void k_scan_seg_regs(const int64_t* coun
       if (stats && rem == 0) bound[quo] = ex;
     }
     carry += __builtin_amdgcn_readlane(x, 63);
-    rem += 64;
-    while (rem >= T) {
+    rem += r64;
+    quo += q64;
+    if (rem >= T) {
       rem -= T;
       ++quo;
     }
