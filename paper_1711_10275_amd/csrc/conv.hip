@@ -1147,6 +1147,7 @@ static unsigned persistent_grid(const void* kern, size_t lds, int64_t n_items, i
 template <typename T, int RING, int KB, bool WT, int NB = 2>
 static sscn_status launch_quad(const T* X, uint32_t x_bytes, const T* W, uint32_t w_bytes, const View& v, int cin,
                                int cout, const Heads<T>& Y, hipStream_t s) {
+  SSCN_TRY(ensure_order(v, s));
   const int max_chunks = v.K * (kTile / 16 + 1);
   const QuadLds L(max_chunks, v.K);
   const int groups = (cout + 63) / 64;

@@ -75,6 +75,7 @@ struct Storage {
   int32_t* in_rows = nullptr;    // n_pairs
   int32_t* out_rows = nullptr;   // n_pairs
   int32_t* order = nullptr;      // n_tiles: per tile group (contiguous range), tiles by decreasing work
+  bool order_built = false;      // `order` is filled on first use (ensure_order)
   // The same pairs as a padded chunk table: output rows cut into tiles of
   // kChunkRows rows; within a tile, per offset, the pairs in chunks of 16
   // (the last chunk padded).  Chunks are numbered tile-major, then by offset.
@@ -115,6 +116,7 @@ struct RulebookData {
   std::mutex chunk_mu;
   hipEvent_t chunk_ready = nullptr;
   hipEvent_t plan_ready = nullptr;   // the same for the row-block plans
+  hipEvent_t order_ready = nullptr;  // and for the tile orders
   ~RulebookData();
 };
 
@@ -142,6 +144,8 @@ struct View {
 sscn_status ensure_chunks(const View& v, hipStream_t s);
 // The same for the row-block plan (K <= 32).
 sscn_status ensure_plan(const View& v, hipStream_t s);
+// The same for the tile order of the view's storage.
+sscn_status ensure_order(const View& v, hipStream_t s);
 
 inline View view_of(const sscn_rulebook_s* rb) {
   const RulebookData* d = rb->d;

@@ -498,11 +498,46 @@ __global__ __launch_bounds__(kOneBlock) void k_scan_seg_regs(const int64_t* coun
     for (int o = t; o < K; o += blockDim.x) stats[1 + o] = (unsigned long long)(bound[o + 1] - bound[o]);
 }
 
+// seg from per-(offset, tile) counts (offset-major, K x T, not aliasing
+// seg) with one workgroup per offset: workgroup o first sums the counts of
+// all offsets before it (every workgroup reads them again; they are few and
+// L2-resident), then scans its own T counts from that base.  stats[1 + o]
+// (if not NULL) = pairs of offset o.  Used where K x T is small, so that the
+// whole scan is one launch spread over K CUs.
+__global__ __launch_bounds__(kOneBlock) void k_scan_seg_offsets(const int64_t* __restrict__ counts,
+                                                                int64_t* __restrict__ seg, int64_t T, int K,
+                                                                unsigned long long* __restrict__ stats) {
+  __shared__ int64_t wave_tot[kOneBlock / 64 + 1];
+  const int o = blockIdx.x;
+  const int t = threadIdx.x;
+  const int64_t first = (int64_t)o * T;
+  int64_t part = 0;
+#pragma unroll 8
+  for (int64_t i = t; i < first; i += kOneBlock) part += counts[i];
+  int64_t base;
+  (void)block_exclusive_scan(part, wave_tot, base);
+  int64_t carry = 0;
+  for (int64_t c0 = 0; c0 < T; c0 += kOneBlock) {
+    const int64_t i = c0 + t;
+    const int64_t v = i < T ? counts[first + i] : 0;
+    int64_t total;
+    const int64_t ex = block_exclusive_scan(v, wave_tot, total);
+    if (i < T) seg[first + i] = base + carry + ex;
+    carry += total;
+  }
+  if (t == 0) {
+    if (o == K - 1) seg[(int64_t)K * T] = base + carry;
+    if (stats) stats[1 + o] = (unsigned long long)carry;
+  }
+}
+
 // seg from counts in one launch where that fits (see k_scan_one_block).
 static void launch_seg_scan_one(const int64_t* counts, int64_t* seg, int64_t count, int64_t n_tiles, int K,
                                 unsigned long long* stats, hipStream_t s) {
   const size_t lds = sizeof(int64_t) * (K + 1);
-  if (count <= 16 * 64 * 32)
+  if (counts != seg && K > 1 && count == K * n_tiles)
+    k_scan_seg_offsets<<<K, kOneBlock, 0, s>>>(counts, seg, n_tiles, K, stats);
+  else if (count <= 16 * 64 * 32)
     k_scan_seg_regs<32><<<1, kOneBlock, lds, s>>>(counts, seg, count, n_tiles, K, stats);
   else if (count <= 16 * 64 * 48)
     k_scan_seg_regs<48><<<1, kOneBlock, lds, s>>>(counts, seg, count, n_tiles, K, stats);
@@ -895,6 +930,25 @@ sscn_status ensure_chunks(const View& v, hipStream_t s) {
   return SSCN_OK;
 }
 
+sscn_status ensure_order(const View& v, hipStream_t s) {
+  RulebookData* d = v.owner;
+  Storage& st = v.st == &d->fwd ? d->fwd : d->bwd;
+  {
+    std::lock_guard<std::mutex> lock(d->chunk_mu);
+    if (!st.order_built) {
+      int cur = 0;
+      SSCN_HIP(hipGetDevice(&cur));
+      if (cur != d->device) return fail(SSCN_ERR_INVALID_ARG, "rule book used on another device");
+      SSCN_TRY(build_tile_order(st, d->K, d->stream));
+      if (!d->order_ready) SSCN_HIP(hipEventCreateWithFlags(&d->order_ready, hipEventDisableTiming));
+      SSCN_HIP(hipEventRecord(d->order_ready, d->stream));
+      st.order_built = true;
+    }
+  }
+  if (s != d->stream) SSCN_HIP(hipStreamWaitEvent(s, d->order_ready, 0));
+  return SSCN_OK;
+}
+
 // ------------------------------------------------------ row-block plan
 // Offset set of every output row as a bit mask.  One thread per pair of
 // offset blockIdx.y (pairs of one offset have distinct output rows).
@@ -1272,7 +1326,7 @@ extern "C" sscn_status ssc_rulebook_build(const int32_t* coords, int64_t n, cons
       if (K <= 32) pa.add(&d->fwd.row_mask, n);
       SSCN_TRY(owned_alloc(d, pa, s));
       if (n > 0) SSCN_TRY(compact_storage(nbr, n, K, d->fwd, s, /*counted=*/true, d->fwd.row_mask));
-      return build_tile_order(d->fwd, K, s);
+      return SSCN_OK;
     };
     if (one_phase) SSCN_TRY(finish((int64_t)K * n));
     std::vector<unsigned long long> host(1 + K);
@@ -1389,8 +1443,6 @@ extern "C" sscn_status sc_rulebook_build(const int32_t* coords, int64_t n, const
       SSCN_HIP(hipGetLastError());
       SSCN_TRY(compact_storage(nbr_out, n_out, K, d->fwd, s, false, d->fwd.row_mask));
       SSCN_TRY(compact_storage(nbr_in, n, K, d->bwd, s, false, d->bwd.row_mask));
-      SSCN_TRY(build_tile_order(d->fwd, K, s));
-      SSCN_TRY(build_tile_order(d->bwd, K, s));
     } else {
       SSCN_TRY(exclusive_scan_i64(d->fwd.seg, d->fwd.seg, 0, s));
       SSCN_TRY(exclusive_scan_i64(d->bwd.seg, d->bwd.seg, 0, s));

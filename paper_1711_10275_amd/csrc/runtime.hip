@@ -100,6 +100,7 @@ RulebookData::~RulebookData() {
   for (void* p : blocks) dev_free(p, stream);
   if (chunk_ready) (void)hipEventDestroy(chunk_ready);
   if (plan_ready) (void)hipEventDestroy(plan_ready);
+  if (order_ready) (void)hipEventDestroy(order_ready);
   if (cur != device) (void)hipSetDevice(cur);
 }
 
