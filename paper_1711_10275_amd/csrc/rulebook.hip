@@ -1287,9 +1287,21 @@ extern "C" sscn_status ssc_rulebook_build(const int32_t* coords, int64_t n, cons
     ta.add(&counts, (size_t)K * n_tiles + 1);
     ta.add(&stats, 1 + K);
     SSCN_TRY(tmp.alloc(ta));
+    // Pair storage for the worst case (every offset of every site) when that
+    // is modest: then it shares one allocation with the rest of the rule
+    // book, compaction is queued before the one readback, and the host waits
+    // once.  Otherwise the exact size comes from the readback first.
+    const bool one_phase = (uint64_t)K * (uint64_t)n * 8u <= (512ull << 20);
+    auto add_pairs = [&](Arena& pa, int64_t cap_pairs) {
+      pa.add(&d->fwd.in_rows, cap_pairs);
+      pa.add(&d->fwd.out_rows, cap_pairs);
+      pa.add(&d->fwd.order, n_tiles);
+      if (K <= 32) pa.add(&d->fwd.row_mask, n);
+    };
     Arena oa;  // owned by the rule book, needed before the readback
     oa.add(&d->fwd.seg, (size_t)K * n_tiles + 1);
     oa.add(&d->out_coords, (size_t)4 * n);
+    if (one_phase) add_pairs(oa, (int64_t)K * n);
     SSCN_TRY(owned_alloc(d, oa, s));
 
     SSCN_TRY(launch_fill_slots(table, cap, -1, s, stats, 1 + K));
@@ -1313,29 +1325,23 @@ extern "C" sscn_status ssc_rulebook_build(const int32_t* coords, int64_t n, cons
         SSCN_HIP(hipGetLastError());
       }
     }
-    // Pair storage for the worst case (every offset of every site) when that
-    // is modest: then compaction and the tile order are queued before the
-    // one readback, and the host waits once.  Otherwise the exact size comes
-    // from the readback first.
-    const bool one_phase = (uint64_t)K * (uint64_t)n * 8u <= (512ull << 20);
-    auto finish = [&](int64_t cap_pairs) -> sscn_status {
-      Arena pa;
-      pa.add(&d->fwd.in_rows, cap_pairs);
-      pa.add(&d->fwd.out_rows, cap_pairs);
-      pa.add(&d->fwd.order, n_tiles);
-      if (K <= 32) pa.add(&d->fwd.row_mask, n);
-      SSCN_TRY(owned_alloc(d, pa, s));
+    auto compact = [&]() -> sscn_status {
       if (n > 0) SSCN_TRY(compact_storage(nbr, n, K, d->fwd, s, /*counted=*/true, d->fwd.row_mask));
       return SSCN_OK;
     };
-    if (one_phase) SSCN_TRY(finish((int64_t)K * n));
+    if (one_phase) SSCN_TRY(compact());
     std::vector<unsigned long long> host(1 + K);
     SSCN_TRY(readback(host.data(), stats, sizeof(unsigned long long) * (1 + K), s));
     SSCN_TRY(flags_error(host[0]));
     int64_t total = 0;
     for (int o = 0; o < K; ++o) total += (d->pairs_per_offset[o] = (int64_t)host[1 + o]);
     d->n_pairs = total;
-    if (!one_phase) SSCN_TRY(finish(total));
+    if (!one_phase) {
+      Arena pa;
+      add_pairs(pa, total);
+      SSCN_TRY(owned_alloc(d, pa, s));
+      SSCN_TRY(compact());
+    }
   }
   guard.release();
   return new_handle(d, out);

@@ -43,6 +43,8 @@ class ConvOutput(ctypes.Structure):
 
 
 _lib = None
+# filter_size is at most 8, so a rule book has at most 8^3 offsets
+_MAX_OFFSETS = 512
 _vp, _i32, _i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
 _SIGS = {
     "ssc_rulebook_build": [_vp, _i64, _vp, _i32, _vp, _vp],
@@ -118,16 +120,15 @@ class Rulebook:
         self._h = handle
         self.device = device
         info = RulebookInfo()
-        _check(lib().sscn_rulebook_query(self._h, ctypes.byref(info), None))
-        K = info.n_offsets
-        ppo = (ctypes.c_int64 * K)()
+        ppo = (ctypes.c_int64 * _MAX_OFFSETS)()
         _check(lib().sscn_rulebook_query(self._h, ctypes.byref(info), ppo))
+        K = info.n_offsets
         self.n_in, self.n_out, self.n_pairs = info.n_in, info.n_out, info.n_pairs
         self.filter_size, self.stride = info.filter_size, info.stride
         self.submanifold, self.transposed = bool(info.submanifold), bool(info.transposed)
         self.n_offsets = K
         self.in_size, self.out_size = tuple(info.in_size), tuple(info.out_size)
-        self.pairs_per_offset = list(ppo)
+        self.pairs_per_offset = list(ppo[:K])
 
     @property
     def handle(self):
