@@ -511,9 +511,16 @@ __global__ __launch_bounds__(kOneBlock) void k_scan_seg_offsets(const int64_t* _
   const int o = blockIdx.x;
   const int t = threadIdx.x;
   const int64_t first = (int64_t)o * T;
+  // two counts per 16-byte load, 16 loads in flight per thread
   int64_t part = 0;
-#pragma unroll 8
-  for (int64_t i = t; i < first; i += kOneBlock) part += counts[i];
+  const longlong2* c2 = reinterpret_cast<const longlong2*>(counts);
+  const int64_t n2 = first / 2;
+#pragma unroll 16
+  for (int64_t q = t; q < n2; q += kOneBlock) {
+    const longlong2 v = c2[q];
+    part += v.x + v.y;
+  }
+  if ((first & 1) && t == 0) part += counts[first - 1];
   int64_t base;
   (void)block_exclusive_scan(part, wave_tot, base);
   int64_t carry = 0;
