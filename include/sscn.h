@@ -135,7 +135,11 @@ sscn_status sscn_rulebook_out_coords(sscn_rulebook rb, int32_t* out_coords, hipS
 sscn_status sscn_rulebook_export(sscn_rulebook rb, int32_t* in_rows, int32_t* out_rows,
                                  int32_t* offsets, hipStream_t stream);
 
-/* Release a rule book or view (storage goes when its last view goes). NULL is a no-op. */
+/* Release a rule book or view (storage goes when its last view goes). NULL is a no-op.
+ * The storage returns to the library's device-memory cache, ordered on the
+ * build stream: work on other streams that still reads the rule book must
+ * be ordered before the build stream's later work (or completed) first.
+ * Cached memory goes back to the device when an allocation would fail. */
 void sscn_rulebook_free(sscn_rulebook rb);
 
 /*

@@ -61,8 +61,9 @@ sscn_status hip_fail(hipError_t e, const char* what);
   } while (0)
 
 // ---------------------------------------------------------------- memory
-// Stream-ordered device allocation from the device's default pool (kept
-// cached by the library so repeated builds do not return memory to the OS).
+// Device allocation for work on stream s from the library's block cache: a
+// block freed on s is reused only by later allocations on s (stream order
+// keeps its previous users first); see runtime.hip.
 sscn_status dev_alloc(void** p, size_t bytes, hipStream_t s);
 void dev_free(void* p, hipStream_t s);
 
