@@ -1005,22 +1005,120 @@ __device__ __forceinline__ int wave_count(int32_t* counter, uint32_t key, bool a
   return base + __popcll(peers & ((1ull << lane) - 1ull));
 }
 
-__global__ void k_plan_hist(const uint32_t* __restrict__ mask, int64_t n, int K, int32_t* __restrict__ hist) {
-  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const bool ok = r < n;
-  (void)wave_count(hist, ok ? plan_key(mask[r], K) : 0u, ok);
+// The counting sort's passes take 256 RPT rows per workgroup of 256 and
+// count in LDS first (one LDS atomic per distinct key per wavefront, then
+// one global atomic per distinct key per workgroup): the keys of surface
+// rows are few and popular, and one global atomic per wavefront on the
+// same few counters serialised the passes (60 us each at 2M rows).  LDS:
+// one counter per key (at most 2^kPlanKeyBits = 128 KB), and the list of
+// the keys the workgroup holds, so that only those are flushed.  RPT (rows
+// per thread) grows with the row count so that there are about 256
+// workgroups (one per CU: the counters take up to 128 KB).
+constexpr int kSortMaxRows = 256 * 16;
+
+struct SortLds {
+  int32_t* cnt;        // bins counters (a multiple of 4)
+  uint16_t* keys;      // distinct keys of the workgroup, in order of first sight
+  int32_t* n_keys;
+};
+__device__ __forceinline__ SortLds sort_lds(char* base, int bins) {
+  const int words = (bins + 3) & ~3;
+  SortLds l;
+  l.cnt = reinterpret_cast<int32_t*>(base);
+  l.n_keys = l.cnt + words;
+  l.keys = reinterpret_cast<uint16_t*>(l.n_keys + 4);
+  // zero the counters (16 bytes per store) and the key count
+  int4* c4 = reinterpret_cast<int4*>(l.cnt);
+  for (int b = threadIdx.x; b < words / 4; b += blockDim.x) c4[b] = make_int4(0, 0, 0, 0);
+  if (threadIdx.x == 0) *l.n_keys = 0;
+  __syncthreads();
+  return l;
+}
+static size_t sort_lds_bytes(int bins) {
+  return sizeof(int32_t) * (((bins + 3) & ~3) + 4) + sizeof(uint16_t) * kSortMaxRows;
+}
+
+// wave_count on the workgroup's LDS counters; a key seen for the first time
+// in the workgroup joins its key list.
+__device__ __forceinline__ int count_in_lds(const SortLds& l, uint32_t key, bool active) {
+  const int lane = threadIdx.x & 63;
+  uint64_t peers = __ballot(active);
+#pragma unroll
+  for (int bit = 0; bit < kPlanKeyBits; ++bit) {
+    const bool set = (key >> bit) & 1u;
+    const uint64_t x = __ballot(set);
+    peers &= set ? x : ~x;
+  }
+  const int leader = peers ? __ffsll((unsigned long long)peers) - 1 : lane;
+  int base = 0;
+  if (active && lane == leader) {
+    base = atomicAdd(&l.cnt[key], __popcll(peers));
+    if (base == 0) l.keys[atomicAdd(l.n_keys, 1)] = (uint16_t)key;
+  }
+  base = __shfl(base, leader, 64);
+  return base + __popcll(peers & ((1ull << lane) - 1ull));
+}
+
+template <int RPT>
+__global__ __launch_bounds__(256) void k_plan_hist(const uint32_t* __restrict__ mask, int64_t n, int K, int bins,
+                                                   int32_t* __restrict__ hist) {
+  static_assert(256 * RPT <= kSortMaxRows, "key list");
+  extern __shared__ __attribute__((aligned(16))) char lds[];
+  const SortLds l = sort_lds(lds, bins);
+  const int64_t r0 = (int64_t)blockIdx.x * (256 * RPT) + threadIdx.x;
+  uint32_t m[RPT];
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) {
+    const int64_t r = r0 + 256 * i;
+    m[i] = r < n ? mask[r] : 0u;
+  }
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) {
+    const bool ok = r0 + 256 * i < n;
+    (void)count_in_lds(l, ok ? plan_key(m[i], K) : 0u, ok);
+  }
+  __syncthreads();
+  for (int j = threadIdx.x; j < *l.n_keys; j += 256) {
+    const int key = l.keys[j];
+    atomicAdd(&hist[key], l.cnt[key]);
+  }
 }
 
 // Counting sort by key (the order inside one key is arbitrary: it changes
-// which rows share a block, never a row's result).
-__global__ void k_plan_sort(const uint32_t* __restrict__ mask, int64_t n, int K, int32_t* __restrict__ cursor,
-                            int32_t* __restrict__ perm, int32_t* __restrict__ pos_of) {
-  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const bool ok = r < n;
-  const int32_t p = wave_count(cursor, ok ? plan_key(mask[r], K) : 0u, ok);
-  if (ok) {
-    perm[p] = (int32_t)r;
-    pos_of[r] = p;
+// which rows share a block, never a row's result): a workgroup ranks its
+// rows per key in LDS, reserves one range per key it holds, then places
+// its rows.
+template <int RPT>
+__global__ __launch_bounds__(256) void k_plan_sort(const uint32_t* __restrict__ mask, int64_t n, int K, int bins,
+                                                   int32_t* __restrict__ cursor, int32_t* __restrict__ perm,
+                                                   int32_t* __restrict__ pos_of) {
+  static_assert(256 * RPT <= kSortMaxRows, "key list");
+  extern __shared__ __attribute__((aligned(16))) char lds[];
+  const SortLds l = sort_lds(lds, bins);
+  const int64_t r0 = (int64_t)blockIdx.x * (256 * RPT) + threadIdx.x;
+  uint32_t key[RPT];
+  int32_t rank[RPT];
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) {
+    const int64_t r = r0 + 256 * i;
+    key[i] = r < n ? plan_key(mask[r], K) : 0u;
+  }
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) rank[i] = count_in_lds(l, key[i], r0 + 256 * i < n);
+  __syncthreads();
+  for (int j = threadIdx.x; j < *l.n_keys; j += 256) {
+    const int k = l.keys[j];
+    l.cnt[k] = atomicAdd(&cursor[k], l.cnt[k]);  // the workgroup's first position for key k
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) {
+    const int64_t r = r0 + 256 * i;
+    if (r < n) {
+      const int32_t p = l.cnt[key[i]] + rank[i];
+      perm[p] = (int32_t)r;
+      pos_of[r] = p;
+    }
   }
 }
 
@@ -1184,10 +1282,18 @@ static sscn_status build_plan(RulebookData* d, Storage& st, int64_t n_rows, int 
       SSCN_HIP(hipGetLastError());
     }
   }
-  k_plan_hist<<<grid_for(n_rows, 256), 256, 0, s>>>(mask, n_rows, K, hist);
+  const int64_t per_wg = ceil_div(n_rows, 256);  // rows per workgroup for 256 workgroups
+  const int rpt = per_wg <= 256 ? 1 : per_wg <= 512 ? 2 : per_wg <= 1024 ? 4 : per_wg <= 2048 ? 8 : 16;
+  const unsigned sort_wgs = (unsigned)ceil_div(n_rows, 256 * rpt);
+  const size_t sort_lds = sort_lds_bytes(bins);
+  auto hist_k = rpt == 1 ? k_plan_hist<1> : rpt == 2 ? k_plan_hist<2> : rpt == 4 ? k_plan_hist<4>
+              : rpt == 8 ? k_plan_hist<8> : k_plan_hist<16>;
+  auto sort_k = rpt == 1 ? k_plan_sort<1> : rpt == 2 ? k_plan_sort<2> : rpt == 4 ? k_plan_sort<4>
+              : rpt == 8 ? k_plan_sort<8> : k_plan_sort<16>;
+  hist_k<<<sort_wgs, 256, sort_lds, s>>>(mask, n_rows, K, bins, hist);
   SSCN_HIP(hipGetLastError());
   SSCN_TRY(scan_i32(hist, bins, s));
-  k_plan_sort<<<grid_for(n_rows, 256), 256, 0, s>>>(mask, n_rows, K, hist, st.perm, pos_of);
+  sort_k<<<sort_wgs, 256, sort_lds, s>>>(mask, n_rows, K, bins, hist, st.perm, pos_of);
   SSCN_HIP(hipGetLastError());
   k_plan_blocks<<<grid_for(nb * 64, 256), 256, 0, s>>>(mask, st.perm, n_rows, nb, bmask, st.b_first);
   SSCN_HIP(hipGetLastError());
