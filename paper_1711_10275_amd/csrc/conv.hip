@@ -522,7 +522,7 @@ __global__ __launch_bounds__(256) void k_conv_quad(
 // registers; the weight tile is double-buffered in LDS with one barrier per
 // step; each wavefront's row tile is private to it.  The plan entries are
 // read from global memory (L2) a step ahead of their use, which keeps the
-// LDS footprint at 27 KB (five workgroups per CU).
+// LDS footprint small (27 KB for 128-byte windows: five workgroups per CU).
 template <typename T, int WB, int NB, int D>
 __device__ __forceinline__ void conv_rows_block(
     const T* __restrict__ X, uint32_t x_bytes, const T* __restrict__ B, uint32_t b_bytes,
@@ -683,7 +683,7 @@ __device__ __forceinline__ void conv_rows_block(
 }
 
 template <typename T, int WB, int NB, int D>
-__global__ __launch_bounds__(256, 5) void k_conv_rows(
+__global__ __launch_bounds__(256, WB == 64 ? 6 : 5) void k_conv_rows(
     const T* __restrict__ X, uint32_t x_bytes, const T* __restrict__ B, uint32_t b_bytes,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ b_first, const int32_t* __restrict__ b_order,
     const uint32_t* __restrict__ items, int64_t n_blocks, int K, int mirror, int kdim, int ncols, Heads<T> Y) {
@@ -1331,7 +1331,8 @@ static sscn_status launch_rows_nb(const T* X, const T* B, const View& v, int kdi
   const int gy = (ncols + 16 * NB - 1) / (16 * NB);
   const uint32_t xb = (uint32_t)((uint64_t)std::max<int64_t>(v.n_in, 1) * kdim * sizeof(T));
   const uint32_t bb = (uint32_t)((uint64_t)v.K * ncols * kdim * sizeof(T));
-  // loads two steps ahead for 64-byte windows (short steps), one otherwise
+  // loads two steps ahead for 64-byte windows (short steps), one otherwise;
+  // six workgroups per CU for 64-byte windows (80 VGPRs), five otherwise
   auto kern = k_conv_rows<T, WB, NB, WB == 64 ? 3 : 2>;
   int cus = 256, per_cu = 1;
   occupancy((const void*)kern, 256, 0, &per_cu, &cus);

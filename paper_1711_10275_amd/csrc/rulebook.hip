@@ -989,11 +989,12 @@ __device__ __forceinline__ uint32_t plan_key(uint32_t m, int K) {
 // serialises on the common ones) and returns the counter's value before this
 // lane's increment.  Lanes find the lanes with the same key by one ballot
 // per key bit, so all of the wavefront's atomics are issued at once.
+template <int BITS = kPlanKeyBits>
 __device__ __forceinline__ int wave_count(int32_t* counter, uint32_t key, bool active) {
   const int lane = threadIdx.x & 63;
   uint64_t peers = __ballot(active);
 #pragma unroll
-  for (int bit = 0; bit < kPlanKeyBits; ++bit) {
+  for (int bit = 0; bit < BITS; ++bit) {
     const bool set = (key >> bit) & 1u;
     const uint64_t x = __ballot(set);
     peers &= set ? x : ~x;
@@ -1231,10 +1232,16 @@ static sscn_status scan_i32(int32_t* p, int64_t count, hipStream_t s) {
 // that workgroups take the longest blocks first.
 __global__ __launch_bounds__(kOneBlock) void k_plan_order(const int32_t* __restrict__ b_first, int64_t nb, int K,
                                                           int32_t* __restrict__ order) {
-  __shared__ int32_t hist[33], cur[33];
-  if (threadIdx.x < 33) hist[threadIdx.x] = 0;
+  // counts per item count, one LDS atomic per distinct count per wavefront
+  // (nearly every block of a surface has one of a few counts)
+  __shared__ int32_t hist[64], cur[64];
+  if (threadIdx.x < 64) hist[threadIdx.x] = 0;
   __syncthreads();
-  for (int64_t b = threadIdx.x; b < nb; b += blockDim.x) atomicAdd(&hist[K - (b_first[b + 1] - b_first[b])], 1);
+  for (int64_t b0 = 0; b0 < nb; b0 += blockDim.x) {
+    const int64_t b = b0 + threadIdx.x;
+    const bool ok = b < nb;
+    (void)wave_count<6>(hist, ok ? (uint32_t)(K - (b_first[b + 1] - b_first[b])) : 0u, ok);
+  }
   __syncthreads();
   if (threadIdx.x == 0) {
     int run = 0;
@@ -1244,8 +1251,12 @@ __global__ __launch_bounds__(kOneBlock) void k_plan_order(const int32_t* __restr
     }
   }
   __syncthreads();
-  for (int64_t b = threadIdx.x; b < nb; b += blockDim.x)
-    order[atomicAdd(&cur[K - (b_first[b + 1] - b_first[b])], 1)] = (int32_t)b;
+  for (int64_t b0 = 0; b0 < nb; b0 += blockDim.x) {
+    const int64_t b = b0 + threadIdx.x;
+    const bool ok = b < nb;
+    const int p = wave_count<6>(cur, ok ? (uint32_t)(K - (b_first[b + 1] - b_first[b])) : 0u, ok);
+    if (ok) order[p] = (int32_t)b;
+  }
 }
 
 // Row-block plan of one direction (seg and pair arrays complete), in the
