@@ -122,23 +122,34 @@ __global__ __launch_bounds__(256) void k_insert(const int4* __restrict__ coords,
 
 // ---------------------------------------------------------------- SSC probe
 // One wavefront per (tile of 64 output sites, slice of P consecutive
-// offsets); blockIdx.y selects the slice.  Many small wavefronts keep enough
-// independent lookups in flight (the probe is bound by the latency of the
-// table reads).  nbr is offset-major [K][n]: nbr[o*n + k] = row of the input
-// at x_k + i_o - (f-1)/2, or -1.  counts[o*n_tiles + t] = number of hits of
-// tile t at offset o (ballot).
+// offsets).  Many small wavefronts keep enough independent lookups in flight
+// (the probe is bound by the table reads).  nbr is offset-major [K][n]:
+// nbr[o*n + k] = row of the site at x_k + i_o - (f-1)/2, or -1.
+// With `mirror`, only the offsets below the centre c = (K-1)/2 are looked
+// up: site j is the neighbour of site k at offset o exactly when k is the
+// neighbour of j at the mirror offset K-1-o (i_{K-1-o} - (f-1)/2 =
+// -(i_o - (f-1)/2)), so each hit also fills nbr[K-1-o][j] = k (those rows
+// start at -1), and nbr[c][k] = k; counts[o*n_tiles + t] = hits of tile t
+// at offset o (ballot) for o < c, the other offsets are counted afterwards
+// (k_count_nbr).  Without it every offset is looked up and counted here
+// (fewer launches: better for small inputs).
+// Inputs from this many sites on use the mirrored SSC probe.
+constexpr int64_t kMirrorProbeMin = 1 << 18;
+
 template <int P>
 __global__ __launch_bounds__(256) void k_ssc_probe(
     const int4* __restrict__ coords, int64_t n, int L0, int L1, int L2, int f,
     const Slot* __restrict__ table, uint64_t mask, int32_t* __restrict__ nbr, int64_t* __restrict__ counts,
-    int64_t n_tiles) {
+    int64_t n_tiles, int mirror) {
   const int lane = threadIdx.x & 63;
   const int plane = f * f, K = f * f * f;
   // Workgroup = 4 tiles x one slice of P offsets.  Logical order: tile
   // groups major, slices minor, and each XCD takes a contiguous run of it,
   // so the lookups that the slices of neighbouring sites share stay in that
   // XCD's L2.
-  const int slices = (K + P - 1) / P;
+  const int ctr = (K - 1) / 2;
+  const int o_end = mirror ? ctr : K;  // offsets looked up
+  const int slices = max((o_end + P - 1) / P, 1);
   const int64_t lb = xcd_remap(blockIdx.x, gridDim.x);
   const int64_t t = (lb / slices) * (blockDim.x / 64) + (threadIdx.x >> 6);
   if (t >= n_tiles) return;  // uniform per wavefront
@@ -148,6 +159,7 @@ __global__ __launch_bounds__(256) void k_ssc_probe(
   const bool site_ok = valid && (unsigned)c.x < (unsigned)kMaxBatch && in_grid(c.y, c.z, c.w, L0, L1, L2);
   const int h = (f - 1) / 2;
   const int o0 = (int)(lb % slices) * P;
+  if (mirror && o0 == 0 && valid) nbr[(int64_t)ctr * n + k] = site_ok ? (int32_t)k : -1;
   // A lookup reads the whole aligned 64-byte line (4 slots) that holds its
   // first slot, and the following lines while the probe sequence runs on
   // (linear probing: stop at the key or at an empty slot), so most lookups
@@ -166,7 +178,7 @@ __global__ __launch_bounds__(256) void k_ssc_probe(
     const int o = o0 + q;
     const int i0 = o / plane, i1 = (o / f) % f, i2 = o % f;
     const int y0 = c.y + i0 - h, y1 = c.z + i1 - h, y2 = c.w + i2 - h;
-    live[q] = o < K && site_ok && in_grid(y0, y1, y2, L0, L1, L2);
+    live[q] = o < o_end && site_ok && in_grid(y0, y1, y2, L0, L1, L2);
     key[q] = pack_key(c.x, y0, y1, y2);
     slot[q] = mix64(key[q]) & mask;
     if (live[q]) read_line(q);
@@ -174,7 +186,7 @@ __global__ __launch_bounds__(256) void k_ssc_probe(
 #pragma unroll
   for (int q = 0; q < P; ++q) {
     const int o = o0 + q;
-    if (o >= K) break;  // uniform
+    if (o >= o_end) break;  // uniform
     int32_t row = -1;
     bool done = !live[q];
     while (!done) {
@@ -196,6 +208,7 @@ __global__ __launch_bounds__(256) void k_ssc_probe(
       }
     }
     if (valid) nbr[(int64_t)o * n + k] = row;
+    if (mirror && row >= 0) nbr[(int64_t)(K - 1 - o) * n + row] = (int32_t)k;
     const unsigned long long bal = __ballot(row >= 0);
     if (lane == 0) counts[(int64_t)o * n_tiles + t] = __popcll(bal);
   }
@@ -209,16 +222,17 @@ __global__ void k_offset_totals(const int64_t* __restrict__ seg, int64_t n_tiles
 }
 
 // Count, per (offset, tile), the present entries of an offset-major
-// neighbour map (used for the SC directions).
+// neighbour map for offsets [o_first, K) (the SC directions; the SSC
+// offsets from the centre on).
 __global__ __launch_bounds__(256) void k_count_nbr(const int32_t* __restrict__ nbr, int64_t n_rows,
                                                    int K, int64_t* __restrict__ counts,
-                                                   int64_t n_tiles) {
+                                                   int64_t n_tiles, int o_first = 0) {
   const int lane = threadIdx.x & 63;
   const int64_t t = (int64_t)blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6);
   if (t >= n_tiles) return;
   const int64_t k = t * kTile + lane;
   const bool valid = k < n_rows;
-  for (int o = 0; o < K; ++o) {
+  for (int o = o_first; o < K; ++o) {
     const int32_t row = valid ? nbr[(int64_t)o * n_rows + k] : -1;
     const unsigned long long m = __ballot(row >= 0);
     if (lane == 0) counts[(int64_t)o * n_tiles + t] = __popcll(m);
@@ -1434,9 +1448,19 @@ extern "C" sscn_status ssc_rulebook_build(const int32_t* coords, int64_t n, cons
                                                (int4*)d->out_coords);
       SSCN_HIP(hipGetLastError());
       constexpr int P = 3;  // lookups per wavefront
-      k_ssc_probe<P><<<(unsigned)(grid_for(n_tiles * 64, 256) * ceil_div(K, P)), 256, 0, s>>>(
-          (const int4*)coords, n, L0, L1, L2, f, table, cap - 1, nbr, counts, n_tiles);
+      // mirrored lookups halve the table reads; they cost two more launches,
+      // which only pays off on larger inputs
+      const bool mirror = n >= kMirrorProbeMin && K > 1;
+      const int c = (K - 1) / 2;  // centre offset
+      if (mirror) SSCN_TRY(fill_i32(nbr + (int64_t)(c + 1) * n, -1, (int64_t)(K - 1 - c) * n, s));
+      const int64_t slices = std::max<int64_t>(ceil_div(mirror ? c : K, P), 1);
+      k_ssc_probe<P><<<(unsigned)(grid_for(n_tiles * 64, 256) * slices), 256, 0, s>>>(
+          (const int4*)coords, n, L0, L1, L2, f, table, cap - 1, nbr, counts, n_tiles, mirror ? 1 : 0);
       SSCN_HIP(hipGetLastError());
+      if (mirror) {
+        k_count_nbr<<<grid_for(n_tiles * 64, 256), 256, 0, s>>>(nbr, n, K, counts, n_tiles, c);
+        SSCN_HIP(hipGetLastError());
+      }
     }
     if (K * n_tiles <= kOneBlockScanMax) {
       launch_seg_scan_one(counts, d->fwd.seg, K * n_tiles, std::max<int64_t>(n_tiles, 1), K, n > 0 ? stats : nullptr,

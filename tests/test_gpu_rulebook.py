@@ -130,3 +130,19 @@ def test_shuffled_rows():
     osc = O.sc_rulebook(cp, size, 2, 2)
     assert_same_rulebook(sc, osc, "shuffled sc")
     np.testing.assert_array_equal(host(sc.out_coords()), osc.out_coords)
+
+
+@pytest.mark.parametrize("f", [3, 5])
+def test_mirrored_probe_on_shuffled_rows(f):
+    """From 2^18 sites on, the SSC build looks up only the offsets below the
+    centre and fills the mirrored ones from each hit; rows in random order
+    (three batches of the 128^3 shapes, about 300k sites) must still give the
+    oracle's rule book exactly, for 3^3 and 5^3 filters."""
+    c, size = coords_for("shapes128")
+    big = np.concatenate([np.concatenate([c[:, :1] + 4 * r, c[:, 1:]], axis=1) for r in range(3)])
+    big = np.ascontiguousarray(big[np.random.default_rng(1).permutation(big.shape[0])]).astype(np.int32)
+    assert big.shape[0] >= 1 << 18
+    rb = sscn.ssc_rulebook_build(dev(big), size, f)
+    orb = O.ssc_rulebook(big, size, f)
+    assert_same_rulebook(rb, orb, f"mirrored ssc f={f}")
+    assert_same_rulebook(rb.transpose(), O.transpose(orb), f"mirrored ssc f={f} transposed")
