@@ -1274,11 +1274,15 @@ __global__ __launch_bounds__(kOneBlock) void k_plan_order(const int32_t* __restr
 }
 
 // Row-block plan of one direction (seg and pair arrays complete), in the
-// rule book's own blocks.
-static sscn_status build_plan(RulebookData* d, Storage& st, int64_t n_rows, int K, hipStream_t s) {
+// rule book's own blocks.  ppo_bound >= 0: the pair counts are not on the
+// host yet (the plan is queued inside the build); at most ppo_bound pairs
+// per offset, and room for nb K items.
+static sscn_status build_plan(RulebookData* d, Storage& st, int64_t n_rows, int K, hipStream_t s,
+                              int64_t ppo_bound = -1) {
   const int64_t nb = ceil_div(n_rows, kPlanRows);
   st.n_blocks = nb;
-  const int64_t cap = std::max<int64_t>(1, std::min<int64_t>(d->n_pairs, nb * K));
+  const int64_t cap =
+      std::max<int64_t>(1, ppo_bound >= 0 ? nb * K : std::min<int64_t>(d->n_pairs, nb * K));
   Arena a;
   a.add(&st.perm, (size_t)nb * kPlanRows);
   a.add(&st.b_first, (size_t)nb + 1);
@@ -1295,8 +1299,9 @@ static sscn_status build_plan(RulebookData* d, Storage& st, int64_t n_rows, int 
   t.add(&bmask, (size_t)nb);
   t.add(&pos_of, (size_t)n_rows);
   SSCN_TRY(tmp.alloc(t));
-  int64_t max_ppo = 0;
-  for (int64_t c : d->pairs_per_offset) max_ppo = std::max(max_ppo, c);
+  int64_t max_ppo = ppo_bound;
+  if (ppo_bound < 0)
+    for (int64_t c : d->pairs_per_offset) max_ppo = std::max(max_ppo, c);
   if (st.row_mask) {
     SSCN_TRY(fill_i32(hist, 0, bins + 1, s));
   } else {
@@ -1478,6 +1483,14 @@ extern "C" sscn_status ssc_rulebook_build(const int32_t* coords, int64_t n, cons
       return SSCN_OK;
     };
     if (one_phase) SSCN_TRY(compact());
+    // With K <= 32 the row-block plan is queued before the readback too: its
+    // launches overlap the build's kernels and the host waits once.
+    const bool eager_plan = one_phase && n > 0 && K <= 32 && n < (int64_t)kPlanNoRow;
+    if (eager_plan) {
+      SSCN_TRY(build_plan(d, d->fwd, n, K, s, /*a site has one neighbour per offset*/ n));
+      SSCN_HIP(hipEventCreateWithFlags(&d->plan_ready, hipEventDisableTiming));
+      SSCN_HIP(hipEventRecord(d->plan_ready, s));
+    }
     std::vector<unsigned long long> host(1 + K);
     SSCN_TRY(readback(host.data(), stats, sizeof(unsigned long long) * (1 + K), s));
     SSCN_TRY(flags_error(host[0]));
