@@ -633,12 +633,24 @@ __device__ __forceinline__ bool site_in_range(int4 c, const ScGeom& g) {
 }
 
 // Record the first visit (smallest j*K + o) of every output location.
+// With `check` (K <= 32 and f >= s: every input in range has a target),
+// also flag inputs outside the grid and repeated locations: two inputs at
+// one location visit the same (output, offset), which two distinct inputs
+// never do, so the output slot keeps the offsets visited so far (its pad
+// word) and a second visit of one is a repeated location.  `copy` (if not
+// NULL) receives the coordinates.
 __global__ __launch_bounds__(256) void k_sc_visit(const int4* __restrict__ coords, int64_t n, ScGeom g,
-                                                  Slot* __restrict__ otable, uint64_t omask) {
+                                                  Slot* __restrict__ otable, uint64_t omask, int check,
+                                                  unsigned long long* __restrict__ flags,
+                                                  int4* __restrict__ copy) {
   const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (j >= n) return;
   const int4 c = coords[j];
-  if (!site_in_range(c, g)) return;
+  if (copy) copy[j] = c;
+  if (!site_in_range(c, g)) {
+    if (check) atomicOr(flags, (unsigned long long)kFlagOutOfRange);
+    return;
+  }
   for (int o = 0; o < g.K; ++o) {
     int y0, y1, y2;
     if (!sc_target(g, c, o, y0, y1, y2)) continue;
@@ -652,6 +664,10 @@ __global__ __launch_bounds__(256) void k_sc_visit(const int4* __restrict__ coord
       slot = (slot + 1) & omask;
     }
     atomicMin(&otable[slot].row, (int32_t)(j * g.K + o));
+    if (check) {
+      const int32_t bit = (int32_t)(1u << o);
+      if (atomicOr(&otable[slot].pad, bit) & bit) atomicOr(flags, (unsigned long long)kFlagDuplicate);
+    }
   }
 }
 
@@ -1543,9 +1559,13 @@ extern "C" sscn_status sc_rulebook_build(const int32_t* coords, int64_t n, const
     const int per_dim = (f + s_ - 1) / s_;
     const int64_t max_out = n * (int64_t)per_dim * per_dim * per_dim;
     const uint64_t cap = table_capacity(n), ocap = table_capacity(max_out);
-    Slot* table; Slot* otable; unsigned long long* stats; int32_t* first; int32_t* rank;
+    Slot* table = nullptr; Slot* otable; unsigned long long* stats; int32_t* first; int32_t* rank;
+    // Repeated locations and range errors: found while visiting the outputs
+    // where every input has one (K <= 32, f >= s), else by an input
+    // dictionary.
+    const bool visit_checks = K <= 32 && f >= s_;
     Arena ta;
-    ta.add(&table, cap);
+    if (!visit_checks) ta.add(&table, cap);
     ta.add(&otable, ocap);
     ta.add(&stats, 2 + K);
     ta.add(&first, (size_t)n * K);
@@ -1555,15 +1575,26 @@ extern "C" sscn_status sc_rulebook_build(const int32_t* coords, int64_t n, const
     ia.add(&d->in_coords, (size_t)4 * n);
     SSCN_TRY(owned_alloc(d, ia, s));
 
-    SSCN_TRY(launch_fill_slots(table, cap, -1, s, stats, 2 + K));
+    if (visit_checks) {
+      SSCN_TRY(launch_fill_slots(otable, ocap, INT32_MAX, s, stats, 2 + K));
+      if (n > 0) {
+        k_sc_visit<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, 1, stats,
+                                                    (int4*)d->in_coords);
+        SSCN_HIP(hipGetLastError());
+      }
+    } else {
+      SSCN_TRY(launch_fill_slots(table, cap, -1, s, stats, 2 + K));
+      if (n > 0) {
+        SSCN_TRY(launch_fill_slots(otable, ocap, INT32_MAX, s));
+        k_insert<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g.L0, g.L1, g.L2, table, cap - 1, stats,
+                                                 (int4*)d->in_coords);
+        SSCN_HIP(hipGetLastError());
+        k_sc_visit<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, 0, stats,
+                                                    nullptr);
+        SSCN_HIP(hipGetLastError());
+      }
+    }
     if (n > 0) {
-      SSCN_TRY(launch_fill_slots(otable, ocap, INT32_MAX, s));
-      // the input dictionary detects repeated locations and range errors
-      k_insert<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g.L0, g.L1, g.L2, table, cap - 1, stats,
-                                               (int4*)d->in_coords);
-      SSCN_HIP(hipGetLastError());
-      k_sc_visit<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1);
-      SSCN_HIP(hipGetLastError());
       k_sc_mark<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, first, stats + 1);
       SSCN_HIP(hipGetLastError());
       SSCN_TRY(exclusive_scan_i32(first, rank, n * K, s));

@@ -104,6 +104,16 @@ def test_empty_and_errors():
             with pytest.raises(sscn.SSCNError) as e:
                 build(dev(np.array(bad, np.int32)))
             assert e.value.code == "out_of_range"
+    # SC with f >= s finds repeated locations while visiting the outputs;
+    # with f < s an input can have no output at all (odd x here), and the
+    # input dictionary must still flag it
+    for f, s_ in ((3, 2), (1, 2)):
+        with pytest.raises(sscn.SSCNError) as e:
+            sscn.sc_rulebook_build(dev(c), (9, 9, 9), f, s_)
+        assert e.value.code == "duplicate", (f, s_)
+        with pytest.raises(sscn.SSCNError) as e:
+            sscn.sc_rulebook_build(dev(np.array([[0, 9, 0, 0]], np.int32)), (9, 9, 9), f, s_)
+        assert e.value.code == "out_of_range", (f, s_)
     with pytest.raises(sscn.SSCNError) as e:
         sscn.ssc_rulebook_build(dev(c[:2]), (8, 8, 8), 4)
     assert e.value.code == "invalid_arg"
