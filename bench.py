@@ -18,11 +18,13 @@ sample of the same workload on the host cores.
 Dominant kernel: k_conv_rows, which runs the forward and the dgrad of the
 layer (same pairs, same channel counts) over the rule book's row-block
 plan.  Its duration is measured with HIP events around the dgrad call,
-which is exactly one launch of it on the current stream (the plan is built
-once per rule book, on its first use; its cost is in every step and is
-reported as plan_build_ms).  `traffic` (HBM bytes per launch) comes from the
+which is exactly one launch of it on the current stream (the SSC build
+queues the plan, so its cost is in rulebook_build_ms and in every step;
+first_forward_extra_ms is what a fresh rule book's first forward costs
+beyond a later one).  `traffic` (HBM bytes per launch) comes from the
 committed counter record in profiles/, and is null when the kernel source
-has changed since those counters were taken.
+has changed since those counters were taken.  `build_roofline` puts the
+SSC build's logical bytes over its wall time against HBM bandwidth.
 
 --copy-calibration runs a plain device copy of known size (256 MiB) so
 that a counter run can scale FETCH_SIZE / WRITE_SIZE by what they read for
@@ -113,6 +115,25 @@ def _event_ms(fn, reps, stream):
     return e0.elapsed_time(e1) / reps
 
 
+def build_roofline(n, K, pairs, ms, what):
+    """Logical bytes of an SSC rule-book build against HBM bandwidth.
+
+    Counted: coordinates read (16 B per site), the hash table filled and
+    written (16-byte slots, capacity the power of two >= 2n), one 16-byte
+    slot read per (site, offset) lookup, the offset-major neighbour map
+    written and read back (4 B per site and offset each way), the pair
+    arrays written (8 B per pair).  The time is the host wall time of the
+    build call (its row-block plan included).
+    """
+    cap = 64
+    while cap < 2 * n:
+        cap *= 2
+    nbytes = 16 * n + 16 * cap + 16 * n + 16 * K * n + 8 * K * n + 8 * pairs
+    achieved = nbytes / (ms * 1e-3) / 1e9
+    return {"stage": what, "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": achieved / PEAK_HBM_GBS, "bytes": nbytes, "ms": ms}
+
+
 def _wall_ms(fn, reps):
     import torch
     fn()
@@ -155,7 +176,7 @@ def sc_then_ssc(tc, size, stream, reps):
 def unet_scenes(stream, reps):
     """Five-level submanifold U-Net forward, 256^3 x 8 scenes, bf16."""
     import torch
-    from paper_1711_10275_amd import unet
+    from paper_1711_10275_amd import sscn, unet
     from paper_1711_10275_amd import synthetic as S
     dev = torch.device("cuda:0")
     c = S.scenes_256()
@@ -163,6 +184,8 @@ def unet_scenes(stream, reps):
     X = torch.from_numpy(S.features(c.shape[0], 32, S.SEED_FEAT + 3, bf16=True)).to(torch.bfloat16).to(dev)
     params = unet.device_params(draw=lambda n, k, ci, co: S.layer_params(n, k, ci, co, bf16=True))
     geom_ms = _wall_ms(lambda: unet.Geometry(tc, (256, 256, 256)), reps)
+    ssc0_ms = _wall_ms(lambda: sscn.ssc_rulebook_build(tc, (256, 256, 256), 3), reps)
+    ssc0_pairs = sscn.ssc_rulebook_build(tc, (256, 256, 256), 3).n_pairs
     # a fresh input: rule books of every level, then the network (lazily built
     # chunk tables included)
     fresh_ms = _wall_ms(lambda: unet.forward(X, unet.Geometry(tc, (256, 256, 256)), params), reps)
@@ -171,7 +194,11 @@ def unet_scenes(stream, reps):
     unfused_ms = _event_ms(lambda: unet.forward(X, geom, params, fused=False), reps, stream)
     fl = unet.flops(geom)
     return {"workload": "unet5_grid256_batch8_scenes_c32to160_bf16", "level_sites": [int(x.shape[0]) for x in geom.coords],
-            "geometry_build_ms": geom_ms, "forward_ms": fwd_ms, "forward_sites_per_s": c.shape[0] / (fwd_ms * 1e-3),
+            "geometry_build_ms": geom_ms,
+            "level0_ssc_build_roofline": build_roofline(int(c.shape[0]), 27, int(ssc0_pairs), ssc0_ms,
+                                                        "SSC 3^3 rule-book build incl. its row-block plan, "
+                                                        "level 0 (about 2M sites)"),
+            "forward_ms": fwd_ms, "forward_sites_per_s": c.shape[0] / (fwd_ms * 1e-3),
             "forward_effective_tflops": fl / (fwd_ms * 1e-3) / 1e12, "flops": fl,
             "forward_unfused_ms": unfused_ms, "geometry_plus_forward_ms": fresh_ms,
             "geometry_plus_forward_sites_per_s": c.shape[0] / (fresh_ms * 1e-3)}
@@ -275,7 +302,7 @@ def main():
                    "step": "rule-book build + forward + backward (dgrad + wgrad)"},
         "effective_tflops_step": 3 * flops_layer / (ms_step * 1e-3) / 1e12,
         "rulebook_build_ms": build_ms,
-        "plan_build_ms": build_fwd_ms - build_ms - fwd_ms,
+        "first_forward_extra_ms": build_fwd_ms - build_ms - fwd_ms,
         "forward_ms": fwd_ms,
         "forward_tflops": flops_layer / (fwd_ms * 1e-3) / 1e12,
         "forward_sites_per_s": n / (fwd_ms * 1e-3),
@@ -288,6 +315,8 @@ def main():
                      "unit": "TFLOP/s", "frac": achieved / PEAK_FP32_MFMA_TFLOPS,
                      "launch_ms": dgrad_ms, "flops_per_launch": flops_layer,
                      "traffic": recorded_traffic()},
+        "build_roofline": build_roofline(int(n), 27, int(pairs), build_ms,
+                                         "SSC 3^3 rule-book build incl. its row-block plan, 100k sites"),
     }
     if not args.no_extra:
         result["extra"] = {"sc_then_ssc": sc_then_ssc(tc, size, stream, reps), "unet": unet_scenes(stream, 5)}
