@@ -159,9 +159,11 @@ def test_sc22_backward_shapes128():
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_affine_relu_and_concat(dtype):
+@pytest.mark.parametrize("c,cb", [(24, 7), (32, 16), (5, 3)])
+def test_affine_relu_and_concat(dtype, c, cb):
+    """16-byte chunk paths (rows of whole chunks) and the element paths."""
     rng = np.random.default_rng(3)
-    n, c = 1000, 24
+    n = 1000
     x = S.bf16_round(rng.standard_normal((n, c)).astype(np.float32)) if dtype == "bf16" else \
         rng.standard_normal((n, c)).astype(np.float32)
     scale = rng.uniform(0.5, 1.5, c).astype(np.float32)
@@ -169,7 +171,7 @@ def test_affine_relu_and_concat(dtype):
     y = host(sscn.affine_relu(dev(x, TD[dtype]), dev(scale), dev(shift)))
     ref = np.maximum(0.0, x.astype(np.float64) * scale + shift)
     assert_close(y, ref, dtype, "affine_relu")
-    b = rng.standard_normal((n, 7)).astype(np.float32)
+    b = rng.standard_normal((n, cb)).astype(np.float32)
     b = S.bf16_round(b) if dtype == "bf16" else b
     cat = host(sscn.concat_cols(dev(x, TD[dtype]), dev(b, TD[dtype])))
     np.testing.assert_array_equal(cat, np.concatenate([x, b], axis=1))
