@@ -1350,9 +1350,12 @@ static sscn_status launch_rows(const T* X, const T* B, const View& v, int kdim, 
   if (v.n_out == 0) return SSCN_OK;
   SSCN_TRY(ensure_plan(v, s));
   // 64 output columns per workgroup when they divide the width, else 32;
-  // 128-byte windows (32 fp32 or 64 bf16 channels) unless a bf16 row is not
-  // a multiple of 128 bytes
-  const bool wide_cols = ncols % 64 == 0;
+  // for bf16 (bound by loads and step latency rather than MFMAs) 64 unless
+  // the width is at most 32: fewer column groups re-read the input rows
+  // fewer times, and a partial last group costs less than a third group at
+  // 96 or 160 columns.  128-byte windows (32 fp32 or 64 bf16 channels)
+  // unless a bf16 row is not a multiple of 128 bytes.
+  const bool wide_cols = sizeof(T) == 2 ? ncols > 32 : ncols % 64 == 0;
   if constexpr (sizeof(T) == 2) {
     if (kdim % 64 != 0)
       return wide_cols ? launch_rows_nb<T, 64, 4>(X, B, v, kdim, ncols, Y, s)
