@@ -670,7 +670,57 @@ __device__ __forceinline__ void conv_rows_block(
       if (t0 + u < n_steps) step(u);
   }
   // lane holds rows 4 g + r of the wavefront's 16, column m of each column block
-  const int4 rows = *reinterpret_cast<const int4*>(perm + blk * kPlanRows + wave * 16 + 4 * g);
+  const int32_t* wrows = perm + blk * kPlanRows + wave * 16;
+  // bf16: 16-byte row pieces when every destination allows them: the
+  // wavefront's 16 x COLS result goes through its quarter of the weight
+  // buffers (free after the last step's barrier) and leaves as whole row
+  // pieces instead of one 2-byte element per lane and row.  (fp32 rows take
+  // 4 bytes per lane already; there the extra registers cost more.)
+  constexpr int RB = COLS * (int)sizeof(T) + 16;  // tile row pitch (bank spread)
+  static_assert(16 * RB <= 2 * 16 * NB * (WB + 16) / 4, "output tile fits a quarter of the weight buffers");
+  bool vec = sizeof(T) == 2 && (ncols * (int)sizeof(T)) % 16 == 0;
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+    if (h < Y.n)
+      vec = vec && reinterpret_cast<uintptr_t>(Y.out[h]) % 16 == 0 && (Y.ld[h] * (int64_t)sizeof(T)) % 16 == 0;
+  if constexpr (sizeof(T) == 2) if (vec) {
+    char* tile = reinterpret_cast<char*>(Bs) + wave * (2 * 16 * NB * (WB + 16) / 4);
+    constexpr int PIECES = COLS * (int)sizeof(T) / 16;  // 16-byte pieces per tile row
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      if (h >= Y.n) break;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const int col = col0 + nb * 16 + m;
+        const bool ok = col < ncols;
+        const float sc = ok && Y.scale[h] ? Y.scale[h][col] : 1.f;
+        const float sh = ok && Y.scale[h] ? Y.shift[h][col] : 0.f;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float v = Y.scale[h] ? fmaxf(0.f, acc[nb][r] * sc + sh) : acc[nb][r];
+          Elem<T>::store(reinterpret_cast<T*>(tile + (4 * g + r) * RB) + nb * 16 + m, v);
+        }
+      }
+      // the wavefront reads back what other lanes wrote
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+      for (int q = lane; q < 16 * PIECES; q += 64) {
+        const int row_in = q / PIECES, piece = q % PIECES;
+        const int col = col0 + piece * (16 / (int)sizeof(T));
+        const int32_t grow = wrows[row_in];
+        if (grow >= 0 && col < ncols)
+          *reinterpret_cast<uint4*>(Y.out[h] + grow * Y.ld[h] + col) =
+              *reinterpret_cast<const uint4*>(tile + row_in * RB + piece * 16);
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+    return;
+  }
+  const int4 rows = *reinterpret_cast<const int4*>(wrows + 4 * g);
   const int rr[4] = {rows.x, rows.y, rows.z, rows.w};
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
