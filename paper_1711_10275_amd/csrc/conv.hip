@@ -523,7 +523,7 @@ __global__ __launch_bounds__(256) void k_conv_quad(
 // step; each wavefront's row tile is private to it.  The plan entries are
 // read from global memory (L2) a step ahead of their use, which keeps the
 // LDS footprint small (27 KB for 128-byte windows: five workgroups per CU).
-template <typename T, int WB, int NB, int D>
+template <typename T, int WB, int NB, int D, int PK>
 __device__ __forceinline__ void conv_rows_block(
     const T* __restrict__ X, uint32_t x_bytes, const T* __restrict__ B, uint32_t b_bytes,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ b_first, const uint32_t* __restrict__ items,
@@ -539,8 +539,10 @@ __device__ __forceinline__ void conv_rows_block(
   const int first = b_first[blk];
   const int n_items = b_first[blk + 1] - first;
   const uint32_t row_bytes = (uint32_t)kdim * sizeof(T);
-  const int ks_n = (int)((row_bytes + WB - 1) / WB);  // steps per item
-  const int n_steps = n_items * ks_n;
+  // PK > 1: rows of WB / PK bytes, PK items per step side by side in the
+  // window (their products simply add up over the window's channels)
+  const int ks_n = PK > 1 ? 1 : (int)((row_bytes + WB - 1) / WB);  // steps per item
+  const int n_steps = PK > 1 ? (n_items + PK - 1) / PK : n_items * ks_n;
   const uint32_t w_stride = (uint32_t)ncols * row_bytes;  // bytes per offset
   const rsrc_t rx = make_rsrc(X, x_bytes), rb = make_rsrc(B, b_bytes);
 
@@ -553,16 +555,19 @@ __device__ __forceinline__ void conv_rows_block(
 
     // lane constants of the coalesced loads
     const uint32_t a_byte = (uint32_t)(lane % LPR) * 16;  // within the window
+    const int a_u = PK > 1 ? (int)(a_byte / row_bytes) : 0;  // item of the step (packed)
+    const uint32_t a_in = a_byte - (uint32_t)a_u * row_bytes;  // byte within its row
     int a_row[NA];                                          // row within the wavefront's 16
 #pragma unroll
     for (int i = 0; i < NA; ++i) a_row[i] = lane / LPR + RPI * i;
-    int b_col[NBP];
+    int b_col[NBP], b_u[NBP];
     uint32_t b_byte[NBP], b_base[NBP];
 #pragma unroll
     for (int q = 0; q < NBP; ++q) {
       const int p = tid + 256 * q;
       b_col[q] = p / LPR;
       b_byte[q] = (uint32_t)(p % LPR) * 16;
+      b_u[q] = PK > 1 ? (int)(b_byte[q] / row_bytes) : 0;
       const int col = col0 + b_col[q];
       b_base[q] = (b_col[q] < COLS && col < ncols) ? (uint32_t)col * row_bytes : kOobOffset;
     }
@@ -589,13 +594,44 @@ __device__ __forceinline__ void conv_rows_block(
     // entry of an item carries the item's offset)
     uint32_t nx_r[NA];
     auto fetch_ent = [&]() {
-      const int it = min(ld_item, n_items - 1);
+      const int it = min(ld_item + a_u, n_items - 1);
 #pragma unroll
       for (int i = 0; i < NA; ++i) nx_r[i] = ents[it * kPlanRows + wave * 16 + a_row[i]];
     };
     fetch_ent();
     auto issue = [&](int slot) {
       const bool live = ld_step < n_steps;
+      if constexpr (PK > 1) {
+        // offset of each of the step's items, from a lane that holds its entries
+        uint32_t soff[PK];
+#pragma unroll
+        for (int u = 0; u < PK; ++u) {
+          const int o = (int)((uint32_t)__builtin_amdgcn_readlane((int)nx_r[0], u * (int)(row_bytes / 16)) >>
+                              kPlanRowBits);
+          soff[u] = (uint32_t)(mirror ? K - 1 - o : o) * w_stride;
+        }
+#pragma unroll
+        for (int i = 0; i < NA; ++i) {
+          const uint32_t r = nx_r[i] & kPlanNoRow;
+          const bool ok = live && ld_item + a_u < n_items && r != kPlanNoRow;
+          const auto v = __builtin_amdgcn_raw_buffer_load_b128(rx, (int)(ok ? r * row_bytes + a_in : kOobOffset), 0, 0);
+          ga[slot][i] = make_uint4(v[0], v[1], v[2], v[3]);
+        }
+#pragma unroll
+        for (int q = 0; q < NBP; ++q) {
+          uint32_t so = soff[0];
+#pragma unroll
+          for (int u = 1; u < PK; ++u) so = b_u[q] == u ? soff[u] : so;
+          const bool ok = live && ld_item + b_u[q] < n_items && b_base[q] != kOobOffset;
+          const auto v = __builtin_amdgcn_raw_buffer_load_b128(
+              rb, (int)(ok ? b_base[q] + (b_byte[q] - (uint32_t)b_u[q] * row_bytes) + so : kOobOffset), 0, 0);
+          gb[slot][q] = make_uint4(v[0], v[1], v[2], v[3]);
+        }
+        ld_item += PK;
+        ++ld_step;
+        fetch_ent();
+        return;
+      }
       const int o = (int)((uint32_t)__builtin_amdgcn_readfirstlane((int)nx_r[0]) >> kPlanRowBits);
       const int ow = mirror ? K - 1 - o : o;
       const uint32_t win = (uint32_t)ld_ks * WB;
@@ -628,9 +664,14 @@ __device__ __forceinline__ void conv_rows_block(
     };
     int mul_item = 0, mul_ks = 0;  // item of the step being multiplied
     auto multiply = [&](int buf) {
-      // a wavefront whose 16 rows have no pair for the item skips the MFMAs
-      const bool skip = ((have >> mul_item) & 1u) == 0;
-      if (++mul_ks == ks_n) { mul_ks = 0; ++mul_item; }
+      // a wavefront whose 16 rows have no pair for the item(s) skips the MFMAs
+      const bool skip = ((have >> mul_item) & ((1u << PK) - 1u)) == 0;
+      if (PK > 1) {
+        mul_item += PK;
+      } else if (++mul_ks == ks_n) {
+        mul_ks = 0;
+        ++mul_item;
+      }
       if (skip) return;
       Oct<T> a[S], b[S][NB];
 #pragma unroll
@@ -732,7 +773,7 @@ __device__ __forceinline__ void conv_rows_block(
   }
 }
 
-template <typename T, int WB, int NB, int D>
+template <typename T, int WB, int NB, int D, int PK>
 __global__ __launch_bounds__(256, WB == 64 ? 6 : 5) void k_conv_rows(
     const T* __restrict__ X, uint32_t x_bytes, const T* __restrict__ B, uint32_t b_bytes,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ b_first, const int32_t* __restrict__ b_order,
@@ -767,7 +808,7 @@ __global__ __launch_bounds__(256, WB == 64 ? 6 : 5) void k_conv_rows(
   }
   for (int64_t idx = wg, round = 0; idx < n_blocks; idx = next(++round)) {
     __syncthreads();  // the previous block's LDS is free
-    conv_rows_block<T, WB, NB, D>(X, x_bytes, B, b_bytes, perm, b_first, items, b_order[idx], K, mirror, kdim,
+    conv_rows_block<T, WB, NB, D, PK>(X, x_bytes, B, b_bytes, perm, b_first, items, b_order[idx], K, mirror, kdim,
                                   ncols, Y, As, Bs, tid, wave, lane, m, g, col0);
   }
 }
@@ -1373,7 +1414,7 @@ static bool rows_eligible(const View& v, int kdim, int ncols) {
          std::max(v.n_in, v.n_out) < (int64_t)kPlanNoRow && ceil_div(v.n_out, kPlanRows) * v.K < INT32_MAX;
 }
 
-template <typename T, int WB, int NB>
+template <typename T, int WB, int NB, int PK = 1>
 static sscn_status launch_rows_nb(const T* X, const T* B, const View& v, int kdim, int ncols, const Heads<T>& Y,
                                   hipStream_t s) {
   const int64_t nb = v.st->n_blocks;
@@ -1383,7 +1424,7 @@ static sscn_status launch_rows_nb(const T* X, const T* B, const View& v, int kdi
   const uint32_t bb = (uint32_t)((uint64_t)v.K * ncols * kdim * sizeof(T));
   // loads two steps ahead for 64-byte windows (short steps), one otherwise;
   // six workgroups per CU for 64-byte windows (80 VGPRs), five otherwise
-  auto kern = k_conv_rows<T, WB, NB, WB == 64 ? 3 : 2>;
+  auto kern = k_conv_rows<T, WB, NB, WB == 64 ? 3 : 2, PK>;
   int cus = 256, per_cu = 1;
   occupancy((const void*)kern, 256, 0, &per_cu, &cus);
   // persistent: one resident wave of workgroups per column group
@@ -1406,7 +1447,16 @@ static sscn_status launch_rows(const T* X, const T* B, const View& v, int kdim, 
   // 96 or 160 columns.  128-byte windows (32 fp32 or 64 bf16 channels)
   // unless a bf16 row is not a multiple of 128 bytes.
   const bool wide_cols = sizeof(T) == 2 ? ncols > 32 : ncols % 64 == 0;
+  // Rows of half a window (32 bf16 or 16 fp32 channels, 16 bf16 in a
+  // 64-byte window): two items per step.
+  const uint32_t row_bytes = (uint32_t)kdim * sizeof(T);
+  if (row_bytes == 64)
+    return wide_cols ? launch_rows_nb<T, 128, 4, 2>(X, B, v, kdim, ncols, Y, s)
+                     : launch_rows_nb<T, 128, 2, 2>(X, B, v, kdim, ncols, Y, s);
   if constexpr (sizeof(T) == 2) {
+    if (row_bytes == 32)
+      return wide_cols ? launch_rows_nb<T, 64, 4, 2>(X, B, v, kdim, ncols, Y, s)
+                       : launch_rows_nb<T, 64, 2, 2>(X, B, v, kdim, ncols, Y, s);
     if (kdim % 64 != 0)
       return wide_cols ? launch_rows_nb<T, 64, 4>(X, B, v, kdim, ncols, Y, s)
                        : launch_rows_nb<T, 64, 2>(X, B, v, kdim, ncols, Y, s);

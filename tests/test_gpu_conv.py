@@ -281,3 +281,26 @@ def test_ssc_filter5(dtype):
     rdx, rdw = O.backward(X, W, G, orb)
     assert_close(host(dx), rdx, dtype, "dgrad")
     assert_close(host(dw), rdw, dtype, "wgrad")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("c", [16, 32])
+def test_packed_items_forward_backward(c, dtype):
+    """Rows of 32 or 64 bytes put two items in each step of the row kernel
+    (fp32 16 channels, bf16 16 and 32 channels): SSC forward and dgrad (the
+    mirror view), SC(2,2) and its transposed (DC) layer, against the oracle."""
+    coords, size = coords_for("shell32")
+    rb = sscn.ssc_rulebook_build(dev(coords), size, 3)
+    orb = O.ssc_rulebook(coords, size, 3)
+    X, W = _draw(coords.shape[0], c, c, 27, 7 + c, dtype)
+    G = S.features(coords.shape[0], c, S.SEED_GRAD + 7 + c, bf16=dtype == "bf16")
+    assert_close(_fwd(rb, X, W, dtype), O.forward(X, W, orb), dtype, f"packed ssc {c}")
+    dx, _ = sscn.sparse_conv_backward(None, dev(W, TD[dtype]), dev(G, TD[dtype]), rb, wgrad=False)
+    assert_close(host(dx), O.backward(X, W, G, orb)[0], dtype, f"packed dgrad {c}")
+    sc = sscn.sc_rulebook_build(dev(coords), size, 2, 2)
+    osc = O.sc_rulebook(coords, size, 2, 2)
+    Xs, Ws = _draw(coords.shape[0], c, 2 * c, 8, 9 + c, dtype)
+    Y = _fwd(sc, Xs, Ws, dtype)
+    assert_close(Y, O.forward(Xs, Ws, osc), dtype, f"packed sc {c}")
+    Yd, Wd = _draw(sc.n_out, c, c, 8, 11 + c, dtype)
+    assert_close(_fwd(sc.transpose(), Yd, Wd, dtype), O.forward(Yd, Wd, O.transpose(osc)), dtype, f"packed dc {c}")
