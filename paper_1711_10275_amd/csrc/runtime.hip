@@ -1,4 +1,4 @@
-// Error reporting, stream-ordered device memory, fills and a device-wide
+// Error reporting, the device-memory block cache, fills and a device-wide
 // exclusive scan used by the rule-book builders.
 #include <cstdio>
 #include <mutex>
