@@ -1669,7 +1669,10 @@ static sscn_status launch_wgrad_reg(const T* X, const T* dY, const View& v, int 
     int cus = 256, per_cu = 1;
     occupancy((const void*)kern, 256, 0, &per_cu, &cus);
     const int64_t target = std::max<int64_t>(1, (int64_t)cus * per_cu / (nzc * nzo));
-    const int64_t tr2 = std::max<int64_t>(1, ceil_div(v.st->n_tiles * S, target));
+    // at most target / S tile ranges, so that the items fit one round
+    // (a few items left for a second round would double the kernel's time)
+    const int64_t ranges = std::max<int64_t>(1, target / S);
+    const int64_t tr2 = std::max<int64_t>(1, ceil_div(v.st->n_tiles, ranges));
     const int64_t total = ceil_div(v.st->n_tiles, tr2) * S;
     SSCN_TRY(fill_f32(dW, 0.f, (int64_t)v.K * cin * cout, s));
     kern<<<dim3((unsigned)total, (unsigned)(nzc * nzo)), 256, 0, s>>>(
