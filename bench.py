@@ -115,20 +115,21 @@ def _event_ms(fn, reps, stream):
     return e0.elapsed_time(e1) / reps
 
 
-def build_roofline(n, K, pairs, ms, what):
+def build_roofline(n, K, pairs, ms, what, slot=8):
     """Logical bytes of an SSC rule-book build against HBM bandwidth.
 
     Counted: coordinates read (16 B per site), the hash table filled and
-    written (16-byte slots, capacity the power of two >= 2n), one 16-byte
-    slot read per (site, offset) lookup, the offset-major neighbour map
-    written and read back (4 B per site and offset each way), the pair
-    arrays written (8 B per pair).  The time is the host wall time of the
-    build call (its row-block plan included).
+    written (slot bytes each: 8 for the 32-bit keys that both workloads
+    here use, capacity the power of two >= 2n), one slot read per (site,
+    offset) lookup, the offset-major neighbour map written and read back
+    (4 B per site and offset each way), the pair arrays written (8 B per
+    pair).  The time is the host wall time of the build call (its
+    row-block plan included).
     """
     cap = 64
     while cap < 2 * n:
         cap *= 2
-    nbytes = 16 * n + 16 * cap + 16 * n + 16 * K * n + 8 * K * n + 8 * pairs
+    nbytes = 16 * n + slot * cap + slot * n + slot * K * n + 8 * K * n + 8 * pairs
     achieved = nbytes / (ms * 1e-3) / 1e9
     return {"stage": what, "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": achieved / PEAK_HBM_GBS, "bytes": nbytes, "ms": ms}

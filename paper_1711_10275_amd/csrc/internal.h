@@ -42,6 +42,7 @@ constexpr int kMaxExtent = 1 << 16;
 // error flags raised by device code
 constexpr int kFlagOutOfRange = 1;
 constexpr int kFlagDuplicate = 2;
+constexpr int kFlagWideKey = 4;  // a batch index too large for 32-bit SSC keys
 
 // ---------------------------------------------------------------- errors
 void set_error(const std::string& msg);

@@ -1,10 +1,13 @@
 // Rule-book construction on the GPU (Sec. 4.2 of the paper).
 //
-// Dictionary: open addressing with linear probing in HBM.  A slot is 16
-// bytes {key, row}: the location (b, x0, x1, x2) packed into 64 bits (16
-// bits per field, b < 2^15 so no key equals the empty marker) and the
-// feature row, so one 16-byte load answers a probe.  Capacity is a power of
-// two >= 2n (load <= 1/2).
+// Dictionary: open addressing with linear probing in HBM.  A slot holds the
+// location (b, x0, x1, x2) as a key and the feature row.  SSC builds use
+// 8-byte slots {32-bit key, row} with the key the linear index
+// ((b L0 + x0) L1 + x1) L2 + x2 whenever every batch index present keeps it
+// below 2^32 - 1 (the empty marker); the insert flags a batch index beyond
+// that and the build is redone with 16-byte slots {64-bit key, row} (16
+// bits per field, b < 2^15 so no key equals the empty marker), which the SC
+// builds always use.  Capacity is a power of two >= 2n (load <= 1/2).
 //
 // Rule book layout: output rows are cut into tiles of kTile = 64 rows (one
 // wavefront); for every offset o and tile t the pairs whose output row lies
@@ -30,6 +33,7 @@
 // transposed (DC / dgrad) direction.
 #include <algorithm>
 #include <cstring>
+#include <type_traits>
 
 #include "internal.h"
 
@@ -73,8 +77,8 @@ __device__ __forceinline__ int32_t table_lookup(const Slot* __restrict__ table, 
 // Also zeroes the first n_zero words of `zero` (the build's counters).
 __global__ void k_fill_slots(Slot* __restrict__ table, uint64_t cap, int32_t row_init,
                              unsigned long long* __restrict__ zero, int n_zero) {
-  if (blockIdx.x == 0)
-    for (int i = threadIdx.x; i < n_zero; i += blockDim.x) zero[i] = 0;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_zero; i += (int64_t)gridDim.x * blockDim.x)
+    zero[i] = 0;
   for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < cap;
        i += (uint64_t)gridDim.x * blockDim.x) {
     Slot v;
@@ -87,6 +91,103 @@ __global__ void k_fill_slots(Slot* __restrict__ table, uint64_t cap, int32_t row
 
 __device__ __forceinline__ bool in_grid(int x0, int x1, int x2, int L0, int L1, int L2) {
   return (unsigned)x0 < (unsigned)L0 && (unsigned)x1 < (unsigned)L1 && (unsigned)x2 < (unsigned)L2;
+}
+
+// 8-byte slots: key in the low word, row in the high word; all ones = empty.
+constexpr uint32_t kEmptyKey32 = ~0u;
+
+__device__ __forceinline__ uint32_t pack_key32(int b, int x0, int x1, int x2, int L0, int L1, int L2) {
+  return (((uint32_t)b * (uint32_t)L0 + (uint32_t)x0) * (uint32_t)L1 + (uint32_t)x1) * (uint32_t)L2 +
+         (uint32_t)x2;
+}
+
+// 32-bit finaliser of MurmurHash3 (public domain).
+__device__ __forceinline__ uint32_t mix32(uint32_t h) {
+  h ^= h >> 16;
+  h *= 0x85ebca6bu;
+  h ^= h >> 13;
+  h *= 0xc2b2ae35u;
+  h ^= h >> 16;
+  return h;
+}
+
+// Home slot of a 32-bit key.  (Keeping runs of consecutive keys in
+// consecutive slots, so that x2 neighbours share a window, clusters the
+// table: the inserts and lookups then take longer, not shorter.)
+__device__ __forceinline__ uint32_t home8(uint32_t key, uint32_t mask) { return mix32(key) & mask; }
+
+// Every 8-byte slot empty; zeroes the first n_zero words of `zero`.
+__global__ void k_fill_slots8(uint4* __restrict__ table, uint64_t pairs,
+                              unsigned long long* __restrict__ zero, int n_zero) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_zero; i += (int64_t)gridDim.x * blockDim.x)
+    zero[i] = 0;
+  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < pairs;
+       i += (uint64_t)gridDim.x * blockDim.x)
+    table[i] = make_uint4(~0u, ~0u, ~0u, ~0u);
+}
+
+// Insert with 8-byte slots, in two passes so that most sites need no
+// atomic (device-wide atomics are far slower than stores):
+//  1. every site stores its word {key, row} into its home slot with a plain
+//     8-byte store; of the sites that share a home slot one word remains;
+//  2. every site reads its home slot back: its own word means it holds the
+//     slot; the same key with another row is a repeated location; otherwise
+//     the site probes on from the home slot with a 64-bit CAS per slot, as
+//     an ordinary linear-probing insert.
+// Slots never become empty again, so every slot between a key's home slot
+// and the slot that holds it is occupied, which is what lookups rely on.
+// batch_lim: batch indices below it keep every key of their sample below
+// the empty marker; a larger one raises kFlagWideKey and inserts nothing.
+__device__ __forceinline__ int site_check8(const int4& c, int L0, int L1, int L2, uint32_t batch_lim) {
+  if ((unsigned)c.x >= (unsigned)kMaxBatch || !in_grid(c.y, c.z, c.w, L0, L1, L2)) return kFlagOutOfRange;
+  if ((uint32_t)c.x >= batch_lim) return kFlagWideKey;
+  return 0;
+}
+
+__global__ __launch_bounds__(256) void k_insert8_store(const int4* __restrict__ coords, int64_t n, int L0, int L1,
+                                                       int L2, uint32_t batch_lim,
+                                                       unsigned long long* __restrict__ table, uint32_t mask,
+                                                       unsigned long long* __restrict__ flags,
+                                                       int4* __restrict__ copy) {
+  int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= n) return;
+  int4 c = coords[j];
+  if (copy) copy[j] = c;
+  const int bad = site_check8(c, L0, L1, L2, batch_lim);
+  if (bad) {
+    atomicOr(flags, (unsigned long long)bad);
+    return;
+  }
+  const uint32_t key = pack_key32(c.x, c.y, c.z, c.w, L0, L1, L2);
+  table[home8(key, mask)] = ((unsigned long long)(uint32_t)j << 32) | key;
+}
+
+__global__ __launch_bounds__(256) void k_insert8_fix(const int4* __restrict__ coords, int64_t n, int L0, int L1,
+                                                     int L2, uint32_t batch_lim,
+                                                     unsigned long long* __restrict__ table, uint32_t mask,
+                                                     unsigned long long* __restrict__ flags) {
+  int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= n) return;
+  const int4 c = coords[j];
+  if (site_check8(c, L0, L1, L2, batch_lim)) return;
+  const uint32_t key = pack_key32(c.x, c.y, c.z, c.w, L0, L1, L2);
+  const unsigned long long word = ((unsigned long long)(uint32_t)j << 32) | key;
+  uint32_t slot = home8(key, mask);
+  const unsigned long long home = table[slot];
+  if (home == word) return;
+  if ((uint32_t)home == key) {
+    atomicOr(flags, (unsigned long long)kFlagDuplicate);
+    return;
+  }
+  while (true) {
+    slot = (slot + 1) & mask;
+    const unsigned long long prev = atomicCAS(&table[slot], ~0ull, word);
+    if (prev == ~0ull) return;
+    if ((uint32_t)prev == key) {
+      atomicOr(flags, (unsigned long long)kFlagDuplicate);
+      return;
+    }
+  }
 }
 
 // Insert every site; flag coordinates outside the grid and repeated
@@ -136,10 +237,10 @@ __global__ __launch_bounds__(256) void k_insert(const int4* __restrict__ coords,
 // Inputs from this many sites on use the mirrored SSC probe.
 constexpr int64_t kMirrorProbeMin = 1 << 18;
 
-template <int P>
+template <int P, bool NARROW>
 __global__ __launch_bounds__(256) void k_ssc_probe(
     const int4* __restrict__ coords, int64_t n, int L0, int L1, int L2, int f,
-    const Slot* __restrict__ table, uint64_t mask, int32_t* __restrict__ nbr, int64_t* __restrict__ counts,
+    const void* __restrict__ table_v, uint64_t mask, int32_t* __restrict__ nbr, int64_t* __restrict__ counts,
     int64_t n_tiles, int mirror) {
   const int lane = threadIdx.x & 63;
   const int plane = f * f, K = f * f * f;
@@ -160,18 +261,33 @@ __global__ __launch_bounds__(256) void k_ssc_probe(
   const int h = (f - 1) / 2;
   const int o0 = (int)(lb % slices) * P;
   if (mirror && o0 == 0 && valid) nbr[(int64_t)ctr * n + k] = site_ok ? (int32_t)k : -1;
-  // A lookup reads the whole aligned 64-byte line (4 slots) that holds its
-  // first slot, and the following lines while the probe sequence runs on
-  // (linear probing: stop at the key or at an empty slot), so most lookups
-  // take a single round trip.
-  uint64_t key[P];
+  // A lookup reads the aligned window of 4 slots that holds its first slot
+  // (64 bytes of 16-byte slots, 32 of 8-byte ones), and the following
+  // windows while the probe sequence runs on (linear probing: stop at the
+  // key or at an empty slot), so most lookups take a single round trip.
+  using Key = typename std::conditional<NARROW, uint32_t, uint64_t>::type;
+  Key key[P];
   uint64_t slot[P];
   bool live[P];
-  Slot v[P][4];
-  auto read_line = [&](int q) {
-    const uint64_t line = slot[q] & ~3ull;
+  Key vk[P][4];
+  int32_t vr[P][4];
+  auto window = [&](uint64_t sl) -> uint64_t { return sl & ~3ull; };
+  auto read_window = [&](int q) {
+    const uint64_t w = window(slot[q]);
+    if constexpr (NARROW) {
+      const uint4* t = reinterpret_cast<const uint4*>(reinterpret_cast<const uint64_t*>(table_v) + w);
+      const uint4 a = t[0], b = t[1];
+      vk[q][0] = a.x; vr[q][0] = (int32_t)a.y; vk[q][1] = a.z; vr[q][1] = (int32_t)a.w;
+      vk[q][2] = b.x; vr[q][2] = (int32_t)b.y; vk[q][3] = b.z; vr[q][3] = (int32_t)b.w;
+    } else {
+      const Slot* t = reinterpret_cast<const Slot*>(table_v) + w;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) v[q][j] = table[line + j];
+      for (int j = 0; j < 4; ++j) {
+        const Slot e = t[j];
+        vk[q][j] = e.key;
+        vr[q][j] = e.row;
+      }
+    }
   };
 #pragma unroll
   for (int q = 0; q < P; ++q) {
@@ -179,10 +295,16 @@ __global__ __launch_bounds__(256) void k_ssc_probe(
     const int i0 = o / plane, i1 = (o / f) % f, i2 = o % f;
     const int y0 = c.y + i0 - h, y1 = c.z + i1 - h, y2 = c.w + i2 - h;
     live[q] = o < o_end && site_ok && in_grid(y0, y1, y2, L0, L1, L2);
-    key[q] = pack_key(c.x, y0, y1, y2);
-    slot[q] = mix64(key[q]) & mask;
-    if (live[q]) read_line(q);
+    if constexpr (NARROW) {
+      key[q] = pack_key32(c.x, y0, y1, y2, L0, L1, L2);
+      slot[q] = home8(key[q], (uint32_t)mask);
+    } else {
+      key[q] = pack_key(c.x, y0, y1, y2);
+      slot[q] = mix64(key[q]) & mask;
+    }
+    if (live[q]) read_window(q);
   }
+  constexpr Key kEmpty = NARROW ? (Key)kEmptyKey32 : (Key)kEmptyKey;
 #pragma unroll
   for (int q = 0; q < P; ++q) {
     const int o = o0 + q;
@@ -190,21 +312,21 @@ __global__ __launch_bounds__(256) void k_ssc_probe(
     int32_t row = -1;
     bool done = !live[q];
     while (!done) {
-      const int from = (int)(slot[q] & 3);
+      const int from = (int)(slot[q] - window(slot[q]));
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         if (!done && j >= from) {
-          if (v[q][j].key == key[q]) {
-            row = v[q][j].row;
+          if (vk[q][j] == key[q]) {
+            row = vr[q][j];
             done = true;
-          } else if (v[q][j].key == kEmptyKey) {
+          } else if (vk[q][j] == kEmpty) {
             done = true;
           }
         }
       }
       if (!done) {
-        slot[q] = ((slot[q] | 3) + 1) & mask;  // first slot of the next line
-        read_line(q);
+        slot[q] = (window(slot[q]) + 4) & mask;  // first slot of the next window
+        read_window(q);
       }
     }
     if (valid) nbr[(int64_t)o * n + k] = row;
@@ -1292,9 +1414,12 @@ __global__ __launch_bounds__(kOneBlock) void k_plan_order(const int32_t* __restr
 // Row-block plan of one direction (seg and pair arrays complete), in the
 // rule book's own blocks.  ppo_bound >= 0: the pair counts are not on the
 // host yet (the plan is queued inside the build); at most ppo_bound pairs
-// per offset, and room for nb K items.
+// per offset, and room for nb K items.  hist0: plan_hist_words(K) zeroed
+// words for the key histogram, or NULL.
+static int64_t plan_hist_words(int K) { return (1 << std::min(K, kPlanKeyBits)) + 1; }
+
 static sscn_status build_plan(RulebookData* d, Storage& st, int64_t n_rows, int K, hipStream_t s,
-                              int64_t ppo_bound = -1) {
+                              int64_t ppo_bound = -1, int32_t* hist0 = nullptr) {
   const int64_t nb = ceil_div(n_rows, kPlanRows);
   st.n_blocks = nb;
   const int64_t cap =
@@ -1308,9 +1433,9 @@ static sscn_status build_plan(RulebookData* d, Storage& st, int64_t n_rows, int 
   if (nb == 0) return fill_i32(st.b_first, 0, 1, s);
   const int bins = 1 << std::min(K, kPlanKeyBits);
   Temps tmp(s);
-  uint32_t* mask = st.row_mask; uint32_t* bmask; int32_t* hist; int32_t* pos_of;
+  uint32_t* mask = st.row_mask; uint32_t* bmask; int32_t* hist = nullptr; int32_t* pos_of;
   Arena t;
-  t.add(&hist, (size_t)bins + 1);
+  if (!(hist0 && mask)) t.add(&hist, (size_t)bins + 1);
   if (!mask) t.add(&mask, (size_t)n_rows);  // right after hist: one fill clears both
   t.add(&bmask, (size_t)nb);
   t.add(&pos_of, (size_t)n_rows);
@@ -1319,7 +1444,8 @@ static sscn_status build_plan(RulebookData* d, Storage& st, int64_t n_rows, int 
   if (ppo_bound < 0)
     for (int64_t c : d->pairs_per_offset) max_ppo = std::max(max_ppo, c);
   if (st.row_mask) {
-    SSCN_TRY(fill_i32(hist, 0, bins + 1, s));
+    if (hist0) hist = hist0;
+    else SSCN_TRY(fill_i32(hist, 0, bins + 1, s));
   } else {
     SSCN_TRY(fill_i32(hist, 0, (int32_t*)(mask + n_rows) - hist, s));
     if (max_ppo > 0) {
@@ -1412,16 +1538,15 @@ static sscn_status new_handle(RulebookData* d, sscn_rulebook* out) {
   return SSCN_OK;
 }
 
-}  // namespace sscn
-
-using namespace sscn;
-
-extern "C" sscn_status ssc_rulebook_build(const int32_t* coords, int64_t n, const int32_t* spatial_size,
-                                          int32_t filter_size, hipStream_t stream, sscn_rulebook* out) {
-  SSCN_TRY(check_common(coords, n, spatial_size, filter_size, out));
-  if (filter_size % 2 == 0) return fail(SSCN_ERR_INVALID_ARG, "SSC needs an odd filter_size");
+// SSC build with 8-byte dictionary slots (batch_lim > 0: batch indices
+// below batch_lim keep the 32-bit keys below the empty marker) or 16-byte
+// ones (batch_lim == 0).  Sets *wide and builds nothing when a batch index
+// reaches batch_lim.
+static sscn_status ssc_build(const int32_t* coords, int64_t n, const int32_t* spatial_size, int32_t filter_size,
+                             hipStream_t stream, uint32_t batch_lim, bool* wide, sscn_rulebook* out) {
   const int f = filter_size, K = f * f * f;
   const int L0 = spatial_size[0], L1 = spatial_size[1], L2 = spatial_size[2];
+  const bool narrow = batch_lim > 0;
   hipStream_t s = stream;
 
   RulebookData* d = new (std::nothrow) RulebookData;
@@ -1439,18 +1564,25 @@ extern "C" sscn_status ssc_rulebook_build(const int32_t* coords, int64_t n, cons
   {
     Temps tmp(s);
     const uint64_t cap = table_capacity(n);
-    Slot* table; int32_t* nbr; int64_t* counts; unsigned long long* stats;
+    Slot* table = nullptr; unsigned long long* table8 = nullptr;
+    int32_t* nbr; int64_t* counts; unsigned long long* stats; int32_t* hist = nullptr;
+    // With K <= 32 the row-block plan is queued before the readback too: its
+    // launches overlap the build's kernels and the host waits once.
+    const bool one_phase = (uint64_t)K * (uint64_t)n * 8u <= (512ull << 20);
+    const bool eager_plan = one_phase && n > 0 && K <= 32 && n < (int64_t)kPlanNoRow;
     Arena ta;
-    ta.add(&table, cap);
+    if (narrow) ta.add(&table8, cap); else ta.add(&table, cap);
     ta.add(&nbr, (size_t)K * n);
     ta.add(&counts, (size_t)K * n_tiles + 1);
     ta.add(&stats, 1 + K);
+    if (eager_plan) ta.add(&hist, (size_t)plan_hist_words(K));  // right after stats: one fill clears both
     SSCN_TRY(tmp.alloc(ta));
+    const int n_zero =
+        (int)ceil_div(hist ? (char*)(hist + plan_hist_words(K)) - (char*)stats : (int64_t)(1 + K) * 8, 8);
     // Pair storage for the worst case (every offset of every site) when that
-    // is modest: then it shares one allocation with the rest of the rule
-    // book, compaction is queued before the one readback, and the host waits
-    // once.  Otherwise the exact size comes from the readback first.
-    const bool one_phase = (uint64_t)K * (uint64_t)n * 8u <= (512ull << 20);
+    // is modest (one_phase): then it shares one allocation with the rest of
+    // the rule book, compaction is queued before the one readback, and the
+    // host waits once.  Otherwise the exact size comes from the readback first.
     auto add_pairs = [&](Arena& pa, int64_t cap_pairs) {
       pa.add(&d->fwd.in_rows, cap_pairs);
       pa.add(&d->fwd.out_rows, cap_pairs);
@@ -1463,10 +1595,23 @@ extern "C" sscn_status ssc_rulebook_build(const int32_t* coords, int64_t n, cons
     if (one_phase) add_pairs(oa, (int64_t)K * n);
     SSCN_TRY(owned_alloc(d, oa, s));
 
-    SSCN_TRY(launch_fill_slots(table, cap, -1, s, stats, 1 + K));
+    if (narrow) {
+      k_fill_slots8<<<(unsigned)std::min<uint64_t>((cap / 2 + 255) / 256, 16384), 256, 0, s>>>(
+          (uint4*)table8, cap / 2, stats, n_zero);
+      SSCN_HIP(hipGetLastError());
+    } else {
+      SSCN_TRY(launch_fill_slots(table, cap, -1, s, stats, n_zero));
+    }
     if (n > 0) {
-      k_insert<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, L0, L1, L2, table, cap - 1, stats,
-                                               (int4*)d->out_coords);
+      if (narrow) {
+        k_insert8_store<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, L0, L1, L2, batch_lim, table8,
+                                                        (uint32_t)(cap - 1), stats, (int4*)d->out_coords);
+        SSCN_HIP(hipGetLastError());
+        k_insert8_fix<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, L0, L1, L2, batch_lim, table8,
+                                                      (uint32_t)(cap - 1), stats);
+      } else
+        k_insert<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, L0, L1, L2, table, cap - 1, stats,
+                                                 (int4*)d->out_coords);
       SSCN_HIP(hipGetLastError());
       constexpr int P = 3;  // lookups per wavefront
       // mirrored lookups halve the table reads; they cost two more launches,
@@ -1475,8 +1620,13 @@ extern "C" sscn_status ssc_rulebook_build(const int32_t* coords, int64_t n, cons
       const int c = (K - 1) / 2;  // centre offset
       if (mirror) SSCN_TRY(fill_i32(nbr + (int64_t)(c + 1) * n, -1, (int64_t)(K - 1 - c) * n, s));
       const int64_t slices = std::max<int64_t>(ceil_div(mirror ? c : K, P), 1);
-      k_ssc_probe<P><<<(unsigned)(grid_for(n_tiles * 64, 256) * slices), 256, 0, s>>>(
-          (const int4*)coords, n, L0, L1, L2, f, table, cap - 1, nbr, counts, n_tiles, mirror ? 1 : 0);
+      const unsigned grid = (unsigned)(grid_for(n_tiles * 64, 256) * slices);
+      if (narrow)
+        k_ssc_probe<P, true><<<grid, 256, 0, s>>>((const int4*)coords, n, L0, L1, L2, f, table8, cap - 1, nbr,
+                                                   counts, n_tiles, mirror ? 1 : 0);
+      else
+        k_ssc_probe<P, false><<<grid, 256, 0, s>>>((const int4*)coords, n, L0, L1, L2, f, table, cap - 1, nbr,
+                                                    counts, n_tiles, mirror ? 1 : 0);
       SSCN_HIP(hipGetLastError());
       if (mirror) {
         k_count_nbr<<<grid_for(n_tiles * 64, 256), 256, 0, s>>>(nbr, n, K, counts, n_tiles, c);
@@ -1499,16 +1649,17 @@ extern "C" sscn_status ssc_rulebook_build(const int32_t* coords, int64_t n, cons
       return SSCN_OK;
     };
     if (one_phase) SSCN_TRY(compact());
-    // With K <= 32 the row-block plan is queued before the readback too: its
-    // launches overlap the build's kernels and the host waits once.
-    const bool eager_plan = one_phase && n > 0 && K <= 32 && n < (int64_t)kPlanNoRow;
     if (eager_plan) {
-      SSCN_TRY(build_plan(d, d->fwd, n, K, s, /*a site has one neighbour per offset*/ n));
+      SSCN_TRY(build_plan(d, d->fwd, n, K, s, /*a site has one neighbour per offset*/ n, hist));
       SSCN_HIP(hipEventCreateWithFlags(&d->plan_ready, hipEventDisableTiming));
       SSCN_HIP(hipEventRecord(d->plan_ready, s));
     }
     std::vector<unsigned long long> host(1 + K);
     SSCN_TRY(readback(host.data(), stats, sizeof(unsigned long long) * (1 + K), s));
+    if (!(host[0] & kFlagOutOfRange) && (host[0] & kFlagWideKey)) {
+      *wide = true;  // the queued work is discarded with d and the temporaries
+      return SSCN_OK;
+    }
     SSCN_TRY(flags_error(host[0]));
     int64_t total = 0;
     for (int o = 0; o < K; ++o) total += (d->pairs_per_offset[o] = (int64_t)host[1 + o]);
@@ -1522,6 +1673,26 @@ extern "C" sscn_status ssc_rulebook_build(const int32_t* coords, int64_t n, cons
   }
   guard.release();
   return new_handle(d, out);
+}
+
+}  // namespace sscn
+
+using namespace sscn;
+
+extern "C" sscn_status ssc_rulebook_build(const int32_t* coords, int64_t n, const int32_t* spatial_size,
+                                          int32_t filter_size, hipStream_t stream, sscn_rulebook* out) {
+  SSCN_TRY(check_common(coords, n, spatial_size, filter_size, out));
+  if (filter_size % 2 == 0) return fail(SSCN_ERR_INVALID_ARG, "SSC needs an odd filter_size");
+  // 32-bit keys while one sample's keys stay below the empty marker 2^32 - 1
+  const uint64_t vol = (uint64_t)spatial_size[0] * (uint64_t)spatial_size[1] * (uint64_t)spatial_size[2];
+  const uint64_t lim = 0xFFFFFFFFull / vol;
+  bool wide = false;
+  if (lim > 0) {
+    SSCN_TRY(ssc_build(coords, n, spatial_size, filter_size, stream, (uint32_t)std::min<uint64_t>(lim, kMaxBatch),
+                       &wide, out));
+    if (!wide) return SSCN_OK;
+  }
+  return ssc_build(coords, n, spatial_size, filter_size, stream, 0, &wide, out);
 }
 
 extern "C" sscn_status sc_rulebook_build(const int32_t* coords, int64_t n, const int32_t* spatial_size,
