@@ -1411,6 +1411,55 @@ __global__ __launch_bounds__(kOneBlock) void k_plan_order(const int32_t* __restr
   }
 }
 
+// k_plan_order with the scan of the item counts before it, in one
+// workgroup (nb <= kSmallScanMax): cnt[b] (items of block b) becomes
+// b_first (exclusive scan, b_first[nb] = total) and order lists the blocks
+// by decreasing count.  The counts stay in LDS for the second pass.
+__global__ __launch_bounds__(kOneBlock) void k_plan_scan_order(int32_t* __restrict__ cnt, int64_t nb, int K,
+                                                               int32_t* __restrict__ order) {
+  constexpr int NW = kOneBlock / 64;
+  __shared__ uint8_t c8[kSmallScanMax];
+  __shared__ int32_t hist[64], cur[64], wsum[NW];
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  if (t < 64) hist[t] = 0;
+  __syncthreads();
+  int carry = 0;
+  for (int64_t b0 = 0; b0 < nb; b0 += kOneBlock) {
+    const int64_t b = b0 + t;
+    const bool ok = b < nb;
+    const int v = ok ? cnt[b] : 0;
+    if (ok) c8[b] = (uint8_t)v;
+    const int inc = wave_inclusive_scan(v);
+    if (lane == 63) wsum[wave] = inc;
+    __syncthreads();
+    int before = carry, total = 0;
+    for (int w = 0; w < NW; ++w) {
+      const int x = wsum[w];
+      before += w < wave ? x : 0;
+      total += x;
+    }
+    if (ok) cnt[b] = before + inc - v;
+    carry += total;
+    (void)wave_count<6>(hist, ok ? (uint32_t)(K - v) : 0u, ok);
+    __syncthreads();  // wsum is rewritten by the next chunk
+  }
+  if (t == 0) {
+    cnt[nb] = carry;
+    int run = 0;
+    for (int c = 0; c <= K; ++c) {
+      cur[c] = run;
+      run += hist[c];
+    }
+  }
+  __syncthreads();
+  for (int64_t b0 = 0; b0 < nb; b0 += kOneBlock) {
+    const int64_t b = b0 + t;
+    const bool ok = b < nb;
+    const int p = wave_count<6>(cur, ok ? (uint32_t)(K - c8[b]) : 0u, ok);
+    if (ok) order[p] = (int32_t)b;
+  }
+}
+
 // Row-block plan of one direction (seg and pair arrays complete), in the
 // rule book's own blocks.  ppo_bound >= 0: the pair counts are not on the
 // host yet (the plan is queued inside the build); at most ppo_bound pairs
@@ -1469,8 +1518,12 @@ static sscn_status build_plan(RulebookData* d, Storage& st, int64_t n_rows, int 
   SSCN_HIP(hipGetLastError());
   k_plan_blocks<<<grid_for(nb * 64, 256), 256, 0, s>>>(mask, st.perm, n_rows, nb, bmask, st.b_first);
   SSCN_HIP(hipGetLastError());
-  SSCN_TRY(scan_i32(st.b_first, nb, s));
-  k_plan_order<<<1, kOneBlock, 0, s>>>(st.b_first, nb, K, st.b_order);
+  if (nb <= kSmallScanMax) {
+    k_plan_scan_order<<<1, kOneBlock, 0, s>>>(st.b_first, nb, K, st.b_order);
+  } else {
+    SSCN_TRY(scan_i32(st.b_first, nb, s));
+    k_plan_order<<<1, kOneBlock, 0, s>>>(st.b_first, nb, K, st.b_order);
+  }
   SSCN_HIP(hipGetLastError());
   k_plan_items<<<grid_for(nb * kPlanRows, 256), 256, 0, s>>>(bmask, st.b_first, nb, st.items);
   SSCN_HIP(hipGetLastError());
