@@ -271,6 +271,7 @@ __global__ __launch_bounds__(256) void k_ssc_probe(
   bool live[P];
   Key vk[P][4];
   int32_t vr[P][4];
+  // (2-slot windows of the 8-byte table probe as fast; 8-slot ones slower)
   auto window = [&](uint64_t sl) -> uint64_t { return sl & ~3ull; };
   auto read_window = [&](int q) {
     const uint64_t w = window(slot[q]);
@@ -363,15 +364,18 @@ __global__ __launch_bounds__(256) void k_count_nbr(const int32_t* __restrict__ n
 
 // Write every present entry at its segment start + its rank among the
 // wavefront's present entries (so segments are sorted by output row).  With
-// row_mask (K <= 32), also the set of offsets present for each row.
+// row_mask (K <= 32), also the set of offsets present for each row.  One
+// workgroup per tile: wavefront w takes the offsets o = w mod 4 (four times
+// the wavefronts of one per tile, to keep more reads in flight), and the
+// row masks of the four are combined in LDS.
 __global__ __launch_bounds__(256) void k_compact(const int32_t* __restrict__ nbr, int64_t n_rows, int K,
                                                  const int64_t* __restrict__ seg, int64_t n_tiles,
                                                  int32_t* __restrict__ in_rows,
                                                  int32_t* __restrict__ out_rows,
                                                  uint32_t* __restrict__ row_mask) {
-  const int lane = threadIdx.x & 63;
-  const int64_t t = (int64_t)blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6);
-  if (t >= n_tiles) return;
+  __shared__ uint32_t part[4][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t t = blockIdx.x;  // one workgroup per tile
   const int64_t k = t * kTile + lane;
   const bool valid = k < n_rows;
   const unsigned long long below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
@@ -384,18 +388,20 @@ __global__ __launch_bounds__(256) void k_compact(const int32_t* __restrict__ nbr
     if (lane + 64 < K) s_hi = seg[(int64_t)(lane + 64) * n_tiles + t];
   }
   uint32_t present = 0;
-  // the rows of up to 8 offsets are requested together (one round trip per 8)
+  // the rows of up to 8 of the wavefront's offsets are requested together
+  // (one round trip per 8)
   constexpr int B = 8;
   int32_t rows[B];
-  for (int o = 0; o < K; ++o) {
-    if (o % B == 0) {
+  for (int i = 0, o = wave; o < K; ++i, o += 4) {
+    if (i % B == 0) {
 #pragma unroll
-      for (int q = 0; q < B; ++q) rows[q] = (valid && o + q < K) ? nbr[(int64_t)(o + q) * n_rows + k] : -1;
+      for (int q = 0; q < B; ++q)
+        rows[q] = (valid && o + 4 * q < K) ? nbr[(int64_t)(o + 4 * q) * n_rows + k] : -1;
     }
     int32_t row = rows[0];
 #pragma unroll
     for (int q = 1; q < B; ++q)
-      if (o % B == q) row = rows[q];
+      if (i % B == q) row = rows[q];
     const unsigned long long m = __ballot(row >= 0);
     int64_t start;
     if (seg_regs) {
@@ -413,7 +419,10 @@ __global__ __launch_bounds__(256) void k_compact(const int32_t* __restrict__ nbr
       present |= 1u << (o & 31);
     }
   }
-  if (row_mask && valid) row_mask[k] = present;
+  if (!row_mask) return;  // uniform
+  part[wave][lane] = present;
+  __syncthreads();
+  if (wave == 0 && valid) row_mask[k] = part[0][lane] | part[1][lane] | part[2][lane] | part[3][lane];
 }
 
 // ------------------------------------------------------------- tile order
@@ -1008,7 +1017,7 @@ static sscn_status compact_storage(const int32_t* nbr, int64_t n_rows, int K, St
     }
   }
   if (st.n_tiles > 0) {
-    k_compact<<<grid_for(st.n_tiles * 64, 256), 256, 0, s>>>(nbr, n_rows, K, st.seg, st.n_tiles, st.in_rows,
+    k_compact<<<(unsigned)st.n_tiles, 256, 0, s>>>(nbr, n_rows, K, st.seg, st.n_tiles, st.in_rows,
                                                              st.out_rows, K <= 32 ? row_mask : nullptr);
     SSCN_HIP(hipGetLastError());
   }
