@@ -182,3 +182,51 @@ def test_dictionary_key_widths(size, batches):
     with pytest.raises(sscn.SSCNError) as e:
         sscn.ssc_rulebook_build(dev(dup), size, 3)
     assert e.value.code == "duplicate"
+
+
+def _home_slot(key, cap):
+    """Home slot of a 32-bit SSC dictionary key (the MurmurHash3 32-bit
+    finaliser of the key, masked to the power-of-two capacity)."""
+    h = key & 0xFFFFFFFF
+    h ^= h >> 16
+    h = (h * 0x85EBCA6B) & 0xFFFFFFFF
+    h ^= h >> 13
+    h = (h * 0xC2B2AE35) & 0xFFFFFFFF
+    h ^= h >> 16
+    return h & (cap - 1)
+
+
+def test_insert_collisions_and_repeats():
+    """The SSC insert stores every site into its home slot, then lets the
+    sites that lost it probe on with CAS.  Sites whose keys share a home
+    slot must all be found, and a repeated location must be reported also
+    when both copies lost their home slot to a third key."""
+    size = (64, 64, 64)
+    rng = np.random.default_rng(7)
+    cells = rng.permutation(64 ** 3)[:4000]
+    pts = np.stack(np.unravel_index(cells, size), axis=1).astype(np.int64)
+    keys = (pts[:, 0] * 64 + pts[:, 1]) * 64 + pts[:, 2]
+    triples = 12
+    n = 3 * triples
+    cap = 64
+    while cap < 2 * (n + 1):
+        cap *= 2
+    by_home = {}
+    for i, k in enumerate(keys):
+        by_home.setdefault(_home_slot(int(k), cap), []).append(i)
+    groups = [v[:2] for v in by_home.values() if len(v) >= 2][:triples]
+    assert len(groups) == triples
+    sites = []
+    for a, c in groups:  # two different locations with one home slot, the first twice
+        sites += [pts[c], pts[a], pts[a]]
+    with_rep = np.concatenate([np.zeros((len(sites), 1), np.int64), np.array(sites)], axis=1).astype(np.int32)
+    for seed in range(4):
+        perm = np.random.default_rng(seed).permutation(with_rep.shape[0])
+        with pytest.raises(sscn.SSCNError) as e:
+            sscn.ssc_rulebook_build(dev(np.ascontiguousarray(with_rep[perm])), size, 3)
+        assert e.value.code == "duplicate"
+    # without the repeats: every colliding site is found (rule book exact)
+    uniq = np.ascontiguousarray(with_rep[np.sort(np.unique(with_rep, axis=0, return_index=True)[1])])
+    for f in (3, 5):
+        assert_same_rulebook(sscn.ssc_rulebook_build(dev(uniq), size, f), O.ssc_rulebook(uniq, size, f),
+                             f"colliding keys f={f}")
