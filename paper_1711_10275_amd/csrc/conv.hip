@@ -523,7 +523,11 @@ __global__ __launch_bounds__(256) void k_conv_quad(
 // step; each wavefront's row tile is private to it.  The plan entries are
 // read from global memory (L2) a step ahead of their use, which keeps the
 // LDS footprint small (27 KB for 128-byte windows: five workgroups per CU).
-template <typename T, int WB, int NB, int D, int PK>
+// TB: B is stored [o][kdim][ncols] instead (the forward's weights as given);
+// a thread then loads 16 bytes of one reduction channel (4 output columns)
+// and writes them to the 4 columns' rows of the weight tile, which spares
+// the forward a transposed copy of W.
+template <typename T, int WB, int NB, int D, int PK, bool TB = false>
 __device__ __forceinline__ void conv_rows_block(
     const T* __restrict__ X, uint32_t x_bytes, const T* __restrict__ B, uint32_t b_bytes,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ b_first, const uint32_t* __restrict__ items,
@@ -565,11 +569,22 @@ __device__ __forceinline__ void conv_rows_block(
 #pragma unroll
     for (int q = 0; q < NBP; ++q) {
       const int p = tid + 256 * q;
-      b_col[q] = p / LPR;
-      b_byte[q] = (uint32_t)(p % LPR) * 16;
-      b_u[q] = PK > 1 ? (int)(b_byte[q] / row_bytes) : 0;
-      const int col = col0 + b_col[q];
-      b_base[q] = (b_col[q] < COLS && col < ncols) ? (uint32_t)col * row_bytes : kOobOffset;
+      if constexpr (TB) {
+        static_assert(PK == 1, "TB reads one item per step");
+        constexpr int PPC = COLS / 4;  // 16-byte pieces per reduction channel
+        const int ch = p / PPC;        // reduction channel within the window
+        b_col[q] = (p % PPC) * 4;
+        b_byte[q] = (uint32_t)ch * sizeof(T);
+        b_u[q] = 0;
+        const int col = col0 + b_col[q];
+        b_base[q] = (ch < WB / (int)sizeof(T) && col < ncols) ? (uint32_t)col * sizeof(T) : kOobOffset;
+      } else {
+        b_col[q] = p / LPR;
+        b_byte[q] = (uint32_t)(p % LPR) * 16;
+        b_u[q] = PK > 1 ? (int)(b_byte[q] / row_bytes) : 0;
+        const int col = col0 + b_col[q];
+        b_base[q] = (b_col[q] < COLS && col < ncols) ? (uint32_t)col * row_bytes : kOobOffset;
+      }
     }
 
     // items for which this wavefront's 16 rows have at least one pair (bit
@@ -646,8 +661,11 @@ __device__ __forceinline__ void conv_rows_block(
 #pragma unroll
       for (int q = 0; q < NBP; ++q) {
         const bool ok = live && win + b_byte[q] < row_bytes && b_base[q] != kOobOffset;
-        const auto v = __builtin_amdgcn_raw_buffer_load_b128(
-            rb, (int)(ok ? b_base[q] + win + b_byte[q] : kOobOffset), (int)((uint32_t)ow * w_stride), 0);
+        // TB: row (win + b_byte) / sizeof(T) of the offset's kdim x ncols matrix
+        const uint32_t off = TB ? (win + b_byte[q]) / (uint32_t)sizeof(T) * ((uint32_t)ncols * sizeof(T)) + b_base[q]
+                                : b_base[q] + win + b_byte[q];
+        const auto v = __builtin_amdgcn_raw_buffer_load_b128(rb, (int)(ok ? off : kOobOffset),
+                                                             (int)((uint32_t)ow * w_stride), 0);
         gb[slot][q] = make_uint4(v[0], v[1], v[2], v[3]);
       }
       if (++ld_ks == ks_n) { ld_ks = 0; ++ld_item; }
@@ -659,8 +677,19 @@ __device__ __forceinline__ void conv_rows_block(
       for (int i = 0; i < NA; ++i)
         *reinterpret_cast<uint4*>(&As[wave][a_row[i] * PITCH + a_byte]) = ga[slot][i];
 #pragma unroll
-      for (int q = 0; q < NBP; ++q)
-        if (b_col[q] < COLS) *reinterpret_cast<uint4*>(&Bs[buf][b_col[q] * PITCH + b_byte[q]]) = gb[slot][q];
+      for (int q = 0; q < NBP; ++q) {
+        if constexpr (TB) {
+          // 4 consecutive columns of one channel: one element in each column's row
+          if (b_byte[q] >= (uint32_t)WB) continue;  // (never, when the pieces fill the threads exactly)
+          char* dst = &Bs[buf][b_col[q] * PITCH + b_byte[q]];
+          *reinterpret_cast<uint32_t*>(dst) = gb[slot][q].x;
+          *reinterpret_cast<uint32_t*>(dst + PITCH) = gb[slot][q].y;
+          *reinterpret_cast<uint32_t*>(dst + 2 * PITCH) = gb[slot][q].z;
+          *reinterpret_cast<uint32_t*>(dst + 3 * PITCH) = gb[slot][q].w;
+        } else if (b_col[q] < COLS) {
+          *reinterpret_cast<uint4*>(&Bs[buf][b_col[q] * PITCH + b_byte[q]]) = gb[slot][q];
+        }
+      }
     };
     int mul_item = 0, mul_ks = 0;  // item of the step being multiplied
     auto multiply = [&](int buf) {
@@ -773,7 +802,7 @@ __device__ __forceinline__ void conv_rows_block(
   }
 }
 
-template <typename T, int WB, int NB, int D, int PK>
+template <typename T, int WB, int NB, int D, int PK, bool TB = false>
 __global__ __launch_bounds__(256, WB == 64 ? 6 : 5) void k_conv_rows(
     const T* __restrict__ X, uint32_t x_bytes, const T* __restrict__ B, uint32_t b_bytes,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ b_first, const int32_t* __restrict__ b_order,
@@ -808,7 +837,7 @@ __global__ __launch_bounds__(256, WB == 64 ? 6 : 5) void k_conv_rows(
   }
   for (int64_t idx = wg, round = 0; idx < n_blocks; idx = next(++round)) {
     __syncthreads();  // the previous block's LDS is free
-    conv_rows_block<T, WB, NB, D, PK>(X, x_bytes, B, b_bytes, perm, b_first, items, b_order[idx], K, mirror, kdim,
+    conv_rows_block<T, WB, NB, D, PK, TB>(X, x_bytes, B, b_bytes, perm, b_first, items, b_order[idx], K, mirror, kdim,
                                   ncols, Y, As, Bs, tid, wave, lane, m, g, col0);
   }
 }
@@ -1414,7 +1443,7 @@ static bool rows_eligible(const View& v, int kdim, int ncols) {
          std::max(v.n_in, v.n_out) < (int64_t)kPlanNoRow && ceil_div(v.n_out, kPlanRows) * v.K < INT32_MAX;
 }
 
-template <typename T, int WB, int NB, int PK = 1>
+template <typename T, int WB, int NB, int PK = 1, bool TB = false>
 static sscn_status launch_rows_nb(const T* X, const T* B, const View& v, int kdim, int ncols, const Heads<T>& Y,
                                   hipStream_t s) {
   const int64_t nb = v.st->n_blocks;
@@ -1424,7 +1453,7 @@ static sscn_status launch_rows_nb(const T* X, const T* B, const View& v, int kdi
   const uint32_t bb = (uint32_t)((uint64_t)v.K * ncols * kdim * sizeof(T));
   // loads two steps ahead for 64-byte windows (short steps), one otherwise;
   // six workgroups per CU for 64-byte windows (80 VGPRs), five otherwise
-  auto kern = k_conv_rows<T, WB, NB, WB == 64 ? 3 : 2, PK>;
+  auto kern = k_conv_rows<T, WB, NB, WB == 64 ? 3 : 2, PK, TB>;
   int cus = 256, per_cu = 1;
   occupancy((const void*)kern, 256, 0, &per_cu, &cus);
   // persistent: one resident wave of workgroups per column group
@@ -1435,9 +1464,20 @@ static sscn_status launch_rows_nb(const T* X, const T* B, const View& v, int kdi
   return SSCN_OK;
 }
 
+// Whether the forward hands launch_rows B as [o][kdim][ncols] (TB): fp32,
+// whole 16-byte pieces of 4 columns, one item per step, and 32-column
+// groups.  There the per-element LDS writes of the half-size weight tile
+// cost less than the transposed copy (SC 64 -> 96 channels: 27.6 -> 24.8
+// us); with 64-column groups they cost more (the 64-channel layer: 136 ->
+// 152 us), and the copy is made.
+template <typename T>
+static bool rows_take_untransposed(int kdim, int ncols) {
+  return sizeof(T) == 4 && ncols % 4 == 0 && ncols % 64 != 0 && kdim * sizeof(T) != 64;
+}
+
 template <typename T>
 static sscn_status launch_rows(const T* X, const T* B, const View& v, int kdim, int ncols, const Heads<T>& Y,
-                               hipStream_t s) {
+                               hipStream_t s, bool untransposed = false) {
   if (v.n_out == 0) return SSCN_OK;
   SSCN_TRY(ensure_plan(v, s));
   // 64 output columns per workgroup when they divide the width, else 32;
@@ -1447,6 +1487,12 @@ static sscn_status launch_rows(const T* X, const T* B, const View& v, int kdim, 
   // 96 or 160 columns.  128-byte windows (32 fp32 or 64 bf16 channels)
   // unless a bf16 row is not a multiple of 128 bytes.
   const bool wide_cols = sizeof(T) == 2 ? ncols > 32 : ncols % 64 == 0;
+  if constexpr (sizeof(T) == 4) {
+    if (untransposed) {
+      if (!rows_take_untransposed<T>(kdim, ncols)) return fail(SSCN_ERR_INVALID_ARG, "weights layout");
+      return launch_rows_nb<T, 128, 2, 1, true>(X, B, v, kdim, ncols, Y, s);
+    }
+  }
   // Rows of half a window (32 bf16 or 16 fp32 channels, 16 bf16 in a
   // 64-byte window): two items per step.
   const uint32_t row_bytes = (uint32_t)kdim * sizeof(T);
@@ -1723,13 +1769,15 @@ static sscn_status check_conv_args(sscn_rulebook rb, int32_t c_in, int32_t c_out
   return SSCN_OK;
 }
 
-// fp32: a transposed copy of W (one small kernel) gives the main kernel
-// contiguous weight loads, which is faster than gathering the stored layout;
-// bf16 reads the stored layout directly.
+// The row kernel takes W as stored where rows_take_untransposed says so (it
+// transposes each weight tile while staging it); otherwise a transposed
+// copy of W (one small kernel) gives it whole 16-byte pieces of each
+// column's reduction channels.
 template <typename T>
 static sscn_status forward_t(const T* X, const T* W, const View& v, int cin, int cout, const Heads<T>& Y, hipStream_t s) {
   if (rows_eligible<T>(v, cin, cout)) {
     if (v.n_out == 0) return SSCN_OK;
+    if (rows_take_untransposed<T>(cin, cout)) return launch_rows<T>(X, W, v, cin, cout, Y, s, true);
     const int64_t total = (int64_t)v.K * cin * cout;
     T* Bt = nullptr;
     SSCN_TRY(dev_alloc((void**)&Bt, sizeof(T) * total, s));
