@@ -311,7 +311,7 @@ def main():
         "wgrad_ms": wgrad_ms,
         "forward_bf16_ms": fwd_bf16_ms,
         "forward_bf16_tflops": flops_layer / (fwd_bf16_ms * 1e-3) / 1e12,
-        "roofline": {"kernel": "k_conv_rows<float, 128, 4, 2, 1> (forward/dgrad main kernel; timed on the dgrad call)",
+        "roofline": {"kernel": "k_conv_rows<float, 128, 4, 2, 1, false> (forward/dgrad main kernel; timed on the dgrad call)",
                      "bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_MFMA_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_FP32_MFMA_TFLOPS,
                      "launch_ms": dgrad_ms, "flops_per_launch": flops_layer,
