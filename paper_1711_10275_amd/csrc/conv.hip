@@ -56,6 +56,10 @@ struct Heads {
   const float* scale[2];
   const float* shift[2];
   int n;
+  // a buffer the row kernel clears on the side (the backward's dW, which the
+  // wgrad kernel after it accumulates into), n_zero floats; 0: none
+  float* zero;
+  int64_t n_zero;
   __device__ __forceinline__ void store(int64_t row, int col, float v) const {
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
@@ -835,6 +839,10 @@ __global__ __launch_bounds__(256, WB == 64 ? 6 : 5) void k_conv_rows(
     else if (share > 1.0f) __builtin_amdgcn_s_setprio(2);
     else if (share > 0.9f) __builtin_amdgcn_s_setprio(1);
   }
+  if (Y.n_zero > 0) {
+    const int64_t stride = (int64_t)gridDim.x * gridDim.y * 256;
+    for (int64_t i = ((int64_t)blockIdx.y * gridDim.x + wg) * 256 + tid; i < Y.n_zero; i += stride) Y.zero[i] = 0.f;
+  }
   for (int64_t idx = wg, round = 0; idx < n_blocks; idx = next(++round)) {
     __syncthreads();  // the previous block's LDS is free
     conv_rows_block<T, WB, NB, D, PK, TB>(X, x_bytes, B, b_bytes, perm, b_first, items, b_order[idx], K, mirror, kdim,
@@ -1447,7 +1455,7 @@ template <typename T, int WB, int NB, int PK = 1, bool TB = false>
 static sscn_status launch_rows_nb(const T* X, const T* B, const View& v, int kdim, int ncols, const Heads<T>& Y,
                                   hipStream_t s) {
   const int64_t nb = v.st->n_blocks;
-  if (nb == 0) return SSCN_OK;
+  if (nb == 0) return Y.n_zero > 0 ? fill_f32(Y.zero, 0.f, Y.n_zero, s) : SSCN_OK;
   const int gy = (ncols + 16 * NB - 1) / (16 * NB);
   const uint32_t xb = (uint32_t)((uint64_t)std::max<int64_t>(v.n_in, 1) * kdim * sizeof(T));
   const uint32_t bb = (uint32_t)((uint64_t)v.K * ncols * kdim * sizeof(T));
@@ -1478,7 +1486,7 @@ static bool rows_take_untransposed(int kdim, int ncols) {
 template <typename T>
 static sscn_status launch_rows(const T* X, const T* B, const View& v, int kdim, int ncols, const Heads<T>& Y,
                                hipStream_t s, bool untransposed = false) {
-  if (v.n_out == 0) return SSCN_OK;
+  if (v.n_out == 0) return Y.n_zero > 0 ? fill_f32(Y.zero, 0.f, Y.n_zero, s) : SSCN_OK;
   SSCN_TRY(ensure_plan(v, s));
   // 64 output columns per workgroup when they divide the width, else 32;
   // for bf16 (bound by loads and step latency rather than MFMAs) 64 unless
@@ -1686,7 +1694,7 @@ __global__ __launch_bounds__(256) void k_wgrad_ring(const T* __restrict__ X, uin
 }
 
 template <typename T, int CA, int CB>
-static sscn_status launch_wgrad_reg(const T* X, const T* dY, const View& v, int cin, int cout, float* dW,
+static sscn_status launch_wgrad_reg(bool zeroed, const T* X, const T* dY, const View& v, int cin, int cout, float* dW,
                                     hipStream_t s, int64_t max_ppo, int64_t n_pairs) {
   (void)max_ppo;
   (void)n_pairs;
@@ -1720,14 +1728,14 @@ static sscn_status launch_wgrad_reg(const T* X, const T* dY, const View& v, int 
     const int64_t ranges = std::max<int64_t>(1, target / S);
     const int64_t tr2 = std::max<int64_t>(1, ceil_div(v.st->n_tiles, ranges));
     const int64_t total = ceil_div(v.st->n_tiles, tr2) * S;
-    SSCN_TRY(fill_f32(dW, 0.f, (int64_t)v.K * cin * cout, s));
+    if (!zeroed) SSCN_TRY(fill_f32(dW, 0.f, (int64_t)v.K * cin * cout, s));
     kern<<<dim3((unsigned)total, (unsigned)(nzc * nzo)), 256, 0, s>>>(
         X, (uint32_t)x_bytes, dY, (uint32_t)y_bytes, v.st->seg, v.st->n_tiles, v.st->in_rows, v.st->out_rows, v.K,
         v.mirror ? 1 : 0, cin, cout, (int)tr2, items, nzc, dW);
     SSCN_HIP(hipGetLastError());
     return SSCN_OK;
   }
-  SSCN_TRY(fill_f32(dW, 0.f, (int64_t)v.K * cin * cout, s));
+  if (!zeroed) SSCN_TRY(fill_f32(dW, 0.f, (int64_t)v.K * cin * cout, s));
   k_wgrad_reg<T, CA, CB><<<dim3((unsigned)n_items, (unsigned)(nzc * nzo)), 256, 0, s>>>(
       X, dY, v.st->seg, v.st->n_tiles, v.st->in_rows, v.st->out_rows, v.K, v.mirror ? 1 : 0, cin, cout, (int)tr,
       nzc, dW);
@@ -1744,12 +1752,13 @@ static int wgrad_blocks(int c) {
   return 1;
 }
 
+// zeroed: dW is already zero on stream s (cleared by the dgrad launch before it).
 template <typename T>
 static sscn_status launch_wgrad(const T* X, const T* dY, const View& v, int cin, int cout, float* dW,
-                                hipStream_t s, int64_t max_ppo, int64_t n_pairs) {
+                                hipStream_t s, int64_t max_ppo, int64_t n_pairs, bool zeroed = false) {
   const int ca = wgrad_blocks(cin), cb = wgrad_blocks(cout);
 #define SSCN_WG(A, B) \
-  if (ca == A && cb == B) return launch_wgrad_reg<T, A, B>(X, dY, v, cin, cout, dW, s, max_ppo, n_pairs);
+  if (ca == A && cb == B) return launch_wgrad_reg<T, A, B>(zeroed, X, dY, v, cin, cout, dW, s, max_ppo, n_pairs);
   SSCN_WG(4, 4) SSCN_WG(4, 2) SSCN_WG(4, 1) SSCN_WG(2, 4) SSCN_WG(2, 2) SSCN_WG(2, 1)
   SSCN_WG(1, 4) SSCN_WG(1, 2) SSCN_WG(1, 1)
 #undef SSCN_WG
@@ -1875,30 +1884,36 @@ extern "C" sscn_status sparse_conv_backward(const void* features, const void* we
   sscn_status st = check_conv_args(rb, c_in, c_out, dtype);
   if (st != SSCN_OK) return st;
   const View v = view_of(rb);
+  const int64_t w_total = (int64_t)v.K * c_in * c_out;
+  bool w_zeroed = false;  // the dgrad launch cleared wgrad on the side
   if (dgrad && v.n_in > 0) {
     if (!weights || (v.n_out > 0 && !dout)) return fail(SSCN_ERR_INVALID_ARG, "NULL weights or dout");
     // dgrad = forward over the transposed rule book with B = W^o (as stored:
     // row ci of W[o] holds the c_out weights feeding input channel ci)
     const View vt = transposed_view(rb);
-    if (dtype == SSCN_F32)
-      st = rows_eligible<float>(vt, c_out, c_in)
-               ? launch_rows<float>((const float*)dout, (const float*)weights, vt, c_out, c_in,
-                                    plain_heads((float*)dgrad, c_in), stream)
-               : launch_conv<float, true>((const float*)dout, (const float*)weights, vt, c_out, c_in,
-                                          plain_heads((float*)dgrad, c_in), stream);
-    else
-      st = rows_eligible<bf16_t>(vt, c_out, c_in)
-               ? launch_rows<bf16_t>((const bf16_t*)dout, (const bf16_t*)weights, vt, c_out, c_in,
-                                     plain_heads((bf16_t*)dgrad, c_in), stream)
-               : launch_conv<bf16_t, true>((const bf16_t*)dout, (const bf16_t*)weights, vt, c_out, c_in,
-                                           plain_heads((bf16_t*)dgrad, c_in), stream);
+    if (dtype == SSCN_F32) {
+      Heads<float> h = plain_heads((float*)dgrad, c_in);
+      if (rows_eligible<float>(vt, c_out, c_in)) {
+        if (wgrad) { h.zero = wgrad; h.n_zero = w_total; w_zeroed = true; }
+        st = launch_rows<float>((const float*)dout, (const float*)weights, vt, c_out, c_in, h, stream);
+      } else {
+        st = launch_conv<float, true>((const float*)dout, (const float*)weights, vt, c_out, c_in, h, stream);
+      }
+    } else {
+      Heads<bf16_t> h = plain_heads((bf16_t*)dgrad, c_in);
+      if (rows_eligible<bf16_t>(vt, c_out, c_in)) {
+        if (wgrad) { h.zero = wgrad; h.n_zero = w_total; w_zeroed = true; }
+        st = launch_rows<bf16_t>((const bf16_t*)dout, (const bf16_t*)weights, vt, c_out, c_in, h, stream);
+      } else {
+        st = launch_conv<bf16_t, true>((const bf16_t*)dout, (const bf16_t*)weights, vt, c_out, c_in, h, stream);
+      }
+    }
     if (st != SSCN_OK) return st;
   }
   if (wgrad) {
-    const int64_t total = (int64_t)v.K * c_in * c_out;
     const RulebookData* d = rb->d;
     if (d->n_pairs == 0) {
-      st = fill_f32(wgrad, 0.f, total, stream);
+      if (!w_zeroed) st = fill_f32(wgrad, 0.f, w_total, stream);
       if (st != SSCN_OK) return st;
     } else {
       if (!features || !dout) return fail(SSCN_ERR_INVALID_ARG, "NULL features or dout");
@@ -1906,10 +1921,10 @@ extern "C" sscn_status sparse_conv_backward(const void* features, const void* we
       for (int64_t c : d->pairs_per_offset) mx = std::max(mx, c);
       if (dtype == SSCN_F32)
         st = launch_wgrad<float>((const float*)features, (const float*)dout, v, c_in, c_out, wgrad, stream, mx,
-                                 d->n_pairs);
+                                 d->n_pairs, w_zeroed);
       else
         st = launch_wgrad<bf16_t>((const bf16_t*)features, (const bf16_t*)dout, v, c_in, c_out, wgrad, stream,
-                                  mx, d->n_pairs);
+                                  mx, d->n_pairs, w_zeroed);
     }
   }
   return st;
