@@ -1605,8 +1605,8 @@ static sscn_status new_handle(RulebookData* d, sscn_rulebook* out) {
 
 // SSC build with 8-byte dictionary slots (batch_lim > 0: batch indices
 // below batch_lim keep the 32-bit keys below the empty marker) or 16-byte
-// ones (batch_lim == 0).  Sets *wide and builds nothing when a batch index
-// reaches batch_lim.
+// ones (batch_lim == 0).  Sets *wide and returns no rule book (its queued
+// work is discarded) when a batch index reaches batch_lim.
 static sscn_status ssc_build(const int32_t* coords, int64_t n, const int32_t* spatial_size, int32_t filter_size,
                              hipStream_t stream, uint32_t batch_lim, bool* wide, sscn_rulebook* out) {
   const int f = filter_size, K = f * f * f;
