@@ -11,6 +11,7 @@ from __future__ import annotations
 import ctypes
 import os
 import re
+import threading
 
 import torch
 
@@ -113,14 +114,20 @@ def _dtype_code(t):
     raise ValueError(f"unsupported dtype {t.dtype} (float32 or bfloat16)")
 
 
+# per-thread query buffers (a ctypes call releases the GIL while it runs)
+_query_bufs = threading.local()
+
+
 class Rulebook:
     """Owning wrapper of an sscn_rulebook handle."""
 
     def __init__(self, handle, device):
         self._h = handle
         self.device = device
-        info = RulebookInfo()
-        ppo = (ctypes.c_int64 * _MAX_OFFSETS)()
+        bufs = _query_bufs.__dict__
+        if not bufs:
+            bufs["info"], bufs["ppo"] = RulebookInfo(), (ctypes.c_int64 * _MAX_OFFSETS)()
+        info, ppo = bufs["info"], bufs["ppo"]
         _check(lib().sscn_rulebook_query(self._h, ctypes.byref(info), ppo))
         K = info.n_offsets
         self.n_in, self.n_out, self.n_pairs = info.n_in, info.n_out, info.n_pairs
@@ -168,11 +175,14 @@ class Rulebook:
             pass
 
 
+_I32x3 = ctypes.c_int32 * 3
+
+
 def _sizes(spatial_size):
     s = tuple(int(v) for v in spatial_size)
     if len(s) != 3:
         raise ValueError("spatial_size must have 3 entries")
-    return (ctypes.c_int32 * 3)(*s)
+    return _I32x3(*s)
 
 
 def ssc_rulebook_build(coords, spatial_size, filter_size=3):
