@@ -161,7 +161,8 @@ def test_mirrored_probe_on_shuffled_rows(f):
 @pytest.mark.parametrize("size,batches", [((1024, 1024, 1024), 3),   # 32-bit keys up to 3 * 2^30 - 1
                                           ((1024, 1024, 1024), 4),   # batch 3 needs 64-bit keys: rebuilt wide
                                           ((65536, 65536, 2), 2)])   # one sample exceeds 32 bits: wide from the start
-def test_dictionary_key_widths(size, batches):
+@pytest.mark.parametrize("f", [3, 5])
+def test_dictionary_key_widths(size, batches, f):
     """SSC dictionaries hold 32-bit keys (linear index of (b, x)) while every
     batch index present keeps them below the empty marker, else 64-bit keys;
     both must give the oracle's rule book, also at the largest coordinates."""
@@ -174,13 +175,13 @@ def test_dictionary_key_widths(size, batches):
     c = np.unique(np.concatenate(parts), axis=0)
     c = np.ascontiguousarray(c[rng.permutation(c.shape[0])]).astype(np.int32)
     assert c[:, 1:].max(axis=0).tolist() == [L - 1 for L in size]
-    rb = sscn.ssc_rulebook_build(dev(c), size, 3)
-    orb = O.ssc_rulebook(c, size, 3)
-    assert_same_rulebook(rb, orb, f"ssc {size} batches={batches}")
+    rb = sscn.ssc_rulebook_build(dev(c), size, f)
+    orb = O.ssc_rulebook(c, size, f)
+    assert_same_rulebook(rb, orb, f"ssc {size} batches={batches} f={f}")
     np.testing.assert_array_equal(host(rb.out_coords()), c)
     dup = np.concatenate([c, c[-1:]])
     with pytest.raises(sscn.SSCNError) as e:
-        sscn.ssc_rulebook_build(dev(dup), size, 3)
+        sscn.ssc_rulebook_build(dev(dup), size, f)
     assert e.value.code == "duplicate"
 
 
