@@ -271,11 +271,6 @@ def macs(rb, cin, cout):
     return rb.n_pairs() * cin * cout
 
 
-def conditioning_bound(X, W, rb):
-    """B[k][co] = sum |X[j][ci]| |W[o][ci][co]|: a scale for rounding errors."""
-    return forward(np.abs(np.asarray(X, np.float64)), np.abs(np.asarray(W, np.float64)), rb)
-
-
 # --------------------------------------------------------------------------
 # network pieces (Sec. 5): pre-activation, row-sampled layers, the U-Net
 # --------------------------------------------------------------------------

@@ -57,10 +57,43 @@ def _bwd_pin_error():
     return max(abs(lhs - np.sum(X * dX)), abs(lhs - np.sum(W * dW)))
 
 
+def _triples_pin_holds():
+    from tests.test_oracle_pins import brute_force_triples
+    rng = np.random.default_rng(8)
+    size = (7, 7, 7)
+    occ = rng.random((2,) + size) < 0.15
+    c = np.argwhere(occ).astype(np.int32)
+    c = c[rng.permutation(c.shape[0])]
+    ok = True
+    for rb, sub, f, s in ((O.ssc_rulebook(c, size, 3), True, 3, 1), (O.sc_rulebook(c, size, 3, 2), False, 3, 2)):
+        want = brute_force_triples(c, rb.out_coords, f, s, sub)
+        ok &= O.canonical_triples(rb).tolist() == [list(t) for t in want]
+    return ok
+
+
 def test_unmutated_pins_hold():
     assert _ssc_pin_error() < 1e-10
     assert _sc_pin_error() < 1e-10
     assert _bwd_pin_error() < 1e-10
+    assert _triples_pin_holds()
+
+
+@pytest.mark.parametrize("keys", [lambda t: (t[:, 1], t[:, 0], t[:, 2]),   # sorted by (o, in, out)
+                                  lambda t: (t[:, 0], t[:, 2], t[:, 1]),   # sorted by (out, o, in)
+                                  lambda t: (t[:, 2], t[:, 1], t[:, 0])])  # sorted by (in, out, o)
+def test_triples_sort_key_caught(monkeypatch, keys):
+    def bad(rb):
+        t = np.concatenate([np.stack([rb.ins[o], rb.outs[o], np.full(rb.ins[o].size, o)], axis=1)
+                            for o in range(rb.K)])
+        return t[np.lexsort(keys(t))].astype(np.int64)
+    monkeypatch.setattr(O, "canonical_triples", bad)
+    assert not _triples_pin_holds()
+
+
+def test_triples_swapped_columns_caught(monkeypatch):
+    orig = O.canonical_triples
+    monkeypatch.setattr(O, "canonical_triples", lambda rb: orig(rb)[:, [1, 0, 2]])
+    assert not _triples_pin_holds()
 
 
 def test_offset_sign_error_caught(monkeypatch):

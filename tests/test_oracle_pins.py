@@ -134,6 +134,43 @@ def test_sc_first_visit_numbering_pure_python():
 
 
 # --------------------------------------------------------------------------
+# canonical export: every pair as (in, out, o), sorted by (o, out, in)
+# --------------------------------------------------------------------------
+def brute_force_triples(coords, out_coords, f, s, submanifold):
+    """All (in, out, o) by comparing every input site with every output site in
+    pure Python (Sec. 4.1: input x feeds output y through offset i when
+    x = y + i - (f-1)/2 for SSC, x = s*y + i for SC), sorted by (o, out, in)
+    with Python's own sort."""
+    c = (f - 1) // 2 if submanifold else 0
+    step = 1 if submanifold else s
+    out = []
+    for j, (bj, *xj) in enumerate(coords.tolist()):
+        for k, (bk, *yk) in enumerate(out_coords.tolist()):
+            if bj != bk:
+                continue
+            i = [xj[d] - step * yk[d] + c for d in range(3)]
+            if all(0 <= v < f for v in i):
+                out.append((j, k, (i[0] * f + i[1]) * f + i[2]))
+    return sorted(out, key=lambda t: (t[2], t[1], t[0]))
+
+
+@pytest.mark.parametrize("kind,size,f,s", [("ssc", (7, 7, 7), 3, 1), ("ssc", (6, 6, 6), 5, 1),
+                                           ("sc", (9, 9, 9), 3, 2), ("sc", (8, 8, 8), 2, 2)])
+def test_canonical_triples_brute_force(kind, size, f, s):
+    c = _small_set(12, size, density=0.12)       # rows shuffled: out order != in order per offset
+    rb = O.ssc_rulebook(c, size, f) if kind == "ssc" else O.sc_rulebook(c, size, f, s)
+    got = O.canonical_triples(rb)
+    assert got.dtype == np.int64 and got.shape == (rb.n_pairs(), 3)
+    want = brute_force_triples(c, rb.out_coords, f, s, kind == "ssc")
+    assert got.tolist() == [list(t) for t in want]
+
+
+def test_canonical_triples_empty():
+    rb = O.ssc_rulebook(np.zeros((0, 4), np.int32), (4, 4, 4), 3)
+    assert O.canonical_triples(rb).shape == (0, 3)
+
+
+# --------------------------------------------------------------------------
 # P2: ShapeContext layer = SSC(1, 27, 3) with identity weights (Sec. 6.3)
 # --------------------------------------------------------------------------
 def test_shapecontext_identity_decodes_rulebook():
