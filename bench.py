@@ -5,37 +5,42 @@ surfaces (sphere shells, planar patches, cylinder shells) voxelised to a
 1-voxel-thick surface, about 100k active sites; C_in = C_out = 64, fp32.
 Features N(0,1), weights N(0, 1/(27 C_in)), upstream gradient N(0,1).
 
-One step = rule-book build (dictionary, neighbour probe, compaction, one
-readback) + forward + backward (dgrad over the transposed rule book, wgrad
-per offset): every stage of the layer.  Inputs are resident in HBM before
-the timed region.  value = active sites / s over whole steps.
+One step = rule-book build (dictionary, neighbour probe, compaction, the
+row-block plan, one readback) + forward + dgrad (over the transposed rule
+book) + wgrad (per offset): every stage of the layer.  Inputs are resident
+in HBM before the timed region.  value = active sites / s over whole steps.
 
-Also reported: per-stage times, useful ("effective") TFLOP/s counting only
-the multiply-adds of real pairs (2 C_in C_out per pair, Table 2), the
-roofline of the dominant kernel and the CPU oracle timed on a bounded
-sample of the same workload on the host cores.
+Dominant kernel: the row-block kernel, launched once by the forward
+(k_conv_rows) and once by the dgrad (k_dgrad_rows, the same code under its
+own name).  Its duration is measured inside the timed steps with a pair of
+HIP events around every dgrad launch (the dgrad is its own call there, so
+the pair brackets exactly that one kernel on its stream); `roofline`
+divides the useful flops of one launch (2 C_in C_out per pair, Table 2) by
+the mean of those durations.  `traffic` (HBM bytes per launch) comes from
+the committed counter record in profiles/ and is null when the kernel
+source has changed since those counters were taken.  `build_roofline` puts
+the SSC build's algorithmic bytes over its wall time against HBM bandwidth;
+the builder's own intermediate (its neighbour map, written and read back)
+is reported beside them and not counted.
 
-Dominant kernel: k_conv_rows, which runs the forward and the dgrad of the
-layer (same pairs, same channel counts) over the rule book's row-block
-plan.  Its duration is measured with HIP events around the dgrad call,
-which is exactly one launch of it on the current stream (the SSC build
-queues the plan, so its cost is in rulebook_build_ms and in every step;
-first_forward_extra_ms is what a fresh rule book's first forward costs
-beyond a later one).  `traffic` (HBM bytes per launch) comes from the
-committed counter record in profiles/, and is null when the kernel source
-has changed since those counters were taken.  `build_roofline` puts the
-SSC build's logical bytes over its wall time against HBM bandwidth.
+Also reported: per-stage times (fp32 and bf16), a cold-cache step (after a
+512 MB flush write), the same layer with its rows shuffled (locality), the
+measured ceilings of the box (a streaming copy and register-only MFMA
+loops), and the CPU oracle timed on a bounded sample of the same workload
+on the host cores.
 
---copy-calibration runs a plain device copy of known size (256 MiB) so
-that a counter run can scale FETCH_SIZE / WRITE_SIZE by what they read for
-it.
+--copy-calibration runs a plain 256 MiB device copy (the measure library's
+k_copy) so that a counter run can scale FETCH_SIZE / WRITE_SIZE by what
+they read for it.
 """
 from __future__ import annotations
 
 import argparse
+import ctypes
 import hashlib
 import json
 import os
+import platform
 import sys
 import time
 
@@ -49,7 +54,9 @@ PEAK_BF16_MFMA_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 METRIC = "SSC 3^3 layer active-sites/s + effective TFLOP/s; rulebook build ms"
 KERNEL_SRC = os.path.join(ROOT, "paper_1711_10275_amd", "csrc", "conv.hip")
-TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "k_conv_rows_ssc128_c64_traffic.json")
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "k_dgrad_rows_ssc128_c64_traffic.json")
+DOMINANT = "k_dgrad_rows<float, 128, 4, 2, 1, false>"
+MEASURE_LIB = os.path.join(ROOT, "paper_1711_10275_amd", "libsscn_measure.so")
 
 
 def kernel_source_hash():
@@ -57,7 +64,8 @@ def kernel_source_hash():
 
 
 def recorded_traffic():
-    """HBM bytes per launch from the committed counter record, if still valid."""
+    """HBM bytes per launch of the dominant kernel from the committed counter
+    record, if it was taken on the current kernel source."""
     try:
         rec = json.load(open(TRAFFIC_RECORD))
     except (OSError, ValueError):
@@ -77,8 +85,20 @@ def parse():
     p.add_argument("--copy-calibration", action="store_true",
                    help="also run a 256 MiB device copy (counter calibration)")
     p.add_argument("--no-extra", action="store_true",
-                   help="skip the SC -> SSC and U-Net figures reported beside the headline layer")
+                   help="skip the SC -> SSC, U-Net, cold-cache, shuffled and ceiling figures")
     return p.parse_args()
+
+
+def host_cpu():
+    model = platform.processor() or "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return model, os.cpu_count()
 
 
 def cpu_baseline(coords, size, X, W, G, budget_s):
@@ -98,12 +118,15 @@ def cpu_baseline(coords, size, X, W, G, budget_s):
         O.backward(X, W, G, orb)
         t_total += time.perf_counter() - t0
         steps += 1
+    model, ncpu = host_cpu()
     return {"value": n * steps / t_total, "unit": "active-sites/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{steps} whole steps (rule book + forward + backward, numpy fp64) of the same "
-                      f"{n}-site workload, {t_total:.1f} s"}
+            "host_cpus": ncpu, "cpu_model": model,
+            "sample": f"{steps} whole steps (rule book + forward + backward, numpy fp64; its matrix products "
+                      f"use {threads} BLAS threads, the rest one) of the same {n}-site workload, {t_total:.1f} s"}
 
 
 def _event_ms(fn, reps, stream):
+    """Mean time per call of back-to-back calls (HIP events on `stream`)."""
     import torch
     fn()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -115,26 +138,6 @@ def _event_ms(fn, reps, stream):
     return e0.elapsed_time(e1) / reps
 
 
-def build_roofline(n, K, pairs, ms, what, slot=8):
-    """Logical bytes of an SSC rule-book build against HBM bandwidth.
-
-    Counted: coordinates read (16 B per site), the hash table filled and
-    written (slot bytes each: 8 for the 32-bit keys that both workloads
-    here use, capacity the power of two >= 2n), one slot read per (site,
-    offset) lookup, the offset-major neighbour map written and read back
-    (4 B per site and offset each way), the pair arrays written (8 B per
-    pair).  The time is the host wall time of the build call (its
-    row-block plan included).
-    """
-    cap = 64
-    while cap < 2 * n:
-        cap *= 2
-    nbytes = 16 * n + slot * cap + slot * n + slot * K * n + 8 * K * n + 8 * pairs
-    achieved = nbytes / (ms * 1e-3) / 1e9
-    return {"stage": what, "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-            "frac": achieved / PEAK_HBM_GBS, "bytes": nbytes, "ms": ms}
-
-
 def _wall_ms(fn, reps):
     import torch
     fn()
@@ -144,6 +147,57 @@ def _wall_ms(fn, reps):
         fn()
     torch.cuda.synchronize()
     return (time.perf_counter() - t0) * 1e3 / reps
+
+
+def table_capacity(n):
+    cap = 64
+    while cap < 2 * n:
+        cap *= 2
+    return cap
+
+
+def build_roofline(n, K, pairs, ms, what, slot=8):
+    """Algorithmic bytes of an SSC rule-book build against HBM bandwidth.
+
+    Counted: coordinates read (16 B per site), the dictionary filled and its
+    slots written (slot bytes each: 8 for the 32-bit keys that both
+    workloads here use; capacity the power of two >= 2n), one slot read per
+    lookup performed (K per site below 2^18 sites; from 2^18 the mirrored
+    probe looks up only the (K - 1) / 2 offsets below the centre and derives
+    the rest), and the pair arrays written (8 B per pair).  Not counted: the
+    builder's neighbour map (4 B per site and offset, written and read back),
+    reported as `intermediate_bytes`.  The time is the host wall time of the
+    build call (its row-block plan and readback included).
+    """
+    cap = table_capacity(n)
+    lookups = K * n if n < (1 << 18) else (K - 1) // 2 * n
+    nbytes = 16 * n + 2 * slot * cap + slot * lookups + 8 * pairs
+    achieved = nbytes / (ms * 1e-3) / 1e9
+    return {"stage": what, "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": achieved / PEAK_HBM_GBS, "bytes": nbytes, "ms": ms, "intermediate_bytes": 8 * K * n}
+
+
+def measured_ceilings():
+    """Copy bandwidth and MFMA-loop rates measured on this GPU."""
+    L = ctypes.CDLL(MEASURE_LIB)
+    L.sscn_measure_copy.argtypes = [ctypes.c_int64, ctypes.c_int, ctypes.POINTER(ctypes.c_double)]
+    L.sscn_measure_mfma.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_double)]
+    out = {}
+    v = ctypes.c_double()
+    if L.sscn_measure_copy(1 << 30, 5, ctypes.byref(v)) == 0:
+        out["copy_1GiB_GBs"] = v.value
+    if L.sscn_measure_mfma(0, 5, ctypes.byref(v)) == 0:
+        out["mfma_f32_16x16x4_TFLOPs"] = v.value
+    if L.sscn_measure_mfma(1, 5, ctypes.byref(v)) == 0:
+        out["mfma_bf16_16x16x32_TFLOPs"] = v.value
+    return out
+
+
+def copy_calibration():
+    L = ctypes.CDLL(MEASURE_LIB)
+    L.sscn_measure_copy.argtypes = [ctypes.c_int64, ctypes.c_int, ctypes.POINTER(ctypes.c_double)]
+    v = ctypes.c_double()
+    L.sscn_measure_copy(256 << 20, 2, ctypes.byref(v))
 
 
 def sc_then_ssc(tc, size, stream, reps):
@@ -188,7 +242,7 @@ def unet_scenes(stream, reps):
     ssc0_ms = _wall_ms(lambda: sscn.ssc_rulebook_build(tc, (256, 256, 256), 3), reps)
     ssc0_pairs = sscn.ssc_rulebook_build(tc, (256, 256, 256), 3).n_pairs
     # a fresh input: rule books of every level, then the network (lazily built
-    # chunk tables included)
+    # tables included)
     fresh_ms = _wall_ms(lambda: unet.forward(X, unet.Geometry(tc, (256, 256, 256)), params), reps)
     geom = unet.Geometry(tc, (256, 256, 256))
     fwd_ms = _event_ms(lambda: unet.forward(X, geom, params), reps, stream)
@@ -225,11 +279,20 @@ def main():
     G = S.features(n, cout, S.SEED_GRAD + 1)
     tc = torch.from_numpy(coords).to(dev)
     tX, tW, tG = (torch.from_numpy(a).to(dev) for a in (X, W, G))
+    stream = torch.cuda.current_stream(dev)
+    dgrad_events = []
 
-    def step():
+    def step(tc=tc, tX=tX, tG=tG, record=False):
         rb = sscn.ssc_rulebook_build(tc, size, 3)
         sscn.sparse_conv_forward(tX, tW, rb)
-        sscn.sparse_conv_backward(tX, tW, tG, rb)
+        if record:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+        sscn.sparse_conv_backward(None, tW, tG, rb, dgrad=True, wgrad=False)
+        if record:
+            e1.record(stream)
+            dgrad_events.append((e0, e1))
+        sscn.sparse_conv_backward(tX, tW, tG, rb, dgrad=False, wgrad=True)
         return rb
 
     for _ in range(args.warmup):
@@ -237,15 +300,15 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        rb = step()
+        rb = step(record=True)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / args.steps
+    launch_ms = sum(a.elapsed_time(b) for a, b in dgrad_events) / len(dgrad_events)
     pairs = rb.n_pairs
     flops_layer = 2.0 * cin * cout * pairs  # useful flops of one pass (fwd, dgrad or wgrad)
 
     # ---- per-stage breakdown (same stream; events bracket the calls) ----
-    stream = torch.cuda.current_stream(dev)
     reps = max(10, args.steps)
     torch.cuda.synchronize()
     tb = time.perf_counter()
@@ -255,36 +318,18 @@ def main():
     build_ms = (time.perf_counter() - tb) * 1e3 / reps
     del rbx
 
-    def timed(fn):
-        fn()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for _ in range(reps):
-            fn()
-        e1.record(stream)
-        e1.synchronize()
-        return e0.elapsed_time(e1) / reps
-
+    timed = lambda fn: _event_ms(fn, reps, stream)
     fwd_ms = timed(lambda: sscn.sparse_conv_forward(tX, tW, rb))
-    # a fresh rule book's first forward also builds its row-block plan
-    torch.cuda.synchronize()
-    tb = time.perf_counter()
-    for _ in range(reps):
-        sscn.sparse_conv_forward(tX, tW, sscn.ssc_rulebook_build(tc, size, 3))
-    torch.cuda.synchronize()
-    build_fwd_ms = (time.perf_counter() - tb) * 1e3 / reps
     dgrad_ms = timed(lambda: sscn.sparse_conv_backward(None, tW, tG, rb, dgrad=True, wgrad=False))
     if args.copy_calibration:
-        src = torch.empty(64 << 20, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
+        copy_calibration()
     wgrad_ms = timed(lambda: sscn.sparse_conv_backward(tX, tW, tG, rb, dgrad=False, wgrad=True))
-    tXb, tWb = tX.to(torch.bfloat16), tW.to(torch.bfloat16)
+    tXb, tWb, tGb = tX.to(torch.bfloat16), tW.to(torch.bfloat16), tG.to(torch.bfloat16)
     fwd_bf16_ms = timed(lambda: sscn.sparse_conv_forward(tXb, tWb, rb))
+    dgrad_bf16_ms = timed(lambda: sscn.sparse_conv_backward(None, tWb, tGb, rb, dgrad=True, wgrad=False))
+    wgrad_bf16_ms = timed(lambda: sscn.sparse_conv_backward(tXb, tWb, tGb, rb, dgrad=False, wgrad=True))
 
-    achieved = flops_layer / (dgrad_ms * 1e-3) / 1e12  # one launch of the dominant kernel
+    achieved = flops_layer / (launch_ms * 1e-3) / 1e12
     result = {
         "metric": METRIC,
         "value": n / (ms_step * 1e-3),
@@ -303,23 +348,52 @@ def main():
                    "step": "rule-book build + forward + backward (dgrad + wgrad)"},
         "effective_tflops_step": 3 * flops_layer / (ms_step * 1e-3) / 1e12,
         "rulebook_build_ms": build_ms,
-        "first_forward_extra_ms": build_fwd_ms - build_ms - fwd_ms,
         "forward_ms": fwd_ms,
         "forward_tflops": flops_layer / (fwd_ms * 1e-3) / 1e12,
         "forward_sites_per_s": n / (fwd_ms * 1e-3),
         "dgrad_ms": dgrad_ms,
         "wgrad_ms": wgrad_ms,
-        "forward_bf16_ms": fwd_bf16_ms,
-        "forward_bf16_tflops": flops_layer / (fwd_bf16_ms * 1e-3) / 1e12,
-        "roofline": {"kernel": "k_conv_rows<float, 128, 4, 2, 1, false> (forward/dgrad main kernel; timed on the dgrad call)",
+        "wgrad_tflops": flops_layer / (wgrad_ms * 1e-3) / 1e12,
+        "bf16": {"forward_ms": fwd_bf16_ms, "dgrad_ms": dgrad_bf16_ms, "wgrad_ms": wgrad_bf16_ms,
+                 "forward_tflops": flops_layer / (fwd_bf16_ms * 1e-3) / 1e12},
+        "roofline": {"kernel": DOMINANT + " (the dgrad launch of the row-block kernel; the forward launches "
+                               "the same code as k_conv_rows)",
                      "bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_MFMA_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_FP32_MFMA_TFLOPS,
-                     "launch_ms": dgrad_ms, "flops_per_launch": flops_layer,
-                     "traffic": recorded_traffic()},
+                     "launch_ms": launch_ms, "launches_timed": len(dgrad_events),
+                     "flops_per_launch": flops_layer, "traffic": recorded_traffic()},
         "build_roofline": build_roofline(int(n), 27, int(pairs), build_ms,
                                          "SSC 3^3 rule-book build incl. its row-block plan, 100k sites"),
     }
     if not args.no_extra:
+        ceil = measured_ceilings()
+        result["measured_ceilings"] = ceil
+        if "mfma_f32_16x16x4_TFLOPs" in ceil:
+            result["roofline"]["peak_measured"] = ceil["mfma_f32_16x16x4_TFLOPs"]
+            result["roofline"]["frac_of_measured"] = achieved / ceil["mfma_f32_16x16x4_TFLOPs"]
+        if "copy_1GiB_GBs" in ceil:
+            result["build_roofline"]["peak_measured"] = ceil["copy_1GiB_GBs"]
+        # cold caches: a 512 MB write evicts the 256 MB last-level cache before one step
+        flush = torch.empty(128 << 20, dtype=torch.float32, device=dev)
+        cold = []
+        for _ in range(3):
+            flush.fill_(1.0)
+            torch.cuda.synchronize()
+            tcold = time.perf_counter()
+            step()
+            torch.cuda.synchronize()
+            cold.append((time.perf_counter() - tcold) * 1e3)
+        del flush
+        result["cold_step_ms"] = float(np.median(cold))
+        # locality: the same sites with their rows shuffled
+        perm_coords = S.shuffled(coords, 77)
+        tcs = torch.from_numpy(perm_coords).to(dev)
+        shuffled_ms = _wall_ms(lambda: step(tc=tcs), reps)
+        rbs = sscn.ssc_rulebook_build(tcs, size, 3)
+        result["shuffled_rows"] = {"step_ms": shuffled_ms,
+                                   "forward_ms": timed(lambda: sscn.sparse_conv_forward(tX, tW, rbs)),
+                                   "dgrad_ms": timed(lambda: sscn.sparse_conv_backward(None, tW, tG, rbs, wgrad=False))}
+        del rbs
         result["extra"] = {"sc_then_ssc": sc_then_ssc(tc, size, stream, reps), "unet": unet_scenes(stream, 5)}
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(coords, size, X, W, G, args.cpu_seconds)

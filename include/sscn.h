@@ -137,9 +137,11 @@ sscn_status sscn_rulebook_export(sscn_rulebook rb, int32_t* in_rows, int32_t* ou
 
 /* Release a rule book or view (storage goes when its last view goes). NULL is a no-op.
  * The storage returns to the library's device-memory cache, ordered on the
- * build stream: work on other streams that still reads the rule book must
- * be ordered before the build stream's later work (or completed) first.
- * Cached memory goes back to the device when an allocation would fail. */
+ * build stream: before it can be handed out again, the build stream is made
+ * to wait (an event per stream) for all work that this library queued on
+ * other streams reading the rule book.  The build stream must therefore
+ * still exist when the last view is freed.  Cached memory goes back to the
+ * device when an allocation would fail. */
 void sscn_rulebook_free(sscn_rulebook rb);
 
 /*
@@ -217,6 +219,15 @@ sscn_status sscn_affine_relu(const void* x, const float* scale, const float* shi
  */
 sscn_status sscn_concat_cols(const void* a, int32_t ca, const void* b, int32_t cb, int64_t n,
                              sscn_dtype dtype, void* y, hipStream_t stream);
+
+/*
+ * sscn_release_cached -- give the library's idle device blocks on the
+ * current device back to the device (after a device-wide synchronisation),
+ * e.g. when another allocator in the process runs out of memory.  Storage
+ * of live rule books is not touched.  Not a paper operation: memory
+ * management of the rule-book storage of Sec. 4.2.
+ */
+sscn_status sscn_release_cached(void);
 
 /* Thread-local message describing the last failure on this thread ("" if none). */
 const char* sscn_last_error(void);

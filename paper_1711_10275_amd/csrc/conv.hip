@@ -806,11 +806,11 @@ __device__ __forceinline__ void conv_rows_block(
   }
 }
 
-template <typename T, int WB, int NB, int D, int PK, bool TB = false>
-__global__ __launch_bounds__(256, WB == 64 ? 6 : 5) void k_conv_rows(
+template <typename T, int WB, int NB, int D, int PK, bool TB>
+__device__ __forceinline__ void conv_rows_run(
     const T* __restrict__ X, uint32_t x_bytes, const T* __restrict__ B, uint32_t b_bytes,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ b_first, const int32_t* __restrict__ b_order,
-    const uint32_t* __restrict__ items, int64_t n_blocks, int K, int mirror, int kdim, int ncols, Heads<T> Y) {
+    const uint32_t* __restrict__ items, int64_t n_blocks, int K, int mirror, int kdim, int ncols, const Heads<T>& Y) {
   constexpr int RPI = 64 / (WB / 16);       // rows per wavefront load
   constexpr int COLS = 16 * NB;             // output columns per workgroup
   constexpr int PITCH = WB + 16;            // LDS bytes per row (bank spread)
@@ -849,6 +849,27 @@ __global__ __launch_bounds__(256, WB == 64 ? 6 : 5) void k_conv_rows(
                                   ncols, Y, As, Bs, tid, wave, lane, m, g, col0);
   }
 }
+
+#define SSCN_ROWS_ARGS                                                                                          \
+  const T *__restrict__ X, uint32_t x_bytes, const T *__restrict__ B, uint32_t b_bytes,                        \
+      const int32_t *__restrict__ perm, const int32_t *__restrict__ b_first, const int32_t *__restrict__ b_order, \
+      const uint32_t *__restrict__ items, int64_t n_blocks, int K, int mirror, int kdim, int ncols, Heads<T> Y
+
+// Forward (and DC) launches.
+template <typename T, int WB, int NB, int D, int PK, bool TB = false>
+__global__ __launch_bounds__(256, WB == 64 ? 6 : 5) void k_conv_rows(SSCN_ROWS_ARGS) {
+  conv_rows_run<T, WB, NB, D, PK, TB>(X, x_bytes, B, b_bytes, perm, b_first, b_order, items, n_blocks, K, mirror,
+                                      kdim, ncols, Y);
+}
+
+// The dgrad launches of sparse_conv_backward: the same kernel under its own
+// name, so that kernel traces tell the two directions apart.
+template <typename T, int WB, int NB, int D, int PK, bool TB = false>
+__global__ __launch_bounds__(256, WB == 64 ? 6 : 5) void k_dgrad_rows(SSCN_ROWS_ARGS) {
+  conv_rows_run<T, WB, NB, D, PK, TB>(X, x_bytes, B, b_bytes, perm, b_first, b_order, items, n_blocks, K, mirror,
+                                      kdim, ncols, Y);
+}
+#undef SSCN_ROWS_ARGS
 
 // Bt[o][n][k] = W[o][k][n]
 template <typename T>
@@ -1451,7 +1472,7 @@ static bool rows_eligible(const View& v, int kdim, int ncols) {
          std::max(v.n_in, v.n_out) < (int64_t)kPlanNoRow && ceil_div(v.n_out, kPlanRows) * v.K < INT32_MAX;
 }
 
-template <typename T, int WB, int NB, int PK = 1, bool TB = false>
+template <typename T, int WB, int NB, int PK = 1, bool TB = false, bool DG = false>
 static sscn_status launch_rows_nb(const T* X, const T* B, const View& v, int kdim, int ncols, const Heads<T>& Y,
                                   hipStream_t s) {
   const int64_t nb = v.st->n_blocks;
@@ -1461,7 +1482,11 @@ static sscn_status launch_rows_nb(const T* X, const T* B, const View& v, int kdi
   const uint32_t bb = (uint32_t)((uint64_t)v.K * ncols * kdim * sizeof(T));
   // loads two steps ahead for 64-byte windows (short steps), one otherwise;
   // six workgroups per CU for 64-byte windows (80 VGPRs), five otherwise
-  auto kern = k_conv_rows<T, WB, NB, WB == 64 ? 3 : 2, PK, TB>;
+  constexpr int D = WB == 64 ? 3 : 2;
+  auto kern = [] {
+    if constexpr (DG) return k_dgrad_rows<T, WB, NB, D, PK, TB>;
+    else return k_conv_rows<T, WB, NB, D, PK, TB>;
+  }();
   int cus = 256, per_cu = 1;
   occupancy((const void*)kern, 256, 0, &per_cu, &cus);
   // persistent: one resident wave of workgroups per column group
@@ -1483,7 +1508,8 @@ static bool rows_take_untransposed(int kdim, int ncols) {
   return sizeof(T) == 4 && ncols % 4 == 0 && ncols % 64 != 0 && kdim * sizeof(T) != 64;
 }
 
-template <typename T>
+// DG: a dgrad launch (k_dgrad_rows), else a forward one (k_conv_rows).
+template <typename T, bool DG = false>
 static sscn_status launch_rows(const T* X, const T* B, const View& v, int kdim, int ncols, const Heads<T>& Y,
                                hipStream_t s, bool untransposed = false) {
   if (v.n_out == 0) return Y.n_zero > 0 ? fill_f32(Y.zero, 0.f, Y.n_zero, s) : SSCN_OK;
@@ -1495,28 +1521,28 @@ static sscn_status launch_rows(const T* X, const T* B, const View& v, int kdim, 
   // 96 or 160 columns.  128-byte windows (32 fp32 or 64 bf16 channels)
   // unless a bf16 row is not a multiple of 128 bytes.
   const bool wide_cols = sizeof(T) == 2 ? ncols > 32 : ncols % 64 == 0;
-  if constexpr (sizeof(T) == 4) {
+  if constexpr (sizeof(T) == 4 && !DG) {
     if (untransposed) {
       if (!rows_take_untransposed<T>(kdim, ncols)) return fail(SSCN_ERR_INVALID_ARG, "weights layout");
-      return launch_rows_nb<T, 128, 2, 1, true>(X, B, v, kdim, ncols, Y, s);
+      return launch_rows_nb<T, 128, 2, 1, true, DG>(X, B, v, kdim, ncols, Y, s);
     }
   }
   // Rows of half a window (32 bf16 or 16 fp32 channels, 16 bf16 in a
   // 64-byte window): two items per step.
   const uint32_t row_bytes = (uint32_t)kdim * sizeof(T);
   if (row_bytes == 64)
-    return wide_cols ? launch_rows_nb<T, 128, 4, 2>(X, B, v, kdim, ncols, Y, s)
-                     : launch_rows_nb<T, 128, 2, 2>(X, B, v, kdim, ncols, Y, s);
+    return wide_cols ? launch_rows_nb<T, 128, 4, 2, false, DG>(X, B, v, kdim, ncols, Y, s)
+                     : launch_rows_nb<T, 128, 2, 2, false, DG>(X, B, v, kdim, ncols, Y, s);
   if constexpr (sizeof(T) == 2) {
     if (row_bytes == 32)
-      return wide_cols ? launch_rows_nb<T, 64, 4, 2>(X, B, v, kdim, ncols, Y, s)
-                       : launch_rows_nb<T, 64, 2, 2>(X, B, v, kdim, ncols, Y, s);
+      return wide_cols ? launch_rows_nb<T, 64, 4, 2, false, DG>(X, B, v, kdim, ncols, Y, s)
+                       : launch_rows_nb<T, 64, 2, 2, false, DG>(X, B, v, kdim, ncols, Y, s);
     if (kdim % 64 != 0)
-      return wide_cols ? launch_rows_nb<T, 64, 4>(X, B, v, kdim, ncols, Y, s)
-                       : launch_rows_nb<T, 64, 2>(X, B, v, kdim, ncols, Y, s);
+      return wide_cols ? launch_rows_nb<T, 64, 4, 1, false, DG>(X, B, v, kdim, ncols, Y, s)
+                       : launch_rows_nb<T, 64, 2, 1, false, DG>(X, B, v, kdim, ncols, Y, s);
   }
-  return wide_cols ? launch_rows_nb<T, 128, 4>(X, B, v, kdim, ncols, Y, s)
-                   : launch_rows_nb<T, 128, 2>(X, B, v, kdim, ncols, Y, s);
+  return wide_cols ? launch_rows_nb<T, 128, 4, 1, false, DG>(X, B, v, kdim, ncols, Y, s)
+                   : launch_rows_nb<T, 128, 2, 1, false, DG>(X, B, v, kdim, ncols, Y, s);
 }
 
 // N contiguous channels of one row as fp32, one raw buffer load (an
@@ -1833,6 +1859,7 @@ extern "C" sscn_status sparse_conv_forward(const void* features, const void* wei
   if (st != SSCN_OK) return st;
   const View v = view_of(rb);
   if (v.n_out == 0) return SSCN_OK;
+  UseNote note{rb->d, stream};
   if (!out || !weights || (v.n_in > 0 && !features))
     return fail(SSCN_ERR_INVALID_ARG, "NULL features, weights or out");
   if (dtype == SSCN_F32)
@@ -1870,6 +1897,7 @@ extern "C" sscn_status sparse_conv_forward_heads(const void* features, const voi
   }
   const View v = view_of(rb);
   if (v.n_out == 0) return SSCN_OK;
+  UseNote note{rb->d, stream};
   if (!weights || (v.n_in > 0 && !features)) return fail(SSCN_ERR_INVALID_ARG, "NULL features or weights");
   if (dtype == SSCN_F32)
     return forward_t<float>((const float*)features, (const float*)weights, v, c_in, c_out,
@@ -1884,6 +1912,7 @@ extern "C" sscn_status sparse_conv_backward(const void* features, const void* we
   sscn_status st = check_conv_args(rb, c_in, c_out, dtype);
   if (st != SSCN_OK) return st;
   const View v = view_of(rb);
+  UseNote note{rb->d, stream};
   const int64_t w_total = (int64_t)v.K * c_in * c_out;
   bool w_zeroed = false;  // the dgrad launch cleared wgrad on the side
   if (dgrad && v.n_in > 0) {
@@ -1895,7 +1924,7 @@ extern "C" sscn_status sparse_conv_backward(const void* features, const void* we
       Heads<float> h = plain_heads((float*)dgrad, c_in);
       if (rows_eligible<float>(vt, c_out, c_in)) {
         if (wgrad) { h.zero = wgrad; h.n_zero = w_total; w_zeroed = true; }
-        st = launch_rows<float>((const float*)dout, (const float*)weights, vt, c_out, c_in, h, stream);
+        st = launch_rows<float, true>((const float*)dout, (const float*)weights, vt, c_out, c_in, h, stream);
       } else {
         st = launch_conv<float, true>((const float*)dout, (const float*)weights, vt, c_out, c_in, h, stream);
       }
@@ -1903,7 +1932,7 @@ extern "C" sscn_status sparse_conv_backward(const void* features, const void* we
       Heads<bf16_t> h = plain_heads((bf16_t*)dgrad, c_in);
       if (rows_eligible<bf16_t>(vt, c_out, c_in)) {
         if (wgrad) { h.zero = wgrad; h.n_zero = w_total; w_zeroed = true; }
-        st = launch_rows<bf16_t>((const bf16_t*)dout, (const bf16_t*)weights, vt, c_out, c_in, h, stream);
+        st = launch_rows<bf16_t, true>((const bf16_t*)dout, (const bf16_t*)weights, vt, c_out, c_in, h, stream);
       } else {
         st = launch_conv<bf16_t, true>((const bf16_t*)dout, (const bf16_t*)weights, vt, c_out, c_in, h, stream);
       }

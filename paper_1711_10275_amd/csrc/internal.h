@@ -119,7 +119,25 @@ struct RulebookData {
   hipEvent_t chunk_ready = nullptr;
   hipEvent_t plan_ready = nullptr;   // the same for the row-block plans
   hipEvent_t order_ready = nullptr;  // and for the tile orders
+  // Work that reads the rule book on streams other than the build stream:
+  // per such stream, an event recorded after its latest use.  The storage
+  // goes back to the block cache on the build stream, so the destructor
+  // first makes the build stream wait for each of these events; later
+  // allocations on the build stream are then ordered after every reader.
+  std::mutex use_mu;
+  std::vector<std::pair<hipStream_t, hipEvent_t>> foreign_uses;
+  void note_use(hipStream_t s);
   ~RulebookData();
+};
+
+// Records, when it goes out of scope, that work reading `d` was queued on
+// `s` (see RulebookData::foreign_uses).
+struct UseNote {
+  RulebookData* d;
+  hipStream_t s;
+  ~UseNote() {
+    if (d) d->note_use(s);
+  }
 };
 
 }  // namespace sscn

@@ -1931,6 +1931,7 @@ extern "C" sscn_status sscn_rulebook_out_coords(sscn_rulebook rb, int32_t* out_c
   if (!out_coords) return fail(SSCN_ERR_INVALID_ARG, "out_coords is NULL");
   // a transposed SC view outputs at the SC's input sites
   const int32_t* src = (rb->transposed && !d->submanifold) ? d->in_coords : d->out_coords;
+  UseNote note{rb->d, s};
   SSCN_HIP(hipMemcpyAsync(out_coords, src, sizeof(int32_t) * 4 * n_out, hipMemcpyDeviceToDevice, s));
   return SSCN_OK;
 }
@@ -1942,6 +1943,7 @@ extern "C" sscn_status sscn_rulebook_export(sscn_rulebook rb, int32_t* in_rows, 
   if (d->n_pairs == 0) return SSCN_OK;
   if (!in_rows || !out_rows || !offsets) return fail(SSCN_ERR_INVALID_ARG, "NULL export array");
   const View v = view_of(rb);
+  UseNote note{rb->d, s};
   // stored segment boundaries per offset: seg[o * n_tiles], read on the host
   std::vector<int64_t> start(d->K + 1);
   int64_t acc = 0;

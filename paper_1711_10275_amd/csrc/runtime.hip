@@ -145,10 +145,33 @@ void occupancy(const void* kern, int block, size_t lds, int* per_cu, int* cus) {
   *cus = n_cu;
 }
 
+void RulebookData::note_use(hipStream_t s) {
+  if (s == stream) return;
+  std::lock_guard<std::mutex> lock(use_mu);
+  hipEvent_t ev = nullptr;
+  for (auto& u : foreign_uses)
+    if (u.first == s) ev = u.second;
+  if (!ev) {
+    if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess) {
+      // without an event the build stream cannot be ordered after s: wait
+      // for s here instead
+      (void)hipGetLastError();
+      (void)hipStreamSynchronize(s);
+      return;
+    }
+    foreign_uses.emplace_back(s, ev);
+  }
+  (void)hipEventRecord(ev, s);
+}
+
 RulebookData::~RulebookData() {
   int cur = 0;
   (void)hipGetDevice(&cur);
   if (cur != device) (void)hipSetDevice(device);
+  for (auto& u : foreign_uses) {
+    (void)hipStreamWaitEvent(stream, u.second, 0);
+    (void)hipEventDestroy(u.second);
+  }
   for (void* p : blocks) dev_free(p, stream);
   if (chunk_ready) (void)hipEventDestroy(chunk_ready);
   if (plan_ready) (void)hipEventDestroy(plan_ready);
@@ -310,3 +333,12 @@ sscn_status exclusive_scan_i32(const int32_t* in, int32_t* out, int64_t count, h
 }  // namespace sscn
 
 extern "C" const char* sscn_last_error(void) { return sscn::g_last_error.c_str(); }
+
+extern "C" sscn_status sscn_release_cached(void) {
+  int dev = 0;
+  SSCN_HIP(hipGetDevice(&dev));
+  sscn::Cache& c = sscn::cache();
+  std::lock_guard<std::mutex> lock(c.mu);
+  sscn::release_idle(c, dev);
+  return SSCN_OK;
+}

@@ -60,6 +60,7 @@ _SIGS = {
     "sparse_conv_backward": [_vp, _vp, _vp, _vp, _i32, _i32, ctypes.c_int, _vp, _vp, _vp],
     "sscn_affine_relu": [_vp, _vp, _vp, _i64, _i32, ctypes.c_int, _vp, _vp],
     "sscn_concat_cols": [_vp, _i32, _vp, _i32, _i64, ctypes.c_int, _vp, _vp],
+    "sscn_release_cached": [],
     "sscn_last_error": [],
 }
 
@@ -296,12 +297,25 @@ def affine_relu(x, scale, shift, out=None):
     shift = _dev_tensor(shift, "shift", torch.float32)
     if scale.numel() != c or shift.numel() != c:
         raise ValueError("scale / shift must have one entry per channel")
-    y = torch.empty_like(x) if out is None else _dev_tensor(out, "out", x.dtype)
+    if scale.device != x.device or shift.device != x.device:
+        raise ValueError("scale / shift must be on x's device")
+    if out is None:
+        y = torch.empty_like(x)
+    else:
+        y = _dev_tensor(out, "out", x.dtype)
+        if y.shape != x.shape or y.device != x.device:
+            raise ValueError(f"out must be a {tuple(x.shape)} tensor on {x.device}")
     with torch.cuda.device(x.device):
         _check(lib().sscn_affine_relu(ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(scale.data_ptr()),
                                       ctypes.c_void_p(shift.data_ptr()), n, c, _dtype_code(x),
                                       ctypes.c_void_p(y.data_ptr()), _stream(x)))
     return y
+
+
+def release_cached(device=None):
+    """Return the library's idle device blocks on `device` to the device."""
+    with torch.cuda.device(device if device is not None else torch.cuda.current_device()):
+        _check(lib().sscn_release_cached())
 
 
 def concat_cols(a, b):

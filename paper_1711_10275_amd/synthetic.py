@@ -224,6 +224,12 @@ def bf16_round(a):
     return out
 
 
+def shuffled(coords, seed):
+    """The same active sites with their rows in a seeded random order (the
+    locality-sensitivity run: feature rows no longer follow the grid)."""
+    return np.ascontiguousarray(coords[np.random.default_rng(seed).permutation(coords.shape[0])])
+
+
 def features(n, c, seed, bf16=False):
     x = np.random.default_rng(seed).standard_normal((n, c), dtype=np.float32)
     return bf16_round(x) if bf16 else x

@@ -1,4 +1,8 @@
-"""GPU forward / backward of SSC, SC and DC layers against the fp64 CPU oracle."""
+"""GPU forward / backward of SSC, SC and DC layers against the fp64 CPU oracle.
+
+wgrad is always checked at the fp32 tolerance: it is an fp32 output, and
+with bf16 inputs every product is exact in fp32 (8-bit significands), so
+only the fp32 accumulation rounds, as in the fp32 layer."""
 import numpy as np
 import pytest
 import torch
@@ -123,7 +127,7 @@ def test_ssc_backward_shapes128(dtype):
     dx, dw = sscn.sparse_conv_backward(dev(X, TD[dtype]), dev(W, TD[dtype]), dev(G, TD[dtype]), rb)
     rdx, rdw = O.backward(X, W, G, orb)
     assert_close(host(dx), rdx, dtype, "dgrad")
-    assert_close(host(dw), rdw, "f32" if dtype == "f32" else "bf16", "wgrad")
+    assert_close(host(dw), rdw, "f32", "wgrad")
     # dgrad only / wgrad only
     dx2, none = sscn.sparse_conv_backward(None, dev(W, TD[dtype]), dev(G, TD[dtype]), rb, wgrad=False)
     assert none is None
@@ -143,7 +147,7 @@ def test_sc_and_dc_backward_small(f, s, dtype):
         dx, dw = sscn.sparse_conv_backward(dev(X, TD[dtype]), dev(W, TD[dtype]), dev(G, TD[dtype]), view)
         rdx, rdw = O.backward(X, W, G, oview)
         assert_close(host(dx), rdx, dtype, "dgrad")
-        assert_close(host(dw), rdw, dtype, "wgrad")
+        assert_close(host(dw), rdw, "f32", "wgrad")
 
 
 def test_sc22_backward_shapes128():
@@ -210,11 +214,23 @@ def _heads_case(rb, orb, cin, cout, dtype, seed):
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("cin,cout", [(64, 64), (32, 48), (24, 128)])
 def test_forward_heads_ssc(cin, cout, dtype):
-    """Activated + plain heads on the 128^3 shapes workload (64-multiple c_out
-    takes the quad kernel, the others the column kernel)."""
+    """Activated + plain heads on the 128^3 shapes workload (the row-block
+    kernel: 64- and 32-column groups, fp32 with and without the transposed
+    weight copy)."""
     coords, size = coords_for("shapes128")
     _heads_case(sscn.ssc_rulebook_build(dev(coords), size, 3), O.ssc_rulebook(coords, size, 3),
                 cin, cout, dtype, 41)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("f,cin,cout", [(5, 16, 24), (3, 12, 20), (3, 20, 130)])
+def test_forward_heads_fallback_kernels(f, cin, cout, dtype):
+    """Heads through the kernels that run where the row-block plan does not:
+    125 offsets (5^3 filter: chunk kernels) and input widths that are not a
+    multiple of 8 (generic kernel), two heads each."""
+    size = (9, 8, 10)
+    c = small_set(80 + f + cin, size, batch=2, density=0.2)
+    _heads_case(sscn.ssc_rulebook_build(dev(c), size, f), O.ssc_rulebook(c, size, f), cin, cout, dtype, 45 + f)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -263,7 +279,7 @@ def test_sc_and_dc_row_blocks(f, s, dtype):
         dx, dw = sscn.sparse_conv_backward(dev(X, TD[dtype]), dev(W, TD[dtype]), dev(G, TD[dtype]), view)
         rdx, rdw = O.backward(X, W, G, oview)
         assert_close(host(dx), rdx, dtype, "dgrad")
-        assert_close(host(dw), rdw, dtype, "wgrad")
+        assert_close(host(dw), rdw, "f32", "wgrad")
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -280,7 +296,7 @@ def test_ssc_filter5(dtype):
     dx, dw = sscn.sparse_conv_backward(dev(X, TD[dtype]), dev(W, TD[dtype]), dev(G, TD[dtype]), rb)
     rdx, rdw = O.backward(X, W, G, orb)
     assert_close(host(dx), rdx, dtype, "dgrad")
-    assert_close(host(dw), rdw, dtype, "wgrad")
+    assert_close(host(dw), rdw, "f32", "wgrad")
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
