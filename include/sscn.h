@@ -187,6 +187,28 @@ sscn_status sparse_conv_forward_heads(const void* features, const void* weights,
                                       const sscn_conv_output* heads, hipStream_t stream);
 
 /*
+ * sparse_conv_forward_noalloc -- sparse_conv_forward for callers that cannot
+ * allocate device memory (code under stream capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments, same kernels and the
+ * same (bit-identical) result; it allocates nothing:
+ *   - the forward's one temporary, a transposed copy of the weights, goes to
+ *     a fixed 8 MiB region of the library's code object (one per device,
+ *     held until the process ends): K * c_in * c_out elements of dtype must
+ *     fit in 8 MiB, else SSCN_ERR_INVALID_ARG (nothing is queued);
+ *   - the rule book's kernel tables must already exist: an SSC rule book
+ *     with at most 32 offsets has them from its build, any other gets them
+ *     from one sparse_conv_forward / sparse_conv_backward on it (same
+ *     direction); otherwise SSCN_ERR_INVALID_ARG, `out` untouched.
+ * Every call on a device shares that device's region, which keeps the last
+ * call's contents: calls that overlap on one device (concurrent streams or
+ * host threads) race on it and must be serialised by the caller.
+ * Asynchronous on `stream`.
+ */
+sscn_status sparse_conv_forward_noalloc(const void* features, const void* weights, sscn_rulebook rb,
+                                        int32_t c_in, int32_t c_out, sscn_dtype dtype, void* out,
+                                        hipStream_t stream);
+
+/*
  * sparse_conv_backward -- gradients of sparse_conv_forward (its adjoint):
  *   dgrad[j] = sum_o sum_{(j,k) in R_o} dout[k] * (W^o)^T   (n_in x c_in)
  *   wgrad[o] = sum_{(j,k) in R_o} features[j]^T dout[k]    (K x c_in x c_out, fp32)

@@ -1423,6 +1423,23 @@ static bool quad_eligible(const View& v, int cin, int cout) {
   return v.K <= 32767 && cin % 8 == 0 && kb <= max_kb && x_bytes < kOobOffset && w_bytes < kOobOffset;
 }
 
+// A temporary copy of the weights (K x c_in x c_out elements): from the
+// block cache, or from the caller's region while a no-allocation entry point
+// runs (then it is not released).
+template <typename T>
+static sscn_status temp_weights(T** p, int64_t count, hipStream_t s) {
+  if (const NoAlloc* na = no_alloc()) {
+    if ((size_t)count * sizeof(T) > na->bytes) return fail(SSCN_ERR_INVALID_ARG, "weights exceed the scratch region");
+    *p = (T*)na->scratch;
+    return SSCN_OK;
+  }
+  return dev_alloc((void**)p, sizeof(T) * count, s);
+}
+
+static void temp_release(void* p, hipStream_t s) {
+  if (!no_alloc()) dev_free(p, s);
+}
+
 template <typename T, bool WT>
 static sscn_status launch_conv(const T* X, const T* W, const View& v, int cin, int cout, const Heads<T>& Y, hipStream_t s) {
   if (v.st->n_tiles == 0) return SSCN_OK;
@@ -1447,17 +1464,17 @@ static sscn_status launch_conv(const T* X, const T* W, const View& v, int cin, i
   T* tmp = nullptr;
   if constexpr (!WT) {
     const int64_t total = (int64_t)v.K * cin * cout;
-    SSCN_TRY(dev_alloc((void**)&tmp, sizeof(T) * total, s));
+    SSCN_TRY(temp_weights(&tmp, total, s));
     k_transpose_w<T><<<(unsigned)std::min<int64_t>(ceil_div(total, 256), 4096), 256, 0, s>>>(W, v.K, cin, cout, tmp);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) {
-      dev_free(tmp, s);
+      temp_release(tmp, s);
       return hip_fail(e, "transpose launch");
     }
     Bt = tmp;
   }
   sscn_status st = launch_generic(X, Bt, v, cin, cout, Y, s);
-  dev_free(tmp, s);
+  temp_release(tmp, s);
   return st;
 }
 
@@ -1815,22 +1832,22 @@ static sscn_status forward_t(const T* X, const T* W, const View& v, int cin, int
     if (rows_take_untransposed<T>(cin, cout)) return launch_rows<T>(X, W, v, cin, cout, Y, s, true);
     const int64_t total = (int64_t)v.K * cin * cout;
     T* Bt = nullptr;
-    SSCN_TRY(dev_alloc((void**)&Bt, sizeof(T) * total, s));
+    SSCN_TRY(temp_weights(&Bt, total, s));
     k_transpose_w<T><<<(unsigned)std::min<int64_t>(ceil_div(total, 256), 4096), 256, 0, s>>>(W, v.K, cin, cout, Bt);
     hipError_t e = hipGetLastError();
     sscn_status st = e == hipSuccess ? launch_rows<T>(X, Bt, v, cin, cout, Y, s) : hip_fail(e, "transpose");
-    dev_free(Bt, s);
+    temp_release(Bt, s);
     return st;
   }
   if (prefer_col<T>(v, cin, cout)) {
     if (v.n_out == 0) return SSCN_OK;
     const int64_t total = (int64_t)v.K * cin * cout;
     T* Bt = nullptr;
-    SSCN_TRY(dev_alloc((void**)&Bt, sizeof(T) * total, s));
+    SSCN_TRY(temp_weights(&Bt, total, s));
     k_transpose_w<T><<<(unsigned)std::min<int64_t>(ceil_div(total, 256), 4096), 256, 0, s>>>(W, v.K, cin, cout, Bt);
     hipError_t e = hipGetLastError();
     sscn_status st = e == hipSuccess ? launch_col<T>(X, Bt, v, cin, cout, Y, s) : hip_fail(e, "transpose");
-    dev_free(Bt, s);
+    temp_release(Bt, s);
     return st;
   }
   if constexpr (sizeof(T) == 2) {
@@ -1839,11 +1856,11 @@ static sscn_status forward_t(const T* X, const T* W, const View& v, int cin, int
     if (v.st->n_tiles == 0) return SSCN_OK;
     const int64_t total = (int64_t)v.K * cin * cout;
     T* Bt = nullptr;
-    SSCN_TRY(dev_alloc((void**)&Bt, sizeof(T) * total, s));
+    SSCN_TRY(temp_weights(&Bt, total, s));
     k_transpose_w<T><<<(unsigned)std::min<int64_t>(ceil_div(total, 256), 4096), 256, 0, s>>>(W, v.K, cin, cout, Bt);
     hipError_t e = hipGetLastError();
     sscn_status st = e == hipSuccess ? launch_conv<T, true>(X, Bt, v, cin, cout, Y, s) : hip_fail(e, "transpose");
-    dev_free(Bt, s);
+    temp_release(Bt, s);
     return st;
   }
 }
@@ -1957,4 +1974,64 @@ extern "C" sscn_status sparse_conv_backward(const void* features, const void* we
     }
   }
   return st;
+}
+
+// ------------------------------------------------ no-allocation forward
+// The forward's only temporary is the transposed copy of the weights.  For
+// callers that cannot allocate device memory, it lives in a fixed region of
+// the library's code object (one copy per device, kept until the process
+// ends).  Host code uses the region only through the device address that
+// hipGetSymbolAddress returns for the current device.
+namespace {
+constexpr size_t kScratchBytes = (size_t)8 << 20;
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+sscn_status scratch_address(void** out) {
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = 0;
+  SSCN_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(SSCN_ERR_INVALID_ARG, "device index out of range");
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    SSCN_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(SSCN_ERR_DEVICE, "no device address for the scratch region");
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return SSCN_OK;
+}
+
+struct NoAllocScope {
+  explicit NoAllocScope(const NoAlloc* na) { set_no_alloc(na); }
+  ~NoAllocScope() { set_no_alloc(nullptr); }
+};
+}  // namespace
+
+extern "C" sscn_status sparse_conv_forward_noalloc(const void* features, const void* weights, sscn_rulebook rb,
+                                                   int32_t c_in, int32_t c_out, sscn_dtype dtype, void* out,
+                                                   hipStream_t stream) {
+  sscn_status st = check_conv_args(rb, c_in, c_out, dtype);
+  if (st != SSCN_OK) return st;
+  const View v = view_of(rb);
+  const size_t w_bytes = (size_t)v.K * c_in * c_out * (dtype == SSCN_F32 ? 4 : 2);
+  if (w_bytes > kScratchBytes)
+    return fail(SSCN_ERR_INVALID_ARG, "weights of " + std::to_string(w_bytes) + " bytes exceed the " +
+                                          std::to_string(kScratchBytes) + "-byte scratch region of the "
+                                          "no-allocation forward");
+  if (v.n_out == 0) return SSCN_OK;
+  if (!out || !weights || (v.n_in > 0 && !features))
+    return fail(SSCN_ERR_INVALID_ARG, "NULL features, weights or out");
+  NoAlloc na;
+  SSCN_TRY(scratch_address(&na.scratch));
+  na.bytes = kScratchBytes;
+  NoAllocScope scope(&na);
+  UseNote note{rb->d, stream};
+  if (dtype == SSCN_F32)
+    return forward_t<float>((const float*)features, (const float*)weights, v, c_in, c_out,
+                            plain_heads((float*)out, c_out), stream);
+  return forward_t<bf16_t>((const bf16_t*)features, (const bf16_t*)weights, v, c_in, c_out,
+                           plain_heads((bf16_t*)out, c_out), stream);
 }

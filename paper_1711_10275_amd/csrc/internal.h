@@ -68,6 +68,16 @@ sscn_status hip_fail(hipError_t e, const char* what);
 sscn_status dev_alloc(void** p, size_t bytes, hipStream_t s);
 void dev_free(void* p, hipStream_t s);
 
+// Set (on the calling thread) while an entry point that must not allocate
+// runs: the rule-book tables built on first use are then an error instead of
+// being built, and temporaries come from the caller-provided region.
+struct NoAlloc {
+  void* scratch = nullptr;  // device address of the temporary region
+  size_t bytes = 0;
+};
+const NoAlloc* no_alloc();
+void set_no_alloc(const NoAlloc* na);
+
 // One direction of a rule book: tiles over the output rows of that
 // direction, offset-major segments, and the pair arrays (pointers into the
 // rule book's device blocks).

@@ -1085,6 +1085,10 @@ sscn_status ensure_chunks(const View& v, hipStream_t s) {
   {
     std::lock_guard<std::mutex> lock(d->chunk_mu);
     if (st.ctile == nullptr) {
+      if (no_alloc())
+        return fail(SSCN_ERR_INVALID_ARG,
+                    "the rule book's chunk table is not built yet and this call may not allocate: run "
+                    "sparse_conv_forward or sparse_conv_backward on it once first");
       int cur = 0;
       SSCN_HIP(hipGetDevice(&cur));
       if (cur != d->device) return fail(SSCN_ERR_INVALID_ARG, "rule book used on another device");
@@ -1104,6 +1108,10 @@ sscn_status ensure_order(const View& v, hipStream_t s) {
   {
     std::lock_guard<std::mutex> lock(d->chunk_mu);
     if (!st.order_built) {
+      if (no_alloc())
+        return fail(SSCN_ERR_INVALID_ARG,
+                    "the rule book's tile order is not built yet and this call may not allocate: run "
+                    "sparse_conv_forward or sparse_conv_backward on it once first");
       int cur = 0;
       SSCN_HIP(hipGetDevice(&cur));
       if (cur != d->device) return fail(SSCN_ERR_INVALID_ARG, "rule book used on another device");
@@ -1555,6 +1563,10 @@ sscn_status ensure_plan(const View& v, hipStream_t s) {
   {
     std::lock_guard<std::mutex> lock(d->chunk_mu);
     if (st.b_first == nullptr) {
+      if (no_alloc())
+        return fail(SSCN_ERR_INVALID_ARG,
+                    "the rule book's row-block plan is not built yet and this call may not allocate: run "
+                    "sparse_conv_forward or sparse_conv_backward on it once first");
       int cur = 0;
       SSCN_HIP(hipGetDevice(&cur));
       if (cur != d->device) return fail(SSCN_ERR_INVALID_ARG, "rule book used on another device");

@@ -101,6 +101,10 @@ sscn_status dev_alloc(void** p, size_t bytes, hipStream_t s) {
   return SSCN_OK;
 }
 
+static thread_local const NoAlloc* t_no_alloc = nullptr;
+const NoAlloc* no_alloc() { return t_no_alloc; }
+void set_no_alloc(const NoAlloc* na) { t_no_alloc = na; }
+
 void dev_free(void* p, hipStream_t s) {
   if (!p) return;
   Cache& c = cache();

@@ -21,6 +21,7 @@ HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "sscn.h")
 
 F32, BF16 = 0, 1
 STATUS = {0: "ok", 1: "invalid_arg", 2: "shape", 3: "out_of_range", 4: "duplicate", 5: "oom", 6: "device"}
+STATUS_CODES = {v: k for k, v in STATUS.items()}
 
 
 class SSCNError(RuntimeError):
@@ -57,6 +58,7 @@ _SIGS = {
     "sscn_rulebook_free": [_vp],
     "sparse_conv_forward": [_vp, _vp, _vp, _i32, _i32, ctypes.c_int, _vp, _vp],
     "sparse_conv_forward_heads": [_vp, _vp, _vp, _i32, _i32, ctypes.c_int, _i32, _vp, _vp],
+    "sparse_conv_forward_noalloc": [_vp, _vp, _vp, _i32, _i32, ctypes.c_int, _vp, _vp],
     "sparse_conv_backward": [_vp, _vp, _vp, _vp, _i32, _i32, ctypes.c_int, _vp, _vp, _vp],
     "sscn_affine_relu": [_vp, _vp, _vp, _i64, _i32, ctypes.c_int, _vp, _vp],
     "sscn_concat_cols": [_vp, _i32, _vp, _i32, _i64, ctypes.c_int, _vp, _vp],
