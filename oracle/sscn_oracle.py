@@ -16,6 +16,8 @@ Submanifold Sparse Convolutional Networks", arXiv:1711.10275):
   input is active, i.e. the output set is the input set         Sec. 4.1
 * DC: the SC connections inverted; output set = SC input set    Sec. 4.1
 * output = 0, then out[k] += in[j] W^i for every (j, k) in R_i   Sec. 4.2
+* MP / AP pooling over SC connections, nearest-neighbour
+  upsampling back through them                   Sec. 4.1, Sec. 5
 * backward: the adjoint of that linear map (the paper trains the
   networks, Sec. 6.2, but does not spell the gradients out)
 
@@ -269,6 +271,99 @@ def canonical_triples(rb):
 def macs(rb, cin, cout):
     """Multiply-adds of one layer: sum over output sites of a*m*n (Table 2)."""
     return rb.n_pairs() * cin * cout
+
+
+# --------------------------------------------------------------------------
+# pooling and upsampling (Sec. 4.1 "Other operators"; Sec. 5 FCN upsampling)
+# --------------------------------------------------------------------------
+NO_ARGMAX = -1   # the zero vector is the maximum (no input receives gradient)
+
+
+def _pool_rulebook(rb):
+    if rb.submanifold:
+        raise InvalidArg("pooling is defined over SC(f, s) connections")
+    return rb
+
+
+def max_pool(X, rb):
+    """MP(f, s): a variant of SC(., ., f, s) whose output at each active site
+    is, per channel, the maximum of the zero vector and the input vectors in
+    its receptive field (Sec. 4.1).  rb is the SC(f, s) rule book.
+
+    Returns (Y, A): Y n_out x C (fp64) and A n_out x C, the offset o of the
+    input that attains each maximum (the smallest such o when several tie),
+    or NO_ARGMAX where no input exceeds zero."""
+    _pool_rulebook(rb)
+    X = np.asarray(X, np.float64)
+    C = X.shape[1]
+    Y = np.zeros((rb.n_out, C), np.float64)
+    A = np.full((rb.n_out, C), NO_ARGMAX, np.int64)
+    for o in range(rb.K):                   # increasing o: a later equal value never wins
+        j, k = rb.ins[o], rb.outs[o]        # within one R_o every output appears once
+        v = X[j]
+        win = v > Y[k]
+        Y[k] = np.where(win, v, Y[k])
+        A[k] = np.where(win, o, A[k])
+    return Y, A
+
+
+def max_pool_backward(dY, A, rb):
+    """Gradient of max_pool: each output element's gradient goes to the
+    input that attained its maximum (none where the zero vector did)."""
+    _pool_rulebook(rb)
+    dY = np.asarray(dY, np.float64)
+    dX = np.zeros((rb.n_in, dY.shape[1]), np.float64)
+    for o in range(rb.K):
+        j, k = rb.ins[o], rb.outs[o]
+        np.add.at(dX, j, np.where(A[k] == o, dY[k], 0.0))
+    return dX
+
+
+def avg_pool(X, rb):
+    """AP(f, s): f^-d times the sum of the active input vectors in the
+    receptive field (Sec. 4.1); inactive sites contribute zero."""
+    _pool_rulebook(rb)
+    X = np.asarray(X, np.float64)
+    Y = np.zeros((rb.n_out, X.shape[1]), np.float64)
+    for o in range(rb.K):
+        np.add.at(Y, rb.outs[o], X[rb.ins[o]])
+    return Y / float(rb.f ** D)
+
+
+def avg_pool_backward(dY, rb):
+    _pool_rulebook(rb)
+    dY = np.asarray(dY, np.float64)
+    dX = np.zeros((rb.n_in, dY.shape[1]), np.float64)
+    for o in range(rb.K):
+        np.add.at(dX, rb.ins[o], dY[rb.outs[o]])
+    return dX / float(rb.f ** D)
+
+
+def upsample_nearest(Y, rb):
+    """Nearest-neighbour upsampling of the FCN (Sec. 5): features on the
+    output sites of an SC(s, s) downsampling are copied back to every input
+    site of it, i.e. input site x receives the features of the output site
+    whose s^d block holds x.  Needs f = s (each input has exactly one such
+    output)."""
+    if rb.submanifold or rb.f != rb.stride:
+        raise InvalidArg("nearest-neighbour upsampling inverts an SC(s, s) downsampling")
+    Y = np.asarray(Y, np.float64)
+    out = np.zeros((rb.n_in, Y.shape[1]), np.float64)
+    for o in range(rb.K):
+        out[rb.ins[o]] = Y[rb.outs[o]]
+    return out
+
+
+def upsample_nearest_backward(dOut, rb):
+    """Gradient of upsample_nearest: each output site sums the gradients of
+    the input sites it was copied to."""
+    if rb.submanifold or rb.f != rb.stride:
+        raise InvalidArg("nearest-neighbour upsampling inverts an SC(s, s) downsampling")
+    dOut = np.asarray(dOut, np.float64)
+    dY = np.zeros((rb.n_out, dOut.shape[1]), np.float64)
+    for o in range(rb.K):
+        np.add.at(dY, rb.outs[o], dOut[rb.ins[o]])
+    return dY
 
 
 # --------------------------------------------------------------------------

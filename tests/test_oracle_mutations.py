@@ -142,3 +142,76 @@ def test_backward_dropped_offset_caught(monkeypatch):
         return dX, dW
     monkeypatch.setattr(O, "backward", bad)
     assert _bwd_pin_error() > 1e-6
+
+
+# --------------------------------------------------------------------------
+# pooling and upsampling
+# --------------------------------------------------------------------------
+def _pool_pins_hold():
+    from tests import test_oracle_pool as P
+    try:
+        for size, f, s in P.CASES:
+            P.test_max_pool_is_relu_of_dense_max_pool(size, f, s)
+            P.test_avg_pool_is_dense_avg_pool(size, f, s)
+        P.test_max_pool_ties_go_to_the_smallest_offset()
+        for size, s in [((8, 8, 8), 2), ((9, 9, 9), 3)]:
+            P.test_upsample_is_dense_nearest(size, s)
+    except AssertionError:
+        return False
+    return True
+
+
+def test_pool_pins_hold_unmutated():
+    assert _pool_pins_hold()
+
+
+def test_max_pool_without_zero_floor_caught(monkeypatch):
+    def bad(X, rb):
+        X = np.asarray(X, np.float64)
+        Y = np.full((rb.n_out, X.shape[1]), -np.inf)
+        A = np.full((rb.n_out, X.shape[1]), O.NO_ARGMAX)
+        for o in range(rb.K):
+            j, k = rb.ins[o], rb.outs[o]
+            win = X[j] > Y[k]
+            Y[k] = np.where(win, X[j], Y[k])
+            A[k] = np.where(win, o, A[k])
+        return Y, A
+    monkeypatch.setattr(O, "max_pool", bad)
+    assert not _pool_pins_hold()
+
+
+def test_max_pool_last_tie_caught(monkeypatch):
+    orig = O.max_pool
+
+    def bad(X, rb):
+        # ties to the largest offset: run the offsets in reverse
+        rb2 = O.Rulebook(rb.f, rb.stride, rb.submanifold, rb.n_in, rb.n_out, rb.in_size, rb.out_size,
+                         rb.ins[::-1], rb.outs[::-1], rb.out_coords)
+        Y, A = orig(X, rb2)
+        return Y, np.where(A >= 0, rb.K - 1 - A, A)
+    monkeypatch.setattr(O, "max_pool", bad)
+    assert not _pool_pins_hold()
+
+
+def test_avg_pool_by_count_caught(monkeypatch):
+    def bad(X, rb):
+        X = np.asarray(X, np.float64)
+        Y = np.zeros((rb.n_out, X.shape[1]))
+        cnt = np.zeros(rb.n_out)
+        for o in range(rb.K):
+            np.add.at(Y, rb.outs[o], X[rb.ins[o]])
+            np.add.at(cnt, rb.outs[o], 1)
+        return Y / cnt[:, None]
+    monkeypatch.setattr(O, "avg_pool", bad)
+    assert not _pool_pins_hold()
+
+
+def test_upsample_wrong_parent_caught(monkeypatch):
+    def bad(Y, rb):
+        Y = np.asarray(Y, np.float64)
+        out = np.zeros((rb.n_in, Y.shape[1]))
+        for o in range(rb.K):
+            out[rb.ins[o]] = Y[np.roll(rb.outs[o], 1)]      # each input gets another input's parent
+        return out
+    monkeypatch.setattr(O, "upsample_nearest", bad)
+    assert not _pool_pins_hold()
