@@ -225,6 +225,59 @@ sscn_status sparse_conv_backward(const void* features, const void* weights, cons
                                  void* dgrad, float* wgrad, hipStream_t stream);
 
 /*
+ * Pooling (Sec. 4.1 "Other operators"): MP(f, s) and AP(f, s) are variants of
+ * SC(., ., f, s) -- same active output sites, same connections -- that
+ * reduce instead of multiply:
+ *   MP: out[k][c] = max(0, max over (j, k) in R_o of features[j][c])
+ *       (the maximum of the zero vector and the active inputs of the field);
+ *   AP: out[k][c] = f^-3 * sum over (j, k) in R_o of features[j][c]
+ *       (inactive sites contribute zero).
+ *   rb        an SC(f, s) rule book (not an SSC one, not a transposed view;
+ *             else SSCN_ERR_INVALID_ARG); rows as in sparse_conv_forward
+ *   features  device n_in x c, out device n_out x c (overwritten), in dtype;
+ *             bf16: the maximum is exact, the AP sum is taken in fp32 and
+ *             rounded once
+ *   argmax    MP only (else ignored, nullable): device uint8 n_out x c, the
+ *             offset o of the input that attains each maximum (the smallest
+ *             such o when several tie), 255 where the zero vector does;
+ *             K = f^3 must be at most 254
+ * Output rows are written once (no atomics): the result is deterministic.
+ */
+typedef enum { SSCN_POOL_MAX = 0, SSCN_POOL_AVG = 1 } sscn_pool_mode;
+sscn_status sscn_pool_forward(const void* features, sscn_rulebook rb, int32_t c, sscn_dtype dtype,
+                              sscn_pool_mode mode, void* out, uint8_t* argmax, hipStream_t stream);
+
+/*
+ * sscn_pool_backward -- gradient of sscn_pool_forward with respect to its
+ * features: MP routes dout[k][c] to the input at offset argmax[k][c] (none
+ * for 255); AP gives every input of the field f^-3 * dout[k][c], summed over
+ * the outputs it belongs to.
+ *   dout    device n_out x c;  argmax  MP: the forward's argmax (nullable for AP)
+ *   dgrad   device n_in x c, overwritten
+ */
+sscn_status sscn_pool_backward(const void* dout, const uint8_t* argmax, sscn_rulebook rb, int32_t c,
+                               sscn_dtype dtype, sscn_pool_mode mode, void* dgrad, hipStream_t stream);
+
+/*
+ * sscn_upsample_forward -- nearest-neighbour upsampling of the FCN (Sec. 5):
+ * undoes the downsampling of an SC(s, s) rule book rb (filter size equal to
+ * the stride, else SSCN_ERR_INVALID_ARG) by copying each of its output
+ * sites' features to every input site in that site's s^3 block.
+ *   features  device rb.n_out x c;  out  device rb.n_in x c (overwritten),
+ *   in the rule book's input row order
+ */
+sscn_status sscn_upsample_forward(const void* features, sscn_rulebook rb, int32_t c, sscn_dtype dtype,
+                                  void* out, hipStream_t stream);
+
+/*
+ * sscn_upsample_backward -- its gradient: dgrad[k] = sum of dout[j] over the
+ * input sites j of output site k's block.
+ *   dout  device rb.n_in x c;  dgrad  device rb.n_out x c (overwritten)
+ */
+sscn_status sscn_upsample_backward(const void* dout, sscn_rulebook rb, int32_t c, sscn_dtype dtype,
+                                   void* dgrad, hipStream_t stream);
+
+/*
  * sscn_affine_relu -- y[r][c] = max(0, x[r][c] * scale[c] + shift[c]) over the
  * n active rows: batch normalisation in inference form followed by ReLU,
  * both restricted to active sites (Sec. 4.1 "Other operators"; the

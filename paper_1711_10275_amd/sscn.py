@@ -62,6 +62,10 @@ _SIGS = {
     "sparse_conv_backward": [_vp, _vp, _vp, _vp, _i32, _i32, ctypes.c_int, _vp, _vp, _vp],
     "sscn_affine_relu": [_vp, _vp, _vp, _i64, _i32, ctypes.c_int, _vp, _vp],
     "sscn_concat_cols": [_vp, _i32, _vp, _i32, _i64, ctypes.c_int, _vp, _vp],
+    "sscn_pool_forward": [_vp, _vp, _i32, ctypes.c_int, ctypes.c_int, _vp, _vp, _vp],
+    "sscn_pool_backward": [_vp, _vp, _vp, _i32, ctypes.c_int, ctypes.c_int, _vp, _vp],
+    "sscn_upsample_forward": [_vp, _vp, _i32, ctypes.c_int, _vp, _vp],
+    "sscn_upsample_backward": [_vp, _vp, _i32, ctypes.c_int, _vp, _vp],
     "sscn_release_cached": [],
     "sscn_last_error": [],
 }
@@ -289,6 +293,72 @@ def sparse_conv_backward(features, weights, dout, rulebook, dgrad=True, wgrad=Tr
                                           ctypes.c_void_p(dw.data_ptr()) if dw is not None else None,
                                           _stream(dout)))
     return dx, dw
+
+
+POOL_MAX, POOL_AVG = 0, 1
+
+
+def _vp_of(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def pool_forward(features, rulebook, mode="max"):
+    """MP / AP over an SC(f, s) rule book: (out, argmax); argmax (uint8, the
+    winning offset per element, 255 for the zero vector) only for "max"."""
+    features = _dev_tensor(features, "features")
+    n, c = features.shape
+    if n != rulebook.n_in:
+        raise ValueError("features do not match the rule book")
+    m = {"max": POOL_MAX, "avg": POOL_AVG}[mode]
+    out = torch.empty((rulebook.n_out, c), dtype=features.dtype, device=features.device)
+    arg = torch.empty((rulebook.n_out, c), dtype=torch.uint8, device=features.device) if m == POOL_MAX else None
+    with torch.cuda.device(features.device):
+        _check(lib().sscn_pool_forward(_vp_of(features), rulebook.handle, c, _dtype_code(features), m,
+                                       _vp_of(out), _vp_of(arg), _stream(features)))
+    return out, arg
+
+
+def pool_backward(dout, rulebook, mode="max", argmax=None):
+    """Gradient of pool_forward with respect to its features."""
+    dout = _dev_tensor(dout, "dout")
+    n, c = dout.shape
+    if n != rulebook.n_out:
+        raise ValueError("dout does not match the rule book")
+    m = {"max": POOL_MAX, "avg": POOL_AVG}[mode]
+    if m == POOL_MAX:
+        argmax = _dev_tensor(argmax, "argmax", torch.uint8)
+        if tuple(argmax.shape) != (n, c):
+            raise ValueError("argmax must match dout")
+    dx = torch.empty((rulebook.n_in, c), dtype=dout.dtype, device=dout.device)
+    with torch.cuda.device(dout.device):
+        _check(lib().sscn_pool_backward(_vp_of(dout), _vp_of(argmax) if m == POOL_MAX else None, rulebook.handle,
+                                        c, _dtype_code(dout), m, _vp_of(dx), _stream(dout)))
+    return dx
+
+
+def upsample_forward(features, rulebook):
+    """Nearest-neighbour upsampling back through an SC(s, s) rule book."""
+    features = _dev_tensor(features, "features")
+    n, c = features.shape
+    if n != rulebook.n_out:
+        raise ValueError("features must live on the rule book's output sites")
+    out = torch.empty((rulebook.n_in, c), dtype=features.dtype, device=features.device)
+    with torch.cuda.device(features.device):
+        _check(lib().sscn_upsample_forward(_vp_of(features), rulebook.handle, c, _dtype_code(features),
+                                           _vp_of(out), _stream(features)))
+    return out
+
+
+def upsample_backward(dout, rulebook):
+    dout = _dev_tensor(dout, "dout")
+    n, c = dout.shape
+    if n != rulebook.n_in:
+        raise ValueError("dout must live on the rule book's input sites")
+    dy = torch.empty((rulebook.n_out, c), dtype=dout.dtype, device=dout.device)
+    with torch.cuda.device(dout.device):
+        _check(lib().sscn_upsample_backward(_vp_of(dout), rulebook.handle, c, _dtype_code(dout), _vp_of(dy),
+                                            _stream(dout)))
+    return dy
 
 
 def affine_relu(x, scale, shift, out=None):
