@@ -448,3 +448,157 @@ def unet_forward(coords, size, X, params, channels, round_to_bf16=True):
         x = unit(f"dec{l}a", x, ssc_rb[l], 2 * channels[l], channels[l])
         x = unit(f"dec{l}b", x, ssc_rb[l], channels[l], channels[l])
     return x
+
+
+# --------------------------------------------------------------------------
+# training (Sec. 4.1: batch normalisation over the active sites, ReLU on
+# them; Sec. 5: pre-activated units, a per-site linear layer and softmax;
+# Sec. 6.2: negative log-likelihood, SGD with Nesterov momentum and L2
+# weight decay)
+# --------------------------------------------------------------------------
+BN_EPS = 1e-5
+BN_MOMENTUM = 0.1
+
+
+def batch_norm_relu_train(X, gamma, beta, eps=BN_EPS):
+    """relu(gamma (x - mean) / sqrt(var + eps) + beta) per channel, with the
+    mean and the (biased) variance taken over the active rows: regular batch
+    normalisation applied to the set of active sites (Sec. 4.1).  Returns
+    (A, mean, var)."""
+    X = np.asarray(X, np.float64)
+    n = X.shape[0]
+    mean = X.sum(axis=0) / n
+    var = ((X - mean) ** 2).sum(axis=0) / n
+    xhat = (X - mean) / np.sqrt(var + eps)
+    return np.maximum(0.0, np.asarray(gamma, np.float64) * xhat + np.asarray(beta, np.float64)), mean, var
+
+
+def batch_norm_relu_backward(dA, X, gamma, beta, mean, var, eps=BN_EPS):
+    """Gradients (dX, dgamma, dbeta) of batch_norm_relu_train at its input X,
+    given dA, the gradient at its output."""
+    X = np.asarray(X, np.float64)
+    gamma = np.asarray(gamma, np.float64)
+    n = X.shape[0]
+    invstd = 1.0 / np.sqrt(var + eps)
+    xhat = (X - mean) * invstd
+    dz = np.where(gamma * xhat + np.asarray(beta, np.float64) > 0.0, np.asarray(dA, np.float64), 0.0)
+    dbeta = dz.sum(axis=0)
+    dgamma = (dz * xhat).sum(axis=0)
+    dX = gamma * invstd / n * (n * dz - dbeta - xhat * dgamma)
+    return dX, dgamma, dbeta
+
+
+def running_stats(running_mean, running_var, mean, var, n, momentum=BN_MOMENTUM):
+    """The inference statistics after one training step: exponential moving
+    averages of the batch mean and the unbiased batch variance."""
+    unbiased = var * n / max(n - 1, 1)
+    return ((1.0 - momentum) * np.asarray(running_mean, np.float64) + momentum * mean,
+            (1.0 - momentum) * np.asarray(running_var, np.float64) + momentum * unbiased)
+
+
+def softmax_nll(logits, labels):
+    """Mean over the active sites of -log softmax(logits)[label], and its
+    gradient with respect to the logits."""
+    z = np.asarray(logits, np.float64)
+    labels = np.asarray(labels, np.int64)
+    n = z.shape[0]
+    m = z.max(axis=1, keepdims=True)
+    e = np.exp(z - m)
+    ssum = e.sum(axis=1, keepdims=True)
+    logp = z - m - np.log(ssum)
+    loss = -logp[np.arange(n), labels].sum() / n
+    d = e / ssum
+    d[np.arange(n), labels] -= 1.0
+    return loss, d / n
+
+
+def sgd_nesterov(p, g, buf, lr, momentum=0.9, weight_decay=1e-4):
+    """One SGD step with Nesterov momentum and L2 weight decay (Sec. 6.2):
+    g' = g + wd p; buf' = momentum buf + g'; p' = p - lr (g' + momentum buf').
+    buf starts at zero.  Returns (p', buf')."""
+    p = np.asarray(p, np.float64)
+    g = np.asarray(g, np.float64) + weight_decay * p
+    buf = momentum * np.asarray(buf, np.float64) + g
+    return p - lr * (g + momentum * buf), buf
+
+
+def unet_train_step(coords, size, X, labels, params, channels, n_classes):
+    """Loss and parameter gradients of one training step of the U-Net of
+    unet_forward, with every unit's batch normalisation in training form
+    (batch statistics of its input over the active sites) and a head on the
+    level-0 output: batch normalisation + ReLU, then a per-site linear layer
+    (an SSC(C_0, n_classes, 1) convolution plus a bias) and softmax, scored
+    by the mean negative log-likelihood of `labels` (one class per input
+    site).  fp64 throughout.
+
+    params(name, k, cin, cout) -> (gamma, beta, W) for every unit, and for
+    name "head" (k = 1, cin = C_0, cout = n_classes) -> (gamma, beta, W, b).
+    Returns (loss, grads, stats): grads[name] = (dgamma, dbeta, dW) and
+    grads["head"] = (dgamma, dbeta, dW, db); stats[name] = (mean, var) of
+    each batch normalisation."""
+    depth = len(channels)
+    ssc_rb, sc_rb = [], []
+    c, sz = np.asarray(coords), tuple(size)
+    for l in range(depth):
+        ssc_rb.append(ssc_rulebook(c, sz, 3))
+        if l + 1 < depth:
+            sc_rb.append(sc_rulebook(c, sz, 2, 2))
+            c, sz = sc_rb[-1].out_coords, sc_rb[-1].out_size
+
+    tape = []                                   # (name, rb, x, a, W, gamma, beta, mean, var)
+    stats = {}
+
+    def unit(name, x, rb, cin, cout):
+        gamma, beta, W = params(name, rb.K, cin, cout)
+        a, mean, var = batch_norm_relu_train(x, gamma, beta)
+        stats[name] = (mean, var)
+        tape.append((name, rb, x, a, W, gamma, beta, mean, var))
+        return forward(a, W, rb)
+
+    x = np.asarray(X, np.float64)
+    skip = []
+    for l in range(depth):
+        x = unit(f"enc{l}a", x, ssc_rb[l], channels[l], channels[l])
+        x = unit(f"enc{l}b", x, ssc_rb[l], channels[l], channels[l])
+        skip.append(x)
+        if l + 1 < depth:
+            x = unit(f"down{l}", x, sc_rb[l], channels[l], channels[l + 1])
+    for l in range(depth - 2, -1, -1):
+        up = unit(f"up{l}", x, transpose(sc_rb[l]), channels[l + 1], channels[l])
+        x = np.concatenate([skip[l], up], axis=1)
+        x = unit(f"dec{l}a", x, ssc_rb[l], 2 * channels[l], channels[l])
+        x = unit(f"dec{l}b", x, ssc_rb[l], channels[l], channels[l])
+    hg, hb, hW, hbias = params("head", 1, channels[0], n_classes)
+    h1 = ssc_rulebook(coords, size, 1)
+    z, hmean, hvar = batch_norm_relu_train(x, hg, hb)
+    stats["head"] = (hmean, hvar)
+    logits = forward(z, hW, h1) + np.asarray(hbias, np.float64)
+    loss, dlogits = softmax_nll(logits, labels)
+
+    grads = {}
+    dz, dhW = backward(z, hW, dlogits, h1)
+    dx, dhg, dhb = batch_norm_relu_backward(dz, x, hg, hb, hmean, hvar)
+    grads["head"] = (dhg, dhb, dhW, dlogits.sum(axis=0))
+
+    def unit_back(dy):
+        name, rb, xin, a, W, gamma, beta, mean, var = tape.pop()
+        da, dW = backward(a, W, dy, rb)
+        dxin, dg, db = batch_norm_relu_backward(da, xin, gamma, beta, mean, var)
+        grads[name] = (dg, db, dW)
+        return name, dxin
+
+    dskip = {}
+    for l in range(depth - 1):
+        _, dx = unit_back(dx)                   # dec{l}b
+        _, dcat = unit_back(dx)                 # dec{l}a
+        C = channels[l]
+        dskip[l] = dcat[:, :C]
+        _, dx = unit_back(dcat[:, C:])          # up{l}: gradient at level l + 1
+    for l in range(depth - 1, -1, -1):
+        if l + 1 < depth:
+            _, dx = unit_back(dx)               # down{l}: into enc{l}b's output ...
+            dx = dx + dskip.pop(l)              # ... which also feeds the concatenation
+        _, dx = unit_back(dx)                   # enc{l}b
+        _, dx = unit_back(dx)                   # enc{l}a
+    assert not tape
+    return loss, grads, stats

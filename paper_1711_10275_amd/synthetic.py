@@ -257,6 +257,23 @@ def layer_params(name, k, cin, cout, seed=SEED_WEIGHT + 3, bf16=True):
     return scale, shift, weights(k, cin, cout, s + 1, bf16=bf16)
 
 
+def train_params(name, k, cin, cout, seed=SEED_WEIGHT + 5, bf16=False):
+    """Parameters of one network layer for training: batch-normalisation
+    gain ~ U(0.5, 1.5) and bias ~ N(0, 0.1) over the input channels, weights
+    W[o][ci][co] ~ N(0, 1/(k cin)); the layer named "head" also gets a bias
+    over its output channels ~ N(0, 0.1)."""
+    scale, shift, w = layer_params(name, k, cin, cout, seed=seed, bf16=bf16)
+    if name != "head":
+        return scale, shift, w
+    s = seed * 1_000_003 + zlib.crc32(name.encode()) + 17
+    return scale, shift, w, np.random.default_rng(s).normal(0.0, 0.1, cout).astype(np.float32)
+
+
+def labels(n, n_classes, seed):
+    """One class per active site, uniform."""
+    return np.random.default_rng(seed).integers(0, n_classes, n).astype(np.int32)
+
+
 def scenes_small(seed=SEED_GEOM + 13, batch=2, L=64, target_per_sample=15_000):
     """The indoor-scene recipe on a small grid (end-to-end network checks)."""
     return scenes_256(seed=seed, batch=batch, L=L, target_per_sample=target_per_sample)

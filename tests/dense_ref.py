@@ -156,3 +156,74 @@ def dense_unet(coords, size, X, params, channels):
         x = ssc(f"dec{l}b", x, l, channels[l], channels[l])
     y = x.numpy()
     return y[coords[:, 0], :, coords[:, 1], coords[:, 2], coords[:, 3]]
+
+
+def dense_unet_train(coords, size, X, labels, params, channels, n_classes, eps=1e-5):
+    """Loss and parameter gradients of the training step of the U-Net, on
+    dense grids with torch autograd in float64.  Batch normalisation uses
+    statistics over the active sites only (the masks); every activation is
+    zeroed outside the active set of its level (the ground state 0); the head
+    is batch normalisation + ReLU, a per-site linear layer with bias and the
+    mean negative log-likelihood over the level-0 sites.  Returns
+    (loss, {name: (dgamma, dbeta, dW[, db])}, {name: (mean, var)})."""
+    coords = np.asarray(coords, np.int64)
+    B = int(coords[:, 0].max()) + 1
+    depth = len(channels)
+    masks = [to_dense(coords, np.ones((coords.shape[0], 1)), size, B)]
+    for _ in range(depth - 1):
+        masks.append((F.conv3d(masks[-1], torch.ones(1, 1, 2, 2, 2, dtype=torch.float64), stride=2) > 0).double())
+    leaves, stats = {}, {}
+
+    def leaf(name, k, cin, cout):
+        p = params(name, k, cin, cout)
+        t = [torch.from_numpy(np.asarray(v, np.float64).copy()).requires_grad_(True) for v in p]
+        leaves[name] = t
+        return t
+
+    def bn_relu(name, x, mask, gamma, beta):
+        n = mask.sum()
+        mean = (x * mask).sum(dim=(0, 2, 3, 4)) / n
+        d = (x - mean.view(1, -1, 1, 1, 1)) * mask
+        var = (d * d).sum(dim=(0, 2, 3, 4)) / n
+        stats[name] = (mean.detach().numpy(), var.detach().numpy())
+        xhat = d / torch.sqrt(var + eps).view(1, -1, 1, 1, 1)
+        return torch.relu(gamma.view(1, -1, 1, 1, 1) * xhat + beta.view(1, -1, 1, 1, 1)) * mask
+
+    def tw(W, f):
+        K, cin, cout = W.shape
+        return W.reshape(f, f, f, cin, cout).permute(4, 3, 0, 1, 2)
+
+    def ssc(name, x, l, cin, cout):
+        g, b, W = leaf(name, 27, cin, cout)
+        return F.conv3d(bn_relu(name, x, masks[l], g, b), tw(W, 3), padding=1) * masks[l]
+
+    def down(name, x, l):
+        g, b, W = leaf(name, 8, channels[l], channels[l + 1])
+        return F.conv3d(bn_relu(name, x, masks[l], g, b), tw(W, 2), stride=2) * masks[l + 1]
+
+    def up(name, x, l):
+        g, b, W = leaf(name, 8, channels[l + 1], channels[l])
+        w = W.reshape(2, 2, 2, channels[l + 1], channels[l]).permute(3, 4, 0, 1, 2)
+        return F.conv_transpose3d(bn_relu(name, x, masks[l + 1], g, b), w, stride=2) * masks[l]
+
+    x = to_dense(coords, X, size, B)
+    skip = []
+    for l in range(depth):
+        x = ssc(f"enc{l}a", x, l, channels[l], channels[l])
+        x = ssc(f"enc{l}b", x, l, channels[l], channels[l])
+        skip.append(x)
+        if l + 1 < depth:
+            x = down(f"down{l}", x, l)
+    for l in range(depth - 2, -1, -1):
+        u = up(f"up{l}", x, l)
+        x = torch.cat([skip[l], u], dim=1)
+        x = ssc(f"dec{l}a", x, l, 2 * channels[l], channels[l])
+        x = ssc(f"dec{l}b", x, l, channels[l], channels[l])
+    hg, hb, hW, hbias = leaf("head", 1, channels[0], n_classes)
+    z = bn_relu("head", x, masks[0], hg, hb)
+    zs = z[coords[:, 0], :, coords[:, 1], coords[:, 2], coords[:, 3]]      # active sites, input row order
+    logits = zs @ hW[0] + hbias
+    loss = F.cross_entropy(logits, torch.from_numpy(np.asarray(labels, np.int64)))
+    loss.backward()
+    grads = {k: tuple(t.grad.numpy().copy() for t in v) for k, v in leaves.items()}
+    return float(loss.detach()), grads, stats

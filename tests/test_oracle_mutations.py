@@ -215,3 +215,85 @@ def test_upsample_wrong_parent_caught(monkeypatch):
         return out
     monkeypatch.setattr(O, "upsample_nearest", bad)
     assert not _pool_pins_hold()
+
+
+# --------------------------------------------------------------------------
+# training step
+# --------------------------------------------------------------------------
+def _train_pins_hold():
+    from tests import test_oracle_train as T
+    try:
+        T.test_batch_norm_relu_is_torch_training_batch_norm()
+        T.test_softmax_nll_is_cross_entropy()
+        T.test_sgd_nesterov_is_torch_sgd()
+        T.test_unet_train_step_matches_dense_autograd((3, 5))
+    except AssertionError:
+        return False
+    return True
+
+
+def test_train_pins_hold_unmutated():
+    assert _train_pins_hold()
+
+
+def test_bn_unbiased_variance_caught(monkeypatch):
+    def bad(X, gamma, beta, eps=O.BN_EPS):
+        X = np.asarray(X, np.float64)
+        n = X.shape[0]
+        mean = X.mean(axis=0)
+        var = ((X - mean) ** 2).sum(axis=0) / (n - 1)
+        return np.maximum(0.0, gamma * (X - mean) / np.sqrt(var + eps) + beta), mean, var
+    monkeypatch.setattr(O, "batch_norm_relu_train", bad)
+    assert not _train_pins_hold()
+
+
+def test_bn_backward_without_relu_mask_caught(monkeypatch):
+    orig = O.batch_norm_relu_backward
+
+    def bad(dA, X, gamma, beta, mean, var, eps=O.BN_EPS):
+        big = np.full_like(np.asarray(beta, np.float64), 1e6)   # every unit "active"
+        return orig(dA, X, gamma, big, mean, var, eps)
+    monkeypatch.setattr(O, "batch_norm_relu_backward", bad)
+    assert not _train_pins_hold()
+
+
+def test_bn_backward_missing_mean_term_caught(monkeypatch):
+    orig = O.batch_norm_relu_backward
+
+    def bad(dA, X, gamma, beta, mean, var, eps=O.BN_EPS):
+        dX, dg, db = orig(dA, X, gamma, beta, mean, var, eps)
+        n = np.asarray(X).shape[0]
+        return dX + np.asarray(gamma) / np.sqrt(var + eps) / n * db, dg, db
+    monkeypatch.setattr(O, "batch_norm_relu_backward", bad)
+    assert not _train_pins_hold()
+
+
+def test_plain_momentum_caught(monkeypatch):
+    def bad(p, g, buf, lr, momentum=0.9, weight_decay=1e-4):
+        g = np.asarray(g) + weight_decay * np.asarray(p)
+        buf = momentum * np.asarray(buf) + g
+        return np.asarray(p) - lr * buf, buf
+    monkeypatch.setattr(O, "sgd_nesterov", bad)
+    assert not _train_pins_hold()
+
+
+def test_missing_weight_decay_caught(monkeypatch):
+    orig = O.sgd_nesterov
+    monkeypatch.setattr(O, "sgd_nesterov", lambda p, g, buf, lr, momentum=0.9, weight_decay=1e-4:
+                        orig(p, g, buf, lr, momentum, 0.0))
+    assert not _train_pins_hold()
+
+
+def test_dropped_skip_gradient_caught(monkeypatch):
+    orig = O.backward
+    calls = {"n": 0}
+
+    def bad(X, W, dY, rb):
+        # the SC (down) layers' input gradients are lost, as if the skip
+        # were the only consumer of each encoder output
+        dX, dW = orig(X, W, dY, rb)
+        if not rb.submanifold and rb.n_out < rb.n_in:
+            dX = np.zeros_like(dX)
+        return dX, dW
+    monkeypatch.setattr(O, "backward", bad)
+    assert not _train_pins_hold()
