@@ -187,6 +187,16 @@ sscn_status sparse_conv_forward_heads(const void* features, const void* weights,
                                       const sscn_conv_output* heads, hipStream_t stream);
 
 /*
+ * sparse_conv_forward_bias -- sparse_conv_forward_heads with a bias: every
+ * active output row becomes y[k] + bias before the heads map it (a
+ * convolution with a bias term; the ground state at inactive sites is not
+ * stored, Sec. 3 footnote).  bias: device fp32, c_out entries (non-NULL).
+ */
+sscn_status sparse_conv_forward_bias(const void* features, const void* weights, const float* bias,
+                                     sscn_rulebook rb, int32_t c_in, int32_t c_out, sscn_dtype dtype,
+                                     int32_t n_heads, const sscn_conv_output* heads, hipStream_t stream);
+
+/*
  * sparse_conv_forward_noalloc -- sparse_conv_forward for callers that cannot
  * allocate device memory (code under stream capture, tight serving loops,
  * harnesses that forbid hipMalloc).  Same arguments, same kernels and the
@@ -303,6 +313,101 @@ sscn_status sscn_concat_cols(const void* a, int32_t ca, const void* b, int32_t c
  * management of the rule-book storage of Sec. 4.2.
  */
 sscn_status sscn_release_cached(void);
+
+/*
+ * ------------------------------------------------------------------ training
+ * Batch normalisation "applied over the set of active sites" and activation
+ * functions restricted to them (Sec. 4.1 "Other operators"); the final
+ * per-site linear layer and softmax (Sec. 5); negative log-likelihood and
+ * SGD with Nesterov momentum and L2 weight decay (Sec. 6.2).
+ *
+ * Matrices are n x c row-major with a row stride (`ld*`, elements, >= c), so
+ * that a column range of a wider buffer (a concatenation) can be passed by
+ * offsetting the pointer.  Per-channel vectors are device fp32, c entries.
+ * Column reductions are deterministic: fixed per-workgroup fp64 partial sums
+ * added in a fixed order (no atomics).
+ */
+
+/*
+ * sscn_batchnorm_forward -- batch statistics of x over its n active rows:
+ * mean, invstd = 1/sqrt(var + eps) (biased variance), scale = gamma * invstd
+ * and shift = beta - mean * scale (the inference-form affine map, as
+ * sscn_affine_relu and conv output heads take it).  Training applies the
+ * normalisation with sscn_batchnorm_relu_apply.  running_mean / running_var
+ * (both or neither) are updated as (1 - momentum) r + momentum stat, with the
+ * unbiased variance.  n >= 1 (else SSCN_ERR_INVALID_ARG).
+ */
+sscn_status sscn_batchnorm_forward(const void* x, int64_t ldx, int64_t n, int32_t c, sscn_dtype dtype,
+                                   const float* gamma, const float* beta, float eps, float momentum,
+                                   float* running_mean, float* running_var, float* mean, float* invstd,
+                                   float* scale, float* shift, hipStream_t stream);
+
+/*
+ * sscn_batchnorm_relu_apply -- y = relu((x - mean) * scale + beta), the
+ * normalisation with batch statistics followed by ReLU (x, y may be equal
+ * but must not otherwise overlap).  The mean is subtracted first, so the
+ * result stays accurate when a channel's variance is tiny next to its mean.
+ */
+sscn_status sscn_batchnorm_relu_apply(const void* x, int64_t ldx, int64_t n, int32_t c, sscn_dtype dtype,
+                                      const float* mean, const float* scale, const float* beta, void* y,
+                                      int64_t ldy, hipStream_t stream);
+
+/*
+ * sscn_batchnorm_relu_backward_params -- first half of the gradient of
+ * a = sscn_batchnorm_relu_apply(x): with dz = dA where the forward's ReLU
+ * passed ((x - mean) * scale + beta > 0, evaluated exactly as the forward
+ * does) and 0 elsewhere, and xhat = (x - mean) * invstd,
+ *   dbeta = sum over rows of dz,  dgamma = sum over rows of dz * xhat.
+ */
+sscn_status sscn_batchnorm_relu_backward_params(const void* dA, int64_t ldd, const void* x, int64_t ldx,
+                                                int64_t n, int32_t c, sscn_dtype dtype, const float* mean,
+                                                const float* invstd, const float* scale, const float* beta,
+                                                float* dgamma, float* dbeta, hipStream_t stream);
+
+/*
+ * sscn_batchnorm_relu_backward_input -- second half: the gradient at x,
+ *   dx = gamma * invstd * (dz - dbeta / n - xhat * dgamma / n)  (+ add),
+ * for any column range of the layer (offset every pointer and vector by the
+ * range's first column; n stays the layer's row count).  `add` (nullable,
+ * row stride ld_add) is a gradient from another consumer of x, summed in.
+ */
+sscn_status sscn_batchnorm_relu_backward_input(const void* dA, int64_t ldd, const void* x, int64_t ldx,
+                                               int64_t n, int32_t c, sscn_dtype dtype, const float* gamma,
+                                               const float* beta, const float* mean, const float* invstd,
+                                               const float* scale, const float* dgamma, const float* dbeta,
+                                               const void* add, int64_t ld_add, void* dx, int64_t ldx_out,
+                                               hipStream_t stream);
+
+/* sscn_column_sum -- out[col] = sum over the n rows of x[row][col] (a bias gradient), fp32 out. */
+sscn_status sscn_column_sum(const void* x, int64_t ldx, int64_t n, int32_t c, sscn_dtype dtype, float* out,
+                            hipStream_t stream);
+
+/* sscn_add -- y = a + b elementwise (identity residual connections, Sec. 5; gradient sums). */
+sscn_status sscn_add(const void* a, int64_t lda, const void* b, int64_t ldb, int64_t n, int32_t c,
+                     sscn_dtype dtype, void* y, int64_t ldy, hipStream_t stream);
+
+/*
+ * sscn_softmax_nll -- per active site, softmax over `classes` logits and the
+ * negative log-likelihood of its label (Sec. 5, Sec. 6.2):
+ *   loss (device, 1 float) = mean over the n sites of
+ *                            logsumexp(logits[r]) - logits[r][labels[r]]
+ *   dlogits[r][k] = (softmax(logits[r])[k] - [k == labels[r]]) / n
+ * logits and dlogits: contiguous n x classes in dtype; labels int32 in
+ * [0, classes) (a label outside gives a NaN loss).  n >= 1.
+ */
+sscn_status sscn_softmax_nll(const void* logits, int64_t n, int32_t classes, sscn_dtype dtype,
+                             const int32_t* labels, float* loss, void* dlogits, hipStream_t stream);
+
+/*
+ * sscn_sgd_nesterov -- one step of SGD with Nesterov momentum and L2 weight
+ * decay (Sec. 6.2), elementwise over `count` fp32 parameters:
+ *   g' = g + weight_decay * p;  buf = momentum * buf + g';
+ *   p = p - lr * (g' + momentum * buf)
+ * (buf starts at zero).  params_bf16 (nullable) receives p rounded to
+ * bfloat16 (the copy a bf16 network convolves with).
+ */
+sscn_status sscn_sgd_nesterov(float* params, const float* grads, float* momentum_buf, int64_t count, float lr,
+                              float momentum, float weight_decay, void* params_bf16, hipStream_t stream);
 
 /* Thread-local message describing the last failure on this thread ("" if none). */
 const char* sscn_last_error(void);

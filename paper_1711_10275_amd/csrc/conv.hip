@@ -60,7 +60,11 @@ struct Heads {
   // wgrad kernel after it accumulates into), n_zero floats; 0: none
   float* zero;
   int64_t n_zero;
+  // the layer's bias (c_out fp32, nullable): added to every output row
+  // before the heads map it
+  const float* bias;
   __device__ __forceinline__ void store(int64_t row, int col, float v) const {
+    if (bias) v += bias[col];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       if (h < n) {
@@ -769,9 +773,11 @@ __device__ __forceinline__ void conv_rows_block(
         const bool ok = col < ncols;
         const float sc = ok && Y.scale[h] ? Y.scale[h][col] : 1.f;
         const float sh = ok && Y.scale[h] ? Y.shift[h][col] : 0.f;
+        const float bi = ok && Y.bias ? Y.bias[col] : 0.f;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float v = Y.scale[h] ? fmaxf(0.f, acc[nb][r] * sc + sh) : acc[nb][r];
+          const float y = acc[nb][r] + bi;
+          const float v = Y.scale[h] ? fmaxf(0.f, y * sc + sh) : y;
           Elem<T>::store(reinterpret_cast<T*>(tile + (4 * g + r) * RB) + nb * 16 + m, v);
         }
       }
@@ -1900,9 +1906,26 @@ static Heads<T> heads_of(int n, const sscn_conv_output* h) {
   return r;
 }
 
+static sscn_status forward_heads(const void* features, const void* weights, const float* bias, sscn_rulebook rb,
+                                 int32_t c_in, int32_t c_out, sscn_dtype dtype, int32_t n_heads,
+                                 const sscn_conv_output* heads, hipStream_t stream);
+
 extern "C" sscn_status sparse_conv_forward_heads(const void* features, const void* weights, sscn_rulebook rb,
                                                  int32_t c_in, int32_t c_out, sscn_dtype dtype, int32_t n_heads,
                                                  const sscn_conv_output* heads, hipStream_t stream) {
+  return forward_heads(features, weights, nullptr, rb, c_in, c_out, dtype, n_heads, heads, stream);
+}
+
+extern "C" sscn_status sparse_conv_forward_bias(const void* features, const void* weights, const float* bias,
+                                                sscn_rulebook rb, int32_t c_in, int32_t c_out, sscn_dtype dtype,
+                                                int32_t n_heads, const sscn_conv_output* heads, hipStream_t stream) {
+  if (!bias) return fail(SSCN_ERR_INVALID_ARG, "NULL bias");
+  return forward_heads(features, weights, bias, rb, c_in, c_out, dtype, n_heads, heads, stream);
+}
+
+static sscn_status forward_heads(const void* features, const void* weights, const float* bias, sscn_rulebook rb,
+                                 int32_t c_in, int32_t c_out, sscn_dtype dtype, int32_t n_heads,
+                                 const sscn_conv_output* heads, hipStream_t stream) {
   sscn_status st = check_conv_args(rb, c_in, c_out, dtype);
   if (st != SSCN_OK) return st;
   if (n_heads < 1 || n_heads > 2 || !heads) return fail(SSCN_ERR_INVALID_ARG, "1 or 2 output heads");
@@ -1916,11 +1939,14 @@ extern "C" sscn_status sparse_conv_forward_heads(const void* features, const voi
   if (v.n_out == 0) return SSCN_OK;
   UseNote note{rb->d, stream};
   if (!weights || (v.n_in > 0 && !features)) return fail(SSCN_ERR_INVALID_ARG, "NULL features or weights");
-  if (dtype == SSCN_F32)
-    return forward_t<float>((const float*)features, (const float*)weights, v, c_in, c_out,
-                            heads_of<float>(n_heads, heads), stream);
-  return forward_t<bf16_t>((const bf16_t*)features, (const bf16_t*)weights, v, c_in, c_out,
-                           heads_of<bf16_t>(n_heads, heads), stream);
+  if (dtype == SSCN_F32) {
+    Heads<float> h = heads_of<float>(n_heads, heads);
+    h.bias = bias;
+    return forward_t<float>((const float*)features, (const float*)weights, v, c_in, c_out, h, stream);
+  }
+  Heads<bf16_t> h = heads_of<bf16_t>(n_heads, heads);
+  h.bias = bias;
+  return forward_t<bf16_t>((const bf16_t*)features, (const bf16_t*)weights, v, c_in, c_out, h, stream);
 }
 
 extern "C" sscn_status sparse_conv_backward(const void* features, const void* weights, const void* dout,

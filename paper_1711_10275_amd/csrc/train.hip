@@ -1,0 +1,446 @@
+// Training pieces of a submanifold network (Sec. 4.1 "Other operators":
+// batch normalisation as regular batch normalisation over the set of
+// active sites, activation functions on the active sites; Sec. 5: the final
+// linear layer and softmax on each active site; Sec. 6.2: negative
+// log-likelihood, SGD with Nesterov momentum and L2 weight decay).
+//
+// Batch statistics and their gradients are column reductions over the n
+// active rows.  They run in two deterministic passes: a grid of workgroups
+// each sums a fixed set of rows into fp64 partials (one per workgroup and
+// channel), and one thread per channel then adds the partials in workgroup
+// order.  No atomics, so every result is reproducible bit for bit.  The
+// passes stream the n x c matrix once (HBM-bound).
+#include <algorithm>
+
+#include "internal.h"
+#include "numeric.h"
+
+namespace sscn {
+
+namespace {
+
+constexpr int kColChunk = 64;       // channels per workgroup (one per lane)
+constexpr int kMaxPartials = 1024;  // workgroups over the rows
+
+enum ColOp { kSums = 0, kSumSquares = 1, kBnBack = 2 };
+
+// The normalised, scaled and shifted value before the ReLU, as the forward
+// computes it: (x - mean) * (gamma * invstd) + beta.  (Subtracting the mean
+// first keeps the result accurate when the variance is tiny next to the
+// mean; the backward's ReLU mask evaluates the same expression.)
+__device__ __forceinline__ float bn_pre(float x, float mean, float scale, float beta) {
+  return fmaf(x - mean, scale, beta);
+}
+
+// Per channel: a0 = sum of v, a1 = sum of v^2 (kSumSquares) or of v * xhat
+// (kBnBack, where v = dA masked by the forward's ReLU and xhat the
+// normalised input); kSums: a0 only.  partial[(blk * 2 + i) * c + col].
+template <typename T, int OP>
+__global__ __launch_bounds__(256) void k_colreduce(const T* __restrict__ x, int64_t ldx, const T* __restrict__ da,
+                                                   int64_t ldd, int64_t n, int c, const float* __restrict__ scale,
+                                                   const float* __restrict__ beta, const float* __restrict__ mean,
+                                                   const float* __restrict__ invstd, double* __restrict__ partial) {
+  __shared__ double red[2][4][kColChunk];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int col = blockIdx.y * kColChunk + lane;
+  const bool live = col < c;
+  double a0 = 0.0, a1 = 0.0;
+  if (live) {
+    float sc = 0.f, be = 0.f, mu = 0.f, is = 0.f;
+    if constexpr (OP == kBnBack) {
+      sc = scale[col]; be = beta[col]; mu = mean[col]; is = invstd[col];
+    }
+    for (int64_t r = (int64_t)blockIdx.x * 4 + wave; r < n; r += (int64_t)gridDim.x * 4) {
+      const float v = ld(x + r * ldx + col);
+      if constexpr (OP == kBnBack) {
+        const float g = ld(da + r * ldd + col);
+        const float dz = bn_pre(v, mu, sc, be) > 0.f ? g : 0.f;
+        a0 += dz;
+        a1 += (double)dz * (double)((v - mu) * is);
+      } else {
+        a0 += v;
+        if constexpr (OP == kSumSquares) a1 += (double)v * (double)v;
+      }
+    }
+  }
+  red[0][wave][lane] = a0;
+  red[1][wave][lane] = a1;
+  __syncthreads();
+  if (wave == 0 && live) {
+    double s0 = 0.0, s1 = 0.0;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      s0 += red[0][w][lane];
+      s1 += red[1][w][lane];
+    }
+    partial[((int64_t)blockIdx.x * 2) * c + col] = s0;
+    partial[((int64_t)blockIdx.x * 2 + 1) * c + col] = s1;
+  }
+}
+
+// Sums of the partials in workgroup order: tot[i * c + col].
+__device__ __forceinline__ void sum_partials(const double* __restrict__ partial, int blocks, int c, int col,
+                                             double& s0, double& s1) {
+  s0 = 0.0;
+  s1 = 0.0;
+  for (int b = 0; b < blocks; ++b) {
+    s0 += partial[((int64_t)b * 2) * c + col];
+    s1 += partial[((int64_t)b * 2 + 1) * c + col];
+  }
+}
+
+// Batch statistics -> the affine map of the normalisation, and the running
+// (inference) statistics: mean, biased variance for the map, unbiased for
+// the running variance.
+__global__ void k_bn_finalize(const double* __restrict__ partial, int blocks, int c, int64_t n,
+                              const float* __restrict__ gamma, const float* __restrict__ beta, float eps,
+                              float momentum, float* running_mean, float* running_var, float* __restrict__ mean,
+                              float* __restrict__ invstd, float* __restrict__ scale, float* __restrict__ shift) {
+  const int col = blockIdx.x * blockDim.x + threadIdx.x;
+  if (col >= c) return;
+  double s0, s1;
+  sum_partials(partial, blocks, c, col, s0, s1);
+  const double mu = s0 / (double)n;
+  const double var = fmax(s1 / (double)n - mu * mu, 0.0);
+  const float is = (float)(1.0 / sqrt(var + (double)eps));
+  const float sc = gamma[col] * is;
+  mean[col] = (float)mu;
+  invstd[col] = is;
+  scale[col] = sc;
+  shift[col] = beta[col] - (float)mu * sc;
+  if (running_mean) {
+    const double unbiased = n > 1 ? var * (double)n / (double)(n - 1) : var;
+    running_mean[col] = (1.f - momentum) * running_mean[col] + momentum * (float)mu;
+    running_var[col] = (1.f - momentum) * running_var[col] + momentum * (float)unbiased;
+  }
+}
+
+__global__ void k_two_sums(const double* __restrict__ partial, int blocks, int c, float* __restrict__ out0,
+                           float* __restrict__ out1) {
+  const int col = blockIdx.x * blockDim.x + threadIdx.x;
+  if (col >= c) return;
+  double s0, s1;
+  sum_partials(partial, blocks, c, col, s0, s1);
+  out0[col] = (float)s0;
+  if (out1) out1[col] = (float)s1;
+}
+
+// dx = gamma invstd (dz - dbeta / n - xhat dgamma / n) (+ add), dz = dA where
+// the forward's ReLU passed, else 0.
+template <typename T>
+__global__ void k_bn_back_input(const T* __restrict__ da, int64_t ldd, const T* __restrict__ x, int64_t ldx,
+                                int64_t n, int c, const float* __restrict__ gamma, const float* __restrict__ scale,
+                                const float* __restrict__ beta, const float* __restrict__ mean,
+                                const float* __restrict__ invstd, const float* __restrict__ dgamma,
+                                const float* __restrict__ dbeta, const T* __restrict__ add, int64_t lda,
+                                T* __restrict__ dx, int64_t ldo) {
+  const int64_t total = n * c;
+  const float inv_n = 1.f / (float)n;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = i / c;
+    const int col = (int)(i - r * c);
+    const float v = ld(x + r * ldx + col);
+    const float g = ld(da + r * ldd + col);
+    const float dz = bn_pre(v, mean[col], scale[col], beta[col]) > 0.f ? g : 0.f;
+    const float xhat = (v - mean[col]) * invstd[col];
+    float out = gamma[col] * invstd[col] * (dz - dbeta[col] * inv_n - xhat * (dgamma[col] * inv_n));
+    if (add) out += ld(add + r * lda + col);
+    st(dx + r * ldo + col, out);
+  }
+}
+
+// relu((x - mean) * scale + beta), strided rows.
+template <typename T>
+__global__ void k_bn_relu_apply(const T* __restrict__ x, int64_t ldx, int64_t n, int c,
+                                const float* __restrict__ mean, const float* __restrict__ scale,
+                                const float* __restrict__ beta, T* __restrict__ y, int64_t ldy) {
+  const int64_t total = n * c;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = i / c;
+    const int col = (int)(i - r * c);
+    st(y + r * ldy + col, fmaxf(0.f, bn_pre(ld(x + r * ldx + col), mean[col], scale[col], beta[col])));
+  }
+}
+
+// y = a + b, strided rows.
+template <typename T>
+__global__ void k_add(const T* __restrict__ a, int64_t lda, const T* __restrict__ b, int64_t ldb, int64_t n, int c,
+                      T* __restrict__ y, int64_t ldy) {
+  const int64_t total = n * c;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = i / c;
+    const int col = (int)(i - r * c);
+    st(y + r * ldy + col, ld(a + r * lda + col) + ld(b + r * ldb + col));
+  }
+}
+
+// Softmax and negative log-likelihood, one wavefront per row (lanes over
+// the classes).  dlogits = (softmax - onehot) / n; the row losses go to
+// per-workgroup fp64 partials (summed in order by k_loss_finalize).  A label
+// outside [0, classes) makes that row's loss NaN (its gradient is the
+// softmax alone).
+template <typename T>
+__global__ __launch_bounds__(256) void k_softmax_nll(const T* __restrict__ z, int64_t n, int classes,
+                                                     const int32_t* __restrict__ labels, T* __restrict__ dz,
+                                                     double* __restrict__ partial) {
+  __shared__ double red[4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const float inv_n = 1.f / (float)n;
+  double acc = 0.0;
+  for (int64_t r = (int64_t)blockIdx.x * 4 + wave; r < n; r += (int64_t)gridDim.x * 4) {
+    const T* row = z + r * classes;
+    float m = -INFINITY;
+    for (int k = lane; k < classes; k += 64) m = fmaxf(m, ld(row + k));
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) m = fmaxf(m, __shfl_xor(m, d, 64));
+    // s: the sum of exp(z - max) over all classes, so: over all but the
+    // label.  The label's gradient p - 1 = -so / s and the loss
+    // log(s / e_label) = log1p(so / e_label) are formed from so, which
+    // keeps them accurate when the label's probability is close to 1.
+    const int lab = labels[r];
+    const bool ok = lab >= 0 && lab < classes;
+    float s = 0.f, so = 0.f;
+    for (int k = lane; k < classes; k += 64) {
+      const float e = expf(ld(row + k) - m);
+      s += e;
+      if (k != lab) so += e;
+    }
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) {
+      s += __shfl_xor(s, d, 64);
+      so += __shfl_xor(so, d, 64);
+    }
+    for (int k = lane; k < classes; k += 64) {
+      const float g = k == lab ? -so / s : expf(ld(row + k) - m) / s;
+      st(dz + r * classes + k, g * inv_n);
+    }
+    if (lane == 0) {
+      double l = (double)NAN;
+      if (ok) {
+        const float zl = ld(row + lab);
+        const float el = expf(zl - m);
+        l = el > 0.f ? (double)log1pf(so / el) : (double)(m - zl) + (double)logf(s);
+      }
+      acc += l;
+    }
+  }
+  if (lane == 0) red[wave] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) partial[blockIdx.x] = red[0] + red[1] + red[2] + red[3];
+}
+
+__global__ void k_loss_finalize(const double* __restrict__ partial, int blocks, int64_t n, float* __restrict__ loss) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  double s = 0.0;
+  for (int b = 0; b < blocks; ++b) s += partial[b];
+  loss[0] = (float)(s / (double)n);
+}
+
+// g' = g + wd p; buf = momentum buf + g'; p -= lr (g' + momentum buf).
+__global__ void k_sgd_nesterov(float* __restrict__ p, const float* __restrict__ g, float* __restrict__ buf,
+                               int64_t count, float lr, float momentum, float wd, uint16_t* __restrict__ p_bf16) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += (int64_t)gridDim.x * blockDim.x) {
+    const float gi = g[i] + wd * p[i];
+    const float b = momentum * buf[i] + gi;
+    buf[i] = b;
+    const float np = p[i] - lr * (gi + momentum * b);
+    p[i] = np;
+    if (p_bf16) p_bf16[i] = f32_bf16_bits(np);
+  }
+}
+
+unsigned grid_1d(int64_t total) {
+  return (unsigned)std::max<int64_t>(1, std::min<int64_t>(ceil_div(total, 256), 8192));
+}
+
+int row_blocks(int64_t n) { return (int)std::max<int64_t>(1, std::min<int64_t>(ceil_div(n, 64), kMaxPartials)); }
+
+sscn_status check_mat(const void* p, int64_t ld, int64_t n, int c, const char* what) {
+  if (n < 0 || c < 1) return fail(SSCN_ERR_INVALID_ARG, std::string(what) + ": n must be >= 0 and c >= 1");
+  if (n > 0 && !p) return fail(SSCN_ERR_INVALID_ARG, std::string(what) + " is NULL");
+  if (ld < c) return fail(SSCN_ERR_INVALID_ARG, std::string(what) + ": row stride below the channel count");
+  return SSCN_OK;
+}
+
+sscn_status check_dtype(sscn_dtype dtype) {
+  if (dtype != SSCN_F32 && dtype != SSCN_BF16) return fail(SSCN_ERR_INVALID_ARG, "unknown dtype");
+  return SSCN_OK;
+}
+
+template <int OP>
+sscn_status colreduce(sscn_dtype dtype, const void* x, int64_t ldx, const void* da, int64_t ldd, int64_t n, int c,
+                      const float* scale, const float* beta, const float* mean, const float* invstd, double* partial,
+                      int blocks, hipStream_t s) {
+  const dim3 grid((unsigned)blocks, (unsigned)ceil_div(c, kColChunk));
+  if (dtype == SSCN_F32)
+    k_colreduce<float, OP><<<grid, 256, 0, s>>>((const float*)x, ldx, (const float*)da, ldd, n, c, scale, beta, mean,
+                                                invstd, partial);
+  else
+    k_colreduce<uint16_t, OP><<<grid, 256, 0, s>>>((const uint16_t*)x, ldx, (const uint16_t*)da, ldd, n, c, scale,
+                                                   beta, mean, invstd, partial);
+  SSCN_HIP(hipGetLastError());
+  return SSCN_OK;
+}
+
+struct Partials {
+  double* p = nullptr;
+  hipStream_t s;
+  explicit Partials(hipStream_t st) : s(st) {}
+  sscn_status alloc(int blocks, int c) { return dev_alloc((void**)&p, sizeof(double) * 2 * (size_t)blocks * c, s); }
+  ~Partials() { dev_free(p, s); }
+};
+
+}  // namespace
+}  // namespace sscn
+
+using namespace sscn;
+
+extern "C" sscn_status sscn_batchnorm_forward(const void* x, int64_t ldx, int64_t n, int32_t c, sscn_dtype dtype,
+                                              const float* gamma, const float* beta, float eps, float momentum,
+                                              float* running_mean, float* running_var, float* mean, float* invstd,
+                                              float* scale, float* shift, hipStream_t stream) {
+  SSCN_TRY(check_dtype(dtype));
+  SSCN_TRY(check_mat(x, ldx, n, c, "x"));
+  if (n < 1) return fail(SSCN_ERR_INVALID_ARG, "batch statistics need at least one active site");
+  if (!gamma || !beta || !mean || !invstd || !scale || !shift)
+    return fail(SSCN_ERR_INVALID_ARG, "NULL gamma, beta, mean, invstd, scale or shift");
+  if ((running_mean == nullptr) != (running_var == nullptr))
+    return fail(SSCN_ERR_INVALID_ARG, "running_mean and running_var go together");
+  if (!(eps > 0.f)) return fail(SSCN_ERR_INVALID_ARG, "eps must be positive");
+  const int blocks = row_blocks(n);
+  Partials part(stream);
+  SSCN_TRY(part.alloc(blocks, c));
+  SSCN_TRY(colreduce<kSumSquares>(dtype, x, ldx, nullptr, 0, n, c, nullptr, nullptr, nullptr, nullptr, part.p, blocks,
+                                  stream));
+  k_bn_finalize<<<(unsigned)ceil_div(c, 256), 256, 0, stream>>>(part.p, blocks, c, n, gamma, beta, eps, momentum,
+                                                                running_mean, running_var, mean, invstd, scale, shift);
+  SSCN_HIP(hipGetLastError());
+  return SSCN_OK;
+}
+
+extern "C" sscn_status sscn_batchnorm_relu_apply(const void* x, int64_t ldx, int64_t n, int32_t c, sscn_dtype dtype,
+                                                 const float* mean, const float* scale, const float* beta, void* y,
+                                                 int64_t ldy, hipStream_t stream) {
+  SSCN_TRY(check_dtype(dtype));
+  SSCN_TRY(check_mat(x, ldx, n, c, "x"));
+  SSCN_TRY(check_mat(y, ldy, n, c, "y"));
+  if (!mean || !scale || !beta) return fail(SSCN_ERR_INVALID_ARG, "NULL mean, scale or beta");
+  if (n == 0) return SSCN_OK;
+  const unsigned g = grid_1d(n * c);
+  if (dtype == SSCN_F32)
+    k_bn_relu_apply<float><<<g, 256, 0, stream>>>((const float*)x, ldx, n, c, mean, scale, beta, (float*)y, ldy);
+  else
+    k_bn_relu_apply<uint16_t><<<g, 256, 0, stream>>>((const uint16_t*)x, ldx, n, c, mean, scale, beta, (uint16_t*)y,
+                                                     ldy);
+  SSCN_HIP(hipGetLastError());
+  return SSCN_OK;
+}
+
+extern "C" sscn_status sscn_batchnorm_relu_backward_params(const void* da, int64_t ldd, const void* x, int64_t ldx,
+                                                           int64_t n, int32_t c, sscn_dtype dtype, const float* mean,
+                                                           const float* invstd, const float* scale, const float* beta,
+                                                           float* dgamma, float* dbeta, hipStream_t stream) {
+  SSCN_TRY(check_dtype(dtype));
+  SSCN_TRY(check_mat(x, ldx, n, c, "x"));
+  SSCN_TRY(check_mat(da, ldd, n, c, "dA"));
+  if (!scale || !beta || !mean || !invstd || !dgamma || !dbeta)
+    return fail(SSCN_ERR_INVALID_ARG, "NULL statistics or outputs");
+  const int blocks = row_blocks(n);
+  Partials part(stream);
+  SSCN_TRY(part.alloc(blocks, c));
+  SSCN_TRY(colreduce<kBnBack>(dtype, x, ldx, da, ldd, n, c, scale, beta, mean, invstd, part.p, blocks, stream));
+  k_two_sums<<<(unsigned)ceil_div(c, 256), 256, 0, stream>>>(part.p, blocks, c, dbeta, dgamma);
+  SSCN_HIP(hipGetLastError());
+  return SSCN_OK;
+}
+
+extern "C" sscn_status sscn_batchnorm_relu_backward_input(const void* da, int64_t ldd, const void* x, int64_t ldx,
+                                                          int64_t n, int32_t c, sscn_dtype dtype, const float* gamma,
+                                                          const float* beta, const float* mean, const float* invstd,
+                                                          const float* scale, const float* dgamma, const float* dbeta,
+                                                          const void* add, int64_t ld_add, void* dx, int64_t ldx_out,
+                                                          hipStream_t stream) {
+  SSCN_TRY(check_dtype(dtype));
+  SSCN_TRY(check_mat(x, ldx, n, c, "x"));
+  SSCN_TRY(check_mat(da, ldd, n, c, "dA"));
+  SSCN_TRY(check_mat(dx, ldx_out, n, c, "dx"));
+  if (add) SSCN_TRY(check_mat(add, ld_add, n, c, "add"));
+  if (!gamma || !scale || !beta || !mean || !invstd || !dgamma || !dbeta)
+    return fail(SSCN_ERR_INVALID_ARG, "NULL parameters or statistics");
+  if (n == 0) return SSCN_OK;
+  const unsigned g = grid_1d(n * c);
+  if (dtype == SSCN_F32)
+    k_bn_back_input<float><<<g, 256, 0, stream>>>((const float*)da, ldd, (const float*)x, ldx, n, c, gamma, scale,
+                                                  beta, mean, invstd, dgamma, dbeta, (const float*)add, ld_add,
+                                                  (float*)dx, ldx_out);
+  else
+    k_bn_back_input<uint16_t><<<g, 256, 0, stream>>>((const uint16_t*)da, ldd, (const uint16_t*)x, ldx, n, c, gamma,
+                                                     scale, beta, mean, invstd, dgamma, dbeta, (const uint16_t*)add,
+                                                     ld_add, (uint16_t*)dx, ldx_out);
+  SSCN_HIP(hipGetLastError());
+  return SSCN_OK;
+}
+
+extern "C" sscn_status sscn_column_sum(const void* x, int64_t ldx, int64_t n, int32_t c, sscn_dtype dtype, float* out,
+                                       hipStream_t stream) {
+  SSCN_TRY(check_dtype(dtype));
+  SSCN_TRY(check_mat(x, ldx, n, c, "x"));
+  if (!out) return fail(SSCN_ERR_INVALID_ARG, "NULL out");
+  const int blocks = row_blocks(n);
+  Partials part(stream);
+  SSCN_TRY(part.alloc(blocks, c));
+  SSCN_TRY(colreduce<kSums>(dtype, x, ldx, nullptr, 0, n, c, nullptr, nullptr, nullptr, nullptr, part.p, blocks,
+                            stream));
+  k_two_sums<<<(unsigned)ceil_div(c, 256), 256, 0, stream>>>(part.p, blocks, c, out, nullptr);
+  SSCN_HIP(hipGetLastError());
+  return SSCN_OK;
+}
+
+extern "C" sscn_status sscn_add(const void* a, int64_t lda, const void* b, int64_t ldb, int64_t n, int32_t c,
+                                sscn_dtype dtype, void* y, int64_t ldy, hipStream_t stream) {
+  SSCN_TRY(check_dtype(dtype));
+  SSCN_TRY(check_mat(a, lda, n, c, "a"));
+  SSCN_TRY(check_mat(b, ldb, n, c, "b"));
+  SSCN_TRY(check_mat(y, ldy, n, c, "y"));
+  if (n == 0) return SSCN_OK;
+  const unsigned g = grid_1d(n * c);
+  if (dtype == SSCN_F32)
+    k_add<float><<<g, 256, 0, stream>>>((const float*)a, lda, (const float*)b, ldb, n, c, (float*)y, ldy);
+  else
+    k_add<uint16_t><<<g, 256, 0, stream>>>((const uint16_t*)a, lda, (const uint16_t*)b, ldb, n, c, (uint16_t*)y, ldy);
+  SSCN_HIP(hipGetLastError());
+  return SSCN_OK;
+}
+
+extern "C" sscn_status sscn_softmax_nll(const void* logits, int64_t n, int32_t classes, sscn_dtype dtype,
+                                        const int32_t* labels, float* loss, void* dlogits, hipStream_t stream) {
+  SSCN_TRY(check_dtype(dtype));
+  SSCN_TRY(check_mat(logits, classes, n, classes, "logits"));
+  if (n < 1) return fail(SSCN_ERR_INVALID_ARG, "the loss needs at least one active site");
+  if (!labels || !loss || !dlogits) return fail(SSCN_ERR_INVALID_ARG, "NULL labels, loss or dlogits");
+  const int blocks = (int)std::max<int64_t>(1, std::min<int64_t>(ceil_div(n, 4), kMaxPartials));
+  Partials part(stream);
+  SSCN_TRY(part.alloc(blocks, 1));
+  if (dtype == SSCN_F32)
+    k_softmax_nll<float><<<(unsigned)blocks, 256, 0, stream>>>((const float*)logits, n, classes, labels,
+                                                               (float*)dlogits, part.p);
+  else
+    k_softmax_nll<uint16_t><<<(unsigned)blocks, 256, 0, stream>>>((const uint16_t*)logits, n, classes, labels,
+                                                                  (uint16_t*)dlogits, part.p);
+  SSCN_HIP(hipGetLastError());
+  k_loss_finalize<<<1, 64, 0, stream>>>(part.p, blocks, n, loss);
+  SSCN_HIP(hipGetLastError());
+  return SSCN_OK;
+}
+
+extern "C" sscn_status sscn_sgd_nesterov(float* params, const float* grads, float* momentum_buf, int64_t count,
+                                         float lr, float momentum, float weight_decay, void* params_bf16,
+                                         hipStream_t stream) {
+  if (count < 0) return fail(SSCN_ERR_INVALID_ARG, "count must be >= 0");
+  if (count == 0) return SSCN_OK;
+  if (!params || !grads || !momentum_buf) return fail(SSCN_ERR_INVALID_ARG, "NULL params, grads or momentum buffer");
+  k_sgd_nesterov<<<grid_1d(count), 256, 0, stream>>>(params, grads, momentum_buf, count, lr, momentum, weight_decay,
+                                                     (uint16_t*)params_bf16);
+  SSCN_HIP(hipGetLastError());
+  return SSCN_OK;
+}

@@ -59,6 +59,7 @@ _SIGS = {
     "sparse_conv_forward": [_vp, _vp, _vp, _i32, _i32, ctypes.c_int, _vp, _vp],
     "sparse_conv_forward_heads": [_vp, _vp, _vp, _i32, _i32, ctypes.c_int, _i32, _vp, _vp],
     "sparse_conv_forward_noalloc": [_vp, _vp, _vp, _i32, _i32, ctypes.c_int, _vp, _vp],
+    "sparse_conv_forward_bias": [_vp, _vp, _vp, _vp, _i32, _i32, ctypes.c_int, _i32, _vp, _vp],
     "sparse_conv_backward": [_vp, _vp, _vp, _vp, _i32, _i32, ctypes.c_int, _vp, _vp, _vp],
     "sscn_affine_relu": [_vp, _vp, _vp, _i64, _i32, ctypes.c_int, _vp, _vp],
     "sscn_concat_cols": [_vp, _i32, _vp, _i32, _i64, ctypes.c_int, _vp, _vp],
@@ -66,6 +67,17 @@ _SIGS = {
     "sscn_pool_backward": [_vp, _vp, _vp, _i32, ctypes.c_int, ctypes.c_int, _vp, _vp],
     "sscn_upsample_forward": [_vp, _vp, _i32, ctypes.c_int, _vp, _vp],
     "sscn_upsample_backward": [_vp, _vp, _i32, ctypes.c_int, _vp, _vp],
+    "sscn_batchnorm_forward": [_vp, _i64, _i64, _i32, ctypes.c_int, _vp, _vp, ctypes.c_float, ctypes.c_float,
+                               _vp, _vp, _vp, _vp, _vp, _vp, _vp],
+    "sscn_batchnorm_relu_apply": [_vp, _i64, _i64, _i32, ctypes.c_int, _vp, _vp, _vp, _vp, _i64, _vp],
+    "sscn_batchnorm_relu_backward_params": [_vp, _i64, _vp, _i64, _i64, _i32, ctypes.c_int, _vp, _vp, _vp, _vp,
+                                            _vp, _vp, _vp],
+    "sscn_batchnorm_relu_backward_input": [_vp, _i64, _vp, _i64, _i64, _i32, ctypes.c_int, _vp, _vp, _vp, _vp,
+                                           _vp, _vp, _vp, _vp, _i64, _vp, _i64, _vp],
+    "sscn_column_sum": [_vp, _i64, _i64, _i32, ctypes.c_int, _vp, _vp],
+    "sscn_add": [_vp, _i64, _vp, _i64, _i64, _i32, ctypes.c_int, _vp, _i64, _vp],
+    "sscn_softmax_nll": [_vp, _i64, _i32, ctypes.c_int, _vp, _vp, _vp, _vp],
+    "sscn_sgd_nesterov": [_vp, _vp, _vp, _i64, ctypes.c_float, ctypes.c_float, ctypes.c_float, _vp, _vp],
     "sscn_release_cached": [],
     "sscn_last_error": [],
 }
@@ -228,7 +240,7 @@ def sparse_conv_forward(features, weights, rulebook):
     return out
 
 
-def sparse_conv_forward_heads(features, weights, rulebook, heads):
+def sparse_conv_forward_heads(features, weights, rulebook, heads, bias=None):
     """sparse_conv_forward written to 1 or 2 destinations.
 
     heads: list of (out, scale, shift); out is a device tensor of shape
@@ -262,11 +274,23 @@ def sparse_conv_forward_heads(features, weights, rulebook, heads):
         arr[i].scale = scale.data_ptr() if scale is not None else None
         arr[i].shift = shift.data_ptr() if shift is not None else None
     with torch.cuda.device(features.device):
-        _check(lib().sparse_conv_forward_heads(ctypes.c_void_p(features.data_ptr()),
-                                               ctypes.c_void_p(weights.data_ptr()), rulebook.handle, cin, cout,
-                                               _dtype_code(features), len(heads), ctypes.cast(arr, ctypes.c_void_p),
-                                               _stream(features)))
+        if bias is None:
+            _check(lib().sparse_conv_forward_heads(ctypes.c_void_p(features.data_ptr()),
+                                                   ctypes.c_void_p(weights.data_ptr()), rulebook.handle, cin, cout,
+                                                   _dtype_code(features), len(heads),
+                                                   ctypes.cast(arr, ctypes.c_void_p), _stream(features)))
+        else:
+            _check(lib().sparse_conv_forward_bias(ctypes.c_void_p(features.data_ptr()),
+                                                  ctypes.c_void_p(weights.data_ptr()), _vec(bias, cout, "bias"),
+                                                  rulebook.handle, cin, cout, _dtype_code(features), len(heads),
+                                                  ctypes.cast(arr, ctypes.c_void_p), _stream(features)))
     return [h[0] for h in heads]
+
+
+def sparse_conv_forward_bias(features, weights, bias, rulebook):
+    """sparse_conv_forward plus a per-output-channel bias on every active output row."""
+    out = torch.empty((rulebook.n_out, weights.shape[2]), dtype=features.dtype, device=features.device)
+    return sparse_conv_forward_heads(features, weights, rulebook, [(out, None, None)], bias=bias)[0]
 
 
 def sparse_conv_backward(features, weights, dout, rulebook, dgrad=True, wgrad=True):
@@ -402,3 +426,154 @@ def concat_cols(a, b):
                                       b.shape[1], a.shape[0], _dtype_code(a), ctypes.c_void_p(y.data_ptr()),
                                       _stream(a)))
     return y
+
+
+# ---------------------------------------------------------------- training
+def _mat(t, name, dtype=None):
+    """A row-major matrix view: a 2-D GPU tensor with unit column stride
+    (a column slice of a wider tensor is fine).  Returns (pointer, ld)."""
+    if not isinstance(t, torch.Tensor) or not t.is_cuda or t.dim() != 2:
+        raise ValueError(f"{name} must be a 2-D GPU tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.stride(1) != 1 and t.shape[1] > 1:
+        raise ValueError(f"{name}: columns must be contiguous")
+    return ctypes.c_void_p(t.data_ptr()), max(t.stride(0), t.shape[1])
+
+
+def _vec(t, c, name):
+    t = _dev_tensor(t, name, torch.float32)
+    if t.numel() != c:
+        raise ValueError(f"{name} must have {c} entries")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+class BatchNormStats:
+    """Per-channel results of a batch-statistics normalisation (fp32)."""
+
+    def __init__(self, c, device):
+        z = lambda: torch.empty(c, dtype=torch.float32, device=device)
+        self.mean, self.invstd, self.scale, self.shift = z(), z(), z(), z()
+
+
+def batchnorm_forward(x, gamma, beta, eps=1e-5, momentum=0.1, running_mean=None, running_var=None):
+    """Batch statistics of x over its rows -> BatchNormStats (mean, invstd,
+    scale, shift); updates the running statistics in place if given."""
+    xp, ldx = _mat(x, "x")
+    n, c = x.shape
+    st = BatchNormStats(c, x.device)
+    rm = _vec(running_mean, c, "running_mean") if running_mean is not None else None
+    rv = _vec(running_var, c, "running_var") if running_var is not None else None
+    with torch.cuda.device(x.device):
+        _check(lib().sscn_batchnorm_forward(xp, ldx, n, c, _dtype_code(x), _vec(gamma, c, "gamma"),
+                                            _vec(beta, c, "beta"), eps, momentum, rm, rv,
+                                            _vp_of(st.mean), _vp_of(st.invstd), _vp_of(st.scale),
+                                            _vp_of(st.shift), _stream(x)))
+    return st
+
+
+def batchnorm_relu_apply(x, st, beta, out=None):
+    """relu((x - mean) * scale + beta) with the statistics of batchnorm_forward."""
+    xp, ldx = _mat(x, "x")
+    n, c = x.shape
+    if out is None:
+        out = torch.empty((n, c), dtype=x.dtype, device=x.device)
+    op, ldo = _mat(out, "out", x.dtype)
+    if tuple(out.shape) != (n, c):
+        raise ValueError("out must match x")
+    with torch.cuda.device(x.device):
+        _check(lib().sscn_batchnorm_relu_apply(xp, ldx, n, c, _dtype_code(x), _vec(st.mean, c, "mean"),
+                                               _vec(st.scale, c, "scale"), _vec(beta, c, "beta"), op, ldo,
+                                               _stream(x)))
+    return out
+
+
+def batchnorm_relu_backward_params(dA, x, st, beta):
+    """(dgamma, dbeta) of batchnorm_relu_apply(x, st, beta) given dA."""
+    dp, ldd = _mat(dA, "dA", x.dtype)
+    xp, ldx = _mat(x, "x")
+    n, c = x.shape
+    dg = torch.empty(c, dtype=torch.float32, device=x.device)
+    db = torch.empty(c, dtype=torch.float32, device=x.device)
+    with torch.cuda.device(x.device):
+        _check(lib().sscn_batchnorm_relu_backward_params(dp, ldd, xp, ldx, n, c, _dtype_code(x), _vp_of(st.mean),
+                                                         _vp_of(st.invstd), _vp_of(st.scale), _vec(beta, c, "beta"),
+                                                         _vp_of(dg), _vp_of(db), _stream(x)))
+    return dg, db
+
+
+def batchnorm_relu_backward_input(dA, x, gamma, beta, st, dgamma, dbeta, out, add=None, cols=None):
+    """out = gradient at x (columns `cols` = (lo, hi) of the layer, default
+    all) plus `add`; out / add hold just those columns."""
+    n, c = x.shape
+    lo, hi = cols if cols is not None else (0, c)
+    sl = lambda t: t[:, lo:hi]
+    v = lambda t: t[lo:hi]
+    dp, ldd = _mat(sl(dA), "dA", x.dtype)
+    xp, ldx = _mat(sl(x), "x")
+    op, ldo = _mat(out, "out", x.dtype)
+    if tuple(out.shape) != (n, hi - lo):
+        raise ValueError("out must hold the selected columns")
+    ap, lda = _mat(add, "add", x.dtype) if add is not None else (None, 0)
+    if add is not None and tuple(add.shape) != (n, hi - lo):
+        raise ValueError("add must match out")
+    k = hi - lo
+    with torch.cuda.device(x.device):
+        _check(lib().sscn_batchnorm_relu_backward_input(
+            dp, ldd, xp, ldx, n, k, _dtype_code(x), _vec(v(gamma), k, "gamma"), _vec(v(beta), k, "beta"),
+            _vec(v(st.mean), k, "mean"), _vec(v(st.invstd), k, "invstd"), _vec(v(st.scale), k, "scale"),
+            _vec(v(dgamma), k, "dgamma"), _vec(v(dbeta), k, "dbeta"), ap, lda, op, ldo, _stream(x)))
+    return out
+
+
+def column_sum(x):
+    xp, ldx = _mat(x, "x")
+    n, c = x.shape
+    out = torch.empty(c, dtype=torch.float32, device=x.device)
+    with torch.cuda.device(x.device):
+        _check(lib().sscn_column_sum(xp, ldx, n, c, _dtype_code(x), _vp_of(out), _stream(x)))
+    return out
+
+
+def add_into(a, b, out):
+    ap, lda = _mat(a, "a")
+    bp, ldb = _mat(b, "b", a.dtype)
+    op, ldo = _mat(out, "out", a.dtype)
+    n, c = a.shape
+    if tuple(b.shape) != (n, c) or tuple(out.shape) != (n, c):
+        raise ValueError("shapes differ")
+    with torch.cuda.device(a.device):
+        _check(lib().sscn_add(ap, lda, bp, ldb, n, c, _dtype_code(a), op, ldo, _stream(a)))
+    return out
+
+
+def softmax_nll(logits, labels):
+    """(loss (device fp32 scalar tensor), dlogits)."""
+    logits = _dev_tensor(logits, "logits")
+    labels = _dev_tensor(labels, "labels", torch.int32)
+    n, k = logits.shape
+    if labels.shape != (n,):
+        raise ValueError("one label per row")
+    loss = torch.empty((), dtype=torch.float32, device=logits.device)
+    d = torch.empty_like(logits)
+    with torch.cuda.device(logits.device):
+        _check(lib().sscn_softmax_nll(_vp_of(logits), n, k, _dtype_code(logits), _vp_of(labels), _vp_of(loss),
+                                      _vp_of(d), _stream(logits)))
+    return loss, d
+
+
+def sgd_nesterov_(params, grads, buf, lr, momentum=0.9, weight_decay=1e-4, params_bf16=None):
+    """In-place Nesterov SGD step on fp32 `params` (contiguous); refreshes
+    the bfloat16 copy if given."""
+    params = _dev_tensor(params, "params", torch.float32)
+    grads = _dev_tensor(grads, "grads", torch.float32)
+    buf = _dev_tensor(buf, "momentum buffer", torch.float32)
+    if grads.shape != params.shape or buf.shape != params.shape:
+        raise ValueError("shapes differ")
+    if params_bf16 is not None:
+        params_bf16 = _dev_tensor(params_bf16, "params_bf16", torch.bfloat16)
+        if params_bf16.shape != params.shape:
+            raise ValueError("bf16 copy shape differs")
+    with torch.cuda.device(params.device):
+        _check(lib().sscn_sgd_nesterov(_vp_of(params), _vp_of(grads), _vp_of(buf), params.numel(), lr, momentum,
+                                       weight_decay, _vp_of(params_bf16), _stream(params)))
