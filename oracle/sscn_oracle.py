@@ -258,6 +258,13 @@ def backward(X, W, dY, rb):
     return dX, dW
 
 
+def forward_bias(X, W, b, rb):
+    """A convolution with a bias term (Sec. 3 footnote): forward(X, W, rb)
+    plus b on every active output row.  Inactive sites are not stored, so
+    the ground state the bias would give them does not appear."""
+    return forward(X, W, rb) + np.asarray(b, np.float64)
+
+
 def canonical_triples(rb):
     """All pairs as (in, out, o) rows sorted by (o, out, in)."""
     if rb.n_pairs() == 0:
@@ -602,3 +609,40 @@ def unet_train_step(coords, size, X, labels, params, channels, n_classes):
         _, dx = unit_back(dx)                   # enc{l}a
     assert not tape
     return loss, grads, stats
+
+
+# --------------------------------------------------------------------------
+# pre-activated residual blocks (Sec. 5): two SSC(3) units and an identity
+# shortcut, same number of input and output features
+# --------------------------------------------------------------------------
+def residual_block(X, rb, p1, p2):
+    """Inference form: X + SSC(relu(affine2(SSC(relu(affine1(X)), W1))), W2)
+    with p = (scale, shift, W) per unit; rb is the level's SSC(3) rule book."""
+    s1, t1, W1 = p1
+    s2, t2, W2 = p2
+    h = forward(affine_relu(X, s1, t1), W1, rb)
+    return np.asarray(X, np.float64) + forward(affine_relu(h, s2, t2), W2, rb)
+
+
+def residual_block_train(X, rb, p1, p2):
+    """Training form (batch statistics in both normalisations), p = (gamma,
+    beta, W).  Returns (Y, cache) for residual_block_train_backward."""
+    X = np.asarray(X, np.float64)
+    g1, b1, W1 = p1
+    g2, b2, W2 = p2
+    a1, m1, v1 = batch_norm_relu_train(X, g1, b1)
+    h = forward(a1, W1, rb)
+    a2, m2, v2 = batch_norm_relu_train(h, g2, b2)
+    return X + forward(a2, W2, rb), (X, rb, p1, p2, a1, m1, v1, h, a2, m2, v2)
+
+
+def residual_block_train_backward(dY, cache):
+    """Gradients of residual_block_train: (dX, (dgamma1, dbeta1, dW1),
+    (dgamma2, dbeta2, dW2)).  The shortcut passes dY to X unchanged."""
+    X, rb, (g1, b1, W1), (g2, b2, W2), a1, m1, v1, h, a2, m2, v2 = cache
+    dY = np.asarray(dY, np.float64)
+    da2, dW2 = backward(a2, W2, dY, rb)
+    dh, dg2, db2 = batch_norm_relu_backward(da2, h, g2, b2, m2, v2)
+    da1, dW1 = backward(a1, W1, dh, rb)
+    dX, dg1, db1 = batch_norm_relu_backward(da1, X, g1, b1, m1, v1)
+    return dY + dX, (dg1, db1, dW1), (dg2, db2, dW2)

@@ -227,3 +227,39 @@ def dense_unet_train(coords, size, X, labels, params, channels, n_classes, eps=1
     loss.backward()
     grads = {k: tuple(t.grad.numpy().copy() for t in v) for k, v in leaves.items()}
     return float(loss.detach()), grads, stats
+
+
+def dense_residual_block(coords, size, X, p1, p2, train=False, G=None, eps=1e-5):
+    """A pre-activated residual block (two SSC(3) units, identity shortcut)
+    on a dense grid in float64.  train: batch statistics over the active
+    sites (masked), else inference affine maps.  With G (the gradient at the
+    output, active rows), also returns the gradients by autograd.  Returns
+    (Y at the active sites, grads or None)."""
+    coords = np.asarray(coords, np.int64)
+    B = int(coords[:, 0].max()) + 1
+    mask = to_dense(coords, np.ones((coords.shape[0], 1)), size, B)
+    x = to_dense(coords, X, size, B).requires_grad_(G is not None)
+    ps = [[torch.from_numpy(np.asarray(v, np.float64).copy()).requires_grad_(G is not None) for v in p] for p in (p1, p2)]
+
+    def pre(h, g, b):
+        if not train:
+            return torch.relu(h * g.view(1, -1, 1, 1, 1) + b.view(1, -1, 1, 1, 1)) * mask
+        n = mask.sum()
+        mean = (h * mask).sum(dim=(0, 2, 3, 4)) / n
+        d = (h - mean.view(1, -1, 1, 1, 1)) * mask
+        var = (d * d).sum(dim=(0, 2, 3, 4)) / n
+        xh = d / torch.sqrt(var + eps).view(1, -1, 1, 1, 1)
+        return torch.relu(g.view(1, -1, 1, 1, 1) * xh + b.view(1, -1, 1, 1, 1)) * mask
+
+    def conv(a, W):
+        K, cin, cout = W.shape
+        return F.conv3d(a, W.reshape(3, 3, 3, cin, cout).permute(4, 3, 0, 1, 2), padding=1) * mask
+
+    h = conv(pre(x, ps[0][0], ps[0][1]), ps[0][2])
+    y = x + conv(pre(h, ps[1][0], ps[1][1]), ps[1][2])
+    ys = y[coords[:, 0], :, coords[:, 1], coords[:, 2], coords[:, 3]]
+    if G is None:
+        return ys.detach().numpy(), None
+    (ys * torch.from_numpy(np.asarray(G, np.float64))).sum().backward()
+    gx = x.grad.numpy()[coords[:, 0], :, coords[:, 1], coords[:, 2], coords[:, 3]]
+    return ys.detach().numpy(), (gx, tuple(t.grad.numpy() for t in ps[0]), tuple(t.grad.numpy() for t in ps[1]))

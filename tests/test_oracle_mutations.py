@@ -297,3 +297,37 @@ def test_dropped_skip_gradient_caught(monkeypatch):
         return dX, dW
     monkeypatch.setattr(O, "backward", bad)
     assert not _train_pins_hold()
+
+
+# --------------------------------------------------------------------------
+# bias and residual blocks
+# --------------------------------------------------------------------------
+def _block_pins_hold():
+    from tests import test_oracle_blocks as T
+    try:
+        for kind, f, s in (("ssc", 3, 1), ("sc", 2, 2)):
+            T.test_forward_bias_is_dense_conv3d_with_bias(kind, f, s)
+        T.test_residual_block_inference_is_dense()
+        T.test_residual_block_training_matches_autograd()
+    except AssertionError:
+        return False
+    return True
+
+
+def test_block_pins_hold_unmutated():
+    assert _block_pins_hold()
+
+
+def test_bias_dropped_caught(monkeypatch):
+    monkeypatch.setattr(O, "forward_bias", lambda X, W, b, rb: O.forward(X, W, rb))
+    assert not _block_pins_hold()
+
+
+def test_residual_without_shortcut_gradient_caught(monkeypatch):
+    orig = O.residual_block_train_backward
+
+    def bad(dY, cache):
+        dX, g1, g2 = orig(dY, cache)
+        return dX - np.asarray(dY), g1, g2
+    monkeypatch.setattr(O, "residual_block_train_backward", bad)
+    assert not _block_pins_hold()
