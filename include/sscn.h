@@ -187,14 +187,22 @@ sscn_status sparse_conv_forward_heads(const void* features, const void* weights,
                                       const sscn_conv_output* heads, hipStream_t stream);
 
 /*
- * sparse_conv_forward_bias -- sparse_conv_forward_heads with a bias: every
- * active output row becomes y[k] + bias before the heads map it (a
- * convolution with a bias term; the ground state at inactive sites is not
- * stored, Sec. 3 footnote).  bias: device fp32, c_out entries (non-NULL).
+ * sparse_conv_forward_ex -- sparse_conv_forward_heads with a bias and a
+ * residual: every active output row becomes
+ *   v[k] = y[k] + bias + residual[k]
+ * before the heads map it.  The bias is a convolution's bias term (the
+ * ground state at inactive sites is not stored, Sec. 3 footnote); the
+ * residual is the identity shortcut of a residual block (Sec. 5: the
+ * block's input, same sites and channels as its output).
+ *   bias         device fp32, c_out entries, nullable
+ *   residual     device n_out x c_out in dtype, row k at residual + k *
+ *                residual_ld, nullable; may be one of the heads' buffers
+ *                only if it is that head's own row (read before written)
  */
-sscn_status sparse_conv_forward_bias(const void* features, const void* weights, const float* bias,
-                                     sscn_rulebook rb, int32_t c_in, int32_t c_out, sscn_dtype dtype,
-                                     int32_t n_heads, const sscn_conv_output* heads, hipStream_t stream);
+sscn_status sparse_conv_forward_ex(const void* features, const void* weights, sscn_rulebook rb, int32_t c_in,
+                                   int32_t c_out, sscn_dtype dtype, const float* bias, const void* residual,
+                                   int64_t residual_ld, int32_t n_heads, const sscn_conv_output* heads,
+                                   hipStream_t stream);
 
 /*
  * sparse_conv_forward_noalloc -- sparse_conv_forward for callers that cannot

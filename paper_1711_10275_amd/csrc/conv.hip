@@ -60,11 +60,15 @@ struct Heads {
   // wgrad kernel after it accumulates into), n_zero floats; 0: none
   float* zero;
   int64_t n_zero;
-  // the layer's bias (c_out fp32, nullable): added to every output row
-  // before the heads map it
+  // the layer's bias (c_out fp32, nullable) and a residual (n_out x c_out in
+  // T, row stride res_ld, nullable): added to every output row before the
+  // heads map it
   const float* bias;
+  const T* res;
+  int64_t res_ld;
   __device__ __forceinline__ void store(int64_t row, int col, float v) const {
     if (bias) v += bias[col];
+    if (res) v += Elem<T>::load(res + row * res_ld + col);
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       if (h < n) {
@@ -776,7 +780,9 @@ __device__ __forceinline__ void conv_rows_block(
         const float bi = ok && Y.bias ? Y.bias[col] : 0.f;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float y = acc[nb][r] + bi;
+          const int32_t rrow = wrows[4 * g + r];
+          const float y = acc[nb][r] + bi +
+                          (Y.res && ok && rrow >= 0 ? Elem<T>::load(Y.res + rrow * Y.res_ld + col) : 0.f);
           const float v = Y.scale[h] ? fmaxf(0.f, y * sc + sh) : y;
           Elem<T>::store(reinterpret_cast<T*>(tile + (4 * g + r) * RB) + nb * 16 + m, v);
         }
@@ -1906,26 +1912,27 @@ static Heads<T> heads_of(int n, const sscn_conv_output* h) {
   return r;
 }
 
-static sscn_status forward_heads(const void* features, const void* weights, const float* bias, sscn_rulebook rb,
-                                 int32_t c_in, int32_t c_out, sscn_dtype dtype, int32_t n_heads,
-                                 const sscn_conv_output* heads, hipStream_t stream);
+static sscn_status forward_heads(const void* features, const void* weights, const float* bias, const void* residual,
+                                 int64_t residual_ld, sscn_rulebook rb, int32_t c_in, int32_t c_out, sscn_dtype dtype,
+                                 int32_t n_heads, const sscn_conv_output* heads, hipStream_t stream);
 
 extern "C" sscn_status sparse_conv_forward_heads(const void* features, const void* weights, sscn_rulebook rb,
                                                  int32_t c_in, int32_t c_out, sscn_dtype dtype, int32_t n_heads,
                                                  const sscn_conv_output* heads, hipStream_t stream) {
-  return forward_heads(features, weights, nullptr, rb, c_in, c_out, dtype, n_heads, heads, stream);
+  return forward_heads(features, weights, nullptr, nullptr, 0, rb, c_in, c_out, dtype, n_heads, heads, stream);
 }
 
-extern "C" sscn_status sparse_conv_forward_bias(const void* features, const void* weights, const float* bias,
-                                                sscn_rulebook rb, int32_t c_in, int32_t c_out, sscn_dtype dtype,
-                                                int32_t n_heads, const sscn_conv_output* heads, hipStream_t stream) {
-  if (!bias) return fail(SSCN_ERR_INVALID_ARG, "NULL bias");
-  return forward_heads(features, weights, bias, rb, c_in, c_out, dtype, n_heads, heads, stream);
+extern "C" sscn_status sparse_conv_forward_ex(const void* features, const void* weights, sscn_rulebook rb,
+                                              int32_t c_in, int32_t c_out, sscn_dtype dtype, const float* bias,
+                                              const void* residual, int64_t residual_ld, int32_t n_heads,
+                                              const sscn_conv_output* heads, hipStream_t stream) {
+  if (residual && residual_ld < c_out) return fail(SSCN_ERR_INVALID_ARG, "residual row stride < c_out");
+  return forward_heads(features, weights, bias, residual, residual_ld, rb, c_in, c_out, dtype, n_heads, heads, stream);
 }
 
-static sscn_status forward_heads(const void* features, const void* weights, const float* bias, sscn_rulebook rb,
-                                 int32_t c_in, int32_t c_out, sscn_dtype dtype, int32_t n_heads,
-                                 const sscn_conv_output* heads, hipStream_t stream) {
+static sscn_status forward_heads(const void* features, const void* weights, const float* bias, const void* residual,
+                                 int64_t residual_ld, sscn_rulebook rb, int32_t c_in, int32_t c_out, sscn_dtype dtype,
+                                 int32_t n_heads, const sscn_conv_output* heads, hipStream_t stream) {
   sscn_status st = check_conv_args(rb, c_in, c_out, dtype);
   if (st != SSCN_OK) return st;
   if (n_heads < 1 || n_heads > 2 || !heads) return fail(SSCN_ERR_INVALID_ARG, "1 or 2 output heads");
@@ -1942,10 +1949,14 @@ static sscn_status forward_heads(const void* features, const void* weights, cons
   if (dtype == SSCN_F32) {
     Heads<float> h = heads_of<float>(n_heads, heads);
     h.bias = bias;
+    h.res = (const float*)residual;
+    h.res_ld = residual_ld;
     return forward_t<float>((const float*)features, (const float*)weights, v, c_in, c_out, h, stream);
   }
   Heads<bf16_t> h = heads_of<bf16_t>(n_heads, heads);
   h.bias = bias;
+  h.res = (const bf16_t*)residual;
+  h.res_ld = residual_ld;
   return forward_t<bf16_t>((const bf16_t*)features, (const bf16_t*)weights, v, c_in, c_out, h, stream);
 }
 

@@ -59,7 +59,7 @@ _SIGS = {
     "sparse_conv_forward": [_vp, _vp, _vp, _i32, _i32, ctypes.c_int, _vp, _vp],
     "sparse_conv_forward_heads": [_vp, _vp, _vp, _i32, _i32, ctypes.c_int, _i32, _vp, _vp],
     "sparse_conv_forward_noalloc": [_vp, _vp, _vp, _i32, _i32, ctypes.c_int, _vp, _vp],
-    "sparse_conv_forward_bias": [_vp, _vp, _vp, _vp, _i32, _i32, ctypes.c_int, _i32, _vp, _vp],
+    "sparse_conv_forward_ex": [_vp, _vp, _vp, _i32, _i32, ctypes.c_int, _vp, _vp, _i64, _i32, _vp, _vp],
     "sparse_conv_backward": [_vp, _vp, _vp, _vp, _i32, _i32, ctypes.c_int, _vp, _vp, _vp],
     "sscn_affine_relu": [_vp, _vp, _vp, _i64, _i32, ctypes.c_int, _vp, _vp],
     "sscn_concat_cols": [_vp, _i32, _vp, _i32, _i64, ctypes.c_int, _vp, _vp],
@@ -240,7 +240,7 @@ def sparse_conv_forward(features, weights, rulebook):
     return out
 
 
-def sparse_conv_forward_heads(features, weights, rulebook, heads, bias=None):
+def sparse_conv_forward_heads(features, weights, rulebook, heads, bias=None, residual=None):
     """sparse_conv_forward written to 1 or 2 destinations.
 
     heads: list of (out, scale, shift); out is a device tensor of shape
@@ -274,23 +274,30 @@ def sparse_conv_forward_heads(features, weights, rulebook, heads, bias=None):
         arr[i].scale = scale.data_ptr() if scale is not None else None
         arr[i].shift = shift.data_ptr() if shift is not None else None
     with torch.cuda.device(features.device):
-        if bias is None:
+        if bias is None and residual is None:
             _check(lib().sparse_conv_forward_heads(ctypes.c_void_p(features.data_ptr()),
                                                    ctypes.c_void_p(weights.data_ptr()), rulebook.handle, cin, cout,
                                                    _dtype_code(features), len(heads),
                                                    ctypes.cast(arr, ctypes.c_void_p), _stream(features)))
         else:
-            _check(lib().sparse_conv_forward_bias(ctypes.c_void_p(features.data_ptr()),
-                                                  ctypes.c_void_p(weights.data_ptr()), _vec(bias, cout, "bias"),
-                                                  rulebook.handle, cin, cout, _dtype_code(features), len(heads),
-                                                  ctypes.cast(arr, ctypes.c_void_p), _stream(features)))
+            rp, rld = (None, 0)
+            if residual is not None:
+                rp, rld = _mat(residual, "residual", features.dtype)
+                if tuple(residual.shape) != (rulebook.n_out, cout):
+                    raise ValueError(f"residual must be ({rulebook.n_out}, {cout})")
+            _check(lib().sparse_conv_forward_ex(ctypes.c_void_p(features.data_ptr()),
+                                                ctypes.c_void_p(weights.data_ptr()), rulebook.handle, cin, cout,
+                                                _dtype_code(features),
+                                                _vec(bias, cout, "bias") if bias is not None else None, rp, rld,
+                                                len(heads), ctypes.cast(arr, ctypes.c_void_p), _stream(features)))
     return [h[0] for h in heads]
 
 
-def sparse_conv_forward_bias(features, weights, bias, rulebook):
-    """sparse_conv_forward plus a per-output-channel bias on every active output row."""
+def sparse_conv_forward_ex(features, weights, rulebook, bias=None, residual=None):
+    """sparse_conv_forward + bias (per output channel) + residual (n_out x c_out)."""
     out = torch.empty((rulebook.n_out, weights.shape[2]), dtype=features.dtype, device=features.device)
-    return sparse_conv_forward_heads(features, weights, rulebook, [(out, None, None)], bias=bias)[0]
+    return sparse_conv_forward_heads(features, weights, rulebook, [(out, None, None)], bias=bias,
+                                     residual=residual)[0]
 
 
 def sparse_conv_backward(features, weights, dout, rulebook, dgrad=True, wgrad=True):

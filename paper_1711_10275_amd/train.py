@@ -108,7 +108,7 @@ def train_step(x, labels, geom, P, lr=0.1, momentum=0.9, weight_decay=1e-4, upda
         h = unit(by_name[f"dec{l}b"], h)
     head = {}
     z = _bn_relu("head", h, P, head)
-    logits = sscn.sparse_conv_forward_bias(z, P.compute["head"], P.master["head"][3], geom.head)
+    logits = sscn.sparse_conv_forward_ex(z, P.compute["head"], geom.head, bias=P.master["head"][3])
     loss, dlogits = sscn.softmax_nll(logits, labels)
 
     grads = {}
