@@ -42,9 +42,11 @@ numpy.searchsorted, and each per-offset product is one numpy matmul.
 from __future__ import annotations
 
 import dataclasses
+import itertools
+
 import numpy as np
 
-D = 3  # spatial dimensions of every layer here
+D = 3  # spatial dimensions unless a layer's grid says otherwise
 
 
 class OracleError(Exception):
@@ -71,17 +73,19 @@ MAX_BATCH = 1 << 15
 MAX_EXTENT = 1 << 16
 
 
-def filter_offsets(f):
-    """F = {0..f-1}^3 as an (f^3, 3) array, row o = (o // f^2, (o // f) % f, o % f)."""
-    return np.array([(i0, i1, i2) for i0 in range(f) for i1 in range(f) for i2 in range(f)],
-                    dtype=np.int64).reshape(-1, 3)
+def filter_offsets(f, d=D):
+    """F = {0..f-1}^d as an (f^d, d) array in lexicographic order (first
+    coordinate most significant): for d = 3, row o = (o // f^2, (o // f) % f, o % f)."""
+    return np.array(list(itertools.product(range(f), repeat=d)), dtype=np.int64).reshape(-1, d)
 
 
 def location_key(coords, size):
-    """One integer per location (b, x0, x1, x2) inside a grid of extent `size`."""
+    """One integer per location (b, x_0, .., x_{d-1}) inside a grid of extent `size`."""
     c = np.asarray(coords, np.int64)
-    L0, L1, L2 = (int(v) for v in size)
-    return ((c[:, 0] * L0 + c[:, 1]) * L1 + c[:, 2]) * L2 + c[:, 3]
+    key = c[:, 0].copy()
+    for dd, L in enumerate(size):
+        key = key * int(L) + c[:, 1 + dd]
+    return key
 
 
 class CoordTable:
@@ -89,8 +93,8 @@ class CoordTable:
 
     def __init__(self, coords, size):
         coords = np.asarray(coords)
-        if coords.ndim != 2 or coords.shape[1] != 4:
-            raise InvalidArg("coords must be n x 4")
+        if coords.ndim != 2 or coords.shape[1] != len(size) + 1:
+            raise InvalidArg("coords must be n x (d + 1) for a d-dimensional grid")
         c = coords.astype(np.int64)
         size = tuple(int(v) for v in size)
         if any(v < 1 or v > MAX_EXTENT for v in size):
@@ -136,11 +140,15 @@ class Rulebook:
     out_size: tuple
     ins: list            # K arrays of input rows
     outs: list           # K arrays of output rows
-    out_coords: np.ndarray  # n_out x 4 int64
+    out_coords: np.ndarray  # n_out x (d + 1) int64
+
+    @property
+    def d(self):
+        return len(self.in_size)
 
     @property
     def K(self):
-        return self.f ** D
+        return self.f ** self.d
 
     def pairs_per_offset(self):
         return np.array([a.size for a in self.ins], np.int64)
@@ -162,7 +170,7 @@ def ssc_rulebook(coords, size, f):
     c = table.coords
     centre = (f - 1) // 2
     ins, outs = [], []
-    for i in filter_offsets(f):
+    for i in filter_offsets(f, len(table.size)):
         q = c.copy()
         q[:, 1:] += i - centre
         j = table.lookup(q)
@@ -197,14 +205,15 @@ def sc_rulebook(coords, size, f, s):
     out_size = sc_output_size(size, f, s)
     table = CoordTable(coords, size)
     c = table.coords
-    n, F = c.shape[0], filter_offsets(f)
+    d = len(size)
+    n, F = c.shape[0], filter_offsets(f, d)
     K = F.shape[0]
     # visit (j, o): y = (x_j - i_o) / s when that is integral and inside the output grid
     t = c[:, None, 1:] - F[None, :, :]                        # n x K x 3
     valid = np.all((t % s == 0) & (t >= 0) & (t // s < np.array(out_size)), axis=2)
     y = t // s
     b = np.broadcast_to(c[:, None, 0:1], (n, K, 1))
-    ycoords = np.concatenate([b, y], axis=2).reshape(n * K, 4)
+    ycoords = np.concatenate([b, y], axis=2).reshape(n * K, d + 1)
     vflat = valid.reshape(n * K)
     visit = np.nonzero(vflat)[0]                              # visit order = (j, o) lexicographic
     keys = location_key(ycoords[visit], out_size)
@@ -334,7 +343,7 @@ def avg_pool(X, rb):
     Y = np.zeros((rb.n_out, X.shape[1]), np.float64)
     for o in range(rb.K):
         np.add.at(Y, rb.outs[o], X[rb.ins[o]])
-    return Y / float(rb.f ** D)
+    return Y / float(rb.K)
 
 
 def avg_pool_backward(dY, rb):
@@ -343,7 +352,7 @@ def avg_pool_backward(dY, rb):
     dX = np.zeros((rb.n_in, dY.shape[1]), np.float64)
     for o in range(rb.K):
         np.add.at(dX, rb.ins[o], dY[rb.outs[o]])
-    return dX / float(rb.f ** D)
+    return dX / float(rb.K)
 
 
 def upsample_nearest(Y, rb):

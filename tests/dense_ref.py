@@ -263,3 +263,56 @@ def dense_residual_block(coords, size, X, p1, p2, train=False, G=None, eps=1e-5)
     (ys * torch.from_numpy(np.asarray(G, np.float64))).sum().backward()
     gx = x.grad.numpy()[coords[:, 0], :, coords[:, 1], coords[:, 2], coords[:, 3]]
     return ys.detach().numpy(), (gx, tuple(t.grad.numpy() for t in ps[0]), tuple(t.grad.numpy() for t in ps[1]))
+
+
+def dense_nd(coords, X, W, size, f, s, submanifold):
+    """SSC / SC in d = 1, 2 or 4 dimensions on a dense grid (float64):
+    conv1d / conv2d for d <= 2; for d = 4 the sum over the last filter axis
+    of conv3d's of shifted 3-D slices.  Returns (active output coords in
+    sorted order, features there)."""
+    coords = np.asarray(coords, np.int64)
+    d = len(size)
+    B = int(coords[:, 0].max()) + 1
+    X = np.asarray(X, np.float64)
+    W = np.asarray(W, np.float64)
+    K, cin, cout = W.shape
+    dense = np.zeros((B, cin) + tuple(size))
+    dense[(coords[:, 0], slice(None)) + tuple(coords[:, 1 + i] for i in range(d))] = X
+    occ = np.zeros((B, 1) + tuple(size))
+    occ[(coords[:, 0], 0) + tuple(coords[:, 1 + i] for i in range(d))] = 1.0
+    w = W.reshape((f,) * d + (cin, cout))
+    w = np.moveaxis(np.moveaxis(w, -1, 0), -1, 1)          # [cout][cin][i0]..[i_{d-1}]
+    pad = (f - 1) // 2 if submanifold else 0
+    stride = 1 if submanifold else s
+
+    def conv(x, wt):
+        xt, wtt = torch.from_numpy(np.ascontiguousarray(x)), torch.from_numpy(np.ascontiguousarray(wt))
+        if d == 1:
+            return F.conv1d(xt, wtt, padding=pad, stride=stride).numpy()
+        if d == 2:
+            return F.conv2d(xt, wtt, padding=pad, stride=stride).numpy()
+        # d = 4: y[..., t] = sum_i3 conv3d(x[..., stride t + i3 - pad], w[..., i3])
+        L3 = x.shape[-1]
+        M3 = (L3 + 2 * pad - f) // stride + 1
+        out = None
+        for t in range(M3):
+            acc = 0.0
+            for i3 in range(f):
+                src = stride * t + i3 - pad
+                if 0 <= src < L3:
+                    acc = acc + F.conv3d(torch.from_numpy(np.ascontiguousarray(x[..., src])),
+                                         torch.from_numpy(np.ascontiguousarray(wt[..., i3])),
+                                         padding=pad, stride=stride).numpy()
+            if out is None:
+                out = np.zeros(np.shape(acc) + (M3,))
+            out[..., t] = acc
+        return out
+
+    y = conv(dense, w)
+    if submanifold:
+        act = coords[np.lexsort(tuple(coords[:, i] for i in range(d, -1, -1)))]
+    else:
+        cnt = conv(occ, np.ones((1, 1) + (f,) * d))[:, 0]
+        act = np.argwhere(cnt > 0)
+    vals = y[(act[:, 0], slice(None)) + tuple(act[:, 1 + i] for i in range(d))]
+    return act.astype(np.int64), vals

@@ -98,7 +98,7 @@ def test_triples_swapped_columns_caught(monkeypatch):
 
 def test_offset_sign_error_caught(monkeypatch):
     orig = O.filter_offsets
-    monkeypatch.setattr(O, "filter_offsets", lambda f: (f - 1) - orig(f))
+    monkeypatch.setattr(O, "filter_offsets", lambda f, d=3: (f - 1) - orig(f, d))
     assert _ssc_pin_error() > 1e-3
 
 
@@ -123,7 +123,7 @@ def test_transposed_weight_caught(monkeypatch):
 def test_wrong_ssc_centre_caught(monkeypatch):
     orig = O.filter_offsets
     # shifting the offsets by one voxel along x2 moves the SSC field off-centre
-    monkeypatch.setattr(O, "filter_offsets", lambda f: orig(f) + np.array([0, 0, 1]))
+    monkeypatch.setattr(O, "filter_offsets", lambda f, d=3: orig(f, d) + np.eye(d, dtype=np.int64)[-1])
     assert _ssc_pin_error() > 1e-3
 
 
@@ -331,3 +331,35 @@ def test_residual_without_shortcut_gradient_caught(monkeypatch):
         return dX - np.asarray(dY), g1, g2
     monkeypatch.setattr(O, "residual_block_train_backward", bad)
     assert not _block_pins_hold()
+
+
+# --------------------------------------------------------------------------
+# other dimensions
+# --------------------------------------------------------------------------
+def _nd_pins_hold():
+    from tests import test_oracle_nd as T
+    try:
+        for case in T.CASES:
+            T.test_nd_rulebook_and_forward(*case)
+        T.test_4d_with_one_position_on_the_last_axis_is_3d(3, 1, True)
+        T.test_4d_with_one_position_on_the_last_axis_is_3d(2, 2, False)
+    except AssertionError:
+        return False
+    return True
+
+
+def test_nd_pins_hold_unmutated():
+    assert _nd_pins_hold()
+
+
+def test_nd_offset_order_reversed_caught(monkeypatch):
+    orig = O.filter_offsets
+    monkeypatch.setattr(O, "filter_offsets", lambda f, d=3: orig(f, d)[:, ::-1].copy())
+    assert not _nd_pins_hold()
+
+
+def test_nd_key_ignoring_an_axis_caught(monkeypatch):
+    orig = O.location_key
+    monkeypatch.setattr(O, "location_key", lambda coords, size: orig(np.asarray(coords)[:, :-1], size[:-1])
+                        if len(size) == 4 else orig(coords, size))
+    assert not _nd_pins_hold()
