@@ -343,7 +343,7 @@ def _nd_pins_hold():
             T.test_nd_rulebook_and_forward(*case)
         T.test_4d_with_one_position_on_the_last_axis_is_3d(3, 1, True)
         T.test_4d_with_one_position_on_the_last_axis_is_3d(2, 2, False)
-    except AssertionError:
+    except (AssertionError, O.OracleError):   # a planted mistake may also make the oracle refuse the input
         return False
     return True
 
