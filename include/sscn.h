@@ -95,6 +95,25 @@ sscn_status sc_rulebook_build(const int32_t* coords, int64_t n, const int32_t* s
                               sscn_rulebook* out);
 
 /*
+ * sscn_rulebook_build_nd -- the rule book of SSC(., ., f) (submanifold != 0,
+ * stride 1) or SC(., ., f, s) on a d-dimensional grid, d = dim in [1, 4]
+ * (the layers are defined for any d, Sec. 3; 4-D data such as RGB-D video,
+ * Sec. 1).  d = 3 is ssc_rulebook_build / sc_rulebook_build.
+ *   coords        device, n x (d + 1) int32 rows (b, x_0, .., x_{d-1}),
+ *                 4-byte aligned
+ *   spatial_size  host, d extents
+ * Offsets are numbered in base f with the first coordinate most
+ * significant (o = ((i_0 f + i_1) f + ..) ); K = f^d <= 512 and
+ * 32768 * prod(spatial_size) < 2^63 (else SSCN_ERR_INVALID_ARG); SC shape
+ * rules, output numbering, errors and storage as in three dimensions, so
+ * every other call takes the result unchanged.  sscn_rulebook_out_coords
+ * then gives n_out x (d + 1) rows.  Blocks the host once.
+ */
+sscn_status sscn_rulebook_build_nd(const int32_t* coords, int64_t n, int32_t dim, const int32_t* spatial_size,
+                                   int32_t filter_size, int32_t stride, int32_t submanifold, hipStream_t stream,
+                                   sscn_rulebook* out);
+
+/*
  * sscn_rulebook_transpose -- the inverted connections R^T_o = {(k, j) :
  * (j, k) in R_o}: the rule book of the deconvolution DC that inverts an SC
  * (Sec. 4.1 "Other operators"); its output set is the SC's input set, in
@@ -108,7 +127,8 @@ sscn_status sscn_rulebook_transpose(sscn_rulebook rb, sscn_rulebook* out);
 typedef struct {
   int64_t n_in, n_out, n_pairs;
   int32_t filter_size, stride, submanifold, transposed, n_offsets;
-  int32_t in_size[3], out_size[3];
+  int32_t dim;                      /* spatial dimensions d (3 unless built by sscn_rulebook_build_nd) */
+  int32_t in_size[4], out_size[4];  /* grid extents; the first d entries are used */
 } sscn_rulebook_info;
 
 /*
@@ -122,8 +142,9 @@ sscn_status sscn_rulebook_query(sscn_rulebook rb, sscn_rulebook_info* info,
                                 int64_t* pairs_per_offset);
 
 /*
- * sscn_rulebook_out_coords -- device n_out x 4 int32 coordinates of the
- * output sites, in output row order, grid of extent info.out_size.
+ * sscn_rulebook_out_coords -- device n_out x (d + 1) int32 coordinates of
+ * the output sites (n_out x 4 for d = 3), in output row order, grid of
+ * extent info.out_size.
  */
 sscn_status sscn_rulebook_out_coords(sscn_rulebook rb, int32_t* out_coords, hipStream_t stream);
 

@@ -38,6 +38,7 @@ constexpr int kTileGroups = 8;
 constexpr uint64_t kEmptyKey = ~0ull;
 constexpr int kMaxBatch = 1 << 15;
 constexpr int kMaxExtent = 1 << 16;
+constexpr int kMaxDim = 4;
 
 // error flags raised by device code
 constexpr int kFlagOutOfRange = 1;
@@ -115,12 +116,13 @@ struct RulebookData {
   int f = 0, stride = 1, K = 0;
   bool submanifold = false;
   int64_t n_in = 0, n_out = 0, n_pairs = 0;
-  int32_t in_size[3] = {0, 0, 0}, out_size[3] = {0, 0, 0};
+  int dim = 3;                   // spatial dimensions d: coordinates are n x (d + 1)
+  int32_t in_size[4] = {0, 0, 0, 0}, out_size[4] = {0, 0, 0, 0};
   std::vector<int64_t> pairs_per_offset;  // host copy, K entries
   Storage fwd;                   // tiles over output rows
   Storage bwd;                   // tiles over input rows (SC only; SSC mirrors fwd)
-  int32_t* out_coords = nullptr; // n_out x 4
-  int32_t* in_coords = nullptr;  // n_in x 4 (SC only; an SSC's input sites are its output sites)
+  int32_t* out_coords = nullptr; // n_out x (d + 1)
+  int32_t* in_coords = nullptr;  // n_in x (d + 1) (SC only; an SSC's input sites are its output sites)
   std::vector<void*> blocks;     // device allocations owning all of the above
   // The chunk tables are built on first use (by the kernels that read
   // them) on the build stream; `chunk_ready` is recorded after the build so

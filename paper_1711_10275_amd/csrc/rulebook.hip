@@ -1921,7 +1921,8 @@ extern "C" sscn_status sscn_rulebook_query(sscn_rulebook rb, sscn_rulebook_info*
   info->submanifold = d->submanifold ? 1 : 0;
   info->transposed = t ? 1 : 0;
   info->n_offsets = d->K;
-  for (int i = 0; i < 3; ++i) {
+  info->dim = d->dim;
+  for (int i = 0; i < kMaxDim; ++i) {
     info->in_size[i] = t ? d->out_size[i] : d->in_size[i];
     info->out_size[i] = t ? d->in_size[i] : d->out_size[i];
   }
@@ -1944,7 +1945,7 @@ extern "C" sscn_status sscn_rulebook_out_coords(sscn_rulebook rb, int32_t* out_c
   // a transposed SC view outputs at the SC's input sites
   const int32_t* src = (rb->transposed && !d->submanifold) ? d->in_coords : d->out_coords;
   UseNote note{rb->d, s};
-  SSCN_HIP(hipMemcpyAsync(out_coords, src, sizeof(int32_t) * 4 * n_out, hipMemcpyDeviceToDevice, s));
+  SSCN_HIP(hipMemcpyAsync(out_coords, src, sizeof(int32_t) * (d->dim + 1) * n_out, hipMemcpyDeviceToDevice, s));
   return SSCN_OK;
 }
 
@@ -1980,4 +1981,379 @@ extern "C" void sscn_rulebook_free(sscn_rulebook rb) {
   if (!rb) return;
   if (rb->d->refs.fetch_sub(1) == 1) delete rb->d;
   delete rb;
+}
+
+// ========================================================== any dimension
+// Rule books of d-dimensional layers for d = 1, 2, 4 (d = 3 takes the tuned
+// builders above).  The method is the same in every dimension (Sec. 3
+// defines the layers on d-dimensional grids; Sec. 1: 4-D data such as RGB-D
+// video): sites are rows (b, x_0, .., x_{d-1}) of an n x (d + 1) int32
+// array, F = {0..f-1}^d is enumerated with the first coordinate most
+// significant, keys are the linear index ((b L_0 + x_0) L_1 + ..) in 64
+// bits.  The dictionary is the 16-byte-slot table, the SSC probe looks up
+// every (offset, site) pair (one lane each, offset-major so that a
+// wavefront reads consecutive sites), and the SC outputs are numbered by
+// first visit exactly as in three dimensions; both directions are then
+// compacted into the same storage as the 3-D builders produce, so the
+// convolution, pooling and export calls are unchanged.
+namespace sscn {
+namespace {
+
+template <int DD>
+struct GeomN {
+  int32_t L[DD];  // input extents
+  int32_t M[DD];  // output extents (SC)
+  int f, s, K;
+};
+
+// Reads site j; false if it lies outside the grid (or the batch range).
+template <int DD>
+__device__ __forceinline__ bool site_n(const int32_t* __restrict__ coords, int64_t j, const GeomN<DD>& g, int& b,
+                                       int (&x)[DD]) {
+  const int32_t* r = coords + j * (DD + 1);
+  b = r[0];
+  bool ok = (unsigned)b < (unsigned)kMaxBatch;
+#pragma unroll
+  for (int q = 0; q < DD; ++q) {
+    x[q] = r[1 + q];
+    ok = ok && (unsigned)x[q] < (unsigned)g.L[q];
+  }
+  return ok;
+}
+
+template <int DD>
+__device__ __forceinline__ uint64_t key_n(int b, const int (&x)[DD], const int32_t (&ext)[DD]) {
+  uint64_t k = (uint64_t)(uint32_t)b;
+#pragma unroll
+  for (int q = 0; q < DD; ++q) k = k * (uint64_t)(uint32_t)ext[q] + (uint64_t)(uint32_t)x[q];
+  return k;
+}
+
+// Offset o -> its filter position (first coordinate most significant).
+template <int DD>
+__device__ __forceinline__ void digits_n(int o, int f, int (&i)[DD]) {
+#pragma unroll
+  for (int q = DD - 1; q >= 0; --q) {
+    i[q] = o % f;
+    o /= f;
+  }
+}
+
+template <int DD>
+__global__ __launch_bounds__(256) void k_insert_n(const int32_t* __restrict__ coords, int64_t n, GeomN<DD> g,
+                                                  Slot* __restrict__ table, uint64_t mask,
+                                                  unsigned long long* __restrict__ flags, int32_t* __restrict__ copy) {
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= n) return;
+  if (copy)
+    for (int q = 0; q <= DD; ++q) copy[j * (DD + 1) + q] = coords[j * (DD + 1) + q];
+  int b, x[DD];
+  if (!site_n<DD>(coords, j, g, b, x)) {
+    atomicOr(flags, (unsigned long long)kFlagOutOfRange);
+    return;
+  }
+  const uint64_t key = key_n<DD>(b, x, g.L);
+  uint64_t slot = mix64(key) & mask;
+  while (true) {
+    const unsigned long long prev = atomicCAS((unsigned long long*)&table[slot].key, (unsigned long long)kEmptyKey,
+                                              (unsigned long long)key);
+    if (prev == kEmptyKey) {
+      table[slot].row = (int32_t)j;
+      return;
+    }
+    if (prev == key) {
+      atomicOr(flags, (unsigned long long)kFlagDuplicate);
+      return;
+    }
+    slot = (slot + 1) & mask;
+  }
+}
+
+// nbr[o n + k] = row of the site at x_k + i_o - (f-1)/2, or -1 (sites
+// outside the grid were flagged by the insert; the build then fails).
+template <int DD>
+__global__ __launch_bounds__(256) void k_probe_n(const int32_t* __restrict__ coords, int64_t n, GeomN<DD> g,
+                                                 const Slot* __restrict__ table, uint64_t mask,
+                                                 int32_t* __restrict__ nbr) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= n * g.K) return;
+  const int o = (int)(idx / n);
+  const int64_t k = idx - (int64_t)o * n;
+  int b, x[DD], i[DD];
+  int32_t j = -1;
+  if (site_n<DD>(coords, k, g, b, x)) {
+    digits_n<DD>(o, g.f, i);
+    const int c = (g.f - 1) / 2;
+    bool in = true;
+#pragma unroll
+    for (int q = 0; q < DD; ++q) {
+      x[q] += i[q] - c;
+      in = in && (unsigned)x[q] < (unsigned)g.L[q];
+    }
+    if (in) j = table_lookup(table, mask, key_n<DD>(b, x, g.L));
+  }
+  nbr[idx] = j;
+}
+
+// Output location that input x reaches through offset o, if any.
+template <int DD>
+__device__ __forceinline__ bool sc_target_n(const GeomN<DD>& g, const int (&x)[DD], int o, int (&y)[DD]) {
+  int i[DD];
+  digits_n<DD>(o, g.f, i);
+  bool ok = true;
+#pragma unroll
+  for (int q = 0; q < DD; ++q) {
+    const int t = x[q] - i[q];
+    ok = ok && t >= 0 && t % g.s == 0;
+    y[q] = t / g.s;
+    ok = ok && y[q] < g.M[q];
+  }
+  return ok;
+}
+
+template <int DD>
+__global__ __launch_bounds__(256) void k_sc_visit_n(const int32_t* __restrict__ coords, int64_t n, GeomN<DD> g,
+                                                    Slot* __restrict__ otable, uint64_t omask) {
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= n) return;
+  int b, x[DD];
+  if (!site_n<DD>(coords, j, g, b, x)) return;
+  for (int o = 0; o < g.K; ++o) {
+    int y[DD];
+    if (!sc_target_n<DD>(g, x, o, y)) continue;
+    const uint64_t key = key_n<DD>(b, y, g.M);
+    uint64_t slot = mix64(key) & omask;
+    while (true) {
+      const unsigned long long prev = atomicCAS((unsigned long long*)&otable[slot].key,
+                                                (unsigned long long)kEmptyKey, (unsigned long long)key);
+      if (prev == kEmptyKey || prev == key) break;
+      slot = (slot + 1) & omask;
+    }
+    atomicMin(&otable[slot].row, (int32_t)(j * g.K + o));
+  }
+}
+
+// first[j K + o] = 1 iff visit (j, o) is the first of its output;
+// per_offset[o] += visits through o.
+template <int DD>
+__global__ __launch_bounds__(256) void k_sc_mark_n(const int32_t* __restrict__ coords, int64_t n, GeomN<DD> g,
+                                                   const Slot* __restrict__ otable, uint64_t omask,
+                                                   int32_t* __restrict__ first,
+                                                   unsigned long long* __restrict__ per_offset) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= n * g.K) return;
+  const int64_t j = idx / g.K;
+  const int o = (int)(idx - j * g.K);
+  int b, x[DD], y[DD];
+  int32_t is_first = 0;
+  if (site_n<DD>(coords, j, g, b, x) && sc_target_n<DD>(g, x, o, y)) {
+    is_first = table_lookup(otable, omask, key_n<DD>(b, y, g.M)) == (int32_t)idx;
+    atomicAdd(&per_offset[o], 1ull);
+  }
+  first[idx] = is_first;
+}
+
+template <int DD>
+__global__ __launch_bounds__(256) void k_sc_assign_n(const int32_t* __restrict__ coords, int64_t n, GeomN<DD> g,
+                                                     const Slot* __restrict__ otable, uint64_t omask,
+                                                     const int32_t* __restrict__ rank, int64_t n_out,
+                                                     int32_t* __restrict__ nbr_out, int32_t* __restrict__ nbr_in,
+                                                     int32_t* __restrict__ out_coords) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= n * g.K) return;
+  const int64_t j = idx / g.K;
+  const int o = (int)(idx - j * g.K);
+  int b, x[DD], y[DD];
+  if (!site_n<DD>(coords, j, g, b, x) || !sc_target_n<DD>(g, x, o, y)) return;
+  const int32_t vmin = table_lookup(otable, omask, key_n<DD>(b, y, g.M));
+  const int32_t k = rank[vmin];
+  nbr_out[(int64_t)o * n_out + k] = (int32_t)j;
+  nbr_in[(int64_t)o * n + j] = k;
+  if (vmin == (int32_t)idx) {
+    out_coords[(int64_t)k * (DD + 1)] = b;
+#pragma unroll
+    for (int q = 0; q < DD; ++q) out_coords[(int64_t)k * (DD + 1) + 1 + q] = y[q];
+  }
+}
+
+template <int DD>
+sscn_status build_nd(const int32_t* coords, int64_t n, const int32_t* size, int f, int stride, bool sub,
+                     hipStream_t s, sscn_rulebook* out) {
+  int K = 1;
+  for (int q = 0; q < DD; ++q) K *= f;
+  GeomN<DD> g;
+  g.f = f; g.s = stride; g.K = K;
+  for (int q = 0; q < DD; ++q) {
+    g.L[q] = size[q];
+    if (sub) {
+      g.M[q] = size[q];
+    } else {
+      if (size[q] < f || (size[q] - f) % stride != 0)
+        return fail(SSCN_ERR_SHAPE, "SC needs L >= f and (L - f) divisible by the stride in every dimension");
+      g.M[q] = (size[q] - f + stride) / stride;
+    }
+  }
+  RulebookData* d = new (std::nothrow) RulebookData;
+  if (!d) return fail(SSCN_ERR_OOM, "host allocation failed");
+  std::unique_ptr<RulebookData> guard(d);
+  (void)hipGetDevice(&d->device);
+  d->stream = s;
+  d->dim = DD;
+  d->f = f; d->stride = sub ? 1 : stride; d->K = K; d->submanifold = sub;
+  d->n_in = n;
+  for (int q = 0; q < DD; ++q) { d->in_size[q] = g.L[q]; d->out_size[q] = g.M[q]; }
+  d->pairs_per_offset.assign(K, 0);
+  {
+    Temps tmp(s);
+    const uint64_t cap = table_capacity(n);
+    Slot* table; unsigned long long* stats;
+    Arena ta;
+    ta.add(&table, cap);
+    ta.add(&stats, 2 + K);
+    SSCN_TRY(tmp.alloc(ta));
+    SSCN_TRY(launch_fill_slots(table, cap, -1, s, stats, 2 + K));
+    if (sub) {
+      d->n_out = n;
+      d->fwd.n_tiles = ceil_div(n, kTile);
+      int32_t* nbr;
+      Arena na;
+      na.add(&nbr, (size_t)K * n);
+      SSCN_TRY(tmp.alloc(na));
+      Arena oa;
+      oa.add(&d->out_coords, (size_t)(DD + 1) * n);
+      oa.add(&d->fwd.seg, (size_t)K * d->fwd.n_tiles + 1);
+      SSCN_TRY(owned_alloc(d, oa, s));
+      if (n > 0) {
+        k_insert_n<DD><<<grid_for(n, 256), 256, 0, s>>>(coords, n, g, table, cap - 1, stats, d->out_coords);
+        SSCN_HIP(hipGetLastError());
+        k_probe_n<DD><<<grid_for(n * K, 256), 256, 0, s>>>(coords, n, g, table, cap - 1, nbr);
+        SSCN_HIP(hipGetLastError());
+        k_count_nbr<<<grid_for(d->fwd.n_tiles * 64, 256), 256, 0, s>>>(nbr, n, K, d->fwd.seg, d->fwd.n_tiles);
+        SSCN_HIP(hipGetLastError());
+      }
+      SSCN_TRY(exclusive_scan_i64(d->fwd.seg, d->fwd.seg, K * d->fwd.n_tiles, s));
+      if (n > 0) {
+        k_offset_totals<<<grid_for(K, 256), 256, 0, s>>>(d->fwd.seg, d->fwd.n_tiles, K, stats);
+        SSCN_HIP(hipGetLastError());
+      }
+      std::vector<unsigned long long> host(2 + K);
+      SSCN_TRY(readback(host.data(), stats, sizeof(unsigned long long) * (2 + K), s));
+      SSCN_TRY(flags_error(host[0]));
+      int64_t total = 0;
+      for (int o = 0; o < K; ++o) total += (d->pairs_per_offset[o] = (int64_t)host[1 + o]);
+      d->n_pairs = total;
+      Arena pa;
+      pa.add(&d->fwd.in_rows, total);
+      pa.add(&d->fwd.out_rows, total);
+      pa.add(&d->fwd.order, d->fwd.n_tiles);
+      SSCN_TRY(owned_alloc(d, pa, s));
+      if (n > 0) SSCN_TRY(compact_storage(nbr, n, K, d->fwd, s, /*counted=*/true));
+    } else {
+      // every input reaches at most prod_q ceil(f / s) outputs
+      const int per = (f + stride - 1) / stride;
+      int64_t max_out = n;
+      for (int q = 0; q < DD; ++q) max_out *= per;
+      const uint64_t ocap = table_capacity(max_out);
+      Slot* otable; int32_t* first; int32_t* rank;
+      Arena sa;
+      sa.add(&otable, ocap);
+      sa.add(&first, (size_t)n * K);
+      sa.add(&rank, (size_t)n * K + 1);
+      SSCN_TRY(tmp.alloc(sa));
+      Arena ia;
+      ia.add(&d->in_coords, (size_t)(DD + 1) * n);
+      SSCN_TRY(owned_alloc(d, ia, s));
+      if (n > 0) {
+        SSCN_TRY(launch_fill_slots(otable, ocap, INT32_MAX, s));
+        k_insert_n<DD><<<grid_for(n, 256), 256, 0, s>>>(coords, n, g, table, cap - 1, stats, d->in_coords);
+        SSCN_HIP(hipGetLastError());
+        k_sc_visit_n<DD><<<grid_for(n, 256), 256, 0, s>>>(coords, n, g, otable, ocap - 1);
+        SSCN_HIP(hipGetLastError());
+        k_sc_mark_n<DD><<<grid_for(n * K, 256), 256, 0, s>>>(coords, n, g, otable, ocap - 1, first, stats + 1);
+        SSCN_HIP(hipGetLastError());
+        SSCN_TRY(exclusive_scan_i32(first, rank, n * K, s));
+        SSCN_HIP(hipMemcpyAsync(stats + 1 + K, rank + (size_t)n * K, sizeof(int32_t), hipMemcpyDeviceToDevice, s));
+      }
+      std::vector<unsigned long long> host(2 + K);
+      SSCN_TRY(readback(host.data(), stats, sizeof(unsigned long long) * (2 + K), s));
+      SSCN_TRY(flags_error(host[0]));
+      int64_t total = 0;
+      for (int o = 0; o < K; ++o) total += (d->pairs_per_offset[o] = (int64_t)host[1 + o]);
+      d->n_pairs = total;
+      const int64_t n_out = n > 0 ? (int64_t)(uint32_t)(host[1 + K] & 0xffffffffull) : 0;
+      d->n_out = n_out;
+      d->fwd.n_tiles = ceil_div(n_out, kTile);
+      d->bwd.n_tiles = ceil_div(n, kTile);
+      Arena oa;
+      oa.add(&d->out_coords, (size_t)(DD + 1) * n_out);
+      oa.add(&d->fwd.seg, (size_t)K * d->fwd.n_tiles + 1);
+      oa.add(&d->bwd.seg, (size_t)K * d->bwd.n_tiles + 1);
+      oa.add(&d->fwd.in_rows, total);
+      oa.add(&d->fwd.out_rows, total);
+      oa.add(&d->bwd.in_rows, total);
+      oa.add(&d->bwd.out_rows, total);
+      oa.add(&d->fwd.order, d->fwd.n_tiles);
+      oa.add(&d->bwd.order, d->bwd.n_tiles);
+      SSCN_TRY(owned_alloc(d, oa, s));
+      if (n > 0) {
+        int32_t* nbr_out; int32_t* nbr_in;
+        Arena na;
+        na.add(&nbr_out, (size_t)K * n_out);
+        na.add(&nbr_in, (size_t)K * n);
+        SSCN_TRY(tmp.alloc(na));
+        SSCN_TRY(fill_i32(nbr_out, -1, (int64_t)K * n_out, s));
+        SSCN_TRY(fill_i32(nbr_in, -1, (int64_t)K * n, s));
+        k_sc_assign_n<DD><<<grid_for(n * K, 256), 256, 0, s>>>(coords, n, g, otable, ocap - 1, rank, n_out, nbr_out,
+                                                               nbr_in, d->out_coords);
+        SSCN_HIP(hipGetLastError());
+        SSCN_TRY(compact_storage(nbr_out, n_out, K, d->fwd, s, false));
+        SSCN_TRY(compact_storage(nbr_in, n, K, d->bwd, s, false));
+      } else {
+        SSCN_TRY(exclusive_scan_i64(d->fwd.seg, d->fwd.seg, 0, s));
+        SSCN_TRY(exclusive_scan_i64(d->bwd.seg, d->bwd.seg, 0, s));
+      }
+    }
+  }
+  guard.release();
+  return new_handle(d, out);
+}
+
+}  // namespace
+}  // namespace sscn
+
+extern "C" sscn_status sscn_rulebook_build_nd(const int32_t* coords, int64_t n, int32_t dim,
+                                              const int32_t* spatial_size, int32_t filter_size, int32_t stride,
+                                              int32_t submanifold, hipStream_t stream, sscn_rulebook* out) {
+  if (!out) return fail(SSCN_ERR_INVALID_ARG, "out handle pointer is NULL");
+  if (dim < 1 || dim > kMaxDim) return fail(SSCN_ERR_INVALID_ARG, "dim must be in [1, 4]");
+  if (!spatial_size) return fail(SSCN_ERR_INVALID_ARG, "spatial_size is NULL");
+  if (submanifold && filter_size % 2 == 0) return fail(SSCN_ERR_INVALID_ARG, "SSC needs an odd filter_size");
+  if (submanifold && stride != 1) return fail(SSCN_ERR_INVALID_ARG, "SSC has stride 1");
+  if (dim == 3) {
+    return submanifold ? ssc_rulebook_build(coords, n, spatial_size, filter_size, stream, out)
+                       : sc_rulebook_build(coords, n, spatial_size, filter_size, stride, stream, out);
+  }
+  if (n < 0) return fail(SSCN_ERR_INVALID_ARG, "n < 0");
+  if (n > 0 && !coords) return fail(SSCN_ERR_INVALID_ARG, "coords is NULL with n > 0");
+  if (n > 0 && ((uintptr_t)coords & 3)) return fail(SSCN_ERR_INVALID_ARG, "coords must be 4-byte aligned");
+  if (filter_size < 1 || filter_size > 8) return fail(SSCN_ERR_INVALID_ARG, "filter_size must be in [1, 8]");
+  if (stride < 1 || stride > 8) return fail(SSCN_ERR_INVALID_ARG, "stride must be in [1, 8]");
+  // keys: kMaxBatch * prod L must stay below 2^63 (and differ from the empty marker)
+  long double vol = (long double)kMaxBatch;
+  int64_t K = 1;
+  for (int q = 0; q < dim; ++q) {
+    if (spatial_size[q] < 1 || spatial_size[q] > kMaxExtent)
+      return fail(SSCN_ERR_INVALID_ARG, "spatial_size entries must be in [1, 65536]");
+    vol *= (long double)spatial_size[q];
+    K *= filter_size;
+  }
+  if (vol >= 9.2e18L) return fail(SSCN_ERR_INVALID_ARG, "32768 * prod(spatial_size) must stay below 2^63");
+  if (K > 512) return fail(SSCN_ERR_INVALID_ARG, "filter_size^dim must be at most 512");
+  if (n * K >= (int64_t)INT32_MAX) return fail(SSCN_ERR_INVALID_ARG, "n * filter_size^dim must be below 2^31");
+  const bool sub = submanifold != 0;
+  switch (dim) {
+    case 1: return build_nd<1>(coords, n, spatial_size, filter_size, stride, sub, stream, out);
+    case 2: return build_nd<2>(coords, n, spatial_size, filter_size, stride, sub, stream, out);
+    default: return build_nd<4>(coords, n, spatial_size, filter_size, stride, sub, stream, out);
+  }
 }

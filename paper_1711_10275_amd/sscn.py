@@ -34,8 +34,8 @@ class RulebookInfo(ctypes.Structure):
     _fields_ = [("n_in", ctypes.c_int64), ("n_out", ctypes.c_int64), ("n_pairs", ctypes.c_int64),
                 ("filter_size", ctypes.c_int32), ("stride", ctypes.c_int32),
                 ("submanifold", ctypes.c_int32), ("transposed", ctypes.c_int32),
-                ("n_offsets", ctypes.c_int32), ("in_size", ctypes.c_int32 * 3),
-                ("out_size", ctypes.c_int32 * 3)]
+                ("n_offsets", ctypes.c_int32), ("dim", ctypes.c_int32), ("in_size", ctypes.c_int32 * 4),
+                ("out_size", ctypes.c_int32 * 4)]
 
 
 class ConvOutput(ctypes.Structure):
@@ -51,6 +51,7 @@ _vp, _i32, _i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
 _SIGS = {
     "ssc_rulebook_build": [_vp, _i64, _vp, _i32, _vp, _vp],
     "sc_rulebook_build": [_vp, _i64, _vp, _i32, _i32, _vp, _vp],
+    "sscn_rulebook_build_nd": [_vp, _i64, _i32, _vp, _i32, _i32, _i32, _vp, _vp],
     "sscn_rulebook_transpose": [_vp, _vp],
     "sscn_rulebook_query": [_vp, _vp, _vp],
     "sscn_rulebook_out_coords": [_vp, _vp, _vp],
@@ -153,7 +154,8 @@ class Rulebook:
         self.filter_size, self.stride = info.filter_size, info.stride
         self.submanifold, self.transposed = bool(info.submanifold), bool(info.transposed)
         self.n_offsets = K
-        self.in_size, self.out_size = tuple(info.in_size), tuple(info.out_size)
+        self.dim = info.dim
+        self.in_size, self.out_size = tuple(info.in_size[:info.dim]), tuple(info.out_size[:info.dim])
         self.pairs_per_offset = list(ppo[:K])
 
     @property
@@ -166,7 +168,7 @@ class Rulebook:
         return Rulebook(h, self.device)
 
     def out_coords(self):
-        out = torch.empty((self.n_out, 4), dtype=torch.int32, device=self.device)
+        out = torch.empty((self.n_out, self.dim + 1), dtype=torch.int32, device=self.device)
         with torch.cuda.device(self.device):
             _check(lib().sscn_rulebook_out_coords(self._h, ctypes.c_void_p(out.data_ptr()), _stream(out)))
         return out
@@ -204,8 +206,23 @@ def _sizes(spatial_size):
     return _I32x3(*s)
 
 
+def _build_nd(coords, spatial_size, filter_size, stride, submanifold):
+    size = tuple(int(v) for v in spatial_size)
+    if not 1 <= len(size) <= 4 or coords.dim() != 2 or coords.shape[1] != len(size) + 1:
+        raise ValueError("coords must be n x (d + 1) for d = len(spatial_size) in [1, 4]")
+    h = ctypes.c_void_p()
+    with torch.cuda.device(coords.device):
+        _check(lib().sscn_rulebook_build_nd(ctypes.c_void_p(coords.data_ptr()), coords.shape[0], len(size),
+                                            (ctypes.c_int32 * len(size))(*size), int(filter_size), int(stride),
+                                            1 if submanifold else 0, _stream(coords), ctypes.byref(h)))
+    return Rulebook(h, coords.device)
+
+
 def ssc_rulebook_build(coords, spatial_size, filter_size=3):
+    """SSC rule book; any d = len(spatial_size) in [1, 4] (coords n x (d + 1))."""
     coords = _dev_tensor(coords, "coords", torch.int32)
+    if len(spatial_size) != 3:
+        return _build_nd(coords, spatial_size, filter_size, 1, True)
     h = ctypes.c_void_p()
     with torch.cuda.device(coords.device):
         _check(lib().ssc_rulebook_build(ctypes.c_void_p(coords.data_ptr()), coords.shape[0],
@@ -215,7 +232,10 @@ def ssc_rulebook_build(coords, spatial_size, filter_size=3):
 
 
 def sc_rulebook_build(coords, spatial_size, filter_size=2, stride=2):
+    """SC rule book; any d = len(spatial_size) in [1, 4] (coords n x (d + 1))."""
     coords = _dev_tensor(coords, "coords", torch.int32)
+    if len(spatial_size) != 3:
+        return _build_nd(coords, spatial_size, filter_size, stride, False)
     h = ctypes.c_void_p()
     with torch.cuda.device(coords.device):
         _check(lib().sc_rulebook_build(ctypes.c_void_p(coords.data_ptr()), coords.shape[0],
