@@ -191,6 +191,9 @@ __global__ __launch_bounds__(NW * 64) void k_gather_mma(
 // offsets reading as zero (used to mask lanes without branches).
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
 constexpr uint32_t kOobOffset = 0x70000000u;  // >= any buffer size accepted on this path
+// LDS bytes per row of a bf16 weight-part plane of the split row kernel
+// (32 channels = 64 bytes, padded against bank conflicts).
+constexpr int kSplitPitch = 80;
 
 __device__ __forceinline__ rsrc_t make_rsrc(const void* p, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
@@ -511,6 +514,78 @@ __global__ __launch_bounds__(256) void k_conv_quad(
   }
 }
 
+// ------------------------------------------------ fp32 as three bf16 terms
+// An fp32 value x splits exactly into x = hi + mid + lo, each a bfloat16:
+// hi keeps the leading 8 significant bits of x (truncated), mid the
+// leading 8 of the remainder x - hi, and lo what is left, which has at
+// most 8 significant bits (fp32 has 24).  A product x w is then the sum of
+// the nine products of the parts; the six with hi/mid/lo "orders" adding up
+// to at most 2 (hi hi, hi mid, mid hi, hi lo, mid mid, lo hi) keep every
+// term down to about 2^-23 |x w|, fp32's own rounding, and bf16 MFMAs
+// (16x16x32, exact products, fp32 accumulation) run them at 16 times the
+// fp32 MFMA rate of this chip: the fp32 contraction costs 6 bf16 MFMAs per
+// 32 reduction channels instead of 8 fp32 ones per 4.
+__device__ __forceinline__ void split3(float x, uint32_t& h, uint32_t& m, uint32_t& l) {
+  h = __float_as_uint(x) & 0xffff0000u;
+  const float r1 = x - __uint_as_float(h);  // exact: x and h share their leading bits
+  m = __float_as_uint(r1) & 0xffff0000u;
+  l = __float_as_uint(r1 - __uint_as_float(m));  // exact, and its low 16 bits are zero
+}
+
+// Two values' parts packed as bfloat16 pairs (element 0 in the low half).
+__device__ __forceinline__ uint32_t pack_hi16(uint32_t lo_elem, uint32_t hi_elem) {
+  return __builtin_amdgcn_perm(hi_elem, lo_elem, 0x07060302u);
+}
+
+// The three part vectors of 8 consecutive fp32 channels (as bf16x8 each).
+__device__ __forceinline__ void split8(const float (&v)[8], bf16x8& h8, bf16x8& m8, bf16x8& l8) {
+  uint32_t h[8], m[8], l[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) split3(v[i], h[i], m[i], l[i]);
+  uint4 a, b, c;
+  a.x = pack_hi16(h[0], h[1]); a.y = pack_hi16(h[2], h[3]); a.z = pack_hi16(h[4], h[5]); a.w = pack_hi16(h[6], h[7]);
+  b.x = pack_hi16(m[0], m[1]); b.y = pack_hi16(m[2], m[3]); b.z = pack_hi16(m[4], m[5]); b.w = pack_hi16(m[6], m[7]);
+  c.x = pack_hi16(l[0], l[1]); c.y = pack_hi16(l[2], l[3]); c.z = pack_hi16(l[4], l[5]); c.w = pack_hi16(l[6], l[7]);
+  h8 = __builtin_bit_cast(bf16x8, a);
+  m8 = __builtin_bit_cast(bf16x8, b);
+  l8 = __builtin_bit_cast(bf16x8, c);
+}
+
+// acc += a b^T over 32 reduction channels from the parts of both operands.
+__device__ __forceinline__ f32x4 mma_split(const bf16x8& ah, const bf16x8& am, const bf16x8& al, const bf16x8& bh,
+                                           const bf16x8& bm, const bf16x8& bl, f32x4 d) {
+  d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bl, d, 0, 0, 0);
+  d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, bm, d, 0, 0, 0);
+  d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bh, d, 0, 0, 0);
+  d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bm, d, 0, 0, 0);
+  d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, bh, d, 0, 0, 0);
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bh, d, 0, 0, 0);
+}
+
+// Weight parts for the split row kernel: planes[p][o][n][k] (p = hi, mid,
+// lo; bf16 bits) with n the output column and k the reduction channel of
+// the launch: TR (forward) reads W[o][k][n], else (dgrad) W[o][n][k].
+template <bool TR>
+__global__ void k_split_w(const float* __restrict__ W, int K, int kdim, int ncols, uint16_t* __restrict__ planes) {
+  const int64_t total = (int64_t)K * kdim * ncols;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+    float w;
+    if constexpr (TR) {
+      const int64_t o = i / ((int64_t)kdim * ncols);
+      const int64_t r = i - o * kdim * ncols;
+      const int n = (int)(r / kdim), k = (int)(r % kdim);
+      w = W[(o * kdim + k) * ncols + n];
+    } else {
+      w = W[i];
+    }
+    uint32_t h, m, l;
+    split3(w, h, m, l);
+    planes[i] = (uint16_t)(h >> 16);
+    planes[total + i] = (uint16_t)(m >> 16);
+    planes[2 * total + i] = (uint16_t)(l >> 16);
+  }
+}
+
 // ---------------------------------------------------- row-block kernel
 // Forward / dgrad over a row-block plan.  A workgroup owns one block of
 // kPlanRows = 64 output rows (rows whose offset sets are alike) and 16 NB
@@ -539,17 +614,26 @@ __global__ __launch_bounds__(256) void k_conv_quad(
 // a thread then loads 16 bytes of one reduction channel (4 output columns)
 // and writes them to the 4 columns' rows of the weight tile, which spares
 // the forward a transposed copy of W.
-template <typename T, int WB, int NB, int D, int PK, bool TB = false>
+// Bytes of one weight-tile buffer of the row kernel: COLS rows of the
+// step's window, or (SP) three planes of COLS rows of 32 bf16 channels.
+template <int WB, int NB, bool SP>
+constexpr int rows_b_bytes() {
+  return SP ? 3 * 16 * NB * kSplitPitch : 16 * NB * (WB + 16);
+}
+
+template <typename T, int WB, int NB, int D, int PK, bool TB = false, bool SP = false>
 __device__ __forceinline__ void conv_rows_block(
-    const T* __restrict__ X, uint32_t x_bytes, const T* __restrict__ B, uint32_t b_bytes,
+    const T* __restrict__ X, uint32_t x_bytes, const void* __restrict__ B, uint32_t b_bytes,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ b_first, const uint32_t* __restrict__ items,
     int64_t blk, int K, int mirror, int kdim, int ncols, const Heads<T>& Y, char (*As)[16 * (WB + 16)],
-    char (*Bs)[16 * NB * (WB + 16)], int tid, int wave, int lane, int m, int g, int col0) {
+    char (*Bs)[rows_b_bytes<WB, NB, SP>()], int tid, int wave, int lane, int m, int g, int col0) {
+  static_assert(!SP || (sizeof(T) == 4 && WB == 128 && PK == 1 && !TB), "split path: fp32, whole windows");
   constexpr int LPR = WB / 16;              // lanes per row window
   constexpr int RPI = 64 / LPR;             // rows per wavefront load
   constexpr int NA = 16 / RPI;              // row loads per wavefront and step
   constexpr int COLS = 16 * NB;             // output columns per workgroup
-  constexpr int NBP = (COLS * LPR + 255) / 256;  // weight pieces per thread and step
+  // weight pieces (16 bytes) per thread and step; SP: 3 planes x COLS rows x 4
+  constexpr int NBP = SP ? (3 * COLS * 4 + 255) / 256 : (COLS * LPR + 255) / 256;
   constexpr int PITCH = WB + 16;            // LDS bytes per row (bank spread)
   constexpr int S = WB / (32 * (int)sizeof(T));  // 32-channel MFMA groups per step
   const int first = b_first[blk];
@@ -559,7 +643,8 @@ __device__ __forceinline__ void conv_rows_block(
   // window (their products simply add up over the window's channels)
   const int ks_n = PK > 1 ? 1 : (int)((row_bytes + WB - 1) / WB);  // steps per item
   const int n_steps = PK > 1 ? (n_items + PK - 1) / PK : n_items * ks_n;
-  const uint32_t w_stride = (uint32_t)ncols * row_bytes;  // bytes per offset
+  // bytes per offset of B (SP: of one bf16 plane)
+  const uint32_t w_stride = (uint32_t)ncols * (SP ? (uint32_t)kdim * 2u : row_bytes);
   const rsrc_t rx = make_rsrc(X, x_bytes), rb = make_rsrc(B, b_bytes);
 
   f32x4 acc[NB];
@@ -581,7 +666,17 @@ __device__ __forceinline__ void conv_rows_block(
 #pragma unroll
     for (int q = 0; q < NBP; ++q) {
       const int p = tid + 256 * q;
-      if constexpr (TB) {
+      if constexpr (SP) {
+        // piece p: plane p / (4 COLS), column (p / 4) % COLS, channels 8 (p % 4) .. + 7
+        const int plane = p / (4 * COLS);
+        b_col[q] = plane * COLS + (p / 4) % COLS;  // row of the LDS tile (plane-major)
+        b_byte[q] = (uint32_t)(p % 4) * 16;        // within the plane row's 64-byte window
+        b_u[q] = 0;
+        const int col = col0 + (p / 4) % COLS;
+        b_base[q] = (plane < 3 && col < ncols)
+                        ? (uint32_t)plane * (uint32_t)K * w_stride + (uint32_t)col * (uint32_t)kdim * 2u
+                        : kOobOffset;
+      } else if constexpr (TB) {
         static_assert(PK == 1, "TB reads one item per step");
         constexpr int PPC = COLS / 4;  // 16-byte pieces per reduction channel
         const int ch = p / PPC;        // reduction channel within the window
@@ -672,10 +767,12 @@ __device__ __forceinline__ void conv_rows_block(
       }
 #pragma unroll
       for (int q = 0; q < NBP; ++q) {
-        const bool ok = live && win + b_byte[q] < row_bytes && b_base[q] != kOobOffset;
+        // SP: the window's 32 channels are 64 bytes of each bf16 plane row
+        const uint32_t bwin = SP ? win / 2u : win;
+        const bool ok = live && bwin + b_byte[q] < (SP ? (uint32_t)kdim * 2u : row_bytes) && b_base[q] != kOobOffset;
         // TB: row (win + b_byte) / sizeof(T) of the offset's kdim x ncols matrix
         const uint32_t off = TB ? (win + b_byte[q]) / (uint32_t)sizeof(T) * ((uint32_t)ncols * sizeof(T)) + b_base[q]
-                                : b_base[q] + win + b_byte[q];
+                                : b_base[q] + bwin + b_byte[q];
         const auto v = __builtin_amdgcn_raw_buffer_load_b128(rb, (int)(ok ? off : kOobOffset),
                                                              (int)((uint32_t)ow * w_stride), 0);
         gb[slot][q] = make_uint4(v[0], v[1], v[2], v[3]);
@@ -690,7 +787,10 @@ __device__ __forceinline__ void conv_rows_block(
         *reinterpret_cast<uint4*>(&As[wave][a_row[i] * PITCH + a_byte]) = ga[slot][i];
 #pragma unroll
       for (int q = 0; q < NBP; ++q) {
-        if constexpr (TB) {
+        if constexpr (SP) {
+          if (b_col[q] < 3 * COLS)
+            *reinterpret_cast<uint4*>(&Bs[buf][b_col[q] * kSplitPitch + b_byte[q]]) = gb[slot][q];
+        } else if constexpr (TB) {
           // 4 consecutive columns of one channel: one element in each column's row
           if (b_byte[q] >= (uint32_t)WB) continue;  // (never, when the pieces fill the threads exactly)
           char* dst = &Bs[buf][b_col[q] * PITCH + b_byte[q]];
@@ -714,6 +814,23 @@ __device__ __forceinline__ void conv_rows_block(
         ++mul_item;
       }
       if (skip) return;
+      if constexpr (SP) {
+        // the row tile's 8 channels of this lane, split; the weights' parts
+        // were split once, before the launch
+        Oct<float> a;
+        lds_oct(a, &As[wave][m * PITCH + 32 * g]);
+        bf16x8 ah, am, al;
+        split8(a.v, ah, am, al);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          const char* bp = &Bs[buf][(nb * 16 + m) * kSplitPitch + 16 * g];
+          const bf16x8 bh = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(bp));
+          const bf16x8 bm = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(bp + COLS * kSplitPitch));
+          const bf16x8 bl = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(bp + 2 * COLS * kSplitPitch));
+          acc[nb] = mma_split(ah, am, al, bh, bm, bl, acc[nb]);
+        }
+        return;
+      }
       Oct<T> a[S], b[S][NB];
 #pragma unroll
       for (int j = 0; j < S; ++j) {
@@ -818,9 +935,9 @@ __device__ __forceinline__ void conv_rows_block(
   }
 }
 
-template <typename T, int WB, int NB, int D, int PK, bool TB>
+template <typename T, int WB, int NB, int D, int PK, bool TB, bool SP>
 __device__ __forceinline__ void conv_rows_run(
-    const T* __restrict__ X, uint32_t x_bytes, const T* __restrict__ B, uint32_t b_bytes,
+    const T* __restrict__ X, uint32_t x_bytes, const void* __restrict__ B, uint32_t b_bytes,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ b_first, const int32_t* __restrict__ b_order,
     const uint32_t* __restrict__ items, int64_t n_blocks, int K, int mirror, int kdim, int ncols, const Heads<T>& Y) {
   constexpr int RPI = 64 / (WB / 16);       // rows per wavefront load
@@ -828,7 +945,7 @@ __device__ __forceinline__ void conv_rows_run(
   constexpr int PITCH = WB + 16;            // LDS bytes per row (bank spread)
   static_assert(WB / (32 * (int)sizeof(T)) >= 1 && 16 % RPI == 0, "window");
   __shared__ __attribute__((aligned(16))) char As[4][16 * PITCH];
-  __shared__ __attribute__((aligned(16))) char Bs[2][COLS * PITCH];
+  __shared__ __attribute__((aligned(16))) char Bs[2][rows_b_bytes<WB, NB, SP>()];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int m = lane & 15, g = lane >> 4;
@@ -857,29 +974,38 @@ __device__ __forceinline__ void conv_rows_run(
   }
   for (int64_t idx = wg, round = 0; idx < n_blocks; idx = next(++round)) {
     __syncthreads();  // the previous block's LDS is free
-    conv_rows_block<T, WB, NB, D, PK, TB>(X, x_bytes, B, b_bytes, perm, b_first, items, b_order[idx], K, mirror, kdim,
-                                  ncols, Y, As, Bs, tid, wave, lane, m, g, col0);
+    conv_rows_block<T, WB, NB, D, PK, TB, SP>(X, x_bytes, B, b_bytes, perm, b_first, items, b_order[idx], K, mirror,
+                                              kdim, ncols, Y, As, Bs, tid, wave, lane, m, g, col0);
   }
 }
 
 #define SSCN_ROWS_ARGS                                                                                          \
-  const T *__restrict__ X, uint32_t x_bytes, const T *__restrict__ B, uint32_t b_bytes,                        \
+  const T *__restrict__ X, uint32_t x_bytes, const void *__restrict__ B, uint32_t b_bytes,                     \
       const int32_t *__restrict__ perm, const int32_t *__restrict__ b_first, const int32_t *__restrict__ b_order, \
       const uint32_t *__restrict__ items, int64_t n_blocks, int K, int mirror, int kdim, int ncols, Heads<T> Y
 
-// Forward (and DC) launches.
-template <typename T, int WB, int NB, int D, int PK, bool TB = false>
-__global__ __launch_bounds__(256, WB == 64 ? 6 : 5) void k_conv_rows(SSCN_ROWS_ARGS) {
-  conv_rows_run<T, WB, NB, D, PK, TB>(X, x_bytes, B, b_bytes, perm, b_first, b_order, items, n_blocks, K, mirror,
-                                      kdim, ncols, Y);
+// Forward (and DC) launches.  SP: fp32 through bf16 parts (B holds the
+// weight planes of k_split_w).
+// Resident workgroups per CU the row kernel is compiled for (its LDS and
+// registers): 6 for 64-byte windows, 5 for 128-byte ones, 4 for the split
+// path (its three weight planes take 40 KB of LDS).
+template <int WB, bool SP>
+constexpr int rows_min_blocks() {
+  return SP ? 4 : (WB == 64 ? 6 : 5);
+}
+
+template <typename T, int WB, int NB, int D, int PK, bool TB = false, bool SP = false>
+__global__ __launch_bounds__(256, (rows_min_blocks<WB, SP>())) void k_conv_rows(SSCN_ROWS_ARGS) {
+  conv_rows_run<T, WB, NB, D, PK, TB, SP>(X, x_bytes, B, b_bytes, perm, b_first, b_order, items, n_blocks, K, mirror,
+                                          kdim, ncols, Y);
 }
 
 // The dgrad launches of sparse_conv_backward: the same kernel under its own
 // name, so that kernel traces tell the two directions apart.
-template <typename T, int WB, int NB, int D, int PK, bool TB = false>
-__global__ __launch_bounds__(256, WB == 64 ? 6 : 5) void k_dgrad_rows(SSCN_ROWS_ARGS) {
-  conv_rows_run<T, WB, NB, D, PK, TB>(X, x_bytes, B, b_bytes, perm, b_first, b_order, items, n_blocks, K, mirror,
-                                      kdim, ncols, Y);
+template <typename T, int WB, int NB, int D, int PK, bool TB = false, bool SP = false>
+__global__ __launch_bounds__(256, (rows_min_blocks<WB, SP>())) void k_dgrad_rows(SSCN_ROWS_ARGS) {
+  conv_rows_run<T, WB, NB, D, PK, TB, SP>(X, x_bytes, B, b_bytes, perm, b_first, b_order, items, n_blocks, K, mirror,
+                                          kdim, ncols, Y);
 }
 #undef SSCN_ROWS_ARGS
 
@@ -1501,20 +1627,21 @@ static bool rows_eligible(const View& v, int kdim, int ncols) {
          std::max(v.n_in, v.n_out) < (int64_t)kPlanNoRow && ceil_div(v.n_out, kPlanRows) * v.K < INT32_MAX;
 }
 
-template <typename T, int WB, int NB, int PK = 1, bool TB = false, bool DG = false>
-static sscn_status launch_rows_nb(const T* X, const T* B, const View& v, int kdim, int ncols, const Heads<T>& Y,
+template <typename T, int WB, int NB, int PK = 1, bool TB = false, bool DG = false, bool SP = false>
+static sscn_status launch_rows_nb(const T* X, const void* B, const View& v, int kdim, int ncols, const Heads<T>& Y,
                                   hipStream_t s) {
   const int64_t nb = v.st->n_blocks;
   if (nb == 0) return Y.n_zero > 0 ? fill_f32(Y.zero, 0.f, Y.n_zero, s) : SSCN_OK;
   const int gy = (ncols + 16 * NB - 1) / (16 * NB);
   const uint32_t xb = (uint32_t)((uint64_t)std::max<int64_t>(v.n_in, 1) * kdim * sizeof(T));
-  const uint32_t bb = (uint32_t)((uint64_t)v.K * ncols * kdim * sizeof(T));
+  // SP: three bf16 planes
+  const uint32_t bb = (uint32_t)((uint64_t)v.K * ncols * kdim * (SP ? 6 : sizeof(T)));
   // loads two steps ahead for 64-byte windows (short steps), one otherwise;
   // six workgroups per CU for 64-byte windows (80 VGPRs), five otherwise
   constexpr int D = WB == 64 ? 3 : 2;
   auto kern = [] {
-    if constexpr (DG) return k_dgrad_rows<T, WB, NB, D, PK, TB>;
-    else return k_conv_rows<T, WB, NB, D, PK, TB>;
+    if constexpr (DG) return k_dgrad_rows<T, WB, NB, D, PK, TB, SP>;
+    else return k_conv_rows<T, WB, NB, D, PK, TB, SP>;
   }();
   int cus = 256, per_cu = 1;
   occupancy((const void*)kern, 256, 0, &per_cu, &cus);
@@ -1537,12 +1664,26 @@ static bool rows_take_untransposed(int kdim, int ncols) {
   return sizeof(T) == 4 && ncols % 4 == 0 && ncols % 64 != 0 && kdim * sizeof(T) != 64;
 }
 
+// Whether an fp32 launch of the row kernel runs through bf16 parts (the
+// weights handed over as the three planes of k_split_w): whole 32-channel
+// windows (rows of 16 channels pair two items per window instead), and
+// the planes within 32-bit buffer offsets.
+static bool rows_split(const View& v, int kdim, int ncols) {
+  return kdim >= 32 && kdim * 4 != 64 && (uint64_t)v.K * ncols * kdim * 6 < kOobOffset;
+}
+
 // DG: a dgrad launch (k_dgrad_rows), else a forward one (k_conv_rows).
-template <typename T, bool DG = false>
-static sscn_status launch_rows(const T* X, const T* B, const View& v, int kdim, int ncols, const Heads<T>& Y,
+// SP: fp32 through bf16 parts, B = the weight planes.
+template <typename T, bool DG = false, bool SP = false>
+static sscn_status launch_rows(const T* X, const void* B, const View& v, int kdim, int ncols, const Heads<T>& Y,
                                hipStream_t s, bool untransposed = false) {
   if (v.n_out == 0) return Y.n_zero > 0 ? fill_f32(Y.zero, 0.f, Y.n_zero, s) : SSCN_OK;
   SSCN_TRY(ensure_plan(v, s));
+  if constexpr (SP) {
+    static_assert(sizeof(T) == 4, "split path: fp32");
+    return ncols % 64 == 0 ? launch_rows_nb<T, 128, 4, 1, false, DG, true>(X, B, v, kdim, ncols, Y, s)
+                           : launch_rows_nb<T, 128, 2, 1, false, DG, true>(X, B, v, kdim, ncols, Y, s);
+  }
   // 64 output columns per workgroup when they divide the width, else 32;
   // for bf16 (bound by loads and step latency rather than MFMAs) 64 unless
   // the width is at most 32: fewer column groups re-read the input rows
@@ -1841,6 +1982,20 @@ template <typename T>
 static sscn_status forward_t(const T* X, const T* W, const View& v, int cin, int cout, const Heads<T>& Y, hipStream_t s) {
   if (rows_eligible<T>(v, cin, cout)) {
     if (v.n_out == 0) return SSCN_OK;
+    if constexpr (sizeof(T) == 4) {
+      if (rows_split(v, cin, cout)) {
+        const int64_t total = (int64_t)v.K * cin * cout;
+        uint16_t* planes = nullptr;
+        SSCN_TRY(temp_weights(&planes, 3 * total, s));
+        k_split_w<true><<<(unsigned)std::min<int64_t>(ceil_div(total, 256), 4096), 256, 0, s>>>(W, v.K, cin, cout,
+                                                                                               planes);
+        hipError_t e = hipGetLastError();
+        sscn_status st = e == hipSuccess ? launch_rows<T, false, true>(X, planes, v, cin, cout, Y, s)
+                                         : hip_fail(e, "weight split");
+        temp_release(planes, s);
+        return st;
+      }
+    }
     if (rows_take_untransposed<T>(cin, cout)) return launch_rows<T>(X, W, v, cin, cout, Y, s, true);
     const int64_t total = (int64_t)v.K * cin * cout;
     T* Bt = nullptr;
@@ -1978,7 +2133,19 @@ extern "C" sscn_status sparse_conv_backward(const void* features, const void* we
       Heads<float> h = plain_heads((float*)dgrad, c_in);
       if (rows_eligible<float>(vt, c_out, c_in)) {
         if (wgrad) { h.zero = wgrad; h.n_zero = w_total; w_zeroed = true; }
-        st = launch_rows<float, true>((const float*)dout, (const float*)weights, vt, c_out, c_in, h, stream);
+        if (rows_split(vt, c_out, c_in)) {
+          // B[o][ci][co] = W[o][ci][co] as stored, in parts
+          uint16_t* planes = nullptr;
+          SSCN_TRY(temp_weights(&planes, 3 * w_total, stream));
+          k_split_w<false><<<(unsigned)std::min<int64_t>(ceil_div(w_total, 256), 4096), 256, 0, stream>>>(
+              (const float*)weights, vt.K, c_out, c_in, planes);
+          hipError_t e = hipGetLastError();
+          st = e == hipSuccess ? launch_rows<float, true, true>((const float*)dout, planes, vt, c_out, c_in, h, stream)
+                               : hip_fail(e, "weight split");
+          temp_release(planes, stream);
+        } else {
+          st = launch_rows<float, true>((const float*)dout, (const float*)weights, vt, c_out, c_in, h, stream);
+        }
       } else {
         st = launch_conv<float, true>((const float*)dout, (const float*)weights, vt, c_out, c_in, h, stream);
       }
@@ -2053,7 +2220,8 @@ extern "C" sscn_status sparse_conv_forward_noalloc(const void* features, const v
   sscn_status st = check_conv_args(rb, c_in, c_out, dtype);
   if (st != SSCN_OK) return st;
   const View v = view_of(rb);
-  const size_t w_bytes = (size_t)v.K * c_in * c_out * (dtype == SSCN_F32 ? 4 : 2);
+  // the weight copy: fp32 in three bf16 parts (6 bytes per weight), bf16 as is
+  const size_t w_bytes = (size_t)v.K * c_in * c_out * (dtype == SSCN_F32 ? 6 : 2);
   if (w_bytes > kScratchBytes)
     return fail(SSCN_ERR_INVALID_ARG, "weights of " + std::to_string(w_bytes) + " bytes exceed the " +
                                           std::to_string(kScratchBytes) + "-byte scratch region of the "
