@@ -1751,6 +1751,8 @@ template <int N> struct RowLoad<bf16_t, N> {
 // pairs in that range evenly (sub[o] ~ pairs of o / mean pairs per offset,
 // so that items have similar sizes).  first[o] = sum of sub[q], q < o.
 constexpr int kWgradMaxK = 128;
+// wgrad on 16x16x32 bf16 MFMAs (see k_wgrad_ring)
+constexpr bool kWgradM32 = true;
 struct WgradItems {
   int32_t first[kWgradMaxK + 1];
 };
@@ -1766,7 +1768,16 @@ struct WgradItems {
 // past the end reads out-of-range offsets, i.e. zeros), so the compiler's
 // wait counts stay exact; a wave's last batch is padded with such empty
 // steps.  Needs X and dY below kOobOffset bytes.
-template <typename T, int CA, int CB, int R>
+// M32: 16x16x32 bf16 MFMAs instead of 16x16x4 fp32 ones.  Such an MFMA
+// takes 8 reduction values per lane; here the reduction runs over the
+// pairs, and 8 consecutive steps give lane (m, g) the pairs 4 s + g, s < 8,
+// of its channel -- exactly the operand layout (lane group g, element s),
+// with the B lanes of group g holding the same 8 pairs.  So the values of 8
+// steps are packed (bf16 in the high half of each 32-bit word, two words per
+// register) and multiplied once per 8 steps.  bf16 inputs enter as they are
+// (exact products); fp32 inputs are split into three bf16 parts and take
+// six MFMAs (as in the row kernel).
+template <typename T, int CA, int CB, int R, bool M32 = false>
 __global__ __launch_bounds__(256) void k_wgrad_ring(const T* __restrict__ X, uint32_t x_bytes,
                                                     const T* __restrict__ dY, uint32_t y_bytes,
                                                     const int64_t* __restrict__ seg, int64_t n_tiles,
@@ -1829,6 +1840,14 @@ __global__ __launch_bounds__(256) void k_wgrad_ring(const T* __restrict__ X, uin
       RowLoad<T, CB>::load(ry, yo + b_lane, yb[ds]);
     };
     const int n_steps = (n_mine + 3) / 4;
+    // M32: planes of the packed operands (3 for fp32 parts, 1 for bf16)
+    constexpr int NP = sizeof(T) == 4 ? 3 : 1;
+    uint32_t pa[M32 ? NP : 1][CA][4], pb[M32 ? NP : 1][CB][4];  // 8 steps, two per register
+    uint32_t ea[M32 ? NP : 1][CA], eb[M32 ? NP : 1][CB];        // the even step's words
+    auto words = [&](float v, uint32_t (&w)[M32 ? NP : 1]) {
+      if constexpr (NP == 3) split3(v, w[0], w[1], w[2]);
+      else w[0] = __float_as_uint(v);  // a bf16 value: its bits in the high half
+    };
     load_batch(wb, 0);
     load_batch(wb + 64, 1);
 #pragma unroll
@@ -1838,11 +1857,61 @@ __global__ __launch_bounds__(256) void k_wgrad_ring(const T* __restrict__ X, uin
 #pragma unroll
       for (int s16 = 0; s16 < 16; ++s16) {
         const int ds = s16 % R;
+        if constexpr (M32) {
+          const int e = s16 % 8;  // element of the group's operands
 #pragma unroll
-        for (int a = 0; a < CA; ++a)
+          for (int a = 0; a < CA; ++a) {
+            uint32_t w[NP];
+            words(xa[ds][a], w);
 #pragma unroll
-          for (int b = 0; b < CB; ++b)
-            d[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(xa[ds][a], yb[ds][b], d[a][b], 0, 0, 0);
+            for (int pl = 0; pl < NP; ++pl) {
+              if (e % 2 == 0) ea[pl][a] = w[pl];
+              else pa[pl][a][e / 2] = pack_hi16(ea[pl][a], w[pl]);
+            }
+          }
+#pragma unroll
+          for (int b = 0; b < CB; ++b) {
+            uint32_t w[NP];
+            words(yb[ds][b], w);
+#pragma unroll
+            for (int pl = 0; pl < NP; ++pl) {
+              if (e % 2 == 0) eb[pl][b] = w[pl];
+              else pb[pl][b][e / 2] = pack_hi16(eb[pl][b], w[pl]);
+            }
+          }
+          if (e == 7) {
+            auto op = [](const uint32_t (&q)[4]) {
+              uint4 u;
+              u.x = q[0]; u.y = q[1]; u.z = q[2]; u.w = q[3];
+              return __builtin_bit_cast(bf16x8, u);
+            };
+            if constexpr (NP == 3) {
+              // the six part products, smallest first; one pass over all
+              // blocks per product keeps the accumulator chains apart
+              constexpr int PA[6] = {0, 1, 2, 0, 1, 0}, PB[6] = {2, 1, 0, 1, 0, 0};
+#pragma unroll
+              for (int pr = 0; pr < 6; ++pr)
+#pragma unroll
+                for (int a = 0; a < CA; ++a)
+#pragma unroll
+                  for (int b = 0; b < CB; ++b)
+                    d[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(op(pa[PA[pr]][a]), op(pb[PB[pr]][b]), d[a][b],
+                                                                      0, 0, 0);
+            } else {
+#pragma unroll
+              for (int a = 0; a < CA; ++a)
+#pragma unroll
+                for (int b = 0; b < CB; ++b)
+                  d[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(op(pa[0][a]), op(pb[0][b]), d[a][b], 0, 0, 0);
+            }
+          }
+        } else {
+#pragma unroll
+          for (int a = 0; a < CA; ++a)
+#pragma unroll
+            for (int b = 0; b < CB; ++b)
+              d[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(xa[ds][a], yb[ds][b], d[a][b], 0, 0, 0);
+        }
         const int nx = s16 + R;  // step to request, relative to this batch
         if (nx < 16)
           fetch_rows(b0 + nx, 0, nx, ds);
@@ -1915,7 +1984,7 @@ static sscn_status launch_wgrad_reg(bool zeroed, const T* X, const T* dY, const 
       items.first[o + 1] = items.first[o] + std::max(1, (int)(p / mean + 0.5));
     }
     const int S = items.first[v.K];
-    auto kern = k_wgrad_ring<T, CA, CB, 4>;
+    auto kern = k_wgrad_ring<T, CA, CB, 4, kWgradM32>;
     int cus = 256, per_cu = 1;
     occupancy((const void*)kern, 256, 0, &per_cu, &cus);
     const int64_t target = std::max<int64_t>(1, (int64_t)cus * per_cu / (nzc * nzo));
