@@ -12,11 +12,12 @@ in HBM before the timed region.  value = active sites / s over whole steps.
 
 Dominant kernel: the row-block kernel, launched once by the forward
 (k_conv_rows) and once by the dgrad (k_dgrad_rows, the same code under its
-own name).  Its duration is measured inside the timed steps with a pair of
-HIP events around every dgrad launch (the dgrad is its own call there, so
-the pair brackets exactly that one kernel on its stream); `roofline`
-divides the useful flops of one launch (2 C_in C_out per pair, Table 2) by
-the mean of those durations.  `traffic` (HBM bytes per launch) comes from
+own name).  Its duration is measured inside the timed steps: before each
+step's backward call the library is asked (sscn_time_next_launch) to
+record a pair of HIP events around its next row-block launch, which is the
+dgrad kernel, on its stream (the small weight-split kernel queued before it
+stays outside the pair); `roofline` divides the useful flops of one launch
+(2 C_in C_out per pair, Table 2) by the mean of those durations.  `traffic` (HBM bytes per launch) comes from
 the committed counter record in profiles/ and is null when the kernel
 source has changed since those counters were taken.  `build_roofline` puts
 the SSC build's algorithmic bytes over its wall time against HBM bandwidth;
@@ -55,7 +56,7 @@ PEAK_HBM_GBS = 8000.0
 METRIC = "SSC 3^3 layer active-sites/s + effective TFLOP/s; rulebook build ms"
 KERNEL_SRC = os.path.join(ROOT, "paper_1711_10275_amd", "csrc", "conv.hip")
 TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "k_dgrad_rows_ssc128_c64_traffic.json")
-DOMINANT = "k_dgrad_rows<float, 128, 4, 2, 1, false>"
+DOMINANT = "k_dgrad_rows<float, 128, 4, 2, 1, false, true>"
 MEASURE_LIB = os.path.join(ROOT, "paper_1711_10275_amd", "libsscn_measure.so")
 
 
@@ -280,31 +281,26 @@ def main():
     tc = torch.from_numpy(coords).to(dev)
     tX, tW, tG = (torch.from_numpy(a).to(dev) for a in (X, W, G))
     stream = torch.cuda.current_stream(dev)
-    dgrad_events = []
+    timers = [sscn.KernelTimer() for _ in range(args.steps)]
 
-    def step(tc=tc, tX=tX, tG=tG, record=False):
+    def step(tc=tc, tX=tX, tG=tG, timer=None):
         rb = sscn.ssc_rulebook_build(tc, size, 3)
         sscn.sparse_conv_forward(tX, tW, rb)
-        if record:
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-        sscn.sparse_conv_backward(None, tW, tG, rb, dgrad=True, wgrad=False)
-        if record:
-            e1.record(stream)
-            dgrad_events.append((e0, e1))
-        sscn.sparse_conv_backward(tX, tW, tG, rb, dgrad=False, wgrad=True)
+        if timer is not None:
+            timer.arm()  # the backward's first row-block launch: the dgrad kernel
+        sscn.sparse_conv_backward(tX, tW, tG, rb)
         return rb
 
     for _ in range(args.warmup):
         rb = step()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        rb = step(record=True)
+    for i in range(args.steps):
+        rb = step(timer=timers[i])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / args.steps
-    launch_ms = sum(a.elapsed_time(b) for a, b in dgrad_events) / len(dgrad_events)
+    launch_ms = sum(t.ms() for t in timers) / len(timers)
     pairs = rb.n_pairs
     flops_layer = 2.0 * cin * cout * pairs  # useful flops of one pass (fwd, dgrad or wgrad)
 
@@ -357,10 +353,10 @@ def main():
         "bf16": {"forward_ms": fwd_bf16_ms, "dgrad_ms": dgrad_bf16_ms, "wgrad_ms": wgrad_bf16_ms,
                  "forward_tflops": flops_layer / (fwd_bf16_ms * 1e-3) / 1e12},
         "roofline": {"kernel": DOMINANT + " (the dgrad launch of the row-block kernel; the forward launches "
-                               "the same code as k_conv_rows)",
+                               "the same code as k_conv_rows; fp32 through three bf16 parts on 16x16x32 MFMAs)",
                      "bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_MFMA_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_FP32_MFMA_TFLOPS,
-                     "launch_ms": launch_ms, "launches_timed": len(dgrad_events),
+                     "launch_ms": launch_ms, "launches_timed": len(timers),
                      "flops_per_launch": flops_layer, "traffic": recorded_traffic()},
         "build_roofline": build_roofline(int(n), 27, int(pairs), build_ms,
                                          "SSC 3^3 rule-book build incl. its row-block plan, 100k sites"),

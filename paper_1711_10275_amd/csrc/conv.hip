@@ -895,11 +895,17 @@ __device__ __forceinline__ void conv_rows_block(
         const float sc = ok && Y.scale[h] ? Y.scale[h][col] : 1.f;
         const float sh = ok && Y.scale[h] ? Y.shift[h][col] : 0.f;
         const float bi = ok && Y.bias ? Y.bias[col] : 0.f;
+        float rv[4] = {0.f, 0.f, 0.f, 0.f};
+        if (Y.res) {  // uniform: layers without a residual skip the row reads
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int32_t rrow = wrows[4 * g + r];
+            if (ok && rrow >= 0) rv[r] = Elem<T>::load(Y.res + rrow * Y.res_ld + col);
+          }
+        }
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int32_t rrow = wrows[4 * g + r];
-          const float y = acc[nb][r] + bi +
-                          (Y.res && ok && rrow >= 0 ? Elem<T>::load(Y.res + rrow * Y.res_ld + col) : 0.f);
+          const float y = acc[nb][r] + bi + rv[r];
           const float v = Y.scale[h] ? fmaxf(0.f, y * sc + sh) : y;
           Elem<T>::store(reinterpret_cast<T*>(tile + (4 * g + r) * RB) + nb * 16 + m, v);
         }
@@ -1647,8 +1653,10 @@ static sscn_status launch_rows_nb(const T* X, const void* B, const View& v, int 
   occupancy((const void*)kern, 256, 0, &per_cu, &cus);
   // persistent: one resident wave of workgroups per column group
   const int64_t gx = std::min<int64_t>(nb, std::max<int64_t>(1, (int64_t)cus * per_cu / gy));
+  timed_launch_begin(s);
   kern<<<dim3((unsigned)gx, (unsigned)gy), 256, 0, s>>>(X, xb, B, bb, v.st->perm, v.st->b_first, v.st->b_order,
                                                          v.st->items, nb, v.K, v.mirror ? 1 : 0, kdim, ncols, Y);
+  timed_launch_end(s);
   SSCN_HIP(hipGetLastError());
   return SSCN_OK;
 }
@@ -1994,9 +2002,11 @@ static sscn_status launch_wgrad_reg(bool zeroed, const T* X, const T* dY, const 
     const int64_t tr2 = std::max<int64_t>(1, ceil_div(v.st->n_tiles, ranges));
     const int64_t total = ceil_div(v.st->n_tiles, tr2) * S;
     if (!zeroed) SSCN_TRY(fill_f32(dW, 0.f, (int64_t)v.K * cin * cout, s));
+    timed_launch_begin(s);
     kern<<<dim3((unsigned)total, (unsigned)(nzc * nzo)), 256, 0, s>>>(
         X, (uint32_t)x_bytes, dY, (uint32_t)y_bytes, v.st->seg, v.st->n_tiles, v.st->in_rows, v.st->out_rows, v.K,
         v.mirror ? 1 : 0, cin, cout, (int)tr2, items, nzc, dW);
+    timed_launch_end(s);
     SSCN_HIP(hipGetLastError());
     return SSCN_OK;
   }

@@ -79,6 +79,13 @@ struct NoAlloc {
 const NoAlloc* no_alloc();
 void set_no_alloc(const NoAlloc* na);
 
+// Events the caller asked to have recorded around the next launch of a
+// row-block or wgrad kernel on this thread (sscn_time_next_launch); the
+// launch records `before` just ahead of the kernel and `after` just behind
+// it, on the kernel's stream, and clears the request.
+void timed_launch_begin(hipStream_t s);
+void timed_launch_end(hipStream_t s);
+
 // One direction of a rule book: tiles over the output rows of that
 // direction, offset-major segments, and the pair arrays (pointers into the
 // rule book's device blocks).

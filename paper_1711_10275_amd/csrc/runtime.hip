@@ -101,6 +101,24 @@ sscn_status dev_alloc(void** p, size_t bytes, hipStream_t s) {
   return SSCN_OK;
 }
 
+static thread_local hipEvent_t t_time_before = nullptr, t_time_after = nullptr;
+static thread_local bool t_time_armed = false;
+
+void timed_launch_begin(hipStream_t s) {
+  if (t_time_before && !t_time_armed) {
+    (void)hipEventRecord(t_time_before, s);
+    t_time_armed = true;
+  }
+}
+
+void timed_launch_end(hipStream_t s) {
+  if (t_time_armed) {
+    (void)hipEventRecord(t_time_after, s);
+    t_time_before = t_time_after = nullptr;
+    t_time_armed = false;
+  }
+}
+
 static thread_local const NoAlloc* t_no_alloc = nullptr;
 const NoAlloc* no_alloc() { return t_no_alloc; }
 void set_no_alloc(const NoAlloc* na) { t_no_alloc = na; }
@@ -337,6 +355,15 @@ sscn_status exclusive_scan_i32(const int32_t* in, int32_t* out, int64_t count, h
 }  // namespace sscn
 
 extern "C" const char* sscn_last_error(void) { return sscn::g_last_error.c_str(); }
+
+extern "C" sscn_status sscn_time_next_launch(hipEvent_t before, hipEvent_t after) {
+  if ((before == nullptr) != (after == nullptr))
+    return sscn::fail(SSCN_ERR_INVALID_ARG, "both events or neither");
+  sscn::t_time_before = before;
+  sscn::t_time_after = after;
+  sscn::t_time_armed = false;
+  return SSCN_OK;
+}
 
 extern "C" sscn_status sscn_release_cached(void) {
   int dev = 0;

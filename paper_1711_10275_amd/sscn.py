@@ -79,6 +79,7 @@ _SIGS = {
     "sscn_add": [_vp, _i64, _vp, _i64, _i64, _i32, ctypes.c_int, _vp, _i64, _vp],
     "sscn_softmax_nll": [_vp, _i64, _i32, ctypes.c_int, _vp, _vp, _vp, _vp],
     "sscn_sgd_nesterov": [_vp, _vp, _vp, _i64, ctypes.c_float, ctypes.c_float, ctypes.c_float, _vp, _vp],
+    "sscn_time_next_launch": [_vp, _vp],
     "sscn_release_cached": [],
     "sscn_last_error": [],
 }
@@ -604,3 +605,39 @@ def sgd_nesterov_(params, grads, buf, lr, momentum=0.9, weight_decay=1e-4, param
     with torch.cuda.device(params.device):
         _check(lib().sscn_sgd_nesterov(_vp_of(params), _vp_of(grads), _vp_of(buf), params.numel(), lr, momentum,
                                        weight_decay, _vp_of(params_bf16), _stream(params)))
+
+
+# ------------------------------------------------------------- measurement
+class KernelTimer:
+    """HIP events recorded by the library around the next row-block or wgrad
+    kernel launched from this thread (sscn_time_next_launch): arm() before
+    the call, ms() after synchronising."""
+
+    def __init__(self):
+        self._hip = ctypes.CDLL("libamdhip64.so")
+        self._hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self._hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self._hip.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        self._hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.before, self.after = ctypes.c_void_p(), ctypes.c_void_p()
+        for e in (self.before, self.after):
+            if self._hip.hipEventCreate(ctypes.byref(e)) != 0:
+                raise RuntimeError("hipEventCreate failed")
+
+    def arm(self):
+        _check(lib().sscn_time_next_launch(self.before, self.after))
+
+    def ms(self):
+        if self._hip.hipEventSynchronize(self.after) != 0:
+            raise RuntimeError("hipEventSynchronize failed")
+        t = ctypes.c_float()
+        if self._hip.hipEventElapsedTime(ctypes.byref(t), self.before, self.after) != 0:
+            raise RuntimeError("hipEventElapsedTime failed (was a kernel launched after arm()?)")
+        return t.value
+
+    def __del__(self):
+        try:
+            for e in (self.before, self.after):
+                self._hip.hipEventDestroy(e)
+        except Exception:
+            pass

@@ -7,7 +7,7 @@ from oracle import sscn_oracle as O
 from paper_1711_10275_amd import blocks, sscn
 from paper_1711_10275_amd import synthetic as S
 from tests.gpu_common import coords_for, dev, host, small_set
-from tests.parity import assert_close
+from tests.parity import assert_close, assert_close_head
 
 pytestmark = pytest.mark.gpu
 
@@ -45,7 +45,7 @@ def test_forward_bias_and_residual(kind, cin, cout, dtype):
                                    bias=dev(bias), residual=dev(res, TD[dtype]))
     ref = O.forward_bias(X, W, bias, orb) + res
     assert_close(host(plain), ref, dtype, "bias + residual")
-    assert_close(host(act), O.affine_relu(ref, scale, shift), dtype, "activated head")
+    assert_close_head(host(act), ref, scale, shift, dtype, "activated head")
 
 
 def _params(c, seed, bf16):

@@ -11,7 +11,7 @@ from oracle import sscn_oracle as O
 from paper_1711_10275_amd import sscn
 from paper_1711_10275_amd import synthetic as S
 from tests.gpu_common import coords_for, dev, host, small_set
-from tests.parity import assert_close
+from tests.parity import assert_close, assert_close_head
 
 pytestmark = pytest.mark.gpu
 
@@ -206,7 +206,7 @@ def _heads_case(rb, orb, cin, cout, dtype, seed):
                                    [(wide[:, cout:2 * cout], dev(scale), dev(shift)), (plain, None, None)])
     ref = O.forward(X, W, orb)
     got = host(wide)
-    assert_close(got[:, cout:2 * cout], O.affine_relu(ref, scale, shift), dtype, "activated head")
+    assert_close_head(got[:, cout:2 * cout], ref, scale, shift, dtype, "activated head")
     assert_close(host(plain), ref, dtype, "plain head")
     assert np.all(got[:, :cout] == 7.0) and np.all(got[:, 2 * cout:] == 7.0), "writes outside the head"
 

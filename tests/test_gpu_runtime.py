@@ -65,3 +65,25 @@ def test_affine_relu_rejects_bad_out():
         sscn.affine_relu(x, s, s, out=torch.empty((10, 3), device="cuda:0"))
     with pytest.raises(ValueError):
         sscn.affine_relu(x, torch.ones(4), s)
+
+
+def test_kernel_timer_brackets_the_row_kernel():
+    """sscn_time_next_launch: the armed events bracket the next row-block
+    launch only (a forward's weight copy stays outside), once."""
+    coords, size = coords_for("shapes128")
+    rb = sscn.ssc_rulebook_build(dev(coords), size, 3)
+    X, W = dev(S.features(coords.shape[0], 64, 95)), dev(S.weights(27, 64, 64, 96))
+    sscn.sparse_conv_forward(X, W, rb)
+    t = sscn.KernelTimer()
+    t.arm()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    sscn.sparse_conv_forward(X, W, rb)
+    e1.record()
+    torch.cuda.synchronize()
+    kernel_ms, call_ms = t.ms(), e0.elapsed_time(e1)
+    assert 0.0 < kernel_ms <= call_ms
+    # used once: a later call leaves the events where they were
+    sscn.sparse_conv_forward(X, W, rb)
+    torch.cuda.synchronize()
+    assert t.ms() == kernel_ms

@@ -20,7 +20,7 @@ from oracle import sscn_oracle as O
 from paper_1711_10275_amd import sscn, unet
 from paper_1711_10275_amd import synthetic as S
 from tests.gpu_common import assert_same_rulebook, dev, host, oracle_levels
-from tests.parity import assert_close
+from tests.parity import assert_close, assert_close_head
 
 pytestmark = pytest.mark.gpu
 
@@ -73,8 +73,11 @@ def _teacher_forced(trace, levels, dtype, rows=None, seed=0, fused=True, full_le
         for i, (dest, hs, hb) in enumerate(outs):
             got = host(dest)
             assert got.shape == (rb.n_out, u.cout), u.name
-            want = ref if hs is None else O.affine_relu(ref, host(hs), host(hb))
-            assert_close(got if pick is None else got[pick], want, dtype, f"{u.name} head {i}")
+            g = got if pick is None else got[pick]
+            if hs is None:
+                assert_close(g, ref, dtype, f"{u.name} head {i}")
+            else:
+                assert_close_head(g, ref, host(hs), host(hb), dtype, f"{u.name} head {i}")
 
 
 @pytest.mark.parametrize("fused", [True, False], ids=["fused", "unfused"])
