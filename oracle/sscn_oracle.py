@@ -34,7 +34,13 @@ notes of the repository):
 * (L - f) must be divisible by s and L >= f (else a shape error);
 * the batch index is part of the location, so samples never interact;
 * two rows at one location is an error (one row per active site);
-* ground state 0, no bias.
+* ground state 0; a bias term, where a layer has one, is added to every
+  active output row (inactive sites are not stored);
+* MP ties go to the smallest offset; AP divides by f^d whatever the number
+  of active inputs; nearest-neighbour upsampling inverts an SC(s, s);
+* batch normalisation in training form normalises with the biased variance
+  over the active rows (eps 1e-5) and keeps running statistics with
+  momentum 0.1 and the unbiased variance.
 
 Only numpy is used; the dictionary is a sorted key array searched with
 numpy.searchsorted, and each per-offset product is one numpy matmul.

@@ -4,8 +4,8 @@
 // upsamples by nearest neighbour).  All of them, and their gradients, are
 // reductions over the pairs of a rule book direction:
 //
-//   AP forward      sum over the SC direction, scale f^-3
-//   AP backward     sum over the transposed direction, scale f^-3
+//   AP forward      sum over the SC direction, scale f^-d (1 / K)
+//   AP backward     sum over the transposed direction, scale f^-d
 //   MP forward      max over the SC direction (records the winning offset)
 //   MP backward     over the transposed direction: the gradient of an
 //                   output element goes to the input at its winning offset

@@ -13,6 +13,7 @@ output into the committed summaries:
                                              contraction kernels
   rulebook_build_scenes256_traffic.txt       per-kernel time and traffic of the
                                              SSC and SC builds at about 2M sites
+  bench_all_workloads_kernel_stats.txt       kernel trace of a whole bench.py run
 
 Calibration: a plain copy of B bytes (the measure library's k_copy) should
 read B and write B; FETCH_SIZE and WRITE_SIZE (KiB per dispatch) are scaled
@@ -50,6 +51,8 @@ PASSES = {
             "-d {D}/lds -o lds --output-format csv -- " + LAYER, None),
     "fetch": ("rocprofv3 --pmc FETCH_SIZE -d {D}/fetch -o fetch --output-format csv -- " + LAYER, None),
     "write": ("rocprofv3 --pmc WRITE_SIZE -d {D}/write -o write --output-format csv -- " + LAYER, None),
+    "all": ("rocprofv3 --kernel-trace --stats -d {D}/all -o all --output-format csv -- "
+            "python -u bench.py --steps 5 --warmup 2 --no-cpu-baseline", "bench_all.json"),
     "btrace": ("rocprofv3 --kernel-trace --stats -d {D}/btrace -o btrace --output-format csv -- " + BUILDS,
                "builds.json"),
     "bfetch": ("rocprofv3 --pmc FETCH_SIZE -d {D}/bfetch -o bfetch --output-format csv -- " + BUILDS, None),
@@ -207,6 +210,36 @@ def record_layer(d, out=PROFILES):
     open(os.path.join(out, "ssc128_c64_mfma_counters.txt"), "w").write("\n".join(txt) + "\n")
 
 
+def record_all(d, out=PROFILES):
+    b = json.loads(open(os.path.join(d, "bench_all.json")).read().strip().splitlines()[-1])
+    stats = kernel_stats(os.path.join(d, "all"))
+    e, u = b["extra"]["sc_then_ssc"], b["extra"]["unet"]
+    txt = ["Kernel statistics of a whole bench.py run: the SSC 3^3 layer step (128^3 x 4 shapes, 100k sites, "
+           "C = 64, fp32 and bf16),",
+           "SC(2,2) 64 -> 96 then SSC 3^3 at 64^3 (fp32, bf16), and the five-level U-Net on 256^3 x 8 scenes "
+           "(about 2M level-0",
+           "sites, bf16, 32 -> 160 channels) with its geometry builds.", "",
+           "Command (repo root, MI355X):", "  " + command("all", "gpurun_out/prof"), "",
+           "bench.py's own figures from this profiled run (the profiler's per-dispatch cost inflates short "
+           "launches and host-bound phases):",
+           f"  layer step {b['ms_per_step']:.3f} ms; dgrad row launch {b['roofline']['launch_ms'] * 1e3:.1f} us "
+           f"(frac {b['roofline']['frac']:.3f})",
+           f"  U-Net forward {u['forward_ms']:.3f} ms = {u['forward_effective_tflops']:.0f} effective TFLOP/s "
+           f"({u['flops']:.4g} flops), unfused heads {u['forward_unfused_ms']:.3f} ms",
+           f"  U-Net geometry (all rule books + plans) {u['geometry_build_ms']:.3f} ms; fresh input (geometry + "
+           f"forward) {u['geometry_plus_forward_ms']:.3f} ms",
+           f"  level-0 SSC build {u['level0_ssc_build_roofline']['ms']:.3f} ms; level sites {u['level_sites']}",
+           f"  SC(2,2) forward fp32 {e['sc_forward_ms_f32'] * 1e3:.1f} us, bf16 {e['sc_forward_ms_bf16'] * 1e3:.1f} "
+           f"us; SSC 64^3 C=96 fp32 {e['ssc_forward_ms_f32'] * 1e3:.1f} us, bf16 "
+           f"{e['ssc_forward_ms_bf16'] * 1e3:.1f} us", ""]
+    tot = sum(r[1] * r[2] for r in stats)
+    rows = [(r[0][:64], r[1], r[2], r[1] * r[2] / 1e3, r[5]) for r in stats if r[5] >= 0.25]
+    txt.append(table(rows, f"{'kernel (all launches of the run)':64s} {'calls':>6s} {'avg us':>9s} "
+                           f"{'total ms':>9s} {'%':>6s}", "{:64s} {:6d} {:9.2f} {:9.3f} {:6.2f}"))
+    txt.append(f"(kernels under 0.25% not listed; all kernels together {tot / 1e3:.1f} ms)")
+    open(os.path.join(out, "bench_all_workloads_kernel_stats.txt"), "w").write("\n".join(txt) + "\n")
+
+
 def record_builds(d, out=PROFILES):
     b = json.loads(open(os.path.join(d, "builds.json")).read().strip().splitlines()[-1])
     stats = kernel_stats(os.path.join(d, "btrace"))
@@ -242,6 +275,7 @@ def main():
             print(command(name, a.show_commands))
         return
     record_layer(a.dir, a.out)
+    record_all(a.dir, a.out)
     record_builds(a.dir, a.out)
 
 
