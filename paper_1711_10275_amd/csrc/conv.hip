@@ -193,7 +193,19 @@ typedef __amdgpu_buffer_rsrc_t rsrc_t;
 constexpr uint32_t kOobOffset = 0x70000000u;  // >= any buffer size accepted on this path
 // LDS bytes per row of a bf16 weight-part plane of the split row kernel
 // (32 channels = 64 bytes, padded against bank conflicts).
-constexpr int kSplitPitch = 80;
+// Weight tiles of the row kernel that arrive by direct-to-LDS loads: one
+// row of CPR 16-byte chunks (4 or 8) per output column (and, for the split
+// path, per bf16 plane), without padding; chunk k of row r is stored in slot
+// k ^ swizzle(r mod 16).  An MFMA operand read takes the same chunk of 16
+// consecutive rows; with these swizzles every 8 consecutive lanes of such a
+// read fall on distinct 16-byte bank groups of a 128-byte bank line, and
+// every 16 on those of a 256-byte one.
+template <int CPR>
+__device__ __forceinline__ int tile_slot(int row, int chunk) {
+  static_assert(CPR == 4 || CPR == 8, "chunks per tile row");
+  const int m = row & 15;
+  return chunk ^ (CPR == 4 ? ((m >> 1) ^ (m >> 2)) & 3 : (m ^ (m >> 3)) & 7);
+}
 
 __device__ __forceinline__ rsrc_t make_rsrc(const void* p, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
@@ -250,6 +262,16 @@ __device__ __forceinline__ void lds_oct(Oct<float>& o, const char* p) {
   const uint4 y = *reinterpret_cast<const uint4*>(p + 16);
   o.v[0] = __uint_as_float(x.x); o.v[1] = __uint_as_float(x.y); o.v[2] = __uint_as_float(x.z); o.v[3] = __uint_as_float(x.w);
   o.v[4] = __uint_as_float(y.x); o.v[5] = __uint_as_float(y.y); o.v[6] = __uint_as_float(y.z); o.v[7] = __uint_as_float(y.w);
+}
+// The same from two 16-byte chunks at p0 and p1 (bf16: p0 holds all 8).
+__device__ __forceinline__ void lds_oct2(Oct<float>& o, const char* p0, const char* p1) {
+  const uint4 x = *reinterpret_cast<const uint4*>(p0);
+  const uint4 y = *reinterpret_cast<const uint4*>(p1);
+  o.v[0] = __uint_as_float(x.x); o.v[1] = __uint_as_float(x.y); o.v[2] = __uint_as_float(x.z); o.v[3] = __uint_as_float(x.w);
+  o.v[4] = __uint_as_float(y.x); o.v[5] = __uint_as_float(y.y); o.v[6] = __uint_as_float(y.z); o.v[7] = __uint_as_float(y.w);
+}
+__device__ __forceinline__ void lds_oct2(Oct<bf16_t>& o, const char* p0, const char*) {
+  o.v = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(p0));
 }
 __device__ __forceinline__ void lds_oct(Oct<bf16_t>& o, const char* p) {
   o.v = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(p));
@@ -615,27 +637,49 @@ __global__ void k_split_w(const float* __restrict__ W, int K, int kdim, int ncol
 // and writes them to the 4 columns' rows of the weight tile, which spares
 // the forward a transposed copy of W.
 // Bytes of one weight-tile buffer of the row kernel: COLS rows of the
-// step's window, or (SP) three planes of COLS rows of 32 bf16 channels.
-template <int WB, int NB, bool SP>
+// step's window (TB: padded rows written from registers; else unpadded rows
+// of direct loads), or (SP) three planes of COLS rows of 32 bf16 channels.
+template <int WB, int NB, bool SP, bool TB>
 constexpr int rows_b_bytes() {
-  return SP ? 3 * 16 * NB * kSplitPitch : 16 * NB * (WB + 16);
+  return TB ? 16 * NB * (WB + 16) : (SP ? 3 * 16 * NB * 64 : 16 * NB * WB);
 }
+// LDS of the row kernel: the four wavefronts' row tiles, then the two weight
+// buffers; the bf16 epilogue reuses all of it.
+template <int WB, int NB, bool SP, bool TB>
+struct RowsLds {
+  static constexpr int PITCH = WB + 16;  // bytes per row-tile row (bank spread)
+  static constexpr int A_BYTES = 4 * 16 * PITCH;
+  static constexpr int B_BYTES = rows_b_bytes<WB, NB, SP, TB>();
+  static constexpr int BYTES = A_BYTES + 2 * B_BYTES;
+};
 
 template <typename T, int WB, int NB, int D, int PK, bool TB = false, bool SP = false>
 __device__ __forceinline__ void conv_rows_block(
     const T* __restrict__ X, uint32_t x_bytes, const void* __restrict__ B, uint32_t b_bytes,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ b_first, const uint32_t* __restrict__ items,
-    int64_t blk, int K, int mirror, int kdim, int ncols, const Heads<T>& Y, char (*As)[16 * (WB + 16)],
-    char (*Bs)[rows_b_bytes<WB, NB, SP>()], int tid, int wave, int lane, int m, int g, int col0) {
+    int64_t blk, int K, int mirror, int kdim, int ncols, const Heads<T>& Y, char* smem, int tid, int wave,
+    int lane, int m, int g, int col0) {
   static_assert(!SP || (sizeof(T) == 4 && WB == 128 && PK == 1 && !TB), "split path: fp32, whole windows");
   constexpr int LPR = WB / 16;              // lanes per row window
   constexpr int RPI = 64 / LPR;             // rows per wavefront load
   constexpr int NA = 16 / RPI;              // row loads per wavefront and step
   constexpr int COLS = 16 * NB;             // output columns per workgroup
-  // weight pieces (16 bytes) per thread and step; SP: 3 planes x COLS rows x 4
-  constexpr int NBP = SP ? (3 * COLS * 4 + 255) / 256 : (COLS * LPR + 255) / 256;
-  constexpr int PITCH = WB + 16;            // LDS bytes per row (bank spread)
+  // The weight tile (TROWS rows of CPR chunks) arrives by direct-to-LDS
+  // loads (except TB): NI wave loads of 64 chunks per step, loads j = wave,
+  // wave + 4, .. by each wavefront; slot c = row * CPR + (slot within the
+  // row) sits at byte 16 c of the tile.  TB: weight pieces (16 bytes) per
+  // thread and step, written to LDS from registers.
+  constexpr bool DB = !TB;
+  constexpr int CPR = SP ? 4 : LPR;
+  constexpr int TROWS = SP ? 3 * COLS : COLS;
+  constexpr int NI = DB ? TROWS * CPR / 64 : 0;
+  constexpr int NJ = (NI + 3) / 4;
+  constexpr int NBP = DB ? 1 : (COLS * LPR + 255) / 256;
+  using L = RowsLds<WB, NB, SP, TB>;
+  constexpr int PITCH = L::PITCH;
   constexpr int S = WB / (32 * (int)sizeof(T));  // 32-channel MFMA groups per step
+  char* const As = smem + wave * 16 * PITCH;     // this wavefront's row tile
+  auto Bs = [&](int buf) { return smem + L::A_BYTES + buf * L::B_BYTES; };
   const int first = b_first[blk];
   const int n_items = b_first[blk + 1] - first;
   const uint32_t row_bytes = (uint32_t)kdim * sizeof(T);
@@ -667,15 +711,11 @@ __device__ __forceinline__ void conv_rows_block(
     for (int q = 0; q < NBP; ++q) {
       const int p = tid + 256 * q;
       if constexpr (SP) {
-        // piece p: plane p / (4 COLS), column (p / 4) % COLS, channels 8 (p % 4) .. + 7
-        const int plane = p / (4 * COLS);
-        b_col[q] = plane * COLS + (p / 4) % COLS;  // row of the LDS tile (plane-major)
-        b_byte[q] = (uint32_t)(p % 4) * 16;        // within the plane row's 64-byte window
+        (void)p;
+        b_col[q] = 0;
+        b_byte[q] = 0;
         b_u[q] = 0;
-        const int col = col0 + (p / 4) % COLS;
-        b_base[q] = (plane < 3 && col < ncols)
-                        ? (uint32_t)plane * (uint32_t)K * w_stride + (uint32_t)col * (uint32_t)kdim * 2u
-                        : kOobOffset;
+        b_base[q] = kOobOffset;
       } else if constexpr (TB) {
         static_assert(PK == 1, "TB reads one item per step");
         constexpr int PPC = COLS / 4;  // 16-byte pieces per reduction channel
@@ -686,12 +726,33 @@ __device__ __forceinline__ void conv_rows_block(
         const int col = col0 + b_col[q];
         b_base[q] = (ch < WB / (int)sizeof(T) && col < ncols) ? (uint32_t)col * sizeof(T) : kOobOffset;
       } else {
-        b_col[q] = p / LPR;
-        b_byte[q] = (uint32_t)(p % LPR) * 16;
-        b_u[q] = PK > 1 ? (int)(b_byte[q] / row_bytes) : 0;
-        const int col = col0 + b_col[q];
-        b_base[q] = (b_col[q] < COLS && col < ncols) ? (uint32_t)col * row_bytes : kOobOffset;
+        (void)p;
+        b_col[q] = 0;
+        b_byte[q] = 0;
+        b_u[q] = 0;
+        b_base[q] = kOobOffset;
       }
+    }
+
+    // this lane's chunk of each of its wavefront's weight loads: byte offset
+    // in B without the offset's part and the window's (SP: in the planes),
+    // the chunk's byte within the window, and (PK > 1) its item of the step
+    uint32_t d_voff[NJ > 0 ? NJ : 1], d_ch[NJ > 0 ? NJ : 1];
+    int d_u[NJ > 0 ? NJ : 1];
+#pragma unroll
+    for (int jj = 0; jj < NJ; ++jj) {
+      const int c = (wave + 4 * jj) * 64 + lane;
+      const int row = c / CPR, chunk = tile_slot<CPR>(row, c % CPR);
+      const int col = row % COLS, plane = row / COLS;
+      d_ch[jj] = (uint32_t)chunk * 16;
+      d_u[jj] = PK > 1 ? (int)(d_ch[jj] / row_bytes) : 0;
+      const bool in = wave + 4 * jj < NI && col0 + col < ncols;
+      if constexpr (SP)
+        d_voff[jj] = in ? (uint32_t)plane * (uint32_t)K * w_stride + (uint32_t)(col0 + col) * (uint32_t)kdim * 2u +
+                              d_ch[jj]
+                        : kOobOffset;
+      else
+        d_voff[jj] = in ? (uint32_t)(col0 + col) * row_bytes + d_ch[jj] - (uint32_t)d_u[jj] * row_bytes : kOobOffset;
     }
 
     // items for which this wavefront's 16 rows have at least one pair (bit
@@ -712,6 +773,11 @@ __device__ __forceinline__ void conv_rows_block(
 
     uint4 ga[D][NA], gb[D][NBP];  // global loads in flight
     int ld_item = 0, ld_ks = 0, ld_step = 0;
+    // per ring slot, the weight tile's offset byte (PK > 1: per item, or
+    // kOobOffset past the last), window byte and whether the step exists
+    // (its tile is loaded a step after its rows)
+    uint32_t dm_off[D][PK], dm_win[D];
+    bool dm_live[D];
     // entries of the next step to be issued, read one step ahead (every
     // entry of an item carries the item's offset)
     uint32_t nx_r[NA];
@@ -740,15 +806,9 @@ __device__ __forceinline__ void conv_rows_block(
           ga[slot][i] = make_uint4(v[0], v[1], v[2], v[3]);
         }
 #pragma unroll
-        for (int q = 0; q < NBP; ++q) {
-          uint32_t so = soff[0];
-#pragma unroll
-          for (int u = 1; u < PK; ++u) so = b_u[q] == u ? soff[u] : so;
-          const bool ok = live && ld_item + b_u[q] < n_items && b_base[q] != kOobOffset;
-          const auto v = __builtin_amdgcn_raw_buffer_load_b128(
-              rb, (int)(ok ? b_base[q] + (b_byte[q] - (uint32_t)b_u[q] * row_bytes) + so : kOobOffset), 0, 0);
-          gb[slot][q] = make_uint4(v[0], v[1], v[2], v[3]);
-        }
+        for (int u = 0; u < PK; ++u) dm_off[slot][u] = ld_item + u < n_items ? soff[u] : kOobOffset;
+        dm_win[slot] = 0;
+        dm_live[slot] = live;
         ld_item += PK;
         ++ld_step;
         fetch_ent();
@@ -757,6 +817,11 @@ __device__ __forceinline__ void conv_rows_block(
       const int o = (int)((uint32_t)__builtin_amdgcn_readfirstlane((int)nx_r[0]) >> kPlanRowBits);
       const int ow = mirror ? K - 1 - o : o;
       const uint32_t win = (uint32_t)ld_ks * WB;
+      if constexpr (DB) {
+        dm_off[slot][0] = (uint32_t)ow * w_stride;
+        dm_win[slot] = SP ? win / 2u : win;  // SP: 32 channels are 64 bytes of each bf16 plane row
+        dm_live[slot] = live;
+      }
 #pragma unroll
       for (int i = 0; i < NA; ++i) {
         const uint32_t r = nx_r[i] & kPlanNoRow;
@@ -766,9 +831,8 @@ __device__ __forceinline__ void conv_rows_block(
         ga[slot][i] = make_uint4(v[0], v[1], v[2], v[3]);
       }
 #pragma unroll
-      for (int q = 0; q < NBP; ++q) {
-        // SP: the window's 32 channels are 64 bytes of each bf16 plane row
-        const uint32_t bwin = SP ? win / 2u : win;
+      for (int q = 0; q < (DB ? 0 : NBP); ++q) {
+        const uint32_t bwin = win;
         const bool ok = live && bwin + b_byte[q] < (SP ? (uint32_t)kdim * 2u : row_bytes) && b_base[q] != kOobOffset;
         // TB: row (win + b_byte) / sizeof(T) of the offset's kdim x ncols matrix
         const uint32_t off = TB ? (win + b_byte[q]) / (uint32_t)sizeof(T) * ((uint32_t)ncols * sizeof(T)) + b_base[q]
@@ -784,22 +848,17 @@ __device__ __forceinline__ void conv_rows_block(
     auto stage = [&](int slot, int buf) {
 #pragma unroll
       for (int i = 0; i < NA; ++i)
-        *reinterpret_cast<uint4*>(&As[wave][a_row[i] * PITCH + a_byte]) = ga[slot][i];
+        *reinterpret_cast<uint4*>(&As[a_row[i] * PITCH + a_byte]) = ga[slot][i];
+      if constexpr (TB) {
 #pragma unroll
-      for (int q = 0; q < NBP; ++q) {
-        if constexpr (SP) {
-          if (b_col[q] < 3 * COLS)
-            *reinterpret_cast<uint4*>(&Bs[buf][b_col[q] * kSplitPitch + b_byte[q]]) = gb[slot][q];
-        } else if constexpr (TB) {
+        for (int q = 0; q < NBP; ++q) {
           // 4 consecutive columns of one channel: one element in each column's row
           if (b_byte[q] >= (uint32_t)WB) continue;  // (never, when the pieces fill the threads exactly)
-          char* dst = &Bs[buf][b_col[q] * PITCH + b_byte[q]];
+          char* dst = &Bs(buf)[b_col[q] * PITCH + b_byte[q]];
           *reinterpret_cast<uint32_t*>(dst) = gb[slot][q].x;
           *reinterpret_cast<uint32_t*>(dst + PITCH) = gb[slot][q].y;
           *reinterpret_cast<uint32_t*>(dst + 2 * PITCH) = gb[slot][q].z;
           *reinterpret_cast<uint32_t*>(dst + 3 * PITCH) = gb[slot][q].w;
-        } else if (b_col[q] < COLS) {
-          *reinterpret_cast<uint4*>(&Bs[buf][b_col[q] * PITCH + b_byte[q]]) = gb[slot][q];
         }
       }
     };
@@ -818,15 +877,16 @@ __device__ __forceinline__ void conv_rows_block(
         // the row tile's 8 channels of this lane, split; the weights' parts
         // were split once, before the launch
         Oct<float> a;
-        lds_oct(a, &As[wave][m * PITCH + 32 * g]);
+        lds_oct(a, &As[m * PITCH + 32 * g]);
         bf16x8 ah, am, al;
         split8(a.v, ah, am, al);
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
-          const char* bp = &Bs[buf][(nb * 16 + m) * kSplitPitch + 16 * g];
+          const int col = nb * 16 + m;
+          const char* bp = &Bs(buf)[(col * CPR + tile_slot<CPR>(col, g)) * 16];
           const bf16x8 bh = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(bp));
-          const bf16x8 bm = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(bp + COLS * kSplitPitch));
-          const bf16x8 bl = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(bp + 2 * COLS * kSplitPitch));
+          const bf16x8 bm = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(bp + COLS * 64));
+          const bf16x8 bl = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(bp + 2 * COLS * 64));
           acc[nb] = mma_split(ah, am, al, bh, bm, bl, acc[nb]);
         }
         return;
@@ -835,9 +895,19 @@ __device__ __forceinline__ void conv_rows_block(
 #pragma unroll
       for (int j = 0; j < S; ++j) {
         const int byte = (32 * j + 8 * g) * (int)sizeof(T);
-        lds_oct(a[j], &As[wave][m * PITCH + byte]);
+        lds_oct(a[j], &As[m * PITCH + byte]);
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) lds_oct(b[j][nb], &Bs[buf][(nb * 16 + m) * PITCH + byte]);
+        for (int nb = 0; nb < NB; ++nb) {
+          const int col = nb * 16 + m;
+          if constexpr (TB) {
+            lds_oct(b[j][nb], &Bs(buf)[col * PITCH + byte]);
+          } else {
+            // chunk byte / 16 (fp32: and the next) of the column's row
+            const char* row = &Bs(buf)[col * CPR * 16];
+            lds_oct2(b[j][nb], row + 16 * tile_slot<CPR>(col, byte / 16),
+                     row + 16 * tile_slot<CPR>(col, (byte / 16 + 1) % CPR));
+          }
+        }
       }
 #pragma unroll
       for (int j = 0; j < S; ++j)
@@ -845,17 +915,53 @@ __device__ __forceinline__ void conv_rows_block(
         for (int nb = 0; nb < NB; ++nb) acc[nb] = mma_oct(a[j], b[j][nb], acc[nb]);
     };
 
-    // step t: its loads are issued at step t - D (ring slot t % D), staged
-    // into LDS at step t - 1 (weight buffer t % 2) and multiplied at step t
+    // the weight tile of the step in ring slot sl into buffer buf
+    auto dma_b = [&](int sl, int buf) {
+      if constexpr (DB) {
+        if (!dm_live[sl]) return;
+        const uint32_t rowlen = SP ? (uint32_t)kdim * 2u : row_bytes;  // bytes of a row of B (SP: of a plane)
+#pragma unroll
+        for (int jj = 0; jj < NJ; ++jj) {
+          if (wave + 4 * jj >= NI) break;
+          auto* dst = (__attribute__((address_space(3))) void*)&Bs(buf)[(wave + 4 * jj) * 1024];
+          if constexpr (PK > 1) {
+            // the chunk's item of the step: its own offset, folded into the lane's address
+            uint32_t so = dm_off[sl][0];
+#pragma unroll
+            for (int u = 1; u < PK; ++u) so = d_u[jj] == u ? dm_off[sl][u] : so;
+            const bool ok = d_voff[jj] != kOobOffset && so != kOobOffset;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, dst, 16, (int)(ok ? d_voff[jj] + so : kOobOffset), 0, 0, 0);
+          } else {
+            const bool ok = d_voff[jj] != kOobOffset && dm_win[sl] + d_ch[jj] < rowlen;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, dst, 16, (int)(ok ? d_voff[jj] + dm_win[sl] : kOobOffset),
+                                                     (int)dm_off[sl][0], 0, 0);
+          }
+        }
+      }
+    };
+    // all of this wavefront's loads issued so far have landed (the direct
+    // weight loads, which the compiler's own waits do not cover)
+    auto wait_loads = [&]() {
+      if constexpr (DB) __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    };
+    // step t: its row loads are issued at step t - D (ring slot t % D) and
+    // staged into LDS at step t - 1, its weight tile is loaded straight into
+    // LDS buffer t % 2 at step t - 1 (SP) or staged from registers there, and
+    // it is multiplied at step t
 #pragma unroll
     for (int q = 0; q < D; ++q) issue(q);
+    dma_b(0, 0);
     stage(0, 0);
+    wait_loads();
     __syncthreads();
     // u = t % (2 D) keeps the ring positions compile-time constants; the row
-    // tile of step t is read before step t + 1's rows overwrite it
+    // tile of step t is read before step t + 1's rows overwrite it, and the
+    // weight buffer of step t + 1 was last read at step t - 1
     auto step = [&](int u) {
       multiply(u % 2);
+      dma_b((u + 1) % D, (u + 1) % 2);
       stage((u + 1) % D, (u + 1) % 2);
+      wait_loads();
       issue(u % D);  // loads of step t + D
       __syncthreads();
     };
@@ -876,14 +982,14 @@ __device__ __forceinline__ void conv_rows_block(
   // pieces instead of one 2-byte element per lane and row.  (fp32 rows take
   // 4 bytes per lane already; there the extra registers cost more.)
   constexpr int RB = COLS * (int)sizeof(T) + 16;  // tile row pitch (bank spread)
-  static_assert(16 * RB <= 2 * 16 * NB * (WB + 16) / 4, "output tile fits a quarter of the weight buffers");
+  static_assert(sizeof(T) == 4 || 4 * 16 * RB <= L::BYTES, "output tiles fit the LDS");
   bool vec = sizeof(T) == 2 && (ncols * (int)sizeof(T)) % 16 == 0;
 #pragma unroll
   for (int h = 0; h < 2; ++h)
     if (h < Y.n)
       vec = vec && reinterpret_cast<uintptr_t>(Y.out[h]) % 16 == 0 && (Y.ld[h] * (int64_t)sizeof(T)) % 16 == 0;
   if constexpr (sizeof(T) == 2) if (vec) {
-    char* tile = reinterpret_cast<char*>(Bs) + wave * (2 * 16 * NB * (WB + 16) / 4);
+    char* tile = smem + wave * 16 * RB;
     constexpr int PIECES = COLS * (int)sizeof(T) / 16;  // 16-byte pieces per tile row
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
@@ -948,10 +1054,8 @@ __device__ __forceinline__ void conv_rows_run(
     const uint32_t* __restrict__ items, int64_t n_blocks, int K, int mirror, int kdim, int ncols, const Heads<T>& Y) {
   constexpr int RPI = 64 / (WB / 16);       // rows per wavefront load
   constexpr int COLS = 16 * NB;             // output columns per workgroup
-  constexpr int PITCH = WB + 16;            // LDS bytes per row (bank spread)
   static_assert(WB / (32 * (int)sizeof(T)) >= 1 && 16 % RPI == 0, "window");
-  __shared__ __attribute__((aligned(16))) char As[4][16 * PITCH];
-  __shared__ __attribute__((aligned(16))) char Bs[2][rows_b_bytes<WB, NB, SP>()];
+  __shared__ __attribute__((aligned(16))) char smem[RowsLds<WB, NB, SP, TB>::BYTES];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int m = lane & 15, g = lane >> 4;
@@ -981,7 +1085,7 @@ __device__ __forceinline__ void conv_rows_run(
   for (int64_t idx = wg, round = 0; idx < n_blocks; idx = next(++round)) {
     __syncthreads();  // the previous block's LDS is free
     conv_rows_block<T, WB, NB, D, PK, TB, SP>(X, x_bytes, B, b_bytes, perm, b_first, items, b_order[idx], K, mirror,
-                                              kdim, ncols, Y, As, Bs, tid, wave, lane, m, g, col0);
+                                              kdim, ncols, Y, smem, tid, wave, lane, m, g, col0);
   }
 }
 
