@@ -621,17 +621,19 @@ __global__ void k_split_w(const float* __restrict__ W, int K, int kdim, int ncol
 // Loads: gathers whose lanes follow the MFMA layout (consecutive lanes on
 // consecutive rows) issue at about a third of the rate of loads in which
 // several consecutive lanes read one contiguous piece of a row, so rows and
-// weights are loaded WB bytes per row with WB / 16 lanes per row, written
-// to LDS, and read back in the MFMA layout: lane (m, g) takes channels
+// weights are loaded WB bytes per row with WB / 16 lanes per row, put in
+// LDS, and read back in the MFMA layout: lane (m, g) takes channels
 // 32 j + 8 g + [0, 8) (j < S) of row m of the step's window (A) and of
 // weight row m of each column block (B).  The MFMAs sum over exactly these
 // channels, so a row's result does not depend on which rows share its
 // block.  B is laid out [o][ncols][kdim] (a contiguous row of reduction
-// channels per output column).  Global loads run D - 1 steps ahead in
-// registers; the weight tile is double-buffered in LDS with one barrier per
-// step; each wavefront's row tile is private to it.  The plan entries are
-// read from global memory (L2) a step ahead of their use, which keeps the
-// LDS footprint small (27 KB for 128-byte windows: five workgroups per CU).
+// channels per output column).  Row gathers run D - 1 steps ahead in
+// registers and each wavefront's row tile is private to it; the weight
+// tile goes straight from memory into one of two LDS buffers (a buffer
+// load with LDS destination: no registers, no LDS writes), one barrier per
+// step.  Taking the weight tile through registers and LDS writes had cost
+// about a quarter of the fp32 kernel's time.  The plan entries are read
+// from global memory (L2) a step ahead of their use.
 // TB: B is stored [o][kdim][ncols] instead (the forward's weights as given);
 // a thread then loads 16 bytes of one reduction channel (4 output columns)
 // and writes them to the 4 columns' rows of the weight tile, which spares
@@ -946,8 +948,10 @@ __device__ __forceinline__ void conv_rows_block(
     };
     // step t: its row loads are issued at step t - D (ring slot t % D) and
     // staged into LDS at step t - 1, its weight tile is loaded straight into
-    // LDS buffer t % 2 at step t - 1 (SP) or staged from registers there, and
-    // it is multiplied at step t
+    // LDS buffer t % 2 at the start of step t - 1 (TB: staged there from
+    // registers), and it is multiplied at step t.  (Row gathers loaded
+    // straight into LDS the same way took bf16 layers 41 -> 61 us: the row
+    // tiles stay staged from registers.)
 #pragma unroll
     for (int q = 0; q < D; ++q) issue(q);
     dma_b(0, 0);
@@ -956,10 +960,11 @@ __device__ __forceinline__ void conv_rows_block(
     __syncthreads();
     // u = t % (2 D) keeps the ring positions compile-time constants; the row
     // tile of step t is read before step t + 1's rows overwrite it, and the
-    // weight buffer of step t + 1 was last read at step t - 1
+    // weight buffer of step t + 1 was last read at step t - 1 (so its loads
+    // can start before step t's multiplications)
     auto step = [&](int u) {
-      multiply(u % 2);
       dma_b((u + 1) % D, (u + 1) % 2);
+      multiply(u % 2);
       stage((u + 1) % D, (u + 1) % 2);
       wait_loads();
       issue(u % D);  // loads of step t + D
