@@ -197,14 +197,17 @@ constexpr uint32_t kOobOffset = 0x70000000u;  // >= any buffer size accepted on 
 // row of CPR 16-byte chunks (4 or 8) per output column (and, for the split
 // path, per bf16 plane), without padding; chunk k of row r is stored in slot
 // k ^ swizzle(r mod 16).  An MFMA operand read takes the same chunk of 16
-// consecutive rows; with these swizzles every 8 consecutive lanes of such a
-// read fall on distinct 16-byte bank groups of a 128-byte bank line, and
-// every 16 on those of a 256-byte one.
+// consecutive rows.  The swizzles are the ones with the fewest LDS
+// bank-conflict cycles in a sweep on the hardware (SQ_LDS_BANK_CONFLICT):
+// for 8-chunk rows r mod 8 (0.02 conflict cycles per LDS cycle with the
+// row tiles' 32-byte padding, against 2.55 unswizzled and 1.19 for
+// (r ^ r / 8) mod 8), for 4-chunk rows (r / 2 ^ r / 4) mod 4 (0.25, against
+// 1.66 for r mod 4).
 template <int CPR>
 __device__ __forceinline__ int tile_slot(int row, int chunk) {
   static_assert(CPR == 4 || CPR == 8, "chunks per tile row");
   const int m = row & 15;
-  return chunk ^ (CPR == 4 ? ((m >> 1) ^ (m >> 2)) & 3 : (m ^ (m >> 3)) & 7);
+  return chunk ^ (CPR == 4 ? ((m >> 1) ^ (m >> 2)) & 3 : m & 7);
 }
 
 __device__ __forceinline__ rsrc_t make_rsrc(const void* p, uint32_t bytes) {
@@ -641,15 +644,21 @@ __global__ void k_split_w(const float* __restrict__ W, int K, int kdim, int ncol
 // Bytes of one weight-tile buffer of the row kernel: COLS rows of the
 // step's window (TB: padded rows written from registers; else unpadded rows
 // of direct loads), or (SP) three planes of COLS rows of 32 bf16 channels.
+// Bytes per row of the row tiles and of the TB weight tile (bank spread:
+// +16 had 1.2 conflict cycles per LDS cycle in bf16 layers, +32 0.02).
+template <int WB>
+constexpr int rows_pitch() {
+  return WB + 32;
+}
 template <int WB, int NB, bool SP, bool TB>
 constexpr int rows_b_bytes() {
-  return TB ? 16 * NB * (WB + 16) : (SP ? 3 * 16 * NB * 64 : 16 * NB * WB);
+  return TB ? 16 * NB * rows_pitch<WB>() : (SP ? 3 * 16 * NB * 64 : 16 * NB * WB);
 }
 // LDS of the row kernel: the four wavefronts' row tiles, then the two weight
 // buffers; the bf16 epilogue reuses all of it.
 template <int WB, int NB, bool SP, bool TB>
 struct RowsLds {
-  static constexpr int PITCH = WB + 16;  // bytes per row-tile row (bank spread)
+  static constexpr int PITCH = rows_pitch<WB>();  // bytes per row-tile row
   static constexpr int A_BYTES = 4 * 16 * PITCH;
   static constexpr int B_BYTES = rows_b_bytes<WB, NB, SP, TB>();
   static constexpr int BYTES = A_BYTES + 2 * B_BYTES;
