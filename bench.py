@@ -126,6 +126,49 @@ def cpu_baseline(coords, size, X, W, G, budget_s):
                       f"use {threads} BLAS threads, the rest one) of the same {n}-site workload, {t_total:.1f} s"}
 
 
+def cpu_ops(coords, size):
+    """The oracle on the further operators (pooling, batch normalisation, a
+    residual block, a small U-Net training step, a 4-d layer), one timed
+    call each, on the host cores: the CPU figures beside ops_extra's."""
+    from oracle import sscn_oracle as O
+    from paper_1711_10275_amd import synthetic as S
+    from paper_1711_10275_amd import unet
+
+    def t(fn):
+        t0 = time.perf_counter()
+        fn()
+        return (time.perf_counter() - t0) * 1e3
+
+    out = {}
+    n = coords.shape[0]
+    sc = O.sc_rulebook(coords, size, 2, 2)
+    X = S.features(n, 64, S.SEED_FEAT + 41)
+    out["max_pool_forward_ms"] = t(lambda: O.max_pool(X, sc))
+    out["avg_pool_forward_ms"] = t(lambda: O.avg_pool(X, sc))
+    g, b = np.ones(64), np.zeros(64)
+    Y, mean, var = O.batch_norm_relu_train(X, g, b)
+    out["batchnorm_forward_shapes128_c64_ms"] = t(lambda: O.batch_norm_relu_train(X, g, b))
+    out["batchnorm_backward_shapes128_c64_ms"] = t(lambda: O.batch_norm_relu_backward(Y, X, g, b, mean, var))
+    rb = O.ssc_rulebook(coords, size, 3)
+    ps = [S.layer_params(f"res{i}", 27, 64, 64, bf16=False) for i in range(2)]
+    out["residual_block_forward_ms"] = t(lambda: O.residual_block(X, rb, ps[0], ps[1]))
+    cs = S.scenes_small(batch=2, L=32, target_per_sample=3000)
+    ch, ncls = (8, 16, 24), 6
+    Xs = S.features(cs.shape[0], ch[0], S.SEED_FEAT + 31)
+    lab = S.labels(cs.shape[0], ncls, 32)
+    out["unet3_train_step_scenes32_ms"] = t(lambda: O.unet_train_step(cs, (32, 32, 32), Xs, lab,
+                                                                       lambda nm, k, ci, co: S.train_params(nm, k, ci,
+                                                                                                            co),
+                                                                       ch, ncls))
+    out["unet3_train_step_scenes32_sites"] = int(cs.shape[0])
+    c4 = S.moving_shells_4d()
+    out["layer_4d_rulebook_ms"] = t(lambda: O.ssc_rulebook(c4, (16, 48, 48, 48), 3))
+    r4 = O.ssc_rulebook(c4, (16, 48, 48, 48), 3)
+    X4, W4 = S.features(c4.shape[0], 32, S.SEED_FEAT + 47), S.weights(81, 32, 32, S.SEED_WEIGHT + 47)
+    out["layer_4d_forward_ms"] = t(lambda: O.forward(X4, W4, r4))
+    return out
+
+
 def _event_ms(fn, reps, stream):
     """Mean time per call of back-to-back calls (HIP events on `stream`)."""
     import torch
@@ -260,6 +303,136 @@ def unet_scenes(stream, reps):
             "geometry_plus_forward_sites_per_s": c.shape[0] / (fresh_ms * 1e-3)}
 
 
+def _hbm(nbytes, ms):
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    return {"ms": ms, "bytes": int(nbytes), "achieved_GBs": gbs, "peak_GBs": PEAK_HBM_GBS, "frac": gbs / PEAK_HBM_GBS}
+
+
+def ops_extra(tc, size, stream, reps):
+    """The operators beyond the convolution (pooling, upsampling, batch
+    normalisation, the training step, residual blocks, bias, 4-d layers),
+    each timed with its algorithmic bytes (HBM-bound operators) or useful
+    flops (convolutions) against the peak."""
+    import torch
+    from paper_1711_10275_amd import blocks, sscn, train, unet
+    from paper_1711_10275_amd import synthetic as S
+    dev = tc.device
+    timed = lambda fn: _event_ms(fn, reps, stream)
+    out = {}
+
+    # MP / AP / nearest-neighbour upsampling over SC(2, 2), 128^3 x 4 shapes, C = 64
+    sc = sscn.sc_rulebook_build(tc, size, 2, 2)
+    n_in, n_out, P = sc.n_in, sc.n_out, sc.n_pairs
+    pool = {"workload": "sc2x2x2s2_grid128_shapes_c64", "n_in": n_in, "n_out": n_out, "pairs": P}
+    for name, dt in (("f32", torch.float32), ("bf16", torch.bfloat16)):
+        e = 4 if dt == torch.float32 else 2
+        X = torch.from_numpy(S.features(n_in, 64, S.SEED_FEAT + 41)).to(dt).to(dev)
+        G = torch.from_numpy(S.features(n_out, 64, S.SEED_GRAD + 41)).to(dt).to(dev)
+        _, arg = sscn.pool_forward(X, sc, "max")
+        xb, yb, ab, pb = n_in * 64 * e, n_out * 64 * e, n_out * 64, 8 * P
+        pool[name] = {
+            "max_forward": _hbm(xb + yb + ab + pb, timed(lambda: sscn.pool_forward(X, sc, "max"))),
+            "max_backward": _hbm(yb + ab + xb + pb, timed(lambda: sscn.pool_backward(G, sc, "max", arg))),
+            "avg_forward": _hbm(xb + yb + pb, timed(lambda: sscn.pool_forward(X, sc, "avg"))),
+            "avg_backward": _hbm(yb + xb + pb, timed(lambda: sscn.pool_backward(G, sc, "avg"))),
+            "upsample_forward": _hbm(yb + xb + pb, timed(lambda: sscn.upsample_forward(G, sc))),
+            "upsample_backward": _hbm(xb + yb + pb, timed(lambda: sscn.upsample_backward(X, sc))),
+        }
+    out["pool"] = pool
+
+    # batch normalisation over the active sites: the U-Net's level-0 size
+    # (256^3 x 8 scenes, 32 channels, bf16) and the 64-channel layer (fp32)
+    c256 = S.scenes_256()
+    bn = {}
+    for name, n, c, dt in (("scenes256_c32_bf16", int(c256.shape[0]), 32, torch.bfloat16),
+                           ("shapes128_c64_f32", int(tc.shape[0]), 64, torch.float32)):
+        e = 4 if dt == torch.float32 else 2
+        x = (torch.from_numpy(S.features(n, c, S.SEED_FEAT + 42)) * 2 + 0.5).to(dt).to(dev)
+        dA = torch.from_numpy(S.features(n, c, S.SEED_GRAD + 42)).to(dt).to(dev)
+        g = torch.ones(c, device=dev)
+        b = torch.zeros(c, device=dev)
+        st = sscn.batchnorm_forward(x, g, b)
+        dg, db = sscn.batchnorm_relu_backward_params(dA, x, st, b)
+        dx = torch.empty_like(x)
+        nb = n * c * e
+        bn[name] = {
+            "stats": _hbm(nb, timed(lambda: sscn.batchnorm_forward(x, g, b))),
+            "apply_relu": _hbm(2 * nb, timed(lambda: sscn.batchnorm_relu_apply(x, st, b))),
+            "backward_params": _hbm(2 * nb, timed(lambda: sscn.batchnorm_relu_backward_params(dA, x, st, b))),
+            "backward_input": _hbm(3 * nb, timed(lambda: sscn.batchnorm_relu_backward_input(dA, x, g, b, st, dg, db,
+                                                                                           dx))),
+        }
+    out["batchnorm"] = bn
+
+    # one whole U-Net training step (forward, backward, SGD) on 256^3 x 8 scenes, bf16
+    t256 = torch.from_numpy(c256).to(dev)
+    ncls = 20
+    geom = train.Geometry(t256, (256, 256, 256))
+    Pm = train.Params(unet.CHANNELS, ncls, lambda nm, k, ci, co: S.train_params(nm, k, ci, co),
+                      dtype=torch.bfloat16)
+    x0 = torch.from_numpy(S.features(c256.shape[0], unet.CHANNELS[0], S.SEED_FEAT + 43, bf16=True)).to(
+        torch.bfloat16).to(dev)
+    lab = torch.from_numpy(S.labels(c256.shape[0], ncls, 44)).to(dev)
+    step_ms = _wall_ms(lambda: train.train_step(x0, lab, geom, Pm), 3)
+    fl = 3 * unet.flops(geom)  # forward, dgrad and wgrad of every convolution (the head aside)
+    out["unet_train_step"] = {"workload": "unet5_grid256_batch8_scenes_c32to160_bf16_20classes",
+                              "ms": step_ms, "sites_per_s": c256.shape[0] / (step_ms * 1e-3),
+                              "conv_flops": fl, "effective_tflops": fl / (step_ms * 1e-3) / 1e12}
+    del geom, Pm, x0, lab
+    # the small three-level network the oracle's training step is timed on
+    cs = S.scenes_small(batch=2, L=32, target_per_sample=3000)
+    ts = torch.from_numpy(cs).to(dev)
+    ch3, ncls3 = (8, 16, 24), 6
+    geom3 = train.Geometry(ts, (32, 32, 32), levels=3)
+    P3 = train.Params(ch3, ncls3, lambda nm, k, ci, co: S.train_params(nm, k, ci, co))
+    xs = torch.from_numpy(S.features(cs.shape[0], ch3[0], S.SEED_FEAT + 31)).to(dev)
+    ls = torch.from_numpy(S.labels(cs.shape[0], ncls3, 32)).to(dev)
+    out["unet3_train_step_scenes32"] = {"workload": "unet3_grid32_batch2_scenes_c8to24_f32_6classes",
+                                        "sites": int(cs.shape[0]),
+                                        "ms": _wall_ms(lambda: train.train_step(xs, ls, geom3, P3), reps)}
+    del geom3, P3
+
+    # pre-activated residual block (two SSC(3) convolutions), 128^3 x 4 shapes, C = 64 fp32
+    rb = sscn.ssc_rulebook_build(tc, size, 3)
+    n = int(tc.shape[0])
+    X = torch.from_numpy(S.features(n, 64, S.SEED_FEAT + 45)).to(dev)
+    ps = [tuple(torch.from_numpy(a).to(dev) for a in S.layer_params(f"res{i}", 27, 64, 64, bf16=False))
+          for i in range(2)]
+    fwd_ms = timed(lambda: blocks.residual_block(X, rb, *ps))
+    G = torch.from_numpy(S.features(n, 64, S.SEED_GRAD + 45)).to(dev)
+
+    def train_block():
+        y, cache = blocks.residual_block_train(X, rb, *ps)
+        blocks.residual_block_train_backward(G, cache)
+
+    train_ms = _wall_ms(train_block, reps)
+    fl2 = 2 * 2.0 * 64 * 64 * rb.n_pairs
+    out["residual_block"] = {"workload": "ssc3x3x3_x2_grid128_shapes_c64_f32", "forward_ms": fwd_ms,
+                             "forward_tflops": fl2 / (fwd_ms * 1e-3) / 1e12, "train_fwd_bwd_ms": train_ms,
+                             "train_tflops": 3 * fl2 / (train_ms * 1e-3) / 1e12}
+    # a layer with a bias and a residual added in its write-out
+    W = ps[0][2]
+    bias = torch.from_numpy(S.features(1, 64, 46)[0]).to(dev)
+    plain_ms = timed(lambda: sscn.sparse_conv_forward(X, W, rb))
+    ex_ms = timed(lambda: sscn.sparse_conv_forward_ex(X, W, rb, bias=bias, residual=X))
+    out["bias_residual_layer"] = {"forward_ms": plain_ms, "forward_bias_residual_ms": ex_ms}
+
+    # 4-d SSC(3) (81 offsets) on moving shells, 16 time steps of 48^3 x 2, C = 32 fp32
+    c4 = S.moving_shells_4d()
+    t4 = torch.from_numpy(c4).to(dev)
+    size4 = (16, 48, 48, 48)
+    build_ms = _wall_ms(lambda: sscn.ssc_rulebook_build(t4, size4, 3), reps)
+    r4 = sscn.ssc_rulebook_build(t4, size4, 3)
+    X4 = torch.from_numpy(S.features(c4.shape[0], 32, S.SEED_FEAT + 47)).to(dev)
+    W4 = torch.from_numpy(S.weights(81, 32, 32, S.SEED_WEIGHT + 47)).to(dev)
+    f4_ms = timed(lambda: sscn.sparse_conv_forward(X4, W4, r4))
+    fl4 = 2.0 * 32 * 32 * r4.n_pairs
+    out["layer_4d"] = {"workload": "ssc3x3x3x3_t16_grid48_batch2_shells_c32_f32", "sites": int(c4.shape[0]),
+                       "pairs": int(r4.n_pairs), "rulebook_build_ms": build_ms, "forward_ms": f4_ms,
+                       "forward_tflops": fl4 / (f4_ms * 1e-3) / 1e12}
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -390,9 +563,12 @@ def main():
                                    "forward_ms": timed(lambda: sscn.sparse_conv_forward(tX, tW, rbs)),
                                    "dgrad_ms": timed(lambda: sscn.sparse_conv_backward(None, tW, tG, rbs, wgrad=False))}
         del rbs
-        result["extra"] = {"sc_then_ssc": sc_then_ssc(tc, size, stream, reps), "unet": unet_scenes(stream, 5)}
+        result["extra"] = {"sc_then_ssc": sc_then_ssc(tc, size, stream, reps), "unet": unet_scenes(stream, 5),
+                           "ops": ops_extra(tc, size, stream, reps)}
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(coords, size, X, W, G, args.cpu_seconds)
+        if not args.no_extra:
+            result["cpu_baseline"]["ops"] = cpu_ops(coords, size)
     print(json.dumps(result))
 
 

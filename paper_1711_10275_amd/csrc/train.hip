@@ -11,6 +11,8 @@
 // order.  No atomics, so every result is reproducible bit for bit.  The
 // passes stream the n x c matrix once (HBM-bound).
 #include <algorithm>
+#include <initializer_list>
+#include <utility>
 
 #include "internal.h"
 #include "numeric.h"
@@ -78,28 +80,153 @@ __global__ __launch_bounds__(256) void k_colreduce(const T* __restrict__ x, int6
   }
 }
 
-// Sums of the partials in workgroup order: tot[i * c + col].
-__device__ __forceinline__ void sum_partials(const double* __restrict__ partial, int blocks, int c, int col,
-                                             double& s0, double& s1) {
-  s0 = 0.0;
-  s1 = 0.0;
-  for (int b = 0; b < blocks; ++b) {
-    s0 += partial[((int64_t)b * 2) * c + col];
-    s1 += partial[((int64_t)b * 2 + 1) * c + col];
+// The same reductions for rows of whole 16-byte pieces (c e a multiple of
+// 16 and at most 1024 bytes, rows 16-byte aligned): lane l of a wavefront
+// loads piece l % LPR of row l / LPR (LPR = pieces per row) of RPW = 64 / LPR
+// rows at once, VPL = 16 / e channels, and keeps fp64 sums for them; a
+// workgroup takes a contiguous range of rows, U row groups in flight per
+// wavefront.  (One channel per lane and one row per wavefront load, as in
+// k_colreduce, left the passes latency-bound: 0.3-0.4 ms for 2M x 32 bf16.)
+// The lanes' sums are then added in a fixed order through LDS, so the result
+// is reproducible.
+template <typename T, int OP>
+__global__ __launch_bounds__(256) void k_colreduce_vec(const T* __restrict__ x, int64_t ldx, const T* __restrict__ da,
+                                                       int64_t ldd, int64_t n, int c, int64_t rows_per_block,
+                                                       const float* __restrict__ scale,
+                                                       const float* __restrict__ beta,
+                                                       const float* __restrict__ mean,
+                                                       const float* __restrict__ invstd,
+                                                       double* __restrict__ partial) {
+  constexpr int VPL = 16 / (int)sizeof(T);  // channels per lane
+  constexpr int U = 4;                      // row groups in flight per wavefront
+  __shared__ double red[4][64][2 * VPL];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lpr = c / VPL;                  // pieces per row
+  const int rpw = 64 / lpr;                 // rows per wavefront load
+  const int cg = lane % lpr, ro = lane / lpr;
+  const bool live = ro < rpw;
+  const int64_t r0 = (int64_t)blockIdx.x * rows_per_block, r1 = min<int64_t>(n, r0 + rows_per_block);
+  double a0[VPL], a1[VPL];
+  float mu[VPL], sc[VPL], be[VPL], is[VPL];
+#pragma unroll
+  for (int v = 0; v < VPL; ++v) {
+    a0[v] = 0.0;
+    a1[v] = 0.0;
+    mu[v] = sc[v] = be[v] = is[v] = 0.f;
   }
+  if constexpr (OP == kBnBack) {
+    if (live) {
+#pragma unroll
+      for (int v = 0; v < VPL; ++v) {
+        const int col = cg * VPL + v;
+        mu[v] = mean[col];
+        sc[v] = scale[col];
+        be[v] = beta[col];
+        is[v] = invstd[col];
+      }
+    }
+  }
+  auto vals = [](const uint4& q, float (&f)[VPL]) {
+    if constexpr (sizeof(T) == 4) {
+      f[0] = __uint_as_float(q.x); f[1] = __uint_as_float(q.y); f[2] = __uint_as_float(q.z); f[3] = __uint_as_float(q.w);
+    } else {
+      const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        f[2 * i] = __uint_as_float(w[i] << 16);
+        f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+      }
+    }
+  };
+  const int64_t step = 4 * (int64_t)rpw;  // rows per workgroup load
+  for (int64_t base = r0 + (int64_t)wave * rpw + ro; base < r1; base += U * step) {
+    uint4 qx[U], qd[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t r = base + u * step;
+      const bool ok = live && r < r1;
+      qx[u] = ok ? *reinterpret_cast<const uint4*>(x + r * ldx + cg * VPL) : make_uint4(0, 0, 0, 0);
+      if constexpr (OP == kBnBack)
+        qd[u] = ok ? *reinterpret_cast<const uint4*>(da + r * ldd + cg * VPL) : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (!(live && base + u * step < r1)) continue;
+      float fx[VPL];
+      vals(qx[u], fx);
+      if constexpr (OP == kBnBack) {
+        float fd[VPL];
+        vals(qd[u], fd);
+#pragma unroll
+        for (int v = 0; v < VPL; ++v) {
+          const float dz = bn_pre(fx[v], mu[v], sc[v], be[v]) > 0.f ? fd[v] : 0.f;
+          a0[v] += dz;
+          a1[v] += (double)dz * (double)((fx[v] - mu[v]) * is[v]);
+        }
+      } else {
+#pragma unroll
+        for (int v = 0; v < VPL; ++v) {
+          a0[v] += fx[v];
+          if constexpr (OP == kSumSquares) a1[v] += (double)fx[v] * (double)fx[v];
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int v = 0; v < VPL; ++v) {
+    red[wave][lane][v] = a0[v];
+    red[wave][lane][VPL + v] = a1[v];
+  }
+  __syncthreads();
+  // value t: sum (t < c) or second sum (c <= t < 2 c) of channel t % c
+  for (int t = threadIdx.x; t < 2 * c; t += blockDim.x) {
+    const int kind = t / c, col = t % c, g = col / VPL, v = col % VPL;
+    double sum = 0.0;
+    for (int w = 0; w < 4; ++w)
+      for (int q = 0; q < rpw; ++q) sum += red[w][q * lpr + g][kind * VPL + v];
+    partial[((int64_t)blockIdx.x * 2 + kind) * c + col] = sum;
+  }
+}
+
+// Sums of the partials of the `blocks` workgroups for channel col: one
+// workgroup of 256 threads per 64 channels, wavefront w adding blocks
+// w, w + 4, .. in order and the four wavefronts' sums then added in order
+// (a fixed order: reproducible).  (One thread adding all blocks in turn took
+// ~0.25 ms for 1024 blocks.)
+__device__ __forceinline__ bool sum_partials(const double* __restrict__ partial, int blocks, int c, double& s0,
+                                             double& s1, int& col) {
+  __shared__ double red[2][4][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  col = blockIdx.x * 64 + lane;
+  double a0 = 0.0, a1 = 0.0;
+  if (col < c) {
+#pragma unroll 8
+    for (int b = wave; b < blocks; b += 4) {
+      a0 += partial[((int64_t)b * 2) * c + col];
+      a1 += partial[((int64_t)b * 2 + 1) * c + col];
+    }
+  }
+  red[0][wave][lane] = a0;
+  red[1][wave][lane] = a1;
+  __syncthreads();
+  if (wave != 0 || col >= c) return false;
+  s0 = ((red[0][0][lane] + red[0][1][lane]) + red[0][2][lane]) + red[0][3][lane];
+  s1 = ((red[1][0][lane] + red[1][1][lane]) + red[1][2][lane]) + red[1][3][lane];
+  return true;
 }
 
 // Batch statistics -> the affine map of the normalisation, and the running
 // (inference) statistics: mean, biased variance for the map, unbiased for
 // the running variance.
-__global__ void k_bn_finalize(const double* __restrict__ partial, int blocks, int c, int64_t n,
-                              const float* __restrict__ gamma, const float* __restrict__ beta, float eps,
-                              float momentum, float* running_mean, float* running_var, float* __restrict__ mean,
-                              float* __restrict__ invstd, float* __restrict__ scale, float* __restrict__ shift) {
-  const int col = blockIdx.x * blockDim.x + threadIdx.x;
-  if (col >= c) return;
+__global__ __launch_bounds__(256) void k_bn_finalize(const double* __restrict__ partial, int blocks, int c,
+                                                     int64_t n, const float* __restrict__ gamma,
+                                                     const float* __restrict__ beta, float eps, float momentum,
+                                                     float* running_mean, float* running_var,
+                                                     float* __restrict__ mean, float* __restrict__ invstd,
+                                                     float* __restrict__ scale, float* __restrict__ shift) {
   double s0, s1;
-  sum_partials(partial, blocks, c, col, s0, s1);
+  int col;
+  if (!sum_partials(partial, blocks, c, s0, s1, col)) return;
   const double mu = s0 / (double)n;
   const double var = fmax(s1 / (double)n - mu * mu, 0.0);
   const float is = (float)(1.0 / sqrt(var + (double)eps));
@@ -115,12 +242,11 @@ __global__ void k_bn_finalize(const double* __restrict__ partial, int blocks, in
   }
 }
 
-__global__ void k_two_sums(const double* __restrict__ partial, int blocks, int c, float* __restrict__ out0,
-                           float* __restrict__ out1) {
-  const int col = blockIdx.x * blockDim.x + threadIdx.x;
-  if (col >= c) return;
+__global__ __launch_bounds__(256) void k_two_sums(const double* __restrict__ partial, int blocks, int c,
+                                                  float* __restrict__ out0, float* __restrict__ out1) {
   double s0, s1;
-  sum_partials(partial, blocks, c, col, s0, s1);
+  int col;
+  if (!sum_partials(partial, blocks, c, s0, s1, col)) return;
   out0[col] = (float)s0;
   if (out1) out1[col] = (float)s1;
 }
@@ -172,6 +298,135 @@ __global__ void k_add(const T* __restrict__ a, int64_t lda, const T* __restrict_
     const int col = (int)(i - r * c);
     st(y + r * ldy + col, ld(a + r * lda + col) + ld(b + r * ldb + col));
   }
+}
+
+// The row-wise passes for rows of whole 16-byte pieces (the layout of
+// k_colreduce_vec: lane l handles VPL = 16 / e channels of row l / LPR of
+// each wavefront's group of RPW = 64 / LPR rows), 16 bytes per load and
+// store; MODE 0: relu((x - mean) * scale + beta), 1: the input gradient of
+// that (as k_bn_back_input), 2: a + b.  (One element per lane with a 64-bit
+// division per element ran the 2M x 32 bf16 passes at ~30% of HBM.)
+template <typename T, int MODE>
+__global__ __launch_bounds__(256) void k_rows_vec(const T* __restrict__ a, int64_t lda, const T* __restrict__ b,
+                                                  int64_t ldb, const T* __restrict__ add, int64_t ldadd, int64_t n,
+                                                  int c, const float* __restrict__ gamma,
+                                                  const float* __restrict__ mean, const float* __restrict__ scale,
+                                                  const float* __restrict__ beta, const float* __restrict__ invstd,
+                                                  const float* __restrict__ dgamma, const float* __restrict__ dbeta,
+                                                  T* __restrict__ y, int64_t ldy) {
+  constexpr int VPL = 16 / (int)sizeof(T);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lpr = c / VPL, rpw = 64 / lpr;
+  const int cg = lane % lpr, ro = lane / lpr;
+  if (ro >= rpw) return;
+  // per-channel constants: k0 = mean, k1 = scale, k2 = beta, k3 = invstd,
+  // k4 = dbeta / n, k5 = dgamma / n, k6 = gamma invstd
+  float k0[VPL], k1[VPL], k2[VPL], k3[VPL], k4[VPL], k5[VPL], k6[VPL];
+  const float inv_n = 1.f / (float)max<int64_t>(n, 1);
+#pragma unroll
+  for (int v = 0; v < VPL; ++v) {
+    const int col = cg * VPL + v;
+    k0[v] = k1[v] = k2[v] = k3[v] = k4[v] = k5[v] = k6[v] = 0.f;
+    if constexpr (MODE == 0) {
+      k0[v] = mean[col]; k1[v] = scale[col]; k2[v] = beta[col];
+    } else if constexpr (MODE == 1) {
+      k0[v] = mean[col]; k1[v] = scale[col]; k2[v] = beta[col]; k3[v] = invstd[col];
+      k4[v] = dbeta[col] * inv_n; k5[v] = dgamma[col] * inv_n; k6[v] = gamma[col] * invstd[col];
+    }
+  }
+  auto unpack = [](const uint4& q, float (&f)[VPL]) {
+    if constexpr (sizeof(T) == 4) {
+      f[0] = __uint_as_float(q.x); f[1] = __uint_as_float(q.y); f[2] = __uint_as_float(q.z); f[3] = __uint_as_float(q.w);
+    } else {
+      const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        f[2 * i] = __uint_as_float(w[i] << 16);
+        f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+      }
+    }
+  };
+  auto pack = [](const float (&f)[VPL]) {
+    uint4 q;
+    if constexpr (sizeof(T) == 4) {
+      q.x = __float_as_uint(f[0]); q.y = __float_as_uint(f[1]); q.z = __float_as_uint(f[2]); q.w = __float_as_uint(f[3]);
+    } else {
+      uint32_t w[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w[i] = (uint32_t)f32_bf16_bits(f[2 * i]) | ((uint32_t)f32_bf16_bits(f[2 * i + 1]) << 16);
+      q.x = w[0]; q.y = w[1]; q.z = w[2]; q.w = w[3];
+    }
+    return q;
+  };
+  const int64_t step = (int64_t)gridDim.x * 4 * rpw;
+  for (int64_t r = ((int64_t)blockIdx.x * 4 + wave) * rpw + ro; r < n; r += step) {
+    float fa[VPL], fo[VPL];
+    unpack(*reinterpret_cast<const uint4*>(a + r * lda + cg * VPL), fa);
+    if constexpr (MODE == 0) {
+#pragma unroll
+      for (int v = 0; v < VPL; ++v) fo[v] = fmaxf(0.f, bn_pre(fa[v], k0[v], k1[v], k2[v]));
+    } else if constexpr (MODE == 1) {
+      float fx[VPL];  // a = dA, b = x
+      unpack(*reinterpret_cast<const uint4*>(b + r * ldb + cg * VPL), fx);
+#pragma unroll
+      for (int v = 0; v < VPL; ++v) {
+        const float dz = bn_pre(fx[v], k0[v], k1[v], k2[v]) > 0.f ? fa[v] : 0.f;
+        const float xhat = (fx[v] - k0[v]) * k3[v];
+        fo[v] = k6[v] * (dz - k4[v] - xhat * k5[v]);
+      }
+      if (add) {
+        float fd[VPL];
+        unpack(*reinterpret_cast<const uint4*>(add + r * ldadd + cg * VPL), fd);
+#pragma unroll
+        for (int v = 0; v < VPL; ++v) fo[v] += fd[v];
+      }
+    } else {
+      float fb[VPL];
+      unpack(*reinterpret_cast<const uint4*>(b + r * ldb + cg * VPL), fb);
+#pragma unroll
+      for (int v = 0; v < VPL; ++v) fo[v] = fa[v] + fb[v];
+    }
+    *reinterpret_cast<uint4*>(y + r * ldy + cg * VPL) = pack(fo);
+  }
+}
+
+// Whether matrices of c channels suit k_rows_vec (each pointer 16-byte
+// aligned with a row stride of whole 16-byte pieces; nullptr is fine).
+bool rows_vec_ok(sscn_dtype dtype, int c, std::initializer_list<std::pair<const void*, int64_t>> mats) {
+  const int e = dtype == SSCN_F32 ? 4 : 2;
+  if ((int64_t)c * e % 16 != 0 || (int64_t)c * e > 1024) return false;
+  for (const auto& m : mats)
+    if (m.first && (reinterpret_cast<uintptr_t>(m.first) % 16 != 0 || m.second * e % 16 != 0)) return false;
+  return true;
+}
+
+template <int MODE>
+sscn_status rows_vec(sscn_dtype dtype, const void* a, int64_t lda, const void* b, int64_t ldb, const void* add,
+                     int64_t ldadd, int64_t n, int c, const float* gamma, const float* mean, const float* scale,
+                     const float* beta, const float* invstd, const float* dgamma, const float* dbeta, void* y,
+                     int64_t ldy, hipStream_t s);
+
+unsigned rows_vec_grid(int64_t n, int c, sscn_dtype dtype) {
+  const int vpl = dtype == SSCN_F32 ? 4 : 8;
+  const int64_t rpw = 64 / (c / vpl);
+  return (unsigned)std::max<int64_t>(1, std::min<int64_t>(ceil_div(n, 4 * rpw), 4096));
+}
+
+template <int MODE>
+sscn_status rows_vec(sscn_dtype dtype, const void* a, int64_t lda, const void* b, int64_t ldb, const void* add,
+                     int64_t ldadd, int64_t n, int c, const float* gamma, const float* mean, const float* scale,
+                     const float* beta, const float* invstd, const float* dgamma, const float* dbeta, void* y,
+                     int64_t ldy, hipStream_t s) {
+  const unsigned g = rows_vec_grid(n, c, dtype);
+  if (dtype == SSCN_F32)
+    k_rows_vec<float, MODE><<<g, 256, 0, s>>>((const float*)a, lda, (const float*)b, ldb, (const float*)add, ldadd, n,
+                                              c, gamma, mean, scale, beta, invstd, dgamma, dbeta, (float*)y, ldy);
+  else
+    k_rows_vec<uint16_t, MODE><<<g, 256, 0, s>>>((const uint16_t*)a, lda, (const uint16_t*)b, ldb,
+                                                 (const uint16_t*)add, ldadd, n, c, gamma, mean, scale, beta, invstd,
+                                                 dgamma, dbeta, (uint16_t*)y, ldy);
+  SSCN_HIP(hipGetLastError());
+  return SSCN_OK;
 }
 
 // Softmax and negative log-likelihood, one wavefront per row (lanes over
@@ -229,10 +484,19 @@ __global__ __launch_bounds__(256) void k_softmax_nll(const T* __restrict__ z, in
   if (threadIdx.x == 0) partial[blockIdx.x] = red[0] + red[1] + red[2] + red[3];
 }
 
-__global__ void k_loss_finalize(const double* __restrict__ partial, int blocks, int64_t n, float* __restrict__ loss) {
-  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+// One wavefront: lane l adds blocks l, l + 64, .. in order, then lane 0 adds
+// the 64 lane sums in order.
+__global__ __launch_bounds__(64) void k_loss_finalize(const double* __restrict__ partial, int blocks, int64_t n,
+                                                      float* __restrict__ loss) {
+  __shared__ double red[64];
+  const int l = threadIdx.x;
+  double a = 0.0;
+  for (int b = l; b < blocks; b += 64) a += partial[b];
+  red[l] = a;
+  __syncthreads();
+  if (l != 0) return;
   double s = 0.0;
-  for (int b = 0; b < blocks; ++b) s += partial[b];
+  for (int i = 0; i < 64; ++i) s += red[i];
   loss[0] = (float)(s / (double)n);
 }
 
@@ -267,10 +531,30 @@ sscn_status check_dtype(sscn_dtype dtype) {
   return SSCN_OK;
 }
 
+// Whether the rows suit k_colreduce_vec: whole 16-byte pieces, at most 1024
+// bytes, 16-byte aligned (both matrices).
+bool colreduce_vec_ok(sscn_dtype dtype, const void* x, int64_t ldx, const void* da, int64_t ldd, int c) {
+  const int e = dtype == SSCN_F32 ? 4 : 2;
+  auto al = [&](const void* p, int64_t ld) { return !p || (reinterpret_cast<uintptr_t>(p) % 16 == 0 && ld * e % 16 == 0); };
+  return (int64_t)c * e % 16 == 0 && (int64_t)c * e <= 1024 && al(x, ldx) && al(da, ldd);
+}
+
 template <int OP>
 sscn_status colreduce(sscn_dtype dtype, const void* x, int64_t ldx, const void* da, int64_t ldd, int64_t n, int c,
                       const float* scale, const float* beta, const float* mean, const float* invstd, double* partial,
                       int blocks, hipStream_t s) {
+  if (colreduce_vec_ok(dtype, x, ldx, da, ldd, c)) {
+    const int64_t rpb = ceil_div(std::max<int64_t>(n, 1), blocks);
+    if (dtype == SSCN_F32)
+      k_colreduce_vec<float, OP><<<(unsigned)blocks, 256, 0, s>>>((const float*)x, ldx, (const float*)da, ldd, n, c,
+                                                                  rpb, scale, beta, mean, invstd, partial);
+    else
+      k_colreduce_vec<uint16_t, OP><<<(unsigned)blocks, 256, 0, s>>>((const uint16_t*)x, ldx, (const uint16_t*)da,
+                                                                     ldd, n, c, rpb, scale, beta, mean, invstd,
+                                                                     partial);
+    SSCN_HIP(hipGetLastError());
+    return SSCN_OK;
+  }
   const dim3 grid((unsigned)blocks, (unsigned)ceil_div(c, kColChunk));
   if (dtype == SSCN_F32)
     k_colreduce<float, OP><<<grid, 256, 0, s>>>((const float*)x, ldx, (const float*)da, ldd, n, c, scale, beta, mean,
@@ -312,7 +596,7 @@ extern "C" sscn_status sscn_batchnorm_forward(const void* x, int64_t ldx, int64_
   SSCN_TRY(part.alloc(blocks, c));
   SSCN_TRY(colreduce<kSumSquares>(dtype, x, ldx, nullptr, 0, n, c, nullptr, nullptr, nullptr, nullptr, part.p, blocks,
                                   stream));
-  k_bn_finalize<<<(unsigned)ceil_div(c, 256), 256, 0, stream>>>(part.p, blocks, c, n, gamma, beta, eps, momentum,
+  k_bn_finalize<<<(unsigned)ceil_div(c, 64), 256, 0, stream>>>(part.p, blocks, c, n, gamma, beta, eps, momentum,
                                                                 running_mean, running_var, mean, invstd, scale, shift);
   SSCN_HIP(hipGetLastError());
   return SSCN_OK;
@@ -326,6 +610,9 @@ extern "C" sscn_status sscn_batchnorm_relu_apply(const void* x, int64_t ldx, int
   SSCN_TRY(check_mat(y, ldy, n, c, "y"));
   if (!mean || !scale || !beta) return fail(SSCN_ERR_INVALID_ARG, "NULL mean, scale or beta");
   if (n == 0) return SSCN_OK;
+  if (rows_vec_ok(dtype, c, {{x, ldx}, {y, ldy}}))
+    return rows_vec<0>(dtype, x, ldx, nullptr, 0, nullptr, 0, n, c, nullptr, mean, scale, beta, nullptr, nullptr,
+                       nullptr, y, ldy, stream);
   const unsigned g = grid_1d(n * c);
   if (dtype == SSCN_F32)
     k_bn_relu_apply<float><<<g, 256, 0, stream>>>((const float*)x, ldx, n, c, mean, scale, beta, (float*)y, ldy);
@@ -349,7 +636,7 @@ extern "C" sscn_status sscn_batchnorm_relu_backward_params(const void* da, int64
   Partials part(stream);
   SSCN_TRY(part.alloc(blocks, c));
   SSCN_TRY(colreduce<kBnBack>(dtype, x, ldx, da, ldd, n, c, scale, beta, mean, invstd, part.p, blocks, stream));
-  k_two_sums<<<(unsigned)ceil_div(c, 256), 256, 0, stream>>>(part.p, blocks, c, dbeta, dgamma);
+  k_two_sums<<<(unsigned)ceil_div(c, 64), 256, 0, stream>>>(part.p, blocks, c, dbeta, dgamma);
   SSCN_HIP(hipGetLastError());
   return SSCN_OK;
 }
@@ -368,6 +655,9 @@ extern "C" sscn_status sscn_batchnorm_relu_backward_input(const void* da, int64_
   if (!gamma || !scale || !beta || !mean || !invstd || !dgamma || !dbeta)
     return fail(SSCN_ERR_INVALID_ARG, "NULL parameters or statistics");
   if (n == 0) return SSCN_OK;
+  if (rows_vec_ok(dtype, c, {{da, ldd}, {x, ldx}, {add, ld_add}, {dx, ldx_out}}))
+    return rows_vec<1>(dtype, da, ldd, x, ldx, add, ld_add, n, c, gamma, mean, scale, beta, invstd, dgamma, dbeta, dx,
+                       ldx_out, stream);
   const unsigned g = grid_1d(n * c);
   if (dtype == SSCN_F32)
     k_bn_back_input<float><<<g, 256, 0, stream>>>((const float*)da, ldd, (const float*)x, ldx, n, c, gamma, scale,
@@ -391,7 +681,7 @@ extern "C" sscn_status sscn_column_sum(const void* x, int64_t ldx, int64_t n, in
   SSCN_TRY(part.alloc(blocks, c));
   SSCN_TRY(colreduce<kSums>(dtype, x, ldx, nullptr, 0, n, c, nullptr, nullptr, nullptr, nullptr, part.p, blocks,
                             stream));
-  k_two_sums<<<(unsigned)ceil_div(c, 256), 256, 0, stream>>>(part.p, blocks, c, out, nullptr);
+  k_two_sums<<<(unsigned)ceil_div(c, 64), 256, 0, stream>>>(part.p, blocks, c, out, nullptr);
   SSCN_HIP(hipGetLastError());
   return SSCN_OK;
 }
@@ -403,6 +693,9 @@ extern "C" sscn_status sscn_add(const void* a, int64_t lda, const void* b, int64
   SSCN_TRY(check_mat(b, ldb, n, c, "b"));
   SSCN_TRY(check_mat(y, ldy, n, c, "y"));
   if (n == 0) return SSCN_OK;
+  if (rows_vec_ok(dtype, c, {{a, lda}, {b, ldb}, {y, ldy}}))
+    return rows_vec<2>(dtype, a, lda, b, ldb, nullptr, 0, n, c, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+                       nullptr, y, ldy, stream);
   const unsigned g = grid_1d(n * c);
   if (dtype == SSCN_F32)
     k_add<float><<<g, 256, 0, stream>>>((const float*)a, lda, (const float*)b, ldb, n, c, (float*)y, ldy);

@@ -274,6 +274,25 @@ def labels(n, n_classes, seed):
     return np.random.default_rng(seed).integers(0, n_classes, n).astype(np.int32)
 
 
+def moving_shells_4d(seed=SEED_GEOM + 21, batch=2, T=16, L=48, shells=3):
+    """Sparse 4-d sets (time x a 3-d grid, the kind of data RGB-D video
+    gives): per sample, sphere shells of radius U(8, 14) whose centres move
+    linearly in time (up to L / 4 over the T steps), each time step
+    voxelised like sphere_shell.  Rows (b, t, x0, x1, x2), sorted."""
+    rng = np.random.default_rng(seed)
+    rows = []
+    for b in range(batch):
+        objs = [(rng.uniform(0.35 * L, 0.65 * L, 3), rng.uniform(-0.25, 0.25, 3) * L / max(T - 1, 1),
+                 rng.uniform(8, 14)) for _ in range(shells)]
+        for t in range(T):
+            pts = np.concatenate([sphere_shell(q + v * t, r, L) for q, v, r in objs])
+            pts = np.unique(pts, axis=0)
+            rows.append(np.concatenate([np.full((pts.shape[0], 1), b, np.int64), np.full((pts.shape[0], 1), t,
+                                                                                      np.int64), pts], axis=1))
+    c = np.unique(np.concatenate(rows), axis=0)
+    return c.astype(np.int32)
+
+
 def scenes_small(seed=SEED_GEOM + 13, batch=2, L=64, target_per_sample=15_000):
     """The indoor-scene recipe on a small grid (end-to-end network checks)."""
     return scenes_256(seed=seed, batch=batch, L=L, target_per_sample=target_per_sample)
