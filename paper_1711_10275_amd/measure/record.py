@@ -232,6 +232,17 @@ def record_all(d, out=PROFILES):
            f"  SC(2,2) forward fp32 {e['sc_forward_ms_f32'] * 1e3:.1f} us, bf16 {e['sc_forward_ms_bf16'] * 1e3:.1f} "
            f"us; SSC 64^3 C=96 fp32 {e['ssc_forward_ms_f32'] * 1e3:.1f} us, bf16 "
            f"{e['ssc_forward_ms_bf16'] * 1e3:.1f} us", ""]
+    o = b["extra"].get("ops")
+    if o:
+        f = lambda d: f"{d['ms'] * 1e3:.1f} us ({100 * d['frac']:.0f}% of HBM)"
+        pl, bn = o["pool"]["f32"], o["batchnorm"]["scenes256_c32_bf16"]
+        txt += [f"  MP forward / backward (SC(2,2), C = 64 fp32) {f(pl['max_forward'])} / {f(pl['max_backward'])}; "
+                f"upsampling {f(pl['upsample_forward'])}",
+                f"  BN at 2M x 32 bf16: statistics {f(bn['stats'])}, apply {f(bn['apply_relu'])}, parameter "
+                f"gradients {f(bn['backward_params'])}, input gradient {f(bn['backward_input'])}",
+                f"  U-Net training step (256^3 x 8, bf16) {o['unet_train_step']['ms']:.2f} ms; residual block "
+                f"forward {o['residual_block']['forward_ms'] * 1e3:.0f} us; 4-d SSC(3) layer forward "
+                f"{o['layer_4d']['forward_ms'] * 1e3:.0f} us", ""]
     tot = sum(r[1] * r[2] for r in stats)
     rows = [(r[0][:64], r[1], r[2], r[1] * r[2] / 1e3, r[5]) for r in stats if r[5] >= 0.25]
     txt.append(table(rows, f"{'kernel (all launches of the run)':64s} {'calls':>6s} {'avg us':>9s} "
