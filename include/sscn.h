@@ -73,7 +73,9 @@ typedef struct sscn_rulebook_s* sscn_rulebook;
  * The output set equals the input set and output row k is input row k.
  * Builds a GPU open-addressing dictionary, probes the f^3 neighbours of
  * every site and compacts the hits into R.  Blocks the host once to read
- * back sizes and error flags.
+ * back sizes and error flags; the row-block plan that the layer kernels
+ * use is queued behind that readback and may still be running on `stream`
+ * when the call returns (work on other streams waits for it).
  */
 sscn_status ssc_rulebook_build(const int32_t* coords, int64_t n, const int32_t* spatial_size,
                                int32_t filter_size, hipStream_t stream, sscn_rulebook* out);

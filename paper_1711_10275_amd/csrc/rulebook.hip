@@ -975,21 +975,42 @@ static sscn_status owned_alloc(RulebookData* d, Arena& a, hipStream_t s) {
   return SSCN_OK;
 }
 
-// Pinned host staging for the single readback of a build.
-static sscn_status readback(void* host, const void* dev, size_t bytes, hipStream_t s) {
-  static thread_local void* pinned = nullptr;
-  static thread_local size_t pinned_bytes = 0;
-  if (pinned_bytes < bytes) {
-    if (pinned) (void)hipHostFree(pinned);
-    pinned = nullptr;
-    pinned_bytes = 0;
-    SSCN_HIP(hipHostMalloc(&pinned, std::max<size_t>(bytes, 4096), hipHostMallocDefault));
-    pinned_bytes = std::max<size_t>(bytes, 4096);
+// The single readback of a build, through pinned host staging, in two
+// halves: readback_begin queues the copy and an event behind it, so that
+// more work can be queued after it before readback_end waits for the copy
+// alone (the GPU then runs that work while the host returns to its caller).
+// One readback in flight per host thread.
+struct ReadbackState {
+  void* pinned = nullptr;
+  size_t bytes = 0;
+  hipEvent_t done = nullptr;
+};
+static thread_local ReadbackState t_readback;
+
+static sscn_status readback_begin(const void* dev, size_t bytes, hipStream_t s) {
+  ReadbackState& r = t_readback;
+  if (r.bytes < bytes) {
+    if (r.pinned) (void)hipHostFree(r.pinned);
+    r.pinned = nullptr;
+    r.bytes = 0;
+    SSCN_HIP(hipHostMalloc(&r.pinned, std::max<size_t>(bytes, 4096), hipHostMallocDefault));
+    r.bytes = std::max<size_t>(bytes, 4096);
   }
-  SSCN_HIP(hipMemcpyAsync(pinned, dev, bytes, hipMemcpyDeviceToHost, s));
-  SSCN_HIP(hipStreamSynchronize(s));
-  std::memcpy(host, pinned, bytes);
+  if (!r.done) SSCN_HIP(hipEventCreateWithFlags(&r.done, hipEventDisableTiming));
+  SSCN_HIP(hipMemcpyAsync(r.pinned, dev, bytes, hipMemcpyDeviceToHost, s));
+  SSCN_HIP(hipEventRecord(r.done, s));
   return SSCN_OK;
+}
+
+static sscn_status readback_end(void* host, size_t bytes) {
+  SSCN_HIP(hipEventSynchronize(t_readback.done));
+  std::memcpy(host, t_readback.pinned, bytes);
+  return SSCN_OK;
+}
+
+static sscn_status readback(void* host, const void* dev, size_t bytes, hipStream_t s) {
+  SSCN_TRY(readback_begin(dev, bytes, s));
+  return readback_end(host, bytes);
 }
 
 static sscn_status launch_fill_slots(Slot* t, uint64_t cap, int32_t row_init, hipStream_t s,
@@ -1726,13 +1747,19 @@ static sscn_status ssc_build(const int32_t* coords, int64_t n, const int32_t* sp
       return SSCN_OK;
     };
     if (one_phase) SSCN_TRY(compact());
+    // The sizes and flags are final here.  The plan is queued behind their
+    // copy: the host waits for the copy only, and the plan's kernels run
+    // while it returns (uses of the plan on other streams wait for
+    // plan_ready).
+    const size_t stat_bytes = sizeof(unsigned long long) * (1 + K);
+    SSCN_TRY(readback_begin(stats, stat_bytes, s));
     if (eager_plan) {
       SSCN_TRY(build_plan(d, d->fwd, n, K, s, /*a site has one neighbour per offset*/ n, hist));
       SSCN_HIP(hipEventCreateWithFlags(&d->plan_ready, hipEventDisableTiming));
       SSCN_HIP(hipEventRecord(d->plan_ready, s));
     }
     std::vector<unsigned long long> host(1 + K);
-    SSCN_TRY(readback(host.data(), stats, sizeof(unsigned long long) * (1 + K), s));
+    SSCN_TRY(readback_end(host.data(), stat_bytes));
     if (!(host[0] & kFlagOutOfRange) && (host[0] & kFlagWideKey)) {
       *wide = true;  // the queued work is discarded with d and the temporaries
       return SSCN_OK;
