@@ -200,22 +200,25 @@ def table_capacity(n):
     return cap
 
 
-def build_roofline(n, K, pairs, ms, what, slot=8):
+def build_roofline(n, K, pairs, ms, what, slot=16):
     """Algorithmic bytes of an SSC rule-book build against HBM bandwidth.
 
-    Counted: coordinates read (16 B per site), the dictionary filled and its
-    slots written (slot bytes each: 8 for the 32-bit keys that both
-    workloads here use; capacity the power of two >= 2n), one slot read per
+    Counted: coordinates read (16 B per site), the dictionary filled (slot
+    bytes per slot: 16 for the grouped slots of the 32-bit keys that both
+    workloads here use; capacity the power of two >= 2n slots), the inserts
+    (a group key and a row, 8 B per site), the two words (8 B) read per
     lookup performed (K per site below 2^18 sites; from 2^18 the mirrored
     probe looks up only the (K - 1) / 2 offsets below the centre and derives
     the rest), and the pair arrays written (8 B per pair).  Not counted: the
     builder's neighbour map (4 B per site and offset, written and read back),
-    reported as `intermediate_bytes`.  The time is the host wall time of the
-    build call (its row-block plan and readback included).
+    reported as `intermediate_bytes`.  The time is the mean host wall time
+    of back-to-back build calls: each call waits for its own readback of
+    sizes and flags, and the row-block plan it queues behind that readback
+    runs before the next call's kernels.
     """
     cap = table_capacity(n)
     lookups = K * n if n < (1 << 18) else (K - 1) // 2 * n
-    nbytes = 16 * n + 2 * slot * cap + slot * lookups + 8 * pairs
+    nbytes = 16 * n + slot * cap + 8 * n + 8 * lookups + 8 * pairs
     achieved = nbytes / (ms * 1e-3) / 1e9
     return {"stage": what, "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": achieved / PEAK_HBM_GBS, "bytes": nbytes, "ms": ms, "intermediate_bytes": 8 * K * n}

@@ -1,13 +1,14 @@
 // Rule-book construction on the GPU (Sec. 4.2 of the paper).
 //
-// Dictionary: open addressing with linear probing in HBM.  A slot holds the
-// location (b, x0, x1, x2) as a key and the feature row.  SSC builds use
-// 8-byte slots {32-bit key, row} with the key the linear index
-// ((b L0 + x0) L1 + x1) L2 + x2 whenever every batch index present keeps it
-// below 2^32 - 1 (the empty marker); the insert flags a batch index beyond
-// that and the build is redone with 16-byte slots {64-bit key, row} (16
-// bits per field, b < 2^15 so no key equals the empty marker), which the SC
-// builds always use.  Capacity is a power of two >= 2n (load <= 1/2).
+// Dictionary: open addressing with linear probing in HBM.  SSC builds key a
+// location by its linear index ((b L0 + x0) L1 + x1) L2 + x2 whenever every
+// batch index present keeps it below 2^32 - 1, and store it by group: a
+// 16-byte slot holds the group key (linear key / 3) and the rows of the
+// group's 3 consecutive linear keys, so that the x2 neighbours of nearby
+// sites share slots.  The insert flags a batch index beyond that limit and
+// the build is redone with 16-byte slots {64-bit key, row} (16 bits per
+// field, b < 2^15 so no key equals the empty marker), which the SC builds
+// always use.  Capacity is a power of two >= 2n slots (load <= 1/2).
 //
 // Rule book layout: output rows are cut into tiles of kTile = 64 rows (one
 // wavefront); for every offset o and tile t the pairs whose output row lies
@@ -111,31 +112,46 @@ __device__ __forceinline__ uint32_t mix32(uint32_t h) {
   return h;
 }
 
-// Home slot of a 32-bit key.  (Keeping runs of consecutive keys in
-// consecutive slots, so that x2 neighbours share a window, clusters the
-// table: the inserts and lookups then take longer, not shorter.)
-__device__ __forceinline__ uint32_t home8(uint32_t key, uint32_t mask) { return mix32(key) & mask; }
+// Grouped slots of the 32-bit keys: word 0 the group key (all ones =
+// empty), words 1..3 the rows of keys 3 g .. 3 g + 2 (all ones = -1 =
+// absent).  A wavefront's 64 consecutive surface sites and three offsets
+// along x2 touch about 60 such slots, against about 125 when every key has
+// a slot of its own (storing runs of consecutive keys in consecutive slots
+// of such a table instead clusters it, which made inserts and lookups
+// slower).  Measured on 2M scene sites: the probe 232 -> 190 us and the
+// insert 104 -> 82 us, against a fill of twice the bytes (9 -> 13 us);
+// groups of 7 in 32-byte slots touch fewer slots (about 44) but took longer
+// (probe 200 us, fill 22 us), and lower or higher loads did not help.
+constexpr uint32_t kGroupKeys = 3;
+constexpr int kGroupWords = 4;  // 16 bytes per slot
 
-// Every 8-byte slot empty; zeroes the first n_zero words of `zero`.
-__global__ void k_fill_slots8(uint4* __restrict__ table, uint64_t pairs,
+__device__ __forceinline__ uint32_t group_home(uint32_t group, uint32_t mask) { return mix32(group) & mask; }
+
+// Every word all ones (empty group keys, absent rows); zeroes the first
+// n_zero words of `zero`.
+__global__ void k_fill_slots8(uint4* __restrict__ table, uint64_t pieces,
                               unsigned long long* __restrict__ zero, int n_zero) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_zero; i += (int64_t)gridDim.x * blockDim.x)
     zero[i] = 0;
-  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < pairs;
+  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < pieces;
        i += (uint64_t)gridDim.x * blockDim.x)
     table[i] = make_uint4(~0u, ~0u, ~0u, ~0u);
 }
 
-// Insert with 8-byte slots, in two passes so that most sites need no
+// Insert into the grouped slots, in two passes so that most sites need no
 // atomic (device-wide atomics are far slower than stores):
-//  1. every site stores its word {key, row} into its home slot with a plain
-//     8-byte store; of the sites that share a home slot one word remains;
-//  2. every site reads its home slot back: its own word means it holds the
-//     slot; the same key with another row is a repeated location; otherwise
-//     the site probes on from the home slot with a 64-bit CAS per slot, as
-//     an ordinary linear-probing insert.
-// Slots never become empty again, so every slot between a key's home slot
-// and the slot that holds it is occupied, which is what lookups rely on.
+//  1. every site stores its group key into the group's home slot with a
+//     plain store; of the groups that share a home slot one key remains;
+//  2. every site reads its home slot back: its own group key means the
+//     group holds the slot (all its sites agree); otherwise the site probes
+//     on from the home slot with a CAS per slot, as an ordinary
+//     linear-probing insert (a slot that holds its group key already was
+//     claimed by another site of the group).  The site then stores its row
+//     in the slot.
+// Slots never become empty again, so every slot between a group's home slot
+// and the slot that holds it is occupied, which is what lookups rely on.  A
+// repeated location stores its row in the same word as the first; the probe
+// finds that (a site whose own lookup returns another row).
 // batch_lim: batch indices below it keep every key of their sample below
 // the empty marker; a larger one raises kFlagWideKey and inserts nothing.
 __device__ __forceinline__ int site_check8(const int4& c, int L0, int L1, int L2, uint32_t batch_lim) {
@@ -145,9 +161,8 @@ __device__ __forceinline__ int site_check8(const int4& c, int L0, int L1, int L2
 }
 
 __global__ __launch_bounds__(256) void k_insert8_store(const int4* __restrict__ coords, int64_t n, int L0, int L1,
-                                                       int L2, uint32_t batch_lim,
-                                                       unsigned long long* __restrict__ table, uint32_t mask,
-                                                       unsigned long long* __restrict__ flags,
+                                                       int L2, uint32_t batch_lim, uint32_t* __restrict__ table,
+                                                       uint32_t mask, unsigned long long* __restrict__ flags,
                                                        int4* __restrict__ copy) {
   int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (j >= n) return;
@@ -158,36 +173,28 @@ __global__ __launch_bounds__(256) void k_insert8_store(const int4* __restrict__ 
     atomicOr(flags, (unsigned long long)bad);
     return;
   }
-  const uint32_t key = pack_key32(c.x, c.y, c.z, c.w, L0, L1, L2);
-  table[home8(key, mask)] = ((unsigned long long)(uint32_t)j << 32) | key;
+  const uint32_t group = pack_key32(c.x, c.y, c.z, c.w, L0, L1, L2) / kGroupKeys;
+  table[(size_t)group_home(group, mask) * kGroupWords] = group;
 }
 
 __global__ __launch_bounds__(256) void k_insert8_fix(const int4* __restrict__ coords, int64_t n, int L0, int L1,
-                                                     int L2, uint32_t batch_lim,
-                                                     unsigned long long* __restrict__ table, uint32_t mask,
-                                                     unsigned long long* __restrict__ flags) {
+                                                     int L2, uint32_t batch_lim, uint32_t* __restrict__ table,
+                                                     uint32_t mask) {
   int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (j >= n) return;
   const int4 c = coords[j];
   if (site_check8(c, L0, L1, L2, batch_lim)) return;
   const uint32_t key = pack_key32(c.x, c.y, c.z, c.w, L0, L1, L2);
-  const unsigned long long word = ((unsigned long long)(uint32_t)j << 32) | key;
-  uint32_t slot = home8(key, mask);
-  const unsigned long long home = table[slot];
-  if (home == word) return;
-  if ((uint32_t)home == key) {
-    atomicOr(flags, (unsigned long long)kFlagDuplicate);
-    return;
-  }
-  while (true) {
-    slot = (slot + 1) & mask;
-    const unsigned long long prev = atomicCAS(&table[slot], ~0ull, word);
-    if (prev == ~0ull) return;
-    if ((uint32_t)prev == key) {
-      atomicOr(flags, (unsigned long long)kFlagDuplicate);
-      return;
+  const uint32_t group = key / kGroupKeys;
+  uint32_t slot = group_home(group, mask);
+  if (table[(size_t)slot * kGroupWords] != group) {
+    while (true) {
+      slot = (slot + 1) & mask;
+      const uint32_t prev = atomicCAS(&table[(size_t)slot * kGroupWords], kEmptyKey32, group);
+      if (prev == kEmptyKey32 || prev == group) break;
     }
   }
+  table[(size_t)slot * kGroupWords + 1 + key % kGroupKeys] = (uint32_t)j;
 }
 
 // Insert every site; flag coordinates outside the grid and repeated
@@ -241,7 +248,7 @@ template <int P, bool NARROW>
 __global__ __launch_bounds__(256) void k_ssc_probe(
     const int4* __restrict__ coords, int64_t n, int L0, int L1, int L2, int f,
     const void* __restrict__ table_v, uint64_t mask, int32_t* __restrict__ nbr, int64_t* __restrict__ counts,
-    int64_t n_tiles, int mirror) {
+    int64_t n_tiles, int mirror, uint32_t batch_lim, unsigned long long* __restrict__ flags) {
   const int lane = threadIdx.x & 63;
   const int plane = f * f, K = f * f * f;
   // Workgroup = 4 tiles x one slice of P offsets.  Logical order: tile
@@ -261,75 +268,115 @@ __global__ __launch_bounds__(256) void k_ssc_probe(
   const int h = (f - 1) / 2;
   const int o0 = (int)(lb % slices) * P;
   if (mirror && o0 == 0 && valid) nbr[(int64_t)ctr * n + k] = site_ok ? (int32_t)k : -1;
-  // A lookup reads the aligned window of 4 slots that holds its first slot
-  // (64 bytes of 16-byte slots, 32 of 8-byte ones), and the following
-  // windows while the probe sequence runs on (linear probing: stop at the
-  // key or at an empty slot), so most lookups take a single round trip.
-  using Key = typename std::conditional<NARROW, uint32_t, uint64_t>::type;
-  Key key[P];
-  uint64_t slot[P];
-  bool live[P];
-  Key vk[P][4];
-  int32_t vr[P][4];
-  // (2-slot windows of the 8-byte table probe as fast; 8-slot ones slower)
-  auto window = [&](uint64_t sl) -> uint64_t { return sl & ~3ull; };
-  auto read_window = [&](int q) {
-    const uint64_t w = window(slot[q]);
-    if constexpr (NARROW) {
-      const uint4* t = reinterpret_cast<const uint4*>(reinterpret_cast<const uint64_t*>(table_v) + w);
-      const uint4 a = t[0], b = t[1];
-      vk[q][0] = a.x; vr[q][0] = (int32_t)a.y; vk[q][1] = a.z; vr[q][1] = (int32_t)a.w;
-      vk[q][2] = b.x; vr[q][2] = (int32_t)b.y; vk[q][3] = b.z; vr[q][3] = (int32_t)b.w;
-    } else {
-      const Slot* t = reinterpret_cast<const Slot*>(table_v) + w;
+  int32_t rows[P];
+  if constexpr (NARROW) {
+    // Grouped slots: a lookup reads the group key and the key's row word of
+    // the group's home slot together (one round trip unless the slot holds
+    // another group), and walks on slot by slot to the group or to an empty
+    // slot.
+    const uint32_t* tb = reinterpret_cast<const uint32_t*>(table_v);
+    uint32_t grp[P], sub[P], slot[P], gw[P], rw[P];
+    bool live[P];
+    auto read_slot = [&](int q) {
+      gw[q] = tb[(size_t)slot[q] * kGroupWords];
+      rw[q] = tb[(size_t)slot[q] * kGroupWords + 1 + sub[q]];
+    };
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+      const int o = o0 + q;
+      const int i0 = o / plane, i1 = (o / f) % f, i2 = o % f;
+      const int y0 = c.y + i0 - h, y1 = c.z + i1 - h, y2 = c.w + i2 - h;
+      live[q] = o < o_end && site_ok && in_grid(y0, y1, y2, L0, L1, L2);
+      const uint32_t key = pack_key32(c.x, y0, y1, y2, L0, L1, L2);
+      grp[q] = key / kGroupKeys;
+      sub[q] = key % kGroupKeys;
+      slot[q] = group_home(grp[q], (uint32_t)mask);
+      if (live[q]) read_slot(q);
+    }
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+      rows[q] = -1;
+      bool done = !live[q];
+      while (!done) {
+        if (gw[q] == grp[q]) {
+          rows[q] = (int32_t)rw[q];
+          done = true;
+        } else if (gw[q] == kEmptyKey32) {
+          done = true;
+        } else {
+          slot[q] = (slot[q] + 1) & (uint32_t)mask;
+          read_slot(q);
+        }
+      }
+    }
+    // A repeated location stored its row in the same word as the first: the
+    // site whose own lookup returns another row reports it (one slice per
+    // site; sites past the batch limit were not inserted).
+    if (o0 == 0 && site_ok && (uint32_t)c.x < batch_lim) {
+      const uint32_t key = pack_key32(c.x, c.y, c.z, c.w, L0, L1, L2);
+      const uint32_t g0 = key / kGroupKeys, s0 = key % kGroupKeys;
+      uint32_t sl = group_home(g0, (uint32_t)mask);
+      while (tb[(size_t)sl * kGroupWords] != g0) sl = (sl + 1) & (uint32_t)mask;  // present: inserted
+      if (tb[(size_t)sl * kGroupWords + 1 + s0] != (uint32_t)k) atomicOr(flags, (unsigned long long)kFlagDuplicate);
+    }
+  } else {
+    // 16-byte slots: a lookup reads the aligned window of 4 slots (64 bytes)
+    // that holds its first slot, and the following windows while the probe
+    // sequence runs on (stop at the key or at an empty slot), so most
+    // lookups take a single round trip.
+    uint64_t key[P], slot[P];
+    bool live[P];
+    uint64_t vk[P][4];
+    int32_t vr[P][4];
+    auto window = [&](uint64_t sl) -> uint64_t { return sl & ~3ull; };
+    auto read_window = [&](int q) {
+      const Slot* tw = reinterpret_cast<const Slot*>(table_v) + window(slot[q]);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const Slot e = t[j];
+        const Slot e = tw[j];
         vk[q][j] = e.key;
         vr[q][j] = e.row;
       }
-    }
-  };
+    };
 #pragma unroll
-  for (int q = 0; q < P; ++q) {
-    const int o = o0 + q;
-    const int i0 = o / plane, i1 = (o / f) % f, i2 = o % f;
-    const int y0 = c.y + i0 - h, y1 = c.z + i1 - h, y2 = c.w + i2 - h;
-    live[q] = o < o_end && site_ok && in_grid(y0, y1, y2, L0, L1, L2);
-    if constexpr (NARROW) {
-      key[q] = pack_key32(c.x, y0, y1, y2, L0, L1, L2);
-      slot[q] = home8(key[q], (uint32_t)mask);
-    } else {
+    for (int q = 0; q < P; ++q) {
+      const int o = o0 + q;
+      const int i0 = o / plane, i1 = (o / f) % f, i2 = o % f;
+      const int y0 = c.y + i0 - h, y1 = c.z + i1 - h, y2 = c.w + i2 - h;
+      live[q] = o < o_end && site_ok && in_grid(y0, y1, y2, L0, L1, L2);
       key[q] = pack_key(c.x, y0, y1, y2);
       slot[q] = mix64(key[q]) & mask;
+      if (live[q]) read_window(q);
     }
-    if (live[q]) read_window(q);
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+      rows[q] = -1;
+      bool done = !live[q];
+      while (!done) {
+        const int from = (int)(slot[q] - window(slot[q]));
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if (!done && j >= from) {
+            if (vk[q][j] == key[q]) {
+              rows[q] = vr[q][j];
+              done = true;
+            } else if (vk[q][j] == kEmptyKey) {
+              done = true;
+            }
+          }
+        }
+        if (!done) {
+          slot[q] = (window(slot[q]) + 4) & mask;  // first slot of the next window
+          read_window(q);
+        }
+      }
+    }
   }
-  constexpr Key kEmpty = NARROW ? (Key)kEmptyKey32 : (Key)kEmptyKey;
 #pragma unroll
   for (int q = 0; q < P; ++q) {
     const int o = o0 + q;
     if (o >= o_end) break;  // uniform
-    int32_t row = -1;
-    bool done = !live[q];
-    while (!done) {
-      const int from = (int)(slot[q] - window(slot[q]));
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        if (!done && j >= from) {
-          if (vk[q][j] == key[q]) {
-            row = vr[q][j];
-            done = true;
-          } else if (vk[q][j] == kEmpty) {
-            done = true;
-          }
-        }
-      }
-      if (!done) {
-        slot[q] = (window(slot[q]) + 4) & mask;  // first slot of the next window
-        read_window(q);
-      }
-    }
+    const int32_t row = rows[q];
     if (valid) nbr[(int64_t)o * n + k] = row;
     if (mirror && row >= 0) nbr[(int64_t)(K - 1 - o) * n + row] = (int32_t)k;
     const unsigned long long bal = __ballot(row >= 0);
@@ -1662,14 +1709,14 @@ static sscn_status ssc_build(const int32_t* coords, int64_t n, const int32_t* sp
   {
     Temps tmp(s);
     const uint64_t cap = table_capacity(n);
-    Slot* table = nullptr; unsigned long long* table8 = nullptr;
+    Slot* table = nullptr; uint32_t* table8 = nullptr;  // table8: grouped slots of kGroupWords words
     int32_t* nbr; int64_t* counts; unsigned long long* stats; int32_t* hist = nullptr;
     // With K <= 32 the row-block plan is queued before the readback too: its
     // launches overlap the build's kernels and the host waits once.
     const bool one_phase = (uint64_t)K * (uint64_t)n * 8u <= (512ull << 20);
     const bool eager_plan = one_phase && n > 0 && K <= 32 && n < (int64_t)kPlanNoRow;
     Arena ta;
-    if (narrow) ta.add(&table8, cap); else ta.add(&table, cap);
+    if (narrow) ta.add(&table8, cap * kGroupWords); else ta.add(&table, cap);
     ta.add(&nbr, (size_t)K * n);
     ta.add(&counts, (size_t)K * n_tiles + 1);
     ta.add(&stats, 1 + K);
@@ -1694,8 +1741,9 @@ static sscn_status ssc_build(const int32_t* coords, int64_t n, const int32_t* sp
     SSCN_TRY(owned_alloc(d, oa, s));
 
     if (narrow) {
-      k_fill_slots8<<<(unsigned)std::min<uint64_t>((cap / 2 + 255) / 256, 16384), 256, 0, s>>>(
-          (uint4*)table8, cap / 2, stats, n_zero);
+      const uint64_t pieces = cap * kGroupWords / 4;  // 16-byte stores
+      k_fill_slots8<<<(unsigned)std::min<uint64_t>((pieces + 255) / 256, 16384), 256, 0, s>>>(
+          (uint4*)table8, pieces, stats, n_zero);
       SSCN_HIP(hipGetLastError());
     } else {
       SSCN_TRY(launch_fill_slots(table, cap, -1, s, stats, n_zero));
@@ -1706,7 +1754,7 @@ static sscn_status ssc_build(const int32_t* coords, int64_t n, const int32_t* sp
                                                         (uint32_t)(cap - 1), stats, (int4*)d->out_coords);
         SSCN_HIP(hipGetLastError());
         k_insert8_fix<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, L0, L1, L2, batch_lim, table8,
-                                                      (uint32_t)(cap - 1), stats);
+                                                      (uint32_t)(cap - 1));
       } else
         k_insert<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, L0, L1, L2, table, cap - 1, stats,
                                                  (int4*)d->out_coords);
@@ -1721,10 +1769,10 @@ static sscn_status ssc_build(const int32_t* coords, int64_t n, const int32_t* sp
       const unsigned grid = (unsigned)(grid_for(n_tiles * 64, 256) * slices);
       if (narrow)
         k_ssc_probe<P, true><<<grid, 256, 0, s>>>((const int4*)coords, n, L0, L1, L2, f, table8, cap - 1, nbr,
-                                                   counts, n_tiles, mirror ? 1 : 0);
+                                                   counts, n_tiles, mirror ? 1 : 0, batch_lim, stats);
       else
         k_ssc_probe<P, false><<<grid, 256, 0, s>>>((const int4*)coords, n, L0, L1, L2, f, table, cap - 1, nbr,
-                                                    counts, n_tiles, mirror ? 1 : 0);
+                                                    counts, n_tiles, mirror ? 1 : 0, 0u, stats);
       SSCN_HIP(hipGetLastError());
       if (mirror) {
         k_count_nbr<<<grid_for(n_tiles * 64, 256), 256, 0, s>>>(nbr, n, K, counts, n_tiles, c);
