@@ -1414,6 +1414,60 @@ __global__ void k_plan_pairs(const int64_t* __restrict__ seg, int64_t n_tiles, c
   items[item * kPlanRows + pos % kPlanRows] = (uint32_t)in_rows[p] | ((uint32_t)o << kPlanRowBits);
 }
 
+// Blocks by decreasing item count, for more blocks than one workgroup takes
+// in a launch: a counting sort over the K + 1 possible counts in two
+// passes.  k_order_hist counts the blocks per count (LDS counters, one
+// global atomic per count per workgroup); k_order_place ranks each
+// workgroup's blocks per count in LDS, reserves one range per count with one
+// global atomic, and writes them (the order inside one count is arbitrary).
+// kOrderPerWg blocks per workgroup.
+constexpr int kOrderPerWg = 4096;
+__global__ __launch_bounds__(256) void k_order_hist(const int32_t* __restrict__ b_first, int64_t nb, int K,
+                                                    int32_t* __restrict__ ohist) {
+  __shared__ int32_t cnt[64];
+  if (threadIdx.x < 64) cnt[threadIdx.x] = 0;
+  __syncthreads();
+  const int64_t b0 = (int64_t)blockIdx.x * kOrderPerWg;
+  for (int i = threadIdx.x; i < kOrderPerWg; i += 256) {
+    const int64_t b = b0 + i;
+    const bool ok = b < nb;
+    (void)wave_count<6>(cnt, ok ? (uint32_t)(K - (b_first[b + 1] - b_first[b])) : 0u, ok);
+  }
+  __syncthreads();
+  if (threadIdx.x <= K && cnt[threadIdx.x] > 0) atomicAdd(&ohist[threadIdx.x], cnt[threadIdx.x]);
+}
+
+__global__ __launch_bounds__(256) void k_order_place(const int32_t* __restrict__ b_first, int64_t nb, int K,
+                                                     const int32_t* __restrict__ ohist, int32_t* __restrict__ ocur,
+                                                     int32_t* __restrict__ order) {
+  __shared__ int32_t cnt[64], base[64];
+  if (threadIdx.x < 64) cnt[threadIdx.x] = 0;
+  __syncthreads();
+  const int64_t b0 = (int64_t)blockIdx.x * kOrderPerWg;
+  constexpr int PER = kOrderPerWg / 256;
+  int rank[PER];
+  uint32_t key[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int64_t b = b0 + threadIdx.x + 256 * i;
+    const bool ok = b < nb;
+    key[i] = ok ? (uint32_t)(K - (b_first[b + 1] - b_first[b])) : 0u;
+    rank[i] = wave_count<6>(cnt, key[i], ok);
+  }
+  __syncthreads();
+  if (threadIdx.x <= K) {
+    int start = 0;  // blocks of larger counts come first
+    for (int c = 0; c < (int)threadIdx.x; ++c) start += ohist[c];
+    base[threadIdx.x] = cnt[threadIdx.x] > 0 ? start + atomicAdd(&ocur[threadIdx.x], cnt[threadIdx.x]) : 0;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int64_t b = b0 + threadIdx.x + 256 * i;
+    if (b < nb) order[base[key[i]] + rank[i]] = (int32_t)b;
+  }
+}
+
 // Exclusive scan of at most kSmallScanMax int32 values in one launch (out
 // may alias in; out[count] = total).  Wavefront w holds elements
 // [2048 w, 2048 w + 2048) in registers, loaded in coalesced chunks of 64;
@@ -1464,44 +1518,13 @@ static sscn_status scan_i32(int32_t* p, int64_t count, hipStream_t s) {
   return exclusive_scan_i32(p, p, count, s);
 }
 
-// Blocks by decreasing item count (a counting sort over the K + 1 possible
-// counts in one workgroup; the order inside one count is arbitrary), so
-// that workgroups take the longest blocks first.
-__global__ __launch_bounds__(kOneBlock) void k_plan_order(const int32_t* __restrict__ b_first, int64_t nb, int K,
-                                                          int32_t* __restrict__ order) {
-  // counts per item count, one LDS atomic per distinct count per wavefront
-  // (nearly every block of a surface has one of a few counts)
-  __shared__ int32_t hist[64], cur[64];
-  if (threadIdx.x < 64) hist[threadIdx.x] = 0;
-  __syncthreads();
-  for (int64_t b0 = 0; b0 < nb; b0 += blockDim.x) {
-    const int64_t b = b0 + threadIdx.x;
-    const bool ok = b < nb;
-    (void)wave_count<6>(hist, ok ? (uint32_t)(K - (b_first[b + 1] - b_first[b])) : 0u, ok);
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int run = 0;
-    for (int c = 0; c <= K; ++c) {
-      cur[c] = run;
-      run += hist[c];
-    }
-  }
-  __syncthreads();
-  for (int64_t b0 = 0; b0 < nb; b0 += blockDim.x) {
-    const int64_t b = b0 + threadIdx.x;
-    const bool ok = b < nb;
-    const int p = wave_count<6>(cur, ok ? (uint32_t)(K - (b_first[b + 1] - b_first[b])) : 0u, ok);
-    if (ok) order[p] = (int32_t)b;
-  }
-}
-
-// k_plan_order with the scan of the item counts before it, in one
-// workgroup (nb <= kScanOrderMax): cnt[b] (items of block b) becomes
-// b_first (exclusive scan, b_first[nb] = total) and order lists the blocks
-// by decreasing count.  The counts stay in LDS for the second pass.
-// (one launch fewer; from some ten thousand blocks on, the separate scan's
-// wider parallelism wins: 2M rows take 54 us fused, 43 us apart)
+// Blocks by decreasing item count, with the scan of the item counts before
+// it, in one workgroup (nb <= kScanOrderMax): cnt[b] (items of block b)
+// becomes b_first (exclusive scan, b_first[nb] = total) and order lists the
+// blocks by decreasing count (a counting sort over the K + 1 possible
+// counts; the order inside one count is arbitrary).  The counts stay in
+// LDS for the second pass.  Beyond kScanOrderMax blocks the scan and the
+// two passes of k_order_hist / k_order_place run wider.
 constexpr int64_t kScanOrderMax = 8192;
 __global__ __launch_bounds__(kOneBlock) void k_plan_scan_order(int32_t* __restrict__ cnt, int64_t nb, int K,
                                                                int32_t* __restrict__ order) {
@@ -1553,7 +1576,9 @@ __global__ __launch_bounds__(kOneBlock) void k_plan_scan_order(int32_t* __restri
 // host yet (the plan is queued inside the build); at most ppo_bound pairs
 // per offset, and room for nb K items.  hist0: plan_hist_words(K) zeroed
 // words for the key histogram, or NULL.
-static int64_t plan_hist_words(int K) { return (1 << std::min(K, kPlanKeyBits)) + 1; }
+// The key histogram (bins + 1 words), then the block-count histogram and
+// cursor of the block order (64 words each).
+static int64_t plan_hist_words(int K) { return (1 << std::min(K, kPlanKeyBits)) + 1 + 128; }
 
 static sscn_status build_plan(RulebookData* d, Storage& st, int64_t n_rows, int K, hipStream_t s,
                               int64_t ppo_bound = -1, int32_t* hist0 = nullptr) {
@@ -1572,7 +1597,7 @@ static sscn_status build_plan(RulebookData* d, Storage& st, int64_t n_rows, int 
   Temps tmp(s);
   uint32_t* mask = st.row_mask; uint32_t* bmask; int32_t* hist = nullptr; int32_t* pos_of;
   Arena t;
-  if (!(hist0 && mask)) t.add(&hist, (size_t)bins + 1);
+  if (!(hist0 && mask)) t.add(&hist, (size_t)plan_hist_words(K));
   if (!mask) t.add(&mask, (size_t)n_rows);  // right after hist: one fill clears both
   t.add(&bmask, (size_t)nb);
   t.add(&pos_of, (size_t)n_rows);
@@ -1582,7 +1607,7 @@ static sscn_status build_plan(RulebookData* d, Storage& st, int64_t n_rows, int 
     for (int64_t c : d->pairs_per_offset) max_ppo = std::max(max_ppo, c);
   if (st.row_mask) {
     if (hist0) hist = hist0;
-    else SSCN_TRY(fill_i32(hist, 0, bins + 1, s));
+    else SSCN_TRY(fill_i32(hist, 0, plan_hist_words(K), s));
   } else {
     SSCN_TRY(fill_i32(hist, 0, (int32_t*)(mask + n_rows) - hist, s));
     if (max_ppo > 0) {
@@ -1610,7 +1635,11 @@ static sscn_status build_plan(RulebookData* d, Storage& st, int64_t n_rows, int 
     k_plan_scan_order<<<1, kOneBlock, 0, s>>>(st.b_first, nb, K, st.b_order);
   } else {
     SSCN_TRY(scan_i32(st.b_first, nb, s));
-    k_plan_order<<<1, kOneBlock, 0, s>>>(st.b_first, nb, K, st.b_order);
+    int32_t* ohist = hist + bins + 1;
+    const unsigned owgs = (unsigned)ceil_div(nb, kOrderPerWg);
+    k_order_hist<<<owgs, 256, 0, s>>>(st.b_first, nb, K, ohist);
+    SSCN_HIP(hipGetLastError());
+    k_order_place<<<owgs, 256, 0, s>>>(st.b_first, nb, K, ohist, ohist + 64, st.b_order);
   }
   SSCN_HIP(hipGetLastError());
   k_plan_items<<<grid_for(nb * kPlanRows, 256), 256, 0, s>>>(bmask, st.b_first, nb, st.items);
