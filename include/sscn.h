@@ -338,12 +338,13 @@ sscn_status sscn_concat_cols(const void* a, int32_t ca, const void* b, int32_t c
 
 /*
  * sscn_time_next_launch -- measurement aid: the next launch of a row-block
- * (forward / dgrad) or wgrad kernel made by a call on this host thread is
- * bracketed by hipEventRecord(before) and hipEventRecord(after) on that
- * kernel's stream, so hipEventElapsedTime(before, after) is that one
- * kernel's time even when the call queues other small kernels around it.
- * The events belong to the caller (created with timing enabled); the
- * request is used once.  NULL, NULL cancels it.  Not a paper operation.
+ * (forward / dgrad) or wgrad kernel made by a call on this host thread
+ * records `before` at that kernel's start and `after` at its end (with the
+ * dispatch itself, hipExtLaunchKernelGGL: no separate event packets), so
+ * hipEventElapsedTime(before, after) is that one kernel's time even when
+ * the call queues other small kernels around it.  The events belong to the
+ * caller (created with timing enabled); the request is used once.  NULL,
+ * NULL cancels it.  Not a paper operation.
  */
 sscn_status sscn_time_next_launch(hipEvent_t before, hipEvent_t after);
 

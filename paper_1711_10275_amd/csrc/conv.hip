@@ -15,6 +15,8 @@
 #include <algorithm>
 #include <cstdlib>
 
+#include <hip/hip_ext.h>
+
 #include "internal.h"
 
 namespace sscn {
@@ -1771,10 +1773,13 @@ static sscn_status launch_rows_nb(const T* X, const void* B, const View& v, int 
   occupancy((const void*)kern, 256, 0, &per_cu, &cus);
   // persistent: one resident wave of workgroups per column group
   const int64_t gx = std::min<int64_t>(nb, std::max<int64_t>(1, (int64_t)cus * per_cu / gy));
-  timed_launch_begin(s);
-  kern<<<dim3((unsigned)gx, (unsigned)gy), 256, 0, s>>>(X, xb, B, bb, v.st->perm, v.st->b_first, v.st->b_order,
-                                                         v.st->items, nb, v.K, v.mirror ? 1 : 0, kdim, ncols, Y);
-  timed_launch_end(s);
+  hipEvent_t t0, t1;
+  if (take_launch_timer(&t0, &t1))
+    hipExtLaunchKernelGGL(kern, dim3((unsigned)gx, (unsigned)gy), dim3(256), 0, s, t0, t1, 0, X, xb, B, bb, v.st->perm,
+                          v.st->b_first, v.st->b_order, v.st->items, nb, v.K, v.mirror ? 1 : 0, kdim, ncols, Y);
+  else
+    kern<<<dim3((unsigned)gx, (unsigned)gy), 256, 0, s>>>(X, xb, B, bb, v.st->perm, v.st->b_first, v.st->b_order,
+                                                           v.st->items, nb, v.K, v.mirror ? 1 : 0, kdim, ncols, Y);
   SSCN_HIP(hipGetLastError());
   return SSCN_OK;
 }
@@ -2120,11 +2125,15 @@ static sscn_status launch_wgrad_reg(bool zeroed, const T* X, const T* dY, const 
     const int64_t tr2 = std::max<int64_t>(1, ceil_div(v.st->n_tiles, ranges));
     const int64_t total = ceil_div(v.st->n_tiles, tr2) * S;
     if (!zeroed) SSCN_TRY(fill_f32(dW, 0.f, (int64_t)v.K * cin * cout, s));
-    timed_launch_begin(s);
-    kern<<<dim3((unsigned)total, (unsigned)(nzc * nzo)), 256, 0, s>>>(
-        X, (uint32_t)x_bytes, dY, (uint32_t)y_bytes, v.st->seg, v.st->n_tiles, v.st->in_rows, v.st->out_rows, v.K,
-        v.mirror ? 1 : 0, cin, cout, (int)tr2, items, nzc, dW);
-    timed_launch_end(s);
+    hipEvent_t t0, t1;
+    if (take_launch_timer(&t0, &t1))
+      hipExtLaunchKernelGGL(kern, dim3((unsigned)total, (unsigned)(nzc * nzo)), dim3(256), 0, s, t0, t1, 0, X,
+                            (uint32_t)x_bytes, dY, (uint32_t)y_bytes, v.st->seg, v.st->n_tiles, v.st->in_rows,
+                            v.st->out_rows, v.K, v.mirror ? 1 : 0, cin, cout, (int)tr2, items, nzc, dW);
+    else
+      kern<<<dim3((unsigned)total, (unsigned)(nzc * nzo)), 256, 0, s>>>(
+          X, (uint32_t)x_bytes, dY, (uint32_t)y_bytes, v.st->seg, v.st->n_tiles, v.st->in_rows, v.st->out_rows, v.K,
+          v.mirror ? 1 : 0, cin, cout, (int)tr2, items, nzc, dW);
     SSCN_HIP(hipGetLastError());
     return SSCN_OK;
   }

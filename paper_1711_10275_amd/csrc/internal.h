@@ -79,12 +79,12 @@ struct NoAlloc {
 const NoAlloc* no_alloc();
 void set_no_alloc(const NoAlloc* na);
 
-// Events the caller asked to have recorded around the next launch of a
-// row-block or wgrad kernel on this thread (sscn_time_next_launch); the
-// launch records `before` just ahead of the kernel and `after` just behind
-// it, on the kernel's stream, and clears the request.
-void timed_launch_begin(hipStream_t s);
-void timed_launch_end(hipStream_t s);
+// Events the caller asked to have recorded at the start and the end of the
+// next launch of a row-block or wgrad kernel on this thread
+// (sscn_time_next_launch): the launch takes them (clearing the request) and
+// records them with its own dispatch (hipExtLaunchKernelGGL), so that no
+// separate event packets idle the GPU between kernels.
+bool take_launch_timer(hipEvent_t* before, hipEvent_t* after);
 
 // One direction of a rule book: tiles over the output rows of that
 // direction, offset-major segments, and the pair arrays (pointers into the
@@ -132,8 +132,9 @@ struct RulebookData {
   int32_t* in_coords = nullptr;  // n_in x (d + 1) (SC only; an SSC's input sites are its output sites)
   std::vector<void*> blocks;     // device allocations owning all of the above
   // The chunk tables are built on first use (by the kernels that read
-  // them) on the build stream; `chunk_ready` is recorded after the build so
-  // that work on other streams can wait for it.
+  // them) on the build stream; when work on another stream needs one,
+  // `chunk_ready` is recorded on the build stream then (after the tables'
+  // kernels) and that stream waits for it.
   std::mutex chunk_mu;
   hipEvent_t chunk_ready = nullptr;
   hipEvent_t plan_ready = nullptr;   // the same for the row-block plans

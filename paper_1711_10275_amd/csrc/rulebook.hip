@@ -118,7 +118,7 @@ __device__ __forceinline__ uint32_t mix32(uint32_t h) {
 // along x2 touch about 60 such slots, against about 125 when every key has
 // a slot of its own (storing runs of consecutive keys in consecutive slots
 // of such a table instead clusters it, which made inserts and lookups
-// slower).  Measured on 2M scene sites: the probe 232 -> 190 us and the
+// slower).  Measured on 2M scene sites: the probe 232 -> 184 us and the
 // insert 104 -> 82 us, against a fill of twice the bytes (9 -> 13 us);
 // groups of 7 in 32-byte slots touch fewer slots (about 44) but took longer
 // (probe 200 us, fill 22 us), and lower or higher loads did not help.
@@ -270,16 +270,19 @@ __global__ __launch_bounds__(256) void k_ssc_probe(
   if (mirror && o0 == 0 && valid) nbr[(int64_t)ctr * n + k] = site_ok ? (int32_t)k : -1;
   int32_t rows[P];
   if constexpr (NARROW) {
-    // Grouped slots: a lookup reads the group key and the key's row word of
-    // the group's home slot together (one round trip unless the slot holds
+    // Grouped slots: a lookup reads the group's home slot whole (one 16-byte
+    // load: the group key and the rows; one round trip unless the slot holds
     // another group), and walks on slot by slot to the group or to an empty
-    // slot.
+    // slot.  (Two 4-byte loads, the key and the row word: 190 us instead of
+    // 184 for the 2M-site scenes.)
+    static_assert(kGroupWords == 4, "one 16-byte load per slot");
     const uint32_t* tb = reinterpret_cast<const uint32_t*>(table_v);
     uint32_t grp[P], sub[P], slot[P], gw[P], rw[P];
     bool live[P];
     auto read_slot = [&](int q) {
-      gw[q] = tb[(size_t)slot[q] * kGroupWords];
-      rw[q] = tb[(size_t)slot[q] * kGroupWords + 1 + sub[q]];
+      const uint4 v = *reinterpret_cast<const uint4*>(tb + (size_t)slot[q] * kGroupWords);
+      gw[q] = v.x;
+      rw[q] = sub[q] == 0 ? v.y : (sub[q] == 1 ? v.z : v.w);
     };
 #pragma unroll
     for (int q = 0; q < P; ++q) {
@@ -1147,6 +1150,19 @@ static sscn_status build_chunks(RulebookData* d, Storage& st, int64_t n_rows, in
   return SSCN_OK;
 }
 
+// Orders work on stream s behind a table built on first use: its kernels
+// were queued on the rule book's own stream, and an event recorded there
+// now follows them.  Events are recorded only when another stream asks (an
+// event packet between two kernels of one stream idles the GPU for some
+// microseconds).  Called with chunk_mu held.
+static sscn_status follow_rulebook_stream(RulebookData* d, hipEvent_t& ev, hipStream_t s) {
+  if (s == d->stream) return SSCN_OK;
+  if (!ev) SSCN_HIP(hipEventCreateWithFlags(&ev, hipEventDisableTiming));
+  SSCN_HIP(hipEventRecord(ev, d->stream));
+  SSCN_HIP(hipStreamWaitEvent(s, ev, 0));
+  return SSCN_OK;
+}
+
 sscn_status ensure_chunks(const View& v, hipStream_t s) {
   RulebookData* d = v.owner;
   Storage& st = v.st == &d->fwd ? d->fwd : d->bwd;
@@ -1162,12 +1178,9 @@ sscn_status ensure_chunks(const View& v, hipStream_t s) {
       if (cur != d->device) return fail(SSCN_ERR_INVALID_ARG, "rule book used on another device");
       const int64_t n_rows = &st == &d->fwd ? d->n_out : d->n_in;
       SSCN_TRY(build_chunks(d, st, n_rows, d->K, d->stream));
-      if (!d->chunk_ready) SSCN_HIP(hipEventCreateWithFlags(&d->chunk_ready, hipEventDisableTiming));
-      SSCN_HIP(hipEventRecord(d->chunk_ready, d->stream));
     }
+    return follow_rulebook_stream(d, d->chunk_ready, s);
   }
-  if (s != d->stream) SSCN_HIP(hipStreamWaitEvent(s, d->chunk_ready, 0));
-  return SSCN_OK;
 }
 
 sscn_status ensure_order(const View& v, hipStream_t s) {
@@ -1184,13 +1197,10 @@ sscn_status ensure_order(const View& v, hipStream_t s) {
       SSCN_HIP(hipGetDevice(&cur));
       if (cur != d->device) return fail(SSCN_ERR_INVALID_ARG, "rule book used on another device");
       SSCN_TRY(build_tile_order(st, d->K, d->stream));
-      if (!d->order_ready) SSCN_HIP(hipEventCreateWithFlags(&d->order_ready, hipEventDisableTiming));
-      SSCN_HIP(hipEventRecord(d->order_ready, d->stream));
       st.order_built = true;
     }
+    return follow_rulebook_stream(d, d->order_ready, s);
   }
-  if (s != d->stream) SSCN_HIP(hipStreamWaitEvent(s, d->order_ready, 0));
-  return SSCN_OK;
 }
 
 // ------------------------------------------------------ row-block plan
@@ -1669,12 +1679,9 @@ sscn_status ensure_plan(const View& v, hipStream_t s) {
       if (cur != d->device) return fail(SSCN_ERR_INVALID_ARG, "rule book used on another device");
       const int64_t n_rows = &st == &d->fwd ? d->n_out : d->n_in;
       SSCN_TRY(build_plan(d, st, n_rows, d->K, d->stream));
-      if (!d->plan_ready) SSCN_HIP(hipEventCreateWithFlags(&d->plan_ready, hipEventDisableTiming));
-      SSCN_HIP(hipEventRecord(d->plan_ready, d->stream));
     }
+    return follow_rulebook_stream(d, d->plan_ready, s);
   }
-  if (s != d->stream) SSCN_HIP(hipStreamWaitEvent(s, d->plan_ready, 0));
-  return SSCN_OK;
 }
 
 static sscn_status check_common(const int32_t* coords, int64_t n, const int32_t* spatial_size,
@@ -1826,15 +1833,11 @@ static sscn_status ssc_build(const int32_t* coords, int64_t n, const int32_t* sp
     if (one_phase) SSCN_TRY(compact());
     // The sizes and flags are final here.  The plan is queued behind their
     // copy: the host waits for the copy only, and the plan's kernels run
-    // while it returns (uses of the plan on other streams wait for
-    // plan_ready).
+    // while it returns (a use of the plan on another stream waits for the
+    // rule book's stream).
     const size_t stat_bytes = sizeof(unsigned long long) * (1 + K);
     SSCN_TRY(readback_begin(stats, stat_bytes, s));
-    if (eager_plan) {
-      SSCN_TRY(build_plan(d, d->fwd, n, K, s, /*a site has one neighbour per offset*/ n, hist));
-      SSCN_HIP(hipEventCreateWithFlags(&d->plan_ready, hipEventDisableTiming));
-      SSCN_HIP(hipEventRecord(d->plan_ready, s));
-    }
+    if (eager_plan) SSCN_TRY(build_plan(d, d->fwd, n, K, s, /*a site has one neighbour per offset*/ n, hist));
     std::vector<unsigned long long> host(1 + K);
     SSCN_TRY(readback_end(host.data(), stat_bytes));
     if (!(host[0] & kFlagOutOfRange) && (host[0] & kFlagWideKey)) {

@@ -102,21 +102,13 @@ sscn_status dev_alloc(void** p, size_t bytes, hipStream_t s) {
 }
 
 static thread_local hipEvent_t t_time_before = nullptr, t_time_after = nullptr;
-static thread_local bool t_time_armed = false;
 
-void timed_launch_begin(hipStream_t s) {
-  if (t_time_before && !t_time_armed) {
-    (void)hipEventRecord(t_time_before, s);
-    t_time_armed = true;
-  }
-}
-
-void timed_launch_end(hipStream_t s) {
-  if (t_time_armed) {
-    (void)hipEventRecord(t_time_after, s);
-    t_time_before = t_time_after = nullptr;
-    t_time_armed = false;
-  }
+bool take_launch_timer(hipEvent_t* before, hipEvent_t* after) {
+  if (!t_time_before) return false;
+  *before = t_time_before;
+  *after = t_time_after;
+  t_time_before = t_time_after = nullptr;
+  return true;
 }
 
 static thread_local const NoAlloc* t_no_alloc = nullptr;
@@ -361,7 +353,6 @@ extern "C" sscn_status sscn_time_next_launch(hipEvent_t before, hipEvent_t after
     return sscn::fail(SSCN_ERR_INVALID_ARG, "both events or neither");
   sscn::t_time_before = before;
   sscn::t_time_after = after;
-  sscn::t_time_armed = false;
   return SSCN_OK;
 }
 
