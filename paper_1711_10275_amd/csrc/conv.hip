@@ -2154,6 +2154,237 @@ static int wgrad_blocks(int c) {
   return 1;
 }
 
+// ------------------------------------------------ row-block wgrad (bf16)
+// dW_o = sum over the pairs (j, k) of offset o of X[j]^T dY[k] for narrow
+// bf16 layers (c_out 32, c_in 32 or 64).  A workgroup takes blocks of the
+// row-block plan (64 output rows k with one item per offset of their
+// union, as the forward walks them): the block's dY rows and each item's
+// gathered X rows go straight into row-major LDS tiles (direct loads, 16
+// bytes per lane; absent rows read zeros), and both MFMA operands are read
+// from those tiles transposed (LDS transpose reads of four 16-bit elements
+// per lane): a 16 x 16 x 32 bf16 MFMA then sums over 32 of the block's rows.
+// Each wavefront keeps the output tiles of its workgroup's offset group
+// (blockIdx.y) in registers over all its blocks; the workgroups' partial
+// sums are added in a fixed order afterwards (k_wgrad_sum), so dW is
+// bit-reproducible.  At these widths the per-pair wgrad gives a lane 4
+// bytes of X and of dY per pair, and its load instructions bind.
+typedef short wg_v4s __attribute__((ext_vector_type(4)));
+
+// Lane (m, g) of a 16 x 16 x 32 operand from a row-major LDS tile of 64 rows
+// (rb bytes each): rows 32 ks + 8 g .. + 7 of column 16 cb + m, through two
+// transpose reads.  In a group of 16 lanes the read hands lane i element
+// (i & 3) of the 8 bytes that lane 4 k + (i >> 2) addressed, as its element
+// k: so lane j addresses row 8 g + 4 h + (j >> 2), columns 16 cb + 4 (j & 3)
+// .. + 3, for the halves h = 0, 1.
+__device__ __forceinline__ bf16x8 tile_operand_tr(const char* tile, int rb, int cb, int ks, int lane) {
+  const int j = lane & 15, g = lane >> 4;
+  const char* p = tile + (32 * ks + 8 * g + (j >> 2)) * rb + (16 * cb + 4 * (j & 3)) * 2;
+  const wg_v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) wg_v4s*)p);
+  const wg_v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) wg_v4s*)(p + 4 * rb));
+  const uint2 a = __builtin_bit_cast(uint2, lo), b = __builtin_bit_cast(uint2, hi);
+  return __builtin_bit_cast(bf16x8, make_uint4(a.x, a.y, b.x, b.y));
+}
+
+// CI x CO channels; OPG offsets per group (grid.y groups); partials
+// P[y][x][oo][CI][CO] (x < gridDim.x workgroups).
+template <int CI, int CO, int OPG>
+__global__ __launch_bounds__(256) void k_wgrad_rows(const bf16_t* __restrict__ X, uint32_t x_bytes,
+                                                    const bf16_t* __restrict__ dY, uint32_t y_bytes,
+                                                    const int32_t* __restrict__ perm,
+                                                    const int32_t* __restrict__ b_first,
+                                                    const int32_t* __restrict__ b_order,
+                                                    const uint32_t* __restrict__ items, int64_t n_blocks, int K,
+                                                    float* __restrict__ part) {
+  constexpr int NTI = CI / 16, NTJ = CO / 16, TPW = NTI * NTJ / 4;
+  static_assert(NTI * NTJ % 4 == 0 && TPW >= 1 && TPW <= 2, "one or two output tiles per wavefront");
+  constexpr int XB = CI * 2, YB = CO * 2;          // bytes per tile row
+  constexpr int XCH = 64 * XB / 1024, YCH = 64 * YB / 1024;  // 1 KB load chunks per tile
+  static_assert(XCH % 4 == 0 && YCH % 4 == 0, "whole chunks per wavefront");
+  __shared__ __attribute__((aligned(16))) char Xs[2][64 * XB];
+  __shared__ __attribute__((aligned(16))) char Ys[64 * YB];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int o_lo = blockIdx.y * OPG, o_hi = min(K, o_lo + OPG);
+  // this wavefront's tiles: t = TPW wave + q, (ti, tj) = (t / NTJ, t % NTJ);
+  // with two tiles per wavefront both share ti
+  const int ti = (TPW * wave) / NTJ;
+  const rsrc_t rx = make_rsrc(X, x_bytes), ry = make_rsrc(dY, y_bytes);
+  f32x4 acc[OPG][TPW];
+#pragma unroll
+  for (int oo = 0; oo < OPG; ++oo)
+#pragma unroll
+    for (int q = 0; q < TPW; ++q) acc[oo][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // per chunk c this lane loads: tile row and 16-byte piece
+  auto x_row = [&](int c) { return (c * 1024 + 16 * lane) / XB; };
+  auto x_piece = [&](int c) { return (uint32_t)((c * 1024 + 16 * lane) % XB); };
+  constexpr int NXC = XCH / 4;  // X chunks per wavefront
+  uint32_t ent[NXC];            // entries of the next item's rows
+  auto load_entries = [&](int64_t item) {
+#pragma unroll
+    for (int i = 0; i < NXC; ++i) ent[i] = items[item * kPlanRows + x_row(wave + 4 * i)];
+  };
+  auto dma_x = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < NXC; ++i) {
+      const int c = wave + 4 * i;
+      const uint32_t r = ent[i] & kPlanNoRow;
+      const uint32_t off = r != kPlanNoRow ? r * (uint32_t)XB + x_piece(c) : kOobOffset;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (__attribute__((address_space(3))) void*)&Xs[buf][c * 1024], 16,
+                                               (int)off, 0, 0, 0);
+    }
+  };
+
+  const int64_t G = gridDim.x, wg = blockIdx.x;
+  auto next = [&](int64_t round) { return round * G + ((round & 1) ? G - 1 - wg : wg); };
+  for (int64_t idx = wg, round = 0; idx < n_blocks; idx = next(++round)) {
+    const int64_t b = b_order[idx];
+    const int64_t first = b_first[b];
+    const int n_items = (int)(b_first[b + 1] - first);
+    // the items of this offset group: [j0, j1) (items are in increasing offset)
+    const uint32_t oj = lane < n_items ? items[(first + lane) * kPlanRows] >> kPlanRowBits : 0xffu;
+    const uint64_t below = __ballot(lane < n_items && (int)oj < o_lo);
+    const uint64_t inside = __ballot(lane < n_items && (int)oj >= o_lo && (int)oj < o_hi);
+    if (inside == 0) continue;  // uniform: no barrier skipped by some wavefronts only
+    int j = __popcll(below);
+    const int j1 = j + __popcll(inside);
+    __syncthreads();  // the previous block's tiles are no longer read
+    // the block's dY rows and the first item's X rows
+#pragma unroll
+    for (int i = 0; i < YCH / 4; ++i) {
+      const int c = wave + 4 * i;
+      const int row = (c * 1024 + 16 * lane) / YB;
+      const int32_t k = perm[b * kPlanRows + row];
+      const uint32_t off = k >= 0 ? (uint32_t)k * YB + (uint32_t)((c * 1024 + 16 * lane) % YB) : kOobOffset;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ry, (__attribute__((address_space(3))) void*)&Ys[c * 1024], 16,
+                                               (int)off, 0, 0, 0);
+    }
+    load_entries(first + j);
+    int buf = 0;
+    dma_x(buf);
+    if (j + 1 < j1) load_entries(first + j + 1);
+    bf16x8 bop[TPW][2];
+    bool have_b = false;
+    int o_cur = __builtin_amdgcn_readfirstlane((int)__shfl(oj, j, 64));
+#pragma unroll
+    for (int oo = 0; oo < OPG; ++oo) {
+      if (j < j1 && o_cur == o_lo + oo) {  // uniform
+        __syncthreads();  // item j's rows (and dY) landed; item j - 1's tile is free
+        if (j + 1 < j1) {
+          dma_x(buf ^ 1);
+          if (j + 2 < j1) load_entries(first + j + 2);
+        }
+        if (!have_b) {
+#pragma unroll
+          for (int q = 0; q < TPW; ++q)
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) bop[q][ks] = tile_operand_tr(Ys, YB, (TPW * wave + q) % NTJ, ks, lane);
+          have_b = true;
+        }
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          const bf16x8 a = tile_operand_tr(Xs[buf], XB, ti, ks, lane);
+#pragma unroll
+          for (int q = 0; q < TPW; ++q)
+            acc[oo][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bop[q][ks], acc[oo][q], 0, 0, 0);
+        }
+        buf ^= 1;
+        ++j;
+        o_cur = __builtin_amdgcn_readfirstlane((int)__shfl(oj, min(j, 63), 64));
+      }
+    }
+  }
+  // partial sums: lane (m, g) holds rows 4 g + r (c_in) of column m (c_out)
+  const int m = lane & 15, g = lane >> 4;
+  float* P = part + ((int64_t)blockIdx.y * gridDim.x + wg) * OPG * CI * CO;
+#pragma unroll
+  for (int oo = 0; oo < OPG; ++oo)
+#pragma unroll
+    for (int q = 0; q < TPW; ++q) {
+      const int tj = (TPW * wave + q) % NTJ;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) P[((int64_t)oo * CI + 16 * ti + 4 * g + r) * CO + 16 * tj + m] = acc[oo][q][r];
+    }
+}
+
+// dW[o'][ci][co] = the sum over the workgroups x of P[y][x][oo][ci][co] for
+// the stored offset o = y OPG + oo (o' = K - 1 - o on a mirrored view), in
+// a fixed order: a workgroup takes 64 consecutive outputs, its wavefront w
+// the partials x = 4 i + w (four running sums, by i mod 4, eight loads in
+// flight), and the sums are added in order of w and i mod 4.
+__global__ __launch_bounds__(256) void k_wgrad_sum(const float* __restrict__ part, int K, int cin, int cout, int opg,
+                                                   int64_t n_wg, int mirror, float* __restrict__ dW) {
+  __shared__ float red[4][64];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t per_o = (int64_t)cin * cout;
+  const int64_t t = (int64_t)blockIdx.x * 64 + lane;
+  const bool ok = t < K * per_o;
+  const int o = ok ? (int)(t / per_o) : 0;
+  const int64_t e = ok ? t % per_o : 0;
+  const int y = o / opg, oo = o % opg;
+  const float* p = part + ((int64_t)y * n_wg * opg + oo) * per_o + e;
+  const int64_t xs = (int64_t)opg * per_o;  // from one workgroup's partials to the next
+  float s[4] = {0.f, 0.f, 0.f, 0.f};
+  int64_t x = wave;
+  for (; x + 28 < n_wg; x += 32) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = ok ? p[(x + 4 * u) * xs] : 0.f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) s[u % 4] += v[u];
+  }
+  for (int u = 0; x < n_wg; x += 4, ++u) s[u % 4] += ok ? p[x * xs] : 0.f;
+  red[wave][lane] = (s[0] + s[1]) + (s[2] + s[3]);
+  __syncthreads();
+  if (wave == 0 && ok)
+    dW[(int64_t)(mirror ? K - 1 - o : o) * per_o + e] = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
+}
+
+// Whether the row-block wgrad takes a bf16 layer: c_out 32 and c_in 32 or
+// 64, and the plan's limits.
+static bool wgrad_rows_eligible(const View& v, int cin, int cout) {
+  return cout == 32 && (cin == 32 || cin == 64) && v.K <= 32 &&
+         (uint64_t)std::max<int64_t>(v.n_in, 1) * cin * 2 < kOobOffset &&
+         (uint64_t)std::max<int64_t>(v.n_out, 1) * cout * 2 < kOobOffset &&
+         std::max(v.n_in, v.n_out) < (int64_t)kPlanNoRow;
+}
+
+template <int CI, int CO, int OPG>
+static sscn_status launch_wgrad_rows_t(const bf16_t* X, const bf16_t* dY, const View& v, float* dW, hipStream_t s) {
+  SSCN_TRY(ensure_plan(v, s));
+  const int64_t nb = v.st->n_blocks;
+  const int groups = (v.K + OPG - 1) / OPG;
+  auto kern = k_wgrad_rows<CI, CO, OPG>;
+  int cus = 256, per_cu = 1;
+  occupancy((const void*)kern, 256, 0, &per_cu, &cus);
+  const int64_t gx = std::max<int64_t>(1, std::min<int64_t>(nb, (int64_t)cus * per_cu / groups));
+  float* part = nullptr;
+  SSCN_TRY(dev_alloc((void**)&part, sizeof(float) * (size_t)gx * groups * OPG * CI * CO, s));
+  const uint32_t xb = (uint32_t)((uint64_t)std::max<int64_t>(v.n_in, 1) * CI * 2);
+  const uint32_t yb = (uint32_t)((uint64_t)std::max<int64_t>(v.n_out, 1) * CO * 2);
+  hipEvent_t t0, t1;
+  if (take_launch_timer(&t0, &t1))
+    hipExtLaunchKernelGGL(kern, dim3((unsigned)gx, (unsigned)groups), dim3(256), 0, s, t0, t1, 0, X, xb, dY, yb,
+                          v.st->perm, v.st->b_first, v.st->b_order, v.st->items, nb, v.K, part);
+  else
+    kern<<<dim3((unsigned)gx, (unsigned)groups), 256, 0, s>>>(X, xb, dY, yb, v.st->perm, v.st->b_first,
+                                                              v.st->b_order, v.st->items, nb, v.K, part);
+  hipError_t e = hipGetLastError();
+  if (e == hipSuccess) {
+    const int64_t total = (int64_t)v.K * CI * CO;
+    k_wgrad_sum<<<(unsigned)ceil_div(total, 64), 256, 0, s>>>(part, v.K, CI, CO, OPG, gx, v.mirror ? 1 : 0, dW);
+    e = hipGetLastError();
+  }
+  dev_free(part, s);
+  return e == hipSuccess ? SSCN_OK : hip_fail(e, "row-block wgrad");
+}
+
+static sscn_status launch_wgrad_rows(const bf16_t* X, const bf16_t* dY, const View& v, int cin, int cout, float* dW,
+                                     hipStream_t s) {
+  if (v.n_out == 0 || v.st->n_tiles == 0) return fill_f32(dW, 0.f, (int64_t)v.K * cin * cout, s);
+  if (cin == 32) return launch_wgrad_rows_t<32, 32, 27>(X, dY, v, dW, s);
+  return launch_wgrad_rows_t<64, 32, 14>(X, dY, v, dW, s);
+}
+
 // zeroed: dW is already zero on stream s (cleared by the dgrad launch before it).
 template <typename T>
 static sscn_status launch_wgrad(const T* X, const T* dY, const View& v, int cin, int cout, float* dW,
@@ -2378,6 +2609,8 @@ extern "C" sscn_status sparse_conv_backward(const void* features, const void* we
       if (dtype == SSCN_F32)
         st = launch_wgrad<float>((const float*)features, (const float*)dout, v, c_in, c_out, wgrad, stream, mx,
                                  d->n_pairs, w_zeroed);
+      else if (wgrad_rows_eligible(v, c_in, c_out) && !no_alloc())
+        st = launch_wgrad_rows((const bf16_t*)features, (const bf16_t*)dout, v, c_in, c_out, wgrad, stream);
       else
         st = launch_wgrad<bf16_t>((const bf16_t*)features, (const bf16_t*)dout, v, c_in, c_out, wgrad, stream,
                                   mx, d->n_pairs, w_zeroed);

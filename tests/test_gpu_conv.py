@@ -320,3 +320,44 @@ def test_packed_items_forward_backward(c, dtype):
     assert_close(Y, O.forward(Xs, Ws, osc), dtype, f"packed sc {c}")
     Yd, Wd = _draw(sc.n_out, c, c, 8, 11 + c, dtype)
     assert_close(_fwd(sc.transpose(), Yd, Wd, dtype), O.forward(Yd, Wd, O.transpose(osc)), dtype, f"packed dc {c}")
+
+
+@pytest.mark.parametrize("config", ["shell32", "shapes128"])
+@pytest.mark.parametrize("cin", [32, 64])
+def test_wgrad_row_blocks_bf16(config, cin):
+    """bf16 wgrad with 32 output channels and 32 or 64 input channels runs
+    over the row-block plan (gathered rows into LDS, transposed operand
+    reads, partial sums added in a fixed order): SSC and its mirror view at
+    the fp32 tolerance against the oracle, bit-identical on a second call,
+    and the same from a wgrad-only call."""
+    coords, size = coords_for(config)
+    rb = sscn.ssc_rulebook_build(dev(coords), size, 3)
+    orb = O.ssc_rulebook(coords, size, 3)
+    n = coords.shape[0]
+    X, W = _draw(n, cin, 32, 27, 20 + cin, "bf16")
+    G = S.features(n, 32, S.SEED_GRAD + 20 + cin, bf16=True)
+    for view, oview in ((rb, orb), (rb.transpose(), O.transpose(orb))):
+        dx, dw = sscn.sparse_conv_backward(dev(X, torch.bfloat16), dev(W, torch.bfloat16),
+                                           dev(G, torch.bfloat16), view)
+        rdw = O.backward(X, W, G, oview)[1]
+        assert_close(host(dw), rdw, "f32", f"row-block wgrad {config} {cin}")
+        _, dw2 = sscn.sparse_conv_backward(dev(X, torch.bfloat16), dev(W, torch.bfloat16),
+                                           dev(G, torch.bfloat16), view, dgrad=False)
+        np.testing.assert_array_equal(host(dw2), host(dw))
+
+
+@pytest.mark.parametrize("cin", [32, 64])
+def test_wgrad_row_blocks_sc_dc_bf16(cin):
+    """The row-block bf16 wgrad on SC(2,2) (8 offsets) and on its transposed
+    (DC) layer, whose plan is built on first use."""
+    coords, size = coords_for("shell32")
+    sc = sscn.sc_rulebook_build(dev(coords), size, 2, 2)
+    osc = O.sc_rulebook(coords, size, 2, 2)
+    for view, oview in ((sc, osc), (sc.transpose(), O.transpose(osc))):
+        X, W = _draw(view.n_in, cin, 32, 8, 30 + cin, "bf16")
+        G = S.features(view.n_out, 32, S.SEED_GRAD + 30 + cin, bf16=True)
+        dx, dw = sscn.sparse_conv_backward(dev(X, torch.bfloat16), dev(W, torch.bfloat16),
+                                           dev(G, torch.bfloat16), view)
+        rdx, rdw = O.backward(X, W, G, oview)
+        assert_close(host(dx), rdx, "bf16", f"dgrad sc/dc {cin}")
+        assert_close(host(dw), rdw, "f32", f"row-block wgrad sc/dc {cin}")
