@@ -2155,8 +2155,8 @@ static int wgrad_blocks(int c) {
 }
 
 // ------------------------------------------------ row-block wgrad (bf16)
-// dW_o = sum over the pairs (j, k) of offset o of X[j]^T dY[k] for narrow
-// bf16 layers (c_out 32, c_in 32 or 64).  A workgroup takes blocks of the
+// dW_o = sum over the pairs (j, k) of offset o of X[j]^T dY[k] for bf16
+// layers of 32 or 64 output and 32 to 128 input channels.  A workgroup takes blocks of the
 // row-block plan (64 output rows k with one item per offset of their
 // union, as the forward walks them): the block's dY rows and each item's
 // gathered X rows go straight into row-major LDS tiles (direct loads, 16
@@ -2186,7 +2186,9 @@ __device__ __forceinline__ bf16x8 tile_operand_tr(const char* tile, int rb, int 
 }
 
 // CI x CO channels; OPG offsets per group (grid.y groups); partials
-// P[y][x][oo][CI][CO] (x < gridDim.x workgroups).
+// P[y][x][oo][CI][CO] (x < gridDim.x workgroups).  The 16 x 16 output tiles
+// t = (ti, tj) are dealt TPW per wavefront in row-major order: either a
+// wavefront's tiles share one row ti (TPW <= NTJ) or cover whole rows.
 template <int CI, int CO, int OPG>
 __global__ __launch_bounds__(256) void k_wgrad_rows(const bf16_t* __restrict__ X, uint32_t x_bytes,
                                                     const bf16_t* __restrict__ dY, uint32_t y_bytes,
@@ -2196,7 +2198,10 @@ __global__ __launch_bounds__(256) void k_wgrad_rows(const bf16_t* __restrict__ X
                                                     const uint32_t* __restrict__ items, int64_t n_blocks, int K,
                                                     float* __restrict__ part) {
   constexpr int NTI = CI / 16, NTJ = CO / 16, TPW = NTI * NTJ / 4;
-  static_assert(NTI * NTJ % 4 == 0 && TPW >= 1 && TPW <= 2, "one or two output tiles per wavefront");
+  constexpr bool ONE_ROW = TPW <= NTJ;               // the wavefront's tiles share ti
+  constexpr int NA = ONE_ROW ? 1 : TPW / NTJ;        // tile rows (A operands) per wavefront
+  constexpr int NB = ONE_ROW ? TPW : NTJ;            // tile columns (B operands) per wavefront
+  static_assert(NTI * NTJ % 4 == 0 && (ONE_ROW ? NTJ % TPW == 0 : TPW % NTJ == 0), "tiles dealt evenly");
   constexpr int XB = CI * 2, YB = CO * 2;          // bytes per tile row
   constexpr int XCH = 64 * XB / 1024, YCH = 64 * YB / 1024;  // 1 KB load chunks per tile
   static_assert(XCH % 4 == 0 && YCH % 4 == 0, "whole chunks per wavefront");
@@ -2204,9 +2209,9 @@ __global__ __launch_bounds__(256) void k_wgrad_rows(const bf16_t* __restrict__ X
   __shared__ __attribute__((aligned(16))) char Ys[64 * YB];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int o_lo = blockIdx.y * OPG, o_hi = min(K, o_lo + OPG);
-  // this wavefront's tiles: t = TPW wave + q, (ti, tj) = (t / NTJ, t % NTJ);
-  // with two tiles per wavefront both share ti
-  const int ti = (TPW * wave) / NTJ;
+  // this wavefront's tiles: t = TPW wave + q, (ti, tj) = (t / NTJ, t % NTJ):
+  // rows ti0 + a (a < NA), columns tj0 + bq (bq < NB)
+  const int ti0 = (TPW * wave) / NTJ, tj0 = ONE_ROW ? (TPW * wave) % NTJ : 0;
   const rsrc_t rx = make_rsrc(X, x_bytes), ry = make_rsrc(dY, y_bytes);
   f32x4 acc[OPG][TPW];
 #pragma unroll
@@ -2262,7 +2267,7 @@ __global__ __launch_bounds__(256) void k_wgrad_rows(const bf16_t* __restrict__ X
     int buf = 0;
     dma_x(buf);
     if (j + 1 < j1) load_entries(first + j + 1);
-    bf16x8 bop[TPW][2];
+    bf16x8 bop[NB][2];
     bool have_b = false;
     int o_cur = __builtin_amdgcn_readfirstlane((int)__shfl(oj, j, 64));
 #pragma unroll
@@ -2275,17 +2280,21 @@ __global__ __launch_bounds__(256) void k_wgrad_rows(const bf16_t* __restrict__ X
         }
         if (!have_b) {
 #pragma unroll
-          for (int q = 0; q < TPW; ++q)
+          for (int bq = 0; bq < NB; ++bq)
 #pragma unroll
-            for (int ks = 0; ks < 2; ++ks) bop[q][ks] = tile_operand_tr(Ys, YB, (TPW * wave + q) % NTJ, ks, lane);
+            for (int ks = 0; ks < 2; ++ks) bop[bq][ks] = tile_operand_tr(Ys, YB, tj0 + bq, ks, lane);
           have_b = true;
         }
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
-          const bf16x8 a = tile_operand_tr(Xs[buf], XB, ti, ks, lane);
 #pragma unroll
-          for (int q = 0; q < TPW; ++q)
-            acc[oo][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bop[q][ks], acc[oo][q], 0, 0, 0);
+          for (int a = 0; a < NA; ++a) {
+            const bf16x8 av = tile_operand_tr(Xs[buf], XB, ti0 + a, ks, lane);
+#pragma unroll
+            for (int bq = 0; bq < NB; ++bq)
+              acc[oo][a * NB + bq] =
+                  __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bop[bq][ks], acc[oo][a * NB + bq], 0, 0, 0);
+          }
         }
         buf ^= 1;
         ++j;
@@ -2300,7 +2309,7 @@ __global__ __launch_bounds__(256) void k_wgrad_rows(const bf16_t* __restrict__ X
   for (int oo = 0; oo < OPG; ++oo)
 #pragma unroll
     for (int q = 0; q < TPW; ++q) {
-      const int tj = (TPW * wave + q) % NTJ;
+      const int ti = ti0 + q / NB, tj = tj0 + q % NB;
 #pragma unroll
       for (int r = 0; r < 4; ++r) P[((int64_t)oo * CI + 16 * ti + 4 * g + r) * CO + 16 * tj + m] = acc[oo][q][r];
     }
@@ -2339,10 +2348,11 @@ __global__ __launch_bounds__(256) void k_wgrad_sum(const float* __restrict__ par
     dW[(int64_t)(mirror ? K - 1 - o : o) * per_o + e] = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
 }
 
-// Whether the row-block wgrad takes a bf16 layer: c_out 32 and c_in 32 or
-// 64, and the plan's limits.
+// Whether the row-block wgrad takes a bf16 layer: c_in x c_out one of
+// 32 x 32, 64 x 32, 64 x 64, 128 x 64, and the plan's limits.
 static bool wgrad_rows_eligible(const View& v, int cin, int cout) {
-  return cout == 32 && (cin == 32 || cin == 64) && v.K <= 32 &&
+  const bool shape = (cout == 32 && (cin == 32 || cin == 64)) || (cout == 64 && (cin == 64 || cin == 128));
+  return shape && v.K <= 32 &&
          (uint64_t)std::max<int64_t>(v.n_in, 1) * cin * 2 < kOobOffset &&
          (uint64_t)std::max<int64_t>(v.n_out, 1) * cout * 2 < kOobOffset &&
          std::max(v.n_in, v.n_out) < (int64_t)kPlanNoRow;
@@ -2381,8 +2391,14 @@ static sscn_status launch_wgrad_rows_t(const bf16_t* X, const bf16_t* dY, const 
 static sscn_status launch_wgrad_rows(const bf16_t* X, const bf16_t* dY, const View& v, int cin, int cout, float* dW,
                                      hipStream_t s) {
   if (v.n_out == 0 || v.st->n_tiles == 0) return fill_f32(dW, 0.f, (int64_t)v.K * cin * cout, s);
-  if (cin == 32) return launch_wgrad_rows_t<32, 32, 27>(X, dY, v, dW, s);
-  return launch_wgrad_rows_t<64, 32, 14>(X, dY, v, dW, s);
+  // offsets per group: the wavefront's accumulators (OPG x TPW x 4 VGPRs)
+  // and operands within about 170 VGPRs
+  if (cout == 32) {
+    if (cin == 32) return launch_wgrad_rows_t<32, 32, 27>(X, dY, v, dW, s);
+    return launch_wgrad_rows_t<64, 32, 14>(X, dY, v, dW, s);
+  }
+  if (cin == 64) return launch_wgrad_rows_t<64, 64, 6>(X, dY, v, dW, s);
+  return launch_wgrad_rows_t<128, 64, 3>(X, dY, v, dW, s);
 }
 
 // zeroed: dW is already zero on stream s (cleared by the dgrad launch before it).

@@ -323,24 +323,24 @@ def test_packed_items_forward_backward(c, dtype):
 
 
 @pytest.mark.parametrize("config", ["shell32", "shapes128"])
-@pytest.mark.parametrize("cin", [32, 64])
-def test_wgrad_row_blocks_bf16(config, cin):
-    """bf16 wgrad with 32 output channels and 32 or 64 input channels runs
-    over the row-block plan (gathered rows into LDS, transposed operand
-    reads, partial sums added in a fixed order): SSC and its mirror view at
-    the fp32 tolerance against the oracle, bit-identical on a second call,
-    and the same from a wgrad-only call."""
+@pytest.mark.parametrize("cin,cout", [(32, 32), (64, 32), (64, 64), (128, 64)])
+def test_wgrad_row_blocks_bf16(config, cin, cout):
+    """bf16 wgrad of these widths runs over the row-block plan (gathered
+    rows into LDS, transposed operand reads, partial sums added in a fixed
+    order; 1, 2, 5 and 9 offset groups): SSC and its mirror view at the fp32
+    tolerance against the oracle, bit-identical on a second call, and the
+    same from a wgrad-only call."""
     coords, size = coords_for(config)
     rb = sscn.ssc_rulebook_build(dev(coords), size, 3)
     orb = O.ssc_rulebook(coords, size, 3)
     n = coords.shape[0]
-    X, W = _draw(n, cin, 32, 27, 20 + cin, "bf16")
-    G = S.features(n, 32, S.SEED_GRAD + 20 + cin, bf16=True)
+    X, W = _draw(n, cin, cout, 27, 20 + cin + cout, "bf16")
+    G = S.features(n, cout, S.SEED_GRAD + 20 + cin + cout, bf16=True)
     for view, oview in ((rb, orb), (rb.transpose(), O.transpose(orb))):
         dx, dw = sscn.sparse_conv_backward(dev(X, torch.bfloat16), dev(W, torch.bfloat16),
                                            dev(G, torch.bfloat16), view)
         rdw = O.backward(X, W, G, oview)[1]
-        assert_close(host(dw), rdw, "f32", f"row-block wgrad {config} {cin}")
+        assert_close(host(dw), rdw, "f32", f"row-block wgrad {config} {cin}x{cout}")
         _, dw2 = sscn.sparse_conv_backward(dev(X, torch.bfloat16), dev(W, torch.bfloat16),
                                            dev(G, torch.bfloat16), view, dgrad=False)
         np.testing.assert_array_equal(host(dw2), host(dw))
