@@ -496,6 +496,12 @@ def main():
     if args.copy_calibration:
         copy_calibration()
     wgrad_ms = timed(lambda: sscn.sparse_conv_backward(tX, tW, tG, rb, dgrad=False, wgrad=True))
+    # the same wgrad with its work items' partial sums added in a fixed order
+    sscn.set_deterministic(True)
+    try:
+        wgrad_det_ms = timed(lambda: sscn.sparse_conv_backward(tX, tW, tG, rb, dgrad=False, wgrad=True))
+    finally:
+        sscn.set_deterministic(False)
     tXb, tWb, tGb = tX.to(torch.bfloat16), tW.to(torch.bfloat16), tG.to(torch.bfloat16)
     fwd_bf16_ms = timed(lambda: sscn.sparse_conv_forward(tXb, tWb, rb))
     dgrad_bf16_ms = timed(lambda: sscn.sparse_conv_backward(None, tWb, tGb, rb, dgrad=True, wgrad=False))
@@ -525,6 +531,7 @@ def main():
         "forward_sites_per_s": n / (fwd_ms * 1e-3),
         "dgrad_ms": dgrad_ms,
         "wgrad_ms": wgrad_ms,
+        "wgrad_deterministic_ms": wgrad_det_ms,
         "wgrad_tflops": flops_layer / (wgrad_ms * 1e-3) / 1e12,
         "bf16": {"forward_ms": fwd_bf16_ms, "dgrad_ms": dgrad_bf16_ms, "wgrad_ms": wgrad_bf16_ms,
                  "forward_tflops": flops_layer / (fwd_bf16_ms * 1e-3) / 1e12},

@@ -358,6 +358,29 @@ sscn_status sscn_time_next_launch(hipEvent_t before, hipEvent_t after);
 sscn_status sscn_release_cached(void);
 
 /*
+ * sscn_set_device_memory_cap -- cap the device memory the library holds per
+ * device (rule-book storage, build temporaries and its cache of idle
+ * blocks) at `bytes`; 0 removes the cap.  A new block that would exceed
+ * it first releases the idle blocks, then fails with SSCN_ERR_OOM as a real
+ * out-of-memory would, so that this path can be exercised (a request that
+ * an idle block of the cache serves allocates nothing and always succeeds).  Read from the
+ * environment variable SSCN_DEVICE_MEMORY_CAP (bytes) at the first
+ * allocation unless set here.  Not a paper operation.
+ */
+sscn_status sscn_set_device_memory_cap(uint64_t bytes);
+
+/*
+ * sscn_set_deterministic -- on != 0: sparse_conv_backward's wgrad adds the
+ * partial sums of its work items in a fixed order instead of with atomic
+ * additions, so dW is bit-reproducible from run to run (for filters of at
+ * most 128 offsets; the bf16 kernel of 32 x 32, 64 x 32, 64 x 64 and
+ * 128 x 64 channels always is).  It costs a buffer of the partial blocks
+ * and one more pass.  Process-wide; off by default.  Not a paper
+ * operation: the reduction order of the sums of Sec. 4.1.
+ */
+sscn_status sscn_set_deterministic(int32_t on);
+
+/*
  * ------------------------------------------------------------------ training
  * Batch normalisation "applied over the set of active sites" and activation
  * functions restricted to them (Sec. 4.1 "Other operators"); the final

@@ -1915,7 +1915,7 @@ __global__ __launch_bounds__(256) void k_wgrad_ring(const T* __restrict__ X, uin
                                                     const int32_t* __restrict__ in_rows,
                                                     const int32_t* __restrict__ out_rows, int K, int mirror,
                                                     int cin, int cout, int tr, WgradItems items, int nzc,
-                                                    float* __restrict__ dW) {
+                                                    float* __restrict__ dW, float* __restrict__ det) {
   static_assert(16 % R == 0, "ring depth must divide a batch");
   const int S = items.first[K];
   const int64_t item = xcd_remap(blockIdx.x, gridDim.x);
@@ -1929,7 +1929,15 @@ __global__ __launch_bounds__(256) void k_wgrad_ring(const T* __restrict__ X, uin
   const int64_t rb = seg[(int64_t)so * n_tiles + t_lo];
   const int64_t rn = seg[(int64_t)so * n_tiles + t_hi] - rb;
   const int64_t pb = rb + rn * sub / n_sub, pe = rb + rn * (sub + 1) / n_sub;
-  if (pb >= pe) return;
+  // det: this item's block goes to its own slot of det (zeros when it has
+  // no pairs) instead of being added to dW, for a fixed-order sum after.
+  constexpr int NE = CA * CB * 4;
+  float* const det_blk = det ? det + (item * gridDim.y + blockIdx.y) * (NE * 64) : nullptr;
+  if (pb >= pe) {
+    if (det_blk)
+      for (int e = threadIdx.x; e < NE * 64; e += 256) det_blk[e] = 0.f;
+    return;
+  }
   const int ci0 = (blockIdx.y % nzc) * 16 * CA, co0 = (blockIdx.y / nzc) * 16 * CB;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int m = lane & 15, g = lane >> 4;
@@ -2058,7 +2066,6 @@ __global__ __launch_bounds__(256) void k_wgrad_ring(const T* __restrict__ X, uin
   }
   // sum the four wavefronts' partial blocks, then add the block to dW
   // (as in k_wgrad_reg)
-  constexpr int NE = CA * CB * 4;
   __shared__ float part[2][NE][64];
   float(*mine)[64] = part[wave & 1];
   if (wave < 2) {
@@ -2085,8 +2092,37 @@ __global__ __launch_bounds__(256) void k_wgrad_ring(const T* __restrict__ X, uin
     const int a = v / (CB * 4), b = (v / 4) % CB, q = v % 4;
     const int mm = l & 15, gg = l >> 4;
     const int ci = ci0 + CA * (4 * gg + q) + a, co = co0 + CB * mm + b;
-    if (ci < cin && co < cout && sum != 0.f) atomicAdd(dW + ((int64_t)o * cin + ci) * cout + co, sum);
+    if (det_blk) det_blk[e] = sum;
+    else if (ci < cin && co < cout && sum != 0.f) atomicAdd(dW + ((int64_t)o * cin + ci) * cout + co, sum);
   }
+}
+
+// Deterministic mode of k_wgrad_ring: dW[o][ci][co] = the sum of the item
+// blocks of offset o in a fixed order (tile ranges, then sub-items), from
+// the blocks the items wrote (element e = v 64 + l of a block holds
+// (ci, co) = (ci0 + CA (4 (l >> 4) + v % 4) + v / (4 CB), co0 + CB (l & 15)
+// + (v / 4) % CB)).
+template <int CA, int CB>
+__global__ void k_wgrad_det_sum(const float* __restrict__ det, int K, int cin, int cout, int nzc, int gy,
+                                int64_t ranges, WgradItems items, float* __restrict__ dW) {
+  constexpr int NE = CA * CB * 4;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t per_o = (int64_t)cin * cout;
+  if (t >= K * per_o) return;
+  const int o = (int)(t / per_o);
+  const int ci = (int)((t % per_o) / cout), co = (int)(t % cout);
+  const int ib = ci / (16 * CA), jb = co / (16 * CB);
+  const int by = jb * nzc + ib;
+  const int dci = ci - ib * 16 * CA, dco = co - jb * 16 * CB;
+  const int a = dci % CA, tt = dci / CA, gg = tt / 4, q = tt % 4;
+  const int b = dco % CB, mm = dco / CB;
+  const int e = ((a * CB + b) * 4 + q) * 64 + gg * 16 + mm;
+  const int S = items.first[K];
+  float sum = 0.f;
+  for (int64_t r = 0; r < ranges; ++r)
+    for (int w = items.first[o]; w < items.first[o + 1]; ++w)
+      sum += det[((r * S + w) * gy + by) * (int64_t)(NE * 64) + e];
+  dW[(int64_t)o * per_o + ci * cout + co] = sum;
 }
 
 template <typename T, int CA, int CB>
@@ -2124,16 +2160,35 @@ static sscn_status launch_wgrad_reg(bool zeroed, const T* X, const T* dY, const 
     const int64_t ranges = std::max<int64_t>(1, target / S);
     const int64_t tr2 = std::max<int64_t>(1, ceil_div(v.st->n_tiles, ranges));
     const int64_t total = ceil_div(v.st->n_tiles, tr2) * S;
-    if (!zeroed) SSCN_TRY(fill_f32(dW, 0.f, (int64_t)v.K * cin * cout, s));
+    // deterministic mode: every item block to its own slot, then a
+    // fixed-order sum (no fill: the sum overwrites dW)
+    const int gy = nzc * nzo;
+    float* det = nullptr;
+    if (deterministic()) {
+      SSCN_TRY(dev_alloc((void**)&det, sizeof(float) * (size_t)total * gy * (CA * CB * 4 * 64), s));
+    } else if (!zeroed) {
+      SSCN_TRY(fill_f32(dW, 0.f, (int64_t)v.K * cin * cout, s));
+    }
     hipEvent_t t0, t1;
     if (take_launch_timer(&t0, &t1))
-      hipExtLaunchKernelGGL(kern, dim3((unsigned)total, (unsigned)(nzc * nzo)), dim3(256), 0, s, t0, t1, 0, X,
+      hipExtLaunchKernelGGL(kern, dim3((unsigned)total, (unsigned)gy), dim3(256), 0, s, t0, t1, 0, X,
                             (uint32_t)x_bytes, dY, (uint32_t)y_bytes, v.st->seg, v.st->n_tiles, v.st->in_rows,
-                            v.st->out_rows, v.K, v.mirror ? 1 : 0, cin, cout, (int)tr2, items, nzc, dW);
+                            v.st->out_rows, v.K, v.mirror ? 1 : 0, cin, cout, (int)tr2, items, nzc, dW, det);
     else
-      kern<<<dim3((unsigned)total, (unsigned)(nzc * nzo)), 256, 0, s>>>(
+      kern<<<dim3((unsigned)total, (unsigned)gy), 256, 0, s>>>(
           X, (uint32_t)x_bytes, dY, (uint32_t)y_bytes, v.st->seg, v.st->n_tiles, v.st->in_rows, v.st->out_rows, v.K,
-          v.mirror ? 1 : 0, cin, cout, (int)tr2, items, nzc, dW);
+          v.mirror ? 1 : 0, cin, cout, (int)tr2, items, nzc, dW, det);
+    if (det) {
+      hipError_t e = hipGetLastError();
+      if (e == hipSuccess) {
+        const int64_t n_out = (int64_t)v.K * cin * cout;
+        k_wgrad_det_sum<CA, CB><<<(unsigned)ceil_div(n_out, 256), 256, 0, s>>>(
+            det, v.K, cin, cout, nzc, gy, total / items.first[v.K], items, dW);
+        e = hipGetLastError();
+      }
+      dev_free(det, s);
+      if (e != hipSuccess) return hip_fail(e, "deterministic wgrad");
+    }
     SSCN_HIP(hipGetLastError());
     return SSCN_OK;
   }

@@ -86,6 +86,12 @@ void set_no_alloc(const NoAlloc* na);
 // separate event packets idle the GPU between kernels.
 bool take_launch_timer(hipEvent_t* before, hipEvent_t* after);
 
+// The cap on the library's device memory per device (0: none), and whether
+// wgrad adds its partial blocks in a fixed order (sscn_set_deterministic).
+void set_device_memory_cap(size_t bytes);
+bool deterministic();
+void set_deterministic(bool on);
+
 // One direction of a rule book: tiles over the output rows of that
 // direction, offset-major segments, and the pair arrays (pointers into the
 // rule book's device blocks).

@@ -1,6 +1,8 @@
 // Error reporting, the device-memory block cache, fills and a device-wide
 // exclusive scan used by the rule-book builders.
+#include <atomic>
 #include <cstdio>
+#include <cstdlib>
 #include <mutex>
 
 #include <map>
@@ -39,6 +41,9 @@ struct Cache {
   std::mutex mu;
   std::map<void*, std::pair<size_t, int>> owned;  // every block: (bytes, device)
   std::map<std::tuple<int, hipStream_t, size_t>, std::vector<void*>> idle;  // freed blocks
+  std::map<int, size_t> held;                     // bytes owned per device
+  size_t cap = 0;                                 // per-device cap on `held` (0: none)
+  bool cap_read = false;                          // SSCN_DEVICE_MEMORY_CAP looked up
 };
 Cache& cache() {
   static Cache* c = new Cache;  // never destroyed: frees may run during exit
@@ -59,6 +64,7 @@ void release_idle(Cache& c, int dev) {
     }
     for (void* q : it->second) {
       (void)hipFree(q);
+      c.held[dev] -= c.owned[q].first;
       c.owned.erase(q);
     }
     it = c.idle.erase(it);
@@ -84,6 +90,20 @@ sscn_status dev_alloc(void** p, size_t bytes, hipStream_t s) {
     if (it->second.empty()) c.idle.erase(it);
     return SSCN_OK;
   }
+  // The cap (sscn_set_device_memory_cap, or SSCN_DEVICE_MEMORY_CAP in bytes
+  // read at the first allocation) makes a new block fail as a real
+  // out-of-memory would, after the same release of idle blocks.
+  if (!c.cap_read) {
+    c.cap_read = true;
+    if (const char* env = std::getenv("SSCN_DEVICE_MEMORY_CAP")) c.cap = (size_t)std::strtoull(env, nullptr, 10);
+  }
+  if (c.cap && c.held[dev] + want > c.cap) {
+    release_idle(c, dev);
+    if (c.held[dev] + want > c.cap)
+      return fail(SSCN_ERR_OOM, std::string("device allocation of ") + std::to_string(bytes) +
+                                    " bytes exceeds the library's device memory cap of " + std::to_string(c.cap) +
+                                    " bytes");
+  }
   hipError_t e = hipMalloc(p, want);
   if (e == hipErrorOutOfMemory) {
     (void)hipGetLastError();
@@ -98,8 +118,20 @@ sscn_status dev_alloc(void** p, size_t bytes, hipStream_t s) {
                     hipGetErrorString(e));
   }
   c.owned[*p] = std::make_pair(want, dev);
+  c.held[dev] += want;
   return SSCN_OK;
 }
+
+void set_device_memory_cap(size_t bytes) {
+  Cache& c = cache();
+  std::lock_guard<std::mutex> lock(c.mu);
+  c.cap = bytes;
+  c.cap_read = true;
+}
+
+static std::atomic<bool> g_deterministic{false};
+bool deterministic() { return g_deterministic.load(std::memory_order_relaxed); }
+void set_deterministic(bool on) { g_deterministic.store(on, std::memory_order_relaxed); }
 
 static thread_local hipEvent_t t_time_before = nullptr, t_time_after = nullptr;
 
@@ -353,6 +385,16 @@ extern "C" sscn_status sscn_time_next_launch(hipEvent_t before, hipEvent_t after
     return sscn::fail(SSCN_ERR_INVALID_ARG, "both events or neither");
   sscn::t_time_before = before;
   sscn::t_time_after = after;
+  return SSCN_OK;
+}
+
+extern "C" sscn_status sscn_set_device_memory_cap(uint64_t bytes) {
+  sscn::set_device_memory_cap((size_t)bytes);
+  return SSCN_OK;
+}
+
+extern "C" sscn_status sscn_set_deterministic(int32_t on) {
+  sscn::set_deterministic(on != 0);
   return SSCN_OK;
 }
 

@@ -81,6 +81,8 @@ _SIGS = {
     "sscn_sgd_nesterov": [_vp, _vp, _vp, _i64, ctypes.c_float, ctypes.c_float, ctypes.c_float, _vp, _vp],
     "sscn_time_next_launch": [_vp, _vp],
     "sscn_release_cached": [],
+    "sscn_set_device_memory_cap": [ctypes.c_uint64],
+    "sscn_set_deterministic": [_i32],
     "sscn_last_error": [],
 }
 
@@ -440,6 +442,17 @@ def release_cached(device=None):
     """Return the library's idle device blocks on `device` to the device."""
     with torch.cuda.device(device if device is not None else torch.cuda.current_device()):
         _check(lib().sscn_release_cached())
+
+
+def set_device_memory_cap(nbytes):
+    """Cap the device memory the library holds per device (0: no cap); an
+    allocation beyond it fails with the out-of-memory status."""
+    _check(lib().sscn_set_device_memory_cap(int(nbytes)))
+
+
+def set_deterministic(on):
+    """wgrad adds its partial sums in a fixed order (bit-reproducible dW)."""
+    _check(lib().sscn_set_deterministic(1 if on else 0))
 
 
 def concat_cols(a, b):

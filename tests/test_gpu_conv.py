@@ -361,3 +361,30 @@ def test_wgrad_row_blocks_sc_dc_bf16(cin):
         rdx, rdw = O.backward(X, W, G, oview)
         assert_close(host(dx), rdx, "bf16", f"dgrad sc/dc {cin}")
         assert_close(host(dw), rdw, "f32", f"row-block wgrad sc/dc {cin}")
+
+
+@pytest.mark.parametrize("dtype,cin,cout", [("f32", 64, 64), ("bf16", 48, 80)])
+def test_wgrad_deterministic_mode(dtype, cin, cout):
+    """With the deterministic mode the per-pair wgrad writes each work item's
+    block to its own slot and adds them in a fixed order: two runs give
+    bit-identical dW, which matches the oracle at the fp32 tolerance (and
+    the atomic mode's result likewise), on the layer and its mirror view."""
+    coords, size = coords_for("shapes128")
+    rb = sscn.ssc_rulebook_build(dev(coords), size, 3)
+    orb = O.ssc_rulebook(coords, size, 3)
+    n = coords.shape[0]
+    X, W = _draw(n, cin, cout, 27, 50 + cin, dtype)
+    G = S.features(n, cout, S.SEED_GRAD + 50 + cin, bf16=dtype == "bf16")
+    for view, oview in ((rb, orb), (rb.transpose(), O.transpose(orb))):
+        rdw = O.backward(X, W, G, oview)[1]
+        args = (dev(X, TD[dtype]), dev(W, TD[dtype]), dev(G, TD[dtype]), view)
+        try:
+            sscn.set_deterministic(True)
+            _, d1 = sscn.sparse_conv_backward(*args, dgrad=False)
+            _, d2 = sscn.sparse_conv_backward(*args)
+        finally:
+            sscn.set_deterministic(False)
+        np.testing.assert_array_equal(host(d1), host(d2))
+        assert_close(host(d1), rdw, "f32", "deterministic wgrad")
+        _, da = sscn.sparse_conv_backward(*args, dgrad=False)
+        assert_close(host(da), rdw, "f32", "atomic wgrad")

@@ -87,3 +87,23 @@ def test_kernel_timer_brackets_the_row_kernel():
     sscn.sparse_conv_forward(X, W, rb)
     torch.cuda.synchronize()
     assert t.ms() == kernel_ms
+
+
+def test_device_memory_cap_gives_oom_and_recovers():
+    """A cap on the library's device memory below what a build needs makes
+    the build fail with the out-of-memory status (after the idle blocks are
+    released, as on a real failure), and leaves the library usable: without
+    the cap the same build succeeds with the oracle's pair count."""
+    coords, size = coords_for("shapes128")
+    tc = dev(coords)
+    sscn.release_cached()  # no idle block of earlier tests serves the build
+    try:
+        sscn.set_device_memory_cap(1 << 20)
+        with pytest.raises(sscn.SSCNError) as err:
+            sscn.ssc_rulebook_build(tc, size, 3)
+        assert err.value.code == "oom"
+    finally:
+        sscn.set_device_memory_cap(0)
+    rb = sscn.ssc_rulebook_build(tc, size, 3)
+    orb = O.ssc_rulebook(coords, size, 3)
+    assert rb.n_pairs == sum(len(x) for x in orb.outs)
