@@ -247,6 +247,32 @@ def copy_calibration():
     L.sscn_measure_copy(256 << 20, 2, ctypes.byref(v))
 
 
+def scaling_in_sites(stream, reps):
+    """Cost against the number of active sites (the paper's O(a) per layer):
+    the SSC 3^3 rule-book build and the fp32 64-channel forward on the
+    1.8k-site shell (32^3), the 100k-site shapes (128^3 x 4) and the 2M-site
+    scenes (256^3 x 8)."""
+    import torch
+    from paper_1711_10275_amd import sscn
+    from paper_1711_10275_amd import synthetic as S
+    out = []
+    for name, coords, size in (("shell32", S.shell_32(), (32,) * 3), ("shapes128", S.shapes_128(), (128,) * 3),
+                               ("scenes256", S.scenes_256(), (256,) * 3)):
+        tc = torch.from_numpy(coords).cuda()
+        n = int(coords.shape[0])
+        build_ms = _wall_ms(lambda: sscn.ssc_rulebook_build(tc, size, 3), reps)
+        rb = sscn.ssc_rulebook_build(tc, size, 3)
+        X = torch.from_numpy(S.features(n, 64, S.SEED_FEAT + 5)).cuda()
+        W = torch.from_numpy(S.weights(27, 64, 64, S.SEED_WEIGHT + 5)).cuda()
+        fwd_ms = _event_ms(lambda: sscn.sparse_conv_forward(X, W, rb), reps, stream)
+        out.append({"set": name, "sites": n, "pairs": int(rb.n_pairs), "rulebook_build_ms": build_ms,
+                    "build_us_per_1k_sites": build_ms * 1e3 / (n / 1e3), "forward_ms_f32_c64": fwd_ms,
+                    "forward_sites_per_s": n / (fwd_ms * 1e-3),
+                    "forward_tflops": 2.0 * 64 * 64 * rb.n_pairs / (fwd_ms * 1e-3) / 1e12})
+        del rb, X, W, tc
+    return out
+
+
 def sc_then_ssc(tc, size, stream, reps):
     """SC(2, 2) 64 -> 96 channels (128^3 -> 64^3), then SSC 3^3 at 64^3 with 96 channels."""
     import torch
@@ -573,7 +599,8 @@ def main():
                                    "forward_ms": timed(lambda: sscn.sparse_conv_forward(tX, tW, rbs)),
                                    "dgrad_ms": timed(lambda: sscn.sparse_conv_backward(None, tW, tG, rbs, wgrad=False))}
         del rbs
-        result["extra"] = {"sc_then_ssc": sc_then_ssc(tc, size, stream, reps), "unet": unet_scenes(stream, 5),
+        result["extra"] = {"sc_then_ssc": sc_then_ssc(tc, size, stream, reps),
+                           "scaling_in_sites": scaling_in_sites(stream, reps), "unet": unet_scenes(stream, 5),
                            "ops": ops_extra(tc, size, stream, reps)}
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(coords, size, X, W, G, args.cpu_seconds)
