@@ -629,9 +629,10 @@ __global__ void k_split_w(const float* __restrict__ W, int K, int kdim, int ncol
 // weights are loaded WB bytes per row with WB / 16 lanes per row, put in
 // LDS, and read back in the MFMA layout: lane (m, g) takes channels
 // 32 j + 8 g + [0, 8) (j < S) of row m of the step's window (A) and of
-// weight row m of each column block (B).  The MFMAs sum over exactly these
-// channels, so a row's result does not depend on which rows share its
-// block.  B is laid out [o][ncols][kdim] (a contiguous row of reduction
+// weight row m of each column block (B).  Each MFMA sums the channels of
+// one item only (absent rows and channels past a row's end read zeros), in
+// ascending item order, so a row's result does not depend on which rows
+// share its block.  B is laid out [o][ncols][kdim] (a contiguous row of reduction
 // channels per output column).  Row gathers run D - 1 steps ahead in
 // registers and each wavefront's row tile is private to it; the weight
 // tile goes straight from memory into one of two LDS buffers (a buffer
@@ -1796,11 +1797,11 @@ static bool rows_take_untransposed(int kdim, int ncols) {
 }
 
 // Whether an fp32 launch of the row kernel runs through bf16 parts (the
-// weights handed over as the three planes of k_split_w): whole 32-channel
-// windows (rows of 16 channels pair two items per window instead), and
-// the planes within 32-bit buffer offsets.
+// weights handed over as the three planes of k_split_w): rows of at least
+// 16 channels (one item per 32-channel window, channels past the row's end
+// read as zeros), and the planes within 32-bit buffer offsets.
 static bool rows_split(const View& v, int kdim, int ncols) {
-  return kdim >= 32 && kdim * 4 != 64 && (uint64_t)v.K * ncols * kdim * 6 < kOobOffset;
+  return kdim >= 16 && (uint64_t)v.K * ncols * kdim * 6 < kOobOffset;
 }
 
 // DG: a dgrad launch (k_dgrad_rows), else a forward one (k_conv_rows).
@@ -1828,16 +1829,16 @@ static sscn_status launch_rows(const T* X, const void* B, const View& v, int kdi
       return launch_rows_nb<T, 128, 2, 1, true, DG>(X, B, v, kdim, ncols, Y, s);
     }
   }
-  // Rows of half a window (32 bf16 or 16 fp32 channels, 16 bf16 in a
-  // 64-byte window): two items per step.
+  // Rows of 32 bf16 channels (half a window): two items per step, each in
+  // an MFMA of its own.  Rows of 16 bf16 channels take one item per 64-byte
+  // window, half of it zeros, and fp32 rows one item per window: an MFMA
+  // over two items' channels would round a row's sum by the pairing of its
+  // block's items, and so by which rows share the block.
   const uint32_t row_bytes = (uint32_t)kdim * sizeof(T);
-  if (row_bytes == 64)
+  if (sizeof(T) == 2 && row_bytes == 64)
     return wide_cols ? launch_rows_nb<T, 128, 4, 2, false, DG>(X, B, v, kdim, ncols, Y, s)
                      : launch_rows_nb<T, 128, 2, 2, false, DG>(X, B, v, kdim, ncols, Y, s);
   if constexpr (sizeof(T) == 2) {
-    if (row_bytes == 32)
-      return wide_cols ? launch_rows_nb<T, 64, 4, 2, false, DG>(X, B, v, kdim, ncols, Y, s)
-                       : launch_rows_nb<T, 64, 2, 2, false, DG>(X, B, v, kdim, ncols, Y, s);
     if (kdim % 64 != 0)
       return wide_cols ? launch_rows_nb<T, 64, 4, 1, false, DG>(X, B, v, kdim, ncols, Y, s)
                        : launch_rows_nb<T, 64, 2, 1, false, DG>(X, B, v, kdim, ncols, Y, s);

@@ -302,9 +302,11 @@ def test_ssc_filter5(dtype):
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("c", [16, 32])
 def test_packed_items_forward_backward(c, dtype):
-    """Rows of 32 or 64 bytes put two items in each step of the row kernel
-    (fp32 16 channels, bf16 16 and 32 channels): SSC forward and dgrad (the
-    mirror view), SC(2,2) and its transposed (DC) layer, against the oracle."""
+    """Short rows in the row kernel: 32 bf16 channels put two items in each
+    step, 16 bf16 channels take one item per 64-byte window, and fp32 rows
+    of 16 channels one item per 32-channel window of bf16 parts: SSC forward
+    and dgrad (the mirror view), SC(2,2) and its transposed (DC) layer,
+    against the oracle."""
     coords, size = coords_for("shell32")
     rb = sscn.ssc_rulebook_build(dev(coords), size, 3)
     orb = O.ssc_rulebook(coords, size, 3)
@@ -320,6 +322,26 @@ def test_packed_items_forward_backward(c, dtype):
     assert_close(Y, O.forward(Xs, Ws, osc), dtype, f"packed sc {c}")
     Yd, Wd = _draw(sc.n_out, c, c, 8, 11 + c, dtype)
     assert_close(_fwd(sc.transpose(), Yd, Wd, dtype), O.forward(Yd, Wd, O.transpose(osc)), dtype, f"packed dc {c}")
+
+
+@pytest.mark.parametrize("dtype,c", [("f32", 16), ("f32", 64), ("bf16", 16), ("bf16", 32), ("bf16", 64)])
+def test_forward_dgrad_independent_of_row_order(dtype, c):
+    """A row's forward and dgrad result is a sum over its own neighbours in
+    ascending offset order, whichever rows share its block of the plan: the
+    same sites listed in another order give bit-identical rows."""
+    coords, size = coords_for("shapes128")
+    n = coords.shape[0]
+    perm = np.random.default_rng(S.SEED_GEOM + 77).permutation(n)
+    X, W = _draw(n, c, c, 27, 60 + c, dtype)
+    G = S.features(n, c, S.SEED_GRAD + 60 + c, bf16=dtype == "bf16")
+    outs = []
+    for order in (np.arange(n), perm):
+        rb = sscn.ssc_rulebook_build(dev(np.ascontiguousarray(coords[order])), size, 3)
+        y = _fwd(rb, X[order], W, dtype)
+        dx, _ = sscn.sparse_conv_backward(None, dev(W, TD[dtype]), dev(G[order], TD[dtype]), rb, wgrad=False)
+        outs.append((y, host(dx)))
+    np.testing.assert_array_equal(outs[1][0], outs[0][0][perm])
+    np.testing.assert_array_equal(outs[1][1], outs[0][1][perm])
 
 
 @pytest.mark.parametrize("config", ["shell32", "shapes128"])
