@@ -852,12 +852,66 @@ __global__ __launch_bounds__(256) void k_sc_visit(const int4* __restrict__ coord
   }
 }
 
+// k_sc_visit where every input sees at most one output (f <= s: offset
+// i = x mod s per dimension, when that is below f) and K <= 32.  The lanes
+// of a wavefront whose inputs share an output (neighbouring rows of sorted
+// coordinates often do: about half of the surface sites of 2^3 cells) are
+// grouped first, and one lane per output does the atomics for its group:
+// the lowest lane, whose visit is the group's smallest (lanes follow the
+// rows), with the group's offsets in one OR.  Two lanes of a group with the
+// same offset are one location twice.
+__global__ __launch_bounds__(256) void k_sc_visit1(const int4* __restrict__ coords, int64_t n, ScGeom g,
+                                                   Slot* __restrict__ otable, uint64_t omask, int check,
+                                                   unsigned long long* __restrict__ flags,
+                                                   int4* __restrict__ copy) {
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int lane = threadIdx.x & 63;
+  const bool valid = j < n;
+  const int4 c = valid ? coords[j] : make_int4(0, 0, 0, 0);
+  if (valid && copy) copy[j] = c;
+  const bool in_range = valid && site_in_range(c, g);
+  if (valid && !in_range && check) atomicOr(flags, (unsigned long long)kFlagOutOfRange);
+  const int i0 = c.y % g.s, i1 = c.z % g.s, i2 = c.w % g.s;
+  const int o = (i0 * g.f + i1) * g.f + i2;
+  const int y0 = c.y / g.s, y1 = c.z / g.s, y2 = c.w / g.s;
+  const bool hit = in_range && i0 < g.f && i1 < g.f && i2 < g.f && y0 < g.M0 && y1 < g.M1 && y2 < g.M2;
+  const uint64_t key = hit ? pack_key(c.x, y0, y1, y2) : kEmptyKey;
+  // the group of each leader: one pass per distinct output of the wavefront
+  uint64_t todo = __ballot(hit), peers = 0;
+  while (todo) {
+    const int l = __ffsll((unsigned long long)todo) - 1;
+    const uint64_t lk = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(key >> 32), l) << 32) |
+                        (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)key, l);
+    const uint64_t p = __ballot(hit && key == lk);
+    if (lane == l) peers = p;
+    todo &= ~p;
+  }
+  // offsets of each group: one ballot per offset
+  uint32_t bits = 0;
+  for (int b = 0; b < g.K; ++b)
+    if (__ballot(hit && o == b) & peers) bits |= 1u << b;
+  if (!peers) return;
+  if (check && __popc(bits) != __popcll(peers)) atomicOr(flags, (unsigned long long)kFlagDuplicate);
+  uint64_t slot = mix64(key) & omask;
+  while (true) {
+    const unsigned long long prev =
+        atomicCAS((unsigned long long*)&otable[slot].key, (unsigned long long)kEmptyKey, (unsigned long long)key);
+    if (prev == kEmptyKey || prev == key) break;
+    slot = (slot + 1) & omask;
+  }
+  atomicMin(&otable[slot].row, (int32_t)(j * g.K + o));
+  if (check && (atomicOr(&otable[slot].pad, (int32_t)bits) & (int32_t)bits))
+    atomicOr(flags, (unsigned long long)kFlagDuplicate);
+}
+
 // first[v] = 1 iff visit v is the first visit of its output; count pairs
 // per offset (wave ballots summed in LDS, one global atomic per block and
-// offset).
+// offset).  one_target (every input sees at most one output): first is
+// indexed by input, first[j] = 1 iff input j makes the first visit of its
+// output.
 __global__ __launch_bounds__(256) void k_sc_mark(const int4* __restrict__ coords, int64_t n, ScGeom g,
                                                  const Slot* __restrict__ otable, uint64_t omask,
-                                                 int32_t* __restrict__ first,
+                                                 int one_target, int32_t* __restrict__ first,
                                                  unsigned long long* __restrict__ per_offset) {
   __shared__ unsigned int cnt[512];
   for (int o = threadIdx.x; o < g.K; o += blockDim.x) cnt[o] = 0;
@@ -867,6 +921,7 @@ __global__ __launch_bounds__(256) void k_sc_mark(const int4* __restrict__ coords
   const int4 c = valid ? coords[j] : make_int4(0, 0, 0, 0);
   const bool ok = valid && site_in_range(c, g);
   const int lane = threadIdx.x & 63;
+  int32_t any_first = 0;
   for (int o = 0; o < g.K; ++o) {
     int y0, y1, y2;
     int32_t is_first = 0;
@@ -875,20 +930,23 @@ __global__ __launch_bounds__(256) void k_sc_mark(const int4* __restrict__ coords
       const int32_t v = (int32_t)(j * g.K + o);
       is_first = table_lookup(otable, omask, pack_key(c.x, y0, y1, y2)) == v;
     }
-    if (valid) first[j * g.K + o] = is_first;
+    if (valid && !one_target) first[j * g.K + o] = is_first;
+    any_first |= is_first;
     const unsigned long long m = __ballot(hit);
     if (lane == 0 && m) atomicAdd(&cnt[o], (unsigned int)__popcll(m));
   }
+  if (valid && one_target) first[j] = any_first;
   __syncthreads();
   for (int o = threadIdx.x; o < g.K; o += blockDim.x)
     if (cnt[o]) atomicAdd(&per_offset[o], (unsigned long long)cnt[o]);
 }
 
-// Per visit: output row = rank of its output's first visit.  Writes the
+// Per visit: output row = rank of its output's first visit (one_target:
+// rank is indexed by input, as first in k_sc_mark).  Writes the
 // output-major map nbr_out[o][k] = j, the input-major map nbr_in[o][j] = k,
 // and the output coordinates (by the first visitor).
 __global__ __launch_bounds__(256) void k_sc_assign(const int4* __restrict__ coords, int64_t n, ScGeom g,
-                                                   const Slot* __restrict__ otable, uint64_t omask,
+                                                   const Slot* __restrict__ otable, uint64_t omask, int one_target,
                                                    const int32_t* __restrict__ rank, int64_t n_out,
                                                    int32_t* __restrict__ nbr_out,
                                                    int32_t* __restrict__ nbr_in,
@@ -901,7 +959,7 @@ __global__ __launch_bounds__(256) void k_sc_assign(const int4* __restrict__ coor
     int y0, y1, y2;
     if (!sc_target(g, c, o, y0, y1, y2)) continue;
     const int32_t vmin = table_lookup(otable, omask, pack_key(c.x, y0, y1, y2));
-    const int32_t k = rank[vmin];
+    const int32_t k = rank[one_target ? vmin / g.K : vmin];
     nbr_out[(int64_t)o * n_out + k] = (int32_t)j;
     nbr_in[(int64_t)o * n + j] = k;
     if (vmin == (int32_t)(j * g.K + o)) out_coords[k] = make_int4(c.x, y0, y1, y2);
@@ -1923,18 +1981,23 @@ extern "C" sscn_status sc_rulebook_build(const int32_t* coords, int64_t n, const
     if (!visit_checks) ta.add(&table, cap);
     ta.add(&otable, ocap);
     ta.add(&stats, 2 + K);
-    ta.add(&first, (size_t)n * K);
-    ta.add(&rank, (size_t)n * K + 1);
+    // every input sees at most one output (f <= s): the visits are grouped
+    // per output inside each wavefront first, and first / rank hold one
+    // entry per input
+    const bool one_target = per_dim == 1 && K <= 32;
+    ta.add(&first, (size_t)n * (one_target ? 1 : K));
+    ta.add(&rank, (size_t)n * (one_target ? 1 : K) + 1);
     SSCN_TRY(tmp.alloc(ta));
     Arena ia;
     ia.add(&d->in_coords, (size_t)4 * n);
     SSCN_TRY(owned_alloc(d, ia, s));
 
+    auto visit = one_target ? k_sc_visit1 : k_sc_visit;
     if (visit_checks) {
       SSCN_TRY(launch_fill_slots(otable, ocap, INT32_MAX, s, stats, 2 + K));
       if (n > 0) {
-        k_sc_visit<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, 1, stats,
-                                                    (int4*)d->in_coords);
+        visit<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, 1, stats,
+                                               (int4*)d->in_coords);
         SSCN_HIP(hipGetLastError());
       }
     } else {
@@ -1944,17 +2007,18 @@ extern "C" sscn_status sc_rulebook_build(const int32_t* coords, int64_t n, const
         k_insert<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g.L0, g.L1, g.L2, table, cap - 1, stats,
                                                  (int4*)d->in_coords);
         SSCN_HIP(hipGetLastError());
-        k_sc_visit<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, 0, stats,
-                                                    nullptr);
+        visit<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, 0, stats, nullptr);
         SSCN_HIP(hipGetLastError());
       }
     }
     if (n > 0) {
-      k_sc_mark<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, first, stats + 1);
+      k_sc_mark<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, one_target ? 1 : 0,
+                                                 first, stats + 1);
       SSCN_HIP(hipGetLastError());
-      SSCN_TRY(exclusive_scan_i32(first, rank, n * K, s));
-      // n_out = rank[n K] joins the readback
-      SSCN_HIP(hipMemcpyAsync(stats + 1 + K, rank + (size_t)n * K, sizeof(int32_t), hipMemcpyDeviceToDevice, s));
+      const int64_t n_visits = one_target ? n : n * K;  // entries of first / rank
+      SSCN_TRY(exclusive_scan_i32(first, rank, n_visits, s));
+      // n_out = rank[n_visits] joins the readback
+      SSCN_HIP(hipMemcpyAsync(stats + 1 + K, rank + (size_t)n_visits, sizeof(int32_t), hipMemcpyDeviceToDevice, s));
 
     }
     std::vector<unsigned long long> host(2 + K);
@@ -1991,7 +2055,8 @@ extern "C" sscn_status sc_rulebook_build(const int32_t* coords, int64_t n, const
       SSCN_TRY(tmp.alloc(na));
       SSCN_TRY(fill_i32(nbr_out, -1, (int64_t)K * n_out, s));
       SSCN_TRY(fill_i32(nbr_in, -1, (int64_t)K * n, s));
-      k_sc_assign<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, rank, n_out,
+      k_sc_assign<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, one_target ? 1 : 0,
+                                                   rank, n_out,
                                                    nbr_out, nbr_in, (int4*)d->out_coords);
       SSCN_HIP(hipGetLastError());
       SSCN_TRY(compact_storage(nbr_out, n_out, K, d->fwd, s, false, d->fwd.row_mask));

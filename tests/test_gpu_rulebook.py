@@ -142,6 +142,27 @@ def test_shuffled_rows():
     np.testing.assert_array_equal(host(sc.out_coords()), osc.out_coords)
 
 
+def test_sc_visits_grouped_per_output():
+    """With f <= s every input sees one output, and the SC build groups the
+    visits of one output inside each wavefront before its atomics: sorted
+    rows (many groups) and shuffled rows (few) give the oracle's rule book
+    and numbering, and a repeated location is reported when both copies
+    fall in one group, in one wavefront but not side by side, and in
+    different wavefronts."""
+    c, size = coords_for("shapes128")
+    perm = np.random.default_rng(5).permutation(c.shape[0])
+    for rows in (c, np.ascontiguousarray(c[perm])):
+        sc = sscn.sc_rulebook_build(dev(rows), size, 2, 2)
+        osc = O.sc_rulebook(rows, size, 2, 2)
+        assert_same_rulebook(sc, osc, "grouped sc22")
+        np.testing.assert_array_equal(host(sc.out_coords()), osc.out_coords)
+    for at, src in ((641, 640), (650, 643), (c.shape[0], 700)):
+        rep = np.ascontiguousarray(np.insert(c, at, c[src], axis=0))
+        with pytest.raises(sscn.SSCNError) as e:
+            sscn.sc_rulebook_build(dev(rep), size, 2, 2)
+        assert e.value.code == "duplicate", (at, src)
+
+
 @pytest.mark.parametrize("f", [3, 5])
 def test_mirrored_probe_on_shuffled_rows(f):
     """From 2^18 sites on, the SSC build looks up only the offsets below the
