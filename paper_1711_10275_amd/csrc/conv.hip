@@ -1797,11 +1797,12 @@ static bool rows_take_untransposed(int kdim, int ncols) {
 }
 
 // Whether an fp32 launch of the row kernel runs through bf16 parts (the
-// weights handed over as the three planes of k_split_w): rows of at least
-// 16 channels (one item per 32-channel window, channels past the row's end
-// read as zeros), and the planes within 32-bit buffer offsets.
+// weights handed over as the three planes of k_split_w): rows of 16 or at
+// least 32 channels (one item per 32-channel window, channels past the
+// row's end read as zeros; rows of 24 channels run faster on the fp32
+// MFMAs), and the planes within 32-bit buffer offsets.
 static bool rows_split(const View& v, int kdim, int ncols) {
-  return kdim >= 16 && (uint64_t)v.K * ncols * kdim * 6 < kOobOffset;
+  return (kdim == 16 || kdim >= 32) && (uint64_t)v.K * ncols * kdim * 6 < kOobOffset;
 }
 
 // DG: a dgrad launch (k_dgrad_rows), else a forward one (k_conv_rows).
@@ -2212,7 +2213,10 @@ static int wgrad_blocks(int c) {
 
 // ------------------------------------------------ row-block wgrad (bf16)
 // dW_o = sum over the pairs (j, k) of offset o of X[j]^T dY[k] for bf16
-// layers of 32 or 64 output and 32 to 128 input channels.  A workgroup takes blocks of the
+// layers of 32, 64, 96, 128 or 160 output channels and a multiple of 32
+// input channels (a workgroup takes one tile of CI input channels and all
+// CO output ones; wider inputs are split over several tiles, each with its
+// own slice of the X rows and all of the dY rows).  A workgroup takes blocks of the
 // row-block plan (64 output rows k with one item per offset of their
 // union, as the forward walks them): the block's dY rows and each item's
 // gathered X rows go straight into row-major LDS tiles (direct loads, 16
@@ -2241,18 +2245,20 @@ __device__ __forceinline__ bf16x8 tile_operand_tr(const char* tile, int rb, int 
   return __builtin_bit_cast(bf16x8, make_uint4(a.x, a.y, b.x, b.y));
 }
 
-// CI x CO channels; OPG offsets per group (grid.y groups); partials
-// P[y][x][oo][CI][CO] (x < gridDim.x workgroups).  The 16 x 16 output tiles
-// t = (ti, tj) are dealt TPW per wavefront in row-major order: either a
-// wavefront's tiles share one row ti (TPW <= NTJ) or cover whole rows.
+// A tile of CI x CO channels; OPG offsets per group; grid.y = channel
+// tiles x groups (y = tile * groups + group; tile = input-channel slice,
+// of x_ld / (2 CI)); partials P[y][x][oo][CI][CO] (x < gridDim.x
+// workgroups).  x_ld, y_ld: bytes per row of X and dY.  The 16 x 16 output
+// tiles t = (ti, tj) are dealt TPW per wavefront in row-major order: either
+// a wavefront's tiles share one row ti (TPW <= NTJ) or cover whole rows.
 template <int CI, int CO, int OPG>
-__global__ __launch_bounds__(256) void k_wgrad_rows(const bf16_t* __restrict__ X, uint32_t x_bytes,
-                                                    const bf16_t* __restrict__ dY, uint32_t y_bytes,
+__global__ __launch_bounds__(256) void k_wgrad_rows(const bf16_t* __restrict__ X, uint32_t x_bytes, uint32_t x_ld,
+                                                    const bf16_t* __restrict__ dY, uint32_t y_bytes, uint32_t y_ld,
                                                     const int32_t* __restrict__ perm,
                                                     const int32_t* __restrict__ b_first,
                                                     const int32_t* __restrict__ b_order,
                                                     const uint32_t* __restrict__ items, int64_t n_blocks, int K,
-                                                    float* __restrict__ part) {
+                                                    int groups, float* __restrict__ part) {
   constexpr int NTI = CI / 16, NTJ = CO / 16, TPW = NTI * NTJ / 4;
   constexpr bool ONE_ROW = TPW <= NTJ;               // the wavefront's tiles share ti
   constexpr int NA = ONE_ROW ? 1 : TPW / NTJ;        // tile rows (A operands) per wavefront
@@ -2264,7 +2270,8 @@ __global__ __launch_bounds__(256) void k_wgrad_rows(const bf16_t* __restrict__ X
   __shared__ __attribute__((aligned(16))) char Xs[2][64 * XB];
   __shared__ __attribute__((aligned(16))) char Ys[64 * YB];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int o_lo = blockIdx.y * OPG, o_hi = min(K, o_lo + OPG);
+  const int o_lo = (int)(blockIdx.y % (unsigned)groups) * OPG, o_hi = min(K, o_lo + OPG);
+  const uint32_t x0 = blockIdx.y / (unsigned)groups * (uint32_t)XB;  // the tile's bytes of an X row
   // this wavefront's tiles: t = TPW wave + q, (ti, tj) = (t / NTJ, t % NTJ):
   // rows ti0 + a (a < NA), columns tj0 + bq (bq < NB)
   const int ti0 = (TPW * wave) / NTJ, tj0 = ONE_ROW ? (TPW * wave) % NTJ : 0;
@@ -2289,7 +2296,7 @@ __global__ __launch_bounds__(256) void k_wgrad_rows(const bf16_t* __restrict__ X
     for (int i = 0; i < NXC; ++i) {
       const int c = wave + 4 * i;
       const uint32_t r = ent[i] & kPlanNoRow;
-      const uint32_t off = r != kPlanNoRow ? r * (uint32_t)XB + x_piece(c) : kOobOffset;
+      const uint32_t off = r != kPlanNoRow ? r * x_ld + x0 + x_piece(c) : kOobOffset;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (__attribute__((address_space(3))) void*)&Xs[buf][c * 1024], 16,
                                                (int)off, 0, 0, 0);
     }
@@ -2315,7 +2322,7 @@ __global__ __launch_bounds__(256) void k_wgrad_rows(const bf16_t* __restrict__ X
       const int c = wave + 4 * i;
       const int row = (c * 1024 + 16 * lane) / YB;
       const int32_t k = perm[b * kPlanRows + row];
-      const uint32_t off = k >= 0 ? (uint32_t)k * YB + (uint32_t)((c * 1024 + 16 * lane) % YB) : kOobOffset;
+      const uint32_t off = k >= 0 ? (uint32_t)k * y_ld + (uint32_t)((c * 1024 + 16 * lane) % YB) : kOobOffset;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(ry, (__attribute__((address_space(3))) void*)&Ys[c * 1024], 16,
                                                (int)off, 0, 0, 0);
     }
@@ -2371,23 +2378,26 @@ __global__ __launch_bounds__(256) void k_wgrad_rows(const bf16_t* __restrict__ X
     }
 }
 
-// dW[o'][ci][co] = the sum over the workgroups x of P[y][x][oo][ci][co] for
-// the stored offset o = y OPG + oo (o' = K - 1 - o on a mirrored view), in
-// a fixed order: a workgroup takes 64 consecutive outputs, its wavefront w
-// the partials x = 4 i + w (four running sums, by i mod 4, eight loads in
+// dW[o'][ci][co] = the sum over the workgroups x of P[y][x][oo][ci'][co]
+// for the stored offset o = g opg + oo and input channel ci = tile ti + ci'
+// (y = tile groups + g; o' = K - 1 - o on a mirrored view), in a fixed
+// order: a workgroup takes 64 consecutive outputs, its wavefront w the
+// partials x = 4 i + w (four running sums, by i mod 4, eight loads in
 // flight), and the sums are added in order of w and i mod 4.
 __global__ __launch_bounds__(256) void k_wgrad_sum(const float* __restrict__ part, int K, int cin, int cout, int opg,
-                                                   int64_t n_wg, int mirror, float* __restrict__ dW) {
+                                                   int ti, int groups, int64_t n_wg, int mirror,
+                                                   float* __restrict__ dW) {
   __shared__ float red[4][64];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int64_t per_o = (int64_t)cin * cout;
+  const int64_t per_o = (int64_t)cin * cout, per_t = (int64_t)ti * cout;
   const int64_t t = (int64_t)blockIdx.x * 64 + lane;
   const bool ok = t < K * per_o;
   const int o = ok ? (int)(t / per_o) : 0;
   const int64_t e = ok ? t % per_o : 0;
-  const int y = o / opg, oo = o % opg;
-  const float* p = part + ((int64_t)y * n_wg * opg + oo) * per_o + e;
-  const int64_t xs = (int64_t)opg * per_o;  // from one workgroup's partials to the next
+  const int ci = (int)(e / cout), tile = ci / ti;
+  const int y = tile * groups + o / opg, oo = o % opg;
+  const float* p = part + ((int64_t)y * n_wg * opg + oo) * per_t + e - (int64_t)tile * per_t;
+  const int64_t xs = (int64_t)opg * per_t;  // from one workgroup's partials to the next
   float s[4] = {0.f, 0.f, 0.f, 0.f};
   int64_t x = wave;
   for (; x + 28 < n_wg; x += 32) {
@@ -2404,10 +2414,12 @@ __global__ __launch_bounds__(256) void k_wgrad_sum(const float* __restrict__ par
     dW[(int64_t)(mirror ? K - 1 - o : o) * per_o + e] = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
 }
 
-// Whether the row-block wgrad takes a bf16 layer: c_in x c_out one of
-// 32 x 32, 64 x 32, 64 x 64, 128 x 64, and the plan's limits.
+// Whether the row-block wgrad takes a bf16 layer: c_out one of 32, 64,
+// 96, 128, 160 and c_in a multiple of 32 (at most 1024), and the plan's
+// limits.
 static bool wgrad_rows_eligible(const View& v, int cin, int cout) {
-  const bool shape = (cout == 32 && (cin == 32 || cin == 64)) || (cout == 64 && (cin == 64 || cin == 128));
+  const bool shape = (cout == 32 || cout == 64 || cout == 96 || cout == 128 || cout == 160) && cin % 32 == 0 &&
+                     cin <= 1024;
   return shape && v.K <= 32 &&
          (uint64_t)std::max<int64_t>(v.n_in, 1) * cin * 2 < kOobOffset &&
          (uint64_t)std::max<int64_t>(v.n_out, 1) * cout * 2 < kOobOffset &&
@@ -2415,29 +2427,36 @@ static bool wgrad_rows_eligible(const View& v, int cin, int cout) {
 }
 
 template <int CI, int CO, int OPG>
-static sscn_status launch_wgrad_rows_t(const bf16_t* X, const bf16_t* dY, const View& v, float* dW, hipStream_t s) {
+static sscn_status launch_wgrad_rows_t(const bf16_t* X, const bf16_t* dY, const View& v, int cin, float* dW,
+                                       hipStream_t s) {
   SSCN_TRY(ensure_plan(v, s));
   const int64_t nb = v.st->n_blocks;
-  const int groups = (v.K + OPG - 1) / OPG;
+  const int groups = (v.K + OPG - 1) / OPG, tiles = cin / CI;
   auto kern = k_wgrad_rows<CI, CO, OPG>;
   int cus = 256, per_cu = 1;
   occupancy((const void*)kern, 256, 0, &per_cu, &cus);
-  const int64_t gx = std::max<int64_t>(1, std::min<int64_t>(nb, (int64_t)cus * per_cu / groups));
+  // one resident wave of workgroups; at least 4 blocks each (fewer partial
+  // sums to add on small layers)
+  const int64_t gx = std::max<int64_t>(
+      1, std::min<int64_t>(ceil_div(nb, 4), (int64_t)cus * per_cu / ((int64_t)groups * tiles)));
   float* part = nullptr;
-  SSCN_TRY(dev_alloc((void**)&part, sizeof(float) * (size_t)gx * groups * OPG * CI * CO, s));
-  const uint32_t xb = (uint32_t)((uint64_t)std::max<int64_t>(v.n_in, 1) * CI * 2);
+  SSCN_TRY(dev_alloc((void**)&part, sizeof(float) * (size_t)gx * groups * tiles * OPG * CI * CO, s));
+  const uint32_t xb = (uint32_t)((uint64_t)std::max<int64_t>(v.n_in, 1) * cin * 2);
   const uint32_t yb = (uint32_t)((uint64_t)std::max<int64_t>(v.n_out, 1) * CO * 2);
+  const dim3 grid((unsigned)gx, (unsigned)(groups * tiles));
   hipEvent_t t0, t1;
   if (take_launch_timer(&t0, &t1))
-    hipExtLaunchKernelGGL(kern, dim3((unsigned)gx, (unsigned)groups), dim3(256), 0, s, t0, t1, 0, X, xb, dY, yb,
-                          v.st->perm, v.st->b_first, v.st->b_order, v.st->items, nb, v.K, part);
+    hipExtLaunchKernelGGL(kern, grid, dim3(256), 0, s, t0, t1, 0, X, xb, (uint32_t)cin * 2u, dY, yb,
+                          (uint32_t)CO * 2u, v.st->perm, v.st->b_first, v.st->b_order, v.st->items, nb, v.K, groups,
+                          part);
   else
-    kern<<<dim3((unsigned)gx, (unsigned)groups), 256, 0, s>>>(X, xb, dY, yb, v.st->perm, v.st->b_first,
-                                                              v.st->b_order, v.st->items, nb, v.K, part);
+    kern<<<grid, 256, 0, s>>>(X, xb, (uint32_t)cin * 2u, dY, yb, (uint32_t)CO * 2u, v.st->perm, v.st->b_first,
+                              v.st->b_order, v.st->items, nb, v.K, groups, part);
   hipError_t e = hipGetLastError();
   if (e == hipSuccess) {
-    const int64_t total = (int64_t)v.K * CI * CO;
-    k_wgrad_sum<<<(unsigned)ceil_div(total, 64), 256, 0, s>>>(part, v.K, CI, CO, OPG, gx, v.mirror ? 1 : 0, dW);
+    const int64_t total = (int64_t)v.K * cin * CO;
+    k_wgrad_sum<<<(unsigned)ceil_div(total, 64), 256, 0, s>>>(part, v.K, cin, CO, OPG, CI, groups, gx,
+                                                              v.mirror ? 1 : 0, dW);
     e = hipGetLastError();
   }
   dev_free(part, s);
@@ -2447,14 +2466,29 @@ static sscn_status launch_wgrad_rows_t(const bf16_t* X, const bf16_t* dY, const 
 static sscn_status launch_wgrad_rows(const bf16_t* X, const bf16_t* dY, const View& v, int cin, int cout, float* dW,
                                      hipStream_t s) {
   if (v.n_out == 0 || v.st->n_tiles == 0) return fill_f32(dW, 0.f, (int64_t)v.K * cin * cout, s);
-  // offsets per group: the wavefront's accumulators (OPG x TPW x 4 VGPRs)
-  // and operands within about 170 VGPRs
-  if (cout == 32) {
-    if (cin == 32) return launch_wgrad_rows_t<32, 32, 27>(X, dY, v, dW, s);
-    return launch_wgrad_rows_t<64, 32, 14>(X, dY, v, dW, s);
+  // Input-channel tiles of 128 (c_in = 128, c_out = 64), 64 where they
+  // divide c_in, else 32; offsets per group: the wavefront's accumulators
+  // (OPG x TPW x 4 VGPRs, TPW = CI CO / 1024) and operands within about 170
+  // VGPRs.
+  const bool t64 = cin % 64 == 0;
+  switch (cout) {
+    case 32:
+      return t64 ? launch_wgrad_rows_t<64, 32, 14>(X, dY, v, cin, dW, s)
+                 : launch_wgrad_rows_t<32, 32, 27>(X, dY, v, cin, dW, s);
+    case 64:
+      if (cin == 128) return launch_wgrad_rows_t<128, 64, 3>(X, dY, v, cin, dW, s);
+      return t64 ? launch_wgrad_rows_t<64, 64, 6>(X, dY, v, cin, dW, s)
+                 : launch_wgrad_rows_t<32, 64, 13>(X, dY, v, cin, dW, s);
+    case 96:
+      return t64 ? launch_wgrad_rows_t<64, 96, 4>(X, dY, v, cin, dW, s)
+                 : launch_wgrad_rows_t<32, 96, 9>(X, dY, v, cin, dW, s);
+    case 128:
+      return t64 ? launch_wgrad_rows_t<64, 128, 3>(X, dY, v, cin, dW, s)
+                 : launch_wgrad_rows_t<32, 128, 6>(X, dY, v, cin, dW, s);
+    default:  // 160
+      return t64 ? launch_wgrad_rows_t<64, 160, 2>(X, dY, v, cin, dW, s)
+                 : launch_wgrad_rows_t<32, 160, 5>(X, dY, v, cin, dW, s);
   }
-  if (cin == 64) return launch_wgrad_rows_t<64, 64, 6>(X, dY, v, dW, s);
-  return launch_wgrad_rows_t<128, 64, 3>(X, dY, v, dW, s);
 }
 
 // zeroed: dW is already zero on stream s (cleared by the dgrad launch before it).

@@ -344,14 +344,21 @@ def test_forward_dgrad_independent_of_row_order(dtype, c):
     np.testing.assert_array_equal(outs[1][1], outs[0][1][perm])
 
 
-@pytest.mark.parametrize("config", ["shell32", "shapes128"])
-@pytest.mark.parametrize("cin,cout", [(32, 32), (64, 32), (64, 64), (128, 64)])
+WG_ROWS = [("shell32", 32, 32), ("shell32", 64, 32), ("shell32", 64, 64), ("shell32", 128, 64),
+           ("shell32", 96, 160), ("shapes128", 32, 32), ("shapes128", 64, 32), ("shapes128", 64, 64),
+           ("shapes128", 128, 64), ("shapes128", 96, 64), ("shapes128", 128, 32), ("shapes128", 96, 96),
+           ("shapes128", 192, 96), ("shapes128", 128, 128), ("shapes128", 256, 128), ("shapes128", 96, 128),
+           ("shapes128", 160, 160), ("shapes128", 128, 160)]
+
+
+@pytest.mark.parametrize("config,cin,cout", WG_ROWS)
 def test_wgrad_row_blocks_bf16(config, cin, cout):
-    """bf16 wgrad of these widths runs over the row-block plan (gathered
-    rows into LDS, transposed operand reads, partial sums added in a fixed
-    order; 1, 2, 5 and 9 offset groups): SSC and its mirror view at the fp32
-    tolerance against the oracle, bit-identical on a second call, and the
-    same from a wgrad-only call."""
+    """bf16 wgrad runs over the row-block plan (gathered rows into LDS,
+    transposed operand reads, partial sums added in a fixed order) for
+    32 to 160 output channels, with the input channels in one tile or split
+    into tiles of 32 or 64: SSC and its mirror view at the fp32 tolerance
+    against the oracle, bit-identical on a second call, and the same from a
+    wgrad-only call."""
     coords, size = coords_for(config)
     rb = sscn.ssc_rulebook_build(dev(coords), size, 3)
     orb = O.ssc_rulebook(coords, size, 3)
@@ -368,16 +375,16 @@ def test_wgrad_row_blocks_bf16(config, cin, cout):
         np.testing.assert_array_equal(host(dw2), host(dw))
 
 
-@pytest.mark.parametrize("cin", [32, 64])
-def test_wgrad_row_blocks_sc_dc_bf16(cin):
+@pytest.mark.parametrize("cin,cout", [(32, 32), (64, 32), (96, 128), (160, 128)])
+def test_wgrad_row_blocks_sc_dc_bf16(cin, cout):
     """The row-block bf16 wgrad on SC(2,2) (8 offsets) and on its transposed
     (DC) layer, whose plan is built on first use."""
     coords, size = coords_for("shell32")
     sc = sscn.sc_rulebook_build(dev(coords), size, 2, 2)
     osc = O.sc_rulebook(coords, size, 2, 2)
     for view, oview in ((sc, osc), (sc.transpose(), O.transpose(osc))):
-        X, W = _draw(view.n_in, cin, 32, 8, 30 + cin, "bf16")
-        G = S.features(view.n_out, 32, S.SEED_GRAD + 30 + cin, bf16=True)
+        X, W = _draw(view.n_in, cin, cout, 8, 30 + cin, "bf16")
+        G = S.features(view.n_out, cout, S.SEED_GRAD + 30 + cin, bf16=True)
         dx, dw = sscn.sparse_conv_backward(dev(X, torch.bfloat16), dev(W, torch.bfloat16),
                                            dev(G, torch.bfloat16), view)
         rdx, rdw = O.backward(X, W, G, oview)
