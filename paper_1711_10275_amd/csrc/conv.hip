@@ -2246,14 +2246,15 @@ __device__ __forceinline__ bf16x8 tile_operand_tr(const char* tile, int rb, int 
 }
 
 // A tile of CI x CO channels; OPG offsets per group; grid.y = channel
-// tiles x groups (y = tile * groups + group; tile = input-channel slice,
-// of x_ld / (2 CI)); partials P[y][x][oo][CI][CO] (x < gridDim.x
-// workgroups).  x_ld, y_ld: bytes per row of X and dY.  The 16 x 16 output
-// tiles t = (ti, tj) are dealt TPW per wavefront in row-major order: either
-// a wavefront's tiles share one row ti (TPW <= NTJ) or cover whole rows.
-template <int CI, int CO, int OPG>
+// tiles x groups (y = tile * groups + group; tile = input-channel slice of
+// CI channels, TILED: x_ld / (2 CI) of them, else one with x_ld = 2 CI);
+// partials P[y][x][oo][CI][CO] (x < gridDim.x workgroups).  x_ld: bytes
+// per row of X.  The 16 x 16 output tiles t = (ti, tj) are dealt TPW per
+// wavefront in row-major order: either a wavefront's tiles share one row ti
+// (TPW <= NTJ) or cover whole rows.
+template <int CI, int CO, int OPG, bool TILED>
 __global__ __launch_bounds__(256) void k_wgrad_rows(const bf16_t* __restrict__ X, uint32_t x_bytes, uint32_t x_ld,
-                                                    const bf16_t* __restrict__ dY, uint32_t y_bytes, uint32_t y_ld,
+                                                    const bf16_t* __restrict__ dY, uint32_t y_bytes,
                                                     const int32_t* __restrict__ perm,
                                                     const int32_t* __restrict__ b_first,
                                                     const int32_t* __restrict__ b_order,
@@ -2270,8 +2271,10 @@ __global__ __launch_bounds__(256) void k_wgrad_rows(const bf16_t* __restrict__ X
   __shared__ __attribute__((aligned(16))) char Xs[2][64 * XB];
   __shared__ __attribute__((aligned(16))) char Ys[64 * YB];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int o_lo = (int)(blockIdx.y % (unsigned)groups) * OPG, o_hi = min(K, o_lo + OPG);
-  const uint32_t x0 = blockIdx.y / (unsigned)groups * (uint32_t)XB;  // the tile's bytes of an X row
+  const int o_lo = (int)(TILED ? blockIdx.y % (unsigned)groups : blockIdx.y) * OPG, o_hi = min(K, o_lo + OPG);
+  // the tile's bytes of an X row, and the row pitch
+  const uint32_t x0 = TILED ? blockIdx.y / (unsigned)groups * (uint32_t)XB : 0u;
+  const uint32_t xp = TILED ? x_ld : (uint32_t)XB;
   // this wavefront's tiles: t = TPW wave + q, (ti, tj) = (t / NTJ, t % NTJ):
   // rows ti0 + a (a < NA), columns tj0 + bq (bq < NB)
   const int ti0 = (TPW * wave) / NTJ, tj0 = ONE_ROW ? (TPW * wave) % NTJ : 0;
@@ -2296,7 +2299,7 @@ __global__ __launch_bounds__(256) void k_wgrad_rows(const bf16_t* __restrict__ X
     for (int i = 0; i < NXC; ++i) {
       const int c = wave + 4 * i;
       const uint32_t r = ent[i] & kPlanNoRow;
-      const uint32_t off = r != kPlanNoRow ? r * x_ld + x0 + x_piece(c) : kOobOffset;
+      const uint32_t off = r != kPlanNoRow ? r * xp + x0 + x_piece(c) : kOobOffset;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (__attribute__((address_space(3))) void*)&Xs[buf][c * 1024], 16,
                                                (int)off, 0, 0, 0);
     }
@@ -2322,7 +2325,7 @@ __global__ __launch_bounds__(256) void k_wgrad_rows(const bf16_t* __restrict__ X
       const int c = wave + 4 * i;
       const int row = (c * 1024 + 16 * lane) / YB;
       const int32_t k = perm[b * kPlanRows + row];
-      const uint32_t off = k >= 0 ? (uint32_t)k * y_ld + (uint32_t)((c * 1024 + 16 * lane) % YB) : kOobOffset;
+      const uint32_t off = k >= 0 ? (uint32_t)k * YB + (uint32_t)((c * 1024 + 16 * lane) % YB) : kOobOffset;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(ry, (__attribute__((address_space(3))) void*)&Ys[c * 1024], 16,
                                                (int)off, 0, 0, 0);
     }
@@ -2394,7 +2397,7 @@ __global__ __launch_bounds__(256) void k_wgrad_sum(const float* __restrict__ par
   const bool ok = t < K * per_o;
   const int o = ok ? (int)(t / per_o) : 0;
   const int64_t e = ok ? t % per_o : 0;
-  const int ci = (int)(e / cout), tile = ci / ti;
+  const int tile = ti == cin ? 0 : (int)(e / cout) / ti;  // (uniform test: one tile needs no divisions)
   const int y = tile * groups + o / opg, oo = o % opg;
   const float* p = part + ((int64_t)y * n_wg * opg + oo) * per_t + e - (int64_t)tile * per_t;
   const int64_t xs = (int64_t)opg * per_t;  // from one workgroup's partials to the next
@@ -2432,7 +2435,7 @@ static sscn_status launch_wgrad_rows_t(const bf16_t* X, const bf16_t* dY, const 
   SSCN_TRY(ensure_plan(v, s));
   const int64_t nb = v.st->n_blocks;
   const int groups = (v.K + OPG - 1) / OPG, tiles = cin / CI;
-  auto kern = k_wgrad_rows<CI, CO, OPG>;
+  auto kern = tiles > 1 ? k_wgrad_rows<CI, CO, OPG, true> : k_wgrad_rows<CI, CO, OPG, false>;
   int cus = 256, per_cu = 1;
   occupancy((const void*)kern, 256, 0, &per_cu, &cus);
   // one resident wave of workgroups; at least 4 blocks each (fewer partial
@@ -2446,12 +2449,11 @@ static sscn_status launch_wgrad_rows_t(const bf16_t* X, const bf16_t* dY, const 
   const dim3 grid((unsigned)gx, (unsigned)(groups * tiles));
   hipEvent_t t0, t1;
   if (take_launch_timer(&t0, &t1))
-    hipExtLaunchKernelGGL(kern, grid, dim3(256), 0, s, t0, t1, 0, X, xb, (uint32_t)cin * 2u, dY, yb,
-                          (uint32_t)CO * 2u, v.st->perm, v.st->b_first, v.st->b_order, v.st->items, nb, v.K, groups,
-                          part);
+    hipExtLaunchKernelGGL(kern, grid, dim3(256), 0, s, t0, t1, 0, X, xb, (uint32_t)cin * 2u, dY, yb, v.st->perm,
+                          v.st->b_first, v.st->b_order, v.st->items, nb, v.K, groups, part);
   else
-    kern<<<grid, 256, 0, s>>>(X, xb, (uint32_t)cin * 2u, dY, yb, (uint32_t)CO * 2u, v.st->perm, v.st->b_first,
-                              v.st->b_order, v.st->items, nb, v.K, groups, part);
+    kern<<<grid, 256, 0, s>>>(X, xb, (uint32_t)cin * 2u, dY, yb, v.st->perm, v.st->b_first, v.st->b_order,
+                              v.st->items, nb, v.K, groups, part);
   hipError_t e = hipGetLastError();
   if (e == hipSuccess) {
     const int64_t total = (int64_t)v.K * cin * CO;
