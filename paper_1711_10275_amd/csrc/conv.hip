@@ -769,29 +769,15 @@ __device__ __forceinline__ void conv_rows_block(
         d_voff[jj] = in ? (uint32_t)(col0 + col) * row_bytes + d_ch[jj] - (uint32_t)d_u[jj] * row_bytes : kOobOffset;
     }
 
-    // items for which this wavefront's 16 rows have at least one pair (bit
-    // per item, wavefront-uniform): lane l tests item l / 16 + 4 q, row l % 16
-    uint32_t have = 0;
-    {
-      uint32_t e[8];
-#pragma unroll
-      for (int q = 0; q < 8; ++q) e[q] = ents[min((lane >> 4) + 4 * q, n_items - 1) * kPlanRows + wave * 16 + m];
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const uint64_t bits = __ballot((e[q] & kPlanNoRow) != kPlanNoRow);
-#pragma unroll
-        for (int h = 0; h < 4; ++h)
-          if ((bits >> (16 * h)) & 0xffffull) have |= 1u << (4 * q + h);
-      }
-    }
-
     uint4 ga[D][NA], gb[D][NBP];  // global loads in flight
     int ld_item = 0, ld_ks = 0, ld_step = 0;
     // per ring slot, the weight tile's offset byte (PK > 1: per item, or
-    // kOobOffset past the last), window byte and whether the step exists
-    // (its tile is loaded a step after its rows)
+    // kOobOffset past the last), window byte, whether the step exists (its
+    // tile is loaded a step after its rows), and whether this wavefront's 16
+    // rows have no pair in it (its MFMAs are skipped; wavefront-uniform: the
+    // lanes' entries cover the 16 rows and the step's items)
     uint32_t dm_off[D][PK], dm_win[D];
-    bool dm_live[D];
+    bool dm_live[D], dm_skip[D];
     // entries of the next step to be issued, read one step ahead (every
     // entry of an item carries the item's offset)
     uint32_t nx_r[NA];
@@ -812,13 +798,16 @@ __device__ __forceinline__ void conv_rows_block(
                               kPlanRowBits);
           soff[u] = (uint32_t)(mirror ? K - 1 - o : o) * w_stride;
         }
+        bool any = false;
 #pragma unroll
         for (int i = 0; i < NA; ++i) {
           const uint32_t r = nx_r[i] & kPlanNoRow;
           const bool ok = live && ld_item + a_u < n_items && r != kPlanNoRow;
+          any = any || ok;
           const auto v = __builtin_amdgcn_raw_buffer_load_b128(rx, (int)(ok ? r * row_bytes + a_in : kOobOffset), 0, 0);
           ga[slot][i] = make_uint4(v[0], v[1], v[2], v[3]);
         }
+        dm_skip[slot] = __ballot(any) == 0;
 #pragma unroll
         for (int u = 0; u < PK; ++u) dm_off[slot][u] = ld_item + u < n_items ? soff[u] : kOobOffset;
         dm_win[slot] = 0;
@@ -836,14 +825,17 @@ __device__ __forceinline__ void conv_rows_block(
         dm_win[slot] = SP ? win / 2u : win;  // SP: 32 channels are 64 bytes of each bf16 plane row
         dm_live[slot] = live;
       }
+      bool any = false;
 #pragma unroll
       for (int i = 0; i < NA; ++i) {
         const uint32_t r = nx_r[i] & kPlanNoRow;
+        any = any || (live && r != kPlanNoRow);
         const bool ok = live && r != kPlanNoRow && win + a_byte < row_bytes;
         const auto v = __builtin_amdgcn_raw_buffer_load_b128(rx, (int)(ok ? r * row_bytes + win + a_byte : kOobOffset),
                                                              0, 0);
         ga[slot][i] = make_uint4(v[0], v[1], v[2], v[3]);
       }
+      dm_skip[slot] = __ballot(any) == 0;
 #pragma unroll
       for (int q = 0; q < (DB ? 0 : NBP); ++q) {
         const uint32_t bwin = win;
@@ -876,17 +868,10 @@ __device__ __forceinline__ void conv_rows_block(
         }
       }
     };
-    int mul_item = 0, mul_ks = 0;  // item of the step being multiplied
-    auto multiply = [&](int buf) {
+    // the step in ring slot sl, with its weight tile in LDS buffer buf
+    auto multiply = [&](int sl, int buf) {
       // a wavefront whose 16 rows have no pair for the item(s) skips the MFMAs
-      const bool skip = ((have >> mul_item) & ((1u << PK) - 1u)) == 0;
-      if (PK > 1) {
-        mul_item += PK;
-      } else if (++mul_ks == ks_n) {
-        mul_ks = 0;
-        ++mul_item;
-      }
-      if (skip) return;
+      if (dm_skip[sl]) return;
       if constexpr (SP) {
         // the row tile's 8 channels of this lane, split; the weights' parts
         // were split once, before the launch
@@ -976,7 +961,7 @@ __device__ __forceinline__ void conv_rows_block(
     // can start before step t's multiplications)
     auto step = [&](int u) {
       dma_b((u + 1) % D, (u + 1) % 2);
-      multiply(u % 2);
+      multiply(u % D, u % 2);
       stage((u + 1) % D, (u + 1) % 2);
       wait_loads();
       issue(u % D);  // loads of step t + D
