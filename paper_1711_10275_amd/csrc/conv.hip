@@ -670,9 +670,9 @@ struct RowsLds {
 template <typename T, int WB, int NB, int D, int PK, bool TB = false, bool SP = false>
 __device__ __forceinline__ void conv_rows_block(
     const T* __restrict__ X, uint32_t x_bytes, const void* __restrict__ B, uint32_t b_bytes,
-    const int32_t* __restrict__ perm, const int32_t* __restrict__ b_first, const uint32_t* __restrict__ items,
-    int64_t blk, int K, int mirror, int kdim, int ncols, const Heads<T>& Y, char* smem, int tid, int wave,
-    int lane, int m, int g, int col0) {
+    const int32_t* __restrict__ perm, const uint32_t* __restrict__ items, int64_t blk, int first, int n_items,
+    int K, int mirror, int kdim, int ncols, const Heads<T>& Y, char* smem, int tid, int wave, int lane, int m, int g,
+    int col0) {
   static_assert(!SP || (sizeof(T) == 4 && WB == 128 && PK == 1 && !TB), "split path: fp32, whole windows");
   constexpr int LPR = WB / 16;              // lanes per row window
   constexpr int RPI = 64 / LPR;             // rows per wavefront load
@@ -694,8 +694,6 @@ __device__ __forceinline__ void conv_rows_block(
   constexpr int S = WB / (32 * (int)sizeof(T));  // 32-channel MFMA groups per step
   char* const As = smem + wave * 16 * PITCH;     // this wavefront's row tile
   auto Bs = [&](int buf) { return smem + L::A_BYTES + buf * L::B_BYTES; };
-  const int first = b_first[blk];
-  const int n_items = b_first[blk + 1] - first;
   const uint32_t row_bytes = (uint32_t)kdim * sizeof(T);
   // PK > 1: rows of WB / PK bytes, PK items per step side by side in the
   // window (their products simply add up over the window's channels)
@@ -1052,7 +1050,7 @@ __device__ __forceinline__ void conv_rows_block(
 template <typename T, int WB, int NB, int D, int PK, bool TB, bool SP>
 __device__ __forceinline__ void conv_rows_run(
     const T* __restrict__ X, uint32_t x_bytes, const void* __restrict__ B, uint32_t b_bytes,
-    const int32_t* __restrict__ perm, const int32_t* __restrict__ b_first, const int32_t* __restrict__ b_order,
+    const int32_t* __restrict__ perm, const int32_t* __restrict__ b_first, const int4* __restrict__ b_rec,
     const uint32_t* __restrict__ items, int64_t n_blocks, int K, int mirror, int kdim, int ncols, const Heads<T>& Y) {
   constexpr int RPI = 64 / (WB / 16);       // rows per wavefront load
   constexpr int COLS = 16 * NB;             // output columns per workgroup
@@ -1071,10 +1069,7 @@ __device__ __forceinline__ void conv_rows_run(
     // priority), so that the ones that finish last are the ones that started
     // with the most work.
     int mine = 0;
-    for (int64_t idx = wg, round = 0; idx < n_blocks; idx = next(++round)) {
-      const int b = b_order[idx];
-      mine += b_first[b + 1] - b_first[b];
-    }
+    for (int64_t idx = wg, round = 0; idx < n_blocks; idx = next(++round)) mine += b_rec[idx].z;
     const float share = (float)mine * (float)G / (float)max(b_first[n_blocks], 1);
     if (share > 1.1f) __builtin_amdgcn_s_setprio(3);
     else if (share > 1.0f) __builtin_amdgcn_s_setprio(2);
@@ -1085,15 +1080,16 @@ __device__ __forceinline__ void conv_rows_run(
     for (int64_t i = ((int64_t)blockIdx.y * gridDim.x + wg) * 256 + tid; i < Y.n_zero; i += stride) Y.zero[i] = 0.f;
   }
   for (int64_t idx = wg, round = 0; idx < n_blocks; idx = next(++round)) {
+    const int4 rec = b_rec[idx];  // (block, first item, items): one load, no chain
     __syncthreads();  // the previous block's LDS is free
-    conv_rows_block<T, WB, NB, D, PK, TB, SP>(X, x_bytes, B, b_bytes, perm, b_first, items, b_order[idx], K, mirror,
+    conv_rows_block<T, WB, NB, D, PK, TB, SP>(X, x_bytes, B, b_bytes, perm, items, rec.x, rec.y, rec.z, K, mirror,
                                               kdim, ncols, Y, smem, tid, wave, lane, m, g, col0);
   }
 }
 
 #define SSCN_ROWS_ARGS                                                                                          \
   const T *__restrict__ X, uint32_t x_bytes, const void *__restrict__ B, uint32_t b_bytes,                     \
-      const int32_t *__restrict__ perm, const int32_t *__restrict__ b_first, const int32_t *__restrict__ b_order, \
+      const int32_t *__restrict__ perm, const int32_t *__restrict__ b_first, const int4 *__restrict__ b_rec,     \
       const uint32_t *__restrict__ items, int64_t n_blocks, int K, int mirror, int kdim, int ncols, Heads<T> Y
 
 // Forward (and DC) launches.  SP: fp32 through bf16 parts (B holds the
@@ -1108,7 +1104,7 @@ constexpr int rows_min_blocks() {
 
 template <typename T, int WB, int NB, int D, int PK, bool TB = false, bool SP = false>
 __global__ __launch_bounds__(256, (rows_min_blocks<WB, SP>())) void k_conv_rows(SSCN_ROWS_ARGS) {
-  conv_rows_run<T, WB, NB, D, PK, TB, SP>(X, x_bytes, B, b_bytes, perm, b_first, b_order, items, n_blocks, K, mirror,
+  conv_rows_run<T, WB, NB, D, PK, TB, SP>(X, x_bytes, B, b_bytes, perm, b_first, b_rec, items, n_blocks, K, mirror,
                                           kdim, ncols, Y);
 }
 
@@ -1116,7 +1112,7 @@ __global__ __launch_bounds__(256, (rows_min_blocks<WB, SP>())) void k_conv_rows(
 // name, so that kernel traces tell the two directions apart.
 template <typename T, int WB, int NB, int D, int PK, bool TB = false, bool SP = false>
 __global__ __launch_bounds__(256, (rows_min_blocks<WB, SP>())) void k_dgrad_rows(SSCN_ROWS_ARGS) {
-  conv_rows_run<T, WB, NB, D, PK, TB, SP>(X, x_bytes, B, b_bytes, perm, b_first, b_order, items, n_blocks, K, mirror,
+  conv_rows_run<T, WB, NB, D, PK, TB, SP>(X, x_bytes, B, b_bytes, perm, b_first, b_rec, items, n_blocks, K, mirror,
                                           kdim, ncols, Y);
 }
 #undef SSCN_ROWS_ARGS
@@ -1762,9 +1758,9 @@ static sscn_status launch_rows_nb(const T* X, const void* B, const View& v, int 
   hipEvent_t t0, t1;
   if (take_launch_timer(&t0, &t1))
     hipExtLaunchKernelGGL(kern, dim3((unsigned)gx, (unsigned)gy), dim3(256), 0, s, t0, t1, 0, X, xb, B, bb, v.st->perm,
-                          v.st->b_first, v.st->b_order, v.st->items, nb, v.K, v.mirror ? 1 : 0, kdim, ncols, Y);
+                          v.st->b_first, v.st->b_rec, v.st->items, nb, v.K, v.mirror ? 1 : 0, kdim, ncols, Y);
   else
-    kern<<<dim3((unsigned)gx, (unsigned)gy), 256, 0, s>>>(X, xb, B, bb, v.st->perm, v.st->b_first, v.st->b_order,
+    kern<<<dim3((unsigned)gx, (unsigned)gy), 256, 0, s>>>(X, xb, B, bb, v.st->perm, v.st->b_first, v.st->b_rec,
                                                            v.st->items, nb, v.K, v.mirror ? 1 : 0, kdim, ncols, Y);
   SSCN_HIP(hipGetLastError());
   return SSCN_OK;
@@ -2242,7 +2238,7 @@ __global__ __launch_bounds__(256) void k_wgrad_rows(const bf16_t* __restrict__ X
                                                     const bf16_t* __restrict__ dY, uint32_t y_bytes,
                                                     const int32_t* __restrict__ perm,
                                                     const int32_t* __restrict__ b_first,
-                                                    const int32_t* __restrict__ b_order,
+                                                    const int4* __restrict__ b_rec,
                                                     const uint32_t* __restrict__ items, int64_t n_blocks, int K,
                                                     int groups, float* __restrict__ part) {
   constexpr int NTI = CI / 16, NTJ = CO / 16, TPW = NTI * NTJ / 4;
@@ -2293,9 +2289,10 @@ __global__ __launch_bounds__(256) void k_wgrad_rows(const bf16_t* __restrict__ X
   const int64_t G = gridDim.x, wg = blockIdx.x;
   auto next = [&](int64_t round) { return round * G + ((round & 1) ? G - 1 - wg : wg); };
   for (int64_t idx = wg, round = 0; idx < n_blocks; idx = next(++round)) {
-    const int64_t b = b_order[idx];
-    const int64_t first = b_first[b];
-    const int n_items = (int)(b_first[b + 1] - first);
+    const int4 rec = b_rec[idx];  // (block, first item, items)
+    const int64_t b = rec.x;
+    const int64_t first = rec.y;
+    const int n_items = rec.z;
     // the items of this offset group: [j0, j1) (items are in increasing offset)
     const uint32_t oj = lane < n_items ? items[(first + lane) * kPlanRows] >> kPlanRowBits : 0xffu;
     const uint64_t below = __ballot(lane < n_items && (int)oj < o_lo);
@@ -2435,9 +2432,9 @@ static sscn_status launch_wgrad_rows_t(const bf16_t* X, const bf16_t* dY, const 
   hipEvent_t t0, t1;
   if (take_launch_timer(&t0, &t1))
     hipExtLaunchKernelGGL(kern, grid, dim3(256), 0, s, t0, t1, 0, X, xb, (uint32_t)cin * 2u, dY, yb, v.st->perm,
-                          v.st->b_first, v.st->b_order, v.st->items, nb, v.K, groups, part);
+                          v.st->b_first, v.st->b_rec, v.st->items, nb, v.K, groups, part);
   else
-    kern<<<grid, 256, 0, s>>>(X, xb, (uint32_t)cin * 2u, dY, yb, v.st->perm, v.st->b_first, v.st->b_order,
+    kern<<<grid, 256, 0, s>>>(X, xb, (uint32_t)cin * 2u, dY, yb, v.st->perm, v.st->b_first, v.st->b_rec,
                               v.st->items, nb, v.K, groups, part);
   hipError_t e = hipGetLastError();
   if (e == hipSuccess) {

@@ -118,7 +118,7 @@ struct Storage {
   int64_t n_blocks = 0;
   int32_t* perm = nullptr;       // kPlanRows * n_blocks: output row at each position, -1 past the end
   int32_t* b_first = nullptr;    // n_blocks + 1: first item of each block
-  int32_t* b_order = nullptr;    // n_blocks: blocks by decreasing item count
+  int4* b_rec = nullptr;         // n_blocks: blocks by decreasing item count, as (block, first item, items, 0)
   uint32_t* items = nullptr;     // kPlanRows per item: input row | offset (as stored) << kPlanRowBits
 };
 

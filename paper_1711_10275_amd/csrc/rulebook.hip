@@ -1487,8 +1487,9 @@ __global__ void k_plan_pairs(const int64_t* __restrict__ seg, int64_t n_tiles, c
 // passes.  k_order_hist counts the blocks per count (LDS counters, one
 // global atomic per count per workgroup); k_order_place ranks each
 // workgroup's blocks per count in LDS, reserves one range per count with one
-// global atomic, and writes them (the order inside one count is arbitrary).
-// kOrderPerWg blocks per workgroup.
+// global atomic, and writes their (block, first item, items, 0) records
+// (the order inside one count is arbitrary).  kOrderPerWg blocks per
+// workgroup.
 constexpr int kOrderPerWg = 4096;
 __global__ __launch_bounds__(256) void k_order_hist(const int32_t* __restrict__ b_first, int64_t nb, int K,
                                                     int32_t* __restrict__ ohist) {
@@ -1507,7 +1508,7 @@ __global__ __launch_bounds__(256) void k_order_hist(const int32_t* __restrict__ 
 
 __global__ __launch_bounds__(256) void k_order_place(const int32_t* __restrict__ b_first, int64_t nb, int K,
                                                      const int32_t* __restrict__ ohist, int32_t* __restrict__ ocur,
-                                                     int32_t* __restrict__ order) {
+                                                     int4* __restrict__ order) {
   __shared__ int32_t cnt[64], base[64];
   if (threadIdx.x < 64) cnt[threadIdx.x] = 0;
   __syncthreads();
@@ -1532,7 +1533,7 @@ __global__ __launch_bounds__(256) void k_order_place(const int32_t* __restrict__
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
     const int64_t b = b0 + threadIdx.x + 256 * i;
-    if (b < nb) order[base[key[i]] + rank[i]] = (int32_t)b;
+    if (b < nb) order[base[key[i]] + rank[i]] = make_int4((int32_t)b, b_first[b], K - (int)key[i], 0);
   }
 }
 
@@ -1589,13 +1590,14 @@ static sscn_status scan_i32(int32_t* p, int64_t count, hipStream_t s) {
 // Blocks by decreasing item count, with the scan of the item counts before
 // it, in one workgroup (nb <= kScanOrderMax): cnt[b] (items of block b)
 // becomes b_first (exclusive scan, b_first[nb] = total) and order lists the
-// blocks by decreasing count (a counting sort over the K + 1 possible
-// counts; the order inside one count is arbitrary).  The counts stay in
+// blocks by decreasing count as (block, first item, items, 0) records (a
+// counting sort over the K + 1 possible counts; the order inside one count
+// is arbitrary).  The counts stay in
 // LDS for the second pass.  Beyond kScanOrderMax blocks the scan and the
 // two passes of k_order_hist / k_order_place run wider.
 constexpr int64_t kScanOrderMax = 8192;
 __global__ __launch_bounds__(kOneBlock) void k_plan_scan_order(int32_t* __restrict__ cnt, int64_t nb, int K,
-                                                               int32_t* __restrict__ order) {
+                                                               int4* __restrict__ order) {
   constexpr int NW = kOneBlock / 64;
   __shared__ uint8_t c8[kScanOrderMax];
   __shared__ int32_t hist[64], cur[64], wsum[NW];
@@ -1635,7 +1637,7 @@ __global__ __launch_bounds__(kOneBlock) void k_plan_scan_order(int32_t* __restri
     const int64_t b = b0 + t;
     const bool ok = b < nb;
     const int p = wave_count<6>(cur, ok ? (uint32_t)(K - c8[b]) : 0u, ok);
-    if (ok) order[p] = (int32_t)b;
+    if (ok) order[p] = make_int4((int32_t)b, cnt[b], (int32_t)c8[b], 0);
   }
 }
 
@@ -1657,7 +1659,7 @@ static sscn_status build_plan(RulebookData* d, Storage& st, int64_t n_rows, int 
   Arena a;
   a.add(&st.perm, (size_t)nb * kPlanRows);
   a.add(&st.b_first, (size_t)nb + 1);
-  a.add(&st.b_order, (size_t)nb);
+  a.add(&st.b_rec, (size_t)nb);
   a.add(&st.items, (size_t)cap * kPlanRows);
   SSCN_TRY(owned_alloc(d, a, s));
   if (nb == 0) return fill_i32(st.b_first, 0, 1, s);
@@ -1700,14 +1702,14 @@ static sscn_status build_plan(RulebookData* d, Storage& st, int64_t n_rows, int 
   k_plan_blocks<<<grid_for(nb * 64, 256), 256, 0, s>>>(mask, st.perm, n_rows, nb, bmask, st.b_first);
   SSCN_HIP(hipGetLastError());
   if (nb <= kScanOrderMax) {
-    k_plan_scan_order<<<1, kOneBlock, 0, s>>>(st.b_first, nb, K, st.b_order);
+    k_plan_scan_order<<<1, kOneBlock, 0, s>>>(st.b_first, nb, K, st.b_rec);
   } else {
     SSCN_TRY(scan_i32(st.b_first, nb, s));
     int32_t* ohist = hist + bins + 1;
     const unsigned owgs = (unsigned)ceil_div(nb, kOrderPerWg);
     k_order_hist<<<owgs, 256, 0, s>>>(st.b_first, nb, K, ohist);
     SSCN_HIP(hipGetLastError());
-    k_order_place<<<owgs, 256, 0, s>>>(st.b_first, nb, K, ohist, ohist + 64, st.b_order);
+    k_order_place<<<owgs, 256, 0, s>>>(st.b_first, nb, K, ohist, ohist + 64, st.b_rec);
   }
   SSCN_HIP(hipGetLastError());
   k_plan_items<<<grid_for(nb * kPlanRows, 256), 256, 0, s>>>(bmask, st.b_first, nb, st.items);
