@@ -1725,13 +1725,14 @@ static sscn_status launch_conv(const T* X, const T* W, const View& v, int cin, i
 }
 
 
-// Row-block kernel: B laid out [o][ncols][kdim]; K <= 32 (offset sets as
-// 32-bit masks), whole 8-channel runs, 32-bit buffer offsets.
+// Row-block kernel: B laid out [o][ncols][kdim]; K <= kPlanMaxK (offset
+// sets of up to three 32-bit words), whole 8-channel runs, 32-bit buffer
+// offsets.
 template <typename T>
 static bool rows_eligible(const View& v, int kdim, int ncols) {
   const uint64_t x_bytes = (uint64_t)std::max<int64_t>(v.n_in, 1) * kdim * sizeof(T);
   const uint64_t b_bytes = (uint64_t)v.K * ncols * kdim * sizeof(T);
-  return v.K <= 32 && kdim % 8 == 0 && x_bytes < kOobOffset && b_bytes < kOobOffset &&
+  return v.K <= kPlanMaxK && kdim % 8 == 0 && x_bytes < kOobOffset && b_bytes < kOobOffset &&
          std::max(v.n_in, v.n_out) < (int64_t)kPlanNoRow && ceil_div(v.n_out, kPlanRows) * v.K < INT32_MAX;
 }
 

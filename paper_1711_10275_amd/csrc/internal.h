@@ -29,8 +29,11 @@ constexpr int kPlanRows = 64;
 // Bits of the key that orders rows by their offset set.
 constexpr int kPlanKeyBits = 15;
 // A plan entry packs an input row (kPlanNoRow: none) below the item's offset.
-constexpr int kPlanRowBits = 27;
+constexpr int kPlanRowBits = 25;  // plan entries: input row | offset << kPlanRowBits (offsets < 128)
 constexpr uint32_t kPlanNoRow = (1u << kPlanRowBits) - 1;
+constexpr int kPlanMaxK = 96;      // offsets of a rule book that gets a row-block plan
+constexpr int kPlanMaskWords = 3;  // words of an offset set of at most kPlanMaxK offsets
+__host__ __device__ constexpr int plan_words(int K) { return (K + 31) / 32; }
 // Tiles are grouped into this many contiguous ranges, one per XCD of the
 // chip (each XCD has its own L2); see the tile order of a rule book.
 constexpr int kTileGroups = 8;
@@ -110,11 +113,11 @@ struct Storage {
   int32_t* c_in = nullptr;       // 16 per chunk: input row, -1 for padding
   uint8_t* c_out = nullptr;      // 16 per chunk: output row - tile start, kChunkRows for padding
   int32_t* c_off = nullptr;      // per chunk: offset (as stored)
-  // Row-block plan (K <= 32): the output rows ordered by the set of offsets
+  // Row-block plan (K <= kPlanMaxK): the output rows ordered by the set of offsets
   // that reach them (rows with similar sets side by side) and cut into
   // blocks of kPlanRows; per block, one item per offset that reaches any of
   // its rows, holding each row's input row for that offset (-1 if none).
-  uint32_t* row_mask = nullptr;  // n_rows when the build provides it: offsets reaching each output row
+  uint32_t* row_mask = nullptr;  // n_rows x plan_words(K) when the build provides it: offsets reaching each output row
   int64_t n_blocks = 0;
   int32_t* perm = nullptr;       // kPlanRows * n_blocks: output row at each position, -1 past the end
   int32_t* b_first = nullptr;    // n_blocks + 1: first item of each block
@@ -188,7 +191,7 @@ struct View {
 // Builds the padded chunk table of the view's storage if it is not there
 // yet and makes `s` wait for it.
 sscn_status ensure_chunks(const View& v, hipStream_t s);
-// The same for the row-block plan (K <= 32).
+// The same for the row-block plan (K <= kPlanMaxK).
 sscn_status ensure_plan(const View& v, hipStream_t s);
 // The same for the tile order of the view's storage.
 sscn_status ensure_order(const View& v, hipStream_t s);

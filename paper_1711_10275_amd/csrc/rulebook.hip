@@ -414,7 +414,8 @@ __global__ __launch_bounds__(256) void k_count_nbr(const int32_t* __restrict__ n
 
 // Write every present entry at its segment start + its rank among the
 // wavefront's present entries (so segments are sorted by output row).  With
-// row_mask (K <= 32), also the set of offsets present for each row.  One
+// row_mask (K <= kPlanMaxK), also the set of offsets present for each row
+// (plan_words(K) words per row, offset o as bit o % 32 of word o / 32).  One
 // workgroup per tile: wavefront w takes the offsets o = w mod 4 (four times
 // the wavefronts of one per tile, to keep more reads in flight), and the
 // row masks of the four are combined in LDS.
@@ -423,7 +424,7 @@ __global__ __launch_bounds__(256) void k_compact(const int32_t* __restrict__ nbr
                                                  int32_t* __restrict__ in_rows,
                                                  int32_t* __restrict__ out_rows,
                                                  uint32_t* __restrict__ row_mask) {
-  __shared__ uint32_t part[4][64];
+  __shared__ uint32_t part[kPlanMaskWords][4][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t t = blockIdx.x;  // one workgroup per tile
   const int64_t k = t * kTile + lane;
@@ -437,7 +438,7 @@ __global__ __launch_bounds__(256) void k_compact(const int32_t* __restrict__ nbr
     if (lane < K) s_lo = seg[(int64_t)lane * n_tiles + t];
     if (lane + 64 < K) s_hi = seg[(int64_t)(lane + 64) * n_tiles + t];
   }
-  uint32_t present = 0;
+  uint32_t present[kPlanMaskWords] = {0u, 0u, 0u};
   // the rows of up to 8 of the wavefront's offsets are requested together
   // (one round trip per 8)
   constexpr int B = 8;
@@ -466,13 +467,20 @@ __global__ __launch_bounds__(256) void k_compact(const int32_t* __restrict__ nbr
       const int64_t pos = start + __popcll(m & below);
       in_rows[pos] = row;
       out_rows[pos] = (int32_t)k;
-      present |= 1u << (o & 31);
+      const uint32_t bit = 1u << (o & 31);
+      present[0] |= o < 32 ? bit : 0u;
+      present[1] |= o >= 32 && o < 64 ? bit : 0u;
+      present[2] |= o >= 64 ? bit : 0u;
     }
   }
   if (!row_mask) return;  // uniform
-  part[wave][lane] = present;
+  const int W = plan_words(K);
+#pragma unroll
+  for (int i = 0; i < kPlanMaskWords; ++i) part[i][wave][lane] = present[i];
   __syncthreads();
-  if (wave == 0 && valid) row_mask[k] = part[0][lane] | part[1][lane] | part[2][lane] | part[3][lane];
+  if (wave == 0 && valid)
+    for (int i = 0; i < W; ++i)
+      row_mask[k * W + i] = part[i][0][lane] | part[i][1][lane] | part[i][2][lane] | part[i][3][lane];
 }
 
 // ------------------------------------------------------------- tile order
@@ -1147,7 +1155,7 @@ static sscn_status compact_storage(const int32_t* nbr, int64_t n_rows, int K, St
   }
   if (st.n_tiles > 0) {
     k_compact<<<(unsigned)st.n_tiles, 256, 0, s>>>(nbr, n_rows, K, st.seg, st.n_tiles, st.in_rows,
-                                                             st.out_rows, K <= 32 ? row_mask : nullptr);
+                                                             st.out_rows, K <= kPlanMaxK ? row_mask : nullptr);
     SSCN_HIP(hipGetLastError());
   }
   return SSCN_OK;
@@ -1262,22 +1270,50 @@ sscn_status ensure_order(const View& v, hipStream_t s) {
 }
 
 // ------------------------------------------------------ row-block plan
-// Offset set of every output row as a bit mask.  One thread per pair of
-// offset blockIdx.y (pairs of one offset have distinct output rows).
+// Offset set of every output row as a bit mask of W words (offset o is bit
+// o % 32 of word o / 32).  One thread per pair of offset blockIdx.y (pairs
+// of one offset have distinct output rows).
 __global__ void k_plan_mask(const int64_t* __restrict__ seg, int64_t n_tiles,
-                            const int32_t* __restrict__ out_rows, uint32_t* __restrict__ mask) {
+                            const int32_t* __restrict__ out_rows, int W, uint32_t* __restrict__ mask) {
   const int o = blockIdx.y;
   const int64_t p = seg[(int64_t)o * n_tiles] + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (p >= seg[(int64_t)(o + 1) * n_tiles]) return;
-  atomicOr(&mask[out_rows[p]], 1u << o);
+  atomicOr(&mask[(int64_t)out_rows[p] * W + (o >> 5)], 1u << (o & 31));
 }
+
+// A row's offset set (W <= kPlanMaskWords words; the rest zero).
+struct RowSet {
+  uint32_t w[kPlanMaskWords];
+};
+__device__ __forceinline__ RowSet load_set(const uint32_t* __restrict__ mask, int64_t r, int W, bool ok) {
+  RowSet m;
+#pragma unroll
+  for (int i = 0; i < kPlanMaskWords; ++i) m.w[i] = ok && i < W ? mask[r * W + i] : 0u;
+  return m;
+}
+// The sort key's offsets for more than 32 offsets (chosen on the host).
+struct KeySel {
+  uint8_t o[kPlanKeyBits];
+};
 
 // Sort key of an offset set: the set itself when it has at most
 // kPlanKeyBits offsets; for 3^3 filters the 12 edge neighbours and 3 of the
 // 6 face neighbours (o = 9 i0 + 3 i1 + i2; the centre is in nearly every
 // set and the corners vary least between neighbouring surface sites);
-// otherwise the highest kPlanKeyBits offsets.
-__device__ __forceinline__ uint32_t plan_key(uint32_t m, int K) {
+// up to 32 offsets otherwise, the highest kPlanKeyBits; beyond 32 the
+// offsets of sel (the host takes those displaced along exactly two axes).
+__device__ __forceinline__ uint32_t plan_key(const RowSet& s, int K, const KeySel& sel) {
+  if (K > 32) {
+    uint32_t k = 0;
+#pragma unroll
+    for (int i = 0; i < kPlanKeyBits; ++i) {
+      const int o = sel.o[i];
+      const uint32_t w = o < 32 ? s.w[0] : (o < 64 ? s.w[1] : s.w[2]);
+      k = (k << 1) | ((w >> (o & 31)) & 1u);
+    }
+    return k;
+  }
+  const uint32_t m = s.w[0];
   if (K <= kPlanKeyBits) return m;
   if (K == 27) {
     constexpr int sel[kPlanKeyBits] = {1, 3, 5, 7, 9, 11, 15, 17, 19, 21, 23, 25, 10, 12, 14};
@@ -1366,22 +1402,22 @@ __device__ __forceinline__ int count_in_lds(const SortLds& l, uint32_t key, bool
 }
 
 template <int RPT>
-__global__ __launch_bounds__(256) void k_plan_hist(const uint32_t* __restrict__ mask, int64_t n, int K, int bins,
-                                                   int32_t* __restrict__ hist) {
+__global__ __launch_bounds__(256) void k_plan_hist(const uint32_t* __restrict__ mask, int64_t n, int K, int W,
+                                                   KeySel sel, int bins, int32_t* __restrict__ hist) {
   static_assert(256 * RPT <= kSortMaxRows, "key list");
   extern __shared__ __attribute__((aligned(16))) char lds[];
   const SortLds l = sort_lds(lds, bins);
   const int64_t r0 = (int64_t)blockIdx.x * (256 * RPT) + threadIdx.x;
-  uint32_t m[RPT];
+  uint32_t key[RPT];
 #pragma unroll
   for (int i = 0; i < RPT; ++i) {
     const int64_t r = r0 + 256 * i;
-    m[i] = r < n ? mask[r] : 0u;
+    key[i] = plan_key(load_set(mask, r, W, r < n), K, sel);
   }
 #pragma unroll
   for (int i = 0; i < RPT; ++i) {
     const bool ok = r0 + 256 * i < n;
-    (void)count_in_lds(l, ok ? plan_key(m[i], K) : 0u, ok);
+    (void)count_in_lds(l, ok ? key[i] : 0u, ok);
   }
   __syncthreads();
   for (int j = threadIdx.x; j < *l.n_keys; j += 256) {
@@ -1395,9 +1431,9 @@ __global__ __launch_bounds__(256) void k_plan_hist(const uint32_t* __restrict__ 
 // rows per key in LDS, reserves one range per key it holds, then places
 // its rows.
 template <int RPT>
-__global__ __launch_bounds__(256) void k_plan_sort(const uint32_t* __restrict__ mask, int64_t n, int K, int bins,
-                                                   int32_t* __restrict__ cursor, int32_t* __restrict__ perm,
-                                                   int32_t* __restrict__ pos_of) {
+__global__ __launch_bounds__(256) void k_plan_sort(const uint32_t* __restrict__ mask, int64_t n, int K, int W,
+                                                   KeySel sel, int bins, int32_t* __restrict__ cursor,
+                                                   int32_t* __restrict__ perm, int32_t* __restrict__ pos_of) {
   static_assert(256 * RPT <= kSortMaxRows, "key list");
   extern __shared__ __attribute__((aligned(16))) char lds[];
   const SortLds l = sort_lds(lds, bins);
@@ -1407,7 +1443,7 @@ __global__ __launch_bounds__(256) void k_plan_sort(const uint32_t* __restrict__ 
 #pragma unroll
   for (int i = 0; i < RPT; ++i) {
     const int64_t r = r0 + 256 * i;
-    key[i] = r < n ? plan_key(mask[r], K) : 0u;
+    key[i] = r < n ? plan_key(load_set(mask, r, W, true), K, sel) : 0u;
   }
 #pragma unroll
   for (int i = 0; i < RPT; ++i) rank[i] = count_in_lds(l, key[i], r0 + 256 * i < n);
@@ -1431,54 +1467,64 @@ __global__ __launch_bounds__(256) void k_plan_sort(const uint32_t* __restrict__ 
 // One wavefront per block: union of the offset sets of its rows and its item
 // count; the positions past the last row are marked empty.
 static_assert(kPlanRows == 64, "one wavefront per plan block");
-__global__ void k_plan_blocks(const uint32_t* __restrict__ mask, int32_t* __restrict__ perm, int64_t n,
+__global__ void k_plan_blocks(const uint32_t* __restrict__ mask, int W, int32_t* __restrict__ perm, int64_t n,
                               int64_t n_blocks, uint32_t* __restrict__ bmask, int32_t* __restrict__ cnt) {
   const int64_t b = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int lane = threadIdx.x & 63;
   if (b >= n_blocks) return;
   const int64_t p = b * kPlanRows + lane;
-  uint32_t u = 0;
-  if (p < n)
-    u = mask[perm[p]];
-  else
+  RowSet u;
+  if (p < n) {
+    u = load_set(mask, perm[p], W, true);
+  } else {
+    u = load_set(mask, 0, W, false);
     perm[p] = -1;
-#pragma unroll
-  for (int d = 32; d >= 1; d >>= 1) u |= (uint32_t)__shfl_xor((int)u, d, 64);
-  if (lane == 0) {
-    bmask[b] = u;
-    cnt[b] = __popc(u);
   }
+  int c = 0;
+#pragma unroll
+  for (int i = 0; i < kPlanMaskWords; ++i) {
+    if (i >= W) break;  // uniform
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) u.w[i] |= (uint32_t)__shfl_xor((int)u.w[i], d, 64);
+    if (lane == 0) bmask[b * W + i] = u.w[i];
+    c += __popc(u.w[i]);
+  }
+  if (lane == 0) cnt[b] = c;
 }
 
 // Thread (block, slot): marks its slot of every item of the block empty
 // (items in ascending offset order).
-__global__ void k_plan_items(const uint32_t* __restrict__ bmask, const int32_t* __restrict__ b_first,
+__global__ void k_plan_items(const uint32_t* __restrict__ bmask, int W, const int32_t* __restrict__ b_first,
                              int64_t n_blocks, uint32_t* __restrict__ items) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t b = t / kPlanRows;
   const int m = (int)(t % kPlanRows);
   if (b >= n_blocks) return;
-  uint32_t u = bmask[b];
   int64_t item = b_first[b];
-  while (u) {
-    const uint32_t o = (uint32_t)(__ffs(u) - 1);
-    u &= u - 1;
-    items[item * kPlanRows + m] = kPlanNoRow | (o << kPlanRowBits);
-    ++item;
+  for (int i = 0; i < W; ++i) {
+    uint32_t u = bmask[b * W + i];
+    while (u) {
+      const uint32_t o = 32u * (uint32_t)i + (uint32_t)(__ffs(u) - 1);
+      u &= u - 1;
+      items[item * kPlanRows + m] = kPlanNoRow | (o << kPlanRowBits);
+      ++item;
+    }
   }
 }
 
 // Every pair into its block's item for its offset, at its row's slot.
 __global__ void k_plan_pairs(const int64_t* __restrict__ seg, int64_t n_tiles, const int32_t* __restrict__ in_rows,
                              const int32_t* __restrict__ out_rows, const int32_t* __restrict__ pos_of,
-                             const uint32_t* __restrict__ bmask, const int32_t* __restrict__ b_first,
+                             const uint32_t* __restrict__ bmask, int W, const int32_t* __restrict__ b_first,
                              uint32_t* __restrict__ items) {
   const int o = blockIdx.y;
   const int64_t p = seg[(int64_t)o * n_tiles] + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (p >= seg[(int64_t)(o + 1) * n_tiles]) return;
   const int32_t pos = pos_of[out_rows[p]];
   const int64_t b = pos / kPlanRows;
-  const int64_t item = b_first[b] + __popc(bmask[b] & ((1u << o) - 1u));
+  // items before offset o's: the block's offsets below o
+  int64_t item = b_first[b] + __popc(bmask[b * W + (o >> 5)] & ((1u << (o & 31)) - 1u));
+  for (int i = 0; i < (o >> 5); ++i) item += __popc(bmask[b * W + i]);
   items[item * kPlanRows + pos % kPlanRows] = (uint32_t)in_rows[p] | ((uint32_t)o << kPlanRowBits);
 }
 
@@ -1489,18 +1535,20 @@ __global__ void k_plan_pairs(const int64_t* __restrict__ seg, int64_t n_tiles, c
 // workgroup's blocks per count in LDS, reserves one range per count with one
 // global atomic, and writes their (block, first item, items, 0) records
 // (the order inside one count is arbitrary).  kOrderPerWg blocks per
-// workgroup.
+// workgroup; kOrderBins counters (item counts 0 .. K <= kPlanMaxK).
 constexpr int kOrderPerWg = 4096;
+constexpr int kOrderBins = 128;
+static_assert(kPlanMaxK < kOrderBins, "one bin per item count");
 __global__ __launch_bounds__(256) void k_order_hist(const int32_t* __restrict__ b_first, int64_t nb, int K,
                                                     int32_t* __restrict__ ohist) {
-  __shared__ int32_t cnt[64];
-  if (threadIdx.x < 64) cnt[threadIdx.x] = 0;
+  __shared__ int32_t cnt[kOrderBins];
+  if (threadIdx.x < kOrderBins) cnt[threadIdx.x] = 0;
   __syncthreads();
   const int64_t b0 = (int64_t)blockIdx.x * kOrderPerWg;
   for (int i = threadIdx.x; i < kOrderPerWg; i += 256) {
     const int64_t b = b0 + i;
     const bool ok = b < nb;
-    (void)wave_count<6>(cnt, ok ? (uint32_t)(K - (b_first[b + 1] - b_first[b])) : 0u, ok);
+    (void)wave_count<7>(cnt, ok ? (uint32_t)(K - (b_first[b + 1] - b_first[b])) : 0u, ok);
   }
   __syncthreads();
   if (threadIdx.x <= K && cnt[threadIdx.x] > 0) atomicAdd(&ohist[threadIdx.x], cnt[threadIdx.x]);
@@ -1509,8 +1557,8 @@ __global__ __launch_bounds__(256) void k_order_hist(const int32_t* __restrict__ 
 __global__ __launch_bounds__(256) void k_order_place(const int32_t* __restrict__ b_first, int64_t nb, int K,
                                                      const int32_t* __restrict__ ohist, int32_t* __restrict__ ocur,
                                                      int4* __restrict__ order) {
-  __shared__ int32_t cnt[64], base[64];
-  if (threadIdx.x < 64) cnt[threadIdx.x] = 0;
+  __shared__ int32_t cnt[kOrderBins], base[kOrderBins];
+  if (threadIdx.x < kOrderBins) cnt[threadIdx.x] = 0;
   __syncthreads();
   const int64_t b0 = (int64_t)blockIdx.x * kOrderPerWg;
   constexpr int PER = kOrderPerWg / 256;
@@ -1521,7 +1569,7 @@ __global__ __launch_bounds__(256) void k_order_place(const int32_t* __restrict__
     const int64_t b = b0 + threadIdx.x + 256 * i;
     const bool ok = b < nb;
     key[i] = ok ? (uint32_t)(K - (b_first[b + 1] - b_first[b])) : 0u;
-    rank[i] = wave_count<6>(cnt, key[i], ok);
+    rank[i] = wave_count<7>(cnt, key[i], ok);
   }
   __syncthreads();
   if (threadIdx.x <= K) {
@@ -1600,9 +1648,9 @@ __global__ __launch_bounds__(kOneBlock) void k_plan_scan_order(int32_t* __restri
                                                                int4* __restrict__ order) {
   constexpr int NW = kOneBlock / 64;
   __shared__ uint8_t c8[kScanOrderMax];
-  __shared__ int32_t hist[64], cur[64], wsum[NW];
+  __shared__ int32_t hist[kOrderBins], cur[kOrderBins], wsum[NW];
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  if (t < 64) hist[t] = 0;
+  if (t < kOrderBins) hist[t] = 0;
   __syncthreads();
   int carry = 0;
   for (int64_t b0 = 0; b0 < nb; b0 += kOneBlock) {
@@ -1621,7 +1669,7 @@ __global__ __launch_bounds__(kOneBlock) void k_plan_scan_order(int32_t* __restri
     }
     if (ok) cnt[b] = before + inc - v;
     carry += total;
-    (void)wave_count<6>(hist, ok ? (uint32_t)(K - v) : 0u, ok);
+    (void)wave_count<7>(hist, ok ? (uint32_t)(K - v) : 0u, ok);
     __syncthreads();  // wsum is rewritten by the next chunk
   }
   if (t == 0) {
@@ -1636,7 +1684,7 @@ __global__ __launch_bounds__(kOneBlock) void k_plan_scan_order(int32_t* __restri
   for (int64_t b0 = 0; b0 < nb; b0 += kOneBlock) {
     const int64_t b = b0 + t;
     const bool ok = b < nb;
-    const int p = wave_count<6>(cur, ok ? (uint32_t)(K - c8[b]) : 0u, ok);
+    const int p = wave_count<7>(cur, ok ? (uint32_t)(K - c8[b]) : 0u, ok);
     if (ok) order[p] = make_int4((int32_t)b, cnt[b], (int32_t)c8[b], 0);
   }
 }
@@ -1647,8 +1695,23 @@ __global__ __launch_bounds__(kOneBlock) void k_plan_scan_order(int32_t* __restri
 // per offset, and room for nb K items.  hist0: plan_hist_words(K) zeroed
 // words for the key histogram, or NULL.
 // The key histogram (bins + 1 words), then the block-count histogram and
-// cursor of the block order (64 words each).
-static int64_t plan_hist_words(int K) { return (1 << std::min(K, kPlanKeyBits)) + 1 + 128; }
+// cursor of the block order (kOrderBins words each).
+static int64_t plan_hist_words(int K) { return (1 << std::min(K, kPlanKeyBits)) + 1 + 2 * kOrderBins; }
+
+// Sort-key offsets for more than 32 offsets: those displaced from the
+// filter's middle along exactly two axes, in increasing o, then the others
+// (the d-dimensional counterpart of the 3^3 filter's edge neighbours).
+static KeySel plan_key_sel(int K, int f, int dim) {
+  KeySel sel{};
+  int n = 0;
+  for (int pass = 0; pass < 2 && n < kPlanKeyBits; ++pass)
+    for (int o = 0; o < K && n < kPlanKeyBits; ++o) {
+      int nz = 0;
+      for (int q = 0, r = o; q < dim; ++q, r /= f) nz += (r % f) != (f - 1) / 2;
+      if ((nz == 2) == (pass == 0)) sel.o[n++] = (uint8_t)o;
+    }
+  return sel;
+}
 
 static sscn_status build_plan(RulebookData* d, Storage& st, int64_t n_rows, int K, hipStream_t s,
                               int64_t ppo_bound = -1, int32_t* hist0 = nullptr) {
@@ -1665,11 +1728,13 @@ static sscn_status build_plan(RulebookData* d, Storage& st, int64_t n_rows, int 
   if (nb == 0) return fill_i32(st.b_first, 0, 1, s);
   const int bins = 1 << std::min(K, kPlanKeyBits);
   Temps tmp(s);
+  const int W = plan_words(K);
+  const KeySel sel = plan_key_sel(K, d->f, d->dim);
   uint32_t* mask = st.row_mask; uint32_t* bmask; int32_t* hist = nullptr; int32_t* pos_of;
   Arena t;
   if (!(hist0 && mask)) t.add(&hist, (size_t)plan_hist_words(K));
-  if (!mask) t.add(&mask, (size_t)n_rows);  // right after hist: one fill clears both
-  t.add(&bmask, (size_t)nb);
+  if (!mask) t.add(&mask, (size_t)n_rows * W);  // right after hist: one fill clears both
+  t.add(&bmask, (size_t)nb * W);
   t.add(&pos_of, (size_t)n_rows);
   SSCN_TRY(tmp.alloc(t));
   int64_t max_ppo = ppo_bound;
@@ -1679,10 +1744,10 @@ static sscn_status build_plan(RulebookData* d, Storage& st, int64_t n_rows, int 
     if (hist0) hist = hist0;
     else SSCN_TRY(fill_i32(hist, 0, plan_hist_words(K), s));
   } else {
-    SSCN_TRY(fill_i32(hist, 0, (int32_t*)(mask + n_rows) - hist, s));
+    SSCN_TRY(fill_i32(hist, 0, (int32_t*)(mask + n_rows * W) - hist, s));
     if (max_ppo > 0) {
       k_plan_mask<<<dim3((unsigned)ceil_div(max_ppo, 256), (unsigned)K), 256, 0, s>>>(st.seg, st.n_tiles,
-                                                                                      st.out_rows, mask);
+                                                                                      st.out_rows, W, mask);
       SSCN_HIP(hipGetLastError());
     }
   }
@@ -1694,12 +1759,12 @@ static sscn_status build_plan(RulebookData* d, Storage& st, int64_t n_rows, int 
               : rpt == 8 ? k_plan_hist<8> : k_plan_hist<16>;
   auto sort_k = rpt == 1 ? k_plan_sort<1> : rpt == 2 ? k_plan_sort<2> : rpt == 4 ? k_plan_sort<4>
               : rpt == 8 ? k_plan_sort<8> : k_plan_sort<16>;
-  hist_k<<<sort_wgs, 256, sort_lds, s>>>(mask, n_rows, K, bins, hist);
+  hist_k<<<sort_wgs, 256, sort_lds, s>>>(mask, n_rows, K, W, sel, bins, hist);
   SSCN_HIP(hipGetLastError());
   SSCN_TRY(scan_i32(hist, bins, s));
-  sort_k<<<sort_wgs, 256, sort_lds, s>>>(mask, n_rows, K, bins, hist, st.perm, pos_of);
+  sort_k<<<sort_wgs, 256, sort_lds, s>>>(mask, n_rows, K, W, sel, bins, hist, st.perm, pos_of);
   SSCN_HIP(hipGetLastError());
-  k_plan_blocks<<<grid_for(nb * 64, 256), 256, 0, s>>>(mask, st.perm, n_rows, nb, bmask, st.b_first);
+  k_plan_blocks<<<grid_for(nb * 64, 256), 256, 0, s>>>(mask, W, st.perm, n_rows, nb, bmask, st.b_first);
   SSCN_HIP(hipGetLastError());
   if (nb <= kScanOrderMax) {
     k_plan_scan_order<<<1, kOneBlock, 0, s>>>(st.b_first, nb, K, st.b_rec);
@@ -1709,14 +1774,14 @@ static sscn_status build_plan(RulebookData* d, Storage& st, int64_t n_rows, int 
     const unsigned owgs = (unsigned)ceil_div(nb, kOrderPerWg);
     k_order_hist<<<owgs, 256, 0, s>>>(st.b_first, nb, K, ohist);
     SSCN_HIP(hipGetLastError());
-    k_order_place<<<owgs, 256, 0, s>>>(st.b_first, nb, K, ohist, ohist + 64, st.b_rec);
+    k_order_place<<<owgs, 256, 0, s>>>(st.b_first, nb, K, ohist, ohist + kOrderBins, st.b_rec);
   }
   SSCN_HIP(hipGetLastError());
-  k_plan_items<<<grid_for(nb * kPlanRows, 256), 256, 0, s>>>(bmask, st.b_first, nb, st.items);
+  k_plan_items<<<grid_for(nb * kPlanRows, 256), 256, 0, s>>>(bmask, W, st.b_first, nb, st.items);
   SSCN_HIP(hipGetLastError());
   if (max_ppo > 0) {
     k_plan_pairs<<<dim3((unsigned)ceil_div(max_ppo, 256), (unsigned)K), 256, 0, s>>>(
-        st.seg, st.n_tiles, st.in_rows, st.out_rows, pos_of, bmask, st.b_first, st.items);
+        st.seg, st.n_tiles, st.in_rows, st.out_rows, pos_of, bmask, W, st.b_first, st.items);
     SSCN_HIP(hipGetLastError());
   }
   return SSCN_OK;
@@ -1724,8 +1789,8 @@ static sscn_status build_plan(RulebookData* d, Storage& st, int64_t n_rows, int 
 
 sscn_status ensure_plan(const View& v, hipStream_t s) {
   RulebookData* d = v.owner;
-  if (d->K > 32 || std::max(d->n_in, d->n_out) >= (int64_t)kPlanNoRow)
-    return fail(SSCN_ERR_INVALID_ARG, "row-block plan needs at most 32 offsets and fewer than 2^27 rows");
+  if (d->K > kPlanMaxK || std::max(d->n_in, d->n_out) >= (int64_t)kPlanNoRow)
+    return fail(SSCN_ERR_INVALID_ARG, "row-block plan needs at most 96 offsets and fewer than 2^25 - 1 rows");
   Storage& st = v.st == &d->fwd ? d->fwd : d->bwd;
   {
     std::lock_guard<std::mutex> lock(d->chunk_mu);
@@ -1807,10 +1872,10 @@ static sscn_status ssc_build(const int32_t* coords, int64_t n, const int32_t* sp
     const uint64_t cap = table_capacity(n);
     Slot* table = nullptr; uint32_t* table8 = nullptr;  // table8: grouped slots of kGroupWords words
     int32_t* nbr; int64_t* counts; unsigned long long* stats; int32_t* hist = nullptr;
-    // With K <= 32 the row-block plan is queued before the readback too: its
+    // With K <= kPlanMaxK the row-block plan is queued before the readback too: its
     // launches overlap the build's kernels and the host waits once.
     const bool one_phase = (uint64_t)K * (uint64_t)n * 8u <= (512ull << 20);
-    const bool eager_plan = one_phase && n > 0 && K <= 32 && n < (int64_t)kPlanNoRow;
+    const bool eager_plan = one_phase && n > 0 && K <= kPlanMaxK && n < (int64_t)kPlanNoRow;
     Arena ta;
     if (narrow) ta.add(&table8, cap * kGroupWords); else ta.add(&table, cap);
     ta.add(&nbr, (size_t)K * n);
@@ -1828,7 +1893,7 @@ static sscn_status ssc_build(const int32_t* coords, int64_t n, const int32_t* sp
       pa.add(&d->fwd.in_rows, cap_pairs);
       pa.add(&d->fwd.out_rows, cap_pairs);
       pa.add(&d->fwd.order, n_tiles);
-      if (K <= 32) pa.add(&d->fwd.row_mask, n);
+      if (K <= kPlanMaxK) pa.add(&d->fwd.row_mask, (size_t)n * plan_words(K));
     };
     Arena oa;  // owned by the rule book, needed before the readback
     oa.add(&d->fwd.seg, (size_t)K * n_tiles + 1);
@@ -2044,9 +2109,9 @@ extern "C" sscn_status sc_rulebook_build(const int32_t* coords, int64_t n, const
     oa.add(&d->bwd.out_rows, total);
     oa.add(&d->fwd.order, d->fwd.n_tiles);
     oa.add(&d->bwd.order, d->bwd.n_tiles);
-    if (K <= 32 && n > 0) {
-      oa.add(&d->fwd.row_mask, n_out);
-      oa.add(&d->bwd.row_mask, n);
+    if (K <= kPlanMaxK && n > 0) {
+      oa.add(&d->fwd.row_mask, (size_t)n_out * plan_words(K));
+      oa.add(&d->bwd.row_mask, (size_t)n * plan_words(K));
     }
     SSCN_TRY(owned_alloc(d, oa, s));
     if (n > 0) {
@@ -2420,8 +2485,9 @@ sscn_status build_nd(const int32_t* coords, int64_t n, const int32_t* size, int 
       pa.add(&d->fwd.in_rows, total);
       pa.add(&d->fwd.out_rows, total);
       pa.add(&d->fwd.order, d->fwd.n_tiles);
+      if (K <= kPlanMaxK && n > 0) pa.add(&d->fwd.row_mask, (size_t)n * plan_words(K));
       SSCN_TRY(owned_alloc(d, pa, s));
-      if (n > 0) SSCN_TRY(compact_storage(nbr, n, K, d->fwd, s, /*counted=*/true));
+      if (n > 0) SSCN_TRY(compact_storage(nbr, n, K, d->fwd, s, /*counted=*/true, d->fwd.row_mask));
     } else {
       // every input reaches at most prod_q ceil(f / s) outputs
       const int per = (f + stride - 1) / stride;

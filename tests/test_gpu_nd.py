@@ -1,7 +1,8 @@
 """Rule books and layers in d = 1, 2 and 4 dimensions on the GPU against the
 oracle: bit-exact rule books and output coordinates, then forward, dgrad
-and wgrad through the unchanged convolution kernels (K = f^d offsets: 9 for
-d = 2 takes the row-block kernel, 81 for d = 4 the chunk kernels)."""
+and wgrad through the unchanged convolution kernels (K = f^d offsets: the
+row-block kernel takes up to 96 of them, with offset sets of one to three
+32-bit words: 9, 25, 36 and 49 in d = 2, 16 and 81 in d = 4)."""
 import numpy as np
 import pytest
 import torch
@@ -27,8 +28,8 @@ def _set(seed, size, batch=2, density=0.3):
 
 
 CASES = [((40,), 3, 1, True), ((40,), 2, 2, False), ((33, 29), 3, 1, True), ((33, 33), 3, 2, False),
-         ((32, 30), 2, 2, False), ((30, 28), 5, 1, True), ((9, 8, 7, 9), 3, 1, True), ((8, 8, 6, 6), 2, 2, False),
-         ((9, 9, 9, 7), 3, 2, False)]
+         ((32, 30), 2, 2, False), ((30, 28), 5, 1, True), ((40, 38), 7, 1, True), ((34, 34), 6, 2, False),
+         ((9, 8, 7, 9), 3, 1, True), ((8, 8, 6, 6), 2, 2, False), ((9, 9, 9, 7), 3, 2, False)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -54,6 +55,25 @@ def test_nd_layer(size, f, s, sub, dtype):
         rdx, rdw = O.backward(X, W, G, oview)
         assert_close(host(dx), rdx, dtype, "dgrad")
         assert_close(host(dw), rdw, "f32", "wgrad")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_4d_shells_row_blocks(dtype):
+    """The 4-d SSC(3) layer of 16 time steps of moving shells (141k sites,
+    81 offsets, 2,203 plan blocks of about 70 items): forward and dgrad
+    over the row-block plan against the oracle."""
+    c = S.moving_shells_4d()
+    size = (16, 48, 48, 48)
+    rb = sscn.ssc_rulebook_build(dev(c), size, 3)
+    orb = O.ssc_rulebook(c, size, 3)
+    bf = dtype == "bf16"
+    X = S.features(c.shape[0], 32, 710, bf16=bf)
+    W = S.weights(81, 32, 32, 711, bf16=bf)
+    y = sscn.sparse_conv_forward(dev(X, TD[dtype]), dev(W, TD[dtype]), rb)
+    assert_close(host(y), O.forward(X, W, orb), dtype, "4-d forward")
+    G = S.features(c.shape[0], 32, 712, bf16=bf)
+    dx, _ = sscn.sparse_conv_backward(None, dev(W, TD[dtype]), dev(G, TD[dtype]), rb, wgrad=False)
+    assert_close(host(dx), O.backward(X, W, G, orb)[0], dtype, "4-d dgrad")
 
 
 def test_nd_errors():
