@@ -236,8 +236,8 @@ sscn_status sparse_conv_forward_ex(const void* features, const void* weights, ss
  *     a fixed 8 MiB region of the library's code object (one per device,
  *     held until the process ends): K * c_in * c_out elements of dtype must
  *     fit in 8 MiB, else SSCN_ERR_INVALID_ARG (nothing is queued);
- *   - the rule book's kernel tables must already exist: an SSC rule book
- *     with at most 32 offsets has them from its build, any other gets them
+ *   - the rule book's kernel tables must already exist: a 3-d SSC rule
+ *     book of filter size 1 or 3 has them from its build, any other gets them
  *     from one sparse_conv_forward / sparse_conv_backward on it (same
  *     direction); otherwise SSCN_ERR_INVALID_ARG, `out` untouched.
  * Every call on a device shares that device's region, which keeps the last
