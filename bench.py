@@ -193,6 +193,22 @@ def _wall_ms(fn, reps):
     return (time.perf_counter() - t0) * 1e3 / reps
 
 
+def _latency_ms(fn, reps):
+    """Mean host time of single calls, each started on an idle GPU."""
+    import torch
+    fn()
+    torch.cuda.synchronize()
+    total = 0.0
+    for _ in range(reps):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        r = fn()
+        total += time.perf_counter() - t0
+        del r
+    torch.cuda.synchronize()
+    return total * 1e3 / reps
+
+
 def table_capacity(n):
     cap = 64
     while cap < 2 * n:
@@ -200,7 +216,7 @@ def table_capacity(n):
     return cap
 
 
-def build_roofline(n, K, pairs, ms, what, slot=16):
+def build_roofline(n, K, pairs, ms, what, slot=16, pairs_ms=None):
     """Algorithmic bytes of an SSC rule-book build against HBM bandwidth.
 
     Counted: coordinates read (16 B per site), the dictionary filled (slot
@@ -214,14 +230,22 @@ def build_roofline(n, K, pairs, ms, what, slot=16):
     reported as `intermediate_bytes`.  The time is the mean host wall time
     of back-to-back build calls: each call waits for its own readback of
     sizes and flags, and the row-block plan it queues behind that readback
-    runs before the next call's kernels.
+    runs before the next call's kernels.  `pairs_ms` (if given) is the
+    latency of one call on an idle GPU, until the pair arrays, sizes and
+    flags are ready (the plan runs after the call returns): the time of the
+    rule book the counted bytes belong to, reported as `rulebook_ms` with
+    its own fraction `frac_rulebook`.
     """
     cap = table_capacity(n)
     lookups = K * n if n < (1 << 18) else (K - 1) // 2 * n
     nbytes = 16 * n + slot * cap + 8 * n + 8 * lookups + 8 * pairs
     achieved = nbytes / (ms * 1e-3) / 1e9
-    return {"stage": what, "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-            "frac": achieved / PEAK_HBM_GBS, "bytes": nbytes, "ms": ms, "intermediate_bytes": 8 * K * n}
+    out = {"stage": what, "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+           "frac": achieved / PEAK_HBM_GBS, "bytes": nbytes, "ms": ms, "intermediate_bytes": 8 * K * n}
+    if pairs_ms is not None:
+        out["rulebook_ms"] = pairs_ms
+        out["frac_rulebook"] = nbytes / (pairs_ms * 1e-3) / 1e9 / PEAK_HBM_GBS
+    return out
 
 
 def measured_ceilings():
@@ -313,6 +337,7 @@ def unet_scenes(stream, reps):
     params = unet.device_params(draw=lambda n, k, ci, co: S.layer_params(n, k, ci, co, bf16=True))
     geom_ms = _wall_ms(lambda: unet.Geometry(tc, (256, 256, 256)), reps)
     ssc0_ms = _wall_ms(lambda: sscn.ssc_rulebook_build(tc, (256, 256, 256), 3), reps)
+    ssc0_lat = _latency_ms(lambda: sscn.ssc_rulebook_build(tc, (256, 256, 256), 3), reps)
     ssc0_pairs = sscn.ssc_rulebook_build(tc, (256, 256, 256), 3).n_pairs
     # a fresh input: rule books of every level, then the network (lazily built
     # tables included)
@@ -325,7 +350,7 @@ def unet_scenes(stream, reps):
             "geometry_build_ms": geom_ms,
             "level0_ssc_build_roofline": build_roofline(int(c.shape[0]), 27, int(ssc0_pairs), ssc0_ms,
                                                         "SSC 3^3 rule-book build incl. its row-block plan, "
-                                                        "level 0 (about 2M sites)"),
+                                                        "level 0 (about 2M sites)", pairs_ms=ssc0_lat),
             "forward_ms": fwd_ms, "forward_sites_per_s": c.shape[0] / (fwd_ms * 1e-3),
             "forward_effective_tflops": fl / (fwd_ms * 1e-3) / 1e12, "flops": fl,
             "forward_unfused_ms": unfused_ms, "geometry_plus_forward_ms": fresh_ms,
@@ -515,6 +540,7 @@ def main():
     torch.cuda.synchronize()
     build_ms = (time.perf_counter() - tb) * 1e3 / reps
     del rbx
+    build_lat_ms = _latency_ms(lambda: sscn.ssc_rulebook_build(tc, size, 3), reps)
 
     timed = lambda fn: _event_ms(fn, reps, stream)
     fwd_ms = timed(lambda: sscn.sparse_conv_forward(tX, tW, rb))
@@ -568,7 +594,8 @@ def main():
                      "launch_ms": launch_ms, "launches_timed": len(timers),
                      "flops_per_launch": flops_layer, "traffic": recorded_traffic()},
         "build_roofline": build_roofline(int(n), 27, int(pairs), build_ms,
-                                         "SSC 3^3 rule-book build incl. its row-block plan, 100k sites"),
+                                         "SSC 3^3 rule-book build incl. its row-block plan, 100k sites",
+                                         pairs_ms=build_lat_ms),
     }
     if not args.no_extra:
         ceil = measured_ceilings()
