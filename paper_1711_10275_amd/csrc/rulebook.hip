@@ -419,14 +419,21 @@ __global__ __launch_bounds__(256) void k_count_nbr(const int32_t* __restrict__ n
 // workgroup per tile: wavefront w takes the offsets o = w mod 4 (four times
 // the wavefronts of one per tile, to keep more reads in flight), and the
 // row masks of the four are combined in LDS.
+// host_stats (if not NULL, pinned host memory): workgroup 0 also copies
+// the n_stats words of stats there (sizes and flags, final before this
+// kernel), in place of a separate copy to the host.
 __global__ __launch_bounds__(256) void k_compact(const int32_t* __restrict__ nbr, int64_t n_rows, int K,
                                                  const int64_t* __restrict__ seg, int64_t n_tiles,
                                                  int32_t* __restrict__ in_rows,
                                                  int32_t* __restrict__ out_rows,
-                                                 uint32_t* __restrict__ row_mask) {
+                                                 uint32_t* __restrict__ row_mask,
+                                                 const unsigned long long* __restrict__ stats,
+                                                 unsigned long long* __restrict__ host_stats, int n_stats) {
   __shared__ uint32_t part[kPlanMaskWords][4][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t t = blockIdx.x;  // one workgroup per tile
+  if (host_stats && t == 0)
+    for (int i = threadIdx.x; i < n_stats; i += blockDim.x) host_stats[i] = stats[i];
   const int64_t k = t * kTile + lane;
   const bool valid = k < n_rows;
   const unsigned long long below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
@@ -1103,17 +1110,27 @@ struct ReadbackState {
 };
 static thread_local ReadbackState t_readback;
 
-static sscn_status readback_begin(const void* dev, size_t bytes, hipStream_t s) {
+// The staging buffer (at least `bytes`), for a kernel to write into
+// directly (then readback_begin with dev = NULL only records the event).
+static sscn_status readback_staging(size_t bytes, void** host) {
   ReadbackState& r = t_readback;
   if (r.bytes < bytes) {
     if (r.pinned) (void)hipHostFree(r.pinned);
     r.pinned = nullptr;
     r.bytes = 0;
-    SSCN_HIP(hipHostMalloc(&r.pinned, std::max<size_t>(bytes, 4096), hipHostMallocDefault));
+    SSCN_HIP(hipHostMalloc(&r.pinned, std::max<size_t>(bytes, 4096), hipHostMallocCoherent));
     r.bytes = std::max<size_t>(bytes, 4096);
   }
+  *host = r.pinned;
+  return SSCN_OK;
+}
+
+static sscn_status readback_begin(const void* dev, size_t bytes, hipStream_t s) {
+  ReadbackState& r = t_readback;
+  void* staging = nullptr;
+  SSCN_TRY(readback_staging(bytes, &staging));
   if (!r.done) SSCN_HIP(hipEventCreateWithFlags(&r.done, hipEventDisableTiming));
-  SSCN_HIP(hipMemcpyAsync(r.pinned, dev, bytes, hipMemcpyDeviceToHost, s));
+  if (dev) SSCN_HIP(hipMemcpyAsync(staging, dev, bytes, hipMemcpyDeviceToHost, s));
   SSCN_HIP(hipEventRecord(r.done, s));
   return SSCN_OK;
 }
@@ -1140,7 +1157,9 @@ static sscn_status launch_fill_slots(Slot* t, uint64_t cap, int32_t row_init, hi
 // Segment table and pair arrays of one direction from an offset-major
 // neighbour map (st.seg, st.in_rows and st.out_rows already allocated).
 static sscn_status compact_storage(const int32_t* nbr, int64_t n_rows, int K, Storage& st, hipStream_t s,
-                                   bool counted, uint32_t* row_mask = nullptr) {
+                                   bool counted, uint32_t* row_mask = nullptr,
+                                   const unsigned long long* stats = nullptr,
+                                   unsigned long long* host_stats = nullptr, int n_stats = 0) {
   if (!counted && st.n_tiles > 0) {
     k_count_nbr<<<grid_for(st.n_tiles * 64, 256), 256, 0, s>>>(nbr, n_rows, K, st.seg, st.n_tiles);
     SSCN_HIP(hipGetLastError());
@@ -1155,7 +1174,8 @@ static sscn_status compact_storage(const int32_t* nbr, int64_t n_rows, int K, St
   }
   if (st.n_tiles > 0) {
     k_compact<<<(unsigned)st.n_tiles, 256, 0, s>>>(nbr, n_rows, K, st.seg, st.n_tiles, st.in_rows,
-                                                             st.out_rows, K <= kPlanMaxK ? row_mask : nullptr);
+                                                             st.out_rows, K <= kPlanMaxK ? row_mask : nullptr,
+                                                             stats, host_stats, n_stats);
     SSCN_HIP(hipGetLastError());
   }
   return SSCN_OK;
@@ -1951,17 +1971,24 @@ static sscn_status ssc_build(const int32_t* coords, int64_t n, const int32_t* sp
         SSCN_HIP(hipGetLastError());
       }
     }
-    auto compact = [&]() -> sscn_status {
-      if (n > 0) SSCN_TRY(compact_storage(nbr, n, K, d->fwd, s, /*counted=*/true, d->fwd.row_mask));
+    const size_t stat_bytes = sizeof(unsigned long long) * (1 + K);
+    // Before the readback, the compaction's first workgroup copies the sizes
+    // and flags to the pinned staging buffer itself (no copy launch).
+    void* staging = nullptr;
+    const bool direct = one_phase && n > 0;
+    if (direct) SSCN_TRY(readback_staging(stat_bytes, &staging));
+    auto compact = [&](bool to_host) -> sscn_status {
+      if (n > 0)
+        SSCN_TRY(compact_storage(nbr, n, K, d->fwd, s, /*counted=*/true, d->fwd.row_mask, stats,
+                                 to_host ? (unsigned long long*)staging : nullptr, 1 + K));
       return SSCN_OK;
     };
-    if (one_phase) SSCN_TRY(compact());
+    if (one_phase) SSCN_TRY(compact(direct));
     // The sizes and flags are final here.  The plan is queued behind their
-    // copy: the host waits for the copy only, and the plan's kernels run
+    // readback: the host waits for that alone, and the plan's kernels run
     // while it returns (a use of the plan on another stream waits for the
     // rule book's stream).
-    const size_t stat_bytes = sizeof(unsigned long long) * (1 + K);
-    SSCN_TRY(readback_begin(stats, stat_bytes, s));
+    SSCN_TRY(readback_begin(direct ? nullptr : stats, stat_bytes, s));
     if (eager_plan) SSCN_TRY(build_plan(d, d->fwd, n, K, s, /*a site has one neighbour per offset*/ n, hist));
     std::vector<unsigned long long> host(1 + K);
     SSCN_TRY(readback_end(host.data(), stat_bytes));
@@ -1977,7 +2004,7 @@ static sscn_status ssc_build(const int32_t* coords, int64_t n, const int32_t* sp
       Arena pa;
       add_pairs(pa, total);
       SSCN_TRY(owned_alloc(d, pa, s));
-      SSCN_TRY(compact());
+      SSCN_TRY(compact(false));
     }
   }
   guard.release();
