@@ -204,19 +204,22 @@ __global__ __launch_bounds__(256) void k_colreduce_vec(const T* __restrict__ x, 
 }
 
 // Sums of the partials of the `blocks` workgroups for channel col: one
-// workgroup of 256 threads per 64 channels, wavefront w adding blocks
-// w, w + 4, .. in order and the four wavefronts' sums then added in order
-// (a fixed order: reproducible).  (One thread adding all blocks in turn took
-// ~0.25 ms for 1024 blocks.)
+// workgroup of kFinThreads threads per 64 channels, wavefront w adding
+// blocks w, w + 16, .. in order, then the sixteen wavefronts' sums added
+// pairwise in a fixed tree (a fixed order: reproducible).  (One thread
+// adding all blocks in turn took ~0.25 ms for 1024 blocks; four wavefronts
+// ~15 us.)
+constexpr int kFinThreads = 1024;
 __device__ __forceinline__ bool sum_partials(const double* __restrict__ partial, int blocks, int c, double& s0,
                                              double& s1, int& col) {
-  __shared__ double red[2][4][64];
+  constexpr int NW = kFinThreads / 64;
+  __shared__ double red[2][NW][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   col = blockIdx.x * 64 + lane;
   double a0 = 0.0, a1 = 0.0;
   if (col < c) {
-#pragma unroll 8
-    for (int b = wave; b < blocks; b += 4) {
+#pragma unroll 4
+    for (int b = wave; b < blocks; b += NW) {
       a0 += partial[((int64_t)b * 2) * c + col];
       a1 += partial[((int64_t)b * 2 + 1) * c + col];
     }
@@ -224,16 +227,24 @@ __device__ __forceinline__ bool sum_partials(const double* __restrict__ partial,
   red[0][wave][lane] = a0;
   red[1][wave][lane] = a1;
   __syncthreads();
+#pragma unroll
+  for (int h = NW / 2; h >= 1; h /= 2) {
+    if (wave < h) {
+      red[0][wave][lane] += red[0][wave + h][lane];
+      red[1][wave][lane] += red[1][wave + h][lane];
+    }
+    __syncthreads();
+  }
   if (wave != 0 || col >= c) return false;
-  s0 = ((red[0][0][lane] + red[0][1][lane]) + red[0][2][lane]) + red[0][3][lane];
-  s1 = ((red[1][0][lane] + red[1][1][lane]) + red[1][2][lane]) + red[1][3][lane];
+  s0 = red[0][0][lane];
+  s1 = red[1][0][lane];
   return true;
 }
 
 // Batch statistics -> the affine map of the normalisation, and the running
 // (inference) statistics: mean, biased variance for the map, unbiased for
 // the running variance.
-__global__ __launch_bounds__(256) void k_bn_finalize(const double* __restrict__ partial, int blocks, int c,
+__global__ __launch_bounds__(kFinThreads) void k_bn_finalize(const double* __restrict__ partial, int blocks, int c,
                                                      int64_t n, const float* __restrict__ gamma,
                                                      const float* __restrict__ beta, float eps, float momentum,
                                                      float* running_mean, float* running_var,
@@ -257,7 +268,7 @@ __global__ __launch_bounds__(256) void k_bn_finalize(const double* __restrict__ 
   }
 }
 
-__global__ __launch_bounds__(256) void k_two_sums(const double* __restrict__ partial, int blocks, int c,
+__global__ __launch_bounds__(kFinThreads) void k_two_sums(const double* __restrict__ partial, int blocks, int c,
                                                   float* __restrict__ out0, float* __restrict__ out1) {
   double s0, s1;
   int col;
@@ -656,7 +667,7 @@ extern "C" sscn_status sscn_batchnorm_forward(const void* x, int64_t ldx, int64_
   SSCN_TRY(part.alloc(blocks, c));
   SSCN_TRY(colreduce<kSumSquares>(dtype, x, ldx, nullptr, 0, n, c, nullptr, nullptr, nullptr, nullptr, part.p, blocks,
                                   stream));
-  k_bn_finalize<<<(unsigned)ceil_div(c, 64), 256, 0, stream>>>(part.p, blocks, c, n, gamma, beta, eps, momentum,
+  k_bn_finalize<<<(unsigned)ceil_div(c, 64), kFinThreads, 0, stream>>>(part.p, blocks, c, n, gamma, beta, eps, momentum,
                                                                 running_mean, running_var, mean, invstd, scale, shift);
   SSCN_HIP(hipGetLastError());
   return SSCN_OK;
@@ -696,7 +707,7 @@ extern "C" sscn_status sscn_batchnorm_relu_backward_params(const void* da, int64
   Partials part(stream);
   SSCN_TRY(part.alloc(blocks, c));
   SSCN_TRY(colreduce<kBnBack>(dtype, x, ldx, da, ldd, n, c, scale, beta, mean, invstd, part.p, blocks, stream));
-  k_two_sums<<<(unsigned)ceil_div(c, 64), 256, 0, stream>>>(part.p, blocks, c, dbeta, dgamma);
+  k_two_sums<<<(unsigned)ceil_div(c, 64), kFinThreads, 0, stream>>>(part.p, blocks, c, dbeta, dgamma);
   SSCN_HIP(hipGetLastError());
   return SSCN_OK;
 }
@@ -741,7 +752,7 @@ extern "C" sscn_status sscn_column_sum(const void* x, int64_t ldx, int64_t n, in
   SSCN_TRY(part.alloc(blocks, c));
   SSCN_TRY(colreduce<kSums>(dtype, x, ldx, nullptr, 0, n, c, nullptr, nullptr, nullptr, nullptr, part.p, blocks,
                             stream));
-  k_two_sums<<<(unsigned)ceil_div(c, 64), 256, 0, stream>>>(part.p, blocks, c, out, nullptr);
+  k_two_sums<<<(unsigned)ceil_div(c, 64), kFinThreads, 0, stream>>>(part.p, blocks, c, out, nullptr);
   SSCN_HIP(hipGetLastError());
   return SSCN_OK;
 }
