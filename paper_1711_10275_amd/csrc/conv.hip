@@ -2238,7 +2238,6 @@ template <int CI, int CO, int OPG, bool TILED>
 __global__ __launch_bounds__(256) void k_wgrad_rows(const bf16_t* __restrict__ X, uint32_t x_bytes, uint32_t x_ld,
                                                     const bf16_t* __restrict__ dY, uint32_t y_bytes,
                                                     const int32_t* __restrict__ perm,
-                                                    const int32_t* __restrict__ b_first,
                                                     const int4* __restrict__ b_rec,
                                                     const uint32_t* __restrict__ items, int64_t n_blocks, int K,
                                                     int groups, float* __restrict__ part) {
@@ -2433,10 +2432,10 @@ static sscn_status launch_wgrad_rows_t(const bf16_t* X, const bf16_t* dY, const 
   hipEvent_t t0, t1;
   if (take_launch_timer(&t0, &t1))
     hipExtLaunchKernelGGL(kern, grid, dim3(256), 0, s, t0, t1, 0, X, xb, (uint32_t)cin * 2u, dY, yb, v.st->perm,
-                          v.st->b_first, v.st->b_rec, v.st->items, nb, v.K, groups, part);
+                          v.st->b_rec, v.st->items, nb, v.K, groups, part);
   else
-    kern<<<grid, 256, 0, s>>>(X, xb, (uint32_t)cin * 2u, dY, yb, v.st->perm, v.st->b_first, v.st->b_rec,
-                              v.st->items, nb, v.K, groups, part);
+    kern<<<grid, 256, 0, s>>>(X, xb, (uint32_t)cin * 2u, dY, yb, v.st->perm, v.st->b_rec, v.st->items, nb, v.K,
+                              groups, part);
   hipError_t e = hipGetLastError();
   if (e == hipSuccess) {
     const int64_t total = (int64_t)v.K * cin * CO;

@@ -417,3 +417,25 @@ def test_wgrad_deterministic_mode(dtype, cin, cout):
         assert_close(host(d1), rdw, "f32", "deterministic wgrad")
         _, da = sscn.sparse_conv_backward(*args, dgrad=False)
         assert_close(host(da), rdw, "f32", "atomic wgrad")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("cin,cout", [(32, 20), (20, 32), (64, 64), (8, 300), (3, 5), (70, 33)])
+def test_filter1_per_row(cin, cout, dtype):
+    """SSC of filter size 1 (one offset, every row paired with itself: a
+    per-row linear map), on the row-block and the generic kernels: forward
+    with and without a bias, dgrad and wgrad against the oracle."""
+    coords, size = coords_for("shapes128")
+    rb = sscn.ssc_rulebook_build(dev(coords), size, 1)
+    orb = O.ssc_rulebook(coords, size, 1)
+    n = coords.shape[0]
+    X, W = _draw(n, cin, cout, 1, 80 + cin, dtype)
+    assert_close(_fwd(rb, X, W, dtype), O.forward(X, W, orb), dtype, f"f=1 forward {cin}x{cout}")
+    bias = S.features(1, cout, S.SEED_WEIGHT + 81 + cin)[0]
+    y = sscn.sparse_conv_forward_ex(dev(X, TD[dtype]), dev(W, TD[dtype]), rb, bias=dev(bias, torch.float32))
+    assert_close(host(y), O.forward_bias(X, W, bias, orb), dtype, f"f=1 bias {cin}x{cout}")
+    G = S.features(n, cout, S.SEED_GRAD + 82 + cin, bf16=dtype == "bf16")
+    dx, dw = sscn.sparse_conv_backward(dev(X, TD[dtype]), dev(W, TD[dtype]), dev(G, TD[dtype]), rb)
+    rdx, rdw = O.backward(X, W, G, orb)
+    assert_close(host(dx), rdx, dtype, f"f=1 dgrad {cin}x{cout}")
+    assert_close(host(dw), rdw, "f32", f"f=1 wgrad {cin}x{cout}")
