@@ -2453,8 +2453,10 @@ static sscn_status launch_wgrad_rows(const bf16_t* X, const bf16_t* dY, const Vi
   // Input-channel tiles of 128 (c_in = 128, c_out = 64), 64 where they
   // divide c_in, else 32; offsets per group: the wavefront's accumulators
   // (OPG x TPW x 4 VGPRs, TPW = CI CO / 1024) and operands within about 170
-  // VGPRs, and for 32 x 32 two groups of 14 (more resident workgroups: the
-  // U-Net training step 15.4 -> 15.1 ms against one group of 27).
+  // VGPRs; fewer where more resident workgroups paid off in the U-Net
+  // training step (32 x 32: two groups of 14 instead of one of 27, 15.4 ->
+  // 15.1 ms; 32 x 96 tiles 5 instead of 9, 64 x 96 tiles 2 instead of 4,
+  // about 0.1 ms each).
   const bool t64 = cin % 64 == 0;
   switch (cout) {
     case 32:
@@ -2465,8 +2467,8 @@ static sscn_status launch_wgrad_rows(const bf16_t* X, const bf16_t* dY, const Vi
       return t64 ? launch_wgrad_rows_t<64, 64, 6>(X, dY, v, cin, dW, s)
                  : launch_wgrad_rows_t<32, 64, 13>(X, dY, v, cin, dW, s);
     case 96:
-      return t64 ? launch_wgrad_rows_t<64, 96, 4>(X, dY, v, cin, dW, s)
-                 : launch_wgrad_rows_t<32, 96, 9>(X, dY, v, cin, dW, s);
+      return t64 ? launch_wgrad_rows_t<64, 96, 2>(X, dY, v, cin, dW, s)
+                 : launch_wgrad_rows_t<32, 96, 5>(X, dY, v, cin, dW, s);
     case 128:
       return t64 ? launch_wgrad_rows_t<64, 128, 3>(X, dY, v, cin, dW, s)
                  : launch_wgrad_rows_t<32, 128, 6>(X, dY, v, cin, dW, s);
