@@ -261,14 +261,15 @@ def test_forward_heads_rejects_bad_heads():
         sscn.sparse_conv_forward_heads(X, W, rb, [(out, None, None)] * 3)
 
 
-@pytest.mark.parametrize("f,s", [(2, 2), (3, 2), (1, 2)])
+@pytest.mark.parametrize("f,s", [(2, 2), (3, 2), (1, 2), (4, 4), (4, 2)])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_sc_and_dc_row_blocks(f, s, dtype):
     """SC / DC with channel counts the row-block kernel takes (multiples of
     8): forward and backward of both directions.  With f = 1, s = 2 the SC
     inputs at odd positions reach no output, so the DC direction has output
-    rows without any pair (they must come out zero)."""
-    size = (8, 8, 8) if (f, s) == (2, 2) else (9, 9, 9)
+    rows without any pair (they must come out zero).  f = 4 gives 64
+    offsets: offset sets of two 32-bit words in both directions' plans."""
+    size = (8, 8, 8) if (f, s) in ((2, 2), (4, 4), (4, 2)) else (9, 9, 9)
     c = small_set(60 + 3 * f + s, size, batch=2, density=0.3)
     rb = sscn.sc_rulebook_build(dev(c), size, f, s)
     orb = O.sc_rulebook(c, size, f, s)
