@@ -523,6 +523,7 @@ __global__ void k_tile_scatter(const int32_t* __restrict__ key, int64_t n_tiles,
 // whole pass in one launch (launches dominate such passes).
 constexpr int kOneBlock = 1024;
 constexpr int64_t kOneBlockScanMax = 1 << 17;     // elements
+constexpr int64_t kOneBlockSegMax = 1 << 15;      // elements, for the in-place segment scans of compaction
 
 // Exclusive prefix of the per-thread values `v` over the workgroup (1024
 // threads = 16 wavefronts); returns the total through `total`.
@@ -1165,7 +1166,9 @@ static sscn_status compact_storage(const int32_t* nbr, int64_t n_rows, int K, St
     SSCN_HIP(hipGetLastError());
   }
   if (!counted) {
-    if (K * st.n_tiles <= kOneBlockScanMax) {
+    // one workgroup up to 32k counts (its time grows with the count: ~10 us
+    // at 32k, ~27 us at 67k), the multi-workgroup scan beyond
+    if (K * st.n_tiles <= kOneBlockSegMax) {
       launch_seg_scan_one(st.seg, st.seg, K * st.n_tiles, std::max<int64_t>(st.n_tiles, 1), K, nullptr, s);
       SSCN_HIP(hipGetLastError());
     } else {
