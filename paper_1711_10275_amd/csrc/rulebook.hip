@@ -957,12 +957,11 @@ __global__ __launch_bounds__(256) void k_sc_mark(const int4* __restrict__ coords
     if (cnt[o]) atomicAdd(&per_offset[o], (unsigned long long)cnt[o]);
 }
 
-// Per visit: output row = rank of its output's first visit (one_target:
-// rank is indexed by input, as first in k_sc_mark).  Writes the
+// Per visit: output row = rank of its output's first visit.  Writes the
 // output-major map nbr_out[o][k] = j, the input-major map nbr_in[o][j] = k,
 // and the output coordinates (by the first visitor).
 __global__ __launch_bounds__(256) void k_sc_assign(const int4* __restrict__ coords, int64_t n, ScGeom g,
-                                                   const Slot* __restrict__ otable, uint64_t omask, int one_target,
+                                                   const Slot* __restrict__ otable, uint64_t omask,
                                                    const int32_t* __restrict__ rank, int64_t n_out,
                                                    int32_t* __restrict__ nbr_out,
                                                    int32_t* __restrict__ nbr_in,
@@ -975,11 +974,76 @@ __global__ __launch_bounds__(256) void k_sc_assign(const int4* __restrict__ coor
     int y0, y1, y2;
     if (!sc_target(g, c, o, y0, y1, y2)) continue;
     const int32_t vmin = table_lookup(otable, omask, pack_key(c.x, y0, y1, y2));
-    const int32_t k = rank[one_target ? vmin / g.K : vmin];
+    const int32_t k = rank[vmin];
     nbr_out[(int64_t)o * n_out + k] = (int32_t)j;
     nbr_in[(int64_t)o * n + j] = k;
     if (vmin == (int32_t)(j * g.K + o)) out_coords[k] = make_int4(c.x, y0, y1, y2);
   }
+}
+
+// k_sc_assign for one_target (every input sees at most one output): besides
+// nbr_out and the output coordinates, the input-major direction is kept as one
+// record per input, tgt[j] = {k, o} ({-1, -1} for an input of no output), and
+// its pair count per (offset, tile of kTile inputs) goes to counts[o][t] for
+// every offset, so that no K x n map is filled, counted and compacted.
+__global__ __launch_bounds__(256) void k_sc_assign1(const int4* __restrict__ coords, int64_t n, ScGeom g,
+                                                    const Slot* __restrict__ otable, uint64_t omask,
+                                                    const int32_t* __restrict__ rank, int64_t n_out,
+                                                    int32_t* __restrict__ nbr_out, int2* __restrict__ tgt,
+                                                    int64_t* __restrict__ counts, int64_t n_tiles,
+                                                    int4* __restrict__ out_coords) {
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t t = j / kTile;  // one tile per wavefront
+  if (t >= n_tiles) return;     // whole wavefronts
+  const int lane = threadIdx.x & 63;
+  const bool valid = j < n;
+  const int4 c = valid ? coords[j] : make_int4(0, 0, 0, 0);
+  int32_t k = -1, oj = -1;
+  if (valid && site_in_range(c, g)) {
+    for (int o = 0; o < g.K; ++o) {
+      int y0, y1, y2;
+      if (!sc_target(g, c, o, y0, y1, y2)) continue;
+      const int32_t vmin = table_lookup(otable, omask, pack_key(c.x, y0, y1, y2));
+      k = rank[vmin / g.K];
+      oj = o;
+      nbr_out[(int64_t)o * n_out + k] = (int32_t)j;
+      if (vmin == (int32_t)(j * g.K + o)) out_coords[k] = make_int4(c.x, y0, y1, y2);
+      break;  // the only output of this input
+    }
+  }
+  if (valid) tgt[j] = make_int2(k, oj);
+  for (int o = 0; o < g.K; ++o) {
+    const unsigned long long m = __ballot(oj == o);
+    if (lane == 0) counts[(int64_t)o * n_tiles + t] = __popcll(m);
+  }
+}
+
+// Pairs and row masks of the input-major direction from the records of
+// k_sc_assign1 (counts already scanned into seg): input j of tile t with
+// offset o goes to seg[o][t] + its rank among the tile's inputs of offset o,
+// the order k_compact gives; its row mask is the one bit of o (K <= 32).
+__global__ __launch_bounds__(256) void k_compact1(const int2* __restrict__ tgt, int64_t n, int K,
+                                                  const int64_t* __restrict__ seg, int64_t n_tiles,
+                                                  int32_t* __restrict__ in_rows, int32_t* __restrict__ out_rows,
+                                                  uint32_t* __restrict__ row_mask) {
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t t = j / kTile;
+  if (t >= n_tiles) return;  // whole wavefronts
+  const int lane = threadIdx.x & 63;
+  const bool valid = j < n;
+  const int2 r = valid ? tgt[j] : make_int2(-1, -1);
+  unsigned long long peers = 0;
+  for (int o = 0; o < K; ++o) {
+    const unsigned long long m = __ballot(r.y == o);
+    if (r.y == o) peers = m;
+  }
+  if (r.y >= 0) {
+    const unsigned long long below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    const int64_t pos = seg[(int64_t)r.y * n_tiles + t] + __popcll(peers & below);
+    in_rows[pos] = r.x;
+    out_rows[pos] = (int32_t)j;
+  }
+  if (row_mask && valid) row_mask[j] = r.y >= 0 ? 1u << r.y : 0u;
 }
 
 // ------------------------------------------------------------- host helpers
@@ -1155,6 +1219,19 @@ static sscn_status launch_fill_slots(Slot* t, uint64_t cap, int32_t row_init, hi
   return SSCN_OK;
 }
 
+// Segment table of one direction from its pair counts per (offset, tile),
+// in place.
+static sscn_status scan_seg(Storage& st, int K, hipStream_t s) {
+  // one workgroup up to 32k counts (its time grows with the count: ~10 us
+  // at 32k, ~27 us at 67k), the multi-workgroup scan beyond
+  if (K * st.n_tiles <= kOneBlockSegMax) {
+    launch_seg_scan_one(st.seg, st.seg, K * st.n_tiles, std::max<int64_t>(st.n_tiles, 1), K, nullptr, s);
+    SSCN_HIP(hipGetLastError());
+    return SSCN_OK;
+  }
+  return exclusive_scan_i64(st.seg, st.seg, K * st.n_tiles, s);
+}
+
 // Segment table and pair arrays of one direction from an offset-major
 // neighbour map (st.seg, st.in_rows and st.out_rows already allocated).
 static sscn_status compact_storage(const int32_t* nbr, int64_t n_rows, int K, Storage& st, hipStream_t s,
@@ -1165,16 +1242,7 @@ static sscn_status compact_storage(const int32_t* nbr, int64_t n_rows, int K, St
     k_count_nbr<<<grid_for(st.n_tiles * 64, 256), 256, 0, s>>>(nbr, n_rows, K, st.seg, st.n_tiles);
     SSCN_HIP(hipGetLastError());
   }
-  if (!counted) {
-    // one workgroup up to 32k counts (its time grows with the count: ~10 us
-    // at 32k, ~27 us at 67k), the multi-workgroup scan beyond
-    if (K * st.n_tiles <= kOneBlockSegMax) {
-      launch_seg_scan_one(st.seg, st.seg, K * st.n_tiles, std::max<int64_t>(st.n_tiles, 1), K, nullptr, s);
-      SSCN_HIP(hipGetLastError());
-    } else {
-      SSCN_TRY(exclusive_scan_i64(st.seg, st.seg, K * st.n_tiles, s));
-    }
-  }
+  if (!counted) SSCN_TRY(scan_seg(st, K, s));
   if (st.n_tiles > 0) {
     k_compact<<<(unsigned)st.n_tiles, 256, 0, s>>>(nbr, n_rows, K, st.seg, st.n_tiles, st.in_rows,
                                                              st.out_rows, K <= kPlanMaxK ? row_mask : nullptr,
@@ -2144,7 +2212,23 @@ extern "C" sscn_status sc_rulebook_build(const int32_t* coords, int64_t n, const
       oa.add(&d->bwd.row_mask, (size_t)n * plan_words(K));
     }
     SSCN_TRY(owned_alloc(d, oa, s));
-    if (n > 0) {
+    if (n > 0 && one_target) {
+      int32_t* nbr_out; int2* tgt;
+      Arena na;
+      na.add(&nbr_out, (size_t)K * n_out);
+      na.add(&tgt, (size_t)n);
+      SSCN_TRY(tmp.alloc(na));
+      SSCN_TRY(fill_i32(nbr_out, -1, (int64_t)K * n_out, s));
+      k_sc_assign1<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, rank, n_out,
+                                                    nbr_out, tgt, d->bwd.seg, d->bwd.n_tiles,
+                                                    (int4*)d->out_coords);
+      SSCN_HIP(hipGetLastError());
+      SSCN_TRY(compact_storage(nbr_out, n_out, K, d->fwd, s, false, d->fwd.row_mask));
+      SSCN_TRY(scan_seg(d->bwd, K, s));
+      k_compact1<<<grid_for(n, 256), 256, 0, s>>>(tgt, n, K, d->bwd.seg, d->bwd.n_tiles, d->bwd.in_rows,
+                                                  d->bwd.out_rows, d->bwd.row_mask);
+      SSCN_HIP(hipGetLastError());
+    } else if (n > 0) {
       int32_t* nbr_out; int32_t* nbr_in;
       Arena na;
       na.add(&nbr_out, (size_t)K * n_out);
@@ -2152,8 +2236,7 @@ extern "C" sscn_status sc_rulebook_build(const int32_t* coords, int64_t n, const
       SSCN_TRY(tmp.alloc(na));
       SSCN_TRY(fill_i32(nbr_out, -1, (int64_t)K * n_out, s));
       SSCN_TRY(fill_i32(nbr_in, -1, (int64_t)K * n, s));
-      k_sc_assign<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, one_target ? 1 : 0,
-                                                   rank, n_out,
+      k_sc_assign<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, rank, n_out,
                                                    nbr_out, nbr_in, (int4*)d->out_coords);
       SSCN_HIP(hipGetLastError());
       SSCN_TRY(compact_storage(nbr_out, n_out, K, d->fwd, s, false, d->fwd.row_mask));
