@@ -868,6 +868,52 @@ __global__ __launch_bounds__(256) void k_sc_visit(const int4* __restrict__ coord
   }
 }
 
+// Where every input sees at most one output (f <= s): its offset o (the
+// position i = x mod s per dimension, when that is below f) and its output
+// y = x div s.  Same result as sc_target over all offsets.
+__device__ __forceinline__ bool sc_target1(const ScGeom& g, int4 c, bool in_range, int& o, int& y0, int& y1,
+                                           int& y2) {
+  const int i0 = c.y % g.s, i1 = c.z % g.s, i2 = c.w % g.s;
+  o = (i0 * g.f + i1) * g.f + i2;
+  y0 = c.y / g.s; y1 = c.z / g.s; y2 = c.w / g.s;
+  return in_range && i0 < g.f && i1 < g.f && i2 < g.f && y0 < g.M0 && y1 < g.M1 && y2 < g.M2;
+}
+
+// Group the hit lanes of a wavefront by output key (one pass per distinct
+// key): the lowest lane of each group, its leader, gets the group's lanes in
+// peers (0 elsewhere); every hit lane gets its leader's lane (-1 elsewhere).
+// Lanes follow the rows, so the leader holds the group's smallest visit.
+__device__ __forceinline__ void sc_group(bool hit, uint64_t key, int lane, uint64_t& peers, int& leader) {
+  uint64_t todo = __ballot(hit);
+  peers = 0;
+  leader = -1;
+  while (todo) {
+    const int l = __ffsll((unsigned long long)todo) - 1;
+    const uint64_t lk = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(key >> 32), l) << 32) |
+                        (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)key, l);
+    const uint64_t p = __ballot(hit && key == lk);
+    if (lane == l) peers = p;
+    if ((p >> lane) & 1) leader = l;
+    todo &= ~p;
+  }
+}
+
+// unsorted[0] = 1 unless the rows are strictly increasing in (batch, x0,
+// x1, x2): such rows hold no location twice (one plain store per
+// wavefront that finds a pair out of order; no atomics).
+__global__ __launch_bounds__(256) void k_sc_order(const int4* __restrict__ coords, int64_t n,
+                                                  int* __restrict__ unsorted) {
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  bool bad = false;
+  if (j >= 1 && j < n) {
+    const int4 a = coords[j - 1], b = coords[j];
+    const bool less = a.x != b.x ? a.x < b.x : a.y != b.y ? a.y < b.y : a.z != b.z ? a.z < b.z : a.w < b.w;
+    bad = !less;
+  }
+  const unsigned long long m = __ballot(bad);
+  if (m && (threadIdx.x & 63) == __ffsll(m) - 1) unsorted[0] = 1;
+}
+
 // k_sc_visit where every input sees at most one output (f <= s: offset
 // i = x mod s per dimension, when that is below f) and K <= 32.  The lanes
 // of a wavefront whose inputs share an output (neighbouring rows of sorted
@@ -879,7 +925,7 @@ __global__ __launch_bounds__(256) void k_sc_visit(const int4* __restrict__ coord
 __global__ __launch_bounds__(256) void k_sc_visit1(const int4* __restrict__ coords, int64_t n, ScGeom g,
                                                    Slot* __restrict__ otable, uint64_t omask, int check,
                                                    unsigned long long* __restrict__ flags,
-                                                   int4* __restrict__ copy) {
+                                                   int4* __restrict__ copy, const int* __restrict__ unsorted) {
   const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int lane = threadIdx.x & 63;
   const bool valid = j < n;
@@ -887,21 +933,12 @@ __global__ __launch_bounds__(256) void k_sc_visit1(const int4* __restrict__ coor
   if (valid && copy) copy[j] = c;
   const bool in_range = valid && site_in_range(c, g);
   if (valid && !in_range && check) atomicOr(flags, (unsigned long long)kFlagOutOfRange);
-  const int i0 = c.y % g.s, i1 = c.z % g.s, i2 = c.w % g.s;
-  const int o = (i0 * g.f + i1) * g.f + i2;
-  const int y0 = c.y / g.s, y1 = c.z / g.s, y2 = c.w / g.s;
-  const bool hit = in_range && i0 < g.f && i1 < g.f && i2 < g.f && y0 < g.M0 && y1 < g.M1 && y2 < g.M2;
+  int o, y0, y1, y2;
+  const bool hit = sc_target1(g, c, in_range, o, y0, y1, y2);
   const uint64_t key = hit ? pack_key(c.x, y0, y1, y2) : kEmptyKey;
-  // the group of each leader: one pass per distinct output of the wavefront
-  uint64_t todo = __ballot(hit), peers = 0;
-  while (todo) {
-    const int l = __ffsll((unsigned long long)todo) - 1;
-    const uint64_t lk = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(key >> 32), l) << 32) |
-                        (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)key, l);
-    const uint64_t p = __ballot(hit && key == lk);
-    if (lane == l) peers = p;
-    todo &= ~p;
-  }
+  uint64_t peers;
+  int leader;
+  sc_group(hit, key, lane, peers, leader);
   // offsets of each group: one ballot per offset
   uint32_t bits = 0;
   for (int b = 0; b < g.K; ++b)
@@ -916,18 +953,18 @@ __global__ __launch_bounds__(256) void k_sc_visit1(const int4* __restrict__ coor
     slot = (slot + 1) & omask;
   }
   atomicMin(&otable[slot].row, (int32_t)(j * g.K + o));
-  if (check && (atomicOr(&otable[slot].pad, (int32_t)bits) & (int32_t)bits))
+  // rows in strictly increasing order hold no location twice: the offsets
+  // are only collected (an atomic per group) for other rows
+  if (check && *unsorted && (atomicOr(&otable[slot].pad, (int32_t)bits) & (int32_t)bits))
     atomicOr(flags, (unsigned long long)kFlagDuplicate);
 }
 
 // first[v] = 1 iff visit v is the first visit of its output; count pairs
 // per offset (wave ballots summed in LDS, one global atomic per block and
-// offset).  one_target (every input sees at most one output): first is
-// indexed by input, first[j] = 1 iff input j makes the first visit of its
-// output.
+// offset).
 __global__ __launch_bounds__(256) void k_sc_mark(const int4* __restrict__ coords, int64_t n, ScGeom g,
                                                  const Slot* __restrict__ otable, uint64_t omask,
-                                                 int one_target, int32_t* __restrict__ first,
+                                                 int32_t* __restrict__ first,
                                                  unsigned long long* __restrict__ per_offset) {
   __shared__ unsigned int cnt[512];
   for (int o = threadIdx.x; o < g.K; o += blockDim.x) cnt[o] = 0;
@@ -937,7 +974,6 @@ __global__ __launch_bounds__(256) void k_sc_mark(const int4* __restrict__ coords
   const int4 c = valid ? coords[j] : make_int4(0, 0, 0, 0);
   const bool ok = valid && site_in_range(c, g);
   const int lane = threadIdx.x & 63;
-  int32_t any_first = 0;
   for (int o = 0; o < g.K; ++o) {
     int y0, y1, y2;
     int32_t is_first = 0;
@@ -946,15 +982,58 @@ __global__ __launch_bounds__(256) void k_sc_mark(const int4* __restrict__ coords
       const int32_t v = (int32_t)(j * g.K + o);
       is_first = table_lookup(otable, omask, pack_key(c.x, y0, y1, y2)) == v;
     }
-    if (valid && !one_target) first[j * g.K + o] = is_first;
-    any_first |= is_first;
+    if (valid) first[j * g.K + o] = is_first;
     const unsigned long long m = __ballot(hit);
     if (lane == 0 && m) atomicAdd(&cnt[o], (unsigned int)__popcll(m));
   }
-  if (valid && one_target) first[j] = any_first;
   __syncthreads();
   for (int o = threadIdx.x; o < g.K; o += blockDim.x)
     if (cnt[o]) atomicAdd(&per_offset[o], (unsigned long long)cnt[o]);
+}
+
+// k_sc_mark where every input sees at most one output: first[j] = 1 iff
+// input j makes the first visit of its output.  Only a group leader (see
+// sc_group) can: it looks up its output's first visit, the other lanes of
+// its group are later rows of the same output.  The workgroup's pair count
+// per offset goes to part[o][workgroup] (summed by k_offset_sums: global
+// atomics on K words from every workgroup serialise).
+__global__ __launch_bounds__(256) void k_sc_mark1(const int4* __restrict__ coords, int64_t n, ScGeom g,
+                                                  const Slot* __restrict__ otable, uint64_t omask,
+                                                  int32_t* __restrict__ first, uint32_t* __restrict__ part) {
+  __shared__ unsigned int cnt[32];
+  if (threadIdx.x < 32) cnt[threadIdx.x] = 0;
+  __syncthreads();
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int lane = threadIdx.x & 63;
+  const bool valid = j < n;
+  const int4 c = valid ? coords[j] : make_int4(0, 0, 0, 0);
+  int o, y0, y1, y2;
+  const bool hit = sc_target1(g, c, valid && site_in_range(c, g), o, y0, y1, y2);
+  const uint64_t key = hit ? pack_key(c.x, y0, y1, y2) : kEmptyKey;
+  uint64_t peers;
+  int leader;
+  sc_group(hit, key, lane, peers, leader);
+  int32_t is_first = 0;
+  if (hit && leader == lane) is_first = table_lookup(otable, omask, key) == (int32_t)(j * g.K + o);
+  if (valid) first[j] = is_first;
+  for (int b = 0; b < g.K; ++b) {
+    const unsigned long long m = __ballot(hit && o == b);
+    if (lane == 0 && m) atomicAdd(&cnt[b], (unsigned int)__popcll(m));
+  }
+  __syncthreads();
+  if (threadIdx.x < g.K) part[(int64_t)threadIdx.x * gridDim.x + blockIdx.x] = cnt[threadIdx.x];
+}
+
+// per_offset[o] = sum of part[o][0 .. n_parts), one workgroup per offset.
+__global__ __launch_bounds__(kOneBlock) void k_offset_sums(const uint32_t* __restrict__ part, int64_t n_parts,
+                                                           unsigned long long* __restrict__ per_offset) {
+  __shared__ int64_t wave_tot[kOneBlock / 64 + 1];
+  const uint32_t* row = part + (int64_t)blockIdx.x * n_parts;
+  int64_t v = 0;
+  for (int64_t i = threadIdx.x; i < n_parts; i += blockDim.x) v += row[i];
+  int64_t total;
+  (void)block_exclusive_scan(v, wave_tot, total);
+  if (threadIdx.x == 0) per_offset[blockIdx.x] = (unsigned long long)total;
 }
 
 // Per visit: output row = rank of its output's first visit.  Writes the
@@ -998,23 +1077,28 @@ __global__ __launch_bounds__(256) void k_sc_assign1(const int4* __restrict__ coo
   const int lane = threadIdx.x & 63;
   const bool valid = j < n;
   const int4 c = valid ? coords[j] : make_int4(0, 0, 0, 0);
-  int32_t k = -1, oj = -1;
-  if (valid && site_in_range(c, g)) {
-    for (int o = 0; o < g.K; ++o) {
-      int y0, y1, y2;
-      if (!sc_target(g, c, o, y0, y1, y2)) continue;
-      const int32_t vmin = table_lookup(otable, omask, pack_key(c.x, y0, y1, y2));
-      k = rank[vmin / g.K];
-      oj = o;
-      nbr_out[(int64_t)o * n_out + k] = (int32_t)j;
-      if (vmin == (int32_t)(j * g.K + o)) out_coords[k] = make_int4(c.x, y0, y1, y2);
-      break;  // the only output of this input
-    }
+  int o, y0, y1, y2;
+  const bool hit = sc_target1(g, c, valid && site_in_range(c, g), o, y0, y1, y2);
+  const uint64_t key = hit ? pack_key(c.x, y0, y1, y2) : kEmptyKey;
+  uint64_t peers;
+  int leader;
+  sc_group(hit, key, lane, peers, leader);
+  // the leader looks up the output row for its group
+  int32_t vmin = -1, k = -1;
+  if (hit && leader == lane) {
+    vmin = table_lookup(otable, omask, key);
+    k = rank[vmin / g.K];
   }
-  if (valid) tgt[j] = make_int2(k, oj);
-  for (int o = 0; o < g.K; ++o) {
-    const unsigned long long m = __ballot(oj == o);
-    if (lane == 0) counts[(int64_t)o * n_tiles + t] = __popcll(m);
+  k = __shfl(k, hit ? leader : lane);
+  const int32_t oj = hit ? o : -1;
+  if (hit) {
+    nbr_out[(int64_t)o * n_out + k] = (int32_t)j;
+    if (vmin == (int32_t)(j * g.K + o)) out_coords[k] = make_int4(c.x, y0, y1, y2);
+  }
+  if (valid) tgt[j] = make_int2(hit ? k : -1, oj);
+  for (int b = 0; b < g.K; ++b) {
+    const unsigned long long m = __ballot(oj == b);
+    if (lane == 0) counts[(int64_t)b * n_tiles + t] = __popcll(m);
   }
 }
 
@@ -2145,40 +2229,58 @@ extern "C" sscn_status sc_rulebook_build(const int32_t* coords, int64_t n, const
     Arena ta;
     if (!visit_checks) ta.add(&table, cap);
     ta.add(&otable, ocap);
-    ta.add(&stats, 2 + K);
+    ta.add(&stats, 3 + K);  // flags, pairs per offset, n_out, rows out of order
     // every input sees at most one output (f <= s): the visits are grouped
     // per output inside each wavefront first, and first / rank hold one
     // entry per input
     const bool one_target = per_dim == 1 && K <= 32;
     ta.add(&first, (size_t)n * (one_target ? 1 : K));
     ta.add(&rank, (size_t)n * (one_target ? 1 : K) + 1);
+    uint32_t* mark_part = nullptr;  // one_target: pair counts per (offset, workgroup of k_sc_mark1)
+    if (one_target) ta.add(&mark_part, (size_t)K * grid_for(std::max<int64_t>(n, 1), 256));
     SSCN_TRY(tmp.alloc(ta));
     Arena ia;
     ia.add(&d->in_coords, (size_t)4 * n);
     SSCN_TRY(owned_alloc(d, ia, s));
 
-    auto visit = one_target ? k_sc_visit1 : k_sc_visit;
+    int* unsorted = (int*)(stats + 2 + K);
     if (visit_checks) {
-      SSCN_TRY(launch_fill_slots(otable, ocap, INT32_MAX, s, stats, 2 + K));
-      if (n > 0) {
-        visit<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, 1, stats,
-                                               (int4*)d->in_coords);
+      SSCN_TRY(launch_fill_slots(otable, ocap, INT32_MAX, s, stats, 3 + K));
+      if (n > 0 && one_target) {
+        k_sc_order<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, unsorted);
+        SSCN_HIP(hipGetLastError());
+        k_sc_visit1<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, 1, stats,
+                                                     (int4*)d->in_coords, unsorted);
+        SSCN_HIP(hipGetLastError());
+      } else if (n > 0) {
+        k_sc_visit<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, 1, stats,
+                                                    (int4*)d->in_coords);
         SSCN_HIP(hipGetLastError());
       }
     } else {
-      SSCN_TRY(launch_fill_slots(table, cap, -1, s, stats, 2 + K));
+      SSCN_TRY(launch_fill_slots(table, cap, -1, s, stats, 3 + K));
       if (n > 0) {
         SSCN_TRY(launch_fill_slots(otable, ocap, INT32_MAX, s));
         k_insert<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g.L0, g.L1, g.L2, table, cap - 1, stats,
                                                  (int4*)d->in_coords);
         SSCN_HIP(hipGetLastError());
-        visit<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, 0, stats, nullptr);
+        if (one_target)
+          k_sc_visit1<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, 0, stats,
+                                                       nullptr, unsorted);
+        else
+          k_sc_visit<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, 0, stats,
+                                                      nullptr);
         SSCN_HIP(hipGetLastError());
       }
     }
     if (n > 0) {
-      k_sc_mark<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, one_target ? 1 : 0,
-                                                 first, stats + 1);
+      if (one_target) {
+        const unsigned nb = grid_for(n, 256);
+        k_sc_mark1<<<nb, 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, first, mark_part);
+        SSCN_HIP(hipGetLastError());
+        k_offset_sums<<<K, kOneBlock, 0, s>>>(mark_part, nb, stats + 1);
+      } else
+        k_sc_mark<<<grid_for(n, 256), 256, 0, s>>>((const int4*)coords, n, g, otable, ocap - 1, first, stats + 1);
       SSCN_HIP(hipGetLastError());
       const int64_t n_visits = one_target ? n : n * K;  // entries of first / rank
       SSCN_TRY(exclusive_scan_i32(first, rank, n_visits, s));

@@ -148,7 +148,10 @@ def test_sc_visits_grouped_per_output():
     rows (many groups) and shuffled rows (few) give the oracle's rule book
     and numbering, and a repeated location is reported when both copies
     fall in one group, in one wavefront but not side by side, and in
-    different wavefronts."""
+    different wavefronts.  Rows in strictly increasing order skip the
+    per-output offset sets (they cannot repeat a location), so the copies
+    also sit side by side across a wavefront and a workgroup boundary,
+    where the order check compares rows of two wavefronts."""
     c, size = coords_for("shapes128")
     perm = np.random.default_rng(5).permutation(c.shape[0])
     for rows in (c, np.ascontiguousarray(c[perm])):
@@ -156,7 +159,7 @@ def test_sc_visits_grouped_per_output():
         osc = O.sc_rulebook(rows, size, 2, 2)
         assert_same_rulebook(sc, osc, "grouped sc22")
         np.testing.assert_array_equal(host(sc.out_coords()), osc.out_coords)
-    for at, src in ((641, 640), (650, 643), (c.shape[0], 700)):
+    for at, src in ((641, 640), (650, 643), (c.shape[0], 700), (64, 63), (256, 255)):
         rep = np.ascontiguousarray(np.insert(c, at, c[src], axis=0))
         with pytest.raises(sscn.SSCNError) as e:
             sscn.sc_rulebook_build(dev(rep), size, 2, 2)
