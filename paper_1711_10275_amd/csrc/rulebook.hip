@@ -945,17 +945,33 @@ __global__ __launch_bounds__(256) void k_sc_visit1(const int4* __restrict__ coor
     if (__ballot(hit && o == b) & peers) bits |= 1u << b;
   if (!peers) return;
   if (check && __popc(bits) != __popcll(peers)) atomicOr(flags, (unsigned long long)kFlagDuplicate);
+  const bool collect = check && *unsorted;
+  const int32_t v = (int32_t)(j * g.K + o);
   uint64_t slot = mix64(key) & omask;
+  if (!collect) {
+    // a slot that already holds the key with a smaller first visit needs no
+    // atomics (its minimum only falls; a stale copy only shows an earlier,
+    // larger state); else the insert starts where this probe stopped
+    while (true) {
+      const Slot e = otable[slot];
+      if (e.key == key) {
+        if (e.row < v) return;
+        break;
+      }
+      if (e.key == kEmptyKey) break;
+      slot = (slot + 1) & omask;
+    }
+  }
   while (true) {
     const unsigned long long prev =
         atomicCAS((unsigned long long*)&otable[slot].key, (unsigned long long)kEmptyKey, (unsigned long long)key);
     if (prev == kEmptyKey || prev == key) break;
     slot = (slot + 1) & omask;
   }
-  atomicMin(&otable[slot].row, (int32_t)(j * g.K + o));
+  atomicMin(&otable[slot].row, v);
   // rows in strictly increasing order hold no location twice: the offsets
   // are only collected (an atomic per group) for other rows
-  if (check && *unsorted && (atomicOr(&otable[slot].pad, (int32_t)bits) & (int32_t)bits))
+  if (collect && (atomicOr(&otable[slot].pad, (int32_t)bits) & (int32_t)bits))
     atomicOr(flags, (unsigned long long)kFlagDuplicate);
 }
 
