@@ -431,8 +431,10 @@ __global__ __launch_bounds__(256) void k_compact(const int32_t* __restrict__ nbr
                                                  unsigned long long* __restrict__ host_stats, int n_stats) {
   __shared__ uint32_t part[kPlanMaskWords][4][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t t = blockIdx.x;  // one workgroup per tile
-  if (host_stats && t == 0)
+  // one workgroup per tile, consecutive tiles on one XCD: the runs of
+  // neighbouring tiles meet inside cache lines, merged in that XCD's L2
+  const int64_t t = xcd_remap(blockIdx.x, gridDim.x);
+  if (host_stats && blockIdx.x == 0)
     for (int i = threadIdx.x; i < n_stats; i += blockDim.x) host_stats[i] = stats[i];
   const int64_t k = t * kTile + lane;
   const bool valid = k < n_rows;
